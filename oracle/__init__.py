@@ -1,0 +1,237 @@
+"""CPU oracle for the PEAT error signature and bit-flip injector.
+
+TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the
+benchmark's ``cpu_baseline`` leg are the only callers.  The GPU library never
+imports, links or executes anything in this directory.
+
+The arithmetic lives in ``peat_oracle.c`` (plain scalar C, IEEE binary64,
+no contraction, no fast-math), built with gcc into ``liboracle.so`` next to
+it.  This module only marshals numpy arrays into that library and returns
+plain Python dicts.
+
+Passages followed (the paper is "PEAT: Pseudo-Error Assessment for GPU Kernel
+Validation in DNN Training"):
+  * Section IV-B.3 "FI Assessment Scores": error = absolute difference of the
+    golden and fault-injected outputs; max, mean and variance of it.
+  * Section III-A and Fig. "Motivating_isclose": closeness with
+    torch.isclose(rtol, atol) -> absolute-threshold mismatch counts.
+  * Section V-D, Fig. "tiny_error_gemm_resnet34": error value histograms.
+  * Section II-B "Error Models": random bit flip at a bit error rate.
+  * Algorithms 1 and 2: Inject() followed by Err(golden set, FI set).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "peat_oracle.c")
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+F32, F16, BF16 = 0, 1, 2
+_DTYPE_CODE = {np.dtype(np.float32): F32, np.dtype(np.float16): F16}
+
+OK, EINVAL, EDTYPE, EBITMASK, ERATE = 0, -1, -2, -3, -4
+
+
+class _Sig(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int64), ("n_valid", ctypes.c_int64),
+        ("n_finite", ctypes.c_int64), ("n_rel", ctypes.c_int64),
+        ("n_nan_golden", ctypes.c_int64), ("n_nan_test", ctypes.c_int64),
+        ("n_inf_golden", ctypes.c_int64), ("n_inf_test", ctypes.c_int64),
+        ("n_nan_pairs", ctypes.c_int64), ("first_nan_index", ctypes.c_int64),
+        ("n_mismatch", ctypes.c_int64 * 8),
+        ("hist_zero", ctypes.c_int64), ("hist_under", ctypes.c_int64),
+        ("hist_over", ctypes.c_int64),
+        ("hist", ctypes.c_int64 * 64),
+        ("max_abs", ctypes.c_double), ("argmax_abs", ctypes.c_int64),
+        ("max_ulp", ctypes.c_int64), ("argmax_ulp", ctypes.c_int64),
+        ("sum_ulp", ctypes.c_uint64),
+        ("max_rel", ctypes.c_double), ("argmax_rel", ctypes.c_int64),
+        ("sum_abs", ctypes.c_double), ("sum_sq", ctypes.c_double),
+        ("sum_rel", ctypes.c_double), ("sum_g2", ctypes.c_double),
+        ("sum_t2", ctypes.c_double), ("sum_gt", ctypes.c_double),
+    ]
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_double) for k in
+                ("mean_abs", "var_abs", "l2_err", "l2_g", "l2_t", "cos",
+                 "mean_rel", "mean_ulp")]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def build(force: bool = False) -> str:
+    """Compile peat_oracle.c with gcc (no contraction, no fast-math)."""
+    if force or not os.path.exists(LIB_PATH) or \
+            os.path.getmtime(LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = LIB_PATH + f".tmp{os.getpid()}"
+        subprocess.check_call([
+            "gcc", "-O2", "-std=c11", "-fPIC", "-shared",
+            "-ffp-contract=off", "-fno-fast-math", "-fno-strict-aliasing",
+            "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+def lib():
+    """Load (building first if absent) the oracle library."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                build()
+            L = ctypes.CDLL(LIB_PATH)
+            L.oracle_signature.restype = ctypes.c_int
+            L.oracle_signature.argtypes = [
+                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_Sig)]
+            L.oracle_stats.restype = ctypes.c_int
+            L.oracle_stats.argtypes = [ctypes.POINTER(_Sig), ctypes.POINTER(_Stats)]
+            L.oracle_philox4x64_10.restype = None
+            L.oracle_philox4x64_10.argtypes = [
+                ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64),
+                ctypes.POINTER(ctypes.c_uint64)]
+            L.oracle_rate_threshold.restype = ctypes.c_uint64
+            L.oracle_rate_threshold.argtypes = [ctypes.c_double, ctypes.POINTER(ctypes.c_int)]
+            L.oracle_inject_decide.restype = ctypes.c_int
+            L.oracle_inject_decide.argtypes = [
+                ctypes.c_int64, ctypes.c_int, ctypes.c_uint64, ctypes.c_double,
+                ctypes.c_uint64, ctypes.POINTER(ctypes.c_int)]
+            L.oracle_inject.restype = ctypes.c_int64
+            L.oracle_inject.argtypes = [
+                ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
+                ctypes.c_double, ctypes.c_uint64]
+            L.oracle_sizeof_sig.restype = ctypes.c_int
+            assert L.oracle_sizeof_sig() == ctypes.sizeof(_Sig)
+            _lib = L
+    return _lib
+
+
+def _code(arr: np.ndarray, dtype_code: int | None) -> int:
+    if dtype_code is not None:
+        return dtype_code
+    if arr.dtype == np.uint16:
+        raise ValueError("uint16 arrays need an explicit dtype code (F16 or BF16)")
+    if arr.dtype == np.uint32:
+        return F32
+    return _DTYPE_CODE[arr.dtype]
+
+
+def _sig_to_dict(s: _Sig, nthr: int) -> dict:
+    d = {}
+    for name, _ in _Sig._fields_:
+        v = getattr(s, name)
+        if name == "n_mismatch":
+            v = [int(v[j]) for j in range(nthr)]
+        elif name == "hist":
+            v = [int(x) for x in v]
+        elif isinstance(v, float):
+            v = float(v)
+        else:
+            v = int(v)
+        d[name] = v
+    return d
+
+
+def signature(golden: np.ndarray, test: np.ndarray, *, dtype: int | None = None,
+              bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), raw: bool = False):
+    """Error signature of (golden, test): dict of every field.
+
+    ``golden``/``test`` are contiguous numpy arrays of float32/float16 or raw
+    bit patterns (uint32 for f32; uint16 with ``dtype=F16``/``BF16``).
+    """
+    g = np.ascontiguousarray(golden).reshape(-1)
+    t = np.ascontiguousarray(test).reshape(-1)
+    if g.shape != t.shape or g.dtype != t.dtype:
+        raise ValueError("golden and test must have the same shape and dtype")
+    code = _code(g, dtype)
+    thr = (ctypes.c_double * 8)(*[float(x) for x in thresholds])
+    out = _Sig()
+    rc = lib().oracle_signature(
+        g.ctypes.data if g.size else None, t.ctypes.data if t.size else None,
+        g.size, code, int(bins[0]), int(bins[1]), int(bins[2]), len(thresholds),
+        thr, ctypes.byref(out))
+    if rc != OK:
+        raise ValueError(f"oracle_signature failed: {rc}")
+    if raw:
+        return out
+    return _sig_to_dict(out, len(thresholds))
+
+
+def signature_rc(golden_ptr, test_ptr, n, code, bins, thresholds) -> int:
+    """Return code of oracle_signature for argument-validation tests."""
+    thr = (ctypes.c_double * max(8, len(thresholds)))(*[float(x) for x in thresholds])
+    out = _Sig()
+    return lib().oracle_signature(golden_ptr, test_ptr, n, code, bins[0], bins[1],
+                                  bins[2], len(thresholds), thr, ctypes.byref(out))
+
+
+def stats(sig: dict) -> dict:
+    s = _Sig()
+    for name, _ in _Sig._fields_:
+        v = sig[name]
+        if name == "n_mismatch":
+            for j, x in enumerate(v):
+                s.n_mismatch[j] = x
+        elif name == "hist":
+            for j, x in enumerate(v):
+                s.hist[j] = x
+        else:
+            setattr(s, name, v)
+    st = _Stats()
+    lib().oracle_stats(ctypes.byref(s), ctypes.byref(st))
+    return {k: float(getattr(st, k)) for k, _ in _Stats._fields_}
+
+
+def philox4x64_10(counter, key):
+    c = (ctypes.c_uint64 * 4)(*[int(x) & (2**64 - 1) for x in counter])
+    k = (ctypes.c_uint64 * 2)(*[int(x) & (2**64 - 1) for x in key])
+    o = (ctypes.c_uint64 * 4)()
+    lib().oracle_philox4x64_10(c, k, o)
+    return [int(x) for x in o]
+
+
+def rate_threshold(rate: float):
+    """(T, all) with T = floor(rate * 2^64)."""
+    a = ctypes.c_int(0)
+    T = lib().oracle_rate_threshold(float(rate), ctypes.byref(a))
+    return int(T), bool(a.value)
+
+
+def inject_decide(i: int, dtype: int, seed: int, rate: float, mask: int):
+    """(flips, bit) for element i alone."""
+    b = ctypes.c_int(-1)
+    rc = lib().oracle_inject_decide(int(i), dtype, seed & (2**64 - 1), float(rate),
+                                    mask & (2**64 - 1), ctypes.byref(b))
+    if rc < 0:
+        raise ValueError(f"oracle_inject_decide failed: {rc}")
+    return bool(rc), (b.value if rc else None)
+
+
+def inject(x: np.ndarray, *, dtype: int | None = None, seed: int, rate: float,
+           mask: int) -> int:
+    """Flip bits of ``x`` in place (x must be C-contiguous); returns the count."""
+    if not x.flags.c_contiguous or not x.flags.writeable:
+        raise ValueError("inject needs a writeable C-contiguous array")
+    code = _code(x, dtype)
+    rc = lib().oracle_inject(x.ctypes.data if x.size else None, x.size, code,
+                             seed & (2**64 - 1), float(rate), mask & (2**64 - 1))
+    if rc < 0:
+        raise ValueError(f"oracle_inject failed: {rc}")
+    return int(rc)
+
+
+def inject_rc(n, code, seed, rate, mask) -> int:
+    """Return code of oracle_inject on a scratch buffer (validation tests)."""
+    buf = np.zeros(max(int(n), 1) * 4, dtype=np.uint8)
+    return int(lib().oracle_inject(buf.ctypes.data, int(n), code, seed, float(rate), mask))

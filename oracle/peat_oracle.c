@@ -1,0 +1,432 @@
+/*
+ * PEAT oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, scalar CPU implementation of the two operations on the hot
+ * path of PEAT's pseudo-error assessment:
+ *
+ *   oracle_signature  the Analyzer's comparison of a golden tensor with a test
+ *                     tensor ("FI Assessment Scores", Section IV-B: the error is
+ *                     the absolute difference of golden and fault-injected
+ *                     values; max, mean and variance of it), extended to the
+ *                     error signature: per-element relative error, ULP distance,
+ *                     a log2-binned error histogram (Section V-D, error value
+ *                     histograms), NaN/Inf counts, absolute-threshold mismatch
+ *                     counts (the closeness test of Section III-A, torch.isclose
+ *                     with rtol = 0), maxima with the lowest index, and the fp64
+ *                     sums from which L2 norms and the cosine follow.
+ *
+ *   oracle_inject     the random-bit-flip error model (Section II-B, "Error
+ *                     Models": parameters flip at a given bit error rate), used
+ *                     by Inject() in Playback FI (Algorithm 1) and Runtime FI
+ *                     (Algorithm 2).
+ *
+ * Only the tests, the package smoke check and the benchmark's CPU-baseline leg
+ * may load this file's library.  It shares no code, header, table or constant
+ * generator with the GPU library; the two are independent by construction.
+ *
+ * Arithmetic: IEEE binary64, round-to-nearest-even, compiled without
+ * contraction or fast-math.  Elements are scanned in increasing index order.
+ * Floating-point sums use Neumaier's compensated summation.
+ *
+ * Every field has a pin in the CPU test suite (closed forms, brute force over
+ * the fp16 grid with exact rational arithmetic, math.fsum, torch float64
+ * library routines, numpy's Philox4x64-10).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define ORACLE_F32 0
+#define ORACLE_F16 1
+#define ORACLE_BF16 2
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_EDTYPE (-2)
+#define ORACLE_EBITMASK (-3)
+#define ORACLE_ERATE (-4)
+
+typedef struct {
+    int64_t n, n_valid, n_finite, n_rel;
+    int64_t n_nan_golden, n_nan_test, n_inf_golden, n_inf_test, n_nan_pairs, first_nan_index;
+    int64_t n_mismatch[8];
+    int64_t hist_zero, hist_under, hist_over;
+    int64_t hist[64];
+    double max_abs;
+    int64_t argmax_abs;
+    int64_t max_ulp;
+    int64_t argmax_ulp;
+    uint64_t sum_ulp;
+    double max_rel;
+    int64_t argmax_rel;
+    double sum_abs, sum_sq, sum_rel, sum_g2, sum_t2, sum_gt;
+} oracle_sig_t;
+
+typedef struct {
+    double mean_abs, var_abs, l2_err, l2_g, l2_t, cos, mean_rel, mean_ulp;
+} oracle_stats_t;
+
+/* ------------------------------------------------------------------------- */
+/* Decoding: bit pattern of element i -> its exact binary64 value.           */
+/* ------------------------------------------------------------------------- */
+
+static int dtype_width(int dtype) {
+    if (dtype == ORACLE_F32) return 32;
+    if (dtype == ORACLE_F16 || dtype == ORACLE_BF16) return 16;
+    return 0;
+}
+
+static uint32_t element_bits(const void *base, int64_t i, int dtype) {
+    if (dtype == ORACLE_F32) {
+        uint32_t b;
+        memcpy(&b, (const unsigned char *)base + 4 * i, 4);
+        return b;
+    }
+    uint16_t h;
+    memcpy(&h, (const unsigned char *)base + 2 * i, 2);
+    return h;
+}
+
+/* IEEE binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits. */
+static double half_value(uint32_t h) {
+    int sign = (h >> 15) & 1;
+    int expo = (h >> 10) & 0x1F;
+    int frac = h & 0x3FF;
+    double v;
+    if (expo == 0x1F)
+        v = frac ? NAN : INFINITY;
+    else if (expo == 0)
+        v = ldexp((double)frac, -24);            /* subnormal: frac * 2^-24 */
+    else
+        v = ldexp((double)(frac | 0x400), expo - 25); /* (1.frac) * 2^(expo-15) */
+    return sign ? -v : v;
+}
+
+static double element_value(uint32_t bits, int dtype) {
+    if (dtype == ORACLE_F16) return half_value(bits);
+    float f;
+    uint32_t b = (dtype == ORACLE_BF16) ? (bits << 16) : bits; /* bf16 = top half of binary32 */
+    memcpy(&f, &b, 4);
+    return (double)f; /* widening binary32 -> binary64 is exact */
+}
+
+/* Distance in units in the last place: the signed-magnitude bit pattern is
+ * mapped to an integer key (+magnitude or -magnitude, so +0 and -0 coincide),
+ * and the ULP distance is the absolute difference of the keys. */
+static int64_t ulp_key(uint32_t bits, int width) {
+    uint32_t sign_bit = 1u << (width - 1);
+    int64_t mag = (int64_t)(bits & (sign_bit - 1));
+    return (bits & sign_bit) ? -mag : mag;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Neumaier compensated summation.                                           */
+/* ------------------------------------------------------------------------- */
+
+typedef struct { double s, c; } csum_t;
+
+static void csum_add(csum_t *acc, double x) {
+    double t = acc->s + x;
+    if (fabs(acc->s) >= fabs(x))
+        acc->c += (acc->s - t) + x;
+    else
+        acc->c += (x - t) + acc->s;
+    acc->s = t;
+}
+
+static double csum_value(const csum_t *acc) { return acc->s + acc->c; }
+
+/* ------------------------------------------------------------------------- */
+/* The error signature.                                                      */
+/* ------------------------------------------------------------------------- */
+
+/* Validation of the histogram and thresholds (same acceptance rules as the
+ * library: -1022 <= lo < hi <= 1024, 1 <= nbins <= 64, nbins divides hi-lo;
+ * 0 <= nthr <= 8 thresholds, each >= 0 and not NaN). */
+static int check_params(int lo, int hi, int nbins, int nthr, const double *thr) {
+    if (lo < -1022 || hi > 1024 || lo >= hi) return ORACLE_EINVAL;
+    if (nbins < 1 || nbins > 64 || (hi - lo) % nbins != 0) return ORACLE_EINVAL;
+    if (nthr < 0 || nthr > 8) return ORACLE_EINVAL;
+    if (nthr > 0 && !thr) return ORACLE_EINVAL;
+    for (int j = 0; j < nthr; ++j)
+        if (isnan(thr[j]) || thr[j] < 0) return ORACLE_EINVAL;
+    return ORACLE_OK;
+}
+
+int oracle_signature(const void *golden, const void *test, int64_t n, int dtype,
+                     int lo, int hi, int nbins, int nthr, const double *thr,
+                     oracle_sig_t *out) {
+    int width = dtype_width(dtype);
+    if (!width) return ORACLE_EDTYPE;
+    if (!out || n < 0 || (n > 0 && (!golden || !test))) return ORACLE_EINVAL;
+    int rc = check_params(lo, hi, nbins, nthr, thr);
+    if (rc) return rc;
+
+    oracle_sig_t s;
+    memset(&s, 0, sizeof s);
+    s.n = n;
+    s.first_nan_index = -1;
+    s.argmax_abs = s.argmax_ulp = s.argmax_rel = -1;
+    s.max_abs = NAN;
+    s.max_rel = NAN;
+    int have_abs = 0, have_ulp = 0, have_rel = 0;
+    int binw = (hi - lo) / nbins; /* binades per bin */
+    csum_t c_abs = {0, 0}, c_sq = {0, 0}, c_rel = {0, 0};
+    csum_t c_g2 = {0, 0}, c_t2 = {0, 0}, c_gt = {0, 0};
+
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t gb = element_bits(golden, i, dtype);
+        uint32_t tb = element_bits(test, i, dtype);
+        double G = element_value(gb, dtype);
+        double T = element_value(tb, dtype);
+
+        /* Step 1: classify.  A pair with a NaN on either side is excluded
+         * from everything except the NaN counts and the mismatch counts. */
+        /* isinf/isnan only promise a nonzero result (glibc's isinf is -1 for
+         * -Inf), so normalise them to 0/1 before counting. */
+        int nan_g = isnan(G) != 0, nan_t = isnan(T) != 0;
+        int inf_g = isinf(G) != 0, inf_t = isinf(T) != 0;
+        s.n_nan_golden += nan_g;
+        s.n_nan_test += nan_t;
+        s.n_inf_golden += inf_g;
+        s.n_inf_test += inf_t;
+        if (nan_g || nan_t) {
+            s.n_nan_pairs += 1;
+            if (s.first_nan_index < 0) s.first_nan_index = i;
+            continue;
+        }
+        s.n_valid += 1;
+
+        /* Step 2: error = absolute difference.  Equal values (including +0 vs
+         * -0 and equal infinities) have error 0; otherwise |RN(T - G)|, which
+         * is +Inf when exactly one side is infinite or the infinities differ. */
+        double a = (G == T) ? 0.0 : fabs(T - G);
+
+        /* Step 3: ULP distance from the bit patterns. */
+        int64_t ku = ulp_key(tb, width) - ulp_key(gb, width);
+        int64_t ulp = ku < 0 ? -ku : ku;
+        s.sum_ulp += (uint64_t)ulp;
+
+        /* Step 4: histogram of the error over binades [2^k, 2^(k+1)). */
+        if (a == 0.0) {
+            s.hist_zero += 1;
+        } else if (isinf(a)) {
+            s.hist_over += 1;
+        } else {
+            int ex;
+            frexp(a, &ex);  /* a = f * 2^ex, f in [0.5, 1) => floor(log2 a) = ex - 1 */
+            int k = ex - 1;
+            if (k < lo)
+                s.hist_under += 1;
+            else if (k >= hi)
+                s.hist_over += 1;
+            else
+                s.hist[(k - lo) / binw] += 1;
+        }
+
+        /* Step 5: mismatches = pairs that are not close under torch.isclose
+         * with rtol = 0 and atol = theta (Section III-A): the error exceeds
+         * theta, or it is infinite (unequal infinities are never close, even
+         * for theta = +Inf). */
+        for (int j = 0; j < nthr; ++j)
+            if (a > thr[j] || isinf(a)) s.n_mismatch[j] += 1;
+
+        /* Step 6: maxima, strict > in increasing index order (lowest index
+         * wins ties). */
+        if (!have_abs || a > s.max_abs) {
+            s.max_abs = a;
+            s.argmax_abs = i;
+            have_abs = 1;
+        }
+        if (!have_ulp || ulp > s.max_ulp) {
+            s.max_ulp = ulp;
+            s.argmax_ulp = i;
+            have_ulp = 1;
+        }
+
+        /* Steps 7-8: sums over pairs whose two values are finite. */
+        if (inf_g || inf_t) continue;
+        s.n_finite += 1;
+        csum_add(&c_abs, a);
+        csum_add(&c_sq, a * a);
+        csum_add(&c_g2, G * G);
+        csum_add(&c_t2, T * T);
+        csum_add(&c_gt, G * T);
+        if (G != 0.0) {
+            double r = a / fabs(G); /* relative error, IEEE division */
+            s.n_rel += 1;
+            csum_add(&c_rel, r);
+            if (!have_rel || r > s.max_rel) {
+                s.max_rel = r;
+                s.argmax_rel = i;
+                have_rel = 1;
+            }
+        }
+    }
+    /* NaN pairs count as mismatches for every threshold. */
+    for (int j = 0; j < nthr; ++j) s.n_mismatch[j] += s.n_nan_pairs;
+
+    s.sum_abs = csum_value(&c_abs);
+    s.sum_sq = csum_value(&c_sq);
+    s.sum_rel = csum_value(&c_rel);
+    s.sum_g2 = csum_value(&c_g2);
+    s.sum_t2 = csum_value(&c_t2);
+    s.sum_gt = csum_value(&c_gt);
+    *out = s;
+    return ORACLE_OK;
+}
+
+/* Derived statistics of a signature (Section IV-B.3 scores: mean and
+ * variance of the error; plus norms, cosine, mean relative error and mean ULP
+ * distance).  The variance is the sample variance (divisor n_finite - 1),
+ * PyTorch's default estimator. */
+int oracle_stats(const oracle_sig_t *s, oracle_stats_t *st) {
+    if (!s || !st) return ORACLE_EINVAL;
+    double nf = (double)s->n_finite;
+    st->mean_abs = s->n_finite > 0 ? s->sum_abs / nf : NAN;
+    st->var_abs = s->n_finite > 1 ? (s->sum_sq - s->sum_abs * s->sum_abs / nf) / (nf - 1.0) : NAN;
+    st->l2_err = sqrt(s->sum_sq);
+    st->l2_g = sqrt(s->sum_g2);
+    st->l2_t = sqrt(s->sum_t2);
+    st->cos = (s->sum_g2 > 0 && s->sum_t2 > 0) ? s->sum_gt / sqrt(s->sum_g2 * s->sum_t2) : NAN;
+    st->mean_rel = s->n_rel > 0 ? s->sum_rel / (double)s->n_rel : NAN;
+    st->mean_ulp = s->n_valid > 0 ? (double)s->sum_ulp / (double)s->n_valid : NAN;
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as    */
+/* easy as 1, 2, 3", SC'11): ten rounds of two 64x64->128 multiplications     */
+/* with the Weyl-sequence key schedule.                                      */
+/* ------------------------------------------------------------------------- */
+
+void oracle_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4]) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ULL, M1 = 0xCA5A826395121157ULL;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ULL, W1 = 0xBB67AE8584CAA73BULL;
+    uint64_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+    uint64_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        unsigned __int128 p0 = (unsigned __int128)M0 * c0;
+        unsigned __int128 p1 = (unsigned __int128)M1 * c2;
+        uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
+        uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += W0;
+        k1 += W1;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Random bit flip at a bit error rate.                                      */
+/* ------------------------------------------------------------------------- */
+
+/* Decision threshold: element i flips iff its 64-bit uniform U_i < T with
+ * T = floor(rate * 2^64) (exact: ldexp scales by a power of two and the
+ * conversion truncates); rate >= 1 flips every element.  Returns 0 with
+ * *all = 1 in that case. */
+uint64_t oracle_rate_threshold(double rate, int *all) {
+    *all = 0;
+    if (rate >= 1.0) {
+        *all = 1;
+        return 0;
+    }
+    if (rate <= 0.0) return 0;
+    return (uint64_t)ldexp(rate, 64);
+}
+
+static void philox_seeded(uint64_t seed, uint64_t c0, uint64_t c1, uint64_t out[4]) {
+    uint64_t ctr[4] = {c0, c1, 0, 0};
+    uint64_t key[2] = {seed, 0};
+    oracle_philox4x64_10(ctr, key, out);
+}
+
+/* The per-element uniform U_i.  Its top byte is byte (i mod 32) of the
+ * 32-byte block A = Philox(key=(seed,0), ctr=(i/32, 0, 0, 0)), bytes numbered
+ * little-endian through words 0..3; its low 56 bits are the low 56 bits of
+ * word (i mod 4) of B = Philox(key, ctr=(i/4, 1, 0, 0)). */
+static uint64_t uniform_of(const uint64_t A[4], const uint64_t B[4], int64_t i) {
+    int byte = (int)(i & 31);
+    uint64_t top = (A[byte >> 3] >> (8 * (byte & 7))) & 0xFF;
+    uint64_t low = B[i & 3] & ((1ULL << 56) - 1);
+    return (top << 56) | low;
+}
+
+/* The flipped bit of element i: y = word 0 of Philox(key, ctr=(i, 2, 0, 0));
+ * j = floor(hi32(y) * popcount(mask) / 2^32) selects the j-th lowest set bit
+ * of the mask. */
+static int chosen_bit(uint64_t seed, int64_t i, uint64_t mask) {
+    uint64_t C[4];
+    philox_seeded(seed, (uint64_t)i, 2, C);
+    uint64_t p = 0;
+    for (int b = 0; b < 64; ++b) p += (mask >> b) & 1;
+    uint64_t j = ((C[0] >> 32) * p) >> 32;
+    for (int b = 0; b < 64; ++b) {
+        if ((mask >> b) & 1) {
+            if (j == 0) return b;
+            --j;
+        }
+    }
+    return -1; /* unreachable for a nonzero mask */
+}
+
+static int check_inject(int dtype, double rate, uint64_t mask) {
+    int width = dtype_width(dtype);
+    if (!width) return ORACLE_EDTYPE;
+    if (mask == 0 || (width < 64 && (mask >> width) != 0)) return ORACLE_EBITMASK;
+    if (isnan(rate) || rate < 0) return ORACLE_ERATE;
+    return ORACLE_OK;
+}
+
+/* Decide element i alone: returns 1 and the bit if it flips, else 0. */
+int oracle_inject_decide(int64_t i, int dtype, uint64_t seed, double rate, uint64_t mask, int *bit) {
+    int rc = check_inject(dtype, rate, mask);
+    if (rc) return rc;
+    int all;
+    uint64_t T = oracle_rate_threshold(rate, &all);
+    uint64_t A[4], B[4];
+    philox_seeded(seed, (uint64_t)i >> 5, 0, A);
+    philox_seeded(seed, (uint64_t)i >> 2, 1, B);
+    int flip = all || uniform_of(A, B, i) < T;
+    if (flip && bit) *bit = chosen_bit(seed, i, mask);
+    return flip;
+}
+
+/* Flip bits of x[0..n) in place; returns the number of flipped elements or a
+ * negative error code. */
+int64_t oracle_inject(void *x, int64_t n, int dtype, uint64_t seed, double rate, uint64_t mask) {
+    int rc = check_inject(dtype, rate, mask);
+    if (rc) return rc;
+    if (n < 0 || (n > 0 && !x)) return ORACLE_EINVAL;
+    int all;
+    uint64_t T = oracle_rate_threshold(rate, &all);
+    int64_t flips = 0;
+    uint64_t A[4], B[4];
+    for (int64_t i = 0; i < n; ++i) {
+        if ((i & 31) == 0 || i == 0) philox_seeded(seed, (uint64_t)i >> 5, 0, A);
+        if ((i & 3) == 0 || i == 0) philox_seeded(seed, (uint64_t)i >> 2, 1, B);
+        if (!(all || uniform_of(A, B, i) < T)) continue;
+        int b = chosen_bit(seed, i, mask);
+        if (dtype == ORACLE_F32) {
+            uint32_t v;
+            memcpy(&v, (unsigned char *)x + 4 * i, 4);
+            v ^= 1u << b;
+            memcpy((unsigned char *)x + 4 * i, &v, 4);
+        } else {
+            uint16_t v;
+            memcpy(&v, (unsigned char *)x + 2 * i, 2);
+            v ^= (uint16_t)(1u << b);
+            memcpy((unsigned char *)x + 2 * i, &v, 2);
+        }
+        ++flips;
+    }
+    return flips;
+}
+
+int oracle_sizeof_sig(void) { return (int)sizeof(oracle_sig_t); }
