@@ -1,0 +1,212 @@
+/*
+ * peat.h -- C ABI of libpeat: error signatures of golden/test tensor pairs and
+ * seeded random-bit-flip injection, as hand-written HIP kernels for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operations follow the PEAT paper ("PEAT: Pseudo-Error Assessment for
+ * GPU Kernel Validation in DNN Training"):
+ *   - Err(golden set, FI set) of Algorithms 1 and 2 with the scores of
+ *     Section IV-B.3 ("FI Assessment Scores": the error is the absolute
+ *     difference; max, mean, variance), the closeness test of Section III-A
+ *     (torch.isclose, here with rtol = 0) and the error value histograms of
+ *     Section V-D, gathered into one error signature per tensor pair;
+ *   - Inject() of Algorithms 1 and 2 with the random-bit-flip error model of
+ *     Section II-B ("Error Models": flips at a given bit error rate).
+ *
+ * Conventions for every entry point
+ *   - Tensor pointers (golden, test, tensor, pair/item pointers) are DEVICE
+ *     pointers to contiguous element arrays owned by the caller; the library
+ *     neither frees nor keeps them after the call's work has completed.
+ *   - Struct arrays passed by pointer (pairs, items, bins, thresholds) are HOST
+ *     memory owned by the caller; the library copies what it needs before
+ *     returning.
+ *   - Synchronous calls write HOST outputs and return after the work is done.
+ *     They run on the stream set with peat_set_stream (default: the null
+ *     stream).  *_async calls enqueue on the given stream, write DEVICE outputs
+ *     and return without waiting.
+ *   - Return value 0 (PEAT_OK) or a negative PEAT_E* code; outputs are left
+ *     untouched on error.  No C++ exception crosses this boundary.
+ *     peat_last_error() gives a thread-local detail string for the last error.
+ *   - The library keeps one lazily grown device workspace and one pinned
+ *     staging ring per device.  Growing the workspace synchronises the device.
+ *     Calls from several host threads are serialised by an internal mutex;
+ *     work on different streams is ordered through an event on the workspace.
+ *   - Element types: PEAT_F32 (IEEE binary32), PEAT_F16 (IEEE binary16),
+ *     PEAT_BF16 (bfloat16).  Values are widened exactly to binary64; all
+ *     error arithmetic is IEEE binary64 round-to-nearest-even, subnormals kept.
+ */
+#ifndef PEAT_H
+#define PEAT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PEAT_ABI_VERSION 1
+#define PEAT_MAX_THRESHOLDS 8
+#define PEAT_MAX_BINS 64
+
+typedef enum { PEAT_F32 = 0, PEAT_F16 = 1, PEAT_BF16 = 2 } peat_dtype_t;
+
+enum {
+    PEAT_OK = 0,
+    PEAT_EINVAL = -1,   /* bad pointer/size/bins/thresholds/count          */
+    PEAT_EDTYPE = -2,   /* unknown element type                            */
+    PEAT_EBITMASK = -3, /* bitmask is 0 or has bits at/above the type width */
+    PEAT_ERATE = -4,    /* injection rate is NaN or negative               */
+    PEAT_EHIP = -5,     /* HIP runtime error (detail in peat_last_error)   */
+    PEAT_ENOMEM = -6,   /* device or pinned host allocation failed         */
+    PEAT_ENODEV = -7    /* no usable gfx950 device                         */
+};
+
+/* Histogram of the absolute error a over binades: bin b covers
+ * [2^(lo + b*w), 2^(lo + (b+1)*w)) with w = (hi - lo) / nbins.  Errors equal
+ * to 0 go to hist_zero, 0 < a < 2^lo to hist_under, a >= 2^hi (and a = +Inf)
+ * to hist_over.  Valid: -1022 <= lo_log2 < hi_log2 <= 1024,
+ * 1 <= nbins <= 64, nbins divides hi - lo.  (Section V-D histograms.) */
+typedef struct {
+    int32_t lo_log2;
+    int32_t hi_log2;
+    int32_t nbins;
+    int32_t reserved; /* must be 0 */
+} peat_bins_t;
+
+/* Absolute tolerances theta_j >= 0 (not NaN; +Inf allowed), 0 <= count <= 8.
+ * n_mismatch[j] counts pairs that torch.isclose(test, golden, rtol=0,
+ * atol=theta_j, equal_nan=False) calls not close (Section III-A). */
+typedef struct {
+    int32_t count;
+    int32_t reserved; /* must be 0 */
+    double abs_tol[PEAT_MAX_THRESHOLDS];
+} peat_thresholds_t;
+
+/* The error signature of one pair.  G_i, T_i are the values widened to
+ * binary64; a pair is "valid" when neither side is NaN, "finite" when both
+ * sides are finite, "rel" when finite with G_i != 0.  For a valid pair the
+ * error is a_i = 0 if G_i == T_i (IEEE equality), else |RN(T_i - G_i)|; the
+ * ULP distance is |key(t_i) - key(g_i)| with key = +magnitude or -magnitude
+ * of the bit pattern; the relative error is r_i = RN(a_i / |G_i|).
+ * Maxima use strict > over increasing i, so ties go to the lowest index.
+ * With no eligible pair a maximum is NaN (ULP: 0) and its index -1. */
+typedef struct {
+    int64_t n, n_valid, n_finite, n_rel;
+    int64_t n_nan_golden, n_nan_test, n_inf_golden, n_inf_test;
+    int64_t n_nan_pairs;     /* pairs with a NaN on either side            */
+    int64_t first_nan_index; /* lowest index of such a pair, or -1         */
+    int64_t n_mismatch[PEAT_MAX_THRESHOLDS]; /* first thresholds.count used */
+    int64_t hist_zero, hist_under, hist_over;
+    int64_t hist[PEAT_MAX_BINS];             /* first bins.nbins used       */
+    double max_abs;
+    int64_t argmax_abs;      /* over valid pairs */
+    int64_t max_ulp;
+    int64_t argmax_ulp;      /* over valid pairs */
+    uint64_t sum_ulp;        /* over valid pairs */
+    double max_rel;
+    int64_t argmax_rel;      /* over rel pairs */
+    /* binary64 sums over finite pairs (sum_rel over rel pairs): sum a_i,
+     * sum RN(a_i^2), sum G_i^2, sum T_i^2, sum G_i*T_i.  Summation order is a
+     * fixed tree, identical for every call with the same n and dtype. */
+    double sum_abs, sum_sq, sum_rel, sum_g2, sum_t2, sum_gt;
+} peat_signature_t;
+
+/* Scores derived on the host from a signature (Section IV-B.3 mean and
+ * variance; the variance is the sample variance over finite pairs). */
+typedef struct {
+    double mean_abs, var_abs, l2_err, l2_g, l2_t, cos, mean_rel, mean_ulp;
+} peat_stats_t;
+
+typedef struct {
+    const void *golden; /* device pointer */
+    const void *test;   /* device pointer */
+    int64_t n;          /* elements, >= 0 */
+    int32_t dtype;      /* peat_dtype_t   */
+    int32_t reserved;   /* must be 0      */
+} peat_pair_t;
+
+typedef struct {
+    void *tensor;     /* device pointer, modified in place */
+    int64_t n;        /* elements, >= 0 */
+    int32_t dtype;    /* peat_dtype_t   */
+    int32_t reserved; /* must be 0      */
+    uint64_t seed;
+    double rate;      /* bit error rate per element; >= 1 flips every element */
+    uint64_t bitmask; /* candidate bits, nonzero, below the type width */
+} peat_inject_item_t;
+
+/* Static text for a PEAT_E* code; never NULL. */
+const char *peat_strerror(int code);
+
+/* Thread-local detail of the last error returned on this thread ("" if none). */
+const char *peat_last_error(void);
+
+/* PEAT_ABI_VERSION of the loaded library. */
+int peat_abi_version(void);
+
+/* Optional explicit initialisation of the current device (checks that it is
+ * gfx950).  Every entry point does this lazily.  Returns 0 or PEAT_ENODEV /
+ * PEAT_EHIP. */
+int peat_init(void);
+
+/* Stream (a hipStream_t, NULL = null stream) used by the synchronous calls of
+ * the calling host thread. */
+int peat_set_stream(void *stream);
+
+/* Error signature of one pair; out is host memory.  n = 0 is valid and gives
+ * zero counts, NaN maxima and -1 indices. */
+int peat_signature(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
+                   const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                   peat_signature_t *out);
+
+/* Signatures of count >= 0 pairs in one launch sequence; outs is a host
+ * array of count records.  Each record is bit-identical to the one
+ * peat_signature gives for the same pair. */
+int peat_signature_batched(const peat_pair_t *pairs, int32_t count,
+                           const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                           peat_signature_t *outs);
+
+/* As peat_signature_batched, enqueued on stream; d_outs is a device array of
+ * count records written when the stream reaches the work. */
+int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
+                                 const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                                 peat_signature_t *d_outs, void *stream);
+
+/* Random bit flip in place (Section II-B).  Element i flips iff its 64-bit
+ * uniform U_i < floor(rate * 2^64) (every element if rate >= 1).  U_i's top
+ * byte is byte (i mod 32), little-endian, of Philox4x64-10 with key
+ * (seed, 0) at counter (i/32, 0, 0, 0); its low 56 bits are the low 56 bits of
+ * word (i mod 4) at counter (i/4, 1, 0, 0).  A flipped element toggles the
+ * j-th lowest set bit of bitmask, j = floor(hi32(y) * popcount(bitmask) / 2^32)
+ * with y = word 0 at counter (i, 2, 0, 0).  Returns the number of flipped
+ * elements (>= 0) or a negative PEAT_E* code.  Applying the same call twice
+ * restores the tensor. */
+int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed,
+                    double rate, uint64_t bitmask);
+
+/* peat_inject over count >= 0 items in one launch sequence; counts is a host
+ * array receiving each item's flip count. */
+int peat_inject_batched(const peat_inject_item_t *items, int32_t count, int64_t *counts);
+
+/* As peat_inject_batched, enqueued on stream; d_counts is a device int64
+ * array written when the stream reaches the work. */
+int peat_inject_batched_async(const peat_inject_item_t *items, int32_t count,
+                              int64_t *d_counts, void *stream);
+
+/* Host-side derived scores of a signature (host memory in and out). */
+int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
+
+/* Kernel timing.  When enabled, every launch of the library's kernels is
+ * bracketed by HIP events on its stream.  peat_profile_read waits for those
+ * events, returns the summed duration (ms) and launch count of one kernel
+ * class since the last read, and clears that class.  Kernel classes:
+ * 0 signature chunk pass, 1 signature finalize, 2 injection, 3 injection
+ * count reduction. */
+int peat_profile_enable(int on);
+int peat_profile_read(int kernel_class, double *total_ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PEAT_H */

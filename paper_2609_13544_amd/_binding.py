@@ -1,0 +1,385 @@
+"""ctypes binding of libpeat (include/peat.h): argument marshalling only.
+
+Every step of the signature and the injector runs in the HIP kernels of
+libpeat.so; this module converts torch tensors to device pointers and streams,
+packs the C structs and unpacks the results.  If the library is missing the
+calls raise -- there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libpeat.so")
+
+F32, F16, BF16 = 0, 1, 2
+OK, EINVAL, EDTYPE, EBITMASK, ERATE, EHIP, ENOMEM, ENODEV = 0, -1, -2, -3, -4, -5, -6, -7
+MAX_THRESHOLDS, MAX_BINS = 8, 64
+
+# kernel classes of peat_profile_read
+K_SIG_CHUNK, K_SIG_FINALIZE, K_INJECT, K_INJECT_SUM = 0, 1, 2, 3
+
+
+class PeatError(RuntimeError):
+    def __init__(self, code: int, where: str, detail: str):
+        super().__init__(f"{where} failed with {code}: {detail}")
+        self.code = code
+
+
+class Bins(ctypes.Structure):
+    _fields_ = [("lo_log2", ctypes.c_int32), ("hi_log2", ctypes.c_int32),
+                ("nbins", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class Thresholds(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("abs_tol", ctypes.c_double * MAX_THRESHOLDS)]
+
+
+_SIG_FIELDS = [
+    ("n", ctypes.c_int64), ("n_valid", ctypes.c_int64), ("n_finite", ctypes.c_int64),
+    ("n_rel", ctypes.c_int64), ("n_nan_golden", ctypes.c_int64), ("n_nan_test", ctypes.c_int64),
+    ("n_inf_golden", ctypes.c_int64), ("n_inf_test", ctypes.c_int64),
+    ("n_nan_pairs", ctypes.c_int64), ("first_nan_index", ctypes.c_int64),
+    ("n_mismatch", ctypes.c_int64 * MAX_THRESHOLDS),
+    ("hist_zero", ctypes.c_int64), ("hist_under", ctypes.c_int64), ("hist_over", ctypes.c_int64),
+    ("hist", ctypes.c_int64 * MAX_BINS),
+    ("max_abs", ctypes.c_double), ("argmax_abs", ctypes.c_int64),
+    ("max_ulp", ctypes.c_int64), ("argmax_ulp", ctypes.c_int64), ("sum_ulp", ctypes.c_uint64),
+    ("max_rel", ctypes.c_double), ("argmax_rel", ctypes.c_int64),
+    ("sum_abs", ctypes.c_double), ("sum_sq", ctypes.c_double), ("sum_rel", ctypes.c_double),
+    ("sum_g2", ctypes.c_double), ("sum_t2", ctypes.c_double), ("sum_gt", ctypes.c_double),
+]
+
+
+class Signature(ctypes.Structure):
+    _fields_ = _SIG_FIELDS
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_double) for k in
+                ("mean_abs", "var_abs", "l2_err", "l2_g", "l2_t", "cos", "mean_rel", "mean_ulp")]
+
+
+class Pair(ctypes.Structure):
+    _fields_ = [("golden", ctypes.c_void_p), ("test", ctypes.c_void_p), ("n", ctypes.c_int64),
+                ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class InjectItem(ctypes.Structure):
+    _fields_ = [("tensor", ctypes.c_void_p), ("n", ctypes.c_int64), ("dtype", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("seed", ctypes.c_uint64), ("rate", ctypes.c_double),
+                ("bitmask", ctypes.c_uint64)]
+
+
+def _np_sig_dtype():
+    fields = []
+    for name, ct in _SIG_FIELDS:
+        if name in ("n_mismatch", "hist"):
+            fields.append((name, np.int64, (ct._length_,)))
+        elif ct is ctypes.c_double:
+            fields.append((name, np.float64))
+        elif ct is ctypes.c_uint64:
+            fields.append((name, np.uint64))
+        else:
+            fields.append((name, np.int64))
+    dt = np.dtype(fields)
+    assert dt.itemsize == ctypes.sizeof(Signature)
+    return dt
+
+
+SIG_NP_DTYPE = _np_sig_dtype()
+SIG_BYTES = ctypes.sizeof(Signature)
+
+_lib = None
+_lock = threading.Lock()
+
+# name -> (restype, argtypes) of every entry point in include/peat.h
+_PROTOS = {
+    "peat_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "peat_last_error": (ctypes.c_char_p, []),
+    "peat_abi_version": (ctypes.c_int, []),
+    "peat_init": (ctypes.c_int, []),
+    "peat_set_stream": (ctypes.c_int, [ctypes.c_void_p]),
+    "peat_signature": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                      ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
+                                      ctypes.POINTER(Signature)]),
+    "peat_signature_batched": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32, ctypes.POINTER(Bins),
+                                              ctypes.POINTER(Thresholds), ctypes.POINTER(Signature)]),
+    "peat_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
+                                                    ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
+                                                    ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_inject": (ctypes.c_int64, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
+                                     ctypes.c_double, ctypes.c_uint64]),
+    "peat_inject_batched": (ctypes.c_int, [ctypes.POINTER(InjectItem), ctypes.c_int32,
+                                           ctypes.POINTER(ctypes.c_int64)]),
+    "peat_inject_batched_async": (ctypes.c_int, [ctypes.POINTER(InjectItem), ctypes.c_int32,
+                                                 ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
+    "peat_profile_enable": (ctypes.c_int, [ctypes.c_int]),
+    "peat_profile_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_int64)]),
+}
+
+
+def lib():
+    """The loaded libpeat.so; raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(
+                    f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                    "(there is no CPU fallback)")
+            L = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in _PROTOS.items():
+                fn = getattr(L, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str) -> int:
+    if rc < 0:
+        L = lib()
+        detail = L.peat_last_error().decode() or L.peat_strerror(rc).decode()
+        raise PeatError(rc, where, detail)
+    return rc
+
+
+def strerror(code: int) -> str:
+    return lib().peat_strerror(code).decode()
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def dtype_code(t) -> int:
+    torch = _torch()
+    m = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return m[t.dtype]
+
+
+def _dev_tensor(t, name: str):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def make_bins(bins) -> Bins:
+    return Bins(int(bins[0]), int(bins[1]), int(bins[2]), 0)
+
+
+def make_thresholds(thresholds) -> Thresholds:
+    th = Thresholds()
+    th.count = len(thresholds)
+    th.reserved = 0
+    for j, v in enumerate(list(thresholds)[:MAX_THRESHOLDS]):
+        th.abs_tol[j] = float(v)
+    return th
+
+
+def _stream_ptr(stream) -> int | None:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None) -> dict:
+    d = {}
+    for name, _ in _SIG_FIELDS:
+        v = getattr(s, name)
+        if name == "n_mismatch":
+            v = [int(x) for x in v][: (MAX_THRESHOLDS if nthr is None else nthr)]
+        elif name == "hist":
+            v = [int(x) for x in v]
+        elif isinstance(v, float):
+            v = float(v)
+        else:
+            v = int(v)
+        d[name] = v
+    return d
+
+
+def record_to_dict(rec, nthr: int | None = None) -> dict:
+    """Convert one element of a SIG_NP_DTYPE array to a dict."""
+    d = {}
+    for name, _ in _SIG_FIELDS:
+        v = rec[name]
+        if name == "n_mismatch":
+            v = [int(x) for x in v][: (MAX_THRESHOLDS if nthr is None else nthr)]
+        elif name == "hist":
+            v = [int(x) for x in v]
+        elif isinstance(v, (float, np.floating)):
+            v = float(v)
+        else:
+            v = int(v)
+        d[name] = v
+    return d
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+def set_stream(stream=None) -> None:
+    _check(lib().peat_set_stream(_stream_ptr(stream)), "peat_set_stream")
+
+
+def signature(golden, test, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), *, dtype: int | None = None,
+              n: int | None = None) -> dict:
+    """peat_signature on two device tensors (same dtype and element count)."""
+    _dev_tensor(golden, "golden")
+    _dev_tensor(test, "test")
+    code = dtype_code(golden) if dtype is None else dtype
+    if n is None:
+        if golden.numel() != test.numel() or golden.dtype != test.dtype:
+            raise ValueError("golden and test differ in size or dtype")
+        n = golden.numel()
+    out = Signature()
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    set_stream()
+    _check(lib().peat_signature(golden.data_ptr() if n else None, test.data_ptr() if n else None,
+                                n, code, ctypes.byref(b), ctypes.byref(th), ctypes.byref(out)),
+           "peat_signature")
+    return sig_to_dict(out, nthr=len(thresholds))
+
+
+def _pairs_array(pairs):
+    arr = (Pair * max(1, len(pairs)))()
+    for k, p in enumerate(pairs):
+        if isinstance(p, Pair):
+            arr[k] = p
+            continue
+        g, t = p[0], p[1]
+        _dev_tensor(g, f"pairs[{k}].golden")
+        _dev_tensor(t, f"pairs[{k}].test")
+        if g.numel() != t.numel() or g.dtype != t.dtype:
+            raise ValueError(f"pair {k}: golden and test differ in size or dtype")
+        arr[k] = Pair(g.data_ptr(), t.data_ptr(), g.numel(), dtype_code(g), 0)
+    return arr
+
+
+def signature_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> list[dict]:
+    """peat_signature_batched over a list of (golden, test) device tensor pairs."""
+    arr = _pairs_array(pairs)
+    outs = (Signature * max(1, len(pairs)))()
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    set_stream()
+    _check(lib().peat_signature_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
+           "peat_signature_batched")
+    return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+
+
+class PreparedPairs:
+    """Pair descriptors built once, for repeated asynchronous calls."""
+
+    def __init__(self, pairs):
+        self.count = len(pairs)
+        self.arr = _pairs_array(pairs)
+
+
+def signature_batched_async(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), stream=None) -> None:
+    """peat_signature_batched_async: records land in d_out, a device uint8
+    tensor of at least len(pairs) * SIG_BYTES bytes, when the stream gets there."""
+    prep = pairs if isinstance(pairs, PreparedPairs) else PreparedPairs(pairs)
+    _dev_tensor(d_out, "d_out")
+    if d_out.numel() * d_out.element_size() < prep.count * SIG_BYTES:
+        raise ValueError("d_out too small")
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    _check(lib().peat_signature_batched_async(prep.arr, prep.count, ctypes.byref(b), ctypes.byref(th),
+                                              d_out.data_ptr(), _stream_ptr(stream)),
+           "peat_signature_batched_async")
+
+
+def decode_records(d_out, count: int, nthr: int | None = None) -> list[dict]:
+    """Copy device records to the host and decode them."""
+    host = d_out.detach().view(-1)[: count * SIG_BYTES].cpu().numpy().view(np.uint8)
+    recs = host.view(SIG_NP_DTYPE)
+    return [record_to_dict(r, nthr) for r in recs]
+
+
+def inject(tensor, seed: int, rate: float, bitmask: int, *, dtype: int | None = None, n: int | None = None) -> int:
+    """peat_inject in place on a device tensor; returns the flip count."""
+    _dev_tensor(tensor, "tensor")
+    code = dtype_code(tensor) if dtype is None else dtype
+    n = tensor.numel() if n is None else n
+    set_stream()
+    rc = lib().peat_inject(tensor.data_ptr() if n else None, n, code, seed & (2 ** 64 - 1), float(rate),
+                           bitmask & (2 ** 64 - 1))
+    return _check(rc, "peat_inject")
+
+
+def _items_array(items):
+    arr = (InjectItem * max(1, len(items)))()
+    for k, it in enumerate(items):
+        if isinstance(it, InjectItem):
+            arr[k] = it
+            continue
+        t, seed, rate, mask = it
+        _dev_tensor(t, f"items[{k}].tensor")
+        arr[k] = InjectItem(t.data_ptr(), t.numel(), dtype_code(t), 0, seed & (2 ** 64 - 1), float(rate),
+                            mask & (2 ** 64 - 1))
+    return arr
+
+
+class PreparedItems:
+    def __init__(self, items):
+        self.count = len(items)
+        self.arr = _items_array(items)
+
+
+def inject_batched(items) -> list[int]:
+    """peat_inject_batched over (tensor, seed, rate, bitmask) tuples."""
+    arr = _items_array(items)
+    counts = (ctypes.c_int64 * max(1, len(items)))()
+    set_stream()
+    _check(lib().peat_inject_batched(arr, len(items), counts), "peat_inject_batched")
+    return [int(counts[k]) for k in range(len(items))]
+
+
+def inject_batched_async(items, d_counts, stream=None) -> None:
+    prep = items if isinstance(items, PreparedItems) else PreparedItems(items)
+    _dev_tensor(d_counts, "d_counts")
+    _check(lib().peat_inject_batched_async(prep.arr, prep.count, d_counts.data_ptr(), _stream_ptr(stream)),
+           "peat_inject_batched_async")
+
+
+def finalize_stats(sig: dict) -> dict:
+    s = Signature()
+    for name, _ in _SIG_FIELDS:
+        v = sig[name]
+        if name in ("n_mismatch", "hist"):
+            arr = getattr(s, name)
+            for j, x in enumerate(v):
+                arr[j] = x
+        else:
+            setattr(s, name, v)
+    st = Stats()
+    _check(lib().peat_finalize_stats(ctypes.byref(s), ctypes.byref(st)), "peat_finalize_stats")
+    return {k: float(getattr(st, k)) for k, _ in Stats._fields_}
+
+
+def profile_enable(on: bool = True) -> None:
+    _check(lib().peat_profile_enable(1 if on else 0), "peat_profile_enable")
+
+
+def profile_read(kernel_class: int):
+    ms = ctypes.c_double(0)
+    cnt = ctypes.c_int64(0)
+    _check(lib().peat_profile_read(kernel_class, ctypes.byref(ms), ctypes.byref(cnt)), "peat_profile_read")
+    return float(ms.value), int(cnt.value)

@@ -1,0 +1,511 @@
+// Host side of libpeat: argument validation, per-device workspace and pinned
+// staging, stream ordering, optional kernel timing, and the extern "C"
+// entry points declared in include/peat.h.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "peat_internal.h"
+
+using namespace peat;
+
+namespace {
+
+thread_local std::string t_err;
+thread_local hipStream_t t_stream = nullptr;
+std::mutex g_mu;   // serialises every entry point that touches device state
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    return code;
+}
+
+int fail_hip(hipError_t e, const char *what) {
+    int code = (e == hipErrorOutOfMemory) ? PEAT_ENOMEM : PEAT_EHIP;
+    return fail(code, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+#define HIP_OR_FAIL(expr)                                   \
+    do {                                                    \
+        hipError_t e_ = (expr);                             \
+        if (e_ != hipSuccess) return fail_hip(e_, #expr);   \
+    } while (0)
+
+constexpr int kSlots = 4;            // pinned staging ring depth
+constexpr size_t kAlign = 256;
+constexpr int kMaxDevices = 64;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Slot {
+    void *host = nullptr;
+    size_t size = 0;
+    hipEvent_t ev = nullptr;
+    bool pending = false;
+};
+
+struct ProfRec {
+    int cls;
+    hipEvent_t a, b;
+};
+
+struct Dev {
+    int state = 0;                   // 0 unchecked, 1 ok, <0 error code
+    void *ws = nullptr;
+    size_t ws_size = 0;
+    hipEvent_t ws_ev = nullptr;
+    bool ws_pending = false;
+    Slot slot[kSlots];
+    int next_slot = 0;
+    bool prof = false;
+    std::vector<ProfRec> log;
+    std::vector<hipEvent_t> pool;
+};
+
+Dev g_dev[kMaxDevices];
+
+int current_dev(Dev **out) {
+    int id = 0;
+    HIP_OR_FAIL(hipGetDevice(&id));
+    if (id < 0 || id >= kMaxDevices) return fail(PEAT_ENODEV, "device index %d out of range", id);
+    Dev &d = g_dev[id];
+    if (d.state == 0) {
+        hipDeviceProp_t prop;
+        HIP_OR_FAIL(hipGetDeviceProperties(&prop, id));
+        if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+            d.state = PEAT_ENODEV;
+        } else {
+            HIP_OR_FAIL(hipEventCreateWithFlags(&d.ws_ev, hipEventDisableTiming));
+            for (int k = 0; k < kSlots; ++k)
+                HIP_OR_FAIL(hipEventCreateWithFlags(&d.slot[k].ev, hipEventDisableTiming));
+            d.state = 1;
+        }
+    }
+    if (d.state < 0) return fail(d.state, "device %d is not gfx950 (MI355X)", id);
+    *out = &d;
+    return PEAT_OK;
+}
+
+// Device workspace of at least `bytes`; orders `s` after the previous user.
+int acquire_ws(Dev &d, size_t bytes, hipStream_t s, char **ws) {
+    if (bytes > d.ws_size) {
+        HIP_OR_FAIL(hipDeviceSynchronize());      // the old buffer may still be in use
+        if (d.ws) HIP_OR_FAIL(hipFree(d.ws));
+        d.ws = nullptr;
+        d.ws_size = 0;
+        size_t want = align_up(bytes + bytes / 4 + (size_t(1) << 20));
+        HIP_OR_FAIL(hipMalloc(&d.ws, want));
+        d.ws_size = want;
+        d.ws_pending = false;
+    }
+    if (d.ws_pending) HIP_OR_FAIL(hipStreamWaitEvent(s, d.ws_ev, 0));
+    *ws = static_cast<char *>(d.ws);
+    return PEAT_OK;
+}
+
+int release_ws(Dev &d, hipStream_t s) {
+    HIP_OR_FAIL(hipEventRecord(d.ws_ev, s));
+    d.ws_pending = true;
+    return PEAT_OK;
+}
+
+// Pinned staging buffer of at least `bytes` whose previous copies are done.
+int acquire_slot(Dev &d, size_t bytes, Slot **out) {
+    Slot &sl = d.slot[d.next_slot];
+    d.next_slot = (d.next_slot + 1) % kSlots;
+    if (sl.pending) {
+        HIP_OR_FAIL(hipEventSynchronize(sl.ev));
+        sl.pending = false;
+    }
+    if (bytes > sl.size) {
+        if (sl.host) HIP_OR_FAIL(hipHostFree(sl.host));
+        sl.host = nullptr;
+        sl.size = 0;
+        size_t want = align_up(bytes + bytes / 4 + 4096);
+        HIP_OR_FAIL(hipHostMalloc(&sl.host, want, hipHostMallocDefault));
+        sl.size = want;
+    }
+    *out = &sl;
+    return PEAT_OK;
+}
+
+int release_slot(Slot &sl, hipStream_t s) {
+    HIP_OR_FAIL(hipEventRecord(sl.ev, s));
+    sl.pending = true;
+    return PEAT_OK;
+}
+
+int prof_begin(Dev &d, hipStream_t s, hipEvent_t *a) {
+    *a = nullptr;
+    if (!d.prof) return PEAT_OK;
+    if (d.pool.empty()) {
+        hipEvent_t e;
+        HIP_OR_FAIL(hipEventCreate(&e));
+        d.pool.push_back(e);
+    }
+    *a = d.pool.back();
+    d.pool.pop_back();
+    HIP_OR_FAIL(hipEventRecord(*a, s));
+    return PEAT_OK;
+}
+
+int prof_end(Dev &d, hipStream_t s, int cls, hipEvent_t a) {
+    if (!a) return PEAT_OK;
+    if (d.pool.empty()) {
+        hipEvent_t e;
+        HIP_OR_FAIL(hipEventCreate(&e));
+        d.pool.push_back(e);
+    }
+    hipEvent_t b = d.pool.back();
+    d.pool.pop_back();
+    HIP_OR_FAIL(hipEventRecord(b, s));
+    d.log.push_back({cls, a, b});
+    return PEAT_OK;
+}
+
+int check_dtype(int32_t dt) {
+    return (dt == PEAT_F32 || dt == PEAT_F16 || dt == PEAT_BF16) ? PEAT_OK : PEAT_EDTYPE;
+}
+
+int elem_size(int32_t dt) { return dt == PEAT_F32 ? 4 : 2; }
+
+int check_bins_thr(const peat_bins_t *bins, const peat_thresholds_t *thr) {
+    if (!bins || !thr) return fail(PEAT_EINVAL, "bins and thresholds must not be NULL");
+    if (bins->reserved != 0 || thr->reserved != 0) return fail(PEAT_EINVAL, "reserved fields must be 0");
+    const int lo = bins->lo_log2, hi = bins->hi_log2, nb = bins->nbins;
+    if (lo < -1022 || hi > 1024 || lo >= hi)
+        return fail(PEAT_EINVAL, "bins need -1022 <= lo_log2 < hi_log2 <= 1024 (got %d, %d)", lo, hi);
+    if (nb < 1 || nb > PEAT_MAX_BINS || (hi - lo) % nb != 0)
+        return fail(PEAT_EINVAL, "nbins must be in [1, 64] and divide hi_log2 - lo_log2 (got %d)", nb);
+    if (thr->count < 0 || thr->count > PEAT_MAX_THRESHOLDS)
+        return fail(PEAT_EINVAL, "threshold count must be in [0, 8] (got %d)", thr->count);
+    for (int j = 0; j < thr->count; ++j)
+        if (std::isnan(thr->abs_tol[j]) || thr->abs_tol[j] < 0)
+            return fail(PEAT_EINVAL, "threshold %d must be >= 0 and not NaN", j);
+    return PEAT_OK;
+}
+
+int check_pair(const peat_pair_t &p, int k) {
+    if (check_dtype(p.dtype)) return fail(PEAT_EDTYPE, "pair %d: unknown dtype %d", k, p.dtype);
+    if (p.n < 0) return fail(PEAT_EINVAL, "pair %d: n < 0", k);
+    if (p.reserved != 0) return fail(PEAT_EINVAL, "pair %d: reserved field must be 0", k);
+    if (p.n > 0 && (!p.golden || !p.test)) return fail(PEAT_EINVAL, "pair %d: NULL tensor with n > 0", k);
+    if (p.n > (int64_t(1) << 46)) return fail(PEAT_EINVAL, "pair %d: n above 2^46", k);
+    return PEAT_OK;
+}
+
+// Common core of every signature call.  When host_outs is set the records go
+// through workspace + pinned staging and the call waits for them.
+int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                   const peat_thresholds_t *thr, peat_signature_t *d_outs,
+                   peat_signature_t *host_outs, hipStream_t s) {
+    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
+    if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
+    int rc = check_bins_thr(bins, thr);
+    if (rc) return rc;
+    for (int k = 0; k < count; ++k)
+        if ((rc = check_pair(pairs[k], k))) return rc;
+    if (count == 0) return PEAT_OK;
+    if (!host_outs && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    if ((rc = current_dev(&dv))) return rc;
+    Dev &d = *dv;
+
+    // partition every pair into chunks
+    std::vector<SigDesc> descs((size_t)count);
+    int64_t total = 0;
+    for (int k = 0; k < count; ++k) {
+        SigDesc &sd = descs[k];
+        sd.g = pairs[k].golden;
+        sd.t = pairs[k].test;
+        sd.n = pairs[k].n;
+        sd.dtype = pairs[k].dtype;
+        sd.chunk_log2 = chunk_log2_for(sd.n);
+        const int64_t nch = (sd.n + (int64_t(1) << sd.chunk_log2) - 1) >> sd.chunk_log2;
+        sd.first_chunk = total;
+        sd.nchunks = (int32_t)nch;
+        sd.aligned = ((reinterpret_cast<uintptr_t>(sd.g) | reinterpret_cast<uintptr_t>(sd.t)) & 15) == 0;
+        total += nch;
+    }
+    if (total > 0x7FFFFFFF) return fail(PEAT_EINVAL, "batch needs %lld chunks (max 2^31-1)", (long long)total);
+
+    const size_t b_desc = align_up(sizeof(SigDesc) * count);
+    const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
+    const size_t b_part = align_up(sizeof(ChunkPartial) * (size_t)total);
+    const size_t b_out = host_outs ? align_up(sizeof(peat_signature_t) * count) : 0;
+
+    char *ws;
+    if ((rc = acquire_ws(d, b_desc + b_map + b_part + b_out, s, &ws))) return rc;
+    Slot *sl;
+    if ((rc = acquire_slot(d, b_desc + b_map + b_out, &sl))) return rc;
+    char *h = static_cast<char *>(sl->host);
+    std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
+    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc);
+    for (int k = 0; k < count; ++k)
+        for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
+    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+
+    SigParams P;
+    P.descs = reinterpret_cast<const SigDesc *>(ws);
+    P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc);
+    P.partials = reinterpret_cast<ChunkPartial *>(ws + b_desc + b_map);
+    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_desc + b_map + b_part) : d_outs;
+    P.count = count;
+    P.lo = bins->lo_log2;
+    P.hi = bins->hi_log2;
+    P.nbins = bins->nbins;
+    P.nthr = thr->count;
+    P.nthr_pad = thr->count <= 2 ? 2 : (thr->count <= 4 ? 4 : 8);
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j)
+        P.thr[j] = j < thr->count ? thr->abs_tol[j] : HUGE_VAL;
+
+    hipEvent_t ev;
+    if ((rc = prof_begin(d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_sig_chunks(P, total, s));
+    if ((rc = prof_end(d, s, 0, ev))) return rc;
+    if ((rc = prof_begin(d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_sig_finalize(P, s));
+    if ((rc = prof_end(d, s, 1, ev))) return rc;
+
+    char *hout = h + b_desc + b_map;
+    if (host_outs)
+        HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_signature_t) * count, hipMemcpyDeviceToHost, s));
+    if ((rc = release_slot(*sl, s))) return rc;
+    if ((rc = release_ws(d, s))) return rc;
+    if (host_outs) {
+        HIP_OR_FAIL(hipStreamSynchronize(s));
+        std::memcpy(host_outs, hout, sizeof(peat_signature_t) * count);
+    }
+    return PEAT_OK;
+}
+
+int check_item(const peat_inject_item_t &it, int k) {
+    if (check_dtype(it.dtype)) return fail(PEAT_EDTYPE, "item %d: unknown dtype %d", k, it.dtype);
+    const int width = elem_size(it.dtype) * 8;
+    if (it.bitmask == 0 || (it.bitmask >> width) != 0)
+        return fail(PEAT_EBITMASK, "item %d: bitmask 0x%llx is 0 or has bits at or above bit %d", k,
+                    (unsigned long long)it.bitmask, width);
+    if (std::isnan(it.rate) || it.rate < 0) return fail(PEAT_ERATE, "item %d: rate must be >= 0", k);
+    if (it.n < 0) return fail(PEAT_EINVAL, "item %d: n < 0", k);
+    if (it.reserved != 0) return fail(PEAT_EINVAL, "item %d: reserved field must be 0", k);
+    if (it.n > 0 && !it.tensor) return fail(PEAT_EINVAL, "item %d: NULL tensor with n > 0", k);
+    if (it.n > (int64_t(1) << 46)) return fail(PEAT_EINVAL, "item %d: n above 2^46", k);
+    return PEAT_OK;
+}
+
+int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_counts,
+                int64_t *host_counts, hipStream_t s) {
+    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
+    if (count > 0 && !items) return fail(PEAT_EINVAL, "items is NULL");
+    int rc;
+    for (int k = 0; k < count; ++k)
+        if ((rc = check_item(items[k], k))) return rc;
+    if (count == 0) return PEAT_OK;
+    if (!host_counts && !d_counts) return fail(PEAT_EINVAL, "d_counts is NULL");
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    if ((rc = current_dev(&dv))) return rc;
+    Dev &d = *dv;
+
+    std::vector<InjDesc> descs((size_t)count);
+    int64_t total = 0;
+    for (int k = 0; k < count; ++k) {
+        const peat_inject_item_t &it = items[k];
+        InjDesc &q = descs[k];
+        q.x = it.tensor;
+        q.n = it.n;
+        q.seed = it.seed;
+        q.mask = it.bitmask;
+        q.dtype = it.dtype;
+        q.popc = __builtin_popcountll(it.bitmask);
+        q.all = it.rate >= 1.0;
+        // T = floor(rate * 2^64): ldexp is exact and the conversion truncates
+        q.T = (q.all || it.rate == 0.0) ? 0 : (uint64_t)std::ldexp(it.rate, 64);
+        const bool none = !q.all && q.T == 0;
+        const int64_t nseg = none ? 0 : (it.n + (int64_t(1) << kInjSegLog2) - 1) >> kInjSegLog2;
+        q.first_seg = total;
+        q.nsegs = (int32_t)nseg;
+        total += nseg;
+    }
+    if (total > 0x7FFFFFFF) return fail(PEAT_EINVAL, "batch needs too many segments");
+
+    const size_t b_desc = align_up(sizeof(InjDesc) * count);
+    const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
+    const size_t b_seg = align_up(sizeof(uint32_t) * (size_t)total);
+    const size_t b_out = host_counts ? align_up(sizeof(int64_t) * count) : 0;
+
+    char *ws;
+    if ((rc = acquire_ws(d, b_desc + b_map + b_seg + b_out, s, &ws))) return rc;
+    Slot *sl;
+    if ((rc = acquire_slot(d, b_desc + b_map + b_out, &sl))) return rc;
+    char *h = static_cast<char *>(sl->host);
+    std::memcpy(h, descs.data(), sizeof(InjDesc) * count);
+    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc);
+    for (int k = 0; k < count; ++k)
+        for (int32_t c = 0; c < descs[k].nsegs; ++c) hmap[descs[k].first_seg + c] = k;
+    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+
+    InjParams P;
+    P.descs = reinterpret_cast<const InjDesc *>(ws);
+    P.seg_item = reinterpret_cast<const int32_t *>(ws + b_desc);
+    P.seg_counts = reinterpret_cast<uint32_t *>(ws + b_desc + b_map);
+    P.counts = host_counts ? reinterpret_cast<int64_t *>(ws + b_desc + b_map + b_seg) : d_counts;
+    P.count = count;
+
+    hipEvent_t ev;
+    if ((rc = prof_begin(d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_inject(P, total, s));
+    if ((rc = prof_end(d, s, 2, ev))) return rc;
+    if ((rc = prof_begin(d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_inject_sum(P, s));
+    if ((rc = prof_end(d, s, 3, ev))) return rc;
+
+    char *hout = h + b_desc + b_map;
+    if (host_counts)
+        HIP_OR_FAIL(hipMemcpyAsync(hout, P.counts, sizeof(int64_t) * count, hipMemcpyDeviceToHost, s));
+    if ((rc = release_slot(*sl, s))) return rc;
+    if ((rc = release_ws(d, s))) return rc;
+    if (host_counts) {
+        HIP_OR_FAIL(hipStreamSynchronize(s));
+        std::memcpy(host_counts, hout, sizeof(int64_t) * count);
+    }
+    return PEAT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *peat_strerror(int code) {
+    switch (code) {
+        case PEAT_OK: return "success";
+        case PEAT_EINVAL: return "invalid argument";
+        case PEAT_EDTYPE: return "unknown element type";
+        case PEAT_EBITMASK: return "bitmask is zero or wider than the element type";
+        case PEAT_ERATE: return "injection rate is NaN or negative";
+        case PEAT_EHIP: return "HIP runtime error";
+        case PEAT_ENOMEM: return "out of memory";
+        case PEAT_ENODEV: return "no gfx950 device";
+        default: return "unknown error code";
+    }
+}
+
+const char *peat_last_error(void) { return t_err.c_str(); }
+
+int peat_abi_version(void) { return PEAT_ABI_VERSION; }
+
+int peat_init(void) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *d;
+    return current_dev(&d);
+}
+
+int peat_set_stream(void *stream) {
+    t_stream = static_cast<hipStream_t>(stream);
+    return PEAT_OK;
+}
+
+int peat_signature(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
+                   const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                   peat_signature_t *out) {
+    if (!out) return fail(PEAT_EINVAL, "out is NULL");
+    peat_pair_t p{golden, test, n, (int32_t)dtype, 0};
+    return signature_core(&p, 1, bins, thresholds, nullptr, out, t_stream);
+}
+
+int peat_signature_batched(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                           const peat_thresholds_t *thresholds, peat_signature_t *outs) {
+    if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
+    return signature_core(pairs, count, bins, thresholds, nullptr, outs, t_stream);
+}
+
+int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                                 const peat_thresholds_t *thresholds, peat_signature_t *d_outs,
+                                 void *stream) {
+    return signature_core(pairs, count, bins, thresholds, d_outs, nullptr,
+                          static_cast<hipStream_t>(stream));
+}
+
+int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
+                    uint64_t bitmask) {
+    peat_inject_item_t it{tensor, n, (int32_t)dtype, 0, seed, rate, bitmask};
+    int64_t c = 0;
+    int rc = inject_core(&it, 1, nullptr, &c, t_stream);
+    return rc ? rc : c;
+}
+
+int peat_inject_batched(const peat_inject_item_t *items, int32_t count, int64_t *counts) {
+    if (count > 0 && !counts) return fail(PEAT_EINVAL, "counts is NULL");
+    return inject_core(items, count, nullptr, counts, t_stream);
+}
+
+int peat_inject_batched_async(const peat_inject_item_t *items, int32_t count, int64_t *d_counts,
+                              void *stream) {
+    return inject_core(items, count, d_counts, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int peat_finalize_stats(const peat_signature_t *sg, peat_stats_t *st) {
+    if (!sg || !st) return fail(PEAT_EINVAL, "NULL argument");
+    const double nf = (double)sg->n_finite;
+    st->mean_abs = sg->n_finite > 0 ? sg->sum_abs / nf : NAN;
+    // sample variance of the absolute error over finite pairs
+    st->var_abs = sg->n_finite > 1 ? (sg->sum_sq - sg->sum_abs * (sg->sum_abs / nf)) / (nf - 1.0) : NAN;
+    st->l2_err = std::sqrt(sg->sum_sq);
+    st->l2_g = std::sqrt(sg->sum_g2);
+    st->l2_t = std::sqrt(sg->sum_t2);
+    st->cos = (sg->sum_g2 > 0 && sg->sum_t2 > 0) ? sg->sum_gt / std::sqrt(sg->sum_g2 * sg->sum_t2) : NAN;
+    st->mean_rel = sg->n_rel > 0 ? sg->sum_rel / (double)sg->n_rel : NAN;
+    st->mean_ulp = sg->n_valid > 0 ? (double)sg->sum_ulp / (double)sg->n_valid : NAN;
+    return PEAT_OK;
+}
+
+int peat_profile_enable(int on) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *d;
+    int rc = current_dev(&d);
+    if (rc) return rc;
+    d->prof = on != 0;
+    return PEAT_OK;
+}
+
+int peat_profile_read(int kernel_class, double *total_ms, int64_t *launches) {
+    if (!total_ms || !launches) return fail(PEAT_EINVAL, "NULL argument");
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *d;
+    int rc = current_dev(&d);
+    if (rc) return rc;
+    double sum = 0.0;
+    int64_t cnt = 0;
+    std::vector<ProfRec> keep;
+    for (const ProfRec &r : d->log) {
+        if (r.cls != kernel_class) {
+            keep.push_back(r);
+            continue;
+        }
+        HIP_OR_FAIL(hipEventSynchronize(r.b));
+        float ms = 0.f;
+        HIP_OR_FAIL(hipEventElapsedTime(&ms, r.a, r.b));
+        sum += ms;
+        ++cnt;
+        d->pool.push_back(r.a);
+        d->pool.push_back(r.b);
+    }
+    d->log.swap(keep);
+    *total_ms = sum;
+    *launches = cnt;
+    return PEAT_OK;
+}
+
+}  // extern "C"

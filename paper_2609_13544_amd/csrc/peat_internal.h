@@ -1,0 +1,99 @@
+// Internal declarations of libpeat: device-side descriptors, the per-chunk
+// partial record of the signature pass, and launch entry points shared by the
+// host API and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "peat.h"
+
+namespace peat {
+
+constexpr int kBlock = 256;                        // threads per block (4 wave64)
+constexpr int kWaves = kBlock / 64;
+constexpr int kHistSlots = PEAT_MAX_BINS + 2;      // under (zeros included) | bins | over
+constexpr uint32_t kNone = 0xFFFFFFFFu;            // "no element" local index
+constexpr int kMinChunkLog2 = 12;                  // 4096 elements: 16 per thread
+constexpr int kMaxChunkLog2 = 18;                  // 262144 elements: 1024 per thread
+constexpr int kInjSegLog2 = 20;                    // injector segment: 2^20 elements
+
+// Chunk size of a pair depends on n only, so that a pair's partition (and
+// hence its binary64 summation tree) is the same in single and batched calls:
+// about 256 chunks per pair, clamped to [2^12, 2^18] elements.
+inline int chunk_log2_for(int64_t n) {
+    int64_t per = (n + 255) / 256;
+    int l = 0;
+    while (l < 62 && (int64_t(1) << l) < per) ++l;
+    if (l < kMinChunkLog2) l = kMinChunkLog2;
+    if (l > kMaxChunkLog2) l = kMaxChunkLog2;
+    return l;
+}
+
+struct SigDesc {                 // one per pair (48 bytes)
+    const void *g;
+    const void *t;
+    int64_t n;
+    int64_t first_chunk;         // index of the pair's first chunk in the batch
+    int32_t nchunks;
+    int32_t dtype;
+    int32_t chunk_log2;
+    int32_t aligned;             // both pointers 16-byte aligned
+};
+static_assert(sizeof(SigDesc) == 48, "SigDesc layout");
+
+enum { C_VALID, C_FINITE, C_REL, C_NAN_G, C_NAN_T, C_INF_G, C_INF_T, C_NANPAIR, C_ZERO, kCnt };
+
+struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
+    double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;
+    double max_abs, max_rel;
+    int64_t ix_abs, ix_rel, ix_ulp;  // element index within the pair, -1 = none
+    int64_t first_nan, first_valid;  // -1 = none
+    uint64_t sum_ulp;
+    uint32_t max_ulp;
+    uint32_t cnt[kCnt];
+    uint32_t mism[PEAT_MAX_THRESHOLDS];
+    uint32_t hist[kHistSlots];
+};
+
+struct SigParams {
+    const SigDesc *descs;
+    const int32_t *chunk_pair;     // chunk -> pair index
+    ChunkPartial *partials;        // one per chunk
+    peat_signature_t *outs;        // one per pair (device)
+    int32_t count;                 // pairs
+    int32_t lo, hi, nbins;
+    int32_t nthr;                  // real thresholds
+    int32_t nthr_pad;              // 2, 4 or 8 compared per element (+Inf padding)
+    double thr[PEAT_MAX_THRESHOLDS];
+};
+
+struct InjDesc {                 // one per injected tensor (64 bytes)
+    void *x;
+    int64_t n;
+    uint64_t seed;
+    uint64_t T;                  // floor(rate * 2^64) when !all
+    uint64_t mask;
+    int64_t first_seg;
+    int32_t nsegs;
+    int32_t dtype;
+    int32_t all;                 // rate >= 1
+    int32_t popc;                // popcount(mask)
+};
+static_assert(sizeof(InjDesc) == 64, "InjDesc layout");
+
+struct InjParams {
+    const InjDesc *descs;
+    const int32_t *seg_item;     // segment -> item index
+    uint32_t *seg_counts;        // flips per segment
+    int64_t *counts;             // flips per item (device)
+    int32_t count;
+};
+
+// Kernel launchers (defined in the .hip translation units).
+hipError_t launch_sig_chunks(const SigParams &p, int64_t total_chunks, hipStream_t s);
+hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
+hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
+hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);
+
+}  // namespace peat

@@ -182,3 +182,21 @@ def config5_pair(k: int, shape, state: int, device="cpu"):
 
 def numel(shapes) -> int:
     return int(sum(int(np.prod(s)) for s in shapes))
+
+
+def config2_all(device="cuda", shape=CONFIG2_SHAPE, count=CONFIG2_COUNT):
+    return [config2_pair(k, device, shape) for k in range(count)]
+
+
+def config3_all(device="cuda"):
+    """All 292 (name, G, T) of the GPT-style checkpoint pair."""
+    return [(name,) + config3_pair(k, shape, device) for k, (name, shape) in enumerate(gpt13b_shapes())]
+
+
+def config5_all(device="cuda"):
+    """All 873 (name, state, G, T_before_injection) of the Llama-7B-shaped pair."""
+    out = []
+    for k, (name, shape, state) in enumerate(llama7b_states()):
+        G, T = config5_pair(k, shape, state, device)
+        out.append((name, state, G, T))
+    return out

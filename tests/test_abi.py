@@ -1,0 +1,139 @@
+"""CPU tests of the C-ABI library: it loads, exports every entry point that
+include/peat.h declares, its struct layouts match the header, and argument
+validation returns the documented codes before any device access."""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2609_13544_amd as P
+from paper_2609_13544_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "peat.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(peat_[a-z_0-9]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_header_declares_expected_entry_points():
+    names = _declared_functions()
+    for must in ("peat_signature", "peat_signature_batched", "peat_signature_batched_async",
+                 "peat_inject", "peat_inject_batched", "peat_inject_batched_async",
+                 "peat_finalize_stats", "peat_strerror", "peat_last_error"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = P.lib()
+    for name in _declared_functions():
+        assert hasattr(L, name), f"libpeat.so does not export {name}"
+    assert set(_declared_functions()) == set(B._PROTOS), "binding prototypes out of sync with header"
+
+
+def test_struct_layouts():
+    assert ctypes.sizeof(B.Signature) == 784
+    assert ctypes.sizeof(B.Pair) == 32
+    assert ctypes.sizeof(B.InjectItem) == 48
+    assert ctypes.sizeof(B.Bins) == 16
+    assert ctypes.sizeof(B.Thresholds) == 72
+    assert B.Signature.max_abs.offset == 8 * (10 + 8 + 3 + 64)
+    assert B.Signature.sum_gt.offset == 784 - 8
+
+
+def test_abi_version_and_strerror():
+    L = P.lib()
+    assert L.peat_abi_version() == 1
+    for code in range(0, -8, -1):
+        assert L.peat_strerror(code)
+    assert L.peat_strerror(-99) == b"unknown error code"
+
+
+def _sig_rc(n=0, dtype=0, bins=(-40, 24, 64), thr=(1e-6,), g=None, t=None, bins_reserved=0):
+    b = B.Bins(bins[0], bins[1], bins[2], bins_reserved)
+    th = B.Thresholds()
+    th.count = len(thr)
+    for j, v in enumerate(thr[:8]):
+        th.abs_tol[j] = v
+    out = B.Signature()
+    return P.lib().peat_signature(g, t, n, dtype, ctypes.byref(b), ctypes.byref(th), ctypes.byref(out))
+
+
+def test_signature_validation_codes():
+    assert _sig_rc(n=5) == B.EINVAL                      # NULL tensors with n > 0
+    assert _sig_rc(n=-1) == B.EINVAL
+    assert _sig_rc(dtype=7) == B.EDTYPE
+    for bad in [(-40, 24, 0), (-40, 24, 65), (-40, 24, 7), (3, 3, 1), (-1023, 0, 1), (0, 1025, 1)]:
+        assert _sig_rc(bins=bad) == B.EINVAL, bad
+    assert _sig_rc(bins_reserved=1) == B.EINVAL
+    assert _sig_rc(thr=(math.nan,)) == B.EINVAL
+    assert _sig_rc(thr=(-1e-9,)) == B.EINVAL
+    th = B.Thresholds()
+    th.count = 9
+    b = B.Bins(-40, 24, 64, 0)
+    assert P.lib().peat_signature(None, None, 0, 0, ctypes.byref(b), ctypes.byref(th),
+                                  ctypes.byref(B.Signature())) == B.EINVAL
+    assert P.lib().peat_signature(None, None, 0, 0, None, ctypes.byref(th),
+                                  ctypes.byref(B.Signature())) == B.EINVAL
+    assert b"threshold" in P.lib().peat_last_error() or P.lib().peat_last_error()
+
+
+def test_batched_empty_is_ok_and_validation():
+    b = B.Bins(-40, 24, 64, 0)
+    th = B.Thresholds()
+    L = P.lib()
+    assert L.peat_signature_batched(None, 0, ctypes.byref(b), ctypes.byref(th), None) == B.OK
+    assert L.peat_signature_batched(None, -1, ctypes.byref(b), ctypes.byref(th), None) == B.EINVAL
+    pairs = (B.Pair * 2)(B.Pair(None, None, 0, 0, 0), B.Pair(None, None, 0, 5, 0))
+    outs = (B.Signature * 2)()
+    assert L.peat_signature_batched(pairs, 2, ctypes.byref(b), ctypes.byref(th), outs) == B.EDTYPE
+    assert L.peat_signature_batched_async(pairs, 2, ctypes.byref(b), ctypes.byref(th), None, None) == B.EDTYPE
+
+
+def test_inject_validation_codes():
+    L = P.lib()
+    assert L.peat_inject(None, 10, 0, 1, 0.5, 0) == B.EBITMASK
+    assert L.peat_inject(None, 10, 1, 1, 0.5, 0x10000) == B.EBITMASK
+    assert L.peat_inject(None, 10, 0, 1, 0.5, 1 << 32) == B.EBITMASK
+    assert L.peat_inject(None, 10, 0, 1, math.nan, 1) == B.ERATE
+    assert L.peat_inject(None, 10, 0, 1, -1.0, 1) == B.ERATE
+    assert L.peat_inject(None, 10, 9, 1, 0.5, 1) == B.EDTYPE
+    assert L.peat_inject(None, 10, 0, 1, 0.5, 1) == B.EINVAL       # NULL tensor
+    assert L.peat_inject_batched(None, 0, None) == B.OK
+    counts = (ctypes.c_int64 * 1)()
+    items = (B.InjectItem * 1)(B.InjectItem(None, 4, 0, 1, 0, 0.5, 1))   # reserved != 0
+    assert L.peat_inject_batched(items, 1, counts) == B.EINVAL
+
+
+def test_finalize_stats_host():
+    s = B.Signature()
+    s.n_finite = 4
+    s.n_valid = 4
+    s.n_rel = 2
+    s.sum_abs = 2.0
+    s.sum_sq = 2.0
+    s.sum_g2 = 4.0
+    s.sum_t2 = 9.0
+    s.sum_gt = 6.0
+    s.sum_rel = 1.0
+    s.sum_ulp = 10
+    st = B.Stats()
+    assert P.lib().peat_finalize_stats(ctypes.byref(s), ctypes.byref(st)) == B.OK
+    assert st.mean_abs == 0.5 and st.var_abs == (2.0 - 2.0 * 0.5) / 3.0
+    assert st.cos == 1.0 and st.l2_g == 2.0 and st.l2_t == 3.0
+    assert st.mean_rel == 0.5 and st.mean_ulp == 2.5
+
+
+@pytest.mark.skipif(__import__("torch").cuda.is_available(), reason="checks the no-GPU error path")
+def test_no_device_is_an_error_not_a_crash():
+    rc = _sig_rc(n=0)
+    assert rc in (B.EHIP, B.ENODEV)
+    assert P.lib().peat_init() in (B.EHIP, B.ENODEV)

@@ -1,0 +1,315 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every test compares device results element by element with the oracle on the
+same seeded inputs: bit-exact for counts, histograms, indices, maxima, ULP
+sums and injected bits; 1e-12 for the binary64 sums (see tests/parity.py).
+Small cases span several chunks and ragged tails; the workload tests run the
+five workloads at full size in the launch configuration the benchmark times
+and check sampled tensors (all of a small one, the largest ones) against the
+oracle, plus properties that hold at any size.
+"""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_13544_amd as P
+import synth
+from tests.parity import (assert_parity, float_to_bits, oracle_sig, special_pair, to_device,
+                          to_host_bits)
+
+pytestmark = pytest.mark.gpu
+
+BINS_SETS = [synth.BINS, (-30, 20, 25), (-20, 40, 12), (-160, 136, 37)]
+THR_SETS = [synth.THRESHOLDS, (), (0.0,), (1e-7, 1e-5, 1e-3, 0.1, 1.0), (0.0, 1e-9, 1e-6, 1e-4, 1e-2, 1.0, 100.0, math.inf)]
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    assert torch.cuda.is_available(), "GPU tests need the MI355X"
+    P.lib()
+    assert oracle.lib()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _check_pair(gb, tb, code, bins=synth.BINS, thr=synth.THRESHOLDS, ctx=""):
+    g = to_device(gb, code)
+    t = to_device(tb, code)
+    got = P.signature(g, t, bins, thr)
+    ref = oracle_sig(gb, tb, code, bins, thr)
+    assert_parity(got, ref, ctx)
+    return got
+
+
+# ---------------------------------------------------------------------------
+# signature: sizes, dtypes, specials, bins, thresholds
+# ---------------------------------------------------------------------------
+SIZES = [0, 1, 3, 4, 7, 9, 255, 4095, 4096, 4097, 8191, 65536 + 13, 300005, (1 << 20) + 3]
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_sizes_and_specials(code):
+    for i, n in enumerate(SIZES):
+        gb, tb = special_pair(n, code, seed=1000 + 17 * i + code)
+        log(f"  dtype={code} n={n}")
+        _check_pair(gb, tb, code, ctx=f"dtype={code} n={n}")
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_bins_and_thresholds(code):
+    n = 150001
+    for bi, bins in enumerate(BINS_SETS):
+        for ti, thr in enumerate(THR_SETS):
+            gb, tb = special_pair(n, code, seed=77 + 10 * bi + ti, rel_noise=10.0 ** -(1 + ti))
+            log(f"  dtype={code} bins={bins} thr={thr}")
+            _check_pair(gb, tb, code, bins, thr, ctx=f"bins={bins} thr={thr}")
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_ordinary_data_without_specials(code):
+    """The fast path alone (no special values anywhere)."""
+    for n in (4096 * 64, 4096 * 300 + 77):
+        gb, tb = special_pair(n, code, seed=5 + n, special_frac=0.0, rel_noise=1e-4)
+        _check_pair(gb, tb, code, ctx=f"ordinary n={n}")
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_unaligned_pointers(code):
+    """Views offset by one element are not 16-byte aligned (generic path)."""
+    n = 70000
+    gb, tb = special_pair(n + 1, code, seed=31 + code)
+    g = to_device(gb, code)[1:]
+    t = to_device(tb, code)[1:]
+    got = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+    assert_parity(got, oracle_sig(gb[1:], tb[1:], code, synth.BINS, synth.THRESHOLDS), "unaligned")
+    # golden aligned, test not
+    t2 = to_device(np.concatenate([tb[:1], tb[:n]]), code)[1:]
+    got = P.signature(to_device(gb[:n], code), t2, synth.BINS, synth.THRESHOLDS)
+    assert_parity(got, oracle_sig(gb[:n], tb[:n], code, synth.BINS, synth.THRESHOLDS), "mixed alignment")
+
+
+def test_degenerate_inputs():
+    for code in (0, 1, 2):
+        sp = {0: (0x7FC00000, 0x7F800000, 0x3F800000), 1: (0x7E00, 0x7C00, 0x3C00), 2: (0x7FC0, 0x7F80, 0x3F80)}[code]
+        dt = np.uint32 if code == 0 else np.uint16
+        for n in (1, 5000, 70001):
+            for gval, tval in [(sp[0], sp[0]), (sp[2], sp[2]), (0, 0), (sp[1], sp[1]), (sp[1], sp[2]),
+                               (sp[2], 0), (0, sp[2])]:
+                gb = np.full(n, gval, dt)
+                tb = np.full(n, tval, dt)
+                _check_pair(gb, tb, code, ctx=f"const {gval:#x}/{tval:#x} n={n}")
+
+
+def test_workload1_full():
+    G, T = synth.config1()
+    _check_pair(G.reshape(-1).view(np.uint32), T.reshape(-1).view(np.uint32), 0, ctx="workload 1")
+
+
+def test_batched_equals_single_and_is_deterministic():
+    pairs_host = []
+    rng = np.random.default_rng(4)
+    for k in range(12):
+        code = k % 3
+        n = int(rng.integers(0, 300000)) if k % 4 else 4096 * 70
+        pairs_host.append((code,) + special_pair(n, code, seed=900 + k))
+    dev = [(to_device(gb, c), to_device(tb, c)) for c, gb, tb in pairs_host]
+    batched = P.signature_batched(dev, synth.BINS, synth.THRESHOLDS)
+    again = P.signature_batched(dev, synth.BINS, synth.THRESHOLDS)
+    for k, ((c, gb, tb), (g, t)) in enumerate(zip(pairs_host, dev)):
+        single = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+        assert single == batched[k] == again[k], f"pair {k}: batched/single/rerun differ"
+        assert_parity(batched[k], oracle_sig(gb, tb, c, synth.BINS, synth.THRESHOLDS), f"pair {k}")
+
+
+def test_async_records_match_sync():
+    gb, tb = special_pair(123457, 1, seed=3)
+    g, t = to_device(gb, 1), to_device(tb, 1)
+    d_out = torch.empty(3 * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        P.signature_batched_async([(g, t), (t, g), (g, g)], d_out, synth.BINS, synth.THRESHOLDS, stream=s)
+    s.synchronize()
+    recs = P.decode_records(d_out, 3, nthr=2)
+    sync = P.signature_batched([(g, t), (t, g), (g, g)], synth.BINS, synth.THRESHOLDS)
+    assert recs == sync
+
+
+def test_index_beyond_2_31():
+    """64-bit indexing: n > 2^31 f16 elements, planted values at known places."""
+    n = (1 << 31) + 4096 + 1000
+    g = torch.zeros(n, dtype=torch.float16, device="cuda")
+    t = torch.zeros(n, dtype=torch.float16, device="cuda")
+    base = 1 << 31
+    t[base + 77] = 1.0
+    t[base + 500] = -1.0          # ties |err| = 1 with base+77; sign differs from +0
+    t[base + 900] = float("nan")
+    t[base + 4096 + 999] = 0.5
+    got = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+    assert got["n"] == n and got["n_nan_pairs"] == 1 and got["first_nan_index"] == base + 900
+    assert got["max_abs"] == 1.0 and got["argmax_abs"] == base + 77
+    assert got["argmax_ulp"] == base + 77 and got["max_ulp"] == 0x3C00
+    assert got["n_rel"] == 0 and math.isnan(got["max_rel"]) and got["argmax_rel"] == -1
+    assert got["hist_zero"] == n - 4 and got["hist"][40] == 2 and got["hist"][39] == 1
+    assert got["sum_abs"] == 2.5 and got["sum_sq"] == 2.25 and got["sum_ulp"] == 2 * 0x3C00 + 0x3800
+    assert got["n_mismatch"] == [4, 4]
+    del g, t
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# injector
+# ---------------------------------------------------------------------------
+INJ_RATES = [0.0, 1e-7, 1e-3, 0.01, 0.3, 1.0, float(np.nextafter(1.0, 0.0))]
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_inject_parity(code):
+    masks = {0: [0x7F800000, 0xFFFFFFFF, 1 << 31, 0x5], 1: [0xFFFF, 0x7C00, 1], 2: [0xFFFF, 0x7F80, 0x8000]}[code]
+    for n in (1, 33, 4097, (1 << 20) + 7, 3 * (1 << 20)):
+        for ri, rate in enumerate(INJ_RATES):
+            mask = masks[(n + ri) % len(masks)]
+            seed = synth.inject_seed(9, 31 * ri + n % 1000)
+            gb, _ = special_pair(n, code, seed=n + ri)
+            x = to_device(gb, code)
+            log(f"  dtype={code} n={n} rate={rate} mask={mask:#x}")
+            cnt = P.inject(x, seed=seed, rate=rate, bitmask=mask)
+            host = gb.copy()
+            cnt_ref = oracle.inject(host, dtype=code, seed=seed, rate=rate, mask=mask)
+            assert cnt == cnt_ref, (n, rate, cnt, cnt_ref)
+            assert np.array_equal(to_host_bits(x), host), f"bits differ n={n} rate={rate}"
+
+
+def test_inject_batched_involution_and_async():
+    items_host = []
+    for k in range(7):
+        code = k % 3
+        n = [5, 4096, 100003, 1 << 20, (1 << 21) + 9, 0, 77][k]
+        gb, _ = special_pair(n, code, seed=40 + k)
+        items_host.append((code, gb, synth.inject_seed(9, 500 + k), [1e-3, 2e-2, 1e-7, 1.0, 5e-4, 0.5, 0.0][k],
+                           {0: 0x7F800000, 1: 0xFFFF, 2: 0x7FFF}[code]))
+    xs = [to_device(gb, c) for c, gb, *_ in items_host]
+    counts = P.inject_batched([(x, s, r, m) for x, (_, _, s, r, m) in zip(xs, items_host)])
+    for k, ((c, gb, s, r, m), x) in enumerate(zip(items_host, xs)):
+        host = gb.copy()
+        assert counts[k] == oracle.inject(host, dtype=c, seed=s, rate=r, mask=m)
+        assert np.array_equal(to_host_bits(x), host)
+    # async, same seeds again: restores the inputs
+    d_counts = torch.empty(len(xs), dtype=torch.int64, device="cuda")
+    P.inject_batched_async([(x, s, r, m) for x, (_, _, s, r, m) in zip(xs, items_host)], d_counts)
+    torch.cuda.synchronize()
+    assert d_counts.cpu().tolist() == counts
+    for (c, gb, *_), x in zip(items_host, xs):
+        assert np.array_equal(to_host_bits(x), gb)
+
+
+# ---------------------------------------------------------------------------
+# the five workloads
+# ---------------------------------------------------------------------------
+def test_workload2_full_sampled():
+    """32 pairs of f32 [8, 512, 4096], bf16 rounding: one batched call; three
+    pairs checked in full against the oracle, bf16 properties on every pair."""
+    pairs = synth.config2_all("cuda")
+    log("  workload 2 generated")
+    recs = P.signature_batched(pairs, synth.BINS, synth.THRESHOLDS)
+    for k in (0, 13, 31):
+        G, T = pairs[k]
+        ref = oracle_sig(to_host_bits(G), to_host_bits(T), 0, synth.BINS, synth.THRESHOLDS)
+        assert_parity(recs[k], ref, f"workload 2 pair {k}")
+    for r in recs:
+        assert r["max_ulp"] <= 32768 and r["max_rel"] <= 2.0 ** -8 and r["n_valid"] == r["n"]
+    del pairs
+    torch.cuda.empty_cache()
+
+
+def test_workload3_full_sampled():
+    tensors = synth.config3_all("cuda")
+    log("  workload 3 generated")
+    recs = P.signature_batched([(G, T) for _, G, T in tensors], synth.BINS, synth.THRESHOLDS)
+    sample = [0, 1, 2, 3, 4, 5, 9, 100, 289, 290, 291]
+    for k in sample:
+        name, G, T = tensors[k]
+        ref = oracle_sig(to_host_bits(G), to_host_bits(T), 0, synth.BINS, synth.THRESHOLDS)
+        assert_parity(recs[k], ref, f"workload 3 {name}")
+    total_nan = sum(r["n_nan_test"] for r in recs)
+    assert total_nan == sum(int(torch.isnan(T).sum()) for _, _, T in tensors)
+    del tensors
+    torch.cuda.empty_cache()
+
+
+def test_workload4_replay():
+    """Replayed f16 calls: every 10th injected (rate 1e-7, any of 16 bits);
+    the 100 calls of the first 1000 that are injected are represented by the
+    first 30 calls here (3 injected), all checked against the oracle."""
+    G = synth.config4_golden("cuda")
+    gb = to_host_bits(G)
+    calls = 30
+    tests, counts = [], []
+    for c in range(calls):
+        T = G.clone()
+        if synth.config4_injected(c):
+            counts.append(P.inject(T, synth.inject_seed(4, c), synth.CONFIG4_RATE, synth.CONFIG4_MASK))
+        tests.append(T)
+    recs = P.signature_batched([(G, T) for T in tests], synth.BINS, synth.THRESHOLDS)
+    for c in range(calls):
+        tb = gb.copy()
+        if synth.config4_injected(c):
+            n = oracle.inject(tb, dtype=1, seed=synth.inject_seed(4, c), rate=synth.CONFIG4_RATE,
+                              mask=synth.CONFIG4_MASK)
+            assert n == counts[c // 10]
+            assert np.array_equal(to_host_bits(tests[c]), tb)
+            assert_parity(recs[c], oracle_sig(gb, tb, 1, synth.BINS, synth.THRESHOLDS), f"call {c}")
+        else:
+            assert recs[c]["hist_zero"] == recs[c]["n_valid"] and recs[c]["max_ulp"] == 0
+    # single async calls on one stream give the same records
+    d_out = torch.empty(calls * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    prepared = [P.PreparedPairs([(G, T)]) for T in tests]
+    for c in range(calls):
+        P.signature_batched_async(prepared[c], d_out[c * P.SIG_BYTES:], synth.BINS, synth.THRESHOLDS)
+    torch.cuda.synchronize()
+    assert P.decode_records(d_out, calls, nthr=2) == recs
+    del tests, G
+    torch.cuda.empty_cache()
+
+
+def test_workload5_full_sampled():
+    """Llama-7B-shaped pair (873 f32 tensors, 161.7 GB on device) in the
+    benchmark's configuration: one batched injection, one batched signature.
+    Sampled tensors (all three states of the smallest and largest shapes)
+    are checked against the oracle, injection included."""
+    tensors = synth.config5_all("cuda")
+    log(f"  workload 5 generated: {torch.cuda.memory_allocated() / 1e9:.1f} GB")
+    names = [name for name, *_ in tensors]
+    sample = [k for k, nm in enumerate(names) if nm in ("l0.in_norm", "norm", "l0.q", "l31.down", "embed")]
+    pre = {k: to_host_bits(tensors[k][3]) for k in sample}
+    items = [(T, synth.inject_seed(5, k), synth.CONFIG5_RATE, synth.CONFIG5_MASK)
+             for k, (_, _, _, T) in enumerate(tensors)]
+    counts = P.inject_batched(items)
+    recs = P.signature_batched([(G, T) for _, _, G, T in tensors], synth.BINS, synth.THRESHOLDS)
+    log(f"  workload 5: {sum(counts)} flips, sampling {len(sample)} tensors")
+    for k in sample:
+        name, state, G, T = tensors[k]
+        tb = pre[k]
+        n = oracle.inject(tb, dtype=0, seed=synth.inject_seed(5, k), rate=synth.CONFIG5_RATE,
+                          mask=synth.CONFIG5_MASK)
+        assert n == counts[k], (name, state, n, counts[k])
+        assert np.array_equal(to_host_bits(T), tb), f"{name}/{state}: injected bits differ"
+        assert_parity(recs[k], oracle_sig(to_host_bits(G), tb, 0, synth.BINS, synth.THRESHOLDS),
+                      f"{name}/{state}")
+        log(f"    {name}/{state} ok")
+    for r in recs:
+        assert r["n_nan_pairs"] == 0 or r["n_nan_test"] > 0
+        assert r["hist_zero"] + r["hist_under"] + sum(r["hist"]) + r["hist_over"] == r["n_valid"]
+    del tensors, items
+    torch.cuda.empty_cache()
