@@ -245,6 +245,7 @@ __device__ __forceinline__ void vec_step(Lane &L, Uni &U, Shared &sh, const SigP
             if (R[j] > L.rthr) rel_candidate(L, a, G[j], li);
         }
         U.common += VEC;
+        L.first_valid = min(L.first_valid, li0);
     } else {
 #pragma unroll
         for (int j = 0; j < VEC; ++j)
