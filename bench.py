@@ -1,0 +1,326 @@
+#!/usr/bin/env python3
+"""Throughput of the error-signature hot path on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic input
+resident in HBM: the batched bit-flip injection into every test tensor (fresh
+seeds each step), then the batched error signature of every (golden, test)
+pair.  The default workload is the Llama-7B-shaped checkpoint pair (weights
+plus both Adam moments: 873 f32 tensors, 20,215,246,848 elements per side,
+161.72 GB signed per step).
+
+Prints ONE JSON line on stdout (everything else goes to stderr):
+  value     golden+test bytes signed per second over the timed steps (GB/s)
+  roofline  the dominant kernel (signature chunk pass): algorithmic bytes per
+            launch / its average launch duration from HIP events on its stream,
+            against the 8 TB/s HBM peak; traffic from the committed rocprofv3
+            counter summary when it was taken on the current kernel source
+  cpu_baseline  the CPU oracle on a bounded sample of the same workload
+
+Modes used to produce the committed profiles: --copy-calibration (a plain
+device copy of known size, for scaling the HBM byte counters).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import threading
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "GB/s of golden+test tensor bytes signed (fraction of HBM peak), 1 MI355X"
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_13544_amd", "csrc", f)
+                  for f in ("signature.hip", "peat_internal.h")]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload: str):
+    """HBM bytes per sig_chunk launch from profiles/, or None when the counters
+    were taken on a different kernel source."""
+    path = os.path.join(PROFILES, f"sig_chunk_{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel_source_sha256_16:\s*`?([0-9a-f]{16})", text)
+    m_val = re.search(r"traffic_bytes_per_launch:\s*`?([0-9.eE+]+)", text)
+    if not m_hash or not m_val or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_val.group(1))
+
+
+# ---------------------------------------------------------------------------
+# workloads
+# ---------------------------------------------------------------------------
+class Workload:
+    name = ""
+    description = ""
+
+    def __init__(self, torch, P, synth):
+        self.torch, self.P, self.synth = torch, P, synth
+        self.pairs = []          # (G, T) device tensors
+        self.items = []          # (T, base_seed, rate, mask) injected each step
+        self.sample = []         # indices of pairs for the CPU baseline
+
+    def inject_items(self, step: int):
+        return [(T, (seed + (step << 40)) & (2 ** 64 - 1), rate, mask) for T, seed, rate, mask in self.items]
+
+    def bytes_signed(self) -> int:
+        return sum(G.numel() * G.element_size() * 2 for G, _ in self.pairs)
+
+    def elements(self) -> int:
+        return sum(G.numel() for G, _ in self.pairs)
+
+
+class Llama7B(Workload):
+    name = "llama7b_ckpt_adam"
+    description = ("Llama-7B-shaped checkpoint pair: weights + Adam m + Adam v, 873 f32 tensors, "
+                   "T = G*(1+1e-7 z) with 1e-8-rate exponent-bit flips")
+
+    def __init__(self, torch, P, synth):
+        super().__init__(torch, P, synth)
+        names = []
+        for k, (name, state, G, T) in enumerate(synth.config5_all("cuda")):
+            self.pairs.append((G, T))
+            self.items.append((T, synth.inject_seed(5, k), synth.CONFIG5_RATE, synth.CONFIG5_MASK))
+            names.append((name, state))
+            if k % 100 == 0:
+                log(f"  generated {k}/873")
+        self.sample = [k for k, (nm, st) in enumerate(names)
+                       if nm in ("embed", "lm_head", "l0.gate", "l0.up", "l0.down")]
+
+
+class GPT13B(Workload):
+    name = "gpt13b_ckpt"
+    description = "GPT-style 1.3B checkpoint pair: 292 f32 tensors, T = G*(1+1e-6 z), NaN at rate 1e-9"
+
+    def __init__(self, torch, P, synth):
+        super().__init__(torch, P, synth)
+        for name, G, T in synth.config3_all("cuda"):
+            self.pairs.append((G, T))
+        self.sample = [0, 1, 4, 8, 10]
+
+
+class Activations(Workload):
+    name = "activations_bf16_rounding"
+    description = "32 f32 [8,512,4096] activation pairs, T = bf16-rounded G"
+
+    def __init__(self, torch, P, synth):
+        super().__init__(torch, P, synth)
+        self.pairs = synth.config2_all("cuda")
+        self.sample = [0, 1, 2, 3]
+
+
+class Replay(Workload):
+    name = "rfi_replay_f16"
+    description = "1000 replayed f16 [4096,4096] calls, every 10th injected at rate 1e-7"
+
+    def __init__(self, torch, P, synth):
+        super().__init__(torch, P, synth)
+        G = synth.config4_golden("cuda")
+        for c in range(synth.CONFIG4_CALLS):
+            T = G.clone()
+            self.pairs.append((G, T))
+            if synth.config4_injected(c):
+                self.items.append((T, synth.inject_seed(4, c), synth.CONFIG4_RATE, synth.CONFIG4_MASK))
+        self.sample = [9, 19, 29]
+
+
+class Single(Workload):
+    name = "single_f32_1024x1024"
+    description = "one f32 [1024,1024] pair with 16 planted bit flips"
+
+    def __init__(self, torch, P, synth):
+        super().__init__(torch, P, synth)
+        import numpy as np
+        G, T = synth.config1()
+        self.pairs = [(torch.from_numpy(G).cuda(), torch.from_numpy(T).cuda())]
+        self.sample = [0]
+        del np
+
+
+WORKLOADS = {"5": Llama7B, "3": GPT13B, "2": Activations, "4": Replay, "1": Single}
+
+
+# ---------------------------------------------------------------------------
+def cpu_baseline(wl: Workload, max_threads: int):
+    """The oracle, as it stands, on the workload's sampled pairs: host copies
+    of the device bytes, one oracle call per pair on a thread pool (ctypes
+    releases the GIL).  Returns GB/s of golden+test bytes signed."""
+    import numpy as np
+    import oracle
+    from tests.parity import to_host_bits
+
+    host = []
+    t0 = time.time()
+    for k in wl.sample:
+        G, T = wl.pairs[k]
+        code = {wl.torch.float32: 0, wl.torch.float16: 1, wl.torch.bfloat16: 2}[G.dtype]
+        host.append((to_host_bits(G), to_host_bits(T), code))
+    copy_s = time.time() - t0
+    nbytes = sum(g.nbytes + t.nbytes for g, t, _ in host)
+    threads = max(1, min(max_threads, len(host), os.cpu_count() or 1))
+    work = list(range(len(host)))
+    lock = threading.Lock()
+
+    def worker():
+        while True:
+            with lock:
+                if not work:
+                    return
+                k = work.pop(0)
+            g, t, code = host[k]
+            oracle.signature(g, t, dtype=code)
+
+    t0 = time.time()
+    ths = [threading.Thread(target=worker) for _ in range(threads)]
+    for th in ths:
+        th.start()
+    for th in ths:
+        th.join()
+    dt = time.time() - t0
+    del np
+    return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(host)} of {len(wl.pairs)} pairs ({nbytes / 1e9:.2f} GB: "
+                      f"{', '.join(str(k) for k in wl.sample)}), oracle {dt:.1f} s wall on {threads} threads, "
+                      f"D2H copy {copy_s:.1f} s not counted"}
+
+
+def copy_calibration(torch, gib: int, reps: int):
+    """A plain device copy of known size, for scaling FETCH_SIZE/WRITE_SIZE."""
+    n = gib * (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 4, "bytes_written": n * 4, "reps": reps}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="5", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=16)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="GIB")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the signature of N GPUs is "
+              f"N independent shards of the pair list with no exchange on the hot path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_13544_amd as P
+    import synth
+
+    if args.copy_calibration:
+        copy_calibration(torch, args.copy_calibration, 5)
+        return
+
+    torch.cuda.set_device(0)
+    log(f"generating workload {args.workload} ...")
+    t0 = time.time()
+    wl = WORKLOADS[args.workload](torch, P, synth)
+    torch.cuda.synchronize()
+    log(f"generated in {time.time() - t0:.1f} s: {len(wl.pairs)} pairs, {wl.bytes_signed() / 1e9:.2f} GB")
+
+    stream = torch.cuda.current_stream()
+    prep_pairs = P.PreparedPairs(wl.pairs)
+    d_out = torch.empty(len(wl.pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    d_counts = torch.empty(max(1, len(wl.items)), dtype=torch.int64, device="cuda")
+    prepared_items = [P.PreparedItems(wl.inject_items(s)) for s in range(args.warmup + args.steps)]
+
+    def step(s):
+        if wl.items:
+            P.inject_batched_async(prepared_items[s], d_counts, stream=stream)
+        P.signature_batched_async(prep_pairs, d_out, synth.BINS, synth.THRESHOLDS, stream=stream)
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    P.profile_enable(True)
+    for k in (P.K_SIG_CHUNK, P.K_SIG_FINALIZE, P.K_INJECT, P.K_INJECT_SUM):
+        P.profile_read(k)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for s in range(args.warmup, args.warmup + args.steps):
+        step(s)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    P.profile_enable(False)
+    chunk_ms, chunk_n = P.profile_read(P.K_SIG_CHUNK)
+    fin_ms, fin_n = P.profile_read(P.K_SIG_FINALIZE)
+    inj_ms, inj_n = P.profile_read(P.K_INJECT)
+    isum_ms, isum_n = P.profile_read(P.K_INJECT_SUM)
+
+    ms_step = ms_total / args.steps
+    nbytes = wl.bytes_signed()
+    value = nbytes / (ms_step / 1e3) / 1e9
+    chunk_avg = chunk_ms / max(1, chunk_n)
+    achieved = nbytes / (chunk_avg / 1e3) / 1e9
+    recs = P.decode_records(d_out, len(wl.pairs), nthr=len(synth.THRESHOLDS))
+    flips = int(d_counts.sum().item()) if wl.items else 0
+    log(f"step {ms_step:.3f} ms: chunk {chunk_avg:.3f} ms, finalize {fin_ms / max(1, fin_n):.3f} ms, "
+        f"inject {inj_ms / max(1, inj_n):.3f} ms + {isum_ms / max(1, isum_n):.3f} ms; "
+        f"last step {flips} flips, {sum(r['n_nan_pairs'] for r in recs)} NaN pairs")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "pairs": len(wl.pairs),
+                   "elements_per_side": wl.elements(), "bytes_signed_per_step": nbytes,
+                   "bins": list(synth.BINS), "thresholds": list(synth.THRESHOLDS),
+                   "step": "batched injection + batched signature" if wl.items else "batched signature"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": committed_traffic(wl.name)},
+        "kernels_ms_per_step": {"sig_chunk": round(chunk_avg, 4),
+                                "sig_finalize": round(fin_ms / max(1, fin_n), 4),
+                                "inject": round(inj_ms / max(1, inj_n), 4) if inj_n else 0.0,
+                                "inject_sum": round(isum_ms / max(1, isum_n), 4) if isum_n else 0.0},
+        "signature_only_GBps": round(nbytes / ((chunk_avg + fin_ms / max(1, fin_n)) / 1e3) / 1e9, 1),
+        "inject_Gelem_per_s": round(sum(T.numel() for T, *_ in wl.items) / (inj_ms / max(1, inj_n) / 1e3) / 1e9, 1)
+        if inj_n else None,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline ...")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
