@@ -12,7 +12,7 @@ namespace peat {
 
 constexpr int kBlock = 256;                        // threads per block (4 wave64)
 constexpr int kWaves = kBlock / 64;
-constexpr int kHistSlots = PEAT_MAX_BINS + 2;      // under (zeros included) | bins | over
+constexpr int kHistSlots = PEAT_MAX_BINS + 3;      // zero | under | bins | over
 constexpr uint32_t kNone = 0xFFFFFFFFu;            // "no element" local index
 constexpr int kMinChunkLog2 = 12;                  // 4096 elements: 16 per thread
 constexpr int kMaxChunkLog2 = 18;                  // 262144 elements: 1024 per thread
@@ -42,7 +42,7 @@ struct SigDesc {                 // one per pair (48 bytes)
 };
 static_assert(sizeof(SigDesc) == 48, "SigDesc layout");
 
-enum { C_VALID, C_FINITE, C_REL, C_NAN_G, C_NAN_T, C_INF_G, C_INF_T, C_NANPAIR, C_ZERO, kCnt };
+enum { C_VALID, C_FINITE, C_REL, C_NAN_G, C_NAN_T, C_INF_G, C_INF_T, C_NANPAIR, kCnt };
 
 struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
     double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;

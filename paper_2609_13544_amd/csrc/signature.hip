@@ -2,9 +2,10 @@
 //
 // Pass 1 (sig_chunk): one 256-thread block per fixed-size chunk of one pair.
 // Each thread streams 16-byte vectors of golden and test (4 f32 or 8 f16/bf16
-// elements), widens them exactly to binary64 and accumulates the signature of
-// its elements; the chunk's record (binary64 partial sums, maxima with their
-// lowest index, integer counts, histogram) goes to one ChunkPartial.
+// elements) from the global address space, widens them exactly to binary64
+// and accumulates the signature of its elements; the chunk's record (binary64
+// partial sums, maxima with their lowest index, integer counts, histogram)
+// goes to one ChunkPartial.
 //
 // Pass 2 (sig_finalize): one block per pair combines its chunk records in a
 // fixed order and writes the peat_signature_t.
@@ -14,22 +15,36 @@
 // variance), the closeness test of Section III-A (torch.isclose, rtol = 0)
 // and the error histograms of Section V-D.
 //
-// Fast path: a wave whose current vectors hold only "ordinary" pairs (both
-// finite, no NaN, golden nonzero, same sign) skips all classification: the
-// relative error uses a Newton-refined reciprocal for the sum and an exact
-// IEEE division only when an element may raise the lane's maximum; counts
-// use wave ballots.  Any other wave (or a ragged tail / unaligned pair)
-// takes the generic per-element path, which evaluates every case.
+// Fast path.  A wave whose current vectors hold only "ordinary" pairs (both
+// finite, no NaN, golden nonzero, same sign) needs no classification:
+//   - the relative error of the sum uses a Newton-refined reciprocal; the
+//     exact IEEE quotient is formed only when a vector may raise the lane's
+//     maximum;
+//   - absolute-error and ULP maxima are tracked per vector (value + vector
+//     number); the element is resolved once per lane at the end of the chunk
+//     by reloading that one vector;
+//   - counts use wave ballots; the histogram uses lane-private LDS counters
+//     addressed through a binary64-exponent -> slot table.
+// Any other vector is deferred: its wave-uniform vector number goes to a
+// per-wave LDS list and the generic per-element path (every IEEE case)
+// processes the list out of the hot loop.  Ragged tails and unaligned pairs
+// use the generic path directly.
 //
-// Determinism: the element -> lane mapping, the per-lane order and the
-// reduction trees depend only on the chunk size, which depends only on n, so
-// single, batched and any-grid-size launches give bit-identical records.
+// Determinism: the element -> lane mapping, per-lane order and reduction
+// trees depend only on the chunk size, which depends only on n, so single,
+// batched and any-grid-size launches give bit-identical records.
 #include "peat_internal.h"
 
 namespace peat {
 namespace {
 
 constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
+constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte vector
+typedef __attribute__((address_space(1))) const u32x4 gvec_t;
+typedef __attribute__((address_space(1))) const uint32_t gu32_t;
+typedef __attribute__((address_space(1))) const uint16_t gu16_t;
 
 template <int DT> struct Tr;
 template <> struct Tr<PEAT_F32>  { static constexpr int VEC = 4, W = 32, U = 4; };
@@ -48,7 +63,7 @@ __device__ __forceinline__ double widen(uint32_t b) {
 }
 
 template <int DT>
-__device__ __forceinline__ uint32_t lane_elem(const uint4 &v, int j) {
+__device__ __forceinline__ uint32_t lane_elem(const u32x4 &v, int j) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
     if constexpr (Tr<DT>::W == 32) {
         return w[j];
@@ -58,11 +73,11 @@ __device__ __forceinline__ uint32_t lane_elem(const uint4 &v, int j) {
 }
 
 template <int DT>
-__device__ __forceinline__ uint32_t load_elem(const void *base, int64_t i) {
+__device__ __forceinline__ uint32_t load_elem(const char *base, int64_t i) {
     if constexpr (Tr<DT>::W == 32) {
-        return static_cast<const uint32_t *>(base)[i];
+        return ((gu32_t *)base)[i];
     } else {
-        return static_cast<const uint16_t *>(base)[i];
+        return ((gu16_t *)base)[i];
     }
 }
 
@@ -80,76 +95,84 @@ __device__ __forceinline__ uint32_t wave_count(bool p) {
     return (uint32_t)__popcll(__ballot(p));
 }
 
-// Binary64 reciprocal: hardware estimate refined by two Newton steps.
+// Binary64 reciprocal for the relative-error sum: the hardware estimate
+// (relative error below 2^-24) refined by one Newton step (below 2^-48).
 __device__ __forceinline__ double recip(double b) {
-    double y = __builtin_amdgcn_rcp(b);
-    double e = __builtin_fma(-b, y, 1.0);
-    y = __builtin_fma(y, e, y);
-    e = __builtin_fma(-b, y, 1.0);
-    return __builtin_fma(y, e, y);
+    const double y = __builtin_amdgcn_rcp(b);
+    return __builtin_fma(y, __builtin_fma(-b, y, 1.0), y);
 }
 
 struct Lane {
     double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;
-    double mx_abs, mx_rel, rthr;
+    double vx_abs;                 // fast path: max |err| per lane ...
+    uint32_t vv_abs;               // ... and the vector number reaching it first
+    uint32_t vu, vv_ulp;           // fast path: max ULP and its vector number
+    double gx_abs;                 // generic path: max |err| and element index
+    uint32_t gi_abs;
+    uint32_t gu, gi_ulp;           // generic path: max ULP and element index
+    double mx_rel, rthr;           // both paths: max rel err, its index, filter
+    uint32_t ix_rel;
     uint64_t s_ulp;
-    uint32_t ix_abs, ix_rel, ix_ulp, mu;
     uint32_t first_nan, first_valid;
     uint32_t cnt[kCnt];                    // generic-path counts (per lane)
     uint32_t mism[PEAT_MAX_THRESHOLDS];    // generic-path mismatches (per lane)
 };
 
 struct Uni {                               // fast-path counts (wave-uniform)
-    uint32_t common;                       // ordinary elements per lane
-    uint32_t zero;
+    uint32_t common;                       // ordinary vectors per lane
     uint32_t mism[PEAT_MAX_THRESHOLDS];
 };
 
 struct Shared {
+    uint8_t slot_of_exp[2048];             // binary64 exponent field -> slot (LDS offset 0)
     uint32_t hist[kHistSlots * kBlock];    // lane-private counters, [slot][lane]
-    uint8_t slot_of_exp[2048];             // binary64 exponent field -> slot
+    uint32_t defer[kWaves][kDeferCap];     // deferred vector numbers per wave
     double rd[kWaves][6];
     double rmax[kWaves][2];
     uint32_t rix[kWaves][5];               // abs, rel, ulp, first_nan, first_valid
     uint32_t rmu[kWaves];
+    uint64_t rulp[kWaves];
     uint32_t rcnt[kWaves][kCnt + PEAT_MAX_THRESHOLDS];
 };
 
 __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
     L.s_abs = L.s_sq = L.s_rel = L.s_g2 = L.s_t2 = L.s_gt = 0.0;
-    L.mx_abs = -1.0;
+    L.vx_abs = -1.0;
+    L.vv_abs = kNone;
+    L.vu = 0;
+    L.vv_ulp = kNone;
+    L.gx_abs = -1.0;
+    L.gi_abs = kNone;
+    L.gu = 0;
+    L.gi_ulp = kNone;
     L.mx_rel = -1.0;
     L.rthr = -1.0;
+    L.ix_rel = kNone;
     L.s_ulp = 0;
-    L.ix_abs = L.ix_rel = L.ix_ulp = kNone;
-    L.mu = 0;
     L.first_nan = L.first_valid = kNone;
 #pragma unroll
     for (int c = 0; c < kCnt; ++c) L.cnt[c] = 0;
 #pragma unroll
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) L.mism[j] = 0;
     U.common = 0;
-    U.zero = 0;
 #pragma unroll
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) U.mism[j] = 0;
 }
 
-__device__ __forceinline__ void rel_candidate(Lane &L, double a, double G, uint32_t li) {
-    double r = a / __builtin_fabs(G);           // IEEE division, correctly rounded
-    if (r > L.mx_rel) {
-        L.mx_rel = r;
-        L.ix_rel = li;
-        L.rthr = r - r * kRelMargin;
-    }
+__device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
+    const uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: sign bit clear
+    atomicAdd(&sh.hist[(uint32_t)sh.slot_of_exp[E] * kBlock + tid], 1u);
 }
 
 // Every case of one pair (NaN, Inf, zero golden, sign change, subnormals).
+// Elements may arrive out of index order (deferred vectors), so the maxima
+// use (value, lowest index) comparisons.
 template <int DT, int NT>
 __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParams &P,
                                              uint32_t gb, uint32_t tb, uint32_t li, int tid) {
-    double G = widen<DT>(gb), T = widen<DT>(tb);
-    bool nan_g = G != G, nan_t = T != T;
-    bool inf_g = __builtin_isinf(G), inf_t = __builtin_isinf(T);
+    const double G = widen<DT>(gb), T = widen<DT>(tb);
+    const bool nan_g = G != G, nan_t = T != T;
+    const bool inf_g = __builtin_isinf(G), inf_t = __builtin_isinf(T);
     L.cnt[C_NAN_G] += nan_g;
     L.cnt[C_NAN_T] += nan_t;
     L.cnt[C_INF_G] += inf_g;
@@ -161,22 +184,20 @@ __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParam
     }
     L.cnt[C_VALID] += 1;
     L.first_valid = min(L.first_valid, li);
-    double a = (G == T) ? 0.0 : __builtin_fabs(T - G);
-    uint32_t ulp = ulp_dist<Tr<DT>::W>(gb, tb);
+    const double a = (G == T) ? 0.0 : __builtin_fabs(T - G);
+    const uint32_t ulp = ulp_dist<Tr<DT>::W>(gb, tb);
     L.s_ulp += ulp;
-    if (ulp > L.mu) {
-        L.mu = ulp;
-        L.ix_ulp = li;
+    if (ulp > L.gu || (ulp == L.gu && li < L.gi_ulp)) {
+        L.gu = ulp;
+        L.gi_ulp = li;
     }
-    uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: no sign bit
-    atomicAdd(&sh.hist[(uint32_t)sh.slot_of_exp[E] * kBlock + tid], 1u);
-    L.cnt[C_ZERO] += (a == 0.0);
-    bool ainf = __builtin_isinf(a);
+    hist_add(sh, a, tid);
+    const bool ainf = __builtin_isinf(a);
 #pragma unroll
     for (int j = 0; j < NT; ++j) L.mism[j] += (a > P.thr[j]) || ainf;
-    if (a > L.mx_abs) {
-        L.mx_abs = a;
-        L.ix_abs = li;
+    if (a > L.gx_abs || (a == L.gx_abs && li < L.gi_abs)) {
+        L.gx_abs = a;
+        L.gi_abs = li;
     }
     if (inf_g || inf_t) return;
     L.cnt[C_FINITE] += 1;
@@ -187,9 +208,9 @@ __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParam
     L.s_gt = __builtin_fma(G, T, L.s_gt);
     if (G != 0.0) {
         L.cnt[C_REL] += 1;
-        double r = a / __builtin_fabs(G);
+        const double r = a / __builtin_fabs(G);
         L.s_rel += r;
-        if (r > L.mx_rel) {
+        if (r > L.mx_rel || (r == L.mx_rel && li < L.ix_rel)) {
             L.mx_rel = r;
             L.ix_rel = li;
             L.rthr = r - r * kRelMargin;
@@ -197,63 +218,115 @@ __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParam
     }
 }
 
-// One 16-byte vector of golden and one of test; li0 = local index of its
-// first element.  Called in wave-uniform control flow with every lane active.
-template <int DT, int NT>
-__device__ __forceinline__ void vec_step(Lane &L, Uni &U, Shared &sh, const SigParams &P,
-                                         const uint4 &gv, const uint4 &tv, uint32_t li0, int tid) {
-    constexpr int VEC = Tr<DT>::VEC;
-    double G[VEC], T[VEC], A[VEC], R[VEC];
-    bool rare = false;
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) {
-        G[j] = widen<DT>(lane_elem<DT>(gv, j));
-        T[j] = widen<DT>(lane_elem<DT>(tv, j));
-        A[j] = __builtin_fabs(T[j] - G[j]);
-        R[j] = A[j] * recip(__builtin_fabs(G[j]));
-        rare |= !__builtin_isfinite(R[j]);      // NaN/Inf on either side, or G == 0
-    }
-    uint32_t sx = (gv.x ^ tv.x) | (gv.y ^ tv.y) | (gv.z ^ tv.z) | (gv.w ^ tv.w);
-    if constexpr (Tr<DT>::W == 32) {
-        rare |= (sx & 0x80000000u) != 0;        // a sign change
-    } else {
-        rare |= (sx & 0x80008000u) != 0;
-    }
-    if (__ballot(rare) == 0) {
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-            const double a = A[j];
-            const uint32_t li = li0 + j;
-            L.s_abs += a;
-            L.s_sq = __builtin_fma(a, a, L.s_sq);
-            L.s_g2 = __builtin_fma(G[j], G[j], L.s_g2);
-            L.s_t2 = __builtin_fma(T[j], T[j], L.s_t2);
-            L.s_gt = __builtin_fma(G[j], T[j], L.s_gt);
-            if (a > L.mx_abs) L.ix_abs = li;
-            L.mx_abs = __builtin_fmax(L.mx_abs, a);
-            uint32_t gb = lane_elem<DT>(gv, j), tb = lane_elem<DT>(tv, j);
-            uint32_t ulp = __sad(tb, gb, 0u);     // same sign: |t - g| of the patterns
-            L.s_ulp += ulp;
-            if (ulp > L.mu) L.ix_ulp = li;
-            L.mu = max(L.mu, ulp);
-            uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);
-            atomicAdd(&sh.hist[(uint32_t)sh.slot_of_exp[E] * kBlock + tid], 1u);
-            U.zero += wave_count(a == 0.0);
-#pragma unroll
-            for (int k = 0; k < NT; ++k) U.mism[k] += wave_count(a > P.thr[k]);
-            L.s_rel += R[j];
-            if (R[j] > L.rthr) rel_candidate(L, a, G[j], li);
-        }
-        U.common += VEC;
-        L.first_valid = min(L.first_valid, li0);
-    } else {
-#pragma unroll
-        for (int j = 0; j < VEC; ++j)
-            generic_elem<DT, NT>(L, sh, P, lane_elem<DT>(gv, j), lane_elem<DT>(tv, j), li0 + j, tid);
-    }
+// |a - b| of two unsigned 32-bit values (v_sad_u32 with a zero addend).
+__device__ __forceinline__ uint32_t absdiff_u32(uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_sad_u32 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
+    return r;
 }
 
-// ---- wave / block reductions (fixed butterfly order) ----------------------
+// max(|a|, |b|) of two binary64 values as one v_max_f64 with absolute-value
+// source modifiers (the operands are never NaN here, so no quieting is needed).
+__device__ __forceinline__ double absmax_f64(double a, double b) {
+    double r;
+    asm("v_max_f64 %0, |%1|, |%2|" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// One 16-byte vector of golden and of test (vector number v of the lane's
+// sequence).  Called in wave-uniform control flow with every lane active.
+// Returns true (wave-uniform) when the vector must go to the generic path.
+//
+// Everything the decision needs -- and every per-vector reduction (maxima,
+// ULP distances, histogram slots) -- is computed before the branch as wave
+// masks and plain values, so the hot block only accumulates; the histogram's
+// table reads are all issued before its atomic adds, so they share one LDS
+// round trip.
+template <int DT, int NT>
+__device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
+                                         const u32x4 &gv, const u32x4 &tv, uint32_t v, int tid) {
+    constexpr int VEC = Tr<DT>::VEC;
+    double G[VEC], T[VEC], E[VEC], R[VEC];
+    uint32_t slot[VEC], u[VEC];
+    uint64_t mrare = 0, mcand = 0;
+    double va = 0.0;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        const uint32_t gb = lane_elem<DT>(gv, j), tb = lane_elem<DT>(tv, j);
+        G[j] = widen<DT>(gb);
+        T[j] = widen<DT>(tb);
+        E[j] = T[j] - G[j];                                   // signed error
+        const double a = __builtin_fabs(E[j]);
+        R[j] = a * recip(__builtin_fabs(G[j]));
+        mrare |= __ballot(!__builtin_isfinite(R[j]));     // NaN/Inf on either side, or G == 0
+        mcand |= __ballot(R[j] > L.rthr);                 // may raise the lane's max rel error
+        va = j ? absmax_f64(va, E[j]) : a;
+        // same sign: the ULP distance is |t - g| of the bit patterns
+        if constexpr (Tr<DT>::W == 32) {
+            u[j] = absdiff_u32(gb, tb);
+        } else {
+            u[j] = __builtin_amdgcn_sad_u16(gb, tb, 0u);
+        }
+        slot[j] = sh.slot_of_exp[(uint32_t)(__double_as_longlong(E[j]) >> 52) & 0x7FFu];
+    }
+    const uint32_t sx = (gv.x ^ tv.x) | (gv.y ^ tv.y) | (gv.z ^ tv.z) | (gv.w ^ tv.w);
+    mrare |= __ballot((sx & (Tr<DT>::W == 32 ? 0x80000000u : 0x80008000u)) != 0);   // a sign change
+    if (mrare != 0) return true;
+
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[slot[j] * kBlock + tid], 1u);
+    uint32_t vu = u[0];
+#pragma unroll
+    for (int j = 1; j < VEC; ++j) vu = max(vu, u[j]);
+    if constexpr (Tr<DT>::W == 32) {
+        // two f32 distances (< 2^31 each) per 32-bit partial sum
+#pragma unroll
+        for (int q = 0; q < VEC / 2; ++q) L.s_ulp += (uint64_t)(u[2 * q] + u[2 * q + 1]);
+    } else {
+        uint32_t us = 0;                       // eight f16/bf16 distances (< 2^16 each)
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) us += u[j];
+        L.s_ulp += us;
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        L.s_abs += __builtin_fabs(E[j]);
+        L.s_sq = __builtin_fma(E[j], E[j], L.s_sq);
+        L.s_g2 = __builtin_fma(G[j], G[j], L.s_g2);
+        L.s_t2 = __builtin_fma(T[j], T[j], L.s_t2);
+        L.s_gt = __builtin_fma(G[j], T[j], L.s_gt);
+        L.s_rel += R[j];
+#pragma unroll
+        for (int k = 0; k < NT; ++k) U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
+    }
+    if (va > L.vx_abs) {
+        L.vx_abs = va;
+        L.vv_abs = v;
+    }
+    if (vu > L.vu) {
+        L.vu = vu;
+        L.vv_ulp = v;
+    }
+    if (mcand != 0) {
+        const uint32_t li0 = (v * kBlock + tid) * VEC;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            if (R[j] > L.rthr) {
+                const double r = __builtin_fabs(E[j]) / __builtin_fabs(G[j]);   // IEEE quotient
+                if (r > L.mx_rel) {
+                    L.mx_rel = r;
+                    L.ix_rel = li0 + j;
+                    L.rthr = r - r * kRelMargin;
+                }
+            }
+        }
+    }
+    U.common += 1;
+    L.first_valid = min(L.first_valid, (v * kBlock + tid) * VEC);
+    return false;
+}
+
+// ---- wave reductions (fixed butterfly order) -------------------------------
 __device__ __forceinline__ double wsum(double v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
@@ -275,24 +348,22 @@ __device__ __forceinline__ uint32_t wmin_u(uint32_t v) {
     return v;
 }
 // (value desc, index asc) over entries with index != kNone
-__device__ __forceinline__ void wmax_d(double &v, uint32_t &ix) {
+template <typename V>
+__device__ __forceinline__ void wmax(V &v, uint32_t &ix) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
-        double ov = __shfl_xor(v, o);
-        uint32_t oi = __shfl_xor(ix, o);
-        bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
+        const V ov = __shfl_xor(v, o);
+        const uint32_t oi = __shfl_xor(ix, o);
+        const bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
         v = take ? ov : v;
         ix = take ? oi : ix;
     }
 }
-__device__ __forceinline__ void wmax_u(uint32_t &v, uint32_t &ix) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        uint32_t ov = __shfl_xor(v, o);
-        uint32_t oi = __shfl_xor(ix, o);
-        bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
-        v = take ? ov : v;
-        ix = take ? oi : ix;
+template <typename V>
+__device__ __forceinline__ void lex_merge(V &v, uint32_t &ix, V ov, uint32_t oi) {
+    if (oi != kNone && (ix == kNone || ov > v || (ov == v && oi < ix))) {
+        v = ov;
+        ix = oi;
     }
 }
 
@@ -301,82 +372,120 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     constexpr int VEC = Tr<DT>::VEC;
     constexpr int U = Tr<DT>::U;
     constexpr int SUPER = kBlock * VEC * U;     // elements per block super-step (4096)
+    constexpr int ESZ = Tr<DT>::W / 8;
     const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
     const int64_t off = cin << d.chunk_log2;    // first element of the chunk
     const int64_t rest = d.n - off;
     const uint32_t len = (uint32_t)(rest < (int64_t(1) << d.chunk_log2) ? rest : (int64_t(1) << d.chunk_log2));
+    const char *gbase = static_cast<const char *>(d.g) + off * ESZ;
+    const char *tbase = static_cast<const char *>(d.t) + off * ESZ;
+    gvec_t *gp = (gvec_t *)gbase;
+    gvec_t *tp = (gvec_t *)tbase;
 
     Lane L;
     Uni Un;
     lane_init(L, Un);
 
     const uint32_t nsuper = d.aligned ? len / SUPER : 0;
-    constexpr int ESZ = Tr<DT>::W / 8;
-    const uint4 *gp = reinterpret_cast<const uint4 *>(static_cast<const char *>(d.g) + off * ESZ);
-    const uint4 *tp = reinterpret_cast<const uint4 *>(static_cast<const char *>(d.t) + off * ESZ);
+    uint32_t ndef = 0;                           // wave-uniform
 
-    if (nsuper > 0) {
-        uint4 gc[U], tc[U];
+    auto flush = [&]() {
+#pragma unroll 1
+        for (uint32_t k = 0; k < ndef; ++k) {
+            const uint32_t v = sh.defer[wave][k];
+            const u32x4 gv = gp[v * kBlock + tid];
+            const u32x4 tv = tp[v * kBlock + tid];
+            const uint32_t li0 = (v * kBlock + tid) * VEC;
+#pragma unroll 1
+            for (int j = 0; j < VEC; ++j)
+                generic_elem<DT, NT>(L, sh, P, lane_elem<DT>(gv, j), lane_elem<DT>(tv, j), li0 + j, tid);
+        }
+        ndef = 0;
+    };
+
+    // Two register sets, used in turn: the loads of super-step s+1 are in
+    // flight while super-step s is processed, without register copies.
+    auto load = [&](u32x4 (&g)[U], u32x4 (&t)[U], uint32_t s) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            gc[u] = gp[u * kBlock + tid];
-            tc[u] = tp[u * kBlock + tid];
+            g[u] = gp[(s * U + u) * kBlock + tid];
+            t[u] = tp[(s * U + u) * kBlock + tid];
         }
-        for (uint32_t s = 0; s < nsuper; ++s) {
-            uint4 gn[U], tn[U];
-            const bool more = s + 1 < nsuper;
-            if (more) {
-                const uint32_t base = (s + 1) * (U * kBlock);
+    };
+    auto step = [&](const u32x4 (&g)[U], const u32x4 (&t)[U], uint32_t s) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    gn[u] = gp[base + u * kBlock + tid];
-                    tn[u] = tp[base + u * kBlock + tid];
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t li0 = ((s * U + u) * kBlock + tid) * VEC;
-                vec_step<DT, NT>(L, Un, sh, P, gc[u], tc[u], li0, tid);
-            }
-            if (more) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    gc[u] = gn[u];
-                    tc[u] = tn[u];
-                }
+        for (int u = 0; u < U; ++u) {
+            const uint32_t v = s * U + u;
+            if (vec_fast<DT, NT>(L, Un, sh, P, g[u], t[u], v, tid)) {
+                sh.defer[wave][ndef] = v;      // every lane writes the same value
+                ++ndef;
             }
         }
+        if (ndef > kDeferCap - U) flush();
+    };
+    if (nsuper > 0) {
+        u32x4 ga[U], ta[U], gb[U], tb[U];
+        load(ga, ta, 0);
+        for (uint32_t s = 0; s < nsuper; s += 2) {
+            if (s + 1 < nsuper) load(gb, tb, s + 1);
+            step(ga, ta, s);
+            if (s + 1 >= nsuper) break;
+            if (s + 2 < nsuper) load(ga, ta, s + 2);
+            step(gb, tb, s + 1);
+        }
+        flush();
     }
     // ragged tail, or the whole chunk when a pointer is not 16-byte aligned
-    const void *gb = static_cast<const char *>(d.g) + off * ESZ;
-    const void *tb = static_cast<const char *>(d.t) + off * ESZ;
+#pragma unroll 1
     for (uint32_t li = nsuper * SUPER + tid; li < len; li += kBlock)
-        generic_elem<DT, NT>(L, sh, P, load_elem<DT>(gb, li), load_elem<DT>(tb, li), li, tid);
+        generic_elem<DT, NT>(L, sh, P, load_elem<DT>(gbase, li), load_elem<DT>(tbase, li), li, tid);
+
+    // ---- resolve the fast-path maxima to element indices -----------------
+    uint32_t fa = kNone, fu = kNone;
+    if (L.vv_abs != kNone) {
+        const u32x4 gv = gp[L.vv_abs * kBlock + tid], tv = tp[L.vv_abs * kBlock + tid];
+#pragma unroll
+        for (int j = VEC - 1; j >= 0; --j) {
+            const double a = __builtin_fabs(widen<DT>(lane_elem<DT>(tv, j)) - widen<DT>(lane_elem<DT>(gv, j)));
+            if (a == L.vx_abs) fa = (L.vv_abs * kBlock + tid) * VEC + j;
+        }
+    }
+    if (L.vv_ulp != kNone) {
+        const u32x4 gv = gp[L.vv_ulp * kBlock + tid], tv = tp[L.vv_ulp * kBlock + tid];
+#pragma unroll
+        for (int j = VEC - 1; j >= 0; --j) {
+            const uint32_t gb = lane_elem<DT>(gv, j), tb = lane_elem<DT>(tv, j);
+            if (max(gb, tb) - min(gb, tb) == L.vu) fu = (L.vv_ulp * kBlock + tid) * VEC + j;
+        }
+    }
+    double mxa = L.vx_abs;
+    uint32_t ixa = fa;
+    lex_merge(mxa, ixa, L.gx_abs, L.gi_abs);
+    uint32_t mu = L.vu, ixu = fu;
+    lex_merge(mu, ixu, L.gu, L.gi_ulp);
 
     // ---- epilogue: reduce the block into the chunk record ----------------
-    const int wave = tid >> 6, lane = tid & 63;
     double sums[6] = {L.s_abs, L.s_sq, L.s_rel, L.s_g2, L.s_t2, L.s_gt};
 #pragma unroll
     for (int k = 0; k < 6; ++k) sums[k] = wsum(sums[k]);
-    double mxa = L.mx_abs, mxr = L.mx_rel;
-    uint32_t ixa = L.ix_abs, ixr = L.ix_rel, ixu = L.ix_ulp, mu = L.mu;
-    wmax_d(mxa, ixa);
-    wmax_d(mxr, ixr);
-    wmax_u(mu, ixu);
-    uint32_t fnan = wmin_u(L.first_nan), fval = wmin_u(L.first_valid);
-    uint64_t sulp = wsum_u64(L.s_ulp);
+    double mxr = L.mx_rel;
+    uint32_t ixr = L.ix_rel;
+    wmax(mxa, ixa);
+    wmax(mxr, ixr);
+    wmax(mu, ixu);
+    const uint32_t fnan = wmin_u(L.first_nan), fval = wmin_u(L.first_valid);
+    const uint64_t sulp = wsum_u64(L.s_ulp);
     uint32_t cnts[kCnt + PEAT_MAX_THRESHOLDS];
 #pragma unroll
     for (int c = 0; c < kCnt; ++c) cnts[c] = wsum_u(L.cnt[c]);
 #pragma unroll
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) cnts[kCnt + j] = j < NT ? wsum_u(L.mism[j]) : 0u;
-    // fast-path (wave-uniform) counts: every element there is valid, finite
-    // and has a nonzero golden
-    const uint32_t common = Un.common * 64u;
+    // fast-path counts: every element there is valid, finite, golden nonzero
+    const uint32_t common = Un.common * 64u * VEC;
     cnts[C_VALID] += common;
     cnts[C_FINITE] += common;
     cnts[C_REL] += common;
-    cnts[C_ZERO] += Un.zero;
 #pragma unroll
     for (int j = 0; j < NT; ++j) cnts[kCnt + j] += Un.mism[j];
     if (lane == 0) {
@@ -390,12 +499,10 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
         sh.rix[wave][3] = fnan;
         sh.rix[wave][4] = fval;
         sh.rmu[wave] = mu;
+        sh.rulp[wave] = sulp;
 #pragma unroll
         for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) sh.rcnt[wave][c] = cnts[c];
     }
-    // the u64 ulp sum is kept per wave in the double scratch (bit copy)
-    __shared__ uint64_t rulp[kWaves];
-    if (lane == 0) rulp[wave] = sulp;
     __syncthreads();
 
     ChunkPartial *out = P.partials + gchunk;
@@ -403,15 +510,13 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     {
         const int slot = tid >> 2, q = tid & 3;
         uint32_t acc = 0;
-        if (slot < kHistSlots) {
-            const uint32_t *row = sh.hist + slot * kBlock + q * 64;
+        const uint32_t *row = sh.hist + slot * kBlock + q * 64;
 #pragma unroll 8
-            for (int c = 0; c < 64; ++c) acc += row[(c + slot + 8 * q) & 63];
-        }
+        for (int c = 0; c < 64; ++c) acc += row[(c + slot + 8 * q) & 63];
         acc += __shfl_xor(acc, 1);
         acc += __shfl_xor(acc, 2);
-        if (q == 0 && slot < kHistSlots) out->hist[slot] = acc;
-        // slots 64, 65 (beyond 256/4 threads): one thread each
+        if (q == 0) out->hist[slot] = acc;
+        // slots 64..66 (beyond 256/4 threads): one thread each
         if (tid < kHistSlots - 64) {
             const int s2 = 64 + tid;
             uint32_t a2 = 0;
@@ -428,19 +533,19 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
         for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] = 0;
         for (int w = 0; w < kWaves; ++w) {
             for (int k = 0; k < 6; ++k) s[k] += sh.rd[w][k];
-            double va = sh.rmax[w][0], vr = sh.rmax[w][1];
-            uint32_t xa = sh.rix[w][0], xr = sh.rix[w][1], xu = sh.rix[w][2];
-            if (xa != kNone && (ia == kNone || va > ma || (va == ma && xa < ia))) { ma = va; ia = xa; }
-            if (xr != kNone && (ir == kNone || vr > mr || (vr == mr && xr < ir))) { mr = vr; ir = xr; }
-            uint32_t vu = sh.rmu[w];
-            if (xu != kNone && (iu == kNone || vu > m || (vu == m && xu < iu))) { m = vu; iu = xu; }
+            lex_merge(ma, ia, sh.rmax[w][0], sh.rix[w][0]);
+            lex_merge(mr, ir, sh.rmax[w][1], sh.rix[w][1]);
+            lex_merge(m, iu, sh.rmu[w], sh.rix[w][2]);
             fn = min(fn, sh.rix[w][3]);
             fv = min(fv, sh.rix[w][4]);
-            su += rulp[w];
+            su += sh.rulp[w];
             for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] += sh.rcnt[w][c];
         }
         // every ULP distance in the chunk is 0: the first valid element is the maximum
-        if (iu == kNone) { m = 0; iu = fv; }
+        if (iu == kNone || m == 0) {
+            m = 0;
+            iu = fv;
+        }
         out->s_abs = s[0];
         out->s_sq = s[1];
         out->s_rel = s[2];
@@ -469,18 +574,19 @@ __global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
     const SigDesc d = P.descs[pair];
     const int64_t cin = gchunk - d.first_chunk;
     const int tid = threadIdx.x;
-    // clear the lane-private histogram counters and build the exponent table
+    // clear the lane-private histogram counters and build the exponent table:
+    // slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi
     for (int i = tid; i < kHistSlots * kBlock; i += kBlock) sh.hist[i] = 0;
     const int w = (P.hi - P.lo) / P.nbins;
     for (int E = tid; E < 2048; E += kBlock) {
         int slot;
         if (E == 0) {
-            slot = 0;                          // error 0 (counted apart, under here)
+            slot = 0;
         } else if (E == 2047) {
-            slot = P.nbins + 1;                // infinite error
+            slot = P.nbins + 2;                // infinite error
         } else {
-            int k = E - 1023;                  // a in [2^k, 2^(k+1))
-            slot = k < P.lo ? 0 : (k >= P.hi ? P.nbins + 1 : 1 + (k - P.lo) / w);
+            const int k = E - 1023;            // a in [2^k, 2^(k+1))
+            slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
         }
         sh.slot_of_exp[E] = (uint8_t)slot;
     }
@@ -505,7 +611,7 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     __shared__ uint64_t su[kWaves][2 + kCnt + PEAT_MAX_THRESHOLDS];
     __shared__ uint64_t sh_hist[kHistSlots];
 
-    // fp64 sums: each thread a fixed strided subset in order, then a fixed tree
+    // binary64 sums: each thread a fixed strided subset in order, then a fixed tree
     double s[6] = {0, 0, 0, 0, 0, 0};
     double ma = -1.0, mr = -1.0;
     int64_t ia = -1, ir = -1, iu = -1, fn = -1, fv = -1;
@@ -534,15 +640,14 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         for (int c = 0; c < m; ++c) h += parts[c].hist[tid];
         sh_hist[tid] = h;
     }
-    // wave reductions (fixed butterfly), then waves in order
 #pragma unroll
     for (int k = 0; k < 6; ++k) s[k] = wsum(s[k]);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
-        double ova = __shfl_xor(ma, o), ovr = __shfl_xor(mr, o);
-        int64_t oia = __shfl_xor(ia, o), oir = __shfl_xor(ir, o), oiu = __shfl_xor(iu, o);
-        uint64_t omu = __shfl_xor(mu, o);
-        int64_t ofn = __shfl_xor(fn, o), ofv = __shfl_xor(fv, o);
+        const double ova = __shfl_xor(ma, o), ovr = __shfl_xor(mr, o);
+        const int64_t oia = __shfl_xor(ia, o), oir = __shfl_xor(ir, o), oiu = __shfl_xor(iu, o);
+        const uint64_t omu = __shfl_xor(mu, o);
+        const int64_t ofn = __shfl_xor(fn, o), ofv = __shfl_xor(fv, o);
         if (oia >= 0 && (ia < 0 || ova > ma || (ova == ma && oia < ia))) { ma = ova; ia = oia; }
         if (oir >= 0 && (ir < 0 || ovr > mr || (ovr == mr && oir < ir))) { mr = ovr; ir = oir; }
         if (oiu >= 0 && (iu < 0 || omu > mu || (omu == mu && oiu < iu))) { mu = omu; iu = oiu; }
@@ -565,21 +670,21 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     if (tid != 0) return;
     double S[6] = {0, 0, 0, 0, 0, 0};
     double MA = -1.0, MR = -1.0;
-    int64_t IA = -1, IR = -1, IU = -1, FN = -1, FV = -1;
+    int64_t IA = -1, IR = -1, IU = -1, FN = -1;
     uint64_t MU = 0, SU = 0, CN[kCnt + PEAT_MAX_THRESHOLDS];
     for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) CN[k] = 0;
     for (int w = 0; w < kWaves; ++w) {
         for (int k = 0; k < 6; ++k) S[k] += sd[w][k];
-        double va = sd[w][6], vr = sd[w][7];
-        int64_t xa = si[w][0], xr = si[w][1], xu = si[w][2];
+        const double va = sd[w][6], vr = sd[w][7];
+        const int64_t xa = si[w][0], xr = si[w][1], xu = si[w][2];
         if (xa >= 0 && (IA < 0 || va > MA || (va == MA && xa < IA))) { MA = va; IA = xa; }
         if (xr >= 0 && (IR < 0 || vr > MR || (vr == MR && xr < IR))) { MR = vr; IR = xr; }
         if (xu >= 0 && (IU < 0 || su[w][0] > MU || (su[w][0] == MU && xu < IU))) { MU = su[w][0]; IU = xu; }
         if (si[w][3] >= 0 && (FN < 0 || si[w][3] < FN)) FN = si[w][3];
-        if (si[w][4] >= 0 && (FV < 0 || si[w][4] < FV)) FV = si[w][4];
         SU += su[w][1];
         for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) CN[k] += su[w][2 + k];
     }
+    const int nb = P.nbins;
     peat_signature_t o;
     o.n = d.n;
     o.n_valid = (int64_t)CN[C_VALID];
@@ -593,10 +698,10 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     o.first_nan_index = FN;
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j)
         o.n_mismatch[j] = j < P.nthr ? (int64_t)(CN[kCnt + j] + CN[C_NANPAIR]) : 0;
-    o.hist_zero = (int64_t)CN[C_ZERO];
-    o.hist_under = (int64_t)sh_hist[0] - (int64_t)CN[C_ZERO];
-    o.hist_over = (int64_t)sh_hist[P.nbins + 1];
-    for (int b = 0; b < PEAT_MAX_BINS; ++b) o.hist[b] = b < P.nbins ? (int64_t)sh_hist[1 + b] : 0;
+    o.hist_zero = (int64_t)sh_hist[0];
+    o.hist_under = (int64_t)sh_hist[1];
+    o.hist_over = (int64_t)sh_hist[nb + 2];
+    for (int b = 0; b < PEAT_MAX_BINS; ++b) o.hist[b] = b < nb ? (int64_t)sh_hist[2 + b] : 0;
     const double qnan = __longlong_as_double(0x7FF8000000000000LL);
     o.max_abs = IA >= 0 ? MA : qnan;
     o.argmax_abs = IA;
@@ -611,7 +716,6 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     o.sum_g2 = S[3];
     o.sum_t2 = S[4];
     o.sum_gt = S[5];
-    (void)FV;
     P.outs[pair] = o;
 }
 
