@@ -76,6 +76,21 @@ __device__ __forceinline__ void flip(const InjDesc &d, uint64_t i) {
     }
 }
 
+constexpr int kQCap = 64 + 32 * 64;   // per-wave queue: < 64 left over + one append of 32 per lane
+
+// Low 56 bits of U_i for a queued candidate (its top byte is 0, so U_i is
+// just these bits): flip the element when they are below T.
+__device__ __forceinline__ uint32_t settle_candidate(const InjDesc &d, uint64_t i) {
+    uint64_t B[4];
+    philox(i >> 2, 1, d.seed, B);
+    const uint64_t low = B[i & 3] & ((uint64_t(1) << 56) - 1);
+    if (low < d.T) {
+        flip(d, i);
+        return 1;
+    }
+    return 0;
+}
+
 __global__ void __launch_bounds__(kBlock) inject_kernel(InjParams P) {
     const int64_t seg = blockIdx.x;
     const int item = P.seg_item[seg];
@@ -86,39 +101,56 @@ __global__ void __launch_bounds__(kBlock) inject_kernel(InjParams P) {
     const uint32_t ngroups = (uint32_t)((len + 31) / 32);
     const uint64_t q0 = s0 >> 5;
     const uint64_t T = d.T;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint32_t flips = 0;
 
     if (!d.all && T < (uint64_t(1) << 56)) {
-        for (uint32_t g = threadIdx.x; g < ngroups; g += kBlock) {
-            const uint64_t q = q0 + g;
-            uint64_t A[4];
-            philox(q, 0, d.seed, A);
-            // exact zero-byte mask of each 32-bit half: bit 7 of a byte is set
-            // iff the byte is zero
+        // An element can flip only if the top byte of U_i is 0.  Each lane
+        // draws one block per group of 32 elements; the zero-byte elements
+        // go to a per-wave queue (segment-relative offsets) whose entries
+        // are settled 64 at a time, one per lane.
+        __shared__ uint32_t queue[kBlock / 64][kQCap];
+        uint32_t qn = 0;                                   // wave-uniform
+        const uint32_t iters = (ngroups + kBlock - 1) / kBlock;
+        for (uint32_t k = 0; k < iters; ++k) {
+            const uint32_t g = k * kBlock + threadIdx.x;
             uint32_t cand = 0;
+            if (g < ngroups) {
+                uint64_t A[4];
+                philox(q0 + g, 0, d.seed, A);
+                // exact zero-byte mask of each 32-bit half: bit 7 of a byte
+                // is set iff the byte is zero
 #pragma unroll
-            for (int w = 0; w < 8; ++w) {
-                const uint32_t v = (uint32_t)(A[w >> 1] >> (32 * (w & 1)));
-                uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v | 0x7F7F7F7Fu);
-                // gather bits 7, 15, 23, 31 into 4 consecutive bits
-                const uint32_t nib = ((z >> 7) & 1u) | ((z >> 14) & 2u) | ((z >> 21) & 4u) | ((z >> 28) & 8u);
-                cand |= nib << (4 * w);
-            }
-            const uint64_t ibase = q << 5;
-            if (n - ibase < 32) cand &= (1u << (uint32_t)(n - ibase)) - 1u;   // ragged end
-            while (cand) {
-                const int b = __ffs(cand) - 1;
-                cand &= cand - 1;
-                const uint64_t i = ibase + (uint64_t)b;
-                uint64_t B[4];
-                philox(i >> 2, 1, d.seed, B);
-                const uint64_t low = B[i & 3] & ((uint64_t(1) << 56) - 1);
-                if (low < T) {     // top byte 0, so U_i = low
-                    flip(d, i);
-                    ++flips;
+                for (int w = 0; w < 8; ++w) {
+                    const uint32_t v = (uint32_t)(A[w >> 1] >> (32 * (w & 1)));
+                    const uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v | 0x7F7F7F7Fu);
+                    const uint32_t nib = ((z >> 7) & 1u) | ((z >> 14) & 2u) | ((z >> 21) & 4u) | ((z >> 28) & 8u);
+                    cand |= nib << (4 * w);
                 }
+                const uint64_t rest = len - ((uint64_t)g << 5);
+                if (rest < 32) cand &= (1u << (uint32_t)rest) - 1u;   // ragged end
+            }
+            // append this iteration's candidates, one per lane per round
+            while (true) {
+                const bool has = cand != 0;
+                const uint64_t m = __ballot(has);
+                if (m == 0) break;
+                if (has) {
+                    const uint32_t pos = qn + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+                    queue[wave][pos] = (g << 5) | (uint32_t)(__ffs(cand) - 1);
+                    cand &= cand - 1;
+                }
+                qn += (uint32_t)__popcll(m);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+            while (qn >= 64) {                              // settle full batches (LIFO)
+                qn -= 64;
+                flips += settle_candidate(d, s0 + queue[wave][qn + lane]);
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
             }
         }
+        if ((uint32_t)lane < qn) flips += settle_candidate(d, s0 + queue[wave][lane]);
     } else {
         // general threshold (rate >= 2^-8) or every element
         const uint64_t Ttop = T >> 56, Tlow = T & ((uint64_t(1) << 56) - 1);

@@ -308,6 +308,11 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
         L.vv_ulp = v;
     }
     if (mcand != 0) {
+        // The filter threshold is shared by the wave: an element whose
+        // relative error is below the wave's running maximum cannot be the
+        // chunk's maximum, so only a few vectors per chunk get here.  Ties
+        // with the maximum still pass (the margin keeps them), and the lanes'
+        // (value, lowest index) maxima are merged at the end of the chunk.
         const uint32_t li0 = (v * kBlock + tid) * VEC;
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
@@ -316,10 +321,13 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
                 if (r > L.mx_rel) {
                     L.mx_rel = r;
                     L.ix_rel = li0 + j;
-                    L.rthr = r - r * kRelMargin;
                 }
             }
         }
+        double wm = L.mx_rel;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) wm = __builtin_fmax(wm, __shfl_xor(wm, o));
+        L.rthr = wm - wm * kRelMargin;
     }
     U.common += 1;
     L.first_valid = min(L.first_valid, (v * kBlock + tid) * VEC);
