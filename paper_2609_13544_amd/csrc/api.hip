@@ -222,22 +222,29 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
     if ((rc = current_dev(&dv))) return rc;
     Dev &d = *dv;
 
-    // partition every pair into chunks
+    // partition every pair into chunks; the chunks of each element type get
+    // one contiguous range of the global numbering (one launch per type)
     std::vector<SigDesc> descs((size_t)count);
     int64_t total = 0;
-    for (int k = 0; k < count; ++k) {
-        SigDesc &sd = descs[k];
-        sd.g = pairs[k].golden;
-        sd.t = pairs[k].test;
-        sd.n = pairs[k].n;
-        sd.dtype = pairs[k].dtype;
-        sd.chunk_log2 = chunk_log2_for(sd.n);
-        const int64_t nch = (sd.n + (int64_t(1) << sd.chunk_log2) - 1) >> sd.chunk_log2;
-        sd.first_chunk = total;
-        sd.nchunks = (int32_t)nch;
-        sd.aligned = ((reinterpret_cast<uintptr_t>(sd.g) | reinterpret_cast<uintptr_t>(sd.t)) & 15) == 0;
-        total += nch;
+    int64_t range[4] = {0, 0, 0, 0};
+    for (int dt = 0; dt < 3; ++dt) {
+        range[dt] = total;
+        for (int k = 0; k < count; ++k) {
+            if (pairs[k].dtype != dt) continue;
+            SigDesc &sd = descs[k];
+            sd.g = pairs[k].golden;
+            sd.t = pairs[k].test;
+            sd.n = pairs[k].n;
+            sd.dtype = pairs[k].dtype;
+            sd.chunk_log2 = chunk_log2_for(sd.n);
+            const int64_t nch = (sd.n + (int64_t(1) << sd.chunk_log2) - 1) >> sd.chunk_log2;
+            sd.first_chunk = total;
+            sd.nchunks = (int32_t)nch;
+            sd.aligned = ((reinterpret_cast<uintptr_t>(sd.g) | reinterpret_cast<uintptr_t>(sd.t)) & 15) == 0;
+            total += nch;
+        }
     }
+    range[3] = total;
     if (total > 0x7FFFFFFF) return fail(PEAT_EINVAL, "batch needs %lld chunks (max 2^31-1)", (long long)total);
 
     const size_t b_desc = align_up(sizeof(SigDesc) * count);
@@ -257,6 +264,7 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
     HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
 
     SigParams P;
+    P.chunk_base = 0;
     P.descs = reinterpret_cast<const SigDesc *>(ws);
     P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc);
     P.partials = reinterpret_cast<ChunkPartial *>(ws + b_desc + b_map);
@@ -272,7 +280,7 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
 
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;
-    HIP_OR_FAIL(launch_sig_chunks(P, total, s));
+    HIP_OR_FAIL(launch_sig_chunks(P, range, s));
     if ((rc = prof_end(d, s, 0, ev))) return rc;
     if ((rc = prof_begin(d, s, &ev))) return rc;
     HIP_OR_FAIL(launch_sig_finalize(P, s));

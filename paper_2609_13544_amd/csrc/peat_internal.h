@@ -57,6 +57,7 @@ struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
 };
 
 struct SigParams {
+    int64_t chunk_base;            // first global chunk of this launch
     const SigDesc *descs;
     const int32_t *chunk_pair;     // chunk -> pair index
     ChunkPartial *partials;        // one per chunk
@@ -91,7 +92,9 @@ struct InjParams {
 };
 
 // Kernel launchers (defined in the .hip translation units).
-hipError_t launch_sig_chunks(const SigParams &p, int64_t total_chunks, hipStream_t s);
+// One launch per element type present: chunks of each type form one
+// contiguous range [range[dt], range[dt + 1]) of the global chunk numbering.
+hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[4], hipStream_t s);
 hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
 hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
 hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);

@@ -43,6 +43,9 @@ constexpr int kDeferCap = 32;            // deferred vectors per wave before a f
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte vector
 typedef __attribute__((address_space(1))) const u32x4 gvec_t;
+// Word 3 of a raw (unstrided, untyped) buffer resource on gfx9-family parts:
+// 32-bit data format, default swizzle and cache policy.
+constexpr int kBufFlags = 0x00020000;
 typedef __attribute__((address_space(1))) const uint32_t gu32_t;
 typedef __attribute__((address_space(1))) const uint16_t gu16_t;
 
@@ -410,15 +413,30 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
                 generic_elem<DT, NT>(L, sh, P, lane_elem<DT>(gv, j), lane_elem<DT>(tv, j), li0 + j, tid);
         }
         ndef = 0;
+        // Nothing of the flush stays in flight: the hot loop's header then
+        // waits only for its own prefetch.
+        __builtin_amdgcn_s_waitcnt(0);
     };
 
     // Two register sets, used in turn: the loads of super-step s+1 are in
-    // flight while super-step s is processed, without register copies.
+    // flight while super-step s is processed, without register copies.  The
+    // prefetch is issued unconditionally (clamped to the last super-step,
+    // where it is a redundant in-bounds reload) so that every path has the
+    // same number of loads outstanding and the waits stay partial.
+    // Buffer loads: the chunk base lives in a scalar resource, the per-lane
+    // offsets are loop-invariant registers and the super-step moves only the
+    // scalar offset, so no address register is rewritten while loads that
+    // read it are in flight.  The resource covers the chunk (at most 2^18
+    // elements = 1 MiB), and reads past its end return zero.
+    const __amdgpu_buffer_rsrc_t grs = __builtin_amdgcn_make_buffer_rsrc((void *)gbase, (short)0, (int)(len * ESZ), kBufFlags);
+    const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc((void *)tbase, (short)0, (int)(len * ESZ), kBufFlags);
+    const uint32_t lane_off = (uint32_t)tid * 16u;
     auto load = [&](u32x4 (&g)[U], u32x4 (&t)[U], uint32_t s) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            g[u] = gp[(s * U + u) * kBlock + tid];
-            t[u] = tp[(s * U + u) * kBlock + tid];
+            const int so = (int)((s * U + u) * (kBlock * 16u));
+            g[u] = __builtin_amdgcn_raw_buffer_load_b128(grs, (int)lane_off, so, 0);
+            t[u] = __builtin_amdgcn_raw_buffer_load_b128(trs, (int)lane_off, so, 0);
         }
     };
     auto step = [&](const u32x4 (&g)[U], const u32x4 (&t)[U], uint32_t s) {
@@ -430,19 +448,31 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
                 ++ndef;
             }
         }
-        if (ndef > kDeferCap - U) flush();
     };
     if (nsuper > 0) {
         u32x4 ga[U], ta[U], gb[U], tb[U];
+        const uint32_t last = nsuper - 1;
         load(ga, ta, 0);
-        for (uint32_t s = 0; s < nsuper; s += 2) {
-            if (s + 1 < nsuper) load(gb, tb, s + 1);
-            step(ga, ta, s);
-            if (s + 1 >= nsuper) break;
-            if (s + 2 < nsuper) load(ga, ta, s + 2);
-            step(gb, tb, s + 1);
+        uint32_t s = 0;
+        // The deferred list is flushed outside the hot loop, which exits
+        // when the list may not hold the next two super-steps.
+        while (s < nsuper) {
+            for (; s < nsuper; s += 2) {
+                load(gb, tb, min(s + 1, last));
+                step(ga, ta, s);
+                if (s + 1 >= nsuper) {
+                    s += 2;
+                    break;
+                }
+                load(ga, ta, min(s + 2, last));
+                step(gb, tb, s + 1);
+                if (ndef > kDeferCap - 2 * U) {
+                    s += 2;
+                    break;
+                }
+            }
+            flush();
         }
-        flush();
     }
     // ragged tail, or the whole chunk when a pointer is not 16-byte aligned
 #pragma unroll 1
@@ -574,10 +604,10 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     }
 }
 
-template <int NT>
+template <int DT, int NT>
 __global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
     __shared__ Shared sh;
-    const int64_t gchunk = blockIdx.x;
+    const int64_t gchunk = P.chunk_base + blockIdx.x;
     const int pair = P.chunk_pair[gchunk];
     const SigDesc d = P.descs[pair];
     const int64_t cin = gchunk - d.first_chunk;
@@ -599,11 +629,7 @@ __global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
         sh.slot_of_exp[E] = (uint8_t)slot;
     }
     __syncthreads();
-    switch (d.dtype) {
-        case PEAT_F32: chunk_body<PEAT_F32, NT>(P, sh, d, cin, gchunk); break;
-        case PEAT_F16: chunk_body<PEAT_F16, NT>(P, sh, d, cin, gchunk); break;
-        default: chunk_body<PEAT_BF16, NT>(P, sh, d, cin, gchunk); break;
-    }
+    chunk_body<DT, NT>(P, sh, d, cin, gchunk);
 }
 
 // ---- pass 2 ----------------------------------------------------------------
@@ -729,15 +755,29 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
 
 }  // namespace
 
-hipError_t launch_sig_chunks(const SigParams &p, int64_t total_chunks, hipStream_t s) {
-    if (total_chunks <= 0) return hipSuccess;
-    dim3 grid((unsigned)total_chunks), block(kBlock);
+template <int DT>
+hipError_t launch_dtype(const SigParams &p, int64_t n, hipStream_t s) {
+    dim3 grid((unsigned)n), block(kBlock);
     switch (p.nthr_pad) {
-        case 2: hipLaunchKernelGGL(sig_chunk<2>, grid, block, 0, s, p); break;
-        case 4: hipLaunchKernelGGL(sig_chunk<4>, grid, block, 0, s, p); break;
-        default: hipLaunchKernelGGL(sig_chunk<8>, grid, block, 0, s, p); break;
+        case 2: hipLaunchKernelGGL((sig_chunk<DT, 2>), grid, block, 0, s, p); break;
+        case 4: hipLaunchKernelGGL((sig_chunk<DT, 4>), grid, block, 0, s, p); break;
+        default: hipLaunchKernelGGL((sig_chunk<DT, 8>), grid, block, 0, s, p); break;
     }
     return hipGetLastError();
+}
+
+hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[4], hipStream_t s) {
+    for (int dt = 0; dt < 3; ++dt) {
+        const int64_t n = range[dt + 1] - range[dt];
+        if (n <= 0) continue;
+        SigParams q = p;
+        q.chunk_base = range[dt];
+        hipError_t e = dt == PEAT_F32 ? launch_dtype<PEAT_F32>(q, n, s)
+                     : dt == PEAT_F16 ? launch_dtype<PEAT_F16>(q, n, s)
+                                      : launch_dtype<PEAT_BF16>(q, n, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s) {
