@@ -275,8 +275,11 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
     P.nbins = bins->nbins;
     P.nthr = thr->count;
     P.nthr_pad = thr->count <= 2 ? 2 : (thr->count <= 4 ? 4 : 8);
-    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j)
+    P.thr_min = HUGE_VAL;
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) {
         P.thr[j] = j < thr->count ? thr->abs_tol[j] : HUGE_VAL;
+        if (P.thr[j] < P.thr_min) P.thr_min = P.thr[j];
+    }
 
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;

@@ -67,6 +67,7 @@ struct SigParams {
     int32_t nthr;                  // real thresholds
     int32_t nthr_pad;              // 2, 4 or 8 compared per element (+Inf padding)
     double thr[PEAT_MAX_THRESHOLDS];
+    double thr_min;                // smallest thr (+Inf when there are none)
 };
 
 struct InjDesc {                 // one per injected tensor (64 bytes)

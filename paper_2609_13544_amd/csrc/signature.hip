@@ -39,6 +39,14 @@ namespace peat {
 namespace {
 
 constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
+// Fast-path limit on the relative error: an element at or above it (or NaN)
+// sends its vector to the generic path.  A sign change between finite golden
+// and test values gives |t - g| >= |g|, i.e. a relative error of at least 1
+// (less the reciprocal's 2^-48), and a zero golden value gives Inf or NaN, so
+// this one comparison also catches every case the fast path does not handle.
+// Below the limit t lies within a factor 1.5 of g, so an f32 ULP distance is
+// below 2^24 and an f16/bf16 one below 2^11.
+constexpr double kRareRel = 0.5;
 constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte vector
@@ -105,29 +113,54 @@ __device__ __forceinline__ double recip(double b) {
     return __builtin_fma(y, __builtin_fma(-b, y, 1.0), y);
 }
 
+// Reciprocals of four magnitudes from one reciprocal of their product (the
+// hardware reciprocal issues at a quarter of the fma rate).  The inputs are
+// widened f32/f16/bf16 values, so the product of four stays a normal binary64
+// number (between 2^-600 and 2^512) and the pairwise products are exact; each
+// result is within a few units of 2^-48 of 1/x.  A zero, Inf or NaN among
+// the four makes all four results NaN or Inf.
+__device__ __forceinline__ void recip4(const double *x, double *r) {
+    const double p01 = x[0] * x[1], p23 = x[2] * x[3];
+    const double inv = recip(p01 * p23);
+    const double i01 = inv * p23, i23 = inv * p01;
+    r[0] = x[1] * i01;
+    r[1] = x[0] * i01;
+    r[2] = x[3] * i23;
+    r[3] = x[2] * i23;
+}
+
 struct Lane {
     double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;
-    double vx_abs;                 // fast path: max |err| per lane ...
-    uint32_t vv_abs;               // ... and the vector number reaching it first
-    uint32_t vu, vv_ulp;           // fast path: max ULP and its vector number
     double gx_abs;                 // generic path: max |err| and element index
     uint32_t gi_abs;
     uint32_t gu, gi_ulp;           // generic path: max ULP and element index
-    double mx_rel, rthr;           // both paths: max rel err, its index, filter
+    double mx_rel;                 // both paths: max rel err and its index
+    double rthr;                   // fast-path filter, at most kRareRel
     uint32_t ix_rel;
     uint64_t s_ulp;
+    uint32_t s_ulp32;              // fast path: ULP sum of the current super-step
     uint32_t first_nan, first_valid;
     uint32_t cnt[kCnt];                    // generic-path counts (per lane)
     uint32_t mism[PEAT_MAX_THRESHOLDS];    // generic-path mismatches (per lane)
 };
 
-struct Uni {                               // fast-path counts (wave-uniform)
+// Fast-path state shared by the wave.  Vectors reach the fast path in
+// increasing vector number, and every element of a later vector has a higher
+// index than every element of an earlier one, so the wave only needs its
+// running maximum and the vector number that first exceeded the previous one:
+// an element equal to the running maximum in a later vector cannot be the
+// (value, lowest index) maximum.
+struct Uni {
     uint32_t common;                       // ordinary vectors per lane
     uint32_t mism[PEAT_MAX_THRESHOLDS];
+    uint32_t first;                        // first ordinary vector number
+    double wx_abs;                         // running max |err| ...
+    uint32_t wv_abs;                       // ... first reached in this vector
+    uint32_t wu, wv_ulp;                   // running max ULP, its vector
 };
 
 struct Shared {
-    uint8_t slot_of_exp[2048];             // binary64 exponent field -> slot (LDS offset 0)
+    uint32_t hrow[2048];                   // binary64 exponent field -> slot * kBlock
     uint32_t hist[kHistSlots * kBlock];    // lane-private counters, [slot][lane]
     uint32_t defer[kWaves][kDeferCap];     // deferred vector numbers per wave
     double rd[kWaves][6];
@@ -140,10 +173,6 @@ struct Shared {
 
 __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
     L.s_abs = L.s_sq = L.s_rel = L.s_g2 = L.s_t2 = L.s_gt = 0.0;
-    L.vx_abs = -1.0;
-    L.vv_abs = kNone;
-    L.vu = 0;
-    L.vv_ulp = kNone;
     L.gx_abs = -1.0;
     L.gi_abs = kNone;
     L.gu = 0;
@@ -152,19 +181,25 @@ __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
     L.rthr = -1.0;
     L.ix_rel = kNone;
     L.s_ulp = 0;
+    L.s_ulp32 = 0;
     L.first_nan = L.first_valid = kNone;
 #pragma unroll
     for (int c = 0; c < kCnt; ++c) L.cnt[c] = 0;
 #pragma unroll
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) L.mism[j] = 0;
     U.common = 0;
+    U.first = kNone;
+    U.wx_abs = -1.0;
+    U.wv_abs = kNone;
+    U.wu = 0;
+    U.wv_ulp = kNone;
 #pragma unroll
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) U.mism[j] = 0;
 }
 
 __device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
     const uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: sign bit clear
-    atomicAdd(&sh.hist[(uint32_t)sh.slot_of_exp[E] * kBlock + tid], 1u);
+    atomicAdd(&sh.hist[sh.hrow[E] + tid], 1u);
 }
 
 // Every case of one pair (NaN, Inf, zero golden, sign change, subnormals).
@@ -216,7 +251,7 @@ __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParam
         if (r > L.mx_rel || (r == L.mx_rel && li < L.ix_rel)) {
             L.mx_rel = r;
             L.ix_rel = li;
-            L.rthr = r - r * kRelMargin;
+            L.rthr = __builtin_fmin(r - r * kRelMargin, kRareRel);
         }
     }
 }
@@ -236,61 +271,112 @@ __device__ __forceinline__ double absmax_f64(double a, double b) {
     return r;
 }
 
+// Wave maximum of a binary64 value, returned as a wave-uniform scalar.
+__device__ __forceinline__ double wave_max_uniform(double x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = __builtin_fmax(x, __shfl_xor(x, o));
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ uint32_t wave_max_uniform_u(uint32_t x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = max(x, (uint32_t)__shfl_xor(x, o));
+    return __builtin_amdgcn_readfirstlane(x);
+}
+
 // One 16-byte vector of golden and of test (vector number v of the lane's
 // sequence).  Called in wave-uniform control flow with every lane active.
 // Returns true (wave-uniform) when the vector must go to the generic path.
 //
-// Everything the decision needs -- and every per-vector reduction (maxima,
-// ULP distances, histogram slots) -- is computed before the branch as wave
-// masks and plain values, so the hot block only accumulates; the histogram's
-// table reads are all issued before its atomic adds, so they share one LDS
-// round trip.
+// Every per-element decision is one wave mask: rare elements, candidates for
+// the max relative error, and a new running maximum of |err| or of the ULP
+// distance all land in one rarely taken branch, so the common path only
+// accumulates.  The histogram's row reads are all issued before its atomic
+// adds, so they share one LDS round trip.
 template <int DT, int NT>
 __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
                                          const u32x4 &gv, const u32x4 &tv, uint32_t v, int tid) {
     constexpr int VEC = Tr<DT>::VEC;
     double G[VEC], T[VEC], E[VEC], R[VEC];
-    uint32_t slot[VEC], u[VEC];
-    uint64_t mrare = 0, mcand = 0;
-    double va = 0.0;
+    uint32_t row[VEC], u[VEC];
+    uint64_t mflag = 0;
+    double AG[VEC], IG[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        G[j] = widen<DT>(lane_elem<DT>(gv, j));
+        AG[j] = __builtin_fabs(G[j]);
+    }
+#pragma unroll
+    for (int q = 0; q < VEC; q += 4) recip4(AG + q, IG + q);
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
         const uint32_t gb = lane_elem<DT>(gv, j), tb = lane_elem<DT>(tv, j);
-        G[j] = widen<DT>(gb);
         T[j] = widen<DT>(tb);
         E[j] = T[j] - G[j];                                   // signed error
-        const double a = __builtin_fabs(E[j]);
-        R[j] = a * recip(__builtin_fabs(G[j]));
-        mrare |= __ballot(!__builtin_isfinite(R[j]));     // NaN/Inf on either side, or G == 0
-        mcand |= __ballot(R[j] > L.rthr);                 // may raise the lane's max rel error
-        va = j ? absmax_f64(va, E[j]) : a;
-        // same sign: the ULP distance is |t - g| of the bit patterns
+        R[j] = __builtin_fabs(E[j]) * IG[j];
+        // rare (>= kRareRel or NaN), or a candidate for the max relative error
+        mflag |= __ballot(!(R[j] < L.rthr));
+        // same sign on the fast path: the ULP distance is |t - g| of the bit patterns
         if constexpr (Tr<DT>::W == 32) {
             u[j] = absdiff_u32(gb, tb);
         } else {
             u[j] = __builtin_amdgcn_sad_u16(gb, tb, 0u);
         }
-        slot[j] = sh.slot_of_exp[(uint32_t)(__double_as_longlong(E[j]) >> 52) & 0x7FFu];
+        row[j] = sh.hrow[(uint32_t)(__double_as_longlong(E[j]) >> 52) & 0x7FFu];
     }
-    const uint32_t sx = (gv.x ^ tv.x) | (gv.y ^ tv.y) | (gv.z ^ tv.z) | (gv.w ^ tv.w);
-    mrare |= __ballot((sx & (Tr<DT>::W == 32 ? 0x80000000u : 0x80008000u)) != 0);   // a sign change
-    if (mrare != 0) return true;
+    double va = absmax_f64(E[0], E[1]);
+#pragma unroll
+    for (int j = 2; j < VEC; ++j) va = absmax_f64(va, E[j]);
+    uint32_t vu = max(u[0], u[1]);
+#pragma unroll
+    for (int j = 2; j < VEC; ++j) vu = max(vu, u[j]);
+    mflag |= __ballot(va > U.wx_abs);
+    mflag |= __ballot(vu > U.wu);
+    if (mflag != 0) {
+        uint64_t mrare = 0, mcand = 0;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            mrare |= __ballot(!(R[j] < kRareRel));
+            mcand |= __ballot(R[j] > L.rthr);
+        }
+        if (mrare != 0) return true;
+        if (mcand != 0) {
+            // The filter threshold is shared by the wave: an element whose
+            // relative error is below the wave's running maximum cannot be
+            // the chunk's maximum, so only a few vectors per chunk get here.
+            // Ties with the maximum still pass (the margin keeps them), and
+            // the lanes' (value, lowest index) maxima are merged at the end
+            // of the chunk.
+            const uint32_t li0 = (v * kBlock + tid) * VEC;
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                if (R[j] > L.rthr) {
+                    const double r = __builtin_fabs(E[j]) / __builtin_fabs(G[j]);   // IEEE quotient
+                    if (r > L.mx_rel) {
+                        L.mx_rel = r;
+                        L.ix_rel = li0 + j;
+                    }
+                }
+            }
+            const double wm = wave_max_uniform(L.mx_rel);
+            L.rthr = __builtin_fmin(wm - wm * kRelMargin, kRareRel);
+        }
+        if (__ballot(va > U.wx_abs) != 0) {
+            U.wx_abs = wave_max_uniform(va);
+            U.wv_abs = v;
+        }
+        if (__ballot(vu > U.wu) != 0) {
+            U.wu = wave_max_uniform_u(vu);
+            U.wv_ulp = v;
+        }
+    }
 
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[slot[j] * kBlock + tid], 1u);
-    uint32_t vu = u[0];
+    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[row[j] + tid], 1u);
 #pragma unroll
-    for (int j = 1; j < VEC; ++j) vu = max(vu, u[j]);
-    if constexpr (Tr<DT>::W == 32) {
-        // two f32 distances (< 2^31 each) per 32-bit partial sum
-#pragma unroll
-        for (int q = 0; q < VEC / 2; ++q) L.s_ulp += (uint64_t)(u[2 * q] + u[2 * q + 1]);
-    } else {
-        uint32_t us = 0;                       // eight f16/bf16 distances (< 2^16 each)
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) us += u[j];
-        L.s_ulp += us;
-    }
+    for (int j = 0; j < VEC; ++j) L.s_ulp32 += u[j];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
         L.s_abs += __builtin_fabs(E[j]);
@@ -299,41 +385,18 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
         L.s_t2 = __builtin_fma(T[j], T[j], L.s_t2);
         L.s_gt = __builtin_fma(G[j], T[j], L.s_gt);
         L.s_rel += R[j];
-#pragma unroll
-        for (int k = 0; k < NT; ++k) U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
     }
-    if (va > L.vx_abs) {
-        L.vx_abs = va;
-        L.vv_abs = v;
-    }
-    if (vu > L.vu) {
-        L.vu = vu;
-        L.vv_ulp = v;
-    }
-    if (mcand != 0) {
-        // The filter threshold is shared by the wave: an element whose
-        // relative error is below the wave's running maximum cannot be the
-        // chunk's maximum, so only a few vectors per chunk get here.  Ties
-        // with the maximum still pass (the margin keeps them), and the lanes'
-        // (value, lowest index) maxima are merged at the end of the chunk.
-        const uint32_t li0 = (v * kBlock + tid) * VEC;
+    // threshold mismatches: nothing to count while the vector's largest
+    // |err| is at most the smallest threshold
+    if (__ballot(va > P.thr_min) != 0) {
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
-            if (R[j] > L.rthr) {
-                const double r = __builtin_fabs(E[j]) / __builtin_fabs(G[j]);   // IEEE quotient
-                if (r > L.mx_rel) {
-                    L.mx_rel = r;
-                    L.ix_rel = li0 + j;
-                }
-            }
-        }
-        double wm = L.mx_rel;
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) wm = __builtin_fmax(wm, __shfl_xor(wm, o));
-        L.rthr = wm - wm * kRelMargin;
+            for (int k = 0; k < NT; ++k) U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
+        }
     }
     U.common += 1;
-    L.first_valid = min(L.first_valid, (v * kBlock + tid) * VEC);
+    if (U.first == kNone) U.first = v;
     return false;
 }
 
@@ -448,6 +511,9 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
                 ++ndef;
             }
         }
+        // at most U * VEC distances below 2^24 each: no 32-bit overflow
+        L.s_ulp += L.s_ulp32;
+        L.s_ulp32 = 0;
     };
     if (nsuper > 0) {
         u32x4 ga[U], ta[U], gb[U], tb[U];
@@ -480,28 +546,36 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
         generic_elem<DT, NT>(L, sh, P, load_elem<DT>(gbase, li), load_elem<DT>(tbase, li), li, tid);
 
     // ---- resolve the fast-path maxima to element indices -----------------
-    uint32_t fa = kNone, fu = kNone;
-    if (L.vv_abs != kNone) {
-        const u32x4 gv = gp[L.vv_abs * kBlock + tid], tv = tp[L.vv_abs * kBlock + tid];
+    // Reload the vector in which the wave's running maximum was first
+    // reached; its lanes holding that value become (value, index) candidates.
+    double mxa = -1.0;
+    uint32_t ixa = kNone, mu = 0, ixu = kNone;
+    if (Un.wv_abs != kNone) {
+        const u32x4 gv = gp[Un.wv_abs * kBlock + tid], tv = tp[Un.wv_abs * kBlock + tid];
 #pragma unroll
         for (int j = VEC - 1; j >= 0; --j) {
             const double a = __builtin_fabs(widen<DT>(lane_elem<DT>(tv, j)) - widen<DT>(lane_elem<DT>(gv, j)));
-            if (a == L.vx_abs) fa = (L.vv_abs * kBlock + tid) * VEC + j;
+            if (a == Un.wx_abs) {
+                mxa = a;
+                ixa = (Un.wv_abs * kBlock + tid) * VEC + j;
+            }
         }
     }
-    if (L.vv_ulp != kNone) {
-        const u32x4 gv = gp[L.vv_ulp * kBlock + tid], tv = tp[L.vv_ulp * kBlock + tid];
+    if (Un.wv_ulp != kNone) {
+        const u32x4 gv = gp[Un.wv_ulp * kBlock + tid], tv = tp[Un.wv_ulp * kBlock + tid];
 #pragma unroll
         for (int j = VEC - 1; j >= 0; --j) {
             const uint32_t gb = lane_elem<DT>(gv, j), tb = lane_elem<DT>(tv, j);
-            if (max(gb, tb) - min(gb, tb) == L.vu) fu = (L.vv_ulp * kBlock + tid) * VEC + j;
+            if (max(gb, tb) - min(gb, tb) == Un.wu) {
+                mu = Un.wu;
+                ixu = (Un.wv_ulp * kBlock + tid) * VEC + j;
+            }
         }
     }
-    double mxa = L.vx_abs;
-    uint32_t ixa = fa;
     lex_merge(mxa, ixa, L.gx_abs, L.gi_abs);
-    uint32_t mu = L.vu, ixu = fu;
     lex_merge(mu, ixu, L.gu, L.gi_ulp);
+    // the first ordinary element of this lane
+    if (Un.first != kNone) L.first_valid = min(L.first_valid, (Un.first * kBlock + tid) * VEC);
 
     // ---- epilogue: reduce the block into the chunk record ----------------
     double sums[6] = {L.s_abs, L.s_sq, L.s_rel, L.s_g2, L.s_t2, L.s_gt};
@@ -626,7 +700,7 @@ __global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
             const int k = E - 1023;            // a in [2^k, 2^(k+1))
             slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
         }
-        sh.slot_of_exp[E] = (uint8_t)slot;
+        sh.hrow[E] = (uint32_t)(slot * kBlock);
     }
     __syncthreads();
     chunk_body<DT, NT>(P, sh, d, cin, gchunk);
