@@ -119,13 +119,14 @@ __global__ void __launch_bounds__(kBlock) inject_kernel(InjParams P) {
                 uint64_t A[4];
                 philox(q0 + g, 0, d.seed, A);
                 // exact zero-byte mask of each 32-bit half: bit 7 of a byte
-                // is set iff the byte is zero
+                // is set iff the byte is zero; one multiply gathers bits
+                // 7, 15, 23, 31 into bits 28..31 (the other partial products
+                // land on distinct lower bits, so nothing carries)
 #pragma unroll
                 for (int w = 0; w < 8; ++w) {
                     const uint32_t v = (uint32_t)(A[w >> 1] >> (32 * (w & 1)));
                     const uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v | 0x7F7F7F7Fu);
-                    const uint32_t nib = ((z >> 7) & 1u) | ((z >> 14) & 2u) | ((z >> 21) & 4u) | ((z >> 28) & 8u);
-                    cand |= nib << (4 * w);
+                    cand |= ((z * 0x00204081u) >> 28) << (4 * w);
                 }
                 const uint64_t rest = len - ((uint64_t)g << 5);
                 if (rest < 32) cand &= (1u << (uint32_t)rest) - 1u;   // ragged end
