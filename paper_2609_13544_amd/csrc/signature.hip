@@ -48,6 +48,10 @@ constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
 // below 2^24 and an f16/bf16 one below 2^11.
 constexpr double kRareRel = 0.5;
 constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
+constexpr int kHistCols = kBlock / 2;     // histogram words per slot
+
+__device__ __forceinline__ uint32_t hist_col(int tid) { return (uint32_t)tid & (kHistCols - 1); }
+__device__ __forceinline__ uint32_t hist_inc(int tid) { return tid < kHistCols ? 1u : 0x10000u; }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte vector
 typedef __attribute__((address_space(1))) const u32x4 gvec_t;
@@ -161,7 +165,11 @@ struct Uni {
 
 struct Shared {
     uint32_t hrow[2048];                   // binary64 exponent field -> slot * kBlock
-    uint32_t hist[kHistSlots * kBlock];    // lane-private counters, [slot][lane]
+    // Lane-private 16-bit counters, two per word: word [slot][t mod 128]
+    // holds lane t's count in its low half when t < 128 and in its high half
+    // otherwise.  The two lanes of a word are in different waves, and a lane
+    // counts at most 2^18 / 256 = 1024 elements per chunk, so no half carries.
+    uint32_t hist[kHistSlots * kHistCols];
     uint32_t defer[kWaves][kDeferCap];     // deferred vector numbers per wave
     double rd[kWaves][6];
     double rmax[kWaves][2];
@@ -199,7 +207,7 @@ __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
 
 __device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
     const uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: sign bit clear
-    atomicAdd(&sh.hist[sh.hrow[E] + tid], 1u);
+    atomicAdd(&sh.hist[sh.hrow[E] + hist_col(tid)], hist_inc(tid));
 }
 
 // Every case of one pair (NaN, Inf, zero golden, sign change, subnormals).
@@ -374,7 +382,7 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
     }
 
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[row[j] + tid], 1u);
+    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[row[j] + hist_col(tid)], hist_inc(tid));
 #pragma unroll
     for (int j = 0; j < VEC; ++j) L.s_ulp32 += u[j];
 #pragma unroll
@@ -618,13 +626,16 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     __syncthreads();
 
     ChunkPartial *out = P.partials + gchunk;
-    // histogram: thread t sums slot t/4 over a quarter of the lanes
+    // histogram: thread t sums slot t/4 over a quarter of the words
     {
         const int slot = tid >> 2, q = tid & 3;
         uint32_t acc = 0;
-        const uint32_t *row = sh.hist + slot * kBlock + q * 64;
+        const uint32_t *row = sh.hist + slot * kHistCols + q * 32;
 #pragma unroll 8
-        for (int c = 0; c < 64; ++c) acc += row[(c + slot + 8 * q) & 63];
+        for (int c = 0; c < 32; ++c) {
+            const uint32_t w = row[(c + slot + 8 * q) & 31];
+            acc += (w & 0xFFFFu) + (w >> 16);
+        }
         acc += __shfl_xor(acc, 1);
         acc += __shfl_xor(acc, 2);
         if (q == 0) out->hist[slot] = acc;
@@ -632,7 +643,10 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
         if (tid < kHistSlots - 64) {
             const int s2 = 64 + tid;
             uint32_t a2 = 0;
-            for (int c = 0; c < kBlock; ++c) a2 += sh.hist[s2 * kBlock + c];
+            for (int c = 0; c < kHistCols; ++c) {
+                const uint32_t w = sh.hist[s2 * kHistCols + c];
+                a2 += (w & 0xFFFFu) + (w >> 16);
+            }
             out->hist[s2] = a2;
         }
     }
@@ -678,8 +692,13 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     }
 }
 
+// Three blocks per CU (12 waves) where the registers allow it without
+// spilling in the hot loop: f32 with two thresholds, the common case.
 template <int DT, int NT>
-__global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
+constexpr int chunk_blocks_per_cu() { return (DT == PEAT_F32 && NT == 2) ? 3 : 2; }
+
+template <int DT, int NT>
+__global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DT, NT>())) sig_chunk(SigParams P) {
     __shared__ Shared sh;
     const int64_t gchunk = P.chunk_base + blockIdx.x;
     const int pair = P.chunk_pair[gchunk];
@@ -688,7 +707,7 @@ __global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
     const int tid = threadIdx.x;
     // clear the lane-private histogram counters and build the exponent table:
     // slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi
-    for (int i = tid; i < kHistSlots * kBlock; i += kBlock) sh.hist[i] = 0;
+    for (int i = tid; i < kHistSlots * kHistCols; i += kBlock) sh.hist[i] = 0;
     const int w = (P.hi - P.lo) / P.nbins;
     for (int E = tid; E < 2048; E += kBlock) {
         int slot;
@@ -700,7 +719,7 @@ __global__ void __launch_bounds__(kBlock, 2) sig_chunk(SigParams P) {
             const int k = E - 1023;            // a in [2^k, 2^(k+1))
             slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
         }
-        sh.hrow[E] = (uint32_t)(slot * kBlock);
+        sh.hrow[E] = (uint32_t)(slot * kHistCols);
     }
     __syncthreads();
     chunk_body<DT, NT>(P, sh, d, cin, gchunk);
