@@ -16,6 +16,10 @@ Prints ONE JSON line on stdout (everything else goes to stderr):
             counter summary when it was taken on the current kernel source
   cpu_baseline  the CPU oracle on a bounded sample of the same workload
 
+Also reported: the read ceiling of the same box (peat_stream_read over a
+16 GiB buffer with the chunk pass's access pattern) and the signature chunk
+pass as a fraction of it; per-step times (median, min, max).
+
 Modes used to produce the committed profiles: --copy-calibration (a plain
 device copy of known size, for scaling the HBM byte counters).
 """
@@ -204,6 +208,29 @@ def cpu_baseline(wl: Workload, max_threads: int):
                       f"D2H copy {copy_s:.1f} s not counted"}
 
 
+def read_ceiling(torch, P, stream, gib: int = 16, reps: int = 5):
+    """GB/s of peat_stream_read over a gib-GiB buffer (best of reps)."""
+    buf = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
+    buf.fill_(0x5A)
+    sink = torch.zeros(-(-buf.numel() // P.STREAM_SPAN), dtype=torch.int32, device="cuda")
+    P.stream_read(buf, sink, stream=stream)          # warm-up
+    torch.cuda.synchronize()
+    P.profile_enable(True)
+    P.profile_read(P.K_STREAM_READ)
+    best = None
+    for _ in range(reps):
+        P.stream_read(buf, sink, stream=stream)
+        torch.cuda.synchronize()
+        ms, n = P.profile_read(P.K_STREAM_READ)
+        best = ms / n if best is None else min(best, ms / n)
+    P.profile_enable(False)
+    nbytes = buf.numel()
+    del buf
+    torch.cuda.empty_cache()
+    return {"GBps": round(nbytes / (best / 1e3) / 1e9, 1), "bytes": nbytes, "ms": round(best, 4),
+            "kernel": "peat_stream_read (16-byte nontemporal buffer loads, 2 MiB per 256-thread block)"}
+
+
 def copy_calibration(torch, gib: int, reps: int):
     """A plain device copy of known size, for scaling FETCH_SIZE/WRITE_SIZE."""
     n = gib * (1 << 30) // 4
@@ -224,6 +251,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="GIB")
+    ap.add_argument("--no-read-ceiling", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -263,14 +291,15 @@ def main():
     P.profile_enable(True)
     for k in (P.K_SIG_CHUNK, P.K_SIG_FINALIZE, P.K_INJECT, P.K_INJECT_SUM):
         P.profile_read(k)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for s in range(args.warmup, args.warmup + args.steps):
+    evs[0].record(stream)
+    for j, s in enumerate(range(args.warmup, args.warmup + args.steps)):
         step(s)
-    ev1.record(stream)
+        evs[j + 1].record(stream)
     torch.cuda.synchronize()
-    ms_total = ev0.elapsed_time(ev1)
+    ms_total = evs[0].elapsed_time(evs[-1])
+    step_ms = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps))
     P.profile_enable(False)
     chunk_ms, chunk_n = P.profile_read(P.K_SIG_CHUNK)
     fin_ms, fin_n = P.profile_read(P.K_SIG_FINALIZE)
@@ -312,10 +341,18 @@ def main():
                                 "sig_finalize": round(fin_ms / max(1, fin_n), 4),
                                 "inject": round(inj_ms / max(1, inj_n), 4) if inj_n else 0.0,
                                 "inject_sum": round(isum_ms / max(1, isum_n), 4) if isum_n else 0.0},
+        "step_ms": {"median": round(step_ms[len(step_ms) // 2], 4), "min": round(step_ms[0], 4),
+                    "max": round(step_ms[-1], 4)},
         "signature_only_GBps": round(nbytes / ((chunk_avg + fin_ms / max(1, fin_n)) / 1e3) / 1e9, 1),
         "inject_Gelem_per_s": round(sum(T.numel() for T, *_ in wl.items) / (inj_ms / max(1, inj_n) / 1e3) / 1e9, 1)
         if inj_n else None,
     }
+    if not args.no_read_ceiling:
+        log("read ceiling ...")
+        del prepared_items
+        rc = read_ceiling(torch, P, stream)
+        rc["sig_chunk_frac_of_ceiling"] = round(achieved / rc["GBps"], 4)
+        out["read_ceiling"] = rc
     if not args.no_cpu_baseline:
         log("cpu baseline ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)

@@ -193,6 +193,18 @@ int peat_inject_batched(const peat_inject_item_t *items, int32_t count, int64_t 
 int peat_inject_batched_async(const peat_inject_item_t *items, int32_t count,
                               int64_t *d_counts, void *stream);
 
+/* Measurement aid, not a step of the method: reads `bytes` bytes of device
+ * memory at `buf` (16-byte aligned, bytes a multiple of 16) with the access
+ * pattern of the signature chunk pass (16-byte nontemporal loads per lane,
+ * 256-thread blocks, a contiguous 2 MiB span per block) and writes the XOR of
+ * the 32-bit words of span k (bytes [k 2^21, (k+1) 2^21) of buf) to
+ * d_sink[k], so that no read can be dropped.  d_sink is a device array of at
+ * least ceil(bytes / 2^21) uint32 words, 4-byte aligned.  Enqueued on
+ * `stream` (NULL: the default stream); timed as kernel class 4.  Its byte
+ * rate is the read ceiling of this access pattern on the device.  Returns
+ * PEAT_EINVAL for bad sizes, alignment or NULL pointers. */
+int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream);
+
 /* Host-side derived scores of a signature (host memory in and out). */
 int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
 
@@ -201,7 +213,7 @@ int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
  * events, returns the summed duration (ms) and launch count of one kernel
  * class since the last read, and clears that class.  Kernel classes:
  * 0 signature chunk pass, 1 signature finalize, 2 injection, 3 injection
- * count reduction. */
+ * count reduction, 4 streaming read (peat_stream_read). */
 int peat_profile_enable(int on);
 int peat_profile_read(int kernel_class, double *total_ms, int64_t *launches);
 

@@ -21,7 +21,7 @@ OK, EINVAL, EDTYPE, EBITMASK, ERATE, EHIP, ENOMEM, ENODEV = 0, -1, -2, -3, -4, -
 MAX_THRESHOLDS, MAX_BINS = 8, 64
 
 # kernel classes of peat_profile_read
-K_SIG_CHUNK, K_SIG_FINALIZE, K_INJECT, K_INJECT_SUM = 0, 1, 2, 3
+K_SIG_CHUNK, K_SIG_FINALIZE, K_INJECT, K_INJECT_SUM, K_STREAM_READ = 0, 1, 2, 3, 4
 
 
 class PeatError(RuntimeError):
@@ -119,6 +119,7 @@ _PROTOS = {
                                            ctypes.POINTER(ctypes.c_int64)]),
     "peat_inject_batched_async": (ctypes.c_int, [ctypes.POINTER(InjectItem), ctypes.c_int32,
                                                  ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
     "peat_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "peat_profile_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
@@ -372,6 +373,22 @@ def finalize_stats(sig: dict) -> dict:
     st = Stats()
     _check(lib().peat_finalize_stats(ctypes.byref(s), ctypes.byref(st)), "peat_finalize_stats")
     return {k: float(getattr(st, k)) for k, _ in Stats._fields_}
+
+
+STREAM_SPAN = 1 << 21     # bytes per block of peat_stream_read
+
+
+def stream_read(buf, d_sink, stream=None) -> None:
+    """peat_stream_read over the bytes of the contiguous device tensor buf;
+    d_sink is a device int32/uint32 tensor of at least ceil(bytes / 2 MiB)
+    elements (one XOR checksum per 2 MiB span)."""
+    _dev_tensor(buf, "buf")
+    _dev_tensor(d_sink, "d_sink")
+    nbytes = buf.numel() * buf.element_size()
+    if d_sink.element_size() != 4 or d_sink.numel() < (nbytes + STREAM_SPAN - 1) // STREAM_SPAN:
+        raise ValueError("d_sink needs one 32-bit word per 2 MiB span")
+    _check(lib().peat_stream_read(buf.data_ptr(), nbytes, d_sink.data_ptr(), _stream_ptr(stream)),
+           "peat_stream_read")
 
 
 def profile_enable(on: bool = True) -> None:

@@ -467,6 +467,24 @@ int peat_inject_batched_async(const peat_inject_item_t *items, int32_t count, in
     return inject_core(items, count, d_counts, nullptr, static_cast<hipStream_t>(stream));
 }
 
+int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream) {
+    if (bytes < 0) return fail(PEAT_EINVAL, "bytes < 0");
+    if (bytes == 0) return PEAT_OK;
+    if (!buf || !d_sink) return fail(PEAT_EINVAL, "NULL pointer with bytes > 0");
+    if (bytes % 16 != 0 || reinterpret_cast<uintptr_t>(buf) % 16 != 0)
+        return fail(PEAT_EINVAL, "buf must be 16-byte aligned and bytes a multiple of 16");
+    if (reinterpret_cast<uintptr_t>(d_sink) % 4 != 0) return fail(PEAT_EINVAL, "d_sink must be 4-byte aligned");
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *d;
+    int rc = current_dev(&d);
+    if (rc) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipEvent_t ev;
+    if ((rc = prof_begin(*d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_stream_read(buf, bytes, d_sink, s));
+    return prof_end(*d, s, 4, ev);
+}
+
 int peat_finalize_stats(const peat_signature_t *sg, peat_stats_t *st) {
     if (!sg || !st) return fail(PEAT_EINVAL, "NULL argument");
     const double nf = (double)sg->n_finite;

@@ -99,5 +99,6 @@ hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[4], hipStre
 hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
 hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
 hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);
+hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
 
 }  // namespace peat

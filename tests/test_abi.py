@@ -113,6 +113,16 @@ def test_inject_validation_codes():
     assert L.peat_inject_batched(items, 1, counts) == B.EINVAL
 
 
+def test_stream_read_validation_codes():
+    L = P.lib()
+    assert L.peat_stream_read(None, 0, None, None) == B.OK          # nothing to read
+    assert L.peat_stream_read(None, -16, None, None) == B.EINVAL
+    assert L.peat_stream_read(None, 16, None, None) == B.EINVAL     # NULL buffer
+    assert L.peat_stream_read(16, 15, 64, None) == B.EINVAL         # size not a multiple of 16
+    assert L.peat_stream_read(8, 16, 64, None) == B.EINVAL          # misaligned buffer
+    assert L.peat_stream_read(16, 16, 2, None) == B.EINVAL          # misaligned sink
+
+
 def test_finalize_stats_host():
     s = B.Signature()
     s.n_finite = 4
