@@ -17,6 +17,8 @@ Validation in DNN Training"):
     torch.isclose(rtol, atol) -> absolute-threshold mismatch counts.
   * Section V-D, Fig. "tiny_error_gemm_resnet34": error value histograms.
   * Section II-B "Error Models": random bit flip at a bit error rate.
+  * Section IV-B.3 "Mean of Top 10% Errors" (the Analyzer's main score,
+    Section IV-C): mean of the k largest errors, k = ceil(n_valid num/den).
   * Algorithms 1 and 2: Inject() followed by Err(golden set, FI set).
 """
 from __future__ import annotations
@@ -35,7 +37,7 @@ LIB_PATH = os.path.join(_HERE, "liboracle.so")
 F32, F16, BF16 = 0, 1, 2
 _DTYPE_CODE = {np.dtype(np.float32): F32, np.dtype(np.float16): F16}
 
-OK, EINVAL, EDTYPE, EBITMASK, ERATE = 0, -1, -2, -3, -4
+OK, EINVAL, EDTYPE, EBITMASK, ERATE, ENOMEM = 0, -1, -2, -3, -4, -6
 
 
 class _Sig(ctypes.Structure):
@@ -57,6 +59,12 @@ class _Sig(ctypes.Structure):
         ("sum_rel", ctypes.c_double), ("sum_g2", ctypes.c_double),
         ("sum_t2", ctypes.c_double), ("sum_gt", ctypes.c_double),
     ]
+
+
+class _TopK(ctypes.Structure):
+    _fields_ = [("n_valid", ctypes.c_int64), ("k", ctypes.c_int64), ("count_above", ctypes.c_int64),
+                ("kth_value", ctypes.c_double), ("sum_topk", ctypes.c_double),
+                ("mean_topk", ctypes.c_double)]
 
 
 class _Stats(ctypes.Structure):
@@ -111,8 +119,13 @@ def lib():
             L.oracle_inject.argtypes = [
                 ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
                 ctypes.c_double, ctypes.c_uint64]
+            L.oracle_topk.restype = ctypes.c_int
+            L.oracle_topk.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                      ctypes.c_int, ctypes.c_int, ctypes.POINTER(_TopK)]
             L.oracle_sizeof_sig.restype = ctypes.c_int
             assert L.oracle_sizeof_sig() == ctypes.sizeof(_Sig)
+            L.oracle_sizeof_topk.restype = ctypes.c_int
+            assert L.oracle_sizeof_topk() == ctypes.sizeof(_TopK)
             _lib = L
     return _lib
 
@@ -235,3 +248,29 @@ def inject_rc(n, code, seed, rate, mask) -> int:
     """Return code of oracle_inject on a scratch buffer (validation tests)."""
     buf = np.zeros(max(int(n), 1) * 4, dtype=np.uint8)
     return int(lib().oracle_inject(buf.ctypes.data, int(n), code, seed, float(rate), mask))
+
+
+def topk(golden: np.ndarray, test: np.ndarray, *, dtype: int | None = None, num: int = 1,
+         den: int = 10) -> dict:
+    """Mean of the k largest errors over the valid pairs, k = ceil(n_valid num/den):
+    dict with n_valid, k, count_above, kth_value, sum_topk, mean_topk."""
+    g = np.ascontiguousarray(golden).reshape(-1)
+    t = np.ascontiguousarray(test).reshape(-1)
+    if g.shape != t.shape or g.dtype != t.dtype:
+        raise ValueError("golden and test must have the same shape and dtype")
+    code = _code(g, dtype)
+    out = _TopK()
+    rc = lib().oracle_topk(g.ctypes.data if g.size else None, t.ctypes.data if t.size else None,
+                           g.size, code, int(num), int(den), ctypes.byref(out))
+    if rc != OK:
+        raise ValueError(f"oracle_topk failed: {rc}")
+    return {name: (float(getattr(out, name)) if typ is ctypes.c_double else int(getattr(out, name)))
+            for name, typ in _TopK._fields_}
+
+
+def topk_rc(n, code, num, den) -> int:
+    """Return code of oracle_topk on zero-filled buffers (validation tests)."""
+    buf = np.zeros(max(int(n), 1) * 4, dtype=np.uint8)
+    out = _TopK()
+    return int(lib().oracle_topk(buf.ctypes.data, buf.ctypes.data, int(n), code, int(num), int(den),
+                                 ctypes.byref(out)))

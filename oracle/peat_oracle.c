@@ -20,6 +20,12 @@
  *                     by Inject() in Playback FI (Algorithm 1) and Runtime FI
  *                     (Algorithm 2).
  *
+ *   oracle_topk       the "mean of the top 10% errors" score (Section IV-B,
+ *                     FI Assessment Scores; the Analyzer's main score,
+ *                     Section IV-C), for any fraction num/den: the errors of
+ *                     the valid pairs sorted in decreasing order, the k largest
+ *                     summed, k = ceil(n_valid * num / den).
+ *
  * Only the tests, the package smoke check and the benchmark's CPU-baseline leg
  * may load this file's library.  It shares no code, header, table or constant
  * generator with the GPU library; the two are independent by construction.
@@ -34,6 +40,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define ORACLE_F32 0
@@ -45,6 +52,7 @@
 #define ORACLE_EDTYPE (-2)
 #define ORACLE_EBITMASK (-3)
 #define ORACLE_ERATE (-4)
+#define ORACLE_ENOMEM (-6)
 
 typedef struct {
     int64_t n, n_valid, n_finite, n_rel;
@@ -430,3 +438,66 @@ int64_t oracle_inject(void *x, int64_t n, int dtype, uint64_t seed, double rate,
 }
 
 int oracle_sizeof_sig(void) { return (int)sizeof(oracle_sig_t); }
+
+/* ------------------------------------------------------------------------ */
+/* Mean of the top errors (Section IV-B, "Mean of Top 10% Errors").         */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t n_valid;      /* pairs with no NaN on either side */
+    int64_t k;            /* ceil(n_valid * num / den) */
+    int64_t count_above;  /* errors strictly greater than kth_value */
+    double kth_value;     /* the k-th largest error (NaN when k == 0) */
+    double sum_topk;      /* sum of the k largest errors (0 when k == 0) */
+    double mean_topk;     /* sum_topk / k (NaN when k == 0) */
+} oracle_topk_t;
+
+static int cmp_desc(const void *x, const void *y) {
+    double a = *(const double *)x, b = *(const double *)y;
+    return (a < b) - (a > b);
+}
+
+int oracle_topk(const void *golden, const void *test, int64_t n, int dtype, int num, int den,
+                oracle_topk_t *out) {
+    if (!dtype_width(dtype)) return ORACLE_EDTYPE;
+    if (!out || n < 0 || (n > 0 && (!golden || !test))) return ORACLE_EINVAL;
+    if (num < 1 || den < num) return ORACLE_EINVAL;
+
+    /* The error of every valid pair, defined as in oracle_signature. */
+    double *a = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    if (!a) return ORACLE_ENOMEM;
+    int64_t m = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        double G = element_value(element_bits(golden, i, dtype), dtype);
+        double T = element_value(element_bits(test, i, dtype), dtype);
+        if (isnan(G) || isnan(T)) continue;
+        a[m++] = (G == T) ? 0.0 : fabs(T - G);
+    }
+    /* Decreasing order; the k largest are a[0..k). */
+    qsort(a, (size_t)m, sizeof(double), cmp_desc);
+
+    oracle_topk_t r;
+    r.n_valid = m;
+    r.k = (int64_t)(((unsigned __int128)m * (unsigned)num + (unsigned)den - 1) / (unsigned)den);
+    r.count_above = 0;
+    r.kth_value = NAN;
+    r.sum_topk = 0.0;
+    r.mean_topk = NAN;
+    if (r.k > 0) {
+        r.kth_value = a[r.k - 1];
+        while (r.count_above < r.k && a[r.count_above] > r.kth_value) r.count_above += 1;
+        if (isinf(a[0])) {
+            r.sum_topk = INFINITY;  /* an infinite error among the k largest */
+        } else {
+            csum_t acc = {0, 0};
+            for (int64_t i = 0; i < r.k; ++i) csum_add(&acc, a[i]);
+            r.sum_topk = csum_value(&acc);
+        }
+        r.mean_topk = r.sum_topk / (double)r.k;
+    }
+    free(a);
+    *out = r;
+    return ORACLE_OK;
+}
+
+int oracle_sizeof_topk(void) { return (int)sizeof(oracle_topk_t); }
