@@ -208,6 +208,27 @@ def cpu_baseline(wl: Workload, max_threads: int):
                       f"D2H copy {copy_s:.1f} s not counted"}
 
 
+def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
+    """The paper's main score, the mean of the top 10% errors, over every pair
+    of the workload (peat_topk_mean_batched: three streaming passes plus the
+    candidate rounds); best of reps, from the library's kernel events."""
+    P.topk_mean_batched(prep_pairs, 1, 10)                       # warm-up
+    P.profile_enable(True)
+    P.profile_read(P.K_TOPK_A)
+    P.profile_read(P.K_TOPK_B)
+    best = None
+    for _ in range(reps):
+        recs = P.topk_mean_batched(prep_pairs, 1, 10)
+        a, na = P.profile_read(P.K_TOPK_A)
+        b, nb = P.profile_read(P.K_TOPK_B)
+        ms = a / max(1, na) + b / max(1, nb)
+        best = ms if best is None else min(best, ms)
+    P.profile_enable(False)
+    return {"ms": round(best, 3), "GBps_of_bytes_signed": round(nbytes / (best / 1e3) / 1e9, 1),
+            "passes": 3, "pairs": len(recs), "k_total": int(sum(r["k"] for r in recs)),
+            "what": "peat_topk_mean_batched, num/den = 1/10, kernel time (excludes the host wait between passes 2 and 3)"}
+
+
 def read_ceiling(torch, P, stream, gib: int = 16, reps: int = 5):
     """GB/s of peat_stream_read over a gib-GiB buffer (best of reps)."""
     buf = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
@@ -252,6 +273,7 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="GIB")
     ap.add_argument("--no-read-ceiling", action="store_true")
+    ap.add_argument("--no-topk", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -347,6 +369,9 @@ def main():
         "inject_Gelem_per_s": round(sum(T.numel() for T, *_ in wl.items) / (inj_ms / max(1, inj_n) / 1e3) / 1e9, 1)
         if inj_n else None,
     }
+    if not args.no_topk:
+        log("top-10% mean ...")
+        out["topk_mean"] = topk_measure(torch, P, prep_pairs, nbytes)
     if not args.no_read_ceiling:
         log("read ceiling ...")
         del prepared_items

@@ -117,6 +117,20 @@ typedef struct {
     double mean_abs, var_abs, l2_err, l2_g, l2_t, cos, mean_rel, mean_ulp;
 } peat_stats_t;
 
+/* Mean of the top errors of one pair (Section IV-B.3, "Mean of Top 10%
+ * Errors", the Analyzer's main score in Section IV-C): the k largest errors
+ * a_i = |T_i - G_i| (the signature's error) over the valid pairs, with
+ * k = ceil(n_valid * num / den). */
+typedef struct {
+    int64_t n_valid;      /* pairs with no NaN on either side */
+    int64_t k;            /* ceil(n_valid * num / den) */
+    int64_t count_above;  /* errors strictly greater than kth_value (< k) */
+    double kth_value;     /* the k-th largest error; NaN when k = 0 */
+    double sum_topk;      /* sum of the k largest errors; 0 when k = 0; +Inf
+                           * when one of them is infinite */
+    double mean_topk;     /* sum_topk / k; NaN when k = 0 */
+} peat_topk_t;
+
 typedef struct {
     const void *golden; /* device pointer */
     const void *test;   /* device pointer */
@@ -172,6 +186,21 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
                                  const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                                  peat_signature_t *d_outs, void *stream);
 
+/* Mean of the k largest errors of one pair, k = ceil(n_valid * num / den)
+ * (num = 1, den = 10: the paper's top-10% mean); out is host memory.
+ * 1 <= num <= den <= 2^20.  Exact selection: n_valid, k, count_above and
+ * kth_value are exact; sum_topk is a binary64 sum in a fixed order (within
+ * 1e-12 relative of the exact sum), bit-identical between calls.  Three
+ * streaming passes over golden and test plus work on the few errors that
+ * share the k-th largest's leading bits; the call waits for its result. */
+int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
+                   int32_t num, int32_t den, peat_topk_t *out);
+
+/* peat_topk_mean over count >= 0 pairs in one launch sequence; outs is a
+ * host array of count records, each bit-identical to the single call's. */
+int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                           peat_topk_t *outs);
+
 /* Random bit flip in place (Section II-B).  Element i flips iff its 64-bit
  * uniform U_i < floor(rate * 2^64) (every element if rate >= 1).  U_i's top
  * byte is byte (i mod 32), little-endian, of Philox4x64-10 with key
@@ -213,7 +242,8 @@ int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
  * events, returns the summed duration (ms) and launch count of one kernel
  * class since the last read, and clears that class.  Kernel classes:
  * 0 signature chunk pass, 1 signature finalize, 2 injection, 3 injection
- * count reduction, 4 streaming read (peat_stream_read). */
+ * count reduction, 4 streaming read (peat_stream_read), 5 top-k passes 1-2
+ * with their selections, 6 top-k pass 3, candidate rounds and finalize. */
 int peat_profile_enable(int on);
 int peat_profile_read(int kernel_class, double *total_ms, int64_t *launches);
 

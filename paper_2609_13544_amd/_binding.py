@@ -21,7 +21,7 @@ OK, EINVAL, EDTYPE, EBITMASK, ERATE, EHIP, ENOMEM, ENODEV = 0, -1, -2, -3, -4, -
 MAX_THRESHOLDS, MAX_BINS = 8, 64
 
 # kernel classes of peat_profile_read
-K_SIG_CHUNK, K_SIG_FINALIZE, K_INJECT, K_INJECT_SUM, K_STREAM_READ = 0, 1, 2, 3, 4
+K_SIG_CHUNK, K_SIG_FINALIZE, K_INJECT, K_INJECT_SUM, K_STREAM_READ, K_TOPK_A, K_TOPK_B = 0, 1, 2, 3, 4, 5, 6
 
 
 class PeatError(RuntimeError):
@@ -63,6 +63,11 @@ class Signature(ctypes.Structure):
 class Stats(ctypes.Structure):
     _fields_ = [(k, ctypes.c_double) for k in
                 ("mean_abs", "var_abs", "l2_err", "l2_g", "l2_t", "cos", "mean_rel", "mean_ulp")]
+
+
+class TopK(ctypes.Structure):
+    _fields_ = [("n_valid", ctypes.c_int64), ("k", ctypes.c_int64), ("count_above", ctypes.c_int64),
+                ("kth_value", ctypes.c_double), ("sum_topk", ctypes.c_double), ("mean_topk", ctypes.c_double)]
 
 
 class Pair(ctypes.Structure):
@@ -119,6 +124,10 @@ _PROTOS = {
                                            ctypes.POINTER(ctypes.c_int64)]),
     "peat_inject_batched_async": (ctypes.c_int, [ctypes.POINTER(InjectItem), ctypes.c_int32,
                                                  ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_topk_mean": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                      ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(TopK)]),
+    "peat_topk_mean_batched": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.c_int32, ctypes.POINTER(TopK)]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
     "peat_profile_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -284,6 +293,42 @@ def signature_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> lis
     _check(lib().peat_signature_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
            "peat_signature_batched")
     return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+
+
+def topk_to_dict(t: TopK) -> dict:
+    return {name: (float(getattr(t, name)) if typ is ctypes.c_double else int(getattr(t, name)))
+            for name, typ in TopK._fields_}
+
+
+def topk_mean(golden, test, num: int = 1, den: int = 10, *, dtype: int | None = None,
+              n: int | None = None) -> dict:
+    """peat_topk_mean: mean of the ceil(n_valid num/den) largest errors of
+    two device tensors (default: the top 10%)."""
+    _dev_tensor(golden, "golden")
+    _dev_tensor(test, "test")
+    code = dtype_code(golden) if dtype is None else dtype
+    if n is None:
+        if golden.numel() != test.numel() or golden.dtype != test.dtype:
+            raise ValueError("golden and test differ in size or dtype")
+        n = golden.numel()
+    out = TopK()
+    set_stream()
+    _check(lib().peat_topk_mean(golden.data_ptr() if n else None, test.data_ptr() if n else None, n, code,
+                                num, den, ctypes.byref(out)), "peat_topk_mean")
+    return topk_to_dict(out)
+
+
+def topk_mean_batched(pairs, num: int = 1, den: int = 10) -> list[dict]:
+    """peat_topk_mean_batched over a list of (golden, test) device tensor pairs
+    (or a PreparedPairs)."""
+    if isinstance(pairs, PreparedPairs):
+        arr, count = pairs.arr, pairs.count
+    else:
+        arr, count = _pairs_array(pairs), len(pairs)
+    outs = (TopK * max(1, count))()
+    set_stream()
+    _check(lib().peat_topk_mean_batched(arr, count, num, den, outs), "peat_topk_mean_batched")
+    return [topk_to_dict(outs[k]) for k in range(count)]
 
 
 class PreparedPairs:

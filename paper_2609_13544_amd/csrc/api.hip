@@ -64,6 +64,8 @@ struct Dev {
     size_t ws_size = 0;
     hipEvent_t ws_ev = nullptr;
     bool ws_pending = false;
+    void *ws2 = nullptr;             // top-k candidate keys (sized after pass 2)
+    size_t ws2_size = 0;
     Slot slot[kSlots];
     int next_slot = 0;
     bool prof = false;
@@ -109,6 +111,22 @@ int acquire_ws(Dev &d, size_t bytes, hipStream_t s, char **ws) {
     }
     if (d.ws_pending) HIP_OR_FAIL(hipStreamWaitEvent(s, d.ws_ev, 0));
     *ws = static_cast<char *>(d.ws);
+    return PEAT_OK;
+}
+
+// Second workspace, used only inside a call that has synchronised its
+// stream: growing it after a device-wide synchronisation is safe.
+int acquire_ws2(Dev &d, size_t bytes, char **ws) {
+    if (bytes > d.ws2_size) {
+        HIP_OR_FAIL(hipDeviceSynchronize());
+        if (d.ws2) HIP_OR_FAIL(hipFree(d.ws2));
+        d.ws2 = nullptr;
+        d.ws2_size = 0;
+        size_t want = align_up(bytes + bytes / 4 + (size_t(1) << 20));
+        HIP_OR_FAIL(hipMalloc(&d.ws2, want));
+        d.ws2_size = want;
+    }
+    *ws = static_cast<char *>(d.ws2);
     return PEAT_OK;
 }
 
@@ -203,30 +221,13 @@ int check_pair(const peat_pair_t &p, int k) {
     return PEAT_OK;
 }
 
-// Common core of every signature call.  When host_outs is set the records go
-// through workspace + pinned staging and the call waits for them.
-int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
-                   const peat_thresholds_t *thr, peat_signature_t *d_outs,
-                   peat_signature_t *host_outs, hipStream_t s) {
-    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
-    if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
-    int rc = check_bins_thr(bins, thr);
-    if (rc) return rc;
-    for (int k = 0; k < count; ++k)
-        if ((rc = check_pair(pairs[k], k))) return rc;
-    if (count == 0) return PEAT_OK;
-    if (!host_outs && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
-
-    std::lock_guard<std::mutex> lock(g_mu);
-    Dev *dv;
-    if ((rc = current_dev(&dv))) return rc;
-    Dev &d = *dv;
-
-    // partition every pair into chunks; the chunks of each element type get
-    // one contiguous range of the global numbering (one launch per type)
-    std::vector<SigDesc> descs((size_t)count);
+// Partition every pair into chunks; the chunks of each element type get one
+// contiguous range [range[dt], range[dt + 1]) of the global numbering (one
+// launch per type).
+int build_descs(const peat_pair_t *pairs, int32_t count, std::vector<SigDesc> &descs, int64_t range[4],
+                int64_t *total_out) {
+    descs.assign((size_t)count, SigDesc{});
     int64_t total = 0;
-    int64_t range[4] = {0, 0, 0, 0};
     for (int dt = 0; dt < 3; ++dt) {
         range[dt] = total;
         for (int k = 0; k < count; ++k) {
@@ -246,6 +247,33 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
     }
     range[3] = total;
     if (total > 0x7FFFFFFF) return fail(PEAT_EINVAL, "batch needs %lld chunks (max 2^31-1)", (long long)total);
+    *total_out = total;
+    return PEAT_OK;
+}
+
+// Common core of every signature call.  When host_outs is set the records go
+// through workspace + pinned staging and the call waits for them.
+int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                   const peat_thresholds_t *thr, peat_signature_t *d_outs,
+                   peat_signature_t *host_outs, hipStream_t s) {
+    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
+    if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
+    int rc = check_bins_thr(bins, thr);
+    if (rc) return rc;
+    for (int k = 0; k < count; ++k)
+        if ((rc = check_pair(pairs[k], k))) return rc;
+    if (count == 0) return PEAT_OK;
+    if (!host_outs && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    if ((rc = current_dev(&dv))) return rc;
+    Dev &d = *dv;
+
+    std::vector<SigDesc> descs;
+    int64_t total = 0;
+    int64_t range[4];
+    if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
 
     const size_t b_desc = align_up(sizeof(SigDesc) * count);
     const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
@@ -395,6 +423,134 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
     return PEAT_OK;
 }
 
+// Mean of the k largest errors: three streaming passes and the candidate
+// rounds (see topk.hip).  The call waits twice: once after pass 2 to size the
+// candidate buffers, once for the records.
+int topk_core(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den, peat_topk_t *outs,
+              hipStream_t s) {
+    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
+    if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
+    if (num < 1 || den < num || den > (1 << 20))
+        return fail(PEAT_EINVAL, "need 1 <= num <= den <= 2^20 (got %d/%d)", num, den);
+    int rc;
+    for (int k = 0; k < count; ++k)
+        if ((rc = check_pair(pairs[k], k))) return rc;
+    if (count == 0) return PEAT_OK;
+    if (!outs) return fail(PEAT_EINVAL, "outs is NULL");
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    if ((rc = current_dev(&dv))) return rc;
+    Dev &d = *dv;
+
+    std::vector<SigDesc> descs;
+    int64_t total = 0;
+    int64_t range[4];
+    if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
+
+    const size_t b_desc = align_up(sizeof(SigDesc) * count);
+    const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
+    const size_t b_state = align_up(sizeof(TopkState) * count);
+    const size_t b_cand = align_up(sizeof(TopkCand) * count);
+    const size_t b_hist = align_up(sizeof(uint64_t) * kTopkBins * (size_t)count);
+    const size_t b_part = align_up(sizeof(double) * (size_t)total);
+    const size_t b_out = align_up(sizeof(peat_topk_t) * count);
+    const size_t o_map = b_desc, o_state = o_map + b_map, o_cand = o_state + b_state;
+    const size_t o_hist = o_cand + b_cand, o_pa = o_hist + b_hist, o_pb = o_pa + b_part, o_out = o_pb + b_part;
+
+    char *ws;
+    if ((rc = acquire_ws(d, o_out + b_out, s, &ws))) return rc;
+    Slot *sl;
+    if ((rc = acquire_slot(d, b_desc + b_map + b_state + b_out, &sl))) return rc;
+    char *h = static_cast<char *>(sl->host);
+    std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
+    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc);
+    for (int k = 0; k < count; ++k)
+        for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
+    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+
+    TopkParams P{};
+    P.chunk_base = 0;
+    P.descs = reinterpret_cast<const SigDesc *>(ws);
+    P.chunk_pair = reinterpret_cast<const int32_t *>(ws + o_map);
+    P.state = reinterpret_cast<TopkState *>(ws + o_state);
+    P.cand = reinterpret_cast<const TopkCand *>(ws + o_cand);
+    P.hist = reinterpret_cast<uint64_t *>(ws + o_hist);
+    P.part_a = reinterpret_cast<double *>(ws + o_pa);
+    P.part_b = reinterpret_cast<double *>(ws + o_pb);
+    P.outs = reinterpret_cast<peat_topk_t *>(ws + o_out);
+    P.count = count;
+    P.num = num;
+    P.den = den;
+    const int64_t nhist = (int64_t)kTopkBins * count;
+
+    // passes 1 and 2 with their selections
+    hipEvent_t ev;
+    if ((rc = prof_begin(d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
+    HIP_OR_FAIL(launch_topk_pass(P, 0, range, s));
+    HIP_OR_FAIL(launch_topk_select(P, 0, s));
+    HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
+    HIP_OR_FAIL(launch_topk_pass(P, 1, range, s));
+    HIP_OR_FAIL(launch_topk_select(P, 1, s));
+    if ((rc = prof_end(d, s, 5, ev))) return rc;
+
+    // size the candidate buffers: the level-1 boundary bin of each pair
+    TopkState *hst = reinterpret_cast<TopkState *>(h + b_desc + b_map);
+    HIP_OR_FAIL(hipMemcpyAsync(hst, P.state, sizeof(TopkState) * count, hipMemcpyDeviceToHost, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    std::vector<TopkCand> cands((size_t)count);
+    std::vector<int32_t> cblk;
+    uint64_t ncand = 0;
+    for (int k = 0; k < count; ++k) {
+        const bool rounds = hst[k].level == 1 && hst[k].status == kTopkActive;
+        const uint64_t c = rounds ? hst[k].cand : 0;
+        cands[k].off = ncand;
+        cands[k].first_blk = (int32_t)cblk.size();
+        cands[k].nblk = (int32_t)((c + kTopkCandBlock - 1) / kTopkCandBlock);
+        for (int32_t b = 0; b < cands[k].nblk; ++b) cblk.push_back(k);
+        ncand += c;
+    }
+    if (cblk.size() > 0x7FFFFFFF) return fail(PEAT_EINVAL, "too many top-k candidates");
+    P.ncblk = (int64_t)cblk.size();
+    // (key, count) entries: at most one per error of the level-1 bin
+    const size_t b_keys = align_up(2 * sizeof(uint64_t) * (ncand > 0 ? ncand : 1));
+    const size_t b_cblk = align_up(sizeof(int32_t) * (cblk.empty() ? 1 : cblk.size()));
+    const size_t b_x = align_up(sizeof(uint64_t) * 2 * (kTopkLevels - 2) * (cblk.empty() ? 1 : cblk.size()));
+    char *w2;
+    if ((rc = acquire_ws2(d, 2 * b_keys + b_cblk + b_x, &w2))) return rc;
+    P.keys[0] = reinterpret_cast<uint64_t *>(w2);
+    P.keys[1] = reinterpret_cast<uint64_t *>(w2 + b_keys);
+    P.cblk_pair = reinterpret_cast<const int32_t *>(w2 + 2 * b_keys);
+    P.xpart = reinterpret_cast<uint64_t *>(w2 + 2 * b_keys + b_cblk);
+    // the stream is idle here, so plain synchronous copies are ordered
+    HIP_OR_FAIL(hipMemcpy(ws + o_cand, cands.data(), sizeof(TopkCand) * count, hipMemcpyHostToDevice));
+    if (!cblk.empty())
+        HIP_OR_FAIL(hipMemcpy(w2 + 2 * b_keys, cblk.data(), sizeof(int32_t) * cblk.size(), hipMemcpyHostToDevice));
+
+    // pass 3, the candidate rounds and the records
+    if ((rc = prof_begin(d, s, &ev))) return rc;
+    HIP_OR_FAIL(launch_topk_pass(P, 2, range, s));
+    if (P.ncblk > 0) {
+        for (int L = 2; L < kTopkLevels; ++L) {
+            HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
+            HIP_OR_FAIL(launch_topk_cand_hist(P, L, s));
+            HIP_OR_FAIL(launch_topk_select(P, L, s));
+            HIP_OR_FAIL(launch_topk_cand_sum(P, L, s));
+        }
+    }
+    HIP_OR_FAIL(launch_topk_finalize(P, s));
+    if ((rc = prof_end(d, s, 6, ev))) return rc;
+
+    char *hout = h + b_desc + b_map + b_state;
+    HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_topk_t) * count, hipMemcpyDeviceToHost, s));
+    if ((rc = release_slot(*sl, s))) return rc;
+    if ((rc = release_ws(d, s))) return rc;
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    std::memcpy(outs, hout, sizeof(peat_topk_t) * count);
+    return PEAT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -465,6 +621,18 @@ int peat_inject_batched(const peat_inject_item_t *items, int32_t count, int64_t 
 int peat_inject_batched_async(const peat_inject_item_t *items, int32_t count, int64_t *d_counts,
                               void *stream) {
     return inject_core(items, count, d_counts, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t dtype, int32_t num,
+                   int32_t den, peat_topk_t *out) {
+    if (!out) return fail(PEAT_EINVAL, "out is NULL");
+    peat_pair_t p{golden, test, n, (int32_t)dtype, 0};
+    return topk_core(&p, 1, num, den, out, t_stream);
+}
+
+int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                           peat_topk_t *outs) {
+    return topk_core(pairs, count, num, den, outs, t_stream);
 }
 
 int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream) {

@@ -92,6 +92,57 @@ struct InjParams {
     int32_t count;
 };
 
+// ---- top-k error mean --------------------------------------------------------
+// Radix selection on the binary64 bit pattern of the error (monotone for
+// a >= 0): digit 0 = bits 62..52 (the binade, 2048 bins), digits 1-4 = 13
+// mantissa bits each (8192 bins).  Levels 0 and 1 are histograms over the
+// tensors (passes 1 and 2); pass 3 sums the errors above the level-1 bin and
+// gathers the errors inside it as (key, count) entries; levels 2-4 run on
+// those entries.
+constexpr int kTopkLevels = 5;
+constexpr int kTopkBins = 8192;                  // bins of digits 1-4
+constexpr int kTopkCandBlock = 16384;            // (key, count) entries per block
+enum { kTopkActive = 0, kTopkDone = 1 };
+
+struct TopkState {               // one per pair (80 bytes), device memory
+    uint64_t n_valid;
+    uint64_t k;
+    uint64_t need;               // k minus the errors above the boundary bin
+    uint64_t cand;               // errors in the boundary bin
+    uint64_t key;                // bits of the boundary fixed so far
+    uint64_t cnt[2];             // entries in keys[0] / keys[1]
+    int32_t level;               // last resolved level, -1 before level 0
+    int32_t status;              // kTopkActive or kTopkDone
+    int32_t d0;                  // level-0 boundary (the binade field)
+    int32_t reserved[3];
+};
+static_assert(sizeof(TopkState) == 80, "TopkState layout");
+
+struct TopkCand {                // one per pair, written by the host after pass 2
+    uint64_t off;                // first entry slot of the pair
+    int32_t first_blk;           // first candidate block
+    int32_t nblk;                // candidate blocks (0: no candidate rounds)
+};
+
+struct TopkParams {
+    int64_t chunk_base;          // first global chunk of this launch
+    const SigDesc *descs;
+    const int32_t *chunk_pair;
+    TopkState *state;
+    const TopkCand *cand;
+    uint64_t *hist;              // count x kTopkBins counters
+    double *part_a;              // pass 2: per chunk, sum of errors above the level-0 bin
+    double *part_b;              // pass 3: per chunk, sum above the level-1 bin inside it
+    uint64_t *keys[2];           // (key, count) entry buffers, 2 words per entry
+    const int32_t *cblk_pair;    // candidate block -> pair
+    uint64_t *xpart;             // per (round, candidate block): exact sums, 2 words
+    peat_topk_t *outs;           // one per pair (device)
+    int64_t ncblk;               // candidate blocks
+    int32_t count;               // pairs
+    int32_t num, den;
+    int32_t level;               // level of a histogram / selection launch
+};
+
 // Kernel launchers (defined in the .hip translation units).
 // One launch per element type present: chunks of each type form one
 // contiguous range [range[dt], range[dt + 1]) of the global chunk numbering.
@@ -100,5 +151,11 @@ hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
 hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
 hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
+hipError_t launch_topk_zero(uint64_t *p, int64_t n, hipStream_t s);
+hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[4], hipStream_t s);
+hipError_t launch_topk_select(const TopkParams &p, int level, hipStream_t s);
+hipError_t launch_topk_cand_hist(const TopkParams &p, int level, hipStream_t s);
+hipError_t launch_topk_cand_sum(const TopkParams &p, int level, hipStream_t s);
+hipError_t launch_topk_finalize(const TopkParams &p, hipStream_t s);
 
 }  // namespace peat

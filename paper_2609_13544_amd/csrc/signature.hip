@@ -33,7 +33,7 @@
 // Determinism: the element -> lane mapping, per-lane order and reduction
 // trees depend only on the chunk size, which depends only on n, so single,
 // batched and any-grid-size launches give bit-identical records.
-#include "peat_internal.h"
+#include "elements.h"
 
 namespace peat {
 namespace {
@@ -53,52 +53,8 @@ constexpr int kHistCols = kBlock / 2;     // histogram words per slot
 __device__ __forceinline__ uint32_t hist_col(int tid) { return (uint32_t)tid & (kHistCols - 1); }
 __device__ __forceinline__ uint32_t hist_inc(int tid) { return tid < kHistCols ? 1u : 0x10000u; }
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte vector
-typedef __attribute__((address_space(1))) const u32x4 gvec_t;
-// Word 3 of a raw (unstrided, untyped) buffer resource on gfx9-family parts:
-// 32-bit data format, default swizzle and cache policy.
-constexpr int kBufFlags = 0x00020000;
-// Cache-policy operand of the streaming loads: the nontemporal bit.  Each
-// byte is read once, and on MI355X the hint raises the read rate of this
-// access pattern from about 6.35 to 7.15 TB/s.
-constexpr int kLoadNT = 2;
-typedef __attribute__((address_space(1))) const uint32_t gu32_t;
-typedef __attribute__((address_space(1))) const uint16_t gu16_t;
-
-template <int DT> struct Tr;
-template <> struct Tr<PEAT_F32>  { static constexpr int VEC = 4, W = 32, U = 4; };
-template <> struct Tr<PEAT_F16>  { static constexpr int VEC = 8, W = 16, U = 2; };
-template <> struct Tr<PEAT_BF16> { static constexpr int VEC = 8, W = 16, U = 2; };
-
-template <int DT>
-__device__ __forceinline__ double widen(uint32_t b) {
-    if constexpr (DT == PEAT_F32) {
-        return (double)__uint_as_float(b);
-    } else if constexpr (DT == PEAT_BF16) {
-        return (double)__uint_as_float(b << 16);
-    } else {
-        return (double)(float)__builtin_bit_cast(_Float16, (uint16_t)b);
-    }
-}
-
-template <int DT>
-__device__ __forceinline__ uint32_t lane_elem(const u32x4 &v, int j) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    if constexpr (Tr<DT>::W == 32) {
-        return w[j];
-    } else {
-        return (w[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-    }
-}
-
-template <int DT>
-__device__ __forceinline__ uint32_t load_elem(const char *base, int64_t i) {
-    if constexpr (Tr<DT>::W == 32) {
-        return ((gu32_t *)base)[i];
-    } else {
-        return ((gu16_t *)base)[i];
-    }
-}
+// super-step unroll: 16-byte vectors per tensor per lane
+template <int DT> constexpr int kUnroll = (DT == PEAT_F32) ? 4 : 2;
 
 // ULP distance of two bit patterns of width W (signed-magnitude keys).
 template <int W>
@@ -456,7 +412,7 @@ __device__ __forceinline__ void lex_merge(V &v, uint32_t &ix, V ov, uint32_t oi)
 template <int DT, int NT>
 __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int64_t cin, int64_t gchunk) {
     constexpr int VEC = Tr<DT>::VEC;
-    constexpr int U = Tr<DT>::U;
+    constexpr int U = kUnroll<DT>;
     constexpr int SUPER = kBlock * VEC * U;     // elements per block super-step (4096)
     constexpr int ESZ = Tr<DT>::W / 8;
     const int tid = threadIdx.x;

@@ -47,6 +47,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(B.Thresholds) == 72
     assert B.Signature.max_abs.offset == 8 * (10 + 8 + 3 + 64)
     assert B.Signature.sum_gt.offset == 784 - 8
+    assert ctypes.sizeof(B.TopK) == 48
 
 
 def test_abi_version_and_strerror():
@@ -121,6 +122,22 @@ def test_stream_read_validation_codes():
     assert L.peat_stream_read(16, 15, 64, None) == B.EINVAL         # size not a multiple of 16
     assert L.peat_stream_read(8, 16, 64, None) == B.EINVAL          # misaligned buffer
     assert L.peat_stream_read(16, 16, 2, None) == B.EINVAL          # misaligned sink
+
+
+def test_topk_validation_codes():
+    L = P.lib()
+    out = B.TopK()
+    outs = (B.TopK * 1)()
+    assert L.peat_topk_mean(None, None, 4, 0, 1, 10, ctypes.byref(out)) == B.EINVAL      # NULL tensors
+    assert L.peat_topk_mean(None, None, 0, 0, 0, 10, ctypes.byref(out)) == B.EINVAL      # num < 1
+    assert L.peat_topk_mean(None, None, 0, 0, 11, 10, ctypes.byref(out)) == B.EINVAL     # num > den
+    assert L.peat_topk_mean(None, None, 0, 0, 1, (1 << 20) + 1, ctypes.byref(out)) == B.EINVAL
+    assert L.peat_topk_mean(None, None, 0, 7, 1, 10, ctypes.byref(out)) == B.EDTYPE
+    assert L.peat_topk_mean(None, None, 0, 0, 1, 10, None) == B.EINVAL
+    assert L.peat_topk_mean_batched(None, 0, 1, 10, outs) == B.OK                        # nothing to do
+    assert L.peat_topk_mean_batched(None, -1, 1, 10, outs) == B.EINVAL
+    pairs = (B.Pair * 1)(B.Pair(None, None, 4, 0, 0))
+    assert L.peat_topk_mean_batched(pairs, 1, 1, 10, outs) == B.EINVAL                    # NULL tensors
 
 
 def test_finalize_stats_host():

@@ -1,0 +1,139 @@
+"""GPU parity of the top-k error mean (peat_topk_mean, the paper's "mean of
+the top 10% errors") against the oracle's sort: n_valid, k, count_above and
+the k-th largest error bit-exact; the sum and mean within 1e-12 relative
+(both are binary64 sums of k non-negative terms: the device's fixed tree plus
+exact integer candidate sums against the oracle's compensated sum).  Cases
+span several chunks with ragged tails in the three element types, special
+values, heavy ties (the candidate rounds on many equal keys), a zero and an
+infinite k-th error, unaligned pointers, batched against single calls, and a
+full-size Llama-7B-shaped tensor."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_13544_amd as P
+import synth
+from tests.parity import special_pair, to_device
+
+pytestmark = pytest.mark.gpu
+
+FRACS = [(1, 10), (1, 100), (1, 1), (3, 7), (1, 1 << 20)]
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def assert_topk(got: dict, ref: dict, ctx: str = ""):
+    for key in ("n_valid", "k", "count_above"):
+        assert got[key] == ref[key], f"{ctx}: {key} {got[key]} != {ref[key]}"
+    for key in ("kth_value", "sum_topk", "mean_topk"):
+        a, b = got[key], ref[key]
+        if math.isnan(b):
+            assert math.isnan(a), f"{ctx}: {key} {a} != NaN"
+        elif math.isinf(b) or key == "kth_value":
+            assert a == b, f"{ctx}: {key} {a!r} != {b!r}"
+        else:
+            assert abs(a - b) <= 1e-12 * abs(b), f"{ctx}: {key} {a!r} vs {b!r}"
+
+
+def same_record(a: dict, b: dict) -> bool:
+    """Bit-identical records (NaN fields compare equal to NaN)."""
+    return all(a[k] == b[k] or (isinstance(a[k], float) and math.isnan(a[k]) and math.isnan(b[k]))
+               for k in a)
+
+
+def check(gb, tb, code, num=1, den=10, ctx=""):
+    got = P.topk_mean(to_device(gb, code), to_device(tb, code), num, den)
+    ref = oracle.topk(gb, tb, dtype=code, num=num, den=den)
+    assert_topk(got, ref, ctx)
+    return got
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_sizes_specials_and_fractions(code):
+    for i, n in enumerate([0, 1, 7, 4095, 4097, 65536 + 13, 300005, (1 << 20) + 3]):
+        gb, tb = special_pair(n, code, seed=4000 + 13 * i + code)
+        for num, den in FRACS:
+            log(f"  dtype={code} n={n} frac={num}/{den}")
+            check(gb, tb, code, num, den, f"dtype={code} n={n} {num}/{den}")
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_ties_and_equal_errors(code):
+    n = 200003
+    rng = np.random.default_rng(55 + code)
+    g = rng.standard_normal(n)
+    # errors on a coarse grid: many equal keys in every boundary bin
+    q = rng.integers(0, 6, n).astype(np.float64)
+    from tests.parity import float_to_bits
+    for name, t in [("grid", g + q * 0.25), ("constant", g + 0.5), ("identical", g.copy())]:
+        gb, tb = float_to_bits(g, code), float_to_bits(t, code)
+        for num, den in FRACS:
+            log(f"  dtype={code} {name} frac={num}/{den}")
+            check(gb, tb, code, num, den, f"{name} {num}/{den}")
+
+
+def test_zero_and_infinite_kth():
+    code = 0
+    n = 100000
+    rng = np.random.default_rng(9)
+    g = rng.standard_normal(n).astype(np.float32)
+    t = g.copy()
+    t[rng.integers(0, n, 50)] += 1.0                     # 50 nonzero errors: the top 10% ends at 0
+    check(g.view(np.uint32), t.view(np.uint32), code, 1, 10, "zero kth")
+    t2 = g.copy()
+    t2[rng.integers(0, n, 20000)] = np.inf               # ~18% infinite errors: the 10th percentile is Inf
+    check(g.view(np.uint32), t2.view(np.uint32), code, 1, 10, "inf kth")
+    check(g.view(np.uint32), t2.view(np.uint32), code, 1, 2, "inf above, finite kth")
+    t3 = np.full(n, np.nan, np.float32)
+    check(g.view(np.uint32), t3.view(np.uint32), code, 1, 10, "all NaN")
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_unaligned_pointers(code):
+    n = 90001
+    gb, tb = special_pair(n + 1, code, seed=71 + code)
+    got = P.topk_mean(to_device(gb, code)[1:], to_device(tb, code)[1:], 1, 10)
+    assert_topk(got, oracle.topk(gb[1:], tb[1:], dtype=code, num=1, den=10), "unaligned")
+
+
+def test_batched_equals_single_and_is_deterministic():
+    pairs_host = []
+    for k, (n, code) in enumerate([(300000, 0), (5000, 1), (1 << 20, 2), (77, 0), (0, 1), (250000, 0)]):
+        pairs_host.append((*special_pair(n, code, seed=900 + k), code))
+    pairs = [(to_device(g, c), to_device(t, c)) for g, t, c in pairs_host]
+    for num, den in ((1, 10), (1, 1000)):
+        batched = P.topk_mean_batched(pairs, num, den)
+        again = P.topk_mean_batched(pairs, num, den)
+        for k, ((g, t, c), (gd, td)) in enumerate(zip(pairs_host, pairs)):
+            single = P.topk_mean(gd, td, num, den)
+            assert same_record(single, batched[k]) and same_record(batched[k], again[k]), f"pair {k}"
+            assert_topk(batched[k], oracle.topk(g, t, dtype=c, num=num, den=den), f"pair {k}")
+
+
+def test_llama7b_tensor_full_size():
+    """Full-size Llama-7B-shaped tensors of the benchmark workload: the gate
+    projection of layer 0 (45 M elements) as weights and as Adam second
+    moment, with the workload's exponent-bit injection applied."""
+    from tests.parity import to_host_bits
+    states = synth.llama7b_states()
+    for k, (name, shape, state) in enumerate(states):
+        if name != "l0.gate" or state not in (0, 2):
+            continue
+        log(f"  {name} state={state} {shape}")
+        G, T = synth.config5_pair(k, shape, state, "cuda")
+        P.inject(T, synth.inject_seed(5, k), synth.CONFIG5_RATE, synth.CONFIG5_MASK)
+        got = P.topk_mean(G, T, 1, 10)
+        ref = oracle.topk(to_host_bits(G), to_host_bits(T), dtype=0, num=1, den=10)
+        assert_topk(got, ref, f"{name} state={state}")
+        assert got["k"] == -(-G.numel() // 10)
+        del G, T
+    torch.cuda.empty_cache()
