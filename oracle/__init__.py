@@ -17,6 +17,8 @@ Validation in DNN Training"):
     torch.isclose(rtol, atol) -> absolute-threshold mismatch counts.
   * Section V-D, Fig. "tiny_error_gemm_resnet34": error value histograms.
   * Section II-B "Error Models": random bit flip at a bit error rate.
+  * Section II-B and Section III-C/V-A: random zero, random NaN, random
+    value (num_pos positions) and the FP16/BF16 cast error.
   * Section IV-B.3 "Mean of Top 10% Errors" (the Analyzer's main score,
     Section IV-C): mean of the k largest errors, k = ceil(n_valid num/den).
   * Algorithms 1 and 2: Inject() followed by Err(golden set, FI set).
@@ -38,6 +40,8 @@ F32, F16, BF16 = 0, 1, 2
 _DTYPE_CODE = {np.dtype(np.float32): F32, np.dtype(np.float16): F16}
 
 OK, EINVAL, EDTYPE, EBITMASK, ERATE, ENOMEM = 0, -1, -2, -3, -4, -6
+MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN = 0, 1, 2, 3
+MAX_POSITIONS = 4096
 
 
 class _Sig(ctypes.Structure):
@@ -122,6 +126,15 @@ def lib():
             L.oracle_topk.restype = ctypes.c_int
             L.oracle_topk.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
                                       ctypes.c_int, ctypes.c_int, ctypes.POINTER(_TopK)]
+            L.oracle_inject_model.restype = ctypes.c_int64
+            L.oracle_inject_model.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
+                                              ctypes.c_double, ctypes.c_int, ctypes.c_uint64]
+            L.oracle_corrupt_positions.restype = ctypes.c_int64
+            L.oracle_corrupt_positions.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                                   ctypes.c_uint64, ctypes.c_int, ctypes.c_int64,
+                                                   ctypes.c_uint64, ctypes.POINTER(ctypes.c_int64)]
+            L.oracle_cast_round.restype = ctypes.c_int
+            L.oracle_cast_round.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]
             L.oracle_sizeof_sig.restype = ctypes.c_int
             assert L.oracle_sizeof_sig() == ctypes.sizeof(_Sig)
             L.oracle_sizeof_topk.restype = ctypes.c_int
@@ -274,3 +287,34 @@ def topk_rc(n, code, num, den) -> int:
     out = _TopK()
     return int(lib().oracle_topk(buf.ctypes.data, buf.ctypes.data, int(n), code, int(num), int(den),
                                  ctypes.byref(out)))
+
+
+def inject_model(x: np.ndarray, *, dtype: int | None = None, seed: int, rate: float, model: int,
+                 mask: int = 0) -> int:
+    """Rate-mode error model in place (0 bit flip, 1 zero, 3 NaN); returns the
+    number of chosen elements (or a negative code)."""
+    if not x.flags.c_contiguous or not x.flags.writeable:
+        raise ValueError("inject_model needs a writeable C-contiguous array")
+    code = _code(x, dtype)
+    return int(lib().oracle_inject_model(x.ctypes.data if x.size else None, x.size, code, seed & (2**64 - 1),
+                                         float(rate), int(model), mask & (2**64 - 1)))
+
+
+def corrupt_positions(x: np.ndarray, *, dtype: int | None = None, seed: int, model: int, num_pos: int,
+                      mask: int = 0):
+    """Position-mode error model in place; returns (rc, positions list)."""
+    if not x.flags.c_contiguous or not x.flags.writeable:
+        raise ValueError("corrupt_positions needs a writeable C-contiguous array")
+    code = _code(x, dtype)
+    pos = (ctypes.c_int64 * max(1, int(num_pos)))()
+    rc = int(lib().oracle_corrupt_positions(x.ctypes.data if x.size else None, x.size, code,
+                                            seed & (2**64 - 1), int(model), int(num_pos), mask & (2**64 - 1),
+                                            pos))
+    return rc, ([int(pos[k]) for k in range(rc)] if rc > 0 else [])
+
+
+def cast_round(x: np.ndarray, to_dtype: int) -> int:
+    """FP16 (1) / BF16 (2) round-to-nearest-even cast of an f32 array in place."""
+    if x.dtype not in (np.float32, np.uint32) or not x.flags.c_contiguous or not x.flags.writeable:
+        raise ValueError("cast_round needs a writeable C-contiguous f32 array")
+    return int(lib().oracle_cast_round(x.ctypes.data if x.size else None, x.size, int(to_dtype)))

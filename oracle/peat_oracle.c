@@ -20,6 +20,15 @@
  *                     by Inject() in Playback FI (Algorithm 1) and Runtime FI
  *                     (Algorithm 2).
  *
+ *   oracle_inject_model, oracle_corrupt_positions, oracle_cast_round
+ *                     the paper's other error models (Section II-B "Error
+ *                     Models"; Section III-C pseudo-errors; Section V-A
+ *                     settings): random zero, random NaN and bit flip at a
+ *                     rate; random value, random zero, random NaN or bit flip
+ *                     at num_pos distinct random positions; the FP16 (and
+ *                     BF16) error, a round-to-nearest-even cast of an FP32
+ *                     tensor.
+ *
  *   oracle_topk       the "mean of the top 10% errors" score (Section IV-B,
  *                     FI Assessment Scores; the Analyzer's main score,
  *                     Section IV-C), for any fraction num/den: the errors of
@@ -501,3 +510,149 @@ int oracle_topk(const void *golden, const void *test, int64_t n, int dtype, int 
 }
 
 int oracle_sizeof_topk(void) { return (int)sizeof(oracle_topk_t); }
+
+/* ------------------------------------------------------------------------ */
+/* Other error models (Section II-B; Section III-C; Section V-A).            */
+/* ------------------------------------------------------------------------ */
+
+#define ORACLE_MODEL_BITFLIP 0
+#define ORACLE_MODEL_ZERO 1
+#define ORACLE_MODEL_VALUE 2
+#define ORACLE_MODEL_NAN 3
+#define ORACLE_MAX_POSITIONS 4096
+
+/* The quiet NaN written by the NaN model: sign 0, exponent all ones, top
+ * mantissa bit set, the rest 0. */
+static uint32_t canonical_nan(int dtype) {
+    return dtype == ORACLE_F32 ? 0x7FC00000u : (dtype == ORACLE_F16 ? 0x7E00u : 0x7FC0u);
+}
+
+static void store_bits(void *x, int64_t i, int dtype, uint32_t v) {
+    if (dtype == ORACLE_F32) {
+        memcpy((unsigned char *)x + 4 * i, &v, 4);
+    } else {
+        uint16_t h = (uint16_t)v;
+        memcpy((unsigned char *)x + 2 * i, &h, 2);
+    }
+}
+
+/* The model's new bits for element i (not for the value model). */
+static uint32_t model_bits(int model, int dtype, uint32_t old, uint64_t seed, int64_t i, uint64_t mask) {
+    if (model == ORACLE_MODEL_ZERO) return 0;
+    if (model == ORACLE_MODEL_NAN) return canonical_nan(dtype);
+    return old ^ (1u << chosen_bit(seed, i, mask));
+}
+
+/* Rate mode: the elements oracle_inject would flip (U_i < T, every element
+ * when rate >= 1) are set to +0 (model 1), to the canonical quiet NaN
+ * (model 3) or bit-flipped (model 0, identical to oracle_inject).  The
+ * mask is used by the bit-flip model only.  Returns the number of chosen
+ * elements or a negative error code. */
+int64_t oracle_inject_model(void *x, int64_t n, int dtype, uint64_t seed, double rate, int model,
+                            uint64_t mask) {
+    if (!dtype_width(dtype)) return ORACLE_EDTYPE;
+    if (model != ORACLE_MODEL_BITFLIP && model != ORACLE_MODEL_ZERO && model != ORACLE_MODEL_NAN)
+        return ORACLE_EINVAL;
+    int rc = check_inject(dtype, rate, model == ORACLE_MODEL_BITFLIP ? mask : 1);
+    if (rc) return rc;
+    if (n < 0 || (n > 0 && !x)) return ORACLE_EINVAL;
+    int all;
+    uint64_t T = oracle_rate_threshold(rate, &all);
+    int64_t count = 0;
+    uint64_t A[4], B[4];
+    for (int64_t i = 0; i < n; ++i) {
+        if ((i & 31) == 0) philox_seeded(seed, (uint64_t)i >> 5, 0, A);
+        if ((i & 3) == 0) philox_seeded(seed, (uint64_t)i >> 2, 1, B);
+        if (!(all || uniform_of(A, B, i) < T)) continue;
+        store_bits(x, i, dtype, model_bits(model, dtype, element_bits(x, i, dtype), seed, i, mask));
+        ++count;
+    }
+    return count;
+}
+
+/* Position mode (the paper's num_pos).  Draw j = 0, 1, 2, ... gives the
+ * block W = Philox(key=(seed,0), ctr=(j, 3, 0, 0)) and the index
+ * p_j = floor(W[0] * n / 2^64); the positions are the first num_pos distinct
+ * p_j in order of appearance.  Position m (drawn at j) becomes +0 (model 1),
+ * the canonical NaN (model 3), a bit flip with the rate mode's bit rule
+ * (model 0), or (model 2, random value) the uncorrupted tensor's value at
+ * index floor(W[1] * n / 2^64) -- a value drawn from the tensor's own
+ * distribution.  0 <= num_pos <= min(n, 4096).  positions (optional) gets
+ * the positions in order.  Returns num_pos or a negative error code. */
+int64_t oracle_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed, int model,
+                                 int64_t num_pos, uint64_t mask, int64_t *positions) {
+    int width = dtype_width(dtype);
+    if (!width) return ORACLE_EDTYPE;
+    if (model < ORACLE_MODEL_BITFLIP || model > ORACLE_MODEL_NAN) return ORACLE_EINVAL;
+    if (model == ORACLE_MODEL_BITFLIP && (mask == 0 || (mask >> width) != 0)) return ORACLE_EBITMASK;
+    if (n < 0 || num_pos < 0 || num_pos > n || num_pos > ORACLE_MAX_POSITIONS) return ORACLE_EINVAL;
+    if (num_pos > 0 && !x) return ORACLE_EINVAL;
+    int64_t pos[ORACLE_MAX_POSITIONS], src[ORACLE_MAX_POSITIONS];
+    int64_t m = 0;
+    for (uint64_t j = 0; m < num_pos; ++j) {
+        uint64_t W[4];
+        philox_seeded(seed, j, 3, W);
+        int64_t p = (int64_t)(((unsigned __int128)W[0] * (uint64_t)n) >> 64);
+        int seen = 0;
+        for (int64_t q = 0; q < m; ++q) seen |= pos[q] == p;
+        if (seen) continue;
+        pos[m] = p;
+        src[m] = (int64_t)(((unsigned __int128)W[1] * (uint64_t)n) >> 64);
+        ++m;
+    }
+    /* every source is read before any position is written */
+    uint32_t val[ORACLE_MAX_POSITIONS];
+    for (int64_t q = 0; q < num_pos; ++q)
+        val[q] = model == ORACLE_MODEL_VALUE ? element_bits(x, src[q], dtype)
+                                             : model_bits(model, dtype, element_bits(x, pos[q], dtype), seed,
+                                                          pos[q], mask);
+    for (int64_t q = 0; q < num_pos; ++q) {
+        store_bits(x, pos[q], dtype, val[q]);
+        if (positions) positions[q] = pos[q];
+    }
+    return num_pos;
+}
+
+/* Round-to-nearest-even of a binary64 value to a binary format with p
+ * significand bits (implicit bit included) and normal exponents
+ * [emin, emax]: the result as a binary64.  Magnitudes at or above the
+ * midpoint between the largest finite value and 2^(emax+1) become Inf. */
+static double round_to_format(double v, int p, int emin, int emax) {
+    if (isnan(v) || isinf(v) || v == 0.0) return v;
+    double a = fabs(v);
+    double overflow = ldexp(2.0 - ldexp(1.0, -p), emax);   /* (2 - 2^-p) 2^emax */
+    if (a >= overflow) return v > 0 ? INFINITY : -INFINITY;
+    int e;
+    frexp(a, &e);                         /* a in [2^(e-1), 2^e) */
+    int exp = e - 1;
+    if (exp < emin) exp = emin;           /* the subnormal range keeps the quantum of 2^emin */
+    double quantum = ldexp(1.0, exp - (p - 1));
+    double r = rint(a / quantum) * quantum; /* a / quantum is exact: a power-of-two scaling */
+    return v > 0 ? r : -r;
+}
+
+/* FP16 / BF16 error (Section III-C): every element of an f32 tensor x[0..n)
+ * is replaced by its round-to-nearest-even value in the narrower type,
+ * widened back (to_dtype 1: binary16, 2: bfloat16).  A NaN becomes the f32
+ * quiet NaN with its sign kept (sign | 0x7FC00000).  Returns 0 or a
+ * negative error code. */
+int oracle_cast_round(void *x, int64_t n, int to_dtype) {
+    if (to_dtype != ORACLE_F16 && to_dtype != ORACLE_BF16) return ORACLE_EDTYPE;
+    if (n < 0 || (n > 0 && !x)) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t b = element_bits(x, i, ORACLE_F32);
+        float f;
+        memcpy(&f, &b, 4);
+        uint32_t out;
+        if (isnan(f)) {
+            out = (b & 0x80000000u) | 0x7FC00000u;
+        } else {
+            double r = to_dtype == ORACLE_F16 ? round_to_format((double)f, 11, -14, 15)
+                                              : round_to_format((double)f, 8, -126, 127);
+            float g = (float)r;           /* exact: r has at most 11 significant bits */
+            memcpy(&out, &g, 4);
+        }
+        store_bits(x, i, ORACLE_F32, out);
+    }
+    return ORACLE_OK;
+}
