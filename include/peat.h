@@ -139,14 +139,26 @@ typedef struct {
     int32_t reserved;   /* must be 0      */
 } peat_pair_t;
 
+/* Error models (Section II-B "Error Models"; Section III-C pseudo-errors). */
+typedef enum {
+    PEAT_MODEL_BITFLIP = 0, /* toggle one bit of the mask (random bit flip)      */
+    PEAT_MODEL_ZERO = 1,    /* set to +0 (random zero)                            */
+    PEAT_MODEL_VALUE = 2,   /* copy of the tensor's value at a random index
+                             * (random value; position mode only)                */
+    PEAT_MODEL_NAN = 3      /* set to the quiet NaN 0x7FC00000 / 0x7E00 / 0x7FC0 */
+} peat_model_t;
+
+#define PEAT_MAX_POSITIONS 4096
+
 typedef struct {
     void *tensor;     /* device pointer, modified in place */
     int64_t n;        /* elements, >= 0 */
     int32_t dtype;    /* peat_dtype_t   */
-    int32_t reserved; /* must be 0      */
+    int32_t model;    /* peat_model_t: BITFLIP (0), ZERO or NAN */
     uint64_t seed;
-    double rate;      /* bit error rate per element; >= 1 flips every element */
-    uint64_t bitmask; /* candidate bits, nonzero, below the type width */
+    double rate;      /* error rate per element; >= 1 chooses every element */
+    uint64_t bitmask; /* BITFLIP: candidate bits, nonzero, below the type
+                       * width; ignored by the other models */
 } peat_inject_item_t;
 
 /* Static text for a PEAT_E* code; never NULL. */
@@ -213,8 +225,37 @@ int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
 int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed,
                     double rate, uint64_t bitmask);
 
+/* peat_inject with another error model at the same rate (Section II-B):
+ * the elements peat_inject would flip (same seed and rate) are set to +0
+ * (PEAT_MODEL_ZERO), to the type's quiet NaN (PEAT_MODEL_NAN) or bit-flipped
+ * (PEAT_MODEL_BITFLIP, identical to peat_inject).  bitmask is ignored by
+ * ZERO and NAN.  Returns the number of chosen elements or a negative code
+ * (PEAT_EINVAL for PEAT_MODEL_VALUE, which needs positions). */
+int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
+                          int32_t model, uint64_t bitmask);
+
+/* The paper's num_pos corruption (Section V-A): exactly num_pos distinct
+ * positions, 0 <= num_pos <= min(n, PEAT_MAX_POSITIONS).  Draw j = 0, 1, ...
+ * takes W = Philox4x64-10 with key (seed, 0) at counter (j, 3, 0, 0) and the
+ * index floor(W[0] * n / 2^64); the positions are the first num_pos distinct
+ * indices in order of appearance.  Each becomes +0, the quiet NaN, a bit
+ * flip (peat_inject's bit rule for that index), or -- PEAT_MODEL_VALUE, a
+ * value from the tensor's own distribution -- the uncorrupted tensor's value
+ * at floor(W[1] * n / 2^64) of the draw that chose it.  positions (host,
+ * num_pos entries, may be NULL) receives the positions in order.  Returns
+ * num_pos or a negative code; waits for the device. */
+int64_t peat_corrupt_positions(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, int32_t model,
+                               int64_t num_pos, uint64_t bitmask, int64_t *positions);
+
+/* The FP16 / BF16 error of Section III-C: every element of an f32 tensor
+ * (device, in place) becomes its round-to-nearest-even value in to_dtype
+ * (PEAT_F16 or PEAT_BF16) widened back to f32; overflow gives +-Inf,
+ * subnormals round correctly, a NaN becomes sign | 0x7FC00000.  Enqueued on
+ * the calling thread's stream (peat_set_stream); does not wait. */
+int peat_cast_round(void *tensor, int64_t n, peat_dtype_t to_dtype);
+
 /* peat_inject over count >= 0 items in one launch sequence; counts is a host
- * array receiving each item's flip count. */
+ * array receiving each item's flip count (chosen elements for ZERO/NAN). */
 int peat_inject_batched(const peat_inject_item_t *items, int32_t count, int64_t *counts);
 
 /* As peat_inject_batched, enqueued on stream; d_counts is a device int64

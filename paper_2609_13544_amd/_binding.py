@@ -17,6 +17,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libpeat.so")
 
 F32, F16, BF16 = 0, 1, 2
+MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN = 0, 1, 2, 3
+MAX_POSITIONS = 4096
 OK, EINVAL, EDTYPE, EBITMASK, ERATE, EHIP, ENOMEM, ENODEV = 0, -1, -2, -3, -4, -5, -6, -7
 MAX_THRESHOLDS, MAX_BINS = 8, 64
 
@@ -77,7 +79,7 @@ class Pair(ctypes.Structure):
 
 class InjectItem(ctypes.Structure):
     _fields_ = [("tensor", ctypes.c_void_p), ("n", ctypes.c_int64), ("dtype", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("seed", ctypes.c_uint64), ("rate", ctypes.c_double),
+                ("model", ctypes.c_int32), ("seed", ctypes.c_uint64), ("rate", ctypes.c_double),
                 ("bitmask", ctypes.c_uint64)]
 
 
@@ -120,6 +122,12 @@ _PROTOS = {
                                                     ctypes.c_void_p, ctypes.c_void_p]),
     "peat_inject": (ctypes.c_int64, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
                                      ctypes.c_double, ctypes.c_uint64]),
+    "peat_inject_model": (ctypes.c_int64, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
+                                           ctypes.c_double, ctypes.c_int32, ctypes.c_uint64]),
+    "peat_corrupt_positions": (ctypes.c_int64, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
+                                                ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64,
+                                                ctypes.POINTER(ctypes.c_int64)]),
+    "peat_cast_round": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]),
     "peat_inject_batched": (ctypes.c_int, [ctypes.POINTER(InjectItem), ctypes.c_int32,
                                            ctypes.POINTER(ctypes.c_int64)]),
     "peat_inject_batched_async": (ctypes.c_int, [ctypes.POINTER(InjectItem), ctypes.c_int32,
@@ -370,15 +378,51 @@ def inject(tensor, seed: int, rate: float, bitmask: int, *, dtype: int | None = 
     return _check(rc, "peat_inject")
 
 
+def inject_model(tensor, seed: int, rate: float, model: int, bitmask: int = 0) -> int:
+    """peat_inject_model in place: the elements peat_inject would flip are set
+    to zero (MODEL_ZERO), NaN (MODEL_NAN) or bit-flipped (MODEL_BITFLIP)."""
+    _dev_tensor(tensor, "tensor")
+    n = tensor.numel()
+    set_stream()
+    rc = lib().peat_inject_model(tensor.data_ptr() if n else None, n, dtype_code(tensor), seed & (2 ** 64 - 1),
+                                 float(rate), int(model), bitmask & (2 ** 64 - 1))
+    return _check(rc, "peat_inject_model")
+
+
+def corrupt_positions(tensor, seed: int, model: int, num_pos: int, bitmask: int = 0) -> list[int]:
+    """peat_corrupt_positions in place (the paper's num_pos corruption);
+    returns the positions in order."""
+    _dev_tensor(tensor, "tensor")
+    n = tensor.numel()
+    pos = (ctypes.c_int64 * max(1, int(num_pos)))()
+    set_stream()
+    rc = lib().peat_corrupt_positions(tensor.data_ptr() if n else None, n, dtype_code(tensor),
+                                      seed & (2 ** 64 - 1), int(model), int(num_pos), bitmask & (2 ** 64 - 1), pos)
+    _check(rc, "peat_corrupt_positions")
+    return [int(pos[k]) for k in range(rc)]
+
+
+def cast_round(tensor, to_dtype: int) -> None:
+    """peat_cast_round: the FP16 (to_dtype=F16) or BF16 error of an f32 device
+    tensor, in place (enqueued on the current stream)."""
+    _dev_tensor(tensor, "tensor")
+    if dtype_code(tensor) != F32:
+        raise ValueError("cast_round needs an f32 tensor")
+    n = tensor.numel()
+    set_stream()
+    _check(lib().peat_cast_round(tensor.data_ptr() if n else None, n, int(to_dtype)), "peat_cast_round")
+
+
 def _items_array(items):
     arr = (InjectItem * max(1, len(items)))()
     for k, it in enumerate(items):
         if isinstance(it, InjectItem):
             arr[k] = it
             continue
-        t, seed, rate, mask = it
+        t, seed, rate, mask = it[:4]
+        model = it[4] if len(it) > 4 else MODEL_BITFLIP
         _dev_tensor(t, f"items[{k}].tensor")
-        arr[k] = InjectItem(t.data_ptr(), t.numel(), dtype_code(t), 0, seed & (2 ** 64 - 1), float(rate),
+        arr[k] = InjectItem(t.data_ptr(), t.numel(), dtype_code(t), model, seed & (2 ** 64 - 1), float(rate),
                             mask & (2 ** 64 - 1))
     return arr
 

@@ -332,12 +332,13 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
 int check_item(const peat_inject_item_t &it, int k) {
     if (check_dtype(it.dtype)) return fail(PEAT_EDTYPE, "item %d: unknown dtype %d", k, it.dtype);
     const int width = elem_size(it.dtype) * 8;
-    if (it.bitmask == 0 || (it.bitmask >> width) != 0)
+    if (it.model != PEAT_MODEL_BITFLIP && it.model != PEAT_MODEL_ZERO && it.model != PEAT_MODEL_NAN)
+        return fail(PEAT_EINVAL, "item %d: model %d is not BITFLIP, ZERO or NAN", k, it.model);
+    if (it.model == PEAT_MODEL_BITFLIP && (it.bitmask == 0 || (it.bitmask >> width) != 0))
         return fail(PEAT_EBITMASK, "item %d: bitmask 0x%llx is 0 or has bits at or above bit %d", k,
                     (unsigned long long)it.bitmask, width);
     if (std::isnan(it.rate) || it.rate < 0) return fail(PEAT_ERATE, "item %d: rate must be >= 0", k);
     if (it.n < 0) return fail(PEAT_EINVAL, "item %d: n < 0", k);
-    if (it.reserved != 0) return fail(PEAT_EINVAL, "item %d: reserved field must be 0", k);
     if (it.n > 0 && !it.tensor) return fail(PEAT_EINVAL, "item %d: NULL tensor with n > 0", k);
     if (it.n > (int64_t(1) << 46)) return fail(PEAT_EINVAL, "item %d: n above 2^46", k);
     return PEAT_OK;
@@ -366,9 +367,10 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
         q.x = it.tensor;
         q.n = it.n;
         q.seed = it.seed;
-        q.mask = it.bitmask;
+        q.mask = it.model == PEAT_MODEL_BITFLIP ? it.bitmask : 1;
         q.dtype = it.dtype;
-        q.popc = __builtin_popcountll(it.bitmask);
+        q.popc = __builtin_popcountll(q.mask);
+        q.model = it.model;
         q.all = it.rate >= 1.0;
         // T = floor(rate * 2^64): ldexp is exact and the conversion truncates
         q.T = (q.all || it.rate == 0.0) ? 0 : (uint64_t)std::ldexp(it.rate, 64);
@@ -607,10 +609,68 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count, const 
 
 int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
                     uint64_t bitmask) {
-    peat_inject_item_t it{tensor, n, (int32_t)dtype, 0, seed, rate, bitmask};
+    peat_inject_item_t it{tensor, n, (int32_t)dtype, PEAT_MODEL_BITFLIP, seed, rate, bitmask};
     int64_t c = 0;
     int rc = inject_core(&it, 1, nullptr, &c, t_stream);
     return rc ? rc : c;
+}
+
+int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
+                          int32_t model, uint64_t bitmask) {
+    peat_inject_item_t it{tensor, n, (int32_t)dtype, model, seed, rate, bitmask};
+    int64_t c = 0;
+    int rc = inject_core(&it, 1, nullptr, &c, t_stream);
+    return rc ? rc : c;
+}
+
+int64_t peat_corrupt_positions(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, int32_t model,
+                               int64_t num_pos, uint64_t bitmask, int64_t *positions) {
+    if (check_dtype(dtype)) return fail(PEAT_EDTYPE, "unknown dtype %d", (int)dtype);
+    if (model < PEAT_MODEL_BITFLIP || model > PEAT_MODEL_NAN) return fail(PEAT_EINVAL, "unknown model %d", model);
+    const int width = elem_size(dtype) * 8;
+    if (model == PEAT_MODEL_BITFLIP && (bitmask == 0 || (bitmask >> width) != 0))
+        return fail(PEAT_EBITMASK, "bitmask 0x%llx is 0 or has bits at or above bit %d",
+                    (unsigned long long)bitmask, width);
+    if (n < 0 || n > (int64_t(1) << 46)) return fail(PEAT_EINVAL, "n must be in [0, 2^46]");
+    if (num_pos < 0 || num_pos > n || num_pos > PEAT_MAX_POSITIONS)
+        return fail(PEAT_EINVAL, "num_pos must be in [0, min(n, %d)] (got %lld)", PEAT_MAX_POSITIONS,
+                    (long long)num_pos);
+    if (num_pos == 0) return 0;
+    if (!tensor) return fail(PEAT_EINVAL, "tensor is NULL");
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    int rc = current_dev(&dv);
+    if (rc) return rc;
+    Dev &d = *dv;
+    hipStream_t s = t_stream;
+    char *ws;
+    if ((rc = acquire_ws(d, sizeof(int64_t) * PEAT_MAX_POSITIONS, s, &ws))) return rc;
+    Slot *sl;
+    if ((rc = acquire_slot(d, sizeof(int64_t) * PEAT_MAX_POSITIONS, &sl))) return rc;
+    int64_t *dpos = reinterpret_cast<int64_t *>(ws);
+    HIP_OR_FAIL(launch_corrupt_positions(tensor, n, dtype, seed, model, num_pos, bitmask, dpos, s));
+    HIP_OR_FAIL(hipMemcpyAsync(sl->host, dpos, sizeof(int64_t) * num_pos, hipMemcpyDeviceToHost, s));
+    if ((rc = release_slot(*sl, s))) return rc;
+    if ((rc = release_ws(d, s))) return rc;
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    const int64_t *hp = static_cast<const int64_t *>(sl->host);
+    if (hp[0] < 0) return fail(PEAT_EHIP, "position draw limit reached before %lld distinct positions", (long long)num_pos);
+    if (positions) std::memcpy(positions, hp, sizeof(int64_t) * num_pos);
+    return num_pos;
+}
+
+int peat_cast_round(void *tensor, int64_t n, peat_dtype_t to_dtype) {
+    if (to_dtype != PEAT_F16 && to_dtype != PEAT_BF16)
+        return fail(PEAT_EDTYPE, "to_dtype must be PEAT_F16 or PEAT_BF16 (got %d)", (int)to_dtype);
+    if (n < 0) return fail(PEAT_EINVAL, "n < 0");
+    if (n == 0) return PEAT_OK;
+    if (!tensor) return fail(PEAT_EINVAL, "tensor is NULL");
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    int rc = current_dev(&dv);
+    if (rc) return rc;
+    HIP_OR_FAIL(launch_cast_round(tensor, n, to_dtype, t_stream));
+    return PEAT_OK;
 }
 
 int peat_inject_batched(const peat_inject_item_t *items, int32_t count, int64_t *counts) {

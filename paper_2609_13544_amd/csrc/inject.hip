@@ -1,5 +1,6 @@
 // Random-bit-flip injector for gfx950 (the RBF error model of Section II-B,
-// used by Inject() in Algorithms 1 and 2).
+// used by Inject() in Algorithms 1 and 2); the same decisions drive the
+// random-zero and random-NaN models at a rate.
 //
 // Element i of a tensor flips iff its 64-bit uniform U_i is below
 // T = floor(rate * 2^64) (every element when rate >= 1).  U_i is built from
@@ -13,66 +14,29 @@
 // draws one block per 32 elements and evaluates the low bits only for the
 // (1 in 256) elements whose top byte is zero.  The tensor is read and written
 // only at flipped elements.
-#include "peat_internal.h"
+#include "philox.h"
 
 namespace peat {
 namespace {
 
-constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ULL, kM1 = 0xCA5A826395121157ULL;
-constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ULL, kW1 = 0xBB67AE8584CAA73BULL;
-
-// 64 x 64 -> 128-bit product from four 32 x 32 -> 64 multiply-adds.
-__device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t b, uint64_t &lo, uint64_t &hi) {
-    const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
-    const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
-    const uint64_t p00 = (uint64_t)a0 * b0;
-    const uint64_t t = (uint64_t)a1 * b0 + (p00 >> 32);
-    const uint64_t u = (uint64_t)a0 * b1 + (uint32_t)t;
-    lo = (u << 32) | (uint32_t)p00;
-    hi = (uint64_t)a1 * b1 + (t >> 32) + (u >> 32);
-}
-
-__device__ __forceinline__ void philox(uint64_t c0, uint64_t c1, uint64_t key, uint64_t out[4]) {
-    uint64_t x0 = c0, x1 = c1, x2 = 0, x3 = 0;
-    uint64_t k0 = key, k1 = 0;
-#pragma unroll
-    for (int r = 0; r < 10; ++r) {
-        uint64_t lo0, hi0, lo1, hi1;
-        mulhilo64(kM0, x0, lo0, hi0);
-        mulhilo64(kM1, x2, lo1, hi1);
-        const uint64_t y0 = hi1 ^ x1 ^ k0;
-        const uint64_t y2 = hi0 ^ x3 ^ k1;
-        x0 = y0;
-        x1 = lo1;
-        x2 = y2;
-        x3 = lo0;
-        k0 += kW0;
-        k1 += kW1;
-    }
-    out[0] = x0;
-    out[1] = x1;
-    out[2] = x2;
-    out[3] = x3;
-}
-
-__device__ __forceinline__ int chosen_bit(const InjDesc &d, uint64_t i) {
-    if (d.popc == 1) return __ffsll((long long)d.mask) - 1;
-    uint64_t C[4];
-    philox(i, 2, d.seed, C);
-    uint64_t j = ((C[0] >> 32) * (uint64_t)d.popc) >> 32;
-    uint64_t m = d.mask;
-    for (uint64_t k = 0; k < j; ++k) m &= m - 1;   // drop the j lowest set bits
-    return __ffsll((long long)m) - 1;
-}
-
+// The chosen element's new bits: a bit flip, +0 or the type's quiet NaN.
 __device__ __forceinline__ void flip(const InjDesc &d, uint64_t i) {
-    const int b = chosen_bit(d, i);
-    if (d.dtype == PEAT_F32) {
-        uint32_t *p = static_cast<uint32_t *>(d.x) + i;
-        *p ^= 1u << b;
+    if (d.model == PEAT_MODEL_BITFLIP) {
+        const int b = chosen_bit(d.seed, d.mask, d.popc, i);
+        if (d.dtype == PEAT_F32) {
+            uint32_t *p = static_cast<uint32_t *>(d.x) + i;
+            *p ^= 1u << b;
+        } else {
+            uint16_t *p = static_cast<uint16_t *>(d.x) + i;
+            *p = (uint16_t)(*p ^ (1u << b));
+        }
     } else {
-        uint16_t *p = static_cast<uint16_t *>(d.x) + i;
-        *p = (uint16_t)(*p ^ (1u << b));
+        const bool nan = d.model == PEAT_MODEL_NAN;
+        if (d.dtype == PEAT_F32) {
+            static_cast<uint32_t *>(d.x)[i] = nan ? 0x7FC00000u : 0u;
+        } else {
+            static_cast<uint16_t *>(d.x)[i] = (uint16_t)(nan ? (d.dtype == PEAT_F16 ? 0x7E00u : 0x7FC0u) : 0u);
+        }
     }
 }
 

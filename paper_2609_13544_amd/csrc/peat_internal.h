@@ -70,7 +70,7 @@ struct SigParams {
     double thr_min;                // smallest thr (+Inf when there are none)
 };
 
-struct InjDesc {                 // one per injected tensor (64 bytes)
+struct InjDesc {                 // one per injected tensor (80 bytes)
     void *x;
     int64_t n;
     uint64_t seed;
@@ -81,8 +81,10 @@ struct InjDesc {                 // one per injected tensor (64 bytes)
     int32_t dtype;
     int32_t all;                 // rate >= 1
     int32_t popc;                // popcount(mask)
+    int32_t model;               // PEAT_MODEL_BITFLIP, _ZERO or _NAN
+    int32_t reserved[3];
 };
-static_assert(sizeof(InjDesc) == 64, "InjDesc layout");
+static_assert(sizeof(InjDesc) == 80, "InjDesc layout");
 
 struct InjParams {
     const InjDesc *descs;
@@ -150,6 +152,9 @@ hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[4], hipStre
 hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
 hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
 hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);
+hipError_t launch_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed, int model, int64_t num_pos,
+                                    uint64_t mask, int64_t *d_positions, hipStream_t s);
+hipError_t launch_cast_round(void *x, int64_t n, int to_dtype, hipStream_t s);
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
 hipError_t launch_topk_zero(uint64_t *p, int64_t n, hipStream_t s);
 hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[4], hipStream_t s);
