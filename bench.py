@@ -50,10 +50,15 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
+    """sha256[:16] of the chunk pass's sources with comments and blank space
+    removed (a comment edit does not change the kernel)."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

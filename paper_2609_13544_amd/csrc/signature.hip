@@ -2,7 +2,7 @@
 //
 // Pass 1 (sig_chunk): one 256-thread block per fixed-size chunk of one pair.
 // Each thread streams 16-byte vectors of golden and test (4 f32 or 8 f16/bf16
-// elements) from the global address space, widens them exactly to binary64
+// elements) through nontemporal buffer loads, widens them exactly to binary64
 // and accumulates the signature of its elements; the chunk's record (binary64
 // partial sums, maxima with their lowest index, integer counts, histogram)
 // goes to one ChunkPartial.
@@ -16,15 +16,19 @@
 // and the error histograms of Section V-D.
 //
 // Fast path.  A wave whose current vectors hold only "ordinary" pairs (both
-// finite, no NaN, golden nonzero, same sign) needs no classification:
-//   - the relative error of the sum uses a Newton-refined reciprocal; the
-//     exact IEEE quotient is formed only when a vector may raise the lane's
-//     maximum;
-//   - absolute-error and ULP maxima are tracked per vector (value + vector
-//     number); the element is resolved once per lane at the end of the chunk
-//     by reloading that one vector;
-//   - counts use wave ballots; the histogram uses lane-private LDS counters
-//     addressed through a binary64-exponent -> slot table.
+// finite, no NaN, golden nonzero, same sign, relative error below 0.5) needs
+// no classification:
+//   - one comparison of the relative error per element flags every other
+//     case (a sign change or a zero golden gives a relative error >= 1 or
+//     NaN) together with the candidates for the maximum relative error; the
+//     exact IEEE quotient is formed only for those candidates;
+//   - reciprocals come from one hardware estimate per four elements plus a
+//     Newton step;
+//   - the maxima of |err| and of the ULP distance are wave-uniform running
+//     records (the vector that first exceeded them), resolved to an element
+//     by one reload at the end of the chunk;
+//   - counts use wave ballots; the histogram uses lane-private 16-bit LDS
+//     counters addressed through a binary64-exponent -> row table.
 // Any other vector is deferred: its wave-uniform vector number goes to a
 // per-wave LDS list and the generic per-element path (every IEEE case)
 // processes the list out of the hot loop.  Ragged tails and unaligned pairs
