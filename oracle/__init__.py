@@ -107,6 +107,11 @@ def lib():
                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
                 ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_Sig)]
+            L.oracle_signature_rtol.restype = ctypes.c_int
+            L.oracle_signature_rtol.argtypes = [
+                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_Sig)]
             L.oracle_stats.restype = ctypes.c_int
             L.oracle_stats.argtypes = [ctypes.POINTER(_Sig), ctypes.POINTER(_Stats)]
             L.oracle_philox4x64_10.restype = None
@@ -169,24 +174,40 @@ def _sig_to_dict(s: _Sig, nthr: int) -> dict:
     return d
 
 
+def split_thresholds(thresholds):
+    """([atol], [rtol]) from absolute tolerances or (atol, rtol) pairs."""
+    atol, rtol = [], []
+    for x in thresholds:
+        if isinstance(x, (tuple, list)):
+            atol.append(float(x[0]))
+            rtol.append(float(x[1]))
+        else:
+            atol.append(float(x))
+            rtol.append(0.0)
+    return atol, rtol
+
+
 def signature(golden: np.ndarray, test: np.ndarray, *, dtype: int | None = None,
               bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), raw: bool = False):
     """Error signature of (golden, test): dict of every field.
 
     ``golden``/``test`` are contiguous numpy arrays of float32/float16 or raw
     bit patterns (uint32 for f32; uint16 with ``dtype=F16``/``BF16``).
+    ``thresholds`` holds absolute tolerances or (atol, rtol) pairs.
     """
     g = np.ascontiguousarray(golden).reshape(-1)
     t = np.ascontiguousarray(test).reshape(-1)
     if g.shape != t.shape or g.dtype != t.dtype:
         raise ValueError("golden and test must have the same shape and dtype")
     code = _code(g, dtype)
-    thr = (ctypes.c_double * 8)(*[float(x) for x in thresholds])
+    atol, rtol = split_thresholds(thresholds)
+    thr = (ctypes.c_double * 8)(*atol)
+    rthr = (ctypes.c_double * 8)(*rtol)
     out = _Sig()
-    rc = lib().oracle_signature(
+    rc = lib().oracle_signature_rtol(
         g.ctypes.data if g.size else None, t.ctypes.data if t.size else None,
         g.size, code, int(bins[0]), int(bins[1]), int(bins[2]), len(thresholds),
-        thr, ctypes.byref(out))
+        thr, rthr, ctypes.byref(out))
     if rc != OK:
         raise ValueError(f"oracle_signature failed: {rc}")
     if raw:
@@ -196,10 +217,12 @@ def signature(golden: np.ndarray, test: np.ndarray, *, dtype: int | None = None,
 
 def signature_rc(golden_ptr, test_ptr, n, code, bins, thresholds) -> int:
     """Return code of oracle_signature for argument-validation tests."""
-    thr = (ctypes.c_double * max(8, len(thresholds)))(*[float(x) for x in thresholds])
+    atol, rtol = split_thresholds(thresholds)
+    thr = (ctypes.c_double * max(8, len(thresholds)))(*atol)
+    rthr = (ctypes.c_double * max(8, len(thresholds)))(*rtol)
     out = _Sig()
-    return lib().oracle_signature(golden_ptr, test_ptr, n, code, bins[0], bins[1],
-                                  bins[2], len(thresholds), thr, ctypes.byref(out))
+    return lib().oracle_signature_rtol(golden_ptr, test_ptr, n, code, bins[0], bins[1],
+                                       bins[2], len(thresholds), thr, rthr, ctypes.byref(out))
 
 
 def stats(sig: dict) -> dict:

@@ -159,24 +159,40 @@ static double csum_value(const csum_t *acc) { return acc->s + acc->c; }
 
 /* Validation of the histogram and thresholds (same acceptance rules as the
  * library: -1022 <= lo < hi <= 1024, 1 <= nbins <= 64, nbins divides hi-lo;
- * 0 <= nthr <= 8 thresholds, each >= 0 and not NaN). */
-static int check_params(int lo, int hi, int nbins, int nthr, const double *thr) {
+ * 0 <= nthr <= 8 thresholds, each absolute and relative tolerance >= 0 and
+ * not NaN). */
+static int check_params(int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr) {
     if (lo < -1022 || hi > 1024 || lo >= hi) return ORACLE_EINVAL;
     if (nbins < 1 || nbins > 64 || (hi - lo) % nbins != 0) return ORACLE_EINVAL;
     if (nthr < 0 || nthr > 8) return ORACLE_EINVAL;
     if (nthr > 0 && !thr) return ORACLE_EINVAL;
-    for (int j = 0; j < nthr; ++j)
+    for (int j = 0; j < nthr; ++j) {
         if (isnan(thr[j]) || thr[j] < 0) return ORACLE_EINVAL;
+        if (rthr && (isnan(rthr[j]) || rthr[j] < 0)) return ORACLE_EINVAL;
+    }
     return ORACLE_OK;
 }
+
+int oracle_signature_rtol(const void *golden, const void *test, int64_t n, int dtype,
+                          int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr,
+                          oracle_sig_t *out);
 
 int oracle_signature(const void *golden, const void *test, int64_t n, int dtype,
                      int lo, int hi, int nbins, int nthr, const double *thr,
                      oracle_sig_t *out) {
+    return oracle_signature_rtol(golden, test, n, dtype, lo, hi, nbins, nthr, thr, NULL, out);
+}
+
+/* The signature with the closeness test of torch.isclose(T, G, rtol, atol)
+ * (Section III-A): threshold j has the absolute tolerance thr[j] and the
+ * relative tolerance rthr[j] (rthr NULL: all 0). */
+int oracle_signature_rtol(const void *golden, const void *test, int64_t n, int dtype,
+                          int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr,
+                          oracle_sig_t *out) {
     int width = dtype_width(dtype);
     if (!width) return ORACLE_EDTYPE;
     if (!out || n < 0 || (n > 0 && (!golden || !test))) return ORACLE_EINVAL;
-    int rc = check_params(lo, hi, nbins, nthr, thr);
+    int rc = check_params(lo, hi, nbins, nthr, thr, rthr);
     if (rc) return rc;
 
     oracle_sig_t s;
@@ -242,11 +258,19 @@ int oracle_signature(const void *golden, const void *test, int64_t n, int dtype,
         }
 
         /* Step 5: mismatches = pairs that are not close under torch.isclose
-         * with rtol = 0 and atol = theta (Section III-A): the error exceeds
-         * theta, or it is infinite (unequal infinities are never close, even
-         * for theta = +Inf). */
-        for (int j = 0; j < nthr; ++j)
-            if (a > thr[j] || isinf(a)) s.n_mismatch[j] += 1;
+         * (Section III-A): equal values are close; otherwise the pair is
+         * close only if the error is finite and at most the allowed error
+         * atol + |rtol * G| (product and sum rounded separately, as torch
+         * forms them; a NaN allowance, from an infinite rtol times a zero
+         * golden value, admits nothing). */
+        for (int j = 0; j < nthr; ++j) {
+            double allowed = thr[j];
+            if (rthr) {
+                double rel = fabs(rthr[j] * G);
+                allowed = thr[j] + rel;
+            }
+            if (a != 0.0 && (isinf(a) || !(a <= allowed))) s.n_mismatch[j] += 1;
+        }
 
         /* Step 6: maxima, strict > in increasing index order (lowest index
          * wins ties). */

@@ -523,3 +523,42 @@ def test_inject_argument_validation():
     assert oracle.inject_rc(10, oracle.F32, 1, -1e-9, 1) == oracle.ERATE
     assert oracle.inject_rc(10, 9, 1, 0.5, 1) == oracle.EDTYPE
     assert oracle.inject_rc(0, oracle.F32, 1, 0.5, 1) == 0
+
+
+# ---------------------------------------------------------------------------
+# Closeness with a relative tolerance (torch.isclose with rtol > 0).
+# ---------------------------------------------------------------------------
+RTOL_SETS = [[(0.0, 1e-3)], [(1e-5, 1e-2), (0.0, 0.5), (1e-3, 0.0)], [(0.0, 2.0 ** -10), (2.0 ** -20, 2.0 ** -11)],
+             [(0.0, np.inf), (np.inf, 0.0), (1.0, 1e300)]]
+
+
+@pytest.mark.parametrize("tset", range(len(RTOL_SETS)))
+def test_mismatch_rtol_against_torch_isclose_f16_grid(tset):
+    tols = RTOL_SETS[tset]
+    t16 = X.all_f16().view(np.float16)             # every binary16 value, NaNs included
+    for gv in (0.0, 1.0, -3.5, 1e-4, 65504.0, -np.inf, np.nan):
+        G = np.full(t16.shape, gv, dtype=np.float16)
+        sig = oracle.signature(G, t16, thresholds=tols)
+        tg = torch.from_numpy(G.astype(np.float64))
+        tt = torch.from_numpy(t16.astype(np.float64))
+        want = [int((~torch.isclose(tt, tg, rtol=r, atol=a, equal_nan=False)).sum()) for a, r in tols]
+        assert sig["n_mismatch"] == want, (gv, tols)
+
+
+def test_mismatch_rtol_random_f32():
+    rng = np.random.default_rng(8)
+    G = (rng.standard_normal(200000) * 10.0 ** rng.integers(-6, 6, 200000)).astype(np.float32)
+    T = (G * (1 + rng.standard_normal(200000) * 10.0 ** rng.integers(-8, 0, 200000))).astype(np.float32)
+    T[::997] = -T[::997]
+    tols = [(1e-6, 1e-3), (0.0, 1e-5), (1e-9, 1e-7), (1e-3, 0.1)]
+    sig = oracle.signature(G, T, thresholds=tols)
+    tg = torch.from_numpy(G.astype(np.float64))
+    tt = torch.from_numpy(T.astype(np.float64))
+    assert sig["n_mismatch"] == [int((~torch.isclose(tt, tg, rtol=r, atol=a, equal_nan=False)).sum())
+                                 for a, r in tols]
+
+
+def test_rtol_validation():
+    g = np.zeros(4, np.float32)
+    assert oracle.signature_rc(g.ctypes.data, g.ctypes.data, 4, 0, (-40, 24, 64), [(1e-6, -1.0)]) == oracle.EINVAL
+    assert oracle.signature_rc(g.ctypes.data, g.ctypes.data, 4, 0, (-40, 24, 64), [(1e-6, float("nan"))]) == oracle.EINVAL
