@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define PEAT_ABI_VERSION 1
+#define PEAT_ABI_VERSION 2
 #define PEAT_MAX_THRESHOLDS 8
 #define PEAT_MAX_BINS 64
 
@@ -73,13 +73,18 @@ typedef struct {
     int32_t reserved; /* must be 0 */
 } peat_bins_t;
 
-/* Absolute tolerances theta_j >= 0 (not NaN; +Inf allowed), 0 <= count <= 8.
- * n_mismatch[j] counts pairs that torch.isclose(test, golden, rtol=0,
- * atol=theta_j, equal_nan=False) calls not close (Section III-A). */
+/* Closeness tests j < count (0 <= count <= 8), each an absolute tolerance
+ * abs_tol[j] and a relative tolerance rel_tol[j], both >= 0 and not NaN
+ * (+Inf allowed).  n_mismatch[j] counts the pairs that torch.isclose(test,
+ * golden, rtol=rel_tol[j], atol=abs_tol[j], equal_nan=False) calls not close
+ * (Section III-A): NaN pairs, and unequal pairs whose error is infinite or
+ * exceeds abs_tol[j] + |rel_tol[j] * G| (product and sum rounded
+ * separately).  rel_tol = 0 is the absolute test. */
 typedef struct {
     int32_t count;
     int32_t reserved; /* must be 0 */
     double abs_tol[PEAT_MAX_THRESHOLDS];
+    double rel_tol[PEAT_MAX_THRESHOLDS];
 } peat_thresholds_t;
 
 /* The error signature of one pair.  G_i, T_i are the values widened to

@@ -39,7 +39,7 @@ class Bins(ctypes.Structure):
 
 class Thresholds(ctypes.Structure):
     _fields_ = [("count", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("abs_tol", ctypes.c_double * MAX_THRESHOLDS)]
+                ("abs_tol", ctypes.c_double * MAX_THRESHOLDS), ("rel_tol", ctypes.c_double * MAX_THRESHOLDS)]
 
 
 _SIG_FIELDS = [
@@ -203,11 +203,16 @@ def make_bins(bins) -> Bins:
 
 
 def make_thresholds(thresholds) -> Thresholds:
+    """Absolute tolerances, or (abs_tol, rel_tol) pairs (torch.isclose's atol
+    and rtol)."""
     th = Thresholds()
     th.count = len(thresholds)
     th.reserved = 0
     for j, v in enumerate(list(thresholds)[:MAX_THRESHOLDS]):
-        th.abs_tol[j] = float(v)
+        if isinstance(v, (tuple, list)):
+            th.abs_tol[j], th.rel_tol[j] = float(v[0]), float(v[1])
+        else:
+            th.abs_tol[j] = float(v)
     return th
 
 

@@ -206,9 +206,12 @@ int check_bins_thr(const peat_bins_t *bins, const peat_thresholds_t *thr) {
         return fail(PEAT_EINVAL, "nbins must be in [1, 64] and divide hi_log2 - lo_log2 (got %d)", nb);
     if (thr->count < 0 || thr->count > PEAT_MAX_THRESHOLDS)
         return fail(PEAT_EINVAL, "threshold count must be in [0, 8] (got %d)", thr->count);
-    for (int j = 0; j < thr->count; ++j)
+    for (int j = 0; j < thr->count; ++j) {
         if (std::isnan(thr->abs_tol[j]) || thr->abs_tol[j] < 0)
             return fail(PEAT_EINVAL, "threshold %d must be >= 0 and not NaN", j);
+        if (std::isnan(thr->rel_tol[j]) || thr->rel_tol[j] < 0)
+            return fail(PEAT_EINVAL, "relative tolerance %d must be >= 0 and not NaN", j);
+    }
     return PEAT_OK;
 }
 
@@ -304,8 +307,12 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
     P.nthr = thr->count;
     P.nthr_pad = thr->count <= 2 ? 2 : (thr->count <= 4 ? 4 : 8);
     P.thr_min = HUGE_VAL;
+    P.any_rtol = 0;
+    P.pad = 0;
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) {
         P.thr[j] = j < thr->count ? thr->abs_tol[j] : HUGE_VAL;
+        P.rthr[j] = j < thr->count ? thr->rel_tol[j] : 0.0;
+        if (P.rthr[j] != 0.0) P.any_rtol = 1;
         if (P.thr[j] < P.thr_min) P.thr_min = P.thr[j];
     }
 

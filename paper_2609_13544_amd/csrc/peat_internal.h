@@ -66,8 +66,11 @@ struct SigParams {
     int32_t lo, hi, nbins;
     int32_t nthr;                  // real thresholds
     int32_t nthr_pad;              // 2, 4 or 8 compared per element (+Inf padding)
-    double thr[PEAT_MAX_THRESHOLDS];
+    double thr[PEAT_MAX_THRESHOLDS];   // absolute tolerances
+    double rthr[PEAT_MAX_THRESHOLDS];  // relative tolerances
     double thr_min;                // smallest thr (+Inf when there are none)
+    int32_t any_rtol;              // some relative tolerance is nonzero
+    int32_t pad;
 };
 
 struct InjDesc {                 // one per injected tensor (80 bytes)

@@ -203,8 +203,13 @@ __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParam
     }
     hist_add(sh, a, tid);
     const bool ainf = __builtin_isinf(a);
+    // not close under torch.isclose: unequal, and the error is infinite or not
+    // within atol + |rtol * G| (a NaN allowance admits nothing)
 #pragma unroll
-    for (int j = 0; j < NT; ++j) L.mism[j] += (a > P.thr[j]) || ainf;
+    for (int j = 0; j < NT; ++j) {
+        const double allowed = P.any_rtol ? __dadd_rn(P.thr[j], __builtin_fabs(__dmul_rn(P.rthr[j], G))) : P.thr[j];
+        L.mism[j] += (a != 0.0) && (ainf || !(a <= allowed));
+    }
     if (a > L.gx_abs || (a == L.gx_abs && li < L.gi_abs)) {
         L.gx_abs = a;
         L.gi_abs = li;
@@ -267,7 +272,7 @@ __device__ __forceinline__ uint32_t wave_max_uniform_u(uint32_t x) {
 // distance all land in one rarely taken branch, so the common path only
 // accumulates.  The histogram's row reads are all issued before its atomic
 // adds, so they share one LDS round trip.
-template <int DT, int NT>
+template <int DT, int NT, bool RT>
 __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
                                          const u32x4 &gv, const u32x4 &tv, uint32_t v, int tid) {
     constexpr int VEC = Tr<DT>::VEC;
@@ -364,7 +369,16 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
 #pragma unroll
-            for (int k = 0; k < NT; ++k) U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
+            for (int k = 0; k < NT; ++k) {
+                if constexpr (RT) {
+                    // torch.isclose's allowance atol + |rtol * G|, rounded step by
+                    // step (never NaN here: G is finite and nonzero)
+                    const double allowed = __dadd_rn(P.thr[k], __builtin_fabs(__dmul_rn(P.rthr[k], G[j])));
+                    U.mism[k] += wave_count(__builtin_fabs(E[j]) > allowed);
+                } else {
+                    U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
+                }
+            }
         }
     }
     U.common += 1;
@@ -413,7 +427,7 @@ __device__ __forceinline__ void lex_merge(V &v, uint32_t &ix, V ov, uint32_t oi)
     }
 }
 
-template <int DT, int NT>
+template <int DT, int NT, bool RT>
 __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int64_t cin, int64_t gchunk) {
     constexpr int VEC = Tr<DT>::VEC;
     constexpr int U = kUnroll<DT>;
@@ -478,7 +492,7 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t v = s * U + u;
-            if (vec_fast<DT, NT>(L, Un, sh, P, g[u], t[u], v, tid)) {
+            if (vec_fast<DT, NT, RT>(L, Un, sh, P, g[u], t[u], v, tid)) {
                 sh.defer[wave][ndef] = v;      // every lane writes the same value
                 ++ndef;
             }
@@ -657,12 +671,12 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
 }
 
 // Three blocks per CU (12 waves) where the registers allow it without
-// spilling in the hot loop: f32 with two thresholds, the common case.
-template <int DT, int NT>
-constexpr int chunk_blocks_per_cu() { return (DT == PEAT_F32 && NT == 2) ? 3 : 2; }
+// spilling in the hot loop: f32 with two absolute thresholds, the common case.
+template <int DT, int NT, bool RT>
+constexpr int chunk_blocks_per_cu() { return (DT == PEAT_F32 && NT == 2 && !RT) ? 3 : 2; }
 
-template <int DT, int NT>
-__global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DT, NT>())) sig_chunk(SigParams P) {
+template <int DT, int NT, bool RT>
+__global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DT, NT, RT>())) sig_chunk(SigParams P) {
     __shared__ Shared sh;
     const int64_t gchunk = P.chunk_base + blockIdx.x;
     const int pair = P.chunk_pair[gchunk];
@@ -686,7 +700,7 @@ __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DT, NT>())) sig_c
         sh.hrow[E] = (uint32_t)(slot * kHistCols);
     }
     __syncthreads();
-    chunk_body<DT, NT>(P, sh, d, cin, gchunk);
+    chunk_body<DT, NT, RT>(P, sh, d, cin, gchunk);
 }
 
 // ---- pass 2 ----------------------------------------------------------------
@@ -812,15 +826,20 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
 
 }  // namespace
 
-template <int DT>
-hipError_t launch_dtype(const SigParams &p, int64_t n, hipStream_t s) {
+template <int DT, bool RT>
+hipError_t launch_dtype_rt(const SigParams &p, int64_t n, hipStream_t s) {
     dim3 grid((unsigned)n), block(kBlock);
     switch (p.nthr_pad) {
-        case 2: hipLaunchKernelGGL((sig_chunk<DT, 2>), grid, block, 0, s, p); break;
-        case 4: hipLaunchKernelGGL((sig_chunk<DT, 4>), grid, block, 0, s, p); break;
-        default: hipLaunchKernelGGL((sig_chunk<DT, 8>), grid, block, 0, s, p); break;
+        case 2: hipLaunchKernelGGL((sig_chunk<DT, 2, RT>), grid, block, 0, s, p); break;
+        case 4: hipLaunchKernelGGL((sig_chunk<DT, 4, RT>), grid, block, 0, s, p); break;
+        default: hipLaunchKernelGGL((sig_chunk<DT, 8, RT>), grid, block, 0, s, p); break;
     }
     return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_dtype(const SigParams &p, int64_t n, hipStream_t s) {
+    return p.any_rtol ? launch_dtype_rt<DT, true>(p, n, s) : launch_dtype_rt<DT, false>(p, n, s);
 }
 
 hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[4], hipStream_t s) {

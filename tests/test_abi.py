@@ -44,7 +44,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(B.Pair) == 32
     assert ctypes.sizeof(B.InjectItem) == 48
     assert ctypes.sizeof(B.Bins) == 16
-    assert ctypes.sizeof(B.Thresholds) == 72
+    assert ctypes.sizeof(B.Thresholds) == 136
     assert B.Signature.max_abs.offset == 8 * (10 + 8 + 3 + 64)
     assert B.Signature.sum_gt.offset == 784 - 8
     assert ctypes.sizeof(B.TopK) == 48
@@ -52,7 +52,7 @@ def test_struct_layouts():
 
 def test_abi_version_and_strerror():
     L = P.lib()
-    assert L.peat_abi_version() == 1
+    assert L.peat_abi_version() == 2
     for code in range(0, -8, -1):
         assert L.peat_strerror(code)
     assert L.peat_strerror(-99) == b"unknown error code"
@@ -77,6 +77,13 @@ def test_signature_validation_codes():
     assert _sig_rc(bins_reserved=1) == B.EINVAL
     assert _sig_rc(thr=(math.nan,)) == B.EINVAL
     assert _sig_rc(thr=(-1e-9,)) == B.EINVAL
+    for bad in (math.nan, -1.0):                           # relative tolerances
+        th = B.Thresholds()
+        th.count = 1
+        th.rel_tol[0] = bad
+        b = B.Bins(-40, 24, 64, 0)
+        assert P.lib().peat_signature(None, None, 0, 0, ctypes.byref(b), ctypes.byref(th),
+                                      ctypes.byref(B.Signature())) == B.EINVAL
     th = B.Thresholds()
     th.count = 9
     b = B.Bins(-40, 24, 64, 0)

@@ -26,7 +26,9 @@ from tests.parity import (assert_parity, float_to_bits, oracle_sig, special_pair
 pytestmark = pytest.mark.gpu
 
 BINS_SETS = [synth.BINS, (-30, 20, 25), (-20, 40, 12), (-160, 136, 37)]
-THR_SETS = [synth.THRESHOLDS, (), (0.0,), (1e-7, 1e-5, 1e-3, 0.1, 1.0), (0.0, 1e-9, 1e-6, 1e-4, 1e-2, 1.0, 100.0, math.inf)]
+THR_SETS = [synth.THRESHOLDS, (), (0.0,), (1e-7, 1e-5, 1e-3, 0.1, 1.0), (0.0, 1e-9, 1e-6, 1e-4, 1e-2, 1.0, 100.0, math.inf),
+            # torch.isclose's relative form: (atol, rtol) pairs
+            ((1e-6, 1e-3), (0.0, 1e-5)), ((0.0, math.inf), (1e-3, 0.1), (1e-9, 2.0 ** -11), (0.0, 0.0))]
 
 
 def log(msg: str) -> None:
