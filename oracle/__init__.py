@@ -71,6 +71,10 @@ class _TopK(ctypes.Structure):
                 ("mean_topk", ctypes.c_double)]
 
 
+class _Series(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int64)] + [(k, ctypes.c_double) for k in ("mean", "var", "std", "min", "max")]
+
+
 class _Stats(ctypes.Structure):
     _fields_ = [(k, ctypes.c_double) for k in
                 ("mean_abs", "var_abs", "l2_err", "l2_g", "l2_t", "cos",
@@ -140,6 +144,13 @@ def lib():
                                                    ctypes.c_uint64, ctypes.POINTER(ctypes.c_int64)]
             L.oracle_cast_round.restype = ctypes.c_int
             L.oracle_cast_round.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]
+            L.oracle_series_stats.restype = ctypes.c_int
+            L.oracle_series_stats.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(_Series)]
+            L.oracle_spearman.restype = ctypes.c_int
+            L.oracle_spearman.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                          ctypes.POINTER(ctypes.c_double)]
+            L.oracle_normalize.restype = ctypes.c_int
+            L.oracle_normalize.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
             L.oracle_sizeof_sig.restype = ctypes.c_int
             assert L.oracle_sizeof_sig() == ctypes.sizeof(_Sig)
             L.oracle_sizeof_topk.restype = ctypes.c_int
@@ -341,3 +352,35 @@ def cast_round(x: np.ndarray, to_dtype: int) -> int:
     if x.dtype not in (np.float32, np.uint32) or not x.flags.c_contiguous or not x.flags.writeable:
         raise ValueError("cast_round needs a writeable C-contiguous f32 array")
     return int(lib().oracle_cast_round(x.ctypes.data if x.size else None, x.size, int(to_dtype)))
+
+
+def series_stats(x) -> dict:
+    """count, mean, sample var, std, min, max of the non-NaN entries."""
+    a = np.ascontiguousarray(x, dtype=np.float64)
+    out = _Series()
+    rc = lib().oracle_series_stats(a.ctypes.data if a.size else None, a.size, ctypes.byref(out))
+    if rc != OK:
+        raise ValueError(f"oracle_series_stats failed: {rc}")
+    return {k: (int(getattr(out, k)) if k == "count" else float(getattr(out, k))) for k, _ in _Series._fields_}
+
+
+def spearman(x, y) -> float:
+    a = np.ascontiguousarray(x, dtype=np.float64)
+    b = np.ascontiguousarray(y, dtype=np.float64)
+    rho = ctypes.c_double()
+    rc = lib().oracle_spearman(a.ctypes.data if a.size else None, b.ctypes.data if b.size else None, a.size,
+                               ctypes.byref(rho))
+    if rc != OK:
+        raise ValueError(f"oracle_spearman failed: {rc}")
+    return float(rho.value)
+
+
+def normalize(scores, units) -> np.ndarray:
+    a = np.ascontiguousarray(scores, dtype=np.float64)
+    b = np.ascontiguousarray(units, dtype=np.float64)
+    out = np.empty_like(a)
+    rc = lib().oracle_normalize(a.ctypes.data if a.size else None, b.ctypes.data if b.size else None, a.size,
+                                out.ctypes.data if a.size else None)
+    if rc != OK:
+        raise ValueError(f"oracle_normalize failed: {rc}")
+    return out

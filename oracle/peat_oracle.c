@@ -29,6 +29,12 @@
  *                     BF16) error, a round-to-nearest-even cast of an FP32
  *                     tensor.
  *
+ *   oracle_series_stats, oracle_spearman, oracle_normalize
+ *                     the Analyzer's statistics over score series (Section
+ *                     IV-C: model-wise (mean, std) of errors across epochs,
+ *                     Spearman rank correlation with model metrics; Section
+ *                     V-C: scores normalised by the FP64 error's score).
+ *
  *   oracle_topk       the "mean of the top 10% errors" score (Section IV-B,
  *                     FI Assessment Scores; the Analyzer's main score,
  *                     Section IV-C), for any fraction num/den: the errors of
@@ -678,5 +684,118 @@ int oracle_cast_round(void *x, int64_t n, int to_dtype) {
         }
         store_bits(x, i, ORACLE_F32, out);
     }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Analyzer statistics over score series (Section IV-C; Section V-C).        */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t count;   /* entries that are not NaN */
+    double mean;     /* their mean (NaN when count = 0) */
+    double var;      /* sample variance, divisor count - 1 (NaN when count < 2) */
+    double std;      /* sqrt(var) */
+    double min, max; /* NaN when count = 0 */
+} oracle_series_t;
+
+/* Mean, sample variance and range of the non-NaN entries of x[0..n): the
+ * (mu, sigma) pair of one operator's scores across epochs (Section IV-C). */
+int oracle_series_stats(const double *x, int64_t n, oracle_series_t *out) {
+    if (!out || n < 0 || (n > 0 && !x)) return ORACLE_EINVAL;
+    oracle_series_t r = {0, NAN, NAN, NAN, NAN, NAN};
+    csum_t acc = {0, 0};
+    for (int64_t i = 0; i < n; ++i) {
+        if (isnan(x[i])) continue;
+        if (r.count == 0 || x[i] < r.min) r.min = x[i];
+        if (r.count == 0 || x[i] > r.max) r.max = x[i];
+        csum_add(&acc, x[i]);
+        r.count += 1;
+    }
+    if (r.count > 0) r.mean = csum_value(&acc) / (double)r.count;
+    if (r.count > 1) {
+        /* second pass about the mean */
+        csum_t sq = {0, 0};
+        for (int64_t i = 0; i < n; ++i) {
+            if (isnan(x[i])) continue;
+            double d = x[i] - r.mean;
+            csum_add(&sq, d * d);
+        }
+        r.var = csum_value(&sq) / (double)(r.count - 1);
+        r.std = sqrt(r.var);
+    }
+    *out = r;
+    return ORACLE_OK;
+}
+
+/* out[i] = scores[i] / units[i]: a score in units of the FP64 error's score
+ * (Section V-C; IEEE division, so 0/0 gives NaN). */
+int oracle_normalize(const double *scores, const double *units, int64_t n, double *out) {
+    if (n < 0 || (n > 0 && (!scores || !units || !out))) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) out[i] = scores[i] / units[i];
+    return ORACLE_OK;
+}
+
+/* Average rank (1-based) of v among the m values w: 1 + #(w < v) plus half
+ * of the other values equal to v. */
+static double average_rank(const double *w, int64_t m, double v) {
+    int64_t less = 0, equal = 0;
+    for (int64_t j = 0; j < m; ++j) {
+        less += w[j] < v;
+        equal += w[j] == v;
+    }
+    return 1.0 + (double)less + (double)(equal - 1) / 2.0;
+}
+
+/* Spearman's rank correlation of the pairs (x[i], y[i]) with neither entry
+ * NaN (Section IV-C): the Pearson correlation of their average ranks.  NaN
+ * when fewer than two pairs remain or either rank vector is constant. */
+int oracle_spearman(const double *x, const double *y, int64_t n, double *rho) {
+    if (!rho || n < 0 || (n > 0 && (!x || !y))) return ORACLE_EINVAL;
+    double *xs = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    double *ys = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    if (!xs || !ys) {
+        free(xs);
+        free(ys);
+        return ORACLE_ENOMEM;
+    }
+    int64_t m = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (isnan(x[i]) || isnan(y[i])) continue;
+        xs[m] = x[i];
+        ys[m] = y[i];
+        ++m;
+    }
+    *rho = NAN;
+    if (m >= 2) {
+        double *rx = (double *)malloc(sizeof(double) * (size_t)m);
+        double *ry = (double *)malloc(sizeof(double) * (size_t)m);
+        if (!rx || !ry) {
+            free(rx);
+            free(ry);
+            free(xs);
+            free(ys);
+            return ORACLE_ENOMEM;
+        }
+        for (int64_t i = 0; i < m; ++i) {
+            rx[i] = average_rank(xs, m, xs[i]);
+            ry[i] = average_rank(ys, m, ys[i]);
+        }
+        /* Pearson correlation of the ranks (both rank vectors have mean (m+1)/2) */
+        double mean = (double)(m + 1) / 2.0;
+        csum_t sxy = {0, 0}, sxx = {0, 0}, syy = {0, 0};
+        for (int64_t i = 0; i < m; ++i) {
+            double dx = rx[i] - mean, dy = ry[i] - mean;
+            csum_add(&sxy, dx * dy);
+            csum_add(&sxx, dx * dx);
+            csum_add(&syy, dy * dy);
+        }
+        double vx = csum_value(&sxx), vy = csum_value(&syy);
+        if (vx > 0 && vy > 0) *rho = csum_value(&sxy) / sqrt(vx * vy);
+        free(rx);
+        free(ry);
+    }
+    free(xs);
+    free(ys);
     return ORACLE_OK;
 }
