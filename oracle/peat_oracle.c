@@ -157,7 +157,9 @@ static void csum_add(csum_t *acc, double x) {
     acc->s = t;
 }
 
-static double csum_value(const csum_t *acc) { return acc->s + acc->c; }
+/* An infinite or NaN running sum is the IEEE value of the whole sum: the
+ * compensation term only corrects rounding, and infinities turn it into NaN. */
+static double csum_value(const csum_t *acc) { return isfinite(acc->s) ? acc->s + acc->c : acc->s; }
 
 /* ------------------------------------------------------------------------- */
 /* The error signature.                                                      */

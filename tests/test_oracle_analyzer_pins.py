@@ -81,3 +81,15 @@ def test_normalize():
     u = np.array([4.0, 0.0, 0.0, -2.0, 2.0])
     got = oracle.normalize(s, u)
     assert got[0] == 0.25 and got[1] == np.inf and math.isnan(got[2]) and got[3] == -2.5 and got[4] == np.inf
+
+
+def test_series_stats_infinite_entries_follow_ieee_sum():
+    # the mean is the IEEE sum over the count: one +inf makes it +inf, +inf
+    # and -inf together make it NaN; the deviations are then undefined (NaN)
+    r = oracle.series_stats([1.0, math.inf, 2.0])
+    assert r["count"] == 3 and r["mean"] == math.inf and r["max"] == math.inf
+    assert math.isnan(r["var"]) and math.isnan(r["std"])
+    r = oracle.series_stats([-math.inf, 4.0])
+    assert r["mean"] == -math.inf and r["min"] == -math.inf
+    r = oracle.series_stats([math.inf, -math.inf, 0.0])
+    assert math.isnan(r["mean"])
