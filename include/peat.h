@@ -280,6 +280,27 @@ int peat_inject_batched_async(const peat_inject_item_t *items, int32_t count,
  * PEAT_EINVAL for bad sizes, alignment or NULL pointers. */
 int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream);
 
+/* Analyzer statistics over a series of scores (host memory in and out):
+ * count of the non-NaN entries, their mean, sample variance (divisor
+ * count - 1) and standard deviation, minimum and maximum -- the (mu, sigma)
+ * of one operator's scores across epochs (Section IV-C) and the Detector's
+ * ranges.  Fields without enough entries are NaN. */
+typedef struct {
+    int64_t count;
+    double mean, var, std, min, max;
+} peat_series_t;
+int peat_series_stats(const double *x, int64_t n, peat_series_t *out);
+
+/* Spearman's rank correlation of the pairs (x[i], y[i]) with no NaN: the
+ * Pearson correlation of average ranks (ties share the mean rank), as the
+ * Analyzer correlates scores with model metrics (Section IV-C).  *rho is NaN
+ * for fewer than two pairs or constant ranks.  Host memory. */
+int peat_spearman(const double *x, const double *y, int64_t n, double *rho);
+
+/* out[i] = scores[i] / units[i]: scores in units of the FP64 error's score
+ * (Section V-C), IEEE division.  Host memory. */
+int peat_normalize_scores(const double *scores, const double *units, int64_t n, double *out);
+
 /* Host-side derived scores of a signature (host memory in and out). */
 int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
 

@@ -9,5 +9,5 @@ from ._binding import (  # noqa: F401
     SIG_NP_DTYPE, STREAM_SPAN, cast_round, corrupt_positions, inject_model, PeatError, PreparedItems, PreparedPairs, decode_records, dtype_code,
     finalize_stats, inject, inject_batched, inject_batched_async, lib, profile_enable,
     profile_read, set_stream, signature, signature_batched, signature_batched_async, stream_read,
-    strerror, topk_mean, topk_mean_batched,
+    strerror, topk_mean, topk_mean_batched, series_stats, spearman, normalize_scores,
 )

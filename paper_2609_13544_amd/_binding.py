@@ -72,6 +72,10 @@ class TopK(ctypes.Structure):
                 ("kth_value", ctypes.c_double), ("sum_topk", ctypes.c_double), ("mean_topk", ctypes.c_double)]
 
 
+class Series(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int64)] + [(k, ctypes.c_double) for k in ("mean", "var", "std", "min", "max")]
+
+
 class Pair(ctypes.Structure):
     _fields_ = [("golden", ctypes.c_void_p), ("test", ctypes.c_void_p), ("n", ctypes.c_int64),
                 ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
@@ -138,6 +142,10 @@ _PROTOS = {
                                               ctypes.c_int32, ctypes.POINTER(TopK)]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
+    "peat_series_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(Series)]),
+    "peat_spearman": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                     ctypes.POINTER(ctypes.c_double)]),
+    "peat_normalize_scores": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
     "peat_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "peat_profile_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_int64)]),
@@ -483,6 +491,39 @@ def stream_read(buf, d_sink, stream=None) -> None:
         raise ValueError("d_sink needs one 32-bit word per 2 MiB span")
     _check(lib().peat_stream_read(buf.data_ptr(), nbytes, d_sink.data_ptr(), _stream_ptr(stream)),
            "peat_stream_read")
+
+
+def series_stats(x) -> dict:
+    """peat_series_stats over a sequence of scores (host)."""
+    a = np.ascontiguousarray(x, dtype=np.float64)
+    out = Series()
+    _check(lib().peat_series_stats(a.ctypes.data if a.size else None, a.size, ctypes.byref(out)),
+           "peat_series_stats")
+    return {k: (int(getattr(out, k)) if k == "count" else float(getattr(out, k))) for k, _ in Series._fields_}
+
+
+def spearman(x, y) -> float:
+    """peat_spearman of two equal-length sequences (host)."""
+    a = np.ascontiguousarray(x, dtype=np.float64)
+    b = np.ascontiguousarray(y, dtype=np.float64)
+    if a.size != b.size:
+        raise ValueError("x and y differ in length")
+    rho = ctypes.c_double()
+    _check(lib().peat_spearman(a.ctypes.data if a.size else None, b.ctypes.data if b.size else None, a.size,
+                               ctypes.byref(rho)), "peat_spearman")
+    return float(rho.value)
+
+
+def normalize_scores(scores, units) -> np.ndarray:
+    """peat_normalize_scores: scores in units of the FP64 error's score."""
+    a = np.ascontiguousarray(scores, dtype=np.float64)
+    b = np.ascontiguousarray(units, dtype=np.float64)
+    if a.size != b.size:
+        raise ValueError("scores and units differ in length")
+    out = np.empty_like(a)
+    _check(lib().peat_normalize_scores(a.ctypes.data if a.size else None, b.ctypes.data if b.size else None,
+                                       a.size, out.ctypes.data if a.size else None), "peat_normalize_scores")
+    return out
 
 
 def profile_enable(on: bool = True) -> None:
