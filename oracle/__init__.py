@@ -36,7 +36,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "peat_oracle.c")
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
-F32, F16, BF16 = 0, 1, 2
+F32, F16, BF16, F64 = 0, 1, 2, 3
 _DTYPE_CODE = {np.dtype(np.float32): F32, np.dtype(np.float16): F16}
 
 OK, EINVAL, EDTYPE, EBITMASK, ERATE, ENOMEM = 0, -1, -2, -3, -4, -6
@@ -116,6 +116,14 @@ def lib():
                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
                 ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_Sig)]
+            L.oracle_signature_mixed.restype = ctypes.c_int
+            L.oracle_signature_mixed.argtypes = [
+                ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_Sig)]
+            L.oracle_topk_mixed.restype = ctypes.c_int
+            L.oracle_topk_mixed.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                            ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_TopK)]
             L.oracle_stats.restype = ctypes.c_int
             L.oracle_stats.argtypes = [ctypes.POINTER(_Sig), ctypes.POINTER(_Stats)]
             L.oracle_philox4x64_10.restype = None
@@ -224,6 +232,58 @@ def signature(golden: np.ndarray, test: np.ndarray, *, dtype: int | None = None,
     if raw:
         return out
     return _sig_to_dict(out, len(thresholds))
+
+
+def _mixed_code(arr: np.ndarray, dtype_code: int | None) -> int:
+    if dtype_code is None and arr.dtype == np.float64:
+        return F64
+    return _code(arr, dtype_code)
+
+
+def signature_mixed(golden: np.ndarray, test: np.ndarray, *, gdtype: int | None = None,
+                    tdtype: int | None = None, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> dict:
+    """Signature of a pair whose golden and test types may differ (float64 is
+    the test side's binary64; uint16 bit patterns need an explicit code)."""
+    g = np.ascontiguousarray(golden).reshape(-1)
+    t = np.ascontiguousarray(test).reshape(-1)
+    if g.shape != t.shape:
+        raise ValueError("golden and test must have the same shape")
+    gc, tc = _mixed_code(g, gdtype), _mixed_code(t, tdtype)
+    atol, rtol = split_thresholds(thresholds)
+    thr = (ctypes.c_double * 8)(*atol)
+    rthr = (ctypes.c_double * 8)(*rtol)
+    out = _Sig()
+    rc = lib().oracle_signature_mixed(
+        g.ctypes.data if g.size else None, gc, t.ctypes.data if t.size else None, tc,
+        g.size, int(bins[0]), int(bins[1]), int(bins[2]), len(thresholds), thr, rthr, ctypes.byref(out))
+    if rc != OK:
+        raise ValueError(f"oracle_signature_mixed failed: {rc}")
+    return _sig_to_dict(out, len(thresholds))
+
+
+def signature_mixed_rc(gcode: int, tcode: int, n: int = 4) -> int:
+    """Return code of oracle_signature_mixed on zero-filled buffers."""
+    buf = np.zeros(max(int(n), 1) * 8, dtype=np.uint8)
+    thr = (ctypes.c_double * 8)()
+    out = _Sig()
+    return int(lib().oracle_signature_mixed(buf.ctypes.data, gcode, buf.ctypes.data, tcode, int(n),
+                                            -40, 24, 64, 0, thr, None, ctypes.byref(out)))
+
+
+def topk_mixed(golden: np.ndarray, test: np.ndarray, *, gdtype: int | None = None,
+               tdtype: int | None = None, num: int = 1, den: int = 10) -> dict:
+    g = np.ascontiguousarray(golden).reshape(-1)
+    t = np.ascontiguousarray(test).reshape(-1)
+    if g.shape != t.shape:
+        raise ValueError("golden and test must have the same shape")
+    out = _TopK()
+    rc = lib().oracle_topk_mixed(g.ctypes.data if g.size else None, _mixed_code(g, gdtype),
+                                 t.ctypes.data if t.size else None, _mixed_code(t, tdtype),
+                                 g.size, int(num), int(den), ctypes.byref(out))
+    if rc != OK:
+        raise ValueError(f"oracle_topk_mixed failed: {rc}")
+    return {k: (float(getattr(out, k)) if k in ("kth_value", "sum_topk", "mean_topk") else int(getattr(out, k)))
+            for k, _ in _TopK._fields_}
 
 
 def signature_rc(golden_ptr, test_ptr, n, code, bins, thresholds) -> int:

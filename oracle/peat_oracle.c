@@ -35,6 +35,12 @@
  *                     Spearman rank correlation with model metrics; Section
  *                     V-C: scores normalised by the FP64 error's score).
  *
+ *   oracle_signature_mixed, oracle_topk_mixed
+ *                     the same two definitions for a golden and a test of
+ *                     different precision (Section III-C: Err(FP16, FP32),
+ *                     the FP32-FP64 error); the ULP distance of such a pair
+ *                     is counted in the narrower format.
+ *
  *   oracle_topk       the "mean of the top 10% errors" score (Section IV-B,
  *                     FI Assessment Scores; the Analyzer's main score,
  *                     Section IV-C), for any fraction num/den: the errors of
@@ -61,6 +67,7 @@
 #define ORACLE_F32 0
 #define ORACLE_F16 1
 #define ORACLE_BF16 2
+#define ORACLE_F64 3   /* test side of a mixed-precision pair only */
 
 #define ORACLE_OK 0
 #define ORACLE_EINVAL (-1)
@@ -142,6 +149,67 @@ static int64_t ulp_key(uint32_t bits, int width) {
     return (bits & sign_bit) ? -mag : mag;
 }
 
+/* ---- mixed-precision pairs (Section III-C: an FP32 golden output against
+ * the output of the same operation in FP16 or in FP64) ------------------- */
+
+/* Value of element i of any supported type, exactly as a binary64. */
+static double element_value_any(const void *base, int64_t i, int dtype) {
+    if (dtype == ORACLE_F64) {
+        double d;
+        memcpy(&d, (const unsigned char *)base + 8 * i, 8);
+        return d;
+    }
+    return element_value(element_bits(base, i, dtype), dtype);
+}
+
+/* Precision p (significand bits, implicit bit included) and the normal
+ * exponent range [emin, emax] of each type. */
+static void format_params(int dtype, int *p, int *emin, int *emax) {
+    switch (dtype) {
+        case ORACLE_F16: *p = 11; *emin = -14; *emax = 15; break;
+        case ORACLE_BF16: *p = 8; *emin = -126; *emax = 127; break;
+        case ORACLE_F64: *p = 53; *emin = -1022; *emax = 1023; break;
+        default: *p = 24; *emin = -126; *emax = 127; break;
+    }
+}
+
+/* Golden and test types that a signature accepts: the golden is FP32, FP16
+ * or BF16 (the golden kernel is never the binary64 one); the test may also be
+ * binary64; and one format must contain the other (precision and both
+ * exponent limits), which excludes FP16 against BF16. */
+static int pair_types_ok(int gdt, int tdt) {
+    if (!dtype_width(gdt)) return 0;
+    if (!dtype_width(tdt) && tdt != ORACLE_F64) return 0;
+    int pg, ming, maxg, pt, mint, maxt;
+    format_params(gdt, &pg, &ming, &maxg);
+    format_params(tdt, &pt, &mint, &maxt);
+    int g_in_t = pg <= pt && ming >= mint && maxg <= maxt;
+    int t_in_g = pt <= pg && mint >= ming && maxt <= maxg;
+    return g_in_t || t_in_g;
+}
+
+/* Position of a value of a format in the ordered list of that format's
+ * non-negative values (0, the subnormals, the normals, then Inf), negated for
+ * a negative value; v is exactly representable in the format, or infinite.
+ * For a value decoded from a bit pattern this is the signed-magnitude key of
+ * the pattern. */
+static int64_t format_index(double v, int p, int emin, int emax) {
+    double a = fabs(v);
+    int64_t idx;
+    if (isinf(a)) {
+        idx = (int64_t)(emax - emin + 2) << (p - 1);
+    } else if (a < ldexp(1.0, emin)) {
+        idx = (int64_t)(a / ldexp(1.0, emin - p + 1));       /* subnormal: multiple of the quantum */
+    } else {
+        int e;
+        frexp(a, &e);
+        int E = e - 1;                                       /* a in [2^E, 2^(E+1)) */
+        int64_t m = (int64_t)(a / ldexp(1.0, E - p + 1));    /* significand in [2^(p-1), 2^p) */
+        idx = ((int64_t)(E - emin) << (p - 1)) + m;
+    }
+    return v < 0 ? -idx : idx;
+}
+
 /* ------------------------------------------------------------------------- */
 /* Neumaier compensated summation.                                           */
 /* ------------------------------------------------------------------------- */
@@ -181,6 +249,11 @@ static int check_params(int lo, int hi, int nbins, int nthr, const double *thr, 
     return ORACLE_OK;
 }
 
+static double round_to_format(double v, int p, int emin, int emax);
+
+int oracle_signature_mixed(const void *golden, int gdt, const void *test, int tdt, int64_t n,
+                           int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr,
+                           oracle_sig_t *out);
 int oracle_signature_rtol(const void *golden, const void *test, int64_t n, int dtype,
                           int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr,
                           oracle_sig_t *out);
@@ -197,8 +270,30 @@ int oracle_signature(const void *golden, const void *test, int64_t n, int dtype,
 int oracle_signature_rtol(const void *golden, const void *test, int64_t n, int dtype,
                           int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr,
                           oracle_sig_t *out) {
-    int width = dtype_width(dtype);
-    if (!width) return ORACLE_EDTYPE;
+    if (!dtype_width(dtype)) return ORACLE_EDTYPE;
+    return oracle_signature_mixed(golden, dtype, test, dtype, n, lo, hi, nbins, nthr, thr, rthr, out);
+}
+
+/* The signature of a pair whose golden and test types may differ (Section
+ * III-C: Err(FP16, FP32) and the FP32-FP64 error).  Both values are taken
+ * exactly as binary64 and every field keeps its definition, except the ULP
+ * distance of a mixed pair, which is counted in the narrower format: the
+ * wider value is first rounded to it (nearest, ties to even, Inf beyond its
+ * range). */
+int oracle_signature_mixed(const void *golden, int gdt, const void *test, int tdt, int64_t n,
+                           int lo, int hi, int nbins, int nthr, const double *thr, const double *rthr,
+                           oracle_sig_t *out) {
+    if (!pair_types_ok(gdt, tdt)) return ORACLE_EDTYPE;
+    int width = dtype_width(gdt);
+    int mixed = gdt != tdt;
+    int np_, nemin, nemax;           /* the narrower format of a mixed pair */
+    {
+        int pg, ming, maxg, pt, mint, maxt;
+        format_params(gdt, &pg, &ming, &maxg);
+        format_params(tdt, &pt, &mint, &maxt);
+        if (pg <= pt) { np_ = pg; nemin = ming; nemax = maxg; }
+        else { np_ = pt; nemin = mint; nemax = maxt; }
+    }
     if (!out || n < 0 || (n > 0 && (!golden || !test))) return ORACLE_EINVAL;
     int rc = check_params(lo, hi, nbins, nthr, thr, rthr);
     if (rc) return rc;
@@ -216,10 +311,8 @@ int oracle_signature_rtol(const void *golden, const void *test, int64_t n, int d
     csum_t c_g2 = {0, 0}, c_t2 = {0, 0}, c_gt = {0, 0};
 
     for (int64_t i = 0; i < n; ++i) {
-        uint32_t gb = element_bits(golden, i, dtype);
-        uint32_t tb = element_bits(test, i, dtype);
-        double G = element_value(gb, dtype);
-        double T = element_value(tb, dtype);
+        double G = element_value_any(golden, i, gdt);
+        double T = element_value_any(test, i, tdt);
 
         /* Step 1: classify.  A pair with a NaN on either side is excluded
          * from everything except the NaN counts and the mismatch counts. */
@@ -243,8 +336,15 @@ int oracle_signature_rtol(const void *golden, const void *test, int64_t n, int d
          * is +Inf when exactly one side is infinite or the infinities differ. */
         double a = (G == T) ? 0.0 : fabs(T - G);
 
-        /* Step 3: ULP distance from the bit patterns. */
-        int64_t ku = ulp_key(tb, width) - ulp_key(gb, width);
+        /* Step 3: ULP distance from the bit patterns; for a mixed pair,
+         * between the positions of the two values in the narrower format. */
+        int64_t ku;
+        if (!mixed) {
+            ku = ulp_key(element_bits(test, i, tdt), width) - ulp_key(element_bits(golden, i, gdt), width);
+        } else {
+            ku = format_index(round_to_format(T, np_, nemin, nemax), np_, nemin, nemax) -
+                 format_index(round_to_format(G, np_, nemin, nemax), np_, nemin, nemax);
+        }
         int64_t ulp = ku < 0 ? -ku : ku;
         s.sum_ulp += (uint64_t)ulp;
 
@@ -498,9 +598,20 @@ static int cmp_desc(const void *x, const void *y) {
     return (a < b) - (a > b);
 }
 
+int oracle_topk_mixed(const void *golden, int gdt, const void *test, int tdt, int64_t n, int num,
+                      int den, oracle_topk_t *out);
+
 int oracle_topk(const void *golden, const void *test, int64_t n, int dtype, int num, int den,
                 oracle_topk_t *out) {
     if (!dtype_width(dtype)) return ORACLE_EDTYPE;
+    return oracle_topk_mixed(golden, dtype, test, dtype, n, num, den, out);
+}
+
+/* The same score for a pair whose golden and test types may differ (the
+ * type rules of oracle_signature_mixed). */
+int oracle_topk_mixed(const void *golden, int gdt, const void *test, int tdt, int64_t n, int num,
+                      int den, oracle_topk_t *out) {
+    if (!pair_types_ok(gdt, tdt)) return ORACLE_EDTYPE;
     if (!out || n < 0 || (n > 0 && (!golden || !test))) return ORACLE_EINVAL;
     if (num < 1 || den < num) return ORACLE_EINVAL;
 
@@ -509,8 +620,8 @@ int oracle_topk(const void *golden, const void *test, int64_t n, int dtype, int 
     if (!a) return ORACLE_ENOMEM;
     int64_t m = 0;
     for (int64_t i = 0; i < n; ++i) {
-        double G = element_value(element_bits(golden, i, dtype), dtype);
-        double T = element_value(element_bits(test, i, dtype), dtype);
+        double G = element_value_any(golden, i, gdt);
+        double T = element_value_any(test, i, tdt);
         if (isnan(G) || isnan(T)) continue;
         a[m++] = (G == T) ? 0.0 : fabs(T - G);
     }
