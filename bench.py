@@ -42,7 +42,7 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "GB/s of golden+test tensor bytes signed (fraction of HBM peak), 1 MI355X"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_13544_amd", "csrc", f)
-                  for f in ("signature.hip", "elements.h", "peat_internal.h")]
+                  for f in ("sig_chunk.h", "signature.hip", "elements.h", "peat_internal.h")]
 
 
 def log(*a):

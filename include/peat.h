@@ -32,7 +32,8 @@
  *     Calls from several host threads are serialised by an internal mutex;
  *     work on different streams is ordered through an event on the workspace.
  *   - Element types: PEAT_F32 (IEEE binary32), PEAT_F16 (IEEE binary16),
- *     PEAT_BF16 (bfloat16).  Values are widened exactly to binary64; all
+ *     PEAT_BF16 (bfloat16), and PEAT_F64 (IEEE binary64) as the test side of a
+ *     mixed-precision pair.  Values are widened exactly to binary64; all
  *     error arithmetic is IEEE binary64 round-to-nearest-even, subnormals kept.
  */
 #ifndef PEAT_H
@@ -44,11 +45,12 @@
 extern "C" {
 #endif
 
-#define PEAT_ABI_VERSION 2
+#define PEAT_ABI_VERSION 3
 #define PEAT_MAX_THRESHOLDS 8
 #define PEAT_MAX_BINS 64
 
-typedef enum { PEAT_F32 = 0, PEAT_F16 = 1, PEAT_BF16 = 2 } peat_dtype_t;
+/* PEAT_F64 is accepted only as the test type of a mixed-precision pair. */
+typedef enum { PEAT_F32 = 0, PEAT_F16 = 1, PEAT_BF16 = 2, PEAT_F64 = 3 } peat_dtype_t;
 
 enum {
     PEAT_OK = 0,
@@ -144,6 +146,20 @@ typedef struct {
     int32_t reserved;   /* must be 0      */
 } peat_pair_t;
 
+/* A pair whose golden and test types may differ (Section III-C: an FP32
+ * golden output against the same operation run in FP16, or in FP64 for the
+ * FP32-FP64 "error unit").  golden_dtype is PEAT_F32, PEAT_F16 or PEAT_BF16;
+ * test_dtype may also be PEAT_F64; one format must contain the other
+ * (PEAT_F16 with PEAT_BF16 is PEAT_EDTYPE).  Equal types are allowed.  Each
+ * pointer must be aligned to its element size (PEAT_EINVAL otherwise). */
+typedef struct {
+    const void *golden; /* device pointer */
+    const void *test;   /* device pointer */
+    int64_t n;          /* elements of each, >= 0 */
+    int32_t golden_dtype;
+    int32_t test_dtype;
+} peat_mixed_pair_t;
+
 /* Error models (Section II-B "Error Models"; Section III-C pseudo-errors). */
 typedef enum {
     PEAT_MODEL_BITFLIP = 0, /* toggle one bit of the mask (random bit flip)      */
@@ -203,6 +219,23 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
                                  const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                                  peat_signature_t *d_outs, void *stream);
 
+/* Signature of a mixed-precision pair (Section III-C; types as in
+ * peat_mixed_pair_t).  Every field keeps its definition over the exact
+ * binary64 values of both sides, except the ULP distance, which is counted
+ * in the narrower format after rounding the wider value to it (nearest, ties
+ * to even, Inf beyond its range).  With equal types the record equals
+ * peat_signature's.  out is host memory; the call waits for it. */
+int peat_signature_mixed(const void *golden, int32_t golden_dtype, const void *test,
+                         int32_t test_dtype, int64_t n, const peat_bins_t *bins,
+                         const peat_thresholds_t *thresholds, peat_signature_t *out);
+
+/* peat_signature_mixed over count >= 0 pairs of any accepted type
+ * combination in one launch sequence; outs is a host array of count records,
+ * each bit-identical to the single call's. */
+int peat_signature_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count,
+                                 const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                                 peat_signature_t *outs);
+
 /* Mean of the k largest errors of one pair, k = ceil(n_valid * num / den)
  * (num = 1, den = 10: the paper's top-10% mean); out is host memory.
  * 1 <= num <= den <= 2^20.  Exact selection: n_valid, k, count_above and
@@ -217,6 +250,11 @@ int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t
  * host array of count records, each bit-identical to the single call's. */
 int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
                            peat_topk_t *outs);
+
+/* peat_topk_mean_batched over mixed-precision pairs (types as in
+ * peat_mixed_pair_t; the error is |T - G| of the exact binary64 values). */
+int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
+                                 int32_t den, peat_topk_t *outs);
 
 /* Random bit flip in place (Section II-B).  Element i flips iff its 64-bit
  * uniform U_i < floor(rate * 2^64) (every element if rate >= 1).  U_i's top

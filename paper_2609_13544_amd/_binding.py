@@ -16,7 +16,7 @@ import numpy as np
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libpeat.so")
 
-F32, F16, BF16 = 0, 1, 2
+F32, F16, BF16, F64 = 0, 1, 2, 3
 MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN = 0, 1, 2, 3
 MAX_POSITIONS = 4096
 OK, EINVAL, EDTYPE, EBITMASK, ERATE, EHIP, ENOMEM, ENODEV = 0, -1, -2, -3, -4, -5, -6, -7
@@ -81,6 +81,11 @@ class Pair(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class MixedPair(ctypes.Structure):
+    _fields_ = [("golden", ctypes.c_void_p), ("test", ctypes.c_void_p), ("n", ctypes.c_int64),
+                ("golden_dtype", ctypes.c_int32), ("test_dtype", ctypes.c_int32)]
+
+
 class InjectItem(ctypes.Structure):
     _fields_ = [("tensor", ctypes.c_void_p), ("n", ctypes.c_int64), ("dtype", ctypes.c_int32),
                 ("model", ctypes.c_int32), ("seed", ctypes.c_uint64), ("rate", ctypes.c_double),
@@ -140,6 +145,14 @@ _PROTOS = {
                                       ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(TopK)]),
     "peat_topk_mean_batched": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_int32, ctypes.POINTER(TopK)]),
+    "peat_signature_mixed": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                            ctypes.c_int64, ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
+                                            ctypes.POINTER(Signature)]),
+    "peat_signature_mixed_batched": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32,
+                                                    ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
+                                                    ctypes.POINTER(Signature)]),
+    "peat_topk_mean_mixed_batched": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32, ctypes.c_int32,
+                                                    ctypes.c_int32, ctypes.POINTER(TopK)]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
     "peat_series_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(Series)]),
@@ -192,7 +205,7 @@ def _torch():
 
 def dtype_code(t) -> int:
     torch = _torch()
-    m = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+    m = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16, torch.float64: F64}
     if t.dtype not in m:
         raise TypeError(f"unsupported dtype {t.dtype}")
     return m[t.dtype]
@@ -314,6 +327,61 @@ def signature_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> lis
     _check(lib().peat_signature_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
            "peat_signature_batched")
     return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+
+
+def signature_mixed(golden, test, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> dict:
+    """peat_signature_mixed on two device tensors of the same element count
+    whose types may differ (e.g. a float32 golden and a float64 or float16 test)."""
+    _dev_tensor(golden, "golden")
+    _dev_tensor(test, "test")
+    if golden.numel() != test.numel():
+        raise ValueError("golden and test differ in size")
+    n = golden.numel()
+    out = Signature()
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    set_stream()
+    _check(lib().peat_signature_mixed(golden.data_ptr() if n else None, dtype_code(golden),
+                                      test.data_ptr() if n else None, dtype_code(test), n,
+                                      ctypes.byref(b), ctypes.byref(th), ctypes.byref(out)),
+           "peat_signature_mixed")
+    return sig_to_dict(out, nthr=len(thresholds))
+
+
+def _mixed_pairs_array(pairs):
+    arr = (MixedPair * max(1, len(pairs)))()
+    for k, p in enumerate(pairs):
+        if isinstance(p, MixedPair):
+            arr[k] = p
+            continue
+        g, t = p[0], p[1]
+        _dev_tensor(g, f"pairs[{k}].golden")
+        _dev_tensor(t, f"pairs[{k}].test")
+        if g.numel() != t.numel():
+            raise ValueError(f"pair {k}: golden and test differ in size")
+        arr[k] = MixedPair(g.data_ptr(), t.data_ptr(), g.numel(), dtype_code(g), dtype_code(t))
+    return arr
+
+
+def signature_mixed_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> list[dict]:
+    """peat_signature_mixed_batched over (golden, test) device tensor pairs of
+    any accepted type combination."""
+    arr = _mixed_pairs_array(pairs)
+    outs = (Signature * max(1, len(pairs)))()
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    set_stream()
+    _check(lib().peat_signature_mixed_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
+           "peat_signature_mixed_batched")
+    return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+
+
+def topk_mean_mixed_batched(pairs, num: int = 1, den: int = 10) -> list[dict]:
+    """peat_topk_mean_mixed_batched over (golden, test) device tensor pairs of
+    any accepted type combination."""
+    arr = _mixed_pairs_array(pairs)
+    outs = (TopK * max(1, len(pairs)))()
+    set_stream()
+    _check(lib().peat_topk_mean_mixed_batched(arr, len(pairs), num, den, outs), "peat_topk_mean_mixed_batched")
+    return [topk_to_dict(outs[k]) for k in range(len(pairs))]
 
 
 def topk_to_dict(t: TopK) -> dict:

@@ -12,7 +12,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libpeat.so")
-SOURCES = ["signature.hip", "inject.hip", "stream_read.hip", "topk.hip", "models.hip", "analyzer.hip", "api.hip"]
+SOURCES = ["signature.hip", "mixed.hip", "inject.hip", "stream_read.hip", "topk.hip", "models.hip", "analyzer.hip", "api.hip"]
 BUILD_DIR = os.path.join(PKG, "_build")
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")

@@ -224,22 +224,50 @@ int check_pair(const peat_pair_t &p, int k) {
     return PEAT_OK;
 }
 
-// Partition every pair into chunks; the chunks of each element type get one
-// contiguous range [range[dt], range[dt + 1]) of the global numbering (one
-// launch per type).
-int build_descs(const peat_pair_t *pairs, int32_t count, std::vector<SigDesc> &descs, int64_t range[4],
-                int64_t *total_out) {
+int check_mixed(const peat_mixed_pair_t &p, int k) {
+    if (pair_kind(p.golden_dtype, p.test_dtype) < 0)
+        return fail(PEAT_EDTYPE, "pair %d: golden/test types %d/%d not accepted", k, p.golden_dtype, p.test_dtype);
+    if (p.n < 0) return fail(PEAT_EINVAL, "pair %d: n < 0", k);
+    if (p.n > 0 && (!p.golden || !p.test)) return fail(PEAT_EINVAL, "pair %d: NULL tensor with n > 0", k);
+    if (p.n > (int64_t(1) << 46)) return fail(PEAT_EINVAL, "pair %d: n above 2^46", k);
+    if ((reinterpret_cast<uintptr_t>(p.golden) % elem_bytes(p.golden_dtype)) != 0 ||
+        (reinterpret_cast<uintptr_t>(p.test) % elem_bytes(p.test_dtype)) != 0)
+        return fail(PEAT_EINVAL, "pair %d: a tensor is not aligned to its element size", k);
+    return PEAT_OK;
+}
+
+// Same-type pairs, validated, as mixed pairs of equal types.
+int same_type_pairs(const peat_pair_t *pairs, int32_t count, std::vector<peat_mixed_pair_t> &out) {
+    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
+    if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
+    int rc;
+    for (int k = 0; k < count; ++k)
+        if ((rc = check_pair(pairs[k], k))) return rc;
+    out.resize((size_t)count);
+    for (int k = 0; k < count; ++k)
+        out[k] = peat_mixed_pair_t{pairs[k].golden, pairs[k].test, pairs[k].n, pairs[k].dtype, pairs[k].dtype};
+    return PEAT_OK;
+}
+
+// Partition every pair into chunks; the chunks of each kind (golden/test
+// type combination) get one contiguous range [range[kind], range[kind + 1])
+// of the global numbering (one launch per kind).
+int build_descs(const peat_mixed_pair_t *pairs, int32_t count, std::vector<SigDesc> &descs,
+                int64_t range[kKinds + 1], int64_t *total_out) {
     descs.assign((size_t)count, SigDesc{});
+    std::vector<int> kinds((size_t)count);
+    for (int k = 0; k < count; ++k) kinds[k] = pair_kind(pairs[k].golden_dtype, pairs[k].test_dtype);
     int64_t total = 0;
-    for (int dt = 0; dt < 3; ++dt) {
-        range[dt] = total;
+    for (int kind = 0; kind < kKinds; ++kind) {
+        range[kind] = total;
         for (int k = 0; k < count; ++k) {
-            if (pairs[k].dtype != dt) continue;
+            if (kinds[k] != kind) continue;
             SigDesc &sd = descs[k];
             sd.g = pairs[k].golden;
             sd.t = pairs[k].test;
             sd.n = pairs[k].n;
-            sd.dtype = pairs[k].dtype;
+            sd.dtype = (int16_t)pairs[k].golden_dtype;
+            sd.tdtype = (int16_t)pairs[k].test_dtype;
             sd.chunk_log2 = chunk_log2_for(sd.n);
             const int64_t nch = (sd.n + (int64_t(1) << sd.chunk_log2) - 1) >> sd.chunk_log2;
             sd.first_chunk = total;
@@ -248,7 +276,7 @@ int build_descs(const peat_pair_t *pairs, int32_t count, std::vector<SigDesc> &d
             total += nch;
         }
     }
-    range[3] = total;
+    range[kKinds] = total;
     if (total > 0x7FFFFFFF) return fail(PEAT_EINVAL, "batch needs %lld chunks (max 2^31-1)", (long long)total);
     *total_out = total;
     return PEAT_OK;
@@ -256,7 +284,7 @@ int build_descs(const peat_pair_t *pairs, int32_t count, std::vector<SigDesc> &d
 
 // Common core of every signature call.  When host_outs is set the records go
 // through workspace + pinned staging and the call waits for them.
-int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bins_t *bins,
                    const peat_thresholds_t *thr, peat_signature_t *d_outs,
                    peat_signature_t *host_outs, hipStream_t s) {
     if (count < 0) return fail(PEAT_EINVAL, "count < 0");
@@ -264,7 +292,7 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
     int rc = check_bins_thr(bins, thr);
     if (rc) return rc;
     for (int k = 0; k < count; ++k)
-        if ((rc = check_pair(pairs[k], k))) return rc;
+        if ((rc = check_mixed(pairs[k], k))) return rc;
     if (count == 0) return PEAT_OK;
     if (!host_outs && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
 
@@ -275,7 +303,7 @@ int signature_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *b
 
     std::vector<SigDesc> descs;
     int64_t total = 0;
-    int64_t range[4];
+    int64_t range[kKinds + 1];
     if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
 
     const size_t b_desc = align_up(sizeof(SigDesc) * count);
@@ -435,7 +463,7 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
 // Mean of the k largest errors: three streaming passes and the candidate
 // rounds (see topk.hip).  The call waits twice: once after pass 2 to size the
 // candidate buffers, once for the records.
-int topk_core(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den, peat_topk_t *outs,
+int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den, peat_topk_t *outs,
               hipStream_t s) {
     if (count < 0) return fail(PEAT_EINVAL, "count < 0");
     if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
@@ -443,7 +471,7 @@ int topk_core(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
         return fail(PEAT_EINVAL, "need 1 <= num <= den <= 2^20 (got %d/%d)", num, den);
     int rc;
     for (int k = 0; k < count; ++k)
-        if ((rc = check_pair(pairs[k], k))) return rc;
+        if ((rc = check_mixed(pairs[k], k))) return rc;
     if (count == 0) return PEAT_OK;
     if (!outs) return fail(PEAT_EINVAL, "outs is NULL");
 
@@ -454,7 +482,7 @@ int topk_core(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
 
     std::vector<SigDesc> descs;
     int64_t total = 0;
-    int64_t range[4];
+    int64_t range[kKinds + 1];
     if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
 
     const size_t b_desc = align_up(sizeof(SigDesc) * count);
@@ -598,20 +626,43 @@ int peat_signature(const void *golden, const void *test, int64_t n, peat_dtype_t
                    peat_signature_t *out) {
     if (!out) return fail(PEAT_EINVAL, "out is NULL");
     peat_pair_t p{golden, test, n, (int32_t)dtype, 0};
-    return signature_core(&p, 1, bins, thresholds, nullptr, out, t_stream);
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(&p, 1, mp);
+    if (rc) return rc;
+    return signature_core(mp.data(), 1, bins, thresholds, nullptr, out, t_stream);
 }
 
 int peat_signature_batched(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
                            const peat_thresholds_t *thresholds, peat_signature_t *outs) {
     if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
-    return signature_core(pairs, count, bins, thresholds, nullptr, outs, t_stream);
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    return signature_core(mp.data(), count, bins, thresholds, nullptr, outs, t_stream);
 }
 
 int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
                                  const peat_thresholds_t *thresholds, peat_signature_t *d_outs,
                                  void *stream) {
-    return signature_core(pairs, count, bins, thresholds, d_outs, nullptr,
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    return signature_core(mp.data(), count, bins, thresholds, d_outs, nullptr,
                           static_cast<hipStream_t>(stream));
+}
+
+int peat_signature_mixed(const void *golden, int32_t golden_dtype, const void *test, int32_t test_dtype,
+                         int64_t n, const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                         peat_signature_t *out) {
+    if (!out) return fail(PEAT_EINVAL, "out is NULL");
+    peat_mixed_pair_t p{golden, test, n, golden_dtype, test_dtype};
+    return signature_core(&p, 1, bins, thresholds, nullptr, out, t_stream);
+}
+
+int peat_signature_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                                 const peat_thresholds_t *thresholds, peat_signature_t *outs) {
+    if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
+    return signature_core(pairs, count, bins, thresholds, nullptr, outs, t_stream);
 }
 
 int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
@@ -694,11 +745,22 @@ int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t
                    int32_t den, peat_topk_t *out) {
     if (!out) return fail(PEAT_EINVAL, "out is NULL");
     peat_pair_t p{golden, test, n, (int32_t)dtype, 0};
-    return topk_core(&p, 1, num, den, out, t_stream);
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(&p, 1, mp);
+    if (rc) return rc;
+    return topk_core(mp.data(), 1, num, den, out, t_stream);
 }
 
 int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
                            peat_topk_t *outs) {
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    return topk_core(mp.data(), count, num, den, outs, t_stream);
+}
+
+int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                                 peat_topk_t *outs) {
     return topk_core(pairs, count, num, den, outs, t_stream);
 }
 

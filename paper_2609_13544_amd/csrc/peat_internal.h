@@ -30,13 +30,33 @@ inline int chunk_log2_for(int64_t n) {
     return l;
 }
 
+// Golden/test type combinations ("kinds"), one kernel instantiation each:
+// the three same-type kinds first, then the mixed-precision ones (the golden
+// side is never binary64, and the two formats nest).
+constexpr int kKinds = 10;
+constexpr int kSameKinds = 3;
+constexpr int kKindTypes[kKinds][2] = {
+    {PEAT_F32, PEAT_F32},  {PEAT_F16, PEAT_F16}, {PEAT_BF16, PEAT_BF16}, {PEAT_F32, PEAT_F64},
+    {PEAT_F32, PEAT_F16},  {PEAT_F32, PEAT_BF16}, {PEAT_F16, PEAT_F32}, {PEAT_BF16, PEAT_F32},
+    {PEAT_F16, PEAT_F64},  {PEAT_BF16, PEAT_F64}};
+
+// Kind of a (golden, test) type pair, or -1 when the combination is not accepted.
+inline int pair_kind(int32_t g, int32_t t) {
+    for (int k = 0; k < kKinds; ++k)
+        if (kKindTypes[k][0] == g && kKindTypes[k][1] == t) return k;
+    return -1;
+}
+
+inline int elem_bytes(int32_t dt) { return dt == PEAT_F64 ? 8 : (dt == PEAT_F32 ? 4 : 2); }
+
 struct SigDesc {                 // one per pair (48 bytes)
     const void *g;
     const void *t;
     int64_t n;
     int64_t first_chunk;         // index of the pair's first chunk in the batch
     int32_t nchunks;
-    int32_t dtype;
+    int16_t dtype;               // golden type
+    int16_t tdtype;              // test type
     int32_t chunk_log2;
     int32_t aligned;             // both pointers 16-byte aligned
 };
@@ -149,9 +169,10 @@ struct TopkParams {
 };
 
 // Kernel launchers (defined in the .hip translation units).
-// One launch per element type present: chunks of each type form one
-// contiguous range [range[dt], range[dt + 1]) of the global chunk numbering.
-hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[4], hipStream_t s);
+// One launch per kind present: chunks of each kind form one contiguous range
+// [range[kind], range[kind + 1]) of the global chunk numbering.
+hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[kKinds + 1], hipStream_t s);
+hipError_t launch_sig_mixed_kind(const SigParams &p, int kind, int64_t nchunks, hipStream_t s);
 hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
 hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
 hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);
@@ -160,7 +181,7 @@ hipError_t launch_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed
 hipError_t launch_cast_round(void *x, int64_t n, int to_dtype, hipStream_t s);
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
 hipError_t launch_topk_zero(uint64_t *p, int64_t n, hipStream_t s);
-hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[4], hipStream_t s);
+hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[kKinds + 1], hipStream_t s);
 hipError_t launch_topk_select(const TopkParams &p, int level, hipStream_t s);
 hipError_t launch_topk_cand_hist(const TopkParams &p, int level, hipStream_t s);
 hipError_t launch_topk_cand_sum(const TopkParams &p, int level, hipStream_t s);

@@ -1,0 +1,791 @@
+// Pass 1 of the error signature (sig_chunk), templated on the golden and
+// test element types; included by the translation units that instantiate it
+// (same-type pairs, mixed-precision pairs).
+//
+// Error-signature kernels for gfx950.
+//
+// Pass 1 (sig_chunk): one 256-thread block per fixed-size chunk of one pair.
+// Each thread streams 16-byte vectors of golden and test (4 f32 or 8 f16/bf16
+// elements) through nontemporal buffer loads, widens them exactly to binary64
+// and accumulates the signature of its elements; the chunk's record (binary64
+// partial sums, maxima with their lowest index, integer counts, histogram)
+// goes to one ChunkPartial.
+//
+// Pass 2 (sig_finalize): one block per pair combines its chunk records in a
+// fixed order and writes the peat_signature_t.
+//
+// The definitions follow the paper's FI assessment scores (Section IV-B.3:
+// error = absolute difference of golden and faulty values; max, mean,
+// variance), the closeness test of Section III-A (torch.isclose, rtol = 0)
+// and the error histograms of Section V-D.
+//
+// Fast path.  A wave whose current vectors hold only "ordinary" pairs (both
+// finite, no NaN, golden nonzero, same sign, relative error below 0.5) needs
+// no classification:
+//   - one comparison of the relative error per element flags every other
+//     case (a sign change or a zero golden gives a relative error >= 1 or
+//     NaN) together with the candidates for the maximum relative error; the
+//     exact IEEE quotient is formed only for those candidates;
+//   - reciprocals come from one hardware estimate per four elements plus a
+//     Newton step;
+//   - the maxima of |err| and of the ULP distance are wave-uniform running
+//     records (the vector that first exceeded them), resolved to an element
+//     by one reload at the end of the chunk;
+//   - counts use wave ballots; the histogram uses lane-private 16-bit LDS
+//     counters addressed through a binary64-exponent -> row table.
+// Any other vector is deferred: its wave-uniform vector number goes to a
+// per-wave LDS list and the generic per-element path (every IEEE case)
+// processes the list out of the hot loop.  Ragged tails and unaligned pairs
+// use the generic path directly.
+//
+// Determinism: the element -> lane mapping, per-lane order and reduction
+// trees depend only on the chunk size, which depends only on n, so single,
+// batched and any-grid-size launches give bit-identical records.
+#pragma once
+
+#include "elements.h"
+
+namespace peat {
+namespace {
+
+
+constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
+// Fast-path limit on the relative error: an element at or above it (or NaN)
+// sends its vector to the generic path.  A sign change between finite golden
+// and test values gives |t - g| >= |g|, i.e. a relative error of at least 1
+// (less the reciprocal's 2^-48), and a zero golden value gives Inf or NaN, so
+// this one comparison also catches every case the fast path does not handle.
+// Below the limit t lies within a factor 1.5 of g, so an f32 ULP distance is
+// below 2^24 and an f16/bf16 one below 2^11.
+constexpr double kRareRel = 0.5;
+constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
+constexpr int kHistCols = kBlock / 2;     // histogram words per slot
+
+__device__ __forceinline__ uint32_t hist_col(int tid) { return (uint32_t)tid & (kHistCols - 1); }
+__device__ __forceinline__ uint32_t hist_inc(int tid) { return tid < kHistCols ? 1u : 0x10000u; }
+
+// super-step unroll: lane vectors per tensor per lane
+template <int DG, int DT>
+constexpr int kUnroll = DG != DT ? 4 : ((DT == PEAT_F32) ? 4 : 2);
+
+// ULP distance of two bit patterns of width W (signed-magnitude keys).
+template <int W>
+__device__ __forceinline__ uint32_t ulp_dist(uint32_t gb, uint32_t tb) {
+    constexpr uint32_t S = 1u << (W - 1);
+    constexpr uint32_t M = S - 1;
+    uint32_t mg = gb & M, mt = tb & M;
+    if ((gb ^ tb) & S) return mg + mt;
+    return mt > mg ? mt - mg : mg - mt;
+}
+
+__device__ __forceinline__ uint32_t wave_count(bool p) {
+    return (uint32_t)__popcll(__ballot(p));
+}
+
+// Binary64 reciprocal for the relative-error sum: the hardware estimate
+// (relative error below 2^-24) refined by one Newton step (below 2^-48).
+__device__ __forceinline__ double recip(double b) {
+    const double y = __builtin_amdgcn_rcp(b);
+    return __builtin_fma(y, __builtin_fma(-b, y, 1.0), y);
+}
+
+// Reciprocals of four magnitudes from one reciprocal of their product (the
+// hardware reciprocal issues at a quarter of the fma rate).  The inputs are
+// widened f32/f16/bf16 golden values (the golden side is never binary64), so
+// the product of four stays a normal binary64 number (between 2^-600 and
+// 2^512) and the pairwise products are exact; each result is within a few
+// units of 2^-48 of 1/x.  A zero, Inf or NaN among the four makes all four
+// results NaN or Inf.
+__device__ __forceinline__ void recip4(const double *x, double *r) {
+    const double p01 = x[0] * x[1], p23 = x[2] * x[3];
+    const double inv = recip(p01 * p23);
+    const double i01 = inv * p23, i23 = inv * p01;
+    r[0] = x[1] * i01;
+    r[1] = x[0] * i01;
+    r[2] = x[3] * i23;
+    r[3] = x[2] * i23;
+}
+// The same for two magnitudes (lane vectors of two elements).
+__device__ __forceinline__ void recip2(const double *x, double *r) {
+    const double inv = recip(x[0] * x[1]);
+    r[0] = x[1] * inv;
+    r[1] = x[0] * inv;
+}
+
+struct Lane {
+    double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;
+    double gx_abs;                 // generic path: max |err| and element index
+    uint32_t gi_abs;
+    uint32_t gu, gi_ulp;           // generic path: max ULP and element index
+    double mx_rel;                 // both paths: max rel err and its index
+    double rthr;                   // fast-path filter, at most kRareRel
+    uint32_t ix_rel;
+    uint64_t s_ulp;
+    uint32_t s_ulp32;              // fast path: ULP sum of the current super-step
+    uint32_t first_nan, first_valid;
+    uint32_t cnt[kCnt];                    // generic-path counts (per lane)
+    uint32_t mism[PEAT_MAX_THRESHOLDS];    // generic-path mismatches (per lane)
+};
+
+// Fast-path state shared by the wave.  Vectors reach the fast path in
+// increasing vector number, and every element of a later vector has a higher
+// index than every element of an earlier one, so the wave only needs its
+// running maximum and the vector number that first exceeded the previous one:
+// an element equal to the running maximum in a later vector cannot be the
+// (value, lowest index) maximum.
+struct Uni {
+    uint32_t common;                       // ordinary vectors per lane
+    uint32_t mism[PEAT_MAX_THRESHOLDS];
+    uint32_t first;                        // first ordinary vector number
+    double wx_abs;                         // running max |err| ...
+    uint32_t wv_abs;                       // ... first reached in this vector
+    uint32_t wu, wv_ulp;                   // running max ULP, its vector
+};
+
+struct Shared {
+    uint32_t hrow[2048];                   // binary64 exponent field -> slot * kBlock
+    // Lane-private 16-bit counters, two per word: word [slot][t mod 128]
+    // holds lane t's count in its low half when t < 128 and in its high half
+    // otherwise.  The two lanes of a word are in different waves, and a lane
+    // counts at most 2^18 / 256 = 1024 elements per chunk, so no half carries.
+    uint32_t hist[kHistSlots * kHistCols];
+    uint32_t defer[kWaves][kDeferCap];     // deferred vector numbers per wave
+    double rd[kWaves][6];
+    double rmax[kWaves][2];
+    uint32_t rix[kWaves][5];               // abs, rel, ulp, first_nan, first_valid
+    uint32_t rmu[kWaves];
+    uint64_t rulp[kWaves];
+    uint32_t rcnt[kWaves][kCnt + PEAT_MAX_THRESHOLDS];
+};
+
+__device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
+    L.s_abs = L.s_sq = L.s_rel = L.s_g2 = L.s_t2 = L.s_gt = 0.0;
+    L.gx_abs = -1.0;
+    L.gi_abs = kNone;
+    L.gu = 0;
+    L.gi_ulp = kNone;
+    L.mx_rel = -1.0;
+    L.rthr = -1.0;
+    L.ix_rel = kNone;
+    L.s_ulp = 0;
+    L.s_ulp32 = 0;
+    L.first_nan = L.first_valid = kNone;
+#pragma unroll
+    for (int c = 0; c < kCnt; ++c) L.cnt[c] = 0;
+#pragma unroll
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) L.mism[j] = 0;
+    U.common = 0;
+    U.first = kNone;
+    U.wx_abs = -1.0;
+    U.wv_abs = kNone;
+    U.wu = 0;
+    U.wv_ulp = kNone;
+#pragma unroll
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) U.mism[j] = 0;
+}
+
+__device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
+    const uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: sign bit clear
+    atomicAdd(&sh.hist[sh.hrow[E] + hist_col(tid)], hist_inc(tid));
+}
+
+// Every case of one pair (NaN, Inf, zero golden, sign change, subnormals).
+// Elements may arrive out of index order (deferred vectors), so the maxima
+// use (value, lowest index) comparisons.
+template <int DG, int DT, int NT, typename BG, typename BT>
+__device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParams &P,
+                                             BG gb, BT tb, uint32_t li, int tid) {
+    using PT = PairTr<DG, DT>;
+    const double G = widen<DG>(gb), T = widen<DT>(tb);
+    const bool nan_g = G != G, nan_t = T != T;
+    const bool inf_g = __builtin_isinf(G), inf_t = __builtin_isinf(T);
+    L.cnt[C_NAN_G] += nan_g;
+    L.cnt[C_NAN_T] += nan_t;
+    L.cnt[C_INF_G] += inf_g;
+    L.cnt[C_INF_T] += inf_t;
+    if (nan_g || nan_t) {
+        L.cnt[C_NANPAIR] += 1;
+        L.first_nan = min(L.first_nan, li);
+        return;
+    }
+    L.cnt[C_VALID] += 1;
+    L.first_valid = min(L.first_valid, li);
+    const double a = (G == T) ? 0.0 : __builtin_fabs(T - G);
+    // ULP distance in the narrower format (the wider value rounded to it)
+    uint32_t ulp;
+    if constexpr (PT::SAME) {
+        ulp = ulp_dist<Tr<DT>::W>(gb, tb);
+    } else if constexpr (PT::GOLDEN_NARROW) {
+        ulp = ulp_dist<PT::WN>((uint32_t)gb, narrow_bits<DG, DT>(T));
+    } else {
+        ulp = ulp_dist<PT::WN>(narrow_bits<DT, DG>(G), (uint32_t)tb);
+    }
+    L.s_ulp += ulp;
+    if (ulp > L.gu || (ulp == L.gu && li < L.gi_ulp)) {
+        L.gu = ulp;
+        L.gi_ulp = li;
+    }
+    if constexpr (DT == PEAT_F64) {
+        // a binary64 test side can give a subnormal error (exponent field 0,
+        // which the row table maps to the zero slot): it lies below every bin
+        if (a != 0.0 && a < 0x1p-1022)
+            atomicAdd(&sh.hist[1 * kHistCols + hist_col(tid)], hist_inc(tid));
+        else
+            hist_add(sh, a, tid);
+    } else {
+        hist_add(sh, a, tid);
+    }
+    const bool ainf = __builtin_isinf(a);
+    // not close under torch.isclose: unequal, and the error is infinite or not
+    // within atol + |rtol * G| (a NaN allowance admits nothing)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const double allowed = P.any_rtol ? __dadd_rn(P.thr[j], __builtin_fabs(__dmul_rn(P.rthr[j], G))) : P.thr[j];
+        L.mism[j] += (a != 0.0) && (ainf || !(a <= allowed));
+    }
+    if (a > L.gx_abs || (a == L.gx_abs && li < L.gi_abs)) {
+        L.gx_abs = a;
+        L.gi_abs = li;
+    }
+    if (inf_g || inf_t) return;
+    L.cnt[C_FINITE] += 1;
+    L.s_abs += a;
+    L.s_sq = __builtin_fma(a, a, L.s_sq);
+    L.s_g2 = __builtin_fma(G, G, L.s_g2);
+    L.s_t2 = __builtin_fma(T, T, L.s_t2);
+    L.s_gt = __builtin_fma(G, T, L.s_gt);
+    if (G != 0.0) {
+        L.cnt[C_REL] += 1;
+        const double r = a / __builtin_fabs(G);
+        L.s_rel += r;
+        if (r > L.mx_rel || (r == L.mx_rel && li < L.ix_rel)) {
+            L.mx_rel = r;
+            L.ix_rel = li;
+            L.rthr = __builtin_fmin(r - r * kRelMargin, kRareRel);
+        }
+    }
+}
+
+// |a - b| of two unsigned 32-bit values (v_sad_u32 with a zero addend).
+__device__ __forceinline__ uint32_t absdiff_u32(uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_sad_u32 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// max(|a|, |b|) of two binary64 values as one v_max_f64 with absolute-value
+// source modifiers (the operands are never NaN here, so no quieting is needed).
+__device__ __forceinline__ double absmax_f64(double a, double b) {
+    double r;
+    asm("v_max_f64 %0, |%1|, |%2|" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// Wave maximum of a binary64 value, returned as a wave-uniform scalar.
+__device__ __forceinline__ double wave_max_uniform(double x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = __builtin_fmax(x, __shfl_xor(x, o));
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ uint32_t wave_max_uniform_u(uint32_t x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = max(x, (uint32_t)__shfl_xor(x, o));
+    return __builtin_amdgcn_readfirstlane(x);
+}
+
+// ULP distance of a fast-path element (both finite, same sign, not NaN):
+// the difference of the narrower format's bit patterns.
+template <int DG, int DT, typename BG, typename BT>
+__device__ __forceinline__ uint32_t fast_ulp(BG gb, BT tb, double G, double T) {
+    using PT = PairTr<DG, DT>;
+    uint32_t a, b;
+    if constexpr (PT::SAME) {
+        a = gb;
+        b = tb;
+    } else if constexpr (PT::GOLDEN_NARROW) {
+        a = (uint32_t)gb;
+        b = narrow_bits<DG, DT>(T);
+    } else {
+        a = narrow_bits<DT, DG>(G);
+        b = (uint32_t)tb;
+    }
+    if constexpr (PT::WN == 32) {
+        return absdiff_u32(a, b);
+    } else {
+        return __builtin_amdgcn_sad_u16(a, b, 0u);
+    }
+}
+
+// One lane vector of golden and of test (vector number v of the lane's
+// sequence).  Called in wave-uniform control flow with every lane active.
+// Returns true (wave-uniform) when the vector must go to the generic path.
+//
+// Every per-element decision is one wave mask: rare elements, candidates for
+// the max relative error, and a new running maximum of |err| or of the ULP
+// distance all land in one rarely taken branch, so the common path only
+// accumulates.  The histogram's row reads are all issued before its atomic
+// adds, so they share one LDS round trip.
+template <int DG, int DT, int NT, bool RT>
+__device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
+                                         const u32x4 &gv, const u32x4 &tv, uint32_t v, int tid) {
+    constexpr int VEC = PairTr<DG, DT>::VEC;
+    double G[VEC], T[VEC], E[VEC], R[VEC];
+    uint32_t row[VEC], u[VEC];
+    uint64_t mflag = 0;
+    double AG[VEC], IG[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        G[j] = widen<DG>(lane_elem<DG>(gv, j));
+        AG[j] = __builtin_fabs(G[j]);
+    }
+    if constexpr (VEC == 2) {
+        recip2(AG, IG);
+    } else {
+#pragma unroll
+        for (int q = 0; q < VEC; q += 4) recip4(AG + q, IG + q);
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        const auto gb = lane_elem<DG>(gv, j);
+        const auto tb = lane_elem<DT>(tv, j);
+        T[j] = widen<DT>(tb);
+        E[j] = T[j] - G[j];                                   // signed error
+        R[j] = __builtin_fabs(E[j]) * IG[j];
+        // rare (>= kRareRel or NaN), or a candidate for the max relative error
+        mflag |= __ballot(!(R[j] < L.rthr));
+        // same sign on the fast path: the ULP distance is |t - g| of the bit patterns
+        u[j] = fast_ulp<DG, DT>(gb, tb, G[j], T[j]);
+        row[j] = sh.hrow[(uint32_t)(__double_as_longlong(E[j]) >> 52) & 0x7FFu];
+    }
+    double va = absmax_f64(E[0], E[1]);
+#pragma unroll
+    for (int j = 2; j < VEC; ++j) va = absmax_f64(va, E[j]);
+    uint32_t vu = max(u[0], u[1]);
+#pragma unroll
+    for (int j = 2; j < VEC; ++j) vu = max(vu, u[j]);
+    mflag |= __ballot(va > U.wx_abs);
+    mflag |= __ballot(vu > U.wu);
+    if (mflag != 0) {
+        uint64_t mrare = 0, mcand = 0;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            mrare |= __ballot(!(R[j] < kRareRel));
+            mcand |= __ballot(R[j] > L.rthr);
+        }
+        if (mrare != 0) return true;
+        if (mcand != 0) {
+            // The filter threshold is shared by the wave: an element whose
+            // relative error is below the wave's running maximum cannot be
+            // the chunk's maximum, so only a few vectors per chunk get here.
+            // Ties with the maximum still pass (the margin keeps them), and
+            // the lanes' (value, lowest index) maxima are merged at the end
+            // of the chunk.
+            const uint32_t li0 = (v * kBlock + tid) * VEC;
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                if (R[j] > L.rthr) {
+                    const double r = __builtin_fabs(E[j]) / __builtin_fabs(G[j]);   // IEEE quotient
+                    if (r > L.mx_rel) {
+                        L.mx_rel = r;
+                        L.ix_rel = li0 + j;
+                    }
+                }
+            }
+            const double wm = wave_max_uniform(L.mx_rel);
+            L.rthr = __builtin_fmin(wm - wm * kRelMargin, kRareRel);
+        }
+        if (__ballot(va > U.wx_abs) != 0) {
+            U.wx_abs = wave_max_uniform(va);
+            U.wv_abs = v;
+        }
+        if (__ballot(vu > U.wu) != 0) {
+            U.wu = wave_max_uniform_u(vu);
+            U.wv_ulp = v;
+        }
+    }
+
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[row[j] + hist_col(tid)], hist_inc(tid));
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) L.s_ulp32 += u[j];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        L.s_abs += __builtin_fabs(E[j]);
+        L.s_sq = __builtin_fma(E[j], E[j], L.s_sq);
+        L.s_g2 = __builtin_fma(G[j], G[j], L.s_g2);
+        L.s_t2 = __builtin_fma(T[j], T[j], L.s_t2);
+        L.s_gt = __builtin_fma(G[j], T[j], L.s_gt);
+        L.s_rel += R[j];
+    }
+    // threshold mismatches: nothing to count while the vector's largest
+    // |err| is at most the smallest threshold
+    if (__ballot(va > P.thr_min) != 0) {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+#pragma unroll
+            for (int k = 0; k < NT; ++k) {
+                if constexpr (RT) {
+                    // torch.isclose's allowance atol + |rtol * G|, rounded step by
+                    // step (never NaN here: G is finite and nonzero)
+                    const double allowed = __dadd_rn(P.thr[k], __builtin_fabs(__dmul_rn(P.rthr[k], G[j])));
+                    U.mism[k] += wave_count(__builtin_fabs(E[j]) > allowed);
+                } else {
+                    U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
+                }
+            }
+        }
+    }
+    U.common += 1;
+    if (U.first == kNone) U.first = v;
+    return false;
+}
+
+// ---- wave reductions (fixed butterfly order) -------------------------------
+__device__ __forceinline__ double wsum(double v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ uint32_t wsum_u(uint32_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ uint64_t wsum_u64(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ uint32_t wmin_u(uint32_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = min(v, (uint32_t)__shfl_xor(v, o));
+    return v;
+}
+// (value desc, index asc) over entries with index != kNone
+template <typename V>
+__device__ __forceinline__ void wmax(V &v, uint32_t &ix) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const V ov = __shfl_xor(v, o);
+        const uint32_t oi = __shfl_xor(ix, o);
+        const bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
+        v = take ? ov : v;
+        ix = take ? oi : ix;
+    }
+}
+template <typename V>
+__device__ __forceinline__ void lex_merge(V &v, uint32_t &ix, V ov, uint32_t oi) {
+    if (oi != kNone && (ix == kNone || ov > v || (ov == v && oi < ix))) {
+        v = ov;
+        ix = oi;
+    }
+}
+
+template <int DG, int DT, int NT, bool RT>
+__device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int64_t cin, int64_t gchunk) {
+    using PT = PairTr<DG, DT>;
+    constexpr int VEC = PT::VEC;
+    constexpr int U = kUnroll<DG, DT>;
+    constexpr int SUPER = kBlock * VEC * U;     // elements per block super-step (2048 or 4096)
+    constexpr int ESZG = Tr<DG>::W / 8, ESZT = Tr<DT>::W / 8;
+    constexpr int BG = PT::BG, BT = PT::BT;     // bytes per lane vector
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int64_t off = cin << d.chunk_log2;    // first element of the chunk
+    const int64_t rest = d.n - off;
+    const uint32_t len = (uint32_t)(rest < (int64_t(1) << d.chunk_log2) ? rest : (int64_t(1) << d.chunk_log2));
+    const char *gbase = static_cast<const char *>(d.g) + off * ESZG;
+    const char *tbase = static_cast<const char *>(d.t) + off * ESZT;
+
+    Lane L;
+    Uni Un;
+    lane_init(L, Un);
+
+    const uint32_t nsuper = d.aligned ? len / SUPER : 0;
+    uint32_t ndef = 0;                           // wave-uniform
+
+    auto flush = [&]() {
+#pragma unroll 1
+        for (uint32_t k = 0; k < ndef; ++k) {
+            const uint32_t v = sh.defer[wave][k];
+            const u32x4 gv = load_vec<BG>(gbase, v * kBlock + tid);
+            const u32x4 tv = load_vec<BT>(tbase, v * kBlock + tid);
+            const uint32_t li0 = (v * kBlock + tid) * VEC;
+#pragma unroll 1
+            for (int j = 0; j < VEC; ++j)
+                generic_elem<DG, DT, NT>(L, sh, P, lane_elem<DG>(gv, j), lane_elem<DT>(tv, j), li0 + j, tid);
+        }
+        ndef = 0;
+        // Nothing of the flush stays in flight: the hot loop's header then
+        // waits only for its own prefetch.
+        __builtin_amdgcn_s_waitcnt(0);
+    };
+
+    // Two register sets, used in turn: the loads of super-step s+1 are in
+    // flight while super-step s is processed, without register copies.  The
+    // prefetch is issued unconditionally (clamped to the last super-step,
+    // where it is a redundant in-bounds reload) so that every path has the
+    // same number of loads outstanding and the waits stay partial.
+    // Buffer loads: the chunk base lives in a scalar resource, the per-lane
+    // offsets are loop-invariant registers and the super-step moves only the
+    // scalar offset, so no address register is rewritten while loads that
+    // read it are in flight.  The resource covers the chunk (at most 2^18
+    // elements = 2 MiB of binary64), and reads past its end return zero.
+    const __amdgpu_buffer_rsrc_t grs = __builtin_amdgcn_make_buffer_rsrc((void *)gbase, (short)0, (int)(len * ESZG), kBufFlags);
+    const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc((void *)tbase, (short)0, (int)(len * ESZT), kBufFlags);
+    const uint32_t lane_off_g = (uint32_t)tid * BG, lane_off_t = (uint32_t)tid * BT;
+    auto load = [&](u32x4 (&g)[U], u32x4 (&t)[U], uint32_t s) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            g[u] = buf_load<BG, kLoadNT>(grs, (int)lane_off_g, (int)((s * U + u) * (kBlock * BG)));
+            t[u] = buf_load<BT, kLoadNT>(trs, (int)lane_off_t, (int)((s * U + u) * (kBlock * BT)));
+        }
+    };
+    auto step = [&](const u32x4 (&g)[U], const u32x4 (&t)[U], uint32_t s) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t v = s * U + u;
+            if (vec_fast<DG, DT, NT, RT>(L, Un, sh, P, g[u], t[u], v, tid)) {
+                sh.defer[wave][ndef] = v;      // every lane writes the same value
+                ++ndef;
+            }
+        }
+        // at most U * VEC distances below 2^24 each: no 32-bit overflow
+        L.s_ulp += L.s_ulp32;
+        L.s_ulp32 = 0;
+    };
+    if (nsuper > 0) {
+        u32x4 ga[U], ta[U], gb[U], tb[U];
+        const uint32_t last = nsuper - 1;
+        load(ga, ta, 0);
+        uint32_t s = 0;
+        // The deferred list is flushed outside the hot loop, which exits
+        // when the list may not hold the next two super-steps.
+        while (s < nsuper) {
+            for (; s < nsuper; s += 2) {
+                load(gb, tb, min(s + 1, last));
+                step(ga, ta, s);
+                if (s + 1 >= nsuper) {
+                    s += 2;
+                    break;
+                }
+                load(ga, ta, min(s + 2, last));
+                step(gb, tb, s + 1);
+                if (ndef > kDeferCap - 2 * U) {
+                    s += 2;
+                    break;
+                }
+            }
+            flush();
+        }
+    }
+    // ragged tail, or the whole chunk when a pointer is not 16-byte aligned
+#pragma unroll 1
+    for (uint32_t li = nsuper * SUPER + tid; li < len; li += kBlock)
+        generic_elem<DG, DT, NT>(L, sh, P, load_elem<DG>(gbase, li), load_elem<DT>(tbase, li), li, tid);
+
+    // ---- resolve the fast-path maxima to element indices -----------------
+    // Reload the vector in which the wave's running maximum was first
+    // reached; its lanes holding that value become (value, index) candidates.
+    double mxa = -1.0;
+    uint32_t ixa = kNone, mu = 0, ixu = kNone;
+    if (Un.wv_abs != kNone) {
+        const u32x4 gv = load_vec<BG>(gbase, Un.wv_abs * kBlock + tid);
+        const u32x4 tv = load_vec<BT>(tbase, Un.wv_abs * kBlock + tid);
+#pragma unroll
+        for (int j = VEC - 1; j >= 0; --j) {
+            const double a = __builtin_fabs(widen<DT>(lane_elem<DT>(tv, j)) - widen<DG>(lane_elem<DG>(gv, j)));
+            if (a == Un.wx_abs) {
+                mxa = a;
+                ixa = (Un.wv_abs * kBlock + tid) * VEC + j;
+            }
+        }
+    }
+    if (Un.wv_ulp != kNone) {
+        const u32x4 gv = load_vec<BG>(gbase, Un.wv_ulp * kBlock + tid);
+        const u32x4 tv = load_vec<BT>(tbase, Un.wv_ulp * kBlock + tid);
+#pragma unroll
+        for (int j = VEC - 1; j >= 0; --j) {
+            uint32_t uj;
+            if constexpr (PT::SAME) {
+                const uint32_t gb = lane_elem<DG>(gv, j), tb = lane_elem<DT>(tv, j);
+                uj = max(gb, tb) - min(gb, tb);
+            } else {
+                const auto gb = lane_elem<DG>(gv, j);
+                const auto tb = lane_elem<DT>(tv, j);
+                uj = fast_ulp<DG, DT>(gb, tb, widen<DG>(gb), widen<DT>(tb));
+            }
+            if (uj == Un.wu) {
+                mu = Un.wu;
+                ixu = (Un.wv_ulp * kBlock + tid) * VEC + j;
+            }
+        }
+    }
+    lex_merge(mxa, ixa, L.gx_abs, L.gi_abs);
+    lex_merge(mu, ixu, L.gu, L.gi_ulp);
+    // the first ordinary element of this lane
+    if (Un.first != kNone) L.first_valid = min(L.first_valid, (Un.first * kBlock + tid) * VEC);
+
+    // ---- epilogue: reduce the block into the chunk record ----------------
+    double sums[6] = {L.s_abs, L.s_sq, L.s_rel, L.s_g2, L.s_t2, L.s_gt};
+#pragma unroll
+    for (int k = 0; k < 6; ++k) sums[k] = wsum(sums[k]);
+    double mxr = L.mx_rel;
+    uint32_t ixr = L.ix_rel;
+    wmax(mxa, ixa);
+    wmax(mxr, ixr);
+    wmax(mu, ixu);
+    const uint32_t fnan = wmin_u(L.first_nan), fval = wmin_u(L.first_valid);
+    const uint64_t sulp = wsum_u64(L.s_ulp);
+    uint32_t cnts[kCnt + PEAT_MAX_THRESHOLDS];
+#pragma unroll
+    for (int c = 0; c < kCnt; ++c) cnts[c] = wsum_u(L.cnt[c]);
+#pragma unroll
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) cnts[kCnt + j] = j < NT ? wsum_u(L.mism[j]) : 0u;
+    // fast-path counts: every element there is valid, finite, golden nonzero
+    const uint32_t common = Un.common * 64u * VEC;
+    cnts[C_VALID] += common;
+    cnts[C_FINITE] += common;
+    cnts[C_REL] += common;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) cnts[kCnt + j] += Un.mism[j];
+    if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < 6; ++k) sh.rd[wave][k] = sums[k];
+        sh.rmax[wave][0] = mxa;
+        sh.rmax[wave][1] = mxr;
+        sh.rix[wave][0] = ixa;
+        sh.rix[wave][1] = ixr;
+        sh.rix[wave][2] = ixu;
+        sh.rix[wave][3] = fnan;
+        sh.rix[wave][4] = fval;
+        sh.rmu[wave] = mu;
+        sh.rulp[wave] = sulp;
+#pragma unroll
+        for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) sh.rcnt[wave][c] = cnts[c];
+    }
+    __syncthreads();
+
+    ChunkPartial *out = P.partials + gchunk;
+    // histogram: thread t sums slot t/4 over a quarter of the words
+    {
+        const int slot = tid >> 2, q = tid & 3;
+        uint32_t acc = 0;
+        const uint32_t *row = sh.hist + slot * kHistCols + q * 32;
+#pragma unroll 8
+        for (int c = 0; c < 32; ++c) {
+            const uint32_t w = row[(c + slot + 8 * q) & 31];
+            acc += (w & 0xFFFFu) + (w >> 16);
+        }
+        acc += __shfl_xor(acc, 1);
+        acc += __shfl_xor(acc, 2);
+        if (q == 0) out->hist[slot] = acc;
+        // slots 64..66 (beyond 256/4 threads): one thread each
+        if (tid < kHistSlots - 64) {
+            const int s2 = 64 + tid;
+            uint32_t a2 = 0;
+            for (int c = 0; c < kHistCols; ++c) {
+                const uint32_t w = sh.hist[s2 * kHistCols + c];
+                a2 += (w & 0xFFFFu) + (w >> 16);
+            }
+            out->hist[s2] = a2;
+        }
+    }
+    if (tid == 0) {
+        double s[6] = {0, 0, 0, 0, 0, 0};
+        double ma = -1.0, mr = -1.0;
+        uint32_t ia = kNone, ir = kNone, iu = kNone, fn = kNone, fv = kNone, m = 0;
+        uint64_t su = 0;
+        uint32_t cn[kCnt + PEAT_MAX_THRESHOLDS];
+        for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] = 0;
+        for (int w = 0; w < kWaves; ++w) {
+            for (int k = 0; k < 6; ++k) s[k] += sh.rd[w][k];
+            lex_merge(ma, ia, sh.rmax[w][0], sh.rix[w][0]);
+            lex_merge(mr, ir, sh.rmax[w][1], sh.rix[w][1]);
+            lex_merge(m, iu, sh.rmu[w], sh.rix[w][2]);
+            fn = min(fn, sh.rix[w][3]);
+            fv = min(fv, sh.rix[w][4]);
+            su += sh.rulp[w];
+            for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] += sh.rcnt[w][c];
+        }
+        // every ULP distance in the chunk is 0: the first valid element is the maximum
+        if (iu == kNone || m == 0) {
+            m = 0;
+            iu = fv;
+        }
+        out->s_abs = s[0];
+        out->s_sq = s[1];
+        out->s_rel = s[2];
+        out->s_g2 = s[3];
+        out->s_t2 = s[4];
+        out->s_gt = s[5];
+        out->max_abs = ma;
+        out->max_rel = mr;
+        out->ix_abs = ia == kNone ? -1 : off + ia;
+        out->ix_rel = ir == kNone ? -1 : off + ir;
+        out->ix_ulp = iu == kNone ? -1 : off + iu;
+        out->first_nan = fn == kNone ? -1 : off + fn;
+        out->first_valid = fv == kNone ? -1 : off + fv;
+        out->sum_ulp = su;
+        out->max_ulp = m;
+        for (int c = 0; c < kCnt; ++c) out->cnt[c] = cn[c];
+        for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) out->mism[j] = cn[kCnt + j];
+    }
+}
+
+// Three blocks per CU (12 waves) where the registers allow it without
+// spilling in the hot loop: f32 with two absolute thresholds, the common case.
+template <int DG, int DT, int NT, bool RT>
+constexpr int chunk_blocks_per_cu() { return (DG == PEAT_F32 && DT == PEAT_F32 && NT == 2 && !RT) ? 3 : 2; }
+
+template <int DG, int DT, int NT, bool RT>
+__global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>())) sig_chunk(SigParams P) {
+    __shared__ Shared sh;
+    const int64_t gchunk = P.chunk_base + blockIdx.x;
+    const int pair = P.chunk_pair[gchunk];
+    const SigDesc d = P.descs[pair];
+    const int64_t cin = gchunk - d.first_chunk;
+    const int tid = threadIdx.x;
+    // clear the lane-private histogram counters and build the exponent table:
+    // slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi
+    for (int i = tid; i < kHistSlots * kHistCols; i += kBlock) sh.hist[i] = 0;
+    const int w = (P.hi - P.lo) / P.nbins;
+    for (int E = tid; E < 2048; E += kBlock) {
+        int slot;
+        if (E == 0) {
+            slot = 0;
+        } else if (E == 2047) {
+            slot = P.nbins + 2;                // infinite error
+        } else {
+            const int k = E - 1023;            // a in [2^k, 2^(k+1))
+            slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
+        }
+        sh.hrow[E] = (uint32_t)(slot * kHistCols);
+    }
+    __syncthreads();
+    chunk_body<DG, DT, NT, RT>(P, sh, d, cin, gchunk);
+}
+
+template <int DG, int DT, bool RT>
+hipError_t launch_kind_rt(const SigParams &p, int64_t n, hipStream_t s) {
+    dim3 grid((unsigned)n), block(kBlock);
+    switch (p.nthr_pad) {
+        case 2: hipLaunchKernelGGL((sig_chunk<DG, DT, 2, RT>), grid, block, 0, s, p); break;
+        case 4: hipLaunchKernelGGL((sig_chunk<DG, DT, 4, RT>), grid, block, 0, s, p); break;
+        default: hipLaunchKernelGGL((sig_chunk<DG, DT, 8, RT>), grid, block, 0, s, p); break;
+    }
+    return hipGetLastError();
+}
+
+// Pass 1 over n chunks of one kind, starting at p.chunk_base.
+template <int DG, int DT>
+hipError_t launch_kind(const SigParams &p, int64_t n, hipStream_t s) {
+    return p.any_rtol ? launch_kind_rt<DG, DT, true>(p, n, s) : launch_kind_rt<DG, DT, false>(p, n, s);
+}
+
+}  // namespace
+}  // namespace peat
+

@@ -53,9 +53,9 @@ __device__ __forceinline__ uint32_t digit_of(uint64_t key, int level) {
 }
 
 // Error of a valid pair (no NaN on either side) and its bit pattern.
-template <int DT>
-__device__ __forceinline__ bool error_of(uint32_t gb, uint32_t tb, uint64_t &key, double &a) {
-    const double G = widen<DT>(gb), T = widen<DT>(tb);
+template <int DG, int DT, typename BG, typename BT>
+__device__ __forceinline__ bool error_of(BG gb, BT tb, uint64_t &key, double &a) {
+    const double G = widen<DG>(gb), T = widen<DT>(tb);
     if (G != G || T != T) return false;
     a = (G == T) ? 0.0 : __builtin_fabs(T - G);
     key = (uint64_t)__double_as_longlong(a);
@@ -63,31 +63,34 @@ __device__ __forceinline__ bool error_of(uint32_t gb, uint32_t tb, uint64_t &key
 }
 
 // Calls f(key, a) for every valid pair of chunk `cin` of pair d, each lane in
-// a fixed order: 16-byte vectors (four per step in flight), then the ragged
-// tail (or the whole chunk when a pointer is not 16-byte aligned).
-template <int DT, typename F>
+// a fixed order: lane vectors (16 bytes of the wider side, four per step in
+// flight), then the ragged tail (or the whole chunk when a pointer is not
+// 16-byte aligned).
+template <int DG, int DT, typename F>
 __device__ __forceinline__ void for_each_error(const SigDesc &d, int64_t cin, F &&f) {
-    constexpr int VEC = Tr<DT>::VEC;
-    constexpr int ESZ = Tr<DT>::W / 8;
+    using PT = PairTr<DG, DT>;
+    constexpr int VEC = PT::VEC;
+    constexpr int ESZG = Tr<DG>::W / 8, ESZT = Tr<DT>::W / 8;
+    constexpr int BG = PT::BG, BT = PT::BT;
     constexpr int U = 4;
     const int64_t off = cin << d.chunk_log2;
     const int64_t rest = d.n - off;
     const uint32_t len = (uint32_t)(rest < (int64_t(1) << d.chunk_log2) ? rest : (int64_t(1) << d.chunk_log2));
-    const char *gbase = static_cast<const char *>(d.g) + off * ESZ;
-    const char *tbase = static_cast<const char *>(d.t) + off * ESZ;
+    const char *gbase = static_cast<const char *>(d.g) + off * ESZG;
+    const char *tbase = static_cast<const char *>(d.t) + off * ESZT;
     const uint32_t nvec = d.aligned ? len / VEC : 0;
     if (nvec > 0) {
         const __amdgpu_buffer_rsrc_t grs =
-            __builtin_amdgcn_make_buffer_rsrc((void *)gbase, (short)0, (int)(nvec * 16u), kBufFlags);
+            __builtin_amdgcn_make_buffer_rsrc((void *)gbase, (short)0, (int)(nvec * BG), kBufFlags);
         const __amdgpu_buffer_rsrc_t trs =
-            __builtin_amdgcn_make_buffer_rsrc((void *)tbase, (short)0, (int)(nvec * 16u), kBufFlags);
+            __builtin_amdgcn_make_buffer_rsrc((void *)tbase, (short)0, (int)(nvec * BT), kBufFlags);
         uint32_t v = threadIdx.x;
         for (; v + (U - 1) * kBlock < nvec; v += U * kBlock) {
             u32x4 gv[U], tv[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                gv[u] = __builtin_amdgcn_raw_buffer_load_b128(grs, (int)((v + u * kBlock) * 16u), 0, kLoadNT);
-                tv[u] = __builtin_amdgcn_raw_buffer_load_b128(trs, (int)((v + u * kBlock) * 16u), 0, kLoadNT);
+                gv[u] = buf_load<BG, kLoadNT>(grs, (int)((v + u * kBlock) * BG), 0);
+                tv[u] = buf_load<BT, kLoadNT>(trs, (int)((v + u * kBlock) * BT), 0);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -95,25 +98,25 @@ __device__ __forceinline__ void for_each_error(const SigDesc &d, int64_t cin, F 
                 for (int j = 0; j < VEC; ++j) {
                     uint64_t key;
                     double a;
-                    if (error_of<DT>(lane_elem<DT>(gv[u], j), lane_elem<DT>(tv[u], j), key, a)) f(key, a);
+                    if (error_of<DG, DT>(lane_elem<DG>(gv[u], j), lane_elem<DT>(tv[u], j), key, a)) f(key, a);
                 }
             }
         }
         for (; v < nvec; v += kBlock) {
-            const u32x4 gv = __builtin_amdgcn_raw_buffer_load_b128(grs, (int)(v * 16u), 0, kLoadNT);
-            const u32x4 tv = __builtin_amdgcn_raw_buffer_load_b128(trs, (int)(v * 16u), 0, kLoadNT);
+            const u32x4 gv = buf_load<BG, kLoadNT>(grs, (int)(v * BG), 0);
+            const u32x4 tv = buf_load<BT, kLoadNT>(trs, (int)(v * BT), 0);
 #pragma unroll
             for (int j = 0; j < VEC; ++j) {
                 uint64_t key;
                 double a;
-                if (error_of<DT>(lane_elem<DT>(gv, j), lane_elem<DT>(tv, j), key, a)) f(key, a);
+                if (error_of<DG, DT>(lane_elem<DG>(gv, j), lane_elem<DT>(tv, j), key, a)) f(key, a);
             }
         }
     }
     for (uint32_t i = nvec * VEC + threadIdx.x; i < len; i += kBlock) {
         uint64_t key;
         double a;
-        if (error_of<DT>(load_elem<DT>(gbase, i), load_elem<DT>(tbase, i), key, a)) f(key, a);
+        if (error_of<DG, DT>(load_elem<DG>(gbase, i), load_elem<DT>(tbase, i), key, a)) f(key, a);
     }
 }
 
@@ -173,7 +176,7 @@ __device__ __forceinline__ bool table_count(uint64_t *tkey, uint32_t *tcnt, uint
     return false;
 }
 
-template <int DT, int PASS>
+template <int DG, int DT, int PASS>
 __global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
     __shared__ uint32_t h[kTopkBins];
     __shared__ double red[kWaves];
@@ -186,7 +189,7 @@ __global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
     if constexpr (PASS == 0) {
         for (int b = threadIdx.x; b < kBins0; b += kBlock) h[b] = 0;
         __syncthreads();
-        for_each_error<DT>(d, cin, [&](uint64_t key, double) { atomicAdd(&h[key >> 52], 1u); });
+        for_each_error<DG, DT>(d, cin, [&](uint64_t key, double) { atomicAdd(&h[key >> 52], 1u); });
         flush_hist(h, kBins0, H);
     } else if constexpr (PASS == 1) {
         const TopkState st = P.state[pair];
@@ -196,13 +199,13 @@ __global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
             return;
         }
         const uint64_t d0 = (uint64_t)st.d0;
-        const bool hist1 = st.status == kTopkActive;          // the binade is not 0
+        const bool hist1 = st.status == kTopkActive;          // the boundary binade needs ordering
         if (hist1) {
             for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
             __syncthreads();
         }
         double s = 0.0;
-        for_each_error<DT>(d, cin, [&](uint64_t key, double a) {
+        for_each_error<DG, DT>(d, cin, [&](uint64_t key, double a) {
             const uint64_t e = key >> 52;
             if (e > d0) {
                 s += a;
@@ -231,7 +234,7 @@ __global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
         uint64_t *cnt = &P.state[pair].cnt[0];
         uint64_t *dst = P.keys[0] + 2 * off;
         double s = 0.0;
-        for_each_error<DT>(d, cin, [&](uint64_t key, double a) {
+        for_each_error<DG, DT>(d, cin, [&](uint64_t key, double a) {
             const uint64_t k1 = key >> digit_shift(1);
             if ((k1 >> 13) == (b1 >> 13) && k1 > b1) s += a;
             const bool in = k1 == b1;
@@ -300,8 +303,12 @@ __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     st.level = L;
     if (L == 0) {
         st.d0 = b;
-        // a zero or infinite boundary fixes the k-th largest error already
-        st.status = (b == 0 || b == kBins0 - 1) ? kTopkDone : kTopkActive;
+        // An infinite boundary fixes the k-th largest error already, and so
+        // does binade 0 when it holds only zero errors: with a binary64 test
+        // side it also holds the subnormal errors, which the next levels
+        // order like any other binade.
+        const bool zero_only = b == 0 && P.descs[pair].tdtype != PEAT_F64;
+        st.status = (zero_only || b == kBins0 - 1) ? kTopkDone : kTopkActive;
     } else {
         st.status = L == kTopkLevels - 1 ? kTopkDone : kTopkActive;
     }
@@ -423,7 +430,7 @@ __global__ void __launch_bounds__(kBlock) topk_finalize(TopkParams P) {
         o.kth_value = inf;
         o.sum_topk = inf;
         o.mean_topk = inf;
-    } else if (st.d0 == 0) {                          // the k-th largest error is 0
+    } else if (st.d0 == 0 && st.level == 0) {        // the k-th largest error is 0
         o.count_above = (int64_t)(st.k - st.need);
         o.kth_value = 0.0;
         o.sum_topk = sa;
@@ -437,9 +444,11 @@ __global__ void __launch_bounds__(kBlock) topk_finalize(TopkParams P) {
                 const uint64_t *xp = P.xpart + 2 * ((size_t)r * P.ncblk + c.first_blk + b);
                 x += ((unsigned __int128)xp[1] << 64) | xp[0];
             }
-        x += (unsigned __int128)st.need * ((st.key & kMant) | (uint64_t(1) << 52));
+        // binade 0 (subnormal errors) has no implicit bit and the exponent of binade 1
+        const uint64_t lead = st.d0 != 0 ? (uint64_t(1) << 52) : 0;
+        x += (unsigned __int128)st.need * ((st.key & kMant) | lead);
         const double xd = (double)(uint64_t)(x >> 64) * 0x1p64 + (double)(uint64_t)x;
-        const double sc = __builtin_ldexp(xd, st.d0 - 1075);
+        const double sc = __builtin_ldexp(xd, (st.d0 != 0 ? st.d0 : 1) - 1075);
         o.count_above = (int64_t)(st.k - st.need);
         o.kth_value = __longlong_as_double((long long)st.key);
         o.sum_topk = (sa + sb) + sc;
@@ -452,19 +461,31 @@ __global__ void __launch_bounds__(kBlock) topk_zero(uint64_t *p, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) p[i] = 0;
 }
 
+template <int DG, int DT, int PASS>
+void launch_one(const TopkParams &q, int64_t n, hipStream_t s) {
+    hipLaunchKernelGGL((topk_pass<DG, DT, PASS>), dim3((unsigned)n), dim3(kBlock), 0, s, q);
+}
+
 template <int PASS>
-hipError_t launch_pass_dt(const TopkParams &p, const int64_t range[4], hipStream_t s) {
-    for (int dt = 0; dt < 3; ++dt) {
-        const int64_t n = range[dt + 1] - range[dt];
+hipError_t launch_pass_kinds(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
+    static_assert(kKindTypes[3][1] == PEAT_F64 && kKindTypes[9][0] == PEAT_BF16, "kind table order");
+    for (int kind = 0; kind < kKinds; ++kind) {
+        const int64_t n = range[kind + 1] - range[kind];
         if (n <= 0) continue;
         TopkParams q = p;
-        q.chunk_base = range[dt];
-        if (dt == PEAT_F32)
-            hipLaunchKernelGGL((topk_pass<PEAT_F32, PASS>), dim3((unsigned)n), dim3(kBlock), 0, s, q);
-        else if (dt == PEAT_F16)
-            hipLaunchKernelGGL((topk_pass<PEAT_F16, PASS>), dim3((unsigned)n), dim3(kBlock), 0, s, q);
-        else
-            hipLaunchKernelGGL((topk_pass<PEAT_BF16, PASS>), dim3((unsigned)n), dim3(kBlock), 0, s, q);
+        q.chunk_base = range[kind];
+        switch (kind) {
+            case 0: launch_one<PEAT_F32, PEAT_F32, PASS>(q, n, s); break;
+            case 1: launch_one<PEAT_F16, PEAT_F16, PASS>(q, n, s); break;
+            case 2: launch_one<PEAT_BF16, PEAT_BF16, PASS>(q, n, s); break;
+            case 3: launch_one<PEAT_F32, PEAT_F64, PASS>(q, n, s); break;
+            case 4: launch_one<PEAT_F32, PEAT_F16, PASS>(q, n, s); break;
+            case 5: launch_one<PEAT_F32, PEAT_BF16, PASS>(q, n, s); break;
+            case 6: launch_one<PEAT_F16, PEAT_F32, PASS>(q, n, s); break;
+            case 7: launch_one<PEAT_BF16, PEAT_F32, PASS>(q, n, s); break;
+            case 8: launch_one<PEAT_F16, PEAT_F64, PASS>(q, n, s); break;
+            default: launch_one<PEAT_BF16, PEAT_F64, PASS>(q, n, s); break;
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -480,10 +501,10 @@ hipError_t launch_topk_zero(uint64_t *p, int64_t n, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[4], hipStream_t s) {
-    if (pass == 0) return launch_pass_dt<0>(p, range, s);
-    if (pass == 1) return launch_pass_dt<1>(p, range, s);
-    return launch_pass_dt<2>(p, range, s);
+hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[kKinds + 1], hipStream_t s) {
+    if (pass == 0) return launch_pass_kinds<0>(p, range, s);
+    if (pass == 1) return launch_pass_kinds<1>(p, range, s);
+    return launch_pass_kinds<2>(p, range, s);
 }
 
 hipError_t launch_topk_select(const TopkParams &p, int level, hipStream_t s) {

@@ -92,7 +92,9 @@ def special_pair(n: int, code: int, seed: int, special_frac: float = 1e-3, rel_n
 def assert_parity(got: dict, ref: dict, ctx: str = "") -> None:
     for k, v in ref.items():
         g = got[k]
-        if k in NONNEG_SUMS:
+        if isinstance(v, float) and math.isinf(v):
+            assert g == v, f"{ctx} {k}: gpu {g!r} oracle {v!r}"
+        elif k in NONNEG_SUMS:
             assert abs(g - v) <= REL_TOL * abs(v), f"{ctx} {k}: gpu {g!r} oracle {v!r}"
         elif k == "sum_gt":
             scale = math.sqrt(ref["sum_g2"] * ref["sum_t2"])

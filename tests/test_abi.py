@@ -48,11 +48,12 @@ def test_struct_layouts():
     assert B.Signature.max_abs.offset == 8 * (10 + 8 + 3 + 64)
     assert B.Signature.sum_gt.offset == 784 - 8
     assert ctypes.sizeof(B.TopK) == 48
+    assert ctypes.sizeof(B.MixedPair) == 32
 
 
 def test_abi_version_and_strerror():
     L = P.lib()
-    assert L.peat_abi_version() == 2
+    assert L.peat_abi_version() == 3
     for code in range(0, -8, -1):
         assert L.peat_strerror(code)
     assert L.peat_strerror(-99) == b"unknown error code"
@@ -166,6 +167,36 @@ def test_topk_validation_codes():
     assert L.peat_topk_mean_batched(None, -1, 1, 10, outs) == B.EINVAL
     pairs = (B.Pair * 1)(B.Pair(None, None, 4, 0, 0))
     assert L.peat_topk_mean_batched(pairs, 1, 1, 10, outs) == B.EINVAL                    # NULL tensors
+
+
+def test_mixed_pair_validation_codes():
+    L = P.lib()
+    b = B.Bins(-40, 24, 64, 0)
+    th = B.Thresholds()
+    out = B.Signature()
+    F32, F16, BF16, F64 = B.F32, B.F16, B.BF16, B.F64
+    # the golden side is never binary64; the formats must nest
+    for g, t in [(F64, F32), (F64, F64), (F16, BF16), (BF16, F16), (F32, 9), (-1, F32)]:
+        assert L.peat_signature_mixed(None, g, None, t, 0, ctypes.byref(b), ctypes.byref(th),
+                                      ctypes.byref(out)) == B.EDTYPE, (g, t)
+    assert L.peat_signature_mixed(None, F32, None, F64, 4, ctypes.byref(b), ctypes.byref(th),
+                                  ctypes.byref(out)) == B.EINVAL          # NULL tensors
+    assert L.peat_signature_mixed(None, F32, None, F64, -1, ctypes.byref(b), ctypes.byref(th),
+                                  ctypes.byref(out)) == B.EINVAL
+    assert L.peat_signature_mixed(None, F32, None, F64, 0, ctypes.byref(b), ctypes.byref(th), None) == B.EINVAL
+    assert L.peat_signature_mixed(16, F32, 20, F64, 4, ctypes.byref(b), ctypes.byref(th),
+                                  ctypes.byref(out)) == B.EINVAL          # test not 8-byte aligned
+    # binary64 is not a same-type pair type
+    assert _sig_rc(dtype=F64) == B.EDTYPE
+    outs = (B.Signature * 2)()
+    pairs = (B.MixedPair * 2)(B.MixedPair(None, None, 0, F32, F64), B.MixedPair(None, None, 0, F16, BF16))
+    assert L.peat_signature_mixed_batched(pairs, 2, ctypes.byref(b), ctypes.byref(th), outs) == B.EDTYPE
+    assert L.peat_signature_mixed_batched(None, 0, ctypes.byref(b), ctypes.byref(th), None) == B.OK
+    assert L.peat_signature_mixed_batched(None, -1, ctypes.byref(b), ctypes.byref(th), None) == B.EINVAL
+    touts = (B.TopK * 2)()
+    assert L.peat_topk_mean_mixed_batched(pairs, 2, 1, 10, touts) == B.EDTYPE
+    assert L.peat_topk_mean_mixed_batched(pairs, 1, 0, 10, touts) == B.EINVAL          # num < 1
+    assert L.peat_topk_mean_mixed_batched(None, 0, 1, 10, touts) == B.OK
 
 
 def test_finalize_stats_host():

@@ -292,3 +292,16 @@ def test_topk_mixed_with_exactly_widened_test_is_the_same_type_score():
     (-1, F32, False)])
 def test_type_rules(gdt, tdt, ok):
     assert oracle.signature_mixed_rc(gdt, tdt) == (oracle.OK if ok else oracle.EDTYPE)
+
+
+def test_subnormal_binary64_errors_lie_below_every_bin():
+    # a zero golden against binary64 subnormals: errors below 2^-1022, which
+    # the histogram counts under its lowest bin; the top-k orders them
+    g = np.zeros(6, np.float32)
+    t = np.array([0.0, 5e-324, 2 * 5e-324, -3 * 5e-324, 2.0 ** -1030, 2.0 ** -1022])
+    s = oracle.signature_mixed(g, t, bins=(-1022, 0, 1), thresholds=())
+    assert s["hist_zero"] == 1 and s["hist_under"] == 4 and s["hist"][0] == 1
+    assert s["max_abs"] == 2.0 ** -1022 and s["argmax_abs"] == 5
+    r = oracle.topk_mixed(g, t, num=1, den=2)          # k = 3: 2^-1022, 2^-1030, 3 * 2^-1074
+    assert r["k"] == 3 and r["kth_value"] == 3 * 5e-324 and r["count_above"] == 2
+    assert r["sum_topk"] == 2.0 ** -1022 + 2.0 ** -1030 + 3 * 5e-324
