@@ -18,10 +18,13 @@ Prints ONE JSON line on stdout (everything else goes to stderr):
 
 Also reported: the read ceiling of the same box (peat_stream_read over a
 16 GiB buffer with the chunk pass's access pattern) and the signature chunk
-pass as a fraction of it; per-step times (median, min, max).
+pass as a fraction of it; per-step times (median, min, max); the top-10%
+error mean of the workload; the signature of mixed-precision pairs (FP32
+golden against FP64 and FP16 outputs).
 
 Modes used to produce the committed profiles: --copy-calibration (a plain
-device copy of known size, for scaling the HBM byte counters).
+device copy of known size, for scaling the HBM byte counters), --mixed-only
+(the mixed-precision measurement alone).
 """
 from __future__ import annotations
 
@@ -234,6 +237,42 @@ def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
             "what": "peat_topk_mean_batched, num/den = 1/10, kernel time (excludes the host wait between passes 2 and 3)"}
 
 
+def mixed_measure(torch, P, reps: int = 5, count: int = 64, shape=(4096, 4096)):
+    """Signature of mixed-precision pairs (Section III-C): FP32 golden outputs
+    against the same outputs in FP64 (a few FP32 ulps of rounding-error-like
+    noise) and in FP16 (the FP16 cast); count pairs of the given shape.  Best
+    of reps of the chunk pass, from the library's kernel events."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2609)
+    golden = [torch.randn(shape, device="cuda", generator=g) for _ in range(count)]
+    res = {}
+    for name, make in (("f32_vs_f64", lambda x: x.double() * (1 + 2.0 ** -23 * torch.randn(
+                            shape, device="cuda", dtype=torch.float64, generator=g))),
+                       ("f32_vs_f16", lambda x: x.half())):
+        tests = [make(x) for x in golden]
+        pairs = list(zip(golden, tests))
+        nbytes = sum(x.numel() * x.element_size() + t.numel() * t.element_size() for x, t in pairs)
+        P.signature_mixed_batched(pairs)                           # warm-up
+        P.profile_enable(True)
+        P.profile_read(P.K_SIG_CHUNK)
+        best = None
+        for _ in range(reps):
+            P.signature_mixed_batched(pairs)
+            ms, n = P.profile_read(P.K_SIG_CHUNK)
+            best = ms / n if best is None else min(best, ms / n)
+        P.profile_enable(False)
+        gbps = nbytes / (best / 1e3) / 1e9
+        res[name] = {"ms": round(best, 4), "bytes": nbytes, "GBps": round(gbps, 1),
+                     "frac_of_hbm_peak": round(gbps / HBM_PEAK_GBS, 4),
+                     "bytes_per_element": tests[0].element_size() + golden[0].element_size()}
+        del tests, pairs
+        torch.cuda.empty_cache()
+    res["config"] = f"{count} pairs of {list(shape)} (FP32 golden, N(0,1))"
+    del golden
+    torch.cuda.empty_cache()
+    return res
+
+
 def read_ceiling(torch, P, stream, gib: int = 16, reps: int = 5):
     """GB/s of peat_stream_read over a gib-GiB buffer (best of reps)."""
     buf = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
@@ -279,6 +318,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="GIB")
     ap.add_argument("--no-read-ceiling", action="store_true")
     ap.add_argument("--no-topk", action="store_true")
+    ap.add_argument("--no-mixed", action="store_true")
+    ap.add_argument("--mixed-only", action="store_true", help="only the mixed-precision measurement")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -292,6 +333,10 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(torch, args.copy_calibration, 5)
+        return
+    if args.mixed_only:
+        torch.cuda.set_device(0)
+        print(json.dumps({"mixed_precision": mixed_measure(torch, P)}), flush=True)
         return
 
     torch.cuda.set_device(0)
@@ -386,6 +431,11 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
+    if not args.no_mixed:
+        log("mixed-precision pairs ...")
+        del wl, prep_pairs, d_out
+        torch.cuda.empty_cache()
+        out["mixed_precision"] = mixed_measure(torch, P)
     print(json.dumps(out), flush=True)
 
 
