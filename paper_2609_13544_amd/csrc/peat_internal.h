@@ -19,10 +19,14 @@ constexpr int kMaxChunkLog2 = 18;                  // 262144 elements: 1024 per 
 constexpr int kInjSegLog2 = 20;                    // injector segment: 2^20 elements
 
 // Chunk size of a pair depends on n only, so that a pair's partition (and
-// hence its binary64 summation tree) is the same in single and batched calls:
-// about 256 chunks per pair, clamped to [2^12, 2^18] elements.
+// hence its binary64 summation tree) is the same in single and batched calls.
+// Below 2^22 elements a pair gets about 256 chunks (a lone pair still spreads
+// over many CUs); from 2^22 on about 64, whose longer blocks amortise the
+// per-chunk set-up and epilogue (batches of 2^24-element pairs run 10-13 %
+// faster than with 256); clamped to [2^12, 2^18] elements.
 inline int chunk_log2_for(int64_t n) {
-    int64_t per = (n + 255) / 256;
+    const int64_t target = n >= (int64_t(1) << 22) ? 64 : 256;
+    int64_t per = (n + target - 1) / target;
     int l = 0;
     while (l < 62 && (int64_t(1) << l) < per) ++l;
     if (l < kMinChunkLog2) l = kMinChunkLog2;
