@@ -17,6 +17,7 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     __shared__ int64_t si[kWaves][5];
     __shared__ uint64_t su[kWaves][2 + kCnt + PEAT_MAX_THRESHOLDS];
     __shared__ uint64_t sh_hist[kHistSlots];
+    __shared__ uint64_t sh_hwave[kWaves][kHistSlots];
 
     // binary64 sums: each thread a fixed strided subset in order, then a fixed tree
     double s[6] = {0, 0, 0, 0, 0, 0};
@@ -41,10 +42,36 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
 #pragma unroll
         for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) cn[kCnt + j] += p.mism[j];
     }
-    // histogram: thread t < slots sums slot t over the chunks
+    // histogram: wave w sums chunks w, w + 4, ... (lane l: slots l and 64 + l),
+    // eight chunks' loads in flight per step; the waves are added in order
+    {
+        uint64_t h0 = 0, h1 = 0;
+        const bool two = lane < kHistSlots - 64;
+        int c = wave;
+        for (; c + 7 * kWaves < m; c += 8 * kWaves) {
+            uint32_t a[8], b[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                a[u] = parts[c + u * kWaves].hist[lane];
+                b[u] = two ? parts[c + u * kWaves].hist[64 + lane] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                h0 += a[u];
+                h1 += b[u];
+            }
+        }
+        for (; c < m; c += kWaves) {
+            h0 += parts[c].hist[lane];
+            if (two) h1 += parts[c].hist[64 + lane];
+        }
+        sh_hwave[wave][lane] = h0;
+        if (two) sh_hwave[wave][64 + lane] = h1;
+    }
+    __syncthreads();
     if (tid < kHistSlots) {
         uint64_t h = 0;
-        for (int c = 0; c < m; ++c) h += parts[c].hist[tid];
+        for (int w = 0; w < kWaves; ++w) h += sh_hwave[w][tid];
         sh_hist[tid] = h;
     }
 #pragma unroll
