@@ -126,10 +126,10 @@ def lib():
                                             ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_TopK)]
             L.oracle_stats.restype = ctypes.c_int
             L.oracle_stats.argtypes = [ctypes.POINTER(_Sig), ctypes.POINTER(_Stats)]
-            L.oracle_philox4x64_10.restype = None
-            L.oracle_philox4x64_10.argtypes = [
-                ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64),
-                ctypes.POINTER(ctypes.c_uint64)]
+            L.oracle_philox4x32_10.restype = None
+            L.oracle_philox4x32_10.argtypes = [
+                ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_uint32),
+                ctypes.POINTER(ctypes.c_uint32)]
             L.oracle_rate_threshold.restype = ctypes.c_uint64
             L.oracle_rate_threshold.argtypes = [ctypes.c_double, ctypes.POINTER(ctypes.c_int)]
             L.oracle_inject_decide.restype = ctypes.c_int
@@ -313,11 +313,12 @@ def stats(sig: dict) -> dict:
     return {k: float(getattr(st, k)) for k, _ in _Stats._fields_}
 
 
-def philox4x64_10(counter, key):
-    c = (ctypes.c_uint64 * 4)(*[int(x) & (2**64 - 1) for x in counter])
-    k = (ctypes.c_uint64 * 2)(*[int(x) & (2**64 - 1) for x in key])
-    o = (ctypes.c_uint64 * 4)()
-    lib().oracle_philox4x64_10(c, k, o)
+def philox4x32_10(counter, key):
+    """One Philox4x32-10 block: four 32-bit counter words, two key words."""
+    c = (ctypes.c_uint32 * 4)(*[int(x) & 0xFFFFFFFF for x in counter])
+    k = (ctypes.c_uint32 * 2)(*[int(x) & 0xFFFFFFFF for x in key])
+    o = (ctypes.c_uint32 * 4)()
+    lib().oracle_philox4x32_10(c, k, o)
     return [int(x) for x in o]
 
 

@@ -57,7 +57,8 @@
  *
  * Every field has a pin in the CPU test suite (closed forms, brute force over
  * the fp16 grid with exact rational arithmetic, math.fsum, torch float64
- * library routines, numpy's Philox4x64-10).
+ * library routines, the Random123 known-answer vectors and rocRAND's
+ * Philox4x32-10).
  */
 #include <math.h>
 #include <stdint.h>
@@ -444,21 +445,21 @@ int oracle_stats(const oracle_sig_t *s, oracle_stats_t *st) {
 }
 
 /* ------------------------------------------------------------------------- */
-/* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as    */
-/* easy as 1, 2, 3", SC'11): ten rounds of two 64x64->128 multiplications     */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as    */
+/* easy as 1, 2, 3", SC'11): ten rounds of two 32x32->64 multiplications     */
 /* with the Weyl-sequence key schedule.                                      */
 /* ------------------------------------------------------------------------- */
 
-void oracle_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4]) {
-    const uint64_t M0 = 0xD2E7470EE14C6C93ULL, M1 = 0xCA5A826395121157ULL;
-    const uint64_t W0 = 0x9E3779B97F4A7C15ULL, W1 = 0xBB67AE8584CAA73BULL;
-    uint64_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
-    uint64_t k0 = key_in[0], k1 = key_in[1];
+void oracle_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4]) {
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+    uint32_t k0 = key_in[0], k1 = key_in[1];
     for (int round = 0; round < 10; ++round) {
-        unsigned __int128 p0 = (unsigned __int128)M0 * c0;
-        unsigned __int128 p1 = (unsigned __int128)M1 * c2;
-        uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
-        uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+        uint64_t p0 = (uint64_t)M0 * c0;
+        uint64_t p1 = (uint64_t)M1 * c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
         c0 = hi1 ^ c1 ^ k0;
         c1 = lo1;
         c2 = hi0 ^ c3 ^ k1;
@@ -490,32 +491,39 @@ uint64_t oracle_rate_threshold(double rate, int *all) {
     return (uint64_t)ldexp(rate, 64);
 }
 
-static void philox_seeded(uint64_t seed, uint64_t c0, uint64_t c1, uint64_t out[4]) {
-    uint64_t ctr[4] = {c0, c1, 0, 0};
-    uint64_t key[2] = {seed, 0};
-    oracle_philox4x64_10(ctr, key, out);
+/* Block number c of stream s under seed: Philox4x32-10 with the key
+ * (lo32(seed), hi32(seed)) at the counter (lo32(c), hi32(c), s, 0). */
+static void philox_seeded(uint64_t seed, uint64_t c, uint32_t s, uint32_t out[4]) {
+    uint32_t ctr[4] = {(uint32_t)c, (uint32_t)(c >> 32), s, 0};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    oracle_philox4x32_10(ctr, key, out);
 }
 
-/* The per-element uniform U_i.  Its top byte is byte (i mod 32) of the
- * 32-byte block A = Philox(key=(seed,0), ctr=(i/32, 0, 0, 0)), bytes numbered
+/* The 64-bit word h (0 or 1) of a block: words 2h (low half) and 2h+1. */
+static uint64_t block_word64(const uint32_t B[4], int h) {
+    return (uint64_t)B[2 * h] | ((uint64_t)B[2 * h + 1] << 32);
+}
+
+/* The per-element uniform U_i.  Its top byte is byte (i mod 16) of the
+ * 16-byte block A of stream 0 at block number i/16, bytes numbered
  * little-endian through words 0..3; its low 56 bits are the low 56 bits of
- * word (i mod 4) of B = Philox(key, ctr=(i/4, 1, 0, 0)). */
-static uint64_t uniform_of(const uint64_t A[4], const uint64_t B[4], int64_t i) {
-    int byte = (int)(i & 31);
-    uint64_t top = (A[byte >> 3] >> (8 * (byte & 7))) & 0xFF;
-    uint64_t low = B[i & 3] & ((1ULL << 56) - 1);
+ * the 64-bit word (i mod 2) of the block B of stream 1 at block number i/2. */
+static uint64_t uniform_of(const uint32_t A[4], const uint32_t B[4], int64_t i) {
+    int byte = (int)(i & 15);
+    uint64_t top = (A[byte >> 2] >> (8 * (byte & 3))) & 0xFF;
+    uint64_t low = block_word64(B, (int)(i & 1)) & ((1ULL << 56) - 1);
     return (top << 56) | low;
 }
 
-/* The flipped bit of element i: y = word 0 of Philox(key, ctr=(i, 2, 0, 0));
- * j = floor(hi32(y) * popcount(mask) / 2^32) selects the j-th lowest set bit
- * of the mask. */
+/* The flipped bit of element i: y = word 0 of the block of stream 2 at block
+ * number i; j = floor(y * popcount(mask) / 2^32) selects the j-th lowest set
+ * bit of the mask. */
 static int chosen_bit(uint64_t seed, int64_t i, uint64_t mask) {
-    uint64_t C[4];
+    uint32_t C[4];
     philox_seeded(seed, (uint64_t)i, 2, C);
     uint64_t p = 0;
     for (int b = 0; b < 64; ++b) p += (mask >> b) & 1;
-    uint64_t j = ((C[0] >> 32) * p) >> 32;
+    uint64_t j = ((uint64_t)C[0] * p) >> 32;
     for (int b = 0; b < 64; ++b) {
         if ((mask >> b) & 1) {
             if (j == 0) return b;
@@ -539,9 +547,9 @@ int oracle_inject_decide(int64_t i, int dtype, uint64_t seed, double rate, uint6
     if (rc) return rc;
     int all;
     uint64_t T = oracle_rate_threshold(rate, &all);
-    uint64_t A[4], B[4];
-    philox_seeded(seed, (uint64_t)i >> 5, 0, A);
-    philox_seeded(seed, (uint64_t)i >> 2, 1, B);
+    uint32_t A[4], B[4];
+    philox_seeded(seed, (uint64_t)i >> 4, 0, A);
+    philox_seeded(seed, (uint64_t)i >> 1, 1, B);
     int flip = all || uniform_of(A, B, i) < T;
     if (flip && bit) *bit = chosen_bit(seed, i, mask);
     return flip;
@@ -556,10 +564,10 @@ int64_t oracle_inject(void *x, int64_t n, int dtype, uint64_t seed, double rate,
     int all;
     uint64_t T = oracle_rate_threshold(rate, &all);
     int64_t flips = 0;
-    uint64_t A[4], B[4];
+    uint32_t A[4], B[4];
     for (int64_t i = 0; i < n; ++i) {
-        if ((i & 31) == 0 || i == 0) philox_seeded(seed, (uint64_t)i >> 5, 0, A);
-        if ((i & 3) == 0 || i == 0) philox_seeded(seed, (uint64_t)i >> 2, 1, B);
+        if ((i & 15) == 0) philox_seeded(seed, (uint64_t)i >> 4, 0, A);
+        if ((i & 1) == 0) philox_seeded(seed, (uint64_t)i >> 1, 1, B);
         if (!(all || uniform_of(A, B, i) < T)) continue;
         int b = chosen_bit(seed, i, mask);
         if (dtype == ORACLE_F32) {
@@ -702,10 +710,10 @@ int64_t oracle_inject_model(void *x, int64_t n, int dtype, uint64_t seed, double
     int all;
     uint64_t T = oracle_rate_threshold(rate, &all);
     int64_t count = 0;
-    uint64_t A[4], B[4];
+    uint32_t A[4], B[4];
     for (int64_t i = 0; i < n; ++i) {
-        if ((i & 31) == 0) philox_seeded(seed, (uint64_t)i >> 5, 0, A);
-        if ((i & 3) == 0) philox_seeded(seed, (uint64_t)i >> 2, 1, B);
+        if ((i & 15) == 0) philox_seeded(seed, (uint64_t)i >> 4, 0, A);
+        if ((i & 1) == 0) philox_seeded(seed, (uint64_t)i >> 1, 1, B);
         if (!(all || uniform_of(A, B, i) < T)) continue;
         store_bits(x, i, dtype, model_bits(model, dtype, element_bits(x, i, dtype), seed, i, mask));
         ++count;
@@ -714,12 +722,12 @@ int64_t oracle_inject_model(void *x, int64_t n, int dtype, uint64_t seed, double
 }
 
 /* Position mode (the paper's num_pos).  Draw j = 0, 1, 2, ... gives the
- * block W = Philox(key=(seed,0), ctr=(j, 3, 0, 0)) and the index
- * p_j = floor(W[0] * n / 2^64); the positions are the first num_pos distinct
- * p_j in order of appearance.  Position m (drawn at j) becomes +0 (model 1),
- * the canonical NaN (model 3), a bit flip with the rate mode's bit rule
- * (model 0), or (model 2, random value) the uncorrupted tensor's value at
- * index floor(W[1] * n / 2^64) -- a value drawn from the tensor's own
+ * block W of stream 3 at block number j, its 64-bit words W0 and W1, and the
+ * index p_j = floor(W0 * n / 2^64); the positions are the first num_pos
+ * distinct p_j in order of appearance.  Position m (drawn at j) becomes +0
+ * (model 1), the canonical NaN (model 3), a bit flip with the rate mode's bit
+ * rule (model 0), or (model 2, random value) the uncorrupted tensor's value
+ * at index floor(W1 * n / 2^64) -- a value drawn from the tensor's own
  * distribution.  0 <= num_pos <= min(n, 4096).  positions (optional) gets
  * the positions in order.  Returns num_pos or a negative error code. */
 int64_t oracle_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed, int model,
@@ -733,14 +741,14 @@ int64_t oracle_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed, i
     int64_t pos[ORACLE_MAX_POSITIONS], src[ORACLE_MAX_POSITIONS];
     int64_t m = 0;
     for (uint64_t j = 0; m < num_pos; ++j) {
-        uint64_t W[4];
+        uint32_t W[4];
         philox_seeded(seed, j, 3, W);
-        int64_t p = (int64_t)(((unsigned __int128)W[0] * (uint64_t)n) >> 64);
+        int64_t p = (int64_t)(((unsigned __int128)block_word64(W, 0) * (uint64_t)n) >> 64);
         int seen = 0;
         for (int64_t q = 0; q < m; ++q) seen |= pos[q] == p;
         if (seen) continue;
         pos[m] = p;
-        src[m] = (int64_t)(((unsigned __int128)W[1] * (uint64_t)n) >> 64);
+        src[m] = (int64_t)(((unsigned __int128)block_word64(W, 1) * (uint64_t)n) >> 64);
         ++m;
     }
     /* every source is read before any position is written */

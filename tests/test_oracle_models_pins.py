@@ -7,10 +7,10 @@ num_pos corrupted positions):
   bit patterns;
 * the rate-mode zero / NaN models choose exactly the elements the bit-flip
   injector flips (same decisions), and the bit-flip model equals it;
-* the position mode against numpy's Philox4x64-10: the first num_pos distinct
-  floor(W0 * n / 2^64) over the blocks at counters (j, 3, 0, 0), random values
-  from floor(W1 * n / 2^64) of the uncorrupted tensor, uniformity of the
-  positions, and the edge cases."""
+* the position mode against rocRAND's Philox4x32-10: the first num_pos
+  distinct floor(W0 * n / 2^64) over the blocks of stream 3 (W0, W1 their
+  64-bit words), random values from floor(W1 * n / 2^64) of the uncorrupted
+  tensor, uniformity of the positions, and the edge cases."""
 from __future__ import annotations
 
 import numpy as np
@@ -18,22 +18,9 @@ import pytest
 import torch
 
 import oracle
+from tests import philox_ref
 
-M64 = 2 ** 64 - 1
 F32, F16, BF16 = oracle.F32, oracle.F16, oracle.BF16
-
-
-def _np_philox_block(counter, key):
-    # numpy increments the counter before each block: block c is produced by
-    # a generator whose counter is set to c - 1
-    c = list(counter)
-    for w in range(4):
-        if c[w] > 0:
-            c[w] -= 1
-            break
-        c[w] = M64
-    bg = np.random.Philox(counter=np.array(c, dtype=np.uint64), key=np.array(key, dtype=np.uint64))
-    return [int(x) for x in bg.random_raw(4)]
 
 
 # ---------------------------------------------------------------------------
@@ -130,22 +117,27 @@ def test_rate_model_validation():
 # ---------------------------------------------------------------------------
 # position mode
 # ---------------------------------------------------------------------------
-def _np_positions(seed, n, num_pos):
-    pos, src, j = [], [], 0
+def _ref_positions(seed, n, num_pos):
+    pos, src, seen, j = [], [], set(), 0
     while len(pos) < num_pos:
-        w = _np_philox_block((j, 3, 0, 0), (seed, 0))
-        p = (w[0] * n) >> 64
-        if p not in pos:
-            pos.append(p)
-            src.append((w[1] * n) >> 64)
-        j += 1
+        W = philox_ref.seeded(seed, np.arange(j, j + 256), 3).astype(np.uint64)
+        for w in W:
+            w0 = int(w[0]) | (int(w[1]) << 32)
+            w1 = int(w[2]) | (int(w[3]) << 32)
+            p = (w0 * n) >> 64
+            if p not in seen and len(pos) < num_pos:
+                seen.add(p)
+                pos.append(p)
+                src.append((w1 * n) >> 64)
+        j += 256
     return pos, src
 
 
+@pytest.mark.skipif(not philox_ref.available(), reason="hipcc (for rocRAND's header) not found")
 @pytest.mark.parametrize("seed", [0, 7, 2 ** 63 + 5])
 @pytest.mark.parametrize("n,num_pos", [(1, 1), (5, 5), (100, 3), (100000, 5), (3000, 1000), (10 ** 9, 4096)])
-def test_positions_against_numpy_philox(seed, n, num_pos):
-    want_pos, want_src = _np_positions(seed, n, num_pos)
+def test_positions_against_rocrand_philox(seed, n, num_pos):
+    want_pos, want_src = _ref_positions(seed, n, num_pos)
     assert len(set(want_pos)) == num_pos and all(0 <= p < n for p in want_pos)
     if n > 10 ** 6:
         # positions only: an oracle call on a dummy tensor is not needed to

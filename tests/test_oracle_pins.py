@@ -2,9 +2,9 @@
 
 Each test fixes a field (or the injector's draw) by something other than the
 oracle: exact integer/rational arithmetic, brute force over every binary16 and
-bfloat16 value, ranks in the sorted set of representable values, numpy's
-Philox4x64-10, torch's float64 isclose/norm/cosine/var, math.fsum, IEEE-754
-closed forms, and the paper's own statement about exponent bit flips
+bfloat16 value, ranks in the sorted set of representable values, the
+Philox4x32-10 known-answer vectors and rocRAND's implementation, torch's
+float64 isclose/norm/cosine/var, math.fsum, IEEE-754 closed forms, and the paper's own statement about exponent bit flips
 (Section II-B "Error Models", fixture in tests/golden/).
 """
 from __future__ import annotations
@@ -18,10 +18,12 @@ import pytest
 import torch
 
 import oracle
+from tests import philox_ref
 from tests import exact_ref as X
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 M64 = (1 << 64) - 1
+M32 = (1 << 32) - 1
 
 SUM_FIELDS = ("sum_abs", "sum_sq", "sum_rel", "sum_g2", "sum_t2", "sum_gt")
 
@@ -44,36 +46,34 @@ def _assert_sig_equal(sig: dict, ref: dict, ctx: str = ""):
 
 
 # ---------------------------------------------------------------------------
-# Philox4x64-10 against numpy's implementation.
-# numpy increments the counter before each block, so block c is produced by a
-# generator whose counter is set to c - 1 (mod 2^256).
+# Philox4x32-10 against the published known-answer vectors (Random123, Salmon
+# et al., SC'11) and rocRAND's implementation.
 # ---------------------------------------------------------------------------
-def _np_philox_block(counter, key):
-    c = list(counter)
-    # c - 1 with borrow across the four 64-bit words
-    for w in range(4):
-        if c[w] > 0:
-            c[w] -= 1
-            break
-        c[w] = M64
-    bg = np.random.Philox(counter=np.array(c, dtype=np.uint64), key=np.array(key, dtype=np.uint64))
-    return [int(x) for x in bg.random_raw(4)]
+KAT = [  # (counter, key, block)
+    ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((M32, M32, M32, M32), (M32, M32), (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
 
 
-@pytest.mark.parametrize("key", [(0, 0), (12345, 0), (0xC0FFEE00 + 5003, 0), (M64, M64), (7, 99)])
-@pytest.mark.parametrize("counter", [(0, 0, 0, 0), (1, 0, 0, 0), (5, 1, 0, 0), (123456789, 2, 0, 0),
-                                     (M64, 0, 0, 0), (M64, M64, M64, M64), (3, 4, 5, 6)])
-def test_philox_matches_numpy(counter, key):
-    assert oracle.philox4x64_10(counter, key) == _np_philox_block(counter, key)
+@pytest.mark.parametrize("counter,key,block", KAT)
+def test_philox_known_answers(counter, key, block):
+    assert oracle.philox4x32_10(counter, key) == list(block)
 
 
-def test_philox_consecutive_blocks_match_numpy_stream():
-    key = (0xDEADBEEF, 0)
-    bg = np.random.Philox(counter=np.array([M64, M64, M64, M64], dtype=np.uint64),
-                          key=np.array(key, dtype=np.uint64))
-    raw = [int(x) for x in bg.random_raw(4 * 64)]
-    for c in range(64):
-        assert oracle.philox4x64_10((c, 0, 0, 0), key) == raw[4 * c:4 * c + 4]
+needs_ref = pytest.mark.skipif(not philox_ref.available(), reason="hipcc (for rocRAND's header) not found")
+
+
+@needs_ref
+def test_philox_matches_rocrand_on_random_counters_and_keys():
+    rng = np.random.default_rng(2609)
+    ctr = rng.integers(0, 1 << 32, (300, 4), dtype=np.uint64).astype(np.uint32)
+    key = rng.integers(0, 1 << 32, (300, 2), dtype=np.uint64).astype(np.uint32)
+    ctr[:20] = [[c, 0, s, 0] for c in range(5) for s in range(4)]      # the library's counters
+    want = philox_ref.blocks(ctr, key)
+    for i in range(ctr.shape[0]):
+        assert oracle.philox4x32_10(ctr[i], key[i]) == [int(x) for x in want[i]], i
 
 
 # ---------------------------------------------------------------------------
@@ -417,30 +417,21 @@ def test_signature_argument_validation():
 # ---------------------------------------------------------------------------
 # Injector.
 # ---------------------------------------------------------------------------
-def _np_stream(key, start_counter, nblocks):
-    c = list(start_counter)
-    for w in range(4):
-        if c[w] > 0:
-            c[w] -= 1
-            break
-        c[w] = M64
-    bg = np.random.Philox(counter=np.array(c, dtype=np.uint64), key=np.array(key, dtype=np.uint64))
-    return bg.random_raw(4 * nblocks).reshape(nblocks, 4)
-
-
-def _np_flips(n, seed, rate, mask):
-    """Flip set and bits from numpy's Philox and the per-element uniform's
-    composition (top byte from the (i/32, 0) block, low 56 bits from the
-    (i/4, 1) block)."""
-    key = (seed, 0)
-    A = _np_stream(key, (0, 0, 0, 0), (n + 31) // 32)
-    B = _np_stream(key, (0, 1, 0, 0), (n + 3) // 4)
+def _ref_flips(n, seed, rate, mask):
+    """Flip set and bits from rocRAND's Philox4x32-10 and the per-element
+    uniform's composition: top byte = byte (i mod 16) of block i/16 of stream
+    0; low 56 bits = 64-bit word (i mod 2) of block i/2 of stream 1; the bit
+    from word 0 of block i of stream 2."""
     i = np.arange(n, dtype=np.uint64)
-    byte = (i & np.uint64(31))
-    word = A[(i >> np.uint64(5)).astype(np.int64), (byte >> np.uint64(3)).astype(np.int64)]
-    top = (word >> (np.uint64(8) * (byte & np.uint64(7)))) & np.uint64(0xFF)
-    low = B[(i >> np.uint64(2)).astype(np.int64), (i & np.uint64(3)).astype(np.int64)] & np.uint64((1 << 56) - 1)
-    U = (top << np.uint64(56)) | low
+    A = philox_ref.seeded(seed, np.arange((n + 15) // 16), 0)
+    B = philox_ref.seeded(seed, np.arange((n + 1) // 2), 1).astype(np.uint64)
+    byte = (i & np.uint64(15)).astype(np.int64)
+    word = A[(i >> np.uint64(4)).astype(np.int64), byte >> 2].astype(np.uint64)
+    top = (word >> (np.uint64(8) * (byte & 3).astype(np.uint64))) & np.uint64(0xFF)
+    h = (i & np.uint64(1)).astype(np.int64)
+    rows = B[(i >> np.uint64(1)).astype(np.int64)]
+    w64 = rows[np.arange(n), 2 * h] | (rows[np.arange(n), 2 * h + 1] << np.uint64(32))
+    U = (top << np.uint64(56)) | (w64 & np.uint64((1 << 56) - 1))
     if rate >= 1:
         flip = np.ones(n, bool)
     else:
@@ -448,22 +439,22 @@ def _np_flips(n, seed, rate, mask):
         flip = U < np.uint64(T) if T < (1 << 64) else np.ones(n, bool)
     setbits = [b for b in range(64) if (mask >> b) & 1]
     p = len(setbits)
-    bits = {}
-    for idx in np.nonzero(flip)[0]:
-        y = int(_np_stream(key, (int(idx), 2, 0, 0), 1)[0, 0])
-        j = ((y >> 32) * p) >> 32
-        bits[int(idx)] = setbits[j]
+    idx = np.nonzero(flip)[0]
+    C = philox_ref.seeded(seed, idx, 2) if idx.size else np.zeros((0, 4), np.uint32)
+    bits = {int(k): setbits[(int(C[r, 0]) * p) >> 32] for r, k in enumerate(idx)}
     return flip, bits
 
 
-@pytest.mark.parametrize("rate,n", [(0.01, 20000), (2e-3, 50000), (0.3, 3000), (2.0 ** -56 * 5, 1000)])
-def test_inject_matches_numpy_philox(rate, n):
-    seed = 0xC0FFEE00 + 17
+@needs_ref
+@pytest.mark.parametrize("rate,n", [(0.01, 20000), (2e-3, 50000), (0.3, 3000), (2.0 ** -56 * 5, 1000),
+                                    (1e-3, 33)])
+def test_inject_matches_rocrand_philox(rate, n):
+    seed = 0xC0FFEE00 + 17 + (5 << 40)
     mask = 0x7F800000
     x = np.random.default_rng(1).standard_normal(n).astype(np.float32).view(np.uint32)
     before = x.copy()
     cnt = oracle.inject(x, seed=seed, rate=rate, mask=mask)
-    flip, bits = _np_flips(n, seed, rate, mask)
+    flip, bits = _ref_flips(n, seed, rate, mask)
     changed = before != x
     assert np.array_equal(changed, flip) and cnt == int(flip.sum())
     for idx, b in bits.items():
