@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PEAT_ABI_VERSION 3
+#define PEAT_ABI_VERSION 4
 #define PEAT_MAX_THRESHOLDS 8
 #define PEAT_MAX_BINS 64
 
@@ -256,15 +256,17 @@ int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
 int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
                                  int32_t den, peat_topk_t *outs);
 
-/* Random bit flip in place (Section II-B).  Element i flips iff its 64-bit
- * uniform U_i < floor(rate * 2^64) (every element if rate >= 1).  U_i's top
- * byte is byte (i mod 32), little-endian, of Philox4x64-10 with key
- * (seed, 0) at counter (i/32, 0, 0, 0); its low 56 bits are the low 56 bits of
- * word (i mod 4) at counter (i/4, 1, 0, 0).  A flipped element toggles the
- * j-th lowest set bit of bitmask, j = floor(hi32(y) * popcount(bitmask) / 2^32)
- * with y = word 0 at counter (i, 2, 0, 0).  Returns the number of flipped
- * elements (>= 0) or a negative PEAT_E* code.  Applying the same call twice
- * restores the tensor. */
+/* Random bit flip in place (Section II-B).  The draws come from
+ * Philox4x32-10 keyed by (lo32(seed), hi32(seed)); "block c of stream s" is
+ * its output at counter (lo32(c), hi32(c), s, 0), four 32-bit words, bytes
+ * and 64-bit words (words 2h, 2h+1) numbered little-endian.  Element i flips
+ * iff its 64-bit uniform U_i < floor(rate * 2^64) (every element if
+ * rate >= 1).  U_i's top byte is byte (i mod 16) of block i/16 of stream 0;
+ * its low 56 bits are the low 56 bits of 64-bit word (i mod 2) of block i/2
+ * of stream 1.  A flipped element toggles the j-th lowest set bit of bitmask,
+ * j = floor(y * popcount(bitmask) / 2^32) with y = word 0 of block i of
+ * stream 2.  Returns the number of flipped elements (>= 0) or a negative
+ * PEAT_E* code.  Applying the same call twice restores the tensor. */
 int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed,
                     double rate, uint64_t bitmask);
 
@@ -279,12 +281,13 @@ int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t 
 
 /* The paper's num_pos corruption (Section V-A): exactly num_pos distinct
  * positions, 0 <= num_pos <= min(n, PEAT_MAX_POSITIONS).  Draw j = 0, 1, ...
- * takes W = Philox4x64-10 with key (seed, 0) at counter (j, 3, 0, 0) and the
- * index floor(W[0] * n / 2^64); the positions are the first num_pos distinct
- * indices in order of appearance.  Each becomes +0, the quiet NaN, a bit
- * flip (peat_inject's bit rule for that index), or -- PEAT_MODEL_VALUE, a
- * value from the tensor's own distribution -- the uncorrupted tensor's value
- * at floor(W[1] * n / 2^64) of the draw that chose it.  positions (host,
+ * takes block j of stream 3 (peat_inject's generator), its 64-bit words W0
+ * and W1, and the index floor(W0 * n / 2^64); the positions are the first
+ * num_pos distinct indices in order of appearance.  Each becomes +0, the
+ * quiet NaN, a bit flip (peat_inject's bit rule for that index), or --
+ * PEAT_MODEL_VALUE, a value from the tensor's own distribution -- the
+ * uncorrupted tensor's value at floor(W1 * n / 2^64) of the draw that chose
+ * it.  positions (host,
  * num_pos entries, may be NULL) receives the positions in order.  Returns
  * num_pos or a negative code; waits for the device. */
 int64_t peat_corrupt_positions(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, int32_t model,

@@ -4,14 +4,15 @@
 //
 // Element i of a tensor flips iff its 64-bit uniform U_i is below
 // T = floor(rate * 2^64) (every element when rate >= 1).  U_i is built from
-// Philox4x64-10 (Salmon et al., SC'11) keyed by (seed, 0):
-//   top byte   = byte (i mod 32) of the block at counter (i/32, 0, 0, 0)
-//   low 56 bits = word (i mod 4) of the block at counter (i/4, 1, 0, 0)
+// Philox4x32-10 (Salmon et al., SC'11) keyed by the seed, block c of stream s
+// at counter (lo32(c), hi32(c), s, 0):
+//   top byte    = byte (i mod 16) of block i/16 of stream 0
+//   low 56 bits = 64-bit word (i mod 2) of block i/2 of stream 1
 // A flipped element toggles the j-th lowest set bit of the mask with
-// j = floor(hi32(y) * popcount(mask) / 2^32), y = word 0 at (i, 2, 0, 0).
+// j = floor(y * popcount(mask) / 2^32), y = word 0 of block i of stream 2.
 //
 // For T < 2^56 an element can only flip when its top byte is 0, so each lane
-// draws one block per 32 elements and evaluates the low bits only for the
+// draws two blocks per 32 elements and evaluates the low bits only for the
 // (1 in 256) elements whose top byte is zero.  The tensor is read and written
 // only at flipped elements.
 #include "philox.h"
@@ -45,9 +46,9 @@ constexpr int kQCap = 64 + 32 * 64;   // per-wave queue: < 64 left over + one ap
 // Low 56 bits of U_i for a queued candidate (its top byte is 0, so U_i is
 // just these bits): flip the element when they are below T.
 __device__ __forceinline__ uint32_t settle_candidate(const InjDesc &d, uint64_t i) {
-    uint64_t B[4];
-    philox(i >> 2, 1, d.seed, B);
-    const uint64_t low = B[i & 3] & ((uint64_t(1) << 56) - 1);
+    uint32_t B[4];
+    philox(i >> 1, 1, d.seed, B);
+    const uint64_t low = block_word64(B, (uint32_t)(i & 1)) & ((uint64_t(1) << 56) - 1);
     if (low < d.T) {
         flip(d, i);
         return 1;
@@ -80,15 +81,17 @@ __global__ void __launch_bounds__(kBlock) inject_kernel(InjParams P) {
             const uint32_t g = k * kBlock + threadIdx.x;
             uint32_t cand = 0;
             if (g < ngroups) {
-                uint64_t A[4];
-                philox(q0 + g, 0, d.seed, A);
-                // exact zero-byte mask of each 32-bit half: bit 7 of a byte
-                // is set iff the byte is zero; one multiply gathers bits
-                // 7, 15, 23, 31 into bits 28..31 (the other partial products
-                // land on distinct lower bits, so nothing carries)
+                // the 32 top bytes of the group: blocks 2(q0+g) and 2(q0+g)+1
+                uint32_t A[8];
+                philox(2 * (q0 + g), 0, d.seed, A);
+                philox(2 * (q0 + g) + 1, 0, d.seed, A + 4);
+                // exact zero-byte mask of each word: bit 7 of a byte is set
+                // iff the byte is zero; one multiply gathers bits 7, 15, 23,
+                // 31 into bits 28..31 (the other partial products land on
+                // distinct lower bits, so nothing carries)
 #pragma unroll
                 for (int w = 0; w < 8; ++w) {
-                    const uint32_t v = (uint32_t)(A[w >> 1] >> (32 * (w & 1)));
+                    const uint32_t v = A[w];
                     const uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v | 0x7F7F7F7Fu);
                     cand |= ((z * 0x00204081u) >> 28) << (4 * w);
                 }
@@ -121,21 +124,24 @@ __global__ void __launch_bounds__(kBlock) inject_kernel(InjParams P) {
         const uint64_t Ttop = T >> 56, Tlow = T & ((uint64_t(1) << 56) - 1);
         for (uint32_t g = threadIdx.x; g < ngroups; g += kBlock) {
             const uint64_t q = q0 + g;
-            uint64_t A[4];
-            if (!d.all) philox(q, 0, d.seed, A);
+            uint32_t A[8];
+            if (!d.all) {
+                philox(2 * q, 0, d.seed, A);
+                philox(2 * q + 1, 0, d.seed, A + 4);
+            }
             const uint64_t ibase = q << 5;
             const uint32_t cnt = (n - ibase) < 32 ? (uint32_t)(n - ibase) : 32u;
             for (uint32_t b = 0; b < cnt; ++b) {
                 const uint64_t i = ibase + b;
                 bool f = d.all;
                 if (!f) {
-                    const uint64_t top = (A[b >> 3] >> (8 * (b & 7))) & 0xFF;
+                    const uint64_t top = (A[b >> 2] >> (8 * (b & 3))) & 0xFF;
                     if (top < Ttop) {
                         f = true;
                     } else if (top == Ttop) {
-                        uint64_t B[4];
-                        philox(i >> 2, 1, d.seed, B);
-                        f = (B[i & 3] & ((uint64_t(1) << 56) - 1)) < Tlow;
+                        uint32_t B[4];
+                        philox(i >> 1, 1, d.seed, B);
+                        f = (block_word64(B, (uint32_t)(i & 1)) & ((uint64_t(1) << 56) - 1)) < Tlow;
                     }
                 }
                 if (f) {

@@ -17,11 +17,8 @@ constexpr int kSet = 8192;                       // hash set of accepted positio
 constexpr uint64_t kFree = ~uint64_t(0);
 constexpr uint64_t kMaxDraws = uint64_t(1) << 24;   // bound of the draw loop
 
-__device__ __forceinline__ uint64_t mulhi64(uint64_t a, uint64_t b) {
-    uint64_t lo, hi;
-    mulhilo64(a, b, lo, hi);
-    return hi;
-}
+// High 64 bits of the 128-bit product a * b (floor(a * b / 2^64)).
+__device__ __forceinline__ uint64_t mulhi64(uint64_t a, uint64_t b) { return __umul64hi(a, b); }
 
 __device__ __forceinline__ uint32_t load_bits(const void *x, int dtype, int64_t i) {
     return dtype == PEAT_F32 ? static_cast<const uint32_t *>(x)[i] : static_cast<const uint16_t *>(x)[i];
@@ -48,10 +45,10 @@ __global__ void __launch_bounds__(kBlock) corrupt_positions_kernel(void *x, int6
     __syncthreads();
     bool complete = false;
     for (uint64_t j0 = 0; j0 < kMaxDraws; j0 += kBlock) {
-        uint64_t W[4];
+        uint32_t W[4];
         philox(j0 + tid, 3, seed, W);
-        cp[tid] = (int64_t)mulhi64(W[0], (uint64_t)n);
-        cs[tid] = (int64_t)mulhi64(W[1], (uint64_t)n);
+        cp[tid] = (int64_t)mulhi64(block_word64(W, 0), (uint64_t)n);
+        cs[tid] = (int64_t)mulhi64(block_word64(W, 1), (uint64_t)n);
         __syncthreads();
         if (tid == 0) {
             int64_t m = m_sh;

@@ -53,7 +53,7 @@ def test_struct_layouts():
 
 def test_abi_version_and_strerror():
     L = P.lib()
-    assert L.peat_abi_version() == 3
+    assert L.peat_abi_version() == 4
     for code in range(0, -8, -1):
         assert L.peat_strerror(code)
     assert L.peat_strerror(-99) == b"unknown error code"
