@@ -1,23 +1,23 @@
-// Pass 1 of the error signature (sig_chunk), templated on the golden and
-// test element types; included by the translation units that instantiate it
-// (same-type pairs, mixed-precision pairs).
+// Pass 1 of the error signature (sig_chunk) for gfx950, templated on the
+// golden and test element types; included by the translation units that
+// instantiate it (same-type pairs in signature.hip, mixed-precision pairs in
+// mixed.hip).  Pass 2 (sig_finalize, in signature.hip) combines a pair's
+// chunk records in a fixed order and writes the peat_signature_t.
 //
-// Error-signature kernels for gfx950.
-//
-// Pass 1 (sig_chunk): one 256-thread block per fixed-size chunk of one pair.
-// Each thread streams 16-byte vectors of golden and test (4 f32 or 8 f16/bf16
-// elements) through nontemporal buffer loads, widens them exactly to binary64
-// and accumulates the signature of its elements; the chunk's record (binary64
+// One 256-thread block per fixed-size chunk of one pair.  Each thread streams
+// lane vectors of golden and test through nontemporal buffer loads: 16 bytes
+// of the wider side (4 f32, 8 f16/bf16 or 2 binary64 elements) and the
+// matching bytes of the other, widens them exactly to binary64 and
+// accumulates the signature of its elements; the chunk's record (binary64
 // partial sums, maxima with their lowest index, integer counts, histogram)
 // goes to one ChunkPartial.
 //
-// Pass 2 (sig_finalize): one block per pair combines its chunk records in a
-// fixed order and writes the peat_signature_t.
-//
 // The definitions follow the paper's FI assessment scores (Section IV-B.3:
 // error = absolute difference of golden and faulty values; max, mean,
-// variance), the closeness test of Section III-A (torch.isclose, rtol = 0)
-// and the error histograms of Section V-D.
+// variance), the closeness test of Section III-A (torch.isclose with absolute
+// and relative tolerances), the error histograms of Section V-D and, for
+// mixed pairs, the precision comparisons of Section III-C (the ULP distance
+// counted in the narrower format).
 //
 // Fast path.  A wave whose current vectors hold only "ordinary" pairs (both
 // finite, no NaN, golden nonzero, same sign, relative error below 0.5) needs
@@ -26,8 +26,8 @@
 //     case (a sign change or a zero golden gives a relative error >= 1 or
 //     NaN) together with the candidates for the maximum relative error; the
 //     exact IEEE quotient is formed only for those candidates;
-//   - reciprocals come from one hardware estimate per four elements plus a
-//     Newton step;
+//   - reciprocals come from one hardware estimate per four (or two) elements
+//     plus a Newton step;
 //   - the maxima of |err| and of the ULP distance are wave-uniform running
 //     records (the vector that first exceeded them), resolved to an element
 //     by one reload at the end of the chunk;
