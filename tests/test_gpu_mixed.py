@@ -220,3 +220,30 @@ def test_topk_and_histogram_of_subnormal_binary64_errors():
             got = P.topk_mean_mixed_batched(pairs, num, den)[0]
             assert_topk(got, oracle.topk_mixed(gb, t, gdtype=F32, tdtype=F64, num=num, den=den),
                         f"{variant} {num}/{den}")
+
+
+def test_mixed_index_beyond_2_31():
+    """64-bit indexing of a mixed pair: n > 2^31, FP32 golden zeros against a
+    binary64 test with planted values at known places (closed forms)."""
+    n = (1 << 31) + 4096 + 1000
+    base = 1 << 31
+    log(f"  mixed f32/f64 n={n}")
+    g = torch.zeros(n, dtype=torch.float32, device="cuda")
+    t = torch.zeros(n, dtype=torch.float64, device="cuda")
+    t[base + 77] = 1.0
+    t[base + 500] = -1.0                       # ties |err| = 1 with base + 77
+    t[base + 900] = float("nan")
+    t[base + 5095] = 0.5 + 2.0 ** -30          # rounds to 0.5 in FP32
+    got = P.signature_mixed(g, t, (-40, 24, 64), (1e-6, 1e-3))
+    assert got["n"] == n and got["n_nan_pairs"] == 1 and got["first_nan_index"] == base + 900
+    assert got["max_abs"] == 1.0 and got["argmax_abs"] == base + 77
+    assert got["max_ulp"] == 0x3F800000 and got["argmax_ulp"] == base + 77
+    assert got["sum_ulp"] == 2 * 0x3F800000 + 0x3F000000
+    assert got["n_rel"] == 0 and math.isnan(got["max_rel"]) and got["argmax_rel"] == -1
+    assert got["hist_zero"] == n - 4 and got["hist"][40] == 2 and got["hist"][39] == 1
+    assert got["sum_abs"] == 2.5 + 2.0 ** -30 and got["n_mismatch"] == [4, 4]
+    tk = P.topk_mean_mixed_batched([(g, t)], 1, 10)[0]
+    assert tk["n_valid"] == n - 1 and tk["k"] == -(-(n - 1) // 10)
+    assert tk["kth_value"] == 0.0 and tk["count_above"] == 3 and tk["sum_topk"] == 2.5 + 2.0 ** -30
+    del g, t
+    torch.cuda.empty_cache()

@@ -148,6 +148,24 @@ def test_async_records_match_sync():
     assert recs == sync
 
 
+def test_chunk_size_rule_boundaries():
+    """Pairs on both sides of the switch from ~256 to ~64 chunks per pair
+    (2^22 elements) and at the 2^18-element chunk cap, against the oracle;
+    batched records equal the single calls."""
+    pairs, hosts = [], []
+    for i, n in enumerate([(1 << 22) - 1, 1 << 22, (1 << 22) + 1, (1 << 24) - 3, (1 << 24) + 4097]):
+        log(f"  f32 n={n}")
+        gb, tb = special_pair(n, 0, seed=7700 + i)
+        g, t = to_device(gb, 0), to_device(tb, 0)
+        got = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+        assert_parity(got, oracle_sig(gb, tb, 0, synth.BINS, synth.THRESHOLDS), f"n={n}")
+        pairs.append((g, t))
+        hosts.append(got)
+    outs = P.signature_batched(pairs, synth.BINS, synth.THRESHOLDS)
+    for a, b in zip(outs, hosts):
+        assert all(a[k] == b[k] or (isinstance(b[k], float) and math.isnan(b[k]) and math.isnan(a[k])) for k in b)
+
+
 def test_index_beyond_2_31():
     """64-bit indexing: n > 2^31 f16 elements, planted values at known places."""
     n = (1 << 31) + 4096 + 1000
