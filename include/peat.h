@@ -172,7 +172,8 @@ typedef enum {
 #define PEAT_MAX_POSITIONS 4096
 
 typedef struct {
-    void *tensor;     /* device pointer, modified in place */
+    void *tensor;     /* device pointer, modified in place, aligned to its
+                       * element size (PEAT_EINVAL otherwise) */
     int64_t n;        /* elements, >= 0 */
     int32_t dtype;    /* peat_dtype_t   */
     int32_t model;    /* peat_model_t: BITFLIP (0), ZERO or NAN */
@@ -289,15 +290,17 @@ int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t 
  * uncorrupted tensor's value at floor(W1 * n / 2^64) of the draw that chose
  * it.  positions (host,
  * num_pos entries, may be NULL) receives the positions in order.  Returns
- * num_pos or a negative code; waits for the device. */
+ * num_pos or a negative code (PEAT_EINVAL also for a tensor not aligned to
+ * its element size); waits for the device. */
 int64_t peat_corrupt_positions(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, int32_t model,
                                int64_t num_pos, uint64_t bitmask, int64_t *positions);
 
 /* The FP16 / BF16 error of Section III-C: every element of an f32 tensor
  * (device, in place) becomes its round-to-nearest-even value in to_dtype
  * (PEAT_F16 or PEAT_BF16) widened back to f32; overflow gives +-Inf,
- * subnormals round correctly, a NaN becomes sign | 0x7FC00000.  Enqueued on
- * the calling thread's stream (peat_set_stream); does not wait. */
+ * subnormals round correctly, a NaN becomes sign | 0x7FC00000.  The tensor
+ * must be 4-byte aligned (PEAT_EINVAL otherwise).  Enqueued on the calling
+ * thread's stream (peat_set_stream); does not wait. */
 int peat_cast_round(void *tensor, int64_t n, peat_dtype_t to_dtype);
 
 /* peat_inject over count >= 0 items in one launch sequence; counts is a host

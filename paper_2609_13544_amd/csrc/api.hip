@@ -376,6 +376,8 @@ int check_item(const peat_inject_item_t &it, int k) {
     if (it.n < 0) return fail(PEAT_EINVAL, "item %d: n < 0", k);
     if (it.n > 0 && !it.tensor) return fail(PEAT_EINVAL, "item %d: NULL tensor with n > 0", k);
     if (it.n > (int64_t(1) << 46)) return fail(PEAT_EINVAL, "item %d: n above 2^46", k);
+    if (reinterpret_cast<uintptr_t>(it.tensor) % elem_size(it.dtype) != 0)
+        return fail(PEAT_EINVAL, "item %d: tensor is not aligned to its element size", k);
     return PEAT_OK;
 }
 
@@ -695,6 +697,8 @@ int64_t peat_corrupt_positions(void *tensor, int64_t n, peat_dtype_t dtype, uint
                     (long long)num_pos);
     if (num_pos == 0) return 0;
     if (!tensor) return fail(PEAT_EINVAL, "tensor is NULL");
+    if (reinterpret_cast<uintptr_t>(tensor) % elem_size(dtype) != 0)
+        return fail(PEAT_EINVAL, "tensor is not aligned to its element size");
     std::lock_guard<std::mutex> lock(g_mu);
     Dev *dv;
     int rc = current_dev(&dv);
@@ -723,6 +727,7 @@ int peat_cast_round(void *tensor, int64_t n, peat_dtype_t to_dtype) {
     if (n < 0) return fail(PEAT_EINVAL, "n < 0");
     if (n == 0) return PEAT_OK;
     if (!tensor) return fail(PEAT_EINVAL, "tensor is NULL");
+    if (reinterpret_cast<uintptr_t>(tensor) % 4 != 0) return fail(PEAT_EINVAL, "tensor is not 4-byte aligned");
     std::lock_guard<std::mutex> lock(g_mu);
     Dev *dv;
     int rc = current_dev(&dv);

@@ -141,6 +141,11 @@ def test_error_model_validation_codes():
     assert L.peat_cast_round(None, 0, 1) == B.OK
     assert L.peat_cast_round(None, 4, 1) == B.EINVAL
     assert L.peat_cast_round(None, 4, 0) == B.EDTYPE
+    # tensors must be aligned to their element size
+    assert L.peat_inject(18, 4, 0, 1, 0.5, 1) == B.EINVAL
+    assert L.peat_inject_model(17, 4, 1, 1, 0.5, 1, 0) == B.EINVAL
+    assert L.peat_corrupt_positions(18, 10, 0, 1, 1, 1, 0, pos) == B.EINVAL
+    assert L.peat_cast_round(18, 4, 1) == B.EINVAL
 
 
 def test_stream_read_validation_codes():
