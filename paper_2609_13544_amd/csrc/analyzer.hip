@@ -9,6 +9,28 @@
 
 #include "peat.h"
 
+namespace {
+
+// Average ranks (1-based) of v: sort once, then give every group of equal
+// values the mean of the positions it spans.
+std::vector<double> average_ranks(const std::vector<double> &v) {
+    const size_t m = v.size();
+    std::vector<size_t> idx(m);
+    std::iota(idx.begin(), idx.end(), size_t(0));
+    std::sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return v[a] < v[b]; });
+    std::vector<double> r(m);
+    for (size_t i = 0; i < m;) {
+        size_t j = i + 1;
+        while (j < m && v[idx[j]] == v[idx[i]]) ++j;
+        const double rank = 0.5 * (double)(i + 1 + j);    // mean of positions i+1 .. j
+        for (size_t k = i; k < j; ++k) r[idx[k]] = rank;
+        i = j;
+    }
+    return r;
+}
+
+}  // namespace
+
 extern "C" {
 
 int peat_series_stats(const double *x, int64_t n, peat_series_t *out) {
@@ -44,28 +66,6 @@ int peat_normalize_scores(const double *scores, const double *units, int64_t n, 
     for (int64_t i = 0; i < n; ++i) out[i] = scores[i] / units[i];
     return PEAT_OK;
 }
-
-namespace {
-
-// Average ranks (1-based) of v: sort once, then give every group of equal
-// values the mean of the positions it spans.
-std::vector<double> average_ranks(const std::vector<double> &v) {
-    const size_t m = v.size();
-    std::vector<size_t> idx(m);
-    std::iota(idx.begin(), idx.end(), size_t(0));
-    std::sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return v[a] < v[b]; });
-    std::vector<double> r(m);
-    for (size_t i = 0; i < m;) {
-        size_t j = i + 1;
-        while (j < m && v[idx[j]] == v[idx[i]]) ++j;
-        const double rank = 0.5 * (double)(i + 1 + j);    // mean of positions i+1 .. j
-        for (size_t k = i; k < j; ++k) r[idx[k]] = rank;
-        i = j;
-    }
-    return r;
-}
-
-}  // namespace
 
 int peat_spearman(const double *x, const double *y, int64_t n, double *rho) {
     if (!rho || n < 0 || (n > 0 && (!x || !y))) return PEAT_EINVAL;
