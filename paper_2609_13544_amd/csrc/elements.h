@@ -58,6 +58,19 @@ __device__ __forceinline__ double widen(B b) {
     }
 }
 
+// Exact binary32 value of one element's bits (types of at most 32 bits).
+template <int DT, typename B>
+__device__ __forceinline__ float widen32(B b) {
+    static_assert(Tr<DT>::W <= 32, "binary32 holds f32, f16 and bf16 values exactly");
+    if constexpr (DT == PEAT_F32) {
+        return __uint_as_float((uint32_t)b);
+    } else if constexpr (DT == PEAT_BF16) {
+        return __uint_as_float((uint32_t)b << 16);
+    } else {
+        return (float)__builtin_bit_cast(_Float16, (uint16_t)b);
+    }
+}
+
 // Bits of element j of a lane vector held in (up to) 16 bytes.
 template <int DT>
 __device__ __forceinline__ auto lane_elem(const u32x4 &v, int j) {

@@ -55,9 +55,16 @@ constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
 // and test values gives |t - g| >= |g|, i.e. a relative error of at least 1
 // (less the reciprocal's 2^-48), and a zero golden value gives Inf or NaN, so
 // this one comparison also catches every case the fast path does not handle.
-// Below the limit t lies within a factor 1.5 of g, so an f32 ULP distance is
-// below 2^24 and an f16/bf16 one below 2^11.
-constexpr double kRareRel = 0.5;
+// Below the limit t lies within a factor 1.25 of g, so:
+//   - t - g is exact in the elements' own format (Sterbenz: t/g in [1/2, 2]);
+//     when the difference is formed in binary32 and rounded, it is at least
+//     |g|/2 in magnitude, which this limit rejects, so a fast-path error is
+//     always the exact difference;
+//   - t^2 = g^2 + 2ge + e^2 and gt = g^2 + ge hold exactly per element, and
+//     the fast path sums g^2, ge and e^2 only: their sums give those of t^2
+//     and gt with a condition number below 2.8;
+//   - an f32 ULP distance is below 2^24 and an f16/bf16 one below 2^11.
+constexpr double kRareRel = 0.25;
 constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
 constexpr int kHistCols = kBlock / 2;     // histogram words per slot
 
@@ -113,7 +120,8 @@ __device__ __forceinline__ void recip2(const double *x, double *r) {
 }
 
 struct Lane {
-    double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;
+    double s_abs, s_rel;           // both paths
+    double s_sq, s_g2, s_ge;       // fast path: sums of e^2, g^2 and g*e
     double gx_abs;                 // generic path: max |err| and element index
     uint32_t gi_abs;
     uint32_t gu, gi_ulp;           // generic path: max ULP and element index
@@ -150,6 +158,8 @@ struct Shared {
     // counts at most 2^18 / 256 = 1024 elements per chunk, so no half carries.
     uint32_t hist[kHistSlots * kHistCols];
     uint32_t defer[kWaves][kDeferCap];     // deferred vector numbers per wave
+    // generic-path sums of a^2, g^2, t^2 and g*t, one column per lane
+    double gsum[4][kBlock];
     double rd[kWaves][6];
     double rmax[kWaves][2];
     uint32_t rix[kWaves][5];               // abs, rel, ulp, first_nan, first_valid
@@ -159,7 +169,7 @@ struct Shared {
 };
 
 __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
-    L.s_abs = L.s_sq = L.s_rel = L.s_g2 = L.s_t2 = L.s_gt = 0.0;
+    L.s_abs = L.s_rel = L.s_sq = L.s_g2 = L.s_ge = 0.0;
     L.gx_abs = -1.0;
     L.gi_abs = kNone;
     L.gu = 0;
@@ -184,6 +194,23 @@ __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) U.mism[j] = 0;
 }
 
+// Generic-path sums of one lane, kept in its LDS column between generic runs.
+struct GenAcc {
+    double sq, g2, t2, gt;
+    __device__ __forceinline__ void load(const Shared &sh, int tid) {
+        sq = sh.gsum[0][tid];
+        g2 = sh.gsum[1][tid];
+        t2 = sh.gsum[2][tid];
+        gt = sh.gsum[3][tid];
+    }
+    __device__ __forceinline__ void store(Shared &sh, int tid) const {
+        sh.gsum[0][tid] = sq;
+        sh.gsum[1][tid] = g2;
+        sh.gsum[2][tid] = t2;
+        sh.gsum[3][tid] = gt;
+    }
+};
+
 __device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
     const uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: sign bit clear
     atomicAdd(&sh.hist[sh.hrow[E] + hist_col(tid)], hist_inc(tid));
@@ -193,7 +220,7 @@ __device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
 // Elements may arrive out of index order (deferred vectors), so the maxima
 // use (value, lowest index) comparisons.
 template <int DG, int DT, int NT, typename BG, typename BT>
-__device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParams &P,
+__device__ __forceinline__ void generic_elem(Lane &L, GenAcc &ga, Shared &sh, const SigParams &P,
                                              BG gb, BT tb, uint32_t li, int tid) {
     using PT = PairTr<DG, DT>;
     const double G = widen<DG>(gb), T = widen<DT>(tb);
@@ -250,10 +277,10 @@ __device__ __forceinline__ void generic_elem(Lane &L, Shared &sh, const SigParam
     if (inf_g || inf_t) return;
     L.cnt[C_FINITE] += 1;
     L.s_abs += a;
-    L.s_sq = __builtin_fma(a, a, L.s_sq);
-    L.s_g2 = __builtin_fma(G, G, L.s_g2);
-    L.s_t2 = __builtin_fma(T, T, L.s_t2);
-    L.s_gt = __builtin_fma(G, T, L.s_gt);
+    ga.sq = __builtin_fma(a, a, ga.sq);
+    ga.g2 = __builtin_fma(G, G, ga.g2);
+    ga.t2 = __builtin_fma(T, T, ga.t2);
+    ga.gt = __builtin_fma(G, T, ga.gt);
     if (G != 0.0) {
         L.cnt[C_REL] += 1;
         const double r = a / __builtin_fabs(G);
@@ -332,13 +359,22 @@ template <int DG, int DT, int NT, bool RT>
 __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
                                          const u32x4 &gv, const u32x4 &tv, uint32_t v, int tid) {
     constexpr int VEC = PairTr<DG, DT>::VEC;
-    double G[VEC], T[VEC], E[VEC], R[VEC];
+    // both sides fit binary32: the difference is formed there (exact on the
+    // fast path) and widened; otherwise in binary64
+    constexpr bool kDiff32 = Tr<DG>::W <= 32 && Tr<DT>::W <= 32;
+    float G32[VEC];
+    double G[VEC], E[VEC], R[VEC];
     uint32_t row[VEC], u[VEC];
     uint64_t mflag = 0;
     double AG[VEC], IG[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
-        G[j] = widen<DG>(lane_elem<DG>(gv, j));
+        if constexpr (kDiff32) {
+            G32[j] = widen32<DG>(lane_elem<DG>(gv, j));
+            G[j] = (double)G32[j];
+        } else {
+            G[j] = widen<DG>(lane_elem<DG>(gv, j));
+        }
         AG[j] = __builtin_fabs(G[j]);
     }
     if constexpr (VEC == 2) {
@@ -351,13 +387,20 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
     for (int j = 0; j < VEC; ++j) {
         const auto gb = lane_elem<DG>(gv, j);
         const auto tb = lane_elem<DT>(tv, j);
-        T[j] = widen<DT>(tb);
-        E[j] = T[j] - G[j];                                   // signed error
+        double Tj;                                            // test value (used by mixed ULPs)
+        if constexpr (kDiff32) {
+            const float T32 = widen32<DT>(tb);
+            E[j] = (double)(T32 - G32[j]);                    // signed error
+            Tj = (double)T32;
+        } else {
+            Tj = widen<DT>(tb);
+            E[j] = Tj - G[j];
+        }
         R[j] = __builtin_fabs(E[j]) * IG[j];
         // rare (>= kRareRel or NaN), or a candidate for the max relative error
         mflag |= __ballot(!(R[j] < L.rthr));
         // same sign on the fast path: the ULP distance is |t - g| of the bit patterns
-        u[j] = fast_ulp<DG, DT>(gb, tb, G[j], T[j]);
+        u[j] = fast_ulp<DG, DT>(gb, tb, G[j], Tj);
         row[j] = sh.hrow[(uint32_t)(__double_as_longlong(E[j]) >> 52) & 0x7FFu];
     }
     double va = absmax_f64(E[0], E[1]);
@@ -416,8 +459,7 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
         L.s_abs += __builtin_fabs(E[j]);
         L.s_sq = __builtin_fma(E[j], E[j], L.s_sq);
         L.s_g2 = __builtin_fma(G[j], G[j], L.s_g2);
-        L.s_t2 = __builtin_fma(T[j], T[j], L.s_t2);
-        L.s_gt = __builtin_fma(G[j], T[j], L.s_gt);
+        L.s_ge = __builtin_fma(G[j], E[j], L.s_ge);
         L.s_rel += R[j];
     }
     // threshold mismatches: nothing to count while the vector's largest
@@ -503,20 +545,30 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     Lane L;
     Uni Un;
     lane_init(L, Un);
+    {
+        const GenAcc zero{0.0, 0.0, 0.0, 0.0};
+        zero.store(sh, tid);                     // this lane's generic-path column
+    }
 
     const uint32_t nsuper = d.aligned ? len / SUPER : 0;
     uint32_t ndef = 0;                           // wave-uniform
 
     auto flush = [&]() {
+        if (ndef != 0) {
+            GenAcc gf;
+            gf.load(sh, tid);
 #pragma unroll 1
-        for (uint32_t k = 0; k < ndef; ++k) {
-            const uint32_t v = sh.defer[wave][k];
-            const u32x4 gv = load_vec<BG>(gbase, v * kBlock + tid);
-            const u32x4 tv = load_vec<BT>(tbase, v * kBlock + tid);
-            const uint32_t li0 = (v * kBlock + tid) * VEC;
+            for (uint32_t k = 0; k < ndef; ++k) {
+                const uint32_t v = sh.defer[wave][k];
+                const u32x4 gv = load_vec<BG>(gbase, v * kBlock + tid);
+                const u32x4 tv = load_vec<BT>(tbase, v * kBlock + tid);
+                const uint32_t li0 = (v * kBlock + tid) * VEC;
 #pragma unroll 1
-            for (int j = 0; j < VEC; ++j)
-                generic_elem<DG, DT, NT>(L, sh, P, lane_elem<DG>(gv, j), lane_elem<DT>(tv, j), li0 + j, tid);
+                for (int j = 0; j < VEC; ++j)
+                    generic_elem<DG, DT, NT>(L, gf, sh, P, lane_elem<DG>(gv, j), lane_elem<DT>(tv, j), li0 + j,
+                                             tid);
+            }
+            gf.store(sh, tid);
         }
         ndef = 0;
         // Nothing of the flush stays in flight: the hot loop's header then
@@ -583,9 +635,11 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
         }
     }
     // ragged tail, or the whole chunk when a pointer is not 16-byte aligned
+    GenAcc ga;
+    ga.load(sh, tid);
 #pragma unroll 1
     for (uint32_t li = nsuper * SUPER + tid; li < len; li += kBlock)
-        generic_elem<DG, DT, NT>(L, sh, P, load_elem<DG>(gbase, li), load_elem<DT>(tbase, li), li, tid);
+        generic_elem<DG, DT, NT>(L, ga, sh, P, load_elem<DG>(gbase, li), load_elem<DT>(tbase, li), li, tid);
 
     // ---- resolve the fast-path maxima to element indices -----------------
     // Reload the vector in which the wave's running maximum was first
@@ -630,7 +684,11 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     if (Un.first != kNone) L.first_valid = min(L.first_valid, (Un.first * kBlock + tid) * VEC);
 
     // ---- epilogue: reduce the block into the chunk record ----------------
-    double sums[6] = {L.s_abs, L.s_sq, L.s_rel, L.s_g2, L.s_t2, L.s_gt};
+    // fast-path t^2 and g*t from their exact per-element identities, then the
+    // generic path's direct sums; a fixed order per lane
+    const double f_t2 = (L.s_g2 + 2.0 * L.s_ge) + L.s_sq;
+    const double f_gt = L.s_g2 + L.s_ge;
+    double sums[6] = {L.s_abs, L.s_sq + ga.sq, L.s_rel, L.s_g2 + ga.g2, f_t2 + ga.t2, f_gt + ga.gt};
 #pragma unroll
     for (int k = 0; k < 6; ++k) sums[k] = wsum(sums[k]);
     double mxr = L.mx_rel;
