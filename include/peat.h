@@ -237,6 +237,12 @@ int peat_signature_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count,
                                  const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                                  peat_signature_t *outs);
 
+/* As peat_signature_mixed_batched, enqueued on stream; d_outs is a device
+ * array of count records written when the stream reaches the work. */
+int peat_signature_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t count,
+                                       const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                                       peat_signature_t *d_outs, void *stream);
+
 /* Mean of the k largest errors of one pair, k = ceil(n_valid * num / den)
  * (num = 1, den = 10: the paper's top-10% mean); out is host memory.
  * 1 <= num <= den <= 2^20.  Exact selection: n_valid, k, count_above and

@@ -10,5 +10,5 @@ from ._binding import (  # noqa: F401
     finalize_stats, inject, inject_batched, inject_batched_async, lib, profile_enable,
     profile_read, set_stream, signature, signature_batched, signature_batched_async, stream_read,
     strerror, topk_mean, topk_mean_batched, series_stats, spearman, normalize_scores,
-    signature_mixed, signature_mixed_batched, topk_mean_mixed_batched,
+    signature_mixed, signature_mixed_batched, signature_mixed_batched_async, topk_mean_mixed_batched,
 )

@@ -151,6 +151,9 @@ _PROTOS = {
     "peat_signature_mixed_batched": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32,
                                                     ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
                                                     ctypes.POINTER(Signature)]),
+    "peat_signature_mixed_batched_async": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32,
+                                                          ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
+                                                          ctypes.c_void_p, ctypes.c_void_p]),
     "peat_topk_mean_mixed_batched": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32, ctypes.c_int32,
                                                     ctypes.c_int32, ctypes.POINTER(TopK)]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
@@ -372,6 +375,20 @@ def signature_mixed_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) 
     _check(lib().peat_signature_mixed_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
            "peat_signature_mixed_batched")
     return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+
+
+def signature_mixed_batched_async(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3),
+                                  stream=None) -> None:
+    """peat_signature_mixed_batched_async: records land in d_out, a device uint8
+    tensor of at least len(pairs) * SIG_BYTES bytes, when the stream gets there."""
+    arr = _mixed_pairs_array(pairs)
+    _dev_tensor(d_out, "d_out")
+    if d_out.numel() * d_out.element_size() < len(pairs) * SIG_BYTES:
+        raise ValueError("d_out too small")
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    _check(lib().peat_signature_mixed_batched_async(arr, len(pairs), ctypes.byref(b), ctypes.byref(th),
+                                                    d_out.data_ptr(), _stream_ptr(stream)),
+           "peat_signature_mixed_batched_async")
 
 
 def topk_mean_mixed_batched(pairs, num: int = 1, den: int = 10) -> list[dict]:

@@ -667,6 +667,12 @@ int peat_signature_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, 
     return signature_core(pairs, count, bins, thresholds, nullptr, outs, t_stream);
 }
 
+int peat_signature_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                                       const peat_thresholds_t *thresholds, peat_signature_t *d_outs,
+                                       void *stream) {
+    return signature_core(pairs, count, bins, thresholds, d_outs, nullptr, static_cast<hipStream_t>(stream));
+}
+
 int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
                     uint64_t bitmask) {
     peat_inject_item_t it{tensor, n, (int32_t)dtype, PEAT_MODEL_BITFLIP, seed, rate, bitmask};

@@ -198,6 +198,8 @@ def test_mixed_pair_validation_codes():
     assert L.peat_signature_mixed_batched(pairs, 2, ctypes.byref(b), ctypes.byref(th), outs) == B.EDTYPE
     assert L.peat_signature_mixed_batched(None, 0, ctypes.byref(b), ctypes.byref(th), None) == B.OK
     assert L.peat_signature_mixed_batched(None, -1, ctypes.byref(b), ctypes.byref(th), None) == B.EINVAL
+    assert L.peat_signature_mixed_batched_async(pairs, 2, ctypes.byref(b), ctypes.byref(th), None, None) == B.EDTYPE
+    assert L.peat_signature_mixed_batched_async(None, 0, ctypes.byref(b), ctypes.byref(th), None, None) == B.OK
     touts = (B.TopK * 2)()
     assert L.peat_topk_mean_mixed_batched(pairs, 2, 1, 10, touts) == B.EDTYPE
     assert L.peat_topk_mean_mixed_batched(pairs, 1, 0, 10, touts) == B.EINVAL          # num < 1

@@ -247,3 +247,19 @@ def test_mixed_index_beyond_2_31():
     assert tk["kth_value"] == 0.0 and tk["count_above"] == 3 and tk["sum_topk"] == 2.5 + 2.0 ** -30
     del g, t
     torch.cuda.empty_cache()
+
+
+def test_mixed_async_records_match_sync():
+    pairs = []
+    for i, (gdt, tdt) in enumerate(KINDS):
+        gb, tb = mixed_pair(70001 + 13 * i, gdt, tdt, seed=9950 + i)
+        pairs.append((dev(gb, gdt), dev(tb, tdt)))
+    sync = P.signature_mixed_batched(pairs, thresholds=THR)
+    d_out = torch.empty(len(pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    P.signature_mixed_batched_async(pairs, d_out, thresholds=THR, stream=stream)
+    stream.synchronize()
+    recs = P.decode_records(d_out, len(pairs), nthr=len(THR))
+    for a, b in zip(recs, sync):
+        assert all(a[k] == b[k] or (isinstance(b[k], float) and math.isnan(b[k]) and math.isnan(a[k])) for k in b)
