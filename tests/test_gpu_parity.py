@@ -333,3 +333,35 @@ def test_workload5_full_sampled():
         assert r["hist_zero"] + r["hist_under"] + sum(r["hist"]) + r["hist_over"] == r["n_valid"]
     del tensors, items
     torch.cuda.empty_cache()
+
+
+def test_threads_on_their_own_streams():
+    """Calls from several host threads, each on its own stream (the stream is
+    per thread), give the same records as the same calls made one by one."""
+    import threading
+    cases = []
+    for i in range(6):
+        gb, tb = special_pair(300007 + 1000 * i, i % 3, seed=8800 + i)
+        cases.append((to_device(gb, i % 3), to_device(tb, i % 3)))
+    want = [P.signature(g, t, synth.BINS, synth.THRESHOLDS) for g, t in cases]
+    got = [None] * len(cases)
+    errors = []
+
+    def work(k):
+        try:
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                for _ in range(3):
+                    got[k] = P.signature(cases[k][0], cases[k][1], synth.BINS, synth.THRESHOLDS)
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    torch.cuda.synchronize()
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(len(cases))]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    for a, b in zip(got, want):
+        assert all(a[k] == b[k] or (isinstance(b[k], float) and math.isnan(b[k]) and math.isnan(a[k])) for k in b)
