@@ -19,8 +19,9 @@ Prints ONE JSON line on stdout (everything else goes to stderr):
 Also reported: the read ceiling of the same box (peat_stream_read over a
 16 GiB buffer with the chunk pass's access pattern) and the signature chunk
 pass as a fraction of it; per-step times (median, min, max); the top-10%
-error mean of the workload; the signature of mixed-precision pairs (FP32
-golden against FP64 and FP16 outputs).
+error mean of the workload; single-call latencies (a 1024x1024 f32 pair
+warm and cold, one f16 [4096, 4096] replay call); the signature of
+mixed-precision pairs (FP32 golden against FP64 and FP16 outputs).
 
 Modes used to produce the committed profiles: --copy-calibration (a plain
 device copy of known size, for scaling the HBM byte counters), --mixed-only
@@ -202,6 +203,12 @@ def cpu_baseline(wl: Workload, max_threads: int):
             g, t, code = host[k]
             oracle.signature(g, t, dtype=code)
 
+    # one core, one pair: per-core rate of the oracle
+    g1, t1, c1 = host[0]
+    t0 = time.time()
+    oracle.signature(g1, t1, dtype=c1)
+    per_core = (g1.nbytes + t1.nbytes) / (time.time() - t0) / 1e9
+
     t0 = time.time()
     ths = [threading.Thread(target=worker) for _ in range(threads)]
     for th in ths:
@@ -211,6 +218,7 @@ def cpu_baseline(wl: Workload, max_threads: int):
     dt = time.time() - t0
     del np
     return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "per_core_value": round(per_core, 3),
             "sample": f"{len(host)} of {len(wl.pairs)} pairs ({nbytes / 1e9:.2f} GB: "
                       f"{', '.join(str(k) for k in wl.sample)}), oracle {dt:.1f} s wall on {threads} threads, "
                       f"D2H copy {copy_s:.1f} s not counted"}
@@ -273,6 +281,54 @@ def mixed_measure(torch, P, reps: int = 5, count: int = 64, shape=(4096, 4096)):
     return res
 
 
+def latency_measure(torch, P, synth, stream, reps: int = 50):
+    """Per-call times of single-pair signatures (async call, HIP events on the
+    stream, chunk pass + finalize): the 1024x1024 f32 pair warm and cold
+    (cold: after reading 1 GiB so the pair is in no cache), the host round
+    trip of the synchronous call, and one f16 [4096, 4096] replay call."""
+    import statistics
+    G, T = synth.config1()
+    g, t = torch.from_numpy(G).cuda(), torch.from_numpy(T).cuda()
+    h = synth.config4_golden("cuda")
+    h2 = h.clone()
+    h2.view(-1)[::9973] += 1.0
+    d_out = torch.empty(P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    flush.fill_(1)
+    sink = torch.zeros(-(-flush.numel() // P.STREAM_SPAN), dtype=torch.int32, device="cuda")
+
+    def timed(prep, cold=False):
+        if cold:
+            P.stream_read(flush, sink, stream=stream)
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        P.signature_batched_async(prep, d_out, synth.BINS, synth.THRESHOLDS, stream=stream)
+        b.record(stream)
+        b.synchronize()
+        return a.elapsed_time(b) * 1e3
+
+    p1, p4 = P.PreparedPairs([(g, t)]), P.PreparedPairs([(h, h2)])
+    for _ in range(5):
+        timed(p1)
+        timed(p4)
+    warm = statistics.median(timed(p1) for _ in range(reps))
+    cold = statistics.median(timed(p1, cold=True) for _ in range(10))
+    f16 = statistics.median(timed(p4) for _ in range(20))
+    walls = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+        walls.append((time.perf_counter() - t0) * 1e6)
+    del flush, sink
+    torch.cuda.empty_cache()
+    return {"single_f32_1024x1024": {"warm_us": round(warm, 1), "cold_us": round(cold, 1),
+                                     "sync_call_wall_us": round(statistics.median(walls), 1)},
+            "replay_f16_4096x4096_call_us": round(f16, 1),
+            "what": "async single-pair signature, HIP events around the call on its stream (chunk pass + "
+                    "finalize + launch gaps); cold = after a 1 GiB read; sync = host round trip of peat_signature"}
+
+
 def read_ceiling(torch, P, stream, gib: int = 16, reps: int = 5):
     """GB/s of peat_stream_read over a gib-GiB buffer (best of reps)."""
     buf = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
@@ -320,6 +376,7 @@ def main():
     ap.add_argument("--no-topk", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--mixed-only", action="store_true", help="only the mixed-precision measurement")
+    ap.add_argument("--no-latency", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -431,6 +488,9 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
+    if not args.no_latency:
+        log("single-call latency ...")
+        out["latency"] = latency_measure(torch, P, synth, stream)
     if not args.no_mixed:
         log("mixed-precision pairs ...")
         del wl, prep_pairs, d_out
