@@ -4,6 +4,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "peat.h"
@@ -69,7 +70,8 @@ static_assert(sizeof(SigDesc) == 48, "SigDesc layout");
 enum { C_VALID, C_FINITE, C_REL, C_NAN_G, C_NAN_T, C_INF_G, C_INF_T, C_NANPAIR, kCnt };
 
 struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
-    double s_abs, s_sq, s_rel, s_g2, s_t2, s_gt;
+    // binary64 sums of each wave of the block: |err|, err^2, rel, g^2, t^2, g*t
+    double s[kWaves][6];
     double max_abs, max_rel;
     int64_t ix_abs, ix_rel, ix_ulp;  // element index within the pair, -1 = none
     int64_t first_nan, first_valid;  // -1 = none
@@ -79,9 +81,14 @@ struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
     uint32_t mism[PEAT_MAX_THRESHOLDS];
     uint32_t hist[kHistSlots];
 };
+// the chunk pass writes the counts followed by the mismatches as one array
+static_assert(offsetof(ChunkPartial, mism) == offsetof(ChunkPartial, cnt) + kCnt * sizeof(uint32_t),
+              "ChunkPartial counts");
 
 struct SigParams {
     int64_t chunk_base;            // first global chunk of this launch
+    int64_t chunk_count;           // chunks of this launch
+    int64_t chunk_group;           // consecutive chunks per block
     const SigDesc *descs;
     const int32_t *chunk_pair;     // chunk -> pair index
     ChunkPartial *partials;        // one per chunk

@@ -4,13 +4,15 @@
 // mixed.hip).  Pass 2 (sig_finalize, in signature.hip) combines a pair's
 // chunk records in a fixed order and writes the peat_signature_t.
 //
-// One 256-thread block per fixed-size chunk of one pair.  Each thread streams
-// lane vectors of golden and test through nontemporal buffer loads: 16 bytes
-// of the wider side (4 f32, 8 f16/bf16 or 2 binary64 elements) and the
-// matching bytes of the other, widens them exactly to binary64 and
-// accumulates the signature of its elements; the chunk's record (binary64
-// partial sums, maxima with their lowest index, integer counts, histogram)
-// goes to one ChunkPartial.
+// 256-thread blocks, each streaming one or two consecutive fixed-size chunks
+// (a chunk lies within one pair).  Each thread streams lane vectors of golden
+// and test through nontemporal buffer loads: 16 bytes of the wider side (4
+// f32, 8 f16/bf16 or 2 binary64 elements) and the matching bytes of the
+// other, widens them exactly to binary64 and accumulates the signature of its
+// elements.  Each chunk's record (ChunkPartial) holds the binary64 partial
+// sums of each of the block's four waves; maxima with their lowest index,
+// integer counts and the histogram are exact and go to the record of the last
+// chunk of the block's run of chunks of one pair.
 //
 // The definitions follow the paper's FI assessment scores (Section IV-B.3:
 // error = absolute difference of golden and faulty values; max, mean,
@@ -29,8 +31,8 @@
 //   - reciprocals come from one hardware estimate per four (or two) elements
 //     plus a Newton step;
 //   - the maxima of |err| and of the ULP distance are wave-uniform running
-//     records (the vector that first exceeded them), resolved to an element
-//     by one reload at the end of the chunk;
+//     records; a vector that raises one is resolved to its element indices
+//     on the spot, while its values are in registers;
 //   - counts use wave ballots; the histogram uses lane-private 16-bit LDS
 //     counters addressed through a binary64-exponent -> row table.
 // Any other vector is deferred: its wave-uniform vector number goes to a
@@ -38,10 +40,13 @@
 // processes the list out of the hot loop.  Ragged tails and unaligned pairs
 // use the generic path directly.
 //
-// Determinism: the element -> lane mapping, per-lane order and reduction
-// trees depend only on the chunk size, which depends only on n, so single,
-// batched and any-grid-size launches give bit-identical records.
+// Determinism: the element -> lane mapping, per-lane order and the wave
+// reductions of the sums depend only on the chunk size, which depends only on
+// n; everything else is exact.  Single, batched and any-grid-size launches
+// give bit-identical signatures.
 #pragma once
+
+#include <atomic>
 
 #include "elements.h"
 
@@ -66,6 +71,14 @@ constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
 //   - an f32 ULP distance is below 2^24 and an f16/bf16 one below 2^11.
 constexpr double kRareRel = 0.25;
 constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
+// Chunks per block: one while the launch has few chunks (every chunk gets a
+// block of its own), two once there are enough for at least kMinRounds rounds
+// of resident blocks: block start-up is shared by two chunks while blocks stay
+// short enough for the hardware to balance the load at the end of the launch.
+constexpr int64_t kMaxGroup = 2;
+constexpr int64_t kMinRounds = 8;
+// a lane's 16-bit histogram counters hold a whole run of chunks
+static_assert(kMaxGroup * (int64_t(1) << kMaxChunkLog2) / kBlock < 65536, "histogram counter width");
 constexpr int kHistCols = kBlock / 2;     // histogram words per slot
 
 __device__ __forceinline__ uint32_t hist_col(int tid) { return (uint32_t)tid & (kHistCols - 1); }
@@ -122,9 +135,9 @@ __device__ __forceinline__ void recip2(const double *x, double *r) {
 struct Lane {
     double s_abs, s_rel;           // both paths
     double s_sq, s_g2, s_ge;       // fast path: sums of e^2, g^2 and g*e
-    double gx_abs;                 // generic path: max |err| and element index
+    double gx_abs;                 // both paths: max |err| and element index
     uint32_t gi_abs;
-    uint32_t gu, gi_ulp;           // generic path: max ULP and element index
+    uint32_t gu, gi_ulp;           // both paths: max ULP and element index
     double mx_rel;                 // both paths: max rel err and its index
     double rthr;                   // fast-path filter, at most kRareRel
     uint32_t ix_rel;
@@ -137,17 +150,15 @@ struct Lane {
 
 // Fast-path state shared by the wave.  Vectors reach the fast path in
 // increasing vector number, and every element of a later vector has a higher
-// index than every element of an earlier one, so the wave only needs its
-// running maximum and the vector number that first exceeded the previous one:
-// an element equal to the running maximum in a later vector cannot be the
-// (value, lowest index) maximum.
+// index than every element of an earlier one, so only a vector that exceeds
+// the wave's running maximum can hold the (value, lowest index) maximum: an
+// element equal to the running maximum in a later vector cannot.
 struct Uni {
     uint32_t common;                       // ordinary vectors per lane
     uint32_t mism[PEAT_MAX_THRESHOLDS];
     uint32_t first;                        // first ordinary vector number
-    double wx_abs;                         // running max |err| ...
-    uint32_t wv_abs;                       // ... first reached in this vector
-    uint32_t wu, wv_ulp;                   // running max ULP, its vector
+    double wx_abs;                         // running max |err|
+    uint32_t wu;                           // running max ULP
 };
 
 struct Shared {
@@ -187,9 +198,7 @@ __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
     U.common = 0;
     U.first = kNone;
     U.wx_abs = -1.0;
-    U.wv_abs = kNone;
     U.wu = 0;
-    U.wv_ulp = kNone;
 #pragma unroll
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) U.mism[j] = 0;
 }
@@ -323,6 +332,16 @@ __device__ __forceinline__ uint32_t wave_max_uniform_u(uint32_t x) {
     return __builtin_amdgcn_readfirstlane(x);
 }
 
+// Merge candidate (ov, oi) into the (value desc, index asc) maximum (v, ix);
+// kNone marks an empty entry.
+template <typename V>
+__device__ __forceinline__ void lex_merge(V &v, uint32_t &ix, V ov, uint32_t oi) {
+    if (oi != kNone && (ix == kNone || ov > v || (ov == v && oi < ix))) {
+        v = ov;
+        ix = oi;
+    }
+}
+
 // ULP distance of a fast-path element (both finite, same sign, not NaN):
 // the difference of the narrower format's bit patterns.
 template <int DG, int DT, typename BG, typename BT>
@@ -357,7 +376,7 @@ __device__ __forceinline__ uint32_t fast_ulp(BG gb, BT tb, double G, double T) {
 // adds, so they share one LDS round trip.
 template <int DG, int DT, int NT, bool RT>
 __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
-                                         const u32x4 &gv, const u32x4 &tv, uint32_t v, int tid) {
+                                         const u32x4 &gv, const u32x4 &tv, uint32_t v, uint32_t ib, int tid) {
     constexpr int VEC = PairTr<DG, DT>::VEC;
     // both sides fit binary32: the difference is formed there (exact on the
     // fast path) and widened; otherwise in binary64
@@ -419,6 +438,7 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
             mcand |= __ballot(R[j] > L.rthr);
         }
         if (mrare != 0) return true;
+        const uint32_t li0 = ib + (v * kBlock + tid) * VEC;
         if (mcand != 0) {
             // The filter threshold is shared by the wave: an element whose
             // relative error is below the wave's running maximum cannot be
@@ -426,7 +446,6 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
             // Ties with the maximum still pass (the margin keeps them), and
             // the lanes' (value, lowest index) maxima are merged at the end
             // of the chunk.
-            const uint32_t li0 = (v * kBlock + tid) * VEC;
 #pragma unroll
             for (int j = 0; j < VEC; ++j) {
                 if (R[j] > L.rthr) {
@@ -440,13 +459,29 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
             const double wm = wave_max_uniform(L.mx_rel);
             L.rthr = __builtin_fmin(wm - wm * kRelMargin, kRareRel);
         }
+        // A new running maximum: the lanes that hold it record its lowest
+        // index in this vector (an equal value in a later vector has a
+        // higher index).  Lane records are (value, lowest index) maxima
+        // shared with the generic path.
         if (__ballot(va > U.wx_abs) != 0) {
             U.wx_abs = wave_max_uniform(va);
-            U.wv_abs = v;
+            if (va == U.wx_abs) {
+                uint32_t ix = kNone;
+#pragma unroll
+                for (int j = VEC - 1; j >= 0; --j)
+                    if (__builtin_fabs(E[j]) == U.wx_abs) ix = li0 + j;
+                lex_merge(L.gx_abs, L.gi_abs, U.wx_abs, ix);
+            }
         }
         if (__ballot(vu > U.wu) != 0) {
             U.wu = wave_max_uniform_u(vu);
-            U.wv_ulp = v;
+            if (vu == U.wu) {
+                uint32_t ix = kNone;
+#pragma unroll
+                for (int j = VEC - 1; j >= 0; --j)
+                    if (u[j] == U.wu) ix = li0 + j;
+                lex_merge(L.gu, L.gi_ulp, U.wu, ix);
+            }
         }
     }
 
@@ -506,6 +541,109 @@ __device__ __forceinline__ uint32_t wmin_u(uint32_t v) {
     for (int o = 32; o >= 1; o >>= 1) v = min(v, (uint32_t)__shfl_xor(v, o));
     return v;
 }
+// ---- wave reductions by DPP (chunk records) ---------------------------------
+// The classic six-step pattern: pairs and quads (quad_perm), half rows and
+// rows (mirrors), then rows 1 and 3 take the last lane of rows 0 and 2
+// (row_bcast:15) and rows 2 and 3 the last lane of row 1 (row_bcast:31), so
+// lane 63 ends with the whole wave's result.  Each lane's data moves through
+// the VALU's data-parallel primitives rather than the LDS crossbar, and the
+// order of the operations is fixed.
+constexpr int kDppXor1 = 0xB1;           // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;           // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+constexpr int kDppBcast15 = 0x142;
+constexpr int kDppBcast31 = 0x143;
+
+// x moved by DPP control C within the rows of mask RM; lanes of the other
+// rows get old.
+template <int C, int RM>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, C, RM, 0xF, false);
+}
+template <int C, int RM>
+__device__ __forceinline__ double dpp_f64(double old, double x) {
+    const uint64_t o = (uint64_t)__double_as_longlong(old), v = (uint64_t)__double_as_longlong(x);
+    const uint32_t lo = dpp_u32<C, RM>((uint32_t)o, (uint32_t)v);
+    const uint32_t hi = dpp_u32<C, RM>((uint32_t)(o >> 32), (uint32_t)(v >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ uint32_t lane63_u32(uint32_t v) { return (uint32_t)__builtin_amdgcn_readlane((int)v, 63); }
+__device__ __forceinline__ double lane63_f64(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    return __longlong_as_double((long long)(((uint64_t)lane63_u32((uint32_t)(b >> 32)) << 32) | lane63_u32((uint32_t)b)));
+}
+
+// One step of each reduction: combine with the value DPP control C brings.
+template <int C, int RM>
+__device__ __forceinline__ void dsum_step(double &v) { v += dpp_f64<C, RM>(0.0, v); }
+template <int C, int RM>
+__device__ __forceinline__ void dsum_step(uint32_t &v) { v += dpp_u32<C, RM>(0u, v); }
+template <int C, int RM>
+__device__ __forceinline__ void dmin_step(uint32_t &v) { v = min(v, dpp_u32<C, RM>(v, v)); }
+template <int C, int RM, typename V>
+__device__ __forceinline__ void dmax_step(V &v, uint32_t &ix) {
+    V ov;
+    if constexpr (sizeof(V) == 8)
+        ov = dpp_f64<C, RM>(v, v);
+    else
+        ov = dpp_u32<C, RM>(v, v);
+    const uint32_t oi = dpp_u32<C, RM>(ix, ix);
+    const bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
+    v = take ? ov : v;
+    ix = take ? oi : ix;
+}
+
+// Wave sum of a binary64 value (fixed order), as a scalar.
+__device__ __forceinline__ double dpp_sum(double v) {
+    dsum_step<kDppXor1, 0xF>(v);
+    dsum_step<kDppXor2, 0xF>(v);
+    dsum_step<kDppHalfMirror, 0xF>(v);
+    dsum_step<kDppMirror, 0xF>(v);
+    dsum_step<kDppBcast15, 0xA>(v);
+    dsum_step<kDppBcast31, 0xC>(v);
+    return lane63_f64(v);
+}
+// Wave sum of a 32-bit count (at most 2^31 in total), as a scalar; zero
+// without any data movement when every lane holds zero.
+__device__ __forceinline__ uint32_t dpp_sum_u32(uint32_t v) {
+    if (__ballot(v != 0) == 0) return 0;
+    dsum_step<kDppXor1, 0xF>(v);
+    dsum_step<kDppXor2, 0xF>(v);
+    dsum_step<kDppHalfMirror, 0xF>(v);
+    dsum_step<kDppMirror, 0xF>(v);
+    dsum_step<kDppBcast15, 0xA>(v);
+    dsum_step<kDppBcast31, 0xC>(v);
+    return lane63_u32(v);
+}
+// Wave minimum of an index (kNone when every lane holds kNone), as a scalar.
+__device__ __forceinline__ uint32_t dpp_min_u32(uint32_t v) {
+    if (__ballot(v != kNone) == 0) return kNone;
+    dmin_step<kDppXor1, 0xF>(v);
+    dmin_step<kDppXor2, 0xF>(v);
+    dmin_step<kDppHalfMirror, 0xF>(v);
+    dmin_step<kDppMirror, 0xF>(v);
+    dmin_step<kDppBcast15, 0xA>(v);
+    dmin_step<kDppBcast31, 0xC>(v);
+    return lane63_u32(v);
+}
+// Wave (value desc, index asc) maximum over entries with index != kNone, as
+// scalars.
+template <typename V>
+__device__ __forceinline__ void dpp_max(V &v, uint32_t &ix) {
+    dmax_step<kDppXor1, 0xF>(v, ix);
+    dmax_step<kDppXor2, 0xF>(v, ix);
+    dmax_step<kDppHalfMirror, 0xF>(v, ix);
+    dmax_step<kDppMirror, 0xF>(v, ix);
+    dmax_step<kDppBcast15, 0xA>(v, ix);
+    dmax_step<kDppBcast31, 0xC>(v, ix);
+    if constexpr (sizeof(V) == 8)
+        v = lane63_f64(v);
+    else
+        v = lane63_u32(v);
+    ix = lane63_u32(ix);
+}
+
 // (value desc, index asc) over entries with index != kNone
 template <typename V>
 __device__ __forceinline__ void wmax(V &v, uint32_t &ix) {
@@ -518,16 +656,47 @@ __device__ __forceinline__ void wmax(V &v, uint32_t &ix) {
         ix = take ? oi : ix;
     }
 }
-template <typename V>
-__device__ __forceinline__ void lex_merge(V &v, uint32_t &ix, V ov, uint32_t oi) {
-    if (oi != kNone && (ix == kNone || ov > v || (ov == v && oi < ix))) {
-        v = ov;
-        ix = oi;
-    }
+
+// A 64-bit value that is the same in every lane, as a scalar.
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
 }
 
+// Position of one chunk: its record, its elements and its super-steps.
+// Every field is uniform over the block.
+struct ChunkCtx {
+    int64_t gchunk;                          // global chunk number (its record)
+    int64_t off;                             // first element of the chunk in its pair
+    const char *gbase, *tbase;               // first element of golden and test
+    int32_t pair;
+    int32_t log2;                            // chunk size of the pair
+    uint32_t len;                            // elements
+    uint32_t nsuper;                         // full super-steps (0 when unaligned)
+};
+
+// The block's chunks: chunk_group consecutive chunks of the launch, streamed
+// back to back; blocks are scheduled by the hardware as compute units free
+// up, which keeps the load balanced.  The first super-step of the next chunk
+// is loaded while the last one of the current chunk is processed and while
+// the chunk's sums are reduced, and the exponent -> row table is built once
+// per block.
+//
+// Only the binary64 sums depend on how elements are grouped, so only they
+// are reduced per chunk, per wave, with no block barrier: each wave writes its
+// six totals into the chunk record.  Everything else (counts, maxima with
+// their lowest index, first indices, the ULP sum, the histogram) is exact and
+// independent of grouping, so it is carried over the block's run of
+// consecutive chunks of one pair (indices relative to the run) and reduced
+// once, into the record of the run's last chunk; the other records of the run
+// hold neutral values there.  A run has at most kMaxGroup (2) chunks of at
+// most 2^18 elements, so a lane counts at most 2048 elements per histogram
+// slot.
 template <int DG, int DT, int NT, bool RT>
-__device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int64_t cin, int64_t gchunk) {
+__device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const SigDesc *__restrict__ descs,
+                                           const int32_t *__restrict__ chunk_pair,
+                                           ChunkPartial *__restrict__ partials) {
     using PT = PairTr<DG, DT>;
     constexpr int VEC = PT::VEC;
     constexpr int U = kUnroll<DG, DT>;
@@ -536,71 +705,78 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
     constexpr int BG = PT::BG, BT = PT::BT;     // bytes per lane vector
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int64_t off = cin << d.chunk_log2;    // first element of the chunk
-    const int64_t rest = d.n - off;
-    const uint32_t len = (uint32_t)(rest < (int64_t(1) << d.chunk_log2) ? rest : (int64_t(1) << d.chunk_log2));
-    const char *gbase = static_cast<const char *>(d.g) + off * ESZG;
-    const char *tbase = static_cast<const char *>(d.t) + off * ESZT;
+    const int64_t nch = P.chunk_count;
+    const uint32_t lane_off_g = (uint32_t)tid * BG, lane_off_t = (uint32_t)tid * BT;
+
+    // A pair's descriptor (scalar loads: the tables are restrict arguments,
+    // never written by the kernel; the values are uniform), and a chunk's
+    // position from it.  Consecutive chunks of one pair reuse the descriptor.
+    struct PairS {
+        const char *g, *t;
+        int64_t n, first;
+        int32_t pair, log2, nchunks, aligned;
+    };
+    auto pair_of = [&](int64_t c) {
+        PairS d;
+        d.pair = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)chunk_pair[P.chunk_base + c]);
+        const SigDesc &dm = descs[d.pair];
+        d.g = reinterpret_cast<const char *>(uniform_u64(reinterpret_cast<uint64_t>(dm.g)));
+        d.t = reinterpret_cast<const char *>(uniform_u64(reinterpret_cast<uint64_t>(dm.t)));
+        d.n = (int64_t)uniform_u64((uint64_t)dm.n);
+        d.first = (int64_t)uniform_u64((uint64_t)dm.first_chunk);
+        d.log2 = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)dm.chunk_log2);
+        d.nchunks = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)dm.nchunks);
+        d.aligned = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)dm.aligned);
+        return d;
+    };
+    auto ctx = [&](const PairS &d, int64_t c) {
+        ChunkCtx x;
+        x.gchunk = P.chunk_base + c;
+        x.pair = d.pair;
+        x.log2 = d.log2;
+        x.off = (x.gchunk - d.first) << d.log2;
+        const int64_t rest = d.n - x.off;
+        x.len = (uint32_t)(rest < (int64_t(1) << d.log2) ? rest : (int64_t(1) << d.log2));
+        x.gbase = d.g + x.off * ESZG;
+        x.tbase = d.t + x.off * ESZT;
+        x.nsuper = d.aligned != 0 ? x.len / SUPER : 0;
+        return x;
+    };
 
     Lane L;
     Uni Un;
-    lane_init(L, Un);
-    {
+    uint32_t ndef;                               // wave-uniform
+    auto reset_sums = [&]() {
+        L.s_abs = L.s_rel = L.s_sq = L.s_g2 = L.s_ge = 0.0;
         const GenAcc zero{0.0, 0.0, 0.0, 0.0};
         zero.store(sh, tid);                     // this lane's generic-path column
-    }
-
-    const uint32_t nsuper = d.aligned ? len / SUPER : 0;
-    uint32_t ndef = 0;                           // wave-uniform
-
-    auto flush = [&]() {
-        if (ndef != 0) {
-            GenAcc gf;
-            gf.load(sh, tid);
-#pragma unroll 1
-            for (uint32_t k = 0; k < ndef; ++k) {
-                const uint32_t v = sh.defer[wave][k];
-                const u32x4 gv = load_vec<BG>(gbase, v * kBlock + tid);
-                const u32x4 tv = load_vec<BT>(tbase, v * kBlock + tid);
-                const uint32_t li0 = (v * kBlock + tid) * VEC;
-#pragma unroll 1
-                for (int j = 0; j < VEC; ++j)
-                    generic_elem<DG, DT, NT>(L, gf, sh, P, lane_elem<DG>(gv, j), lane_elem<DT>(tv, j), li0 + j,
-                                             tid);
-            }
-            gf.store(sh, tid);
-        }
-        ndef = 0;
-        // Nothing of the flush stays in flight: the hot loop's header then
-        // waits only for its own prefetch.
-        __builtin_amdgcn_s_waitcnt(0);
     };
 
-    // Two register sets, used in turn: the loads of super-step s+1 are in
-    // flight while super-step s is processed, without register copies.  The
-    // prefetch is issued unconditionally (clamped to the last super-step,
-    // where it is a redundant in-bounds reload) so that every path has the
-    // same number of loads outstanding and the waits stay partial.
     // Buffer loads: the chunk base lives in a scalar resource, the per-lane
     // offsets are loop-invariant registers and the super-step moves only the
     // scalar offset, so no address register is rewritten while loads that
-    // read it are in flight.  The resource covers the chunk (at most 2^18
-    // elements = 2 MiB of binary64), and reads past its end return zero.
-    const __amdgpu_buffer_rsrc_t grs = __builtin_amdgcn_make_buffer_rsrc((void *)gbase, (short)0, (int)(len * ESZG), kBufFlags);
-    const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc((void *)tbase, (short)0, (int)(len * ESZT), kBufFlags);
-    const uint32_t lane_off_g = (uint32_t)tid * BG, lane_off_t = (uint32_t)tid * BT;
-    auto load = [&](u32x4 (&g)[U], u32x4 (&t)[U], uint32_t s) {
+    // read it are in flight.  The resources cover the chunk (at most 2^18
+    // elements = 2 MiB of binary64); reads past its end return zero.
+    auto load_at = [&](u32x4 (&g)[U], u32x4 (&t)[U], const char *gb, const char *tb, uint32_t len, uint32_t s) {
+        const __amdgpu_buffer_rsrc_t grs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)gb, (short)0, (int)(len * ESZG), kBufFlags);
+        const __amdgpu_buffer_rsrc_t trs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)tb, (short)0, (int)(len * ESZT), kBufFlags);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             g[u] = buf_load<BG, kLoadNT>(grs, (int)lane_off_g, (int)((s * U + u) * (kBlock * BG)));
             t[u] = buf_load<BT, kLoadNT>(trs, (int)lane_off_t, (int)((s * U + u) * (kBlock * BT)));
         }
     };
-    auto step = [&](const u32x4 (&g)[U], const u32x4 (&t)[U], uint32_t s) {
+    auto load = [&](u32x4 (&g)[U], u32x4 (&t)[U], const ChunkCtx &c, uint32_t s) {
+        load_at(g, t, c.gbase, c.tbase, c.len, s);
+    };
+    // ib: index of the chunk's first element relative to the run
+    auto step = [&](const u32x4 (&g)[U], const u32x4 (&t)[U], uint32_t s, uint32_t ib) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t v = s * U + u;
-            if (vec_fast<DG, DT, NT, RT>(L, Un, sh, P, g[u], t[u], v, tid)) {
+            if (vec_fast<DG, DT, NT, RT>(L, Un, sh, P, g[u], t[u], v, ib, tid)) {
                 sh.defer[wave][ndef] = v;      // every lane writes the same value
                 ++ndef;
             }
@@ -609,203 +785,283 @@ __device__ void chunk_body(const SigParams &P, Shared &sh, const SigDesc &d, int
         L.s_ulp += L.s_ulp32;
         L.s_ulp32 = 0;
     };
-    if (nsuper > 0) {
-        u32x4 ga[U], ta[U], gb[U], tb[U];
-        const uint32_t last = nsuper - 1;
-        load(ga, ta, 0);
-        uint32_t s = 0;
-        // The deferred list is flushed outside the hot loop, which exits
-        // when the list may not hold the next two super-steps.
-        while (s < nsuper) {
-            for (; s < nsuper; s += 2) {
-                load(gb, tb, min(s + 1, last));
-                step(ga, ta, s);
-                if (s + 1 >= nsuper) {
-                    s += 2;
-                    break;
-                }
-                load(ga, ta, min(s + 2, last));
-                step(gb, tb, s + 1);
-                if (ndef > kDeferCap - 2 * U) {
-                    s += 2;
-                    break;
-                }
-            }
-            flush();
-        }
-    }
-    // ragged tail, or the whole chunk when a pointer is not 16-byte aligned
-    GenAcc ga;
-    ga.load(sh, tid);
+    // The deferred vectors of the current chunk through the generic path.
+    auto flush = [&](const ChunkCtx &c, uint32_t ib) {
+        if (ndef != 0) {
+            GenAcc gf;
+            gf.load(sh, tid);
 #pragma unroll 1
-    for (uint32_t li = nsuper * SUPER + tid; li < len; li += kBlock)
-        generic_elem<DG, DT, NT>(L, ga, sh, P, load_elem<DG>(gbase, li), load_elem<DT>(tbase, li), li, tid);
+            for (uint32_t k = 0; k < ndef; ++k) {
+                const uint32_t v = sh.defer[wave][k];
+                const u32x4 gv = load_vec<BG>(c.gbase, v * kBlock + tid);
+                const u32x4 tv = load_vec<BT>(c.tbase, v * kBlock + tid);
+                const uint32_t li0 = ib + (v * kBlock + tid) * VEC;
+#pragma unroll 1
+                for (int j = 0; j < VEC; ++j)
+                    generic_elem<DG, DT, NT>(L, gf, sh, P, lane_elem<DG>(gv, j), lane_elem<DT>(tv, j), li0 + j,
+                                             tid);
+            }
+            gf.store(sh, tid);
+            ndef = 0;
+            // nothing of the flush stays in flight: the hot loop then waits
+            // only for its own loads
+            __builtin_amdgcn_s_waitcnt(0);
+        }
+    };
 
-    // ---- resolve the fast-path maxima to element indices -----------------
-    // Reload the vector in which the wave's running maximum was first
-    // reached; its lanes holding that value become (value, index) candidates.
-    double mxa = -1.0;
-    uint32_t ixa = kNone, mu = 0, ixu = kNone;
-    if (Un.wv_abs != kNone) {
-        const u32x4 gv = load_vec<BG>(gbase, Un.wv_abs * kBlock + tid);
-        const u32x4 tv = load_vec<BT>(tbase, Un.wv_abs * kBlock + tid);
+    // End of a chunk: the ragged tail (or the whole chunk when a pointer is
+    // not 16-byte aligned) and the wave's binary64 sums.  Fast-path t^2 and
+    // g*t come from their exact per-element identities, then the generic
+    // path's direct sums are added; a fixed order per lane.
+    auto chunk_end = [&](const ChunkCtx &c, uint32_t ib, bool run_end) {
+        GenAcc ga;
+        ga.load(sh, tid);
+#pragma unroll 1
+        for (uint32_t li = c.nsuper * SUPER + tid; li < c.len; li += kBlock)
+            generic_elem<DG, DT, NT>(L, ga, sh, P, load_elem<DG>(c.gbase, li), load_elem<DT>(c.tbase, li), ib + li,
+                                     tid);
+        // the first ordinary element of this lane in the chunk
+        if (Un.first != kNone) {
+            L.first_valid = min(L.first_valid, ib + (Un.first * kBlock + tid) * VEC);
+            Un.first = kNone;
+        }
+        ChunkPartial *out = partials + c.gchunk;
+        {
+            const double f_t2 = (L.s_g2 + 2.0 * L.s_ge) + L.s_sq;
+            const double f_gt = L.s_g2 + L.s_ge;
+            const double lane_sums[6] = {L.s_abs, L.s_sq + ga.sq, L.s_rel, L.s_g2 + ga.g2, f_t2 + ga.t2, f_gt + ga.gt};
 #pragma unroll
-        for (int j = VEC - 1; j >= 0; --j) {
-            const double a = __builtin_fabs(widen<DT>(lane_elem<DT>(tv, j)) - widen<DG>(lane_elem<DG>(gv, j)));
-            if (a == Un.wx_abs) {
-                mxa = a;
-                ixa = (Un.wv_abs * kBlock + tid) * VEC + j;
+            for (int k = 0; k < 6; ++k) {
+                const double v = dpp_sum(lane_sums[k]);
+                if (lane == 0) out->s[wave][k] = v;
             }
         }
-    }
-    if (Un.wv_ulp != kNone) {
-        const u32x4 gv = load_vec<BG>(gbase, Un.wv_ulp * kBlock + tid);
-        const u32x4 tv = load_vec<BT>(tbase, Un.wv_ulp * kBlock + tid);
-#pragma unroll
-        for (int j = VEC - 1; j >= 0; --j) {
-            uint32_t uj;
-            if constexpr (PT::SAME) {
-                const uint32_t gb = lane_elem<DG>(gv, j), tb = lane_elem<DT>(tv, j);
-                uj = max(gb, tb) - min(gb, tb);
-            } else {
-                const auto gb = lane_elem<DG>(gv, j);
-                const auto tb = lane_elem<DT>(tv, j);
-                uj = fast_ulp<DG, DT>(gb, tb, widen<DG>(gb), widen<DT>(tb));
+        reset_sums();
+        if (!run_end && wave == 0) {
+            // neutral values: this chunk's counts, maxima and histogram are
+            // carried into the record of the run's last chunk
+            out->hist[lane] = 0;
+            if (lane < kHistSlots - 64) out->hist[64 + lane] = 0;
+            if (lane < kCnt + PEAT_MAX_THRESHOLDS) {
+                int k = lane;
+                asm volatile("" : "+v"(k));
+                reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(out) + offsetof(ChunkPartial, cnt))[k] = 0;
             }
-            if (uj == Un.wu) {
-                mu = Un.wu;
-                ixu = (Un.wv_ulp * kBlock + tid) * VEC + j;
+            if (lane == 0) {
+                // -1 formed here rather than kept live (and spilled) across the hot loop
+                int32_t m1;
+                asm volatile("v_mov_b32 %0, -1" : "=v"(m1));
+                const int64_t none = m1;
+                out->max_abs = (double)none;
+                out->max_rel = (double)none;
+                out->ix_abs = out->ix_rel = out->ix_ulp = none;
+                out->first_nan = out->first_valid = none;
+                out->sum_ulp = 0;
+                out->max_ulp = 0;
             }
         }
-    }
-    lex_merge(mxa, ixa, L.gx_abs, L.gi_abs);
-    lex_merge(mu, ixu, L.gu, L.gi_ulp);
-    // the first ordinary element of this lane
-    if (Un.first != kNone) L.first_valid = min(L.first_valid, (Un.first * kBlock + tid) * VEC);
+    };
 
-    // ---- epilogue: reduce the block into the chunk record ----------------
-    // fast-path t^2 and g*t from their exact per-element identities, then the
-    // generic path's direct sums; a fixed order per lane
-    const double f_t2 = (L.s_g2 + 2.0 * L.s_ge) + L.s_sq;
-    const double f_gt = L.s_g2 + L.s_ge;
-    double sums[6] = {L.s_abs, L.s_sq + ga.sq, L.s_rel, L.s_g2 + ga.g2, f_t2 + ga.t2, f_gt + ga.gt};
+    // End of a run: counts, maxima, first indices, ULP sum and histogram of
+    // the block go into the record of the run's last chunk (indices made
+    // relative to the pair by run_off); then the run state starts afresh.
+    auto run_end_reduce = [&](const ChunkCtx &c, int64_t run_off) {
+        {
+            double mxa = L.gx_abs, mxr = L.mx_rel;
+            uint32_t ixa = L.gi_abs, ixr = L.ix_rel, mu = L.gu, ixu = L.gi_ulp;
+            dpp_max(mxa, ixa);
+            dpp_max(mxr, ixr);
+            dpp_max(mu, ixu);
+            const uint32_t fnan = dpp_min_u32(L.first_nan), fval = dpp_min_u32(L.first_valid);
+            // at most 2^43 per lane (2048 distances below 2^32): exact in binary64
+            const uint64_t sulp = (uint64_t)dpp_sum((double)L.s_ulp);
+            if (lane == 0) {
+                sh.rmax[wave][0] = mxa;
+                sh.rmax[wave][1] = mxr;
+                sh.rix[wave][0] = ixa;
+                sh.rix[wave][1] = ixr;
+                sh.rix[wave][2] = ixu;
+                sh.rix[wave][3] = fnan;
+                sh.rix[wave][4] = fval;
+                sh.rmu[wave] = mu;
+                sh.rulp[wave] = sulp;
+            }
+        }
+        {
+            // fast-path counts: every element there is valid, finite, golden nonzero
+            const uint32_t common = Un.common * 64u * VEC;
 #pragma unroll
-    for (int k = 0; k < 6; ++k) sums[k] = wsum(sums[k]);
-    double mxr = L.mx_rel;
-    uint32_t ixr = L.ix_rel;
-    wmax(mxa, ixa);
-    wmax(mxr, ixr);
-    wmax(mu, ixu);
-    const uint32_t fnan = wmin_u(L.first_nan), fval = wmin_u(L.first_valid);
-    const uint64_t sulp = wsum_u64(L.s_ulp);
-    uint32_t cnts[kCnt + PEAT_MAX_THRESHOLDS];
+            for (int k = 0; k < kCnt; ++k) {
+                const uint32_t v = dpp_sum_u32(L.cnt[k]) + ((k == C_VALID || k == C_FINITE || k == C_REL) ? common : 0u);
+                if (lane == 0) sh.rcnt[wave][k] = v;
+            }
 #pragma unroll
-    for (int c = 0; c < kCnt; ++c) cnts[c] = wsum_u(L.cnt[c]);
-#pragma unroll
-    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) cnts[kCnt + j] = j < NT ? wsum_u(L.mism[j]) : 0u;
-    // fast-path counts: every element there is valid, finite, golden nonzero
-    const uint32_t common = Un.common * 64u * VEC;
-    cnts[C_VALID] += common;
-    cnts[C_FINITE] += common;
-    cnts[C_REL] += common;
-#pragma unroll
-    for (int j = 0; j < NT; ++j) cnts[kCnt + j] += Un.mism[j];
-    if (lane == 0) {
-#pragma unroll
-        for (int k = 0; k < 6; ++k) sh.rd[wave][k] = sums[k];
-        sh.rmax[wave][0] = mxa;
-        sh.rmax[wave][1] = mxr;
-        sh.rix[wave][0] = ixa;
-        sh.rix[wave][1] = ixr;
-        sh.rix[wave][2] = ixu;
-        sh.rix[wave][3] = fnan;
-        sh.rix[wave][4] = fval;
-        sh.rmu[wave] = mu;
-        sh.rulp[wave] = sulp;
-#pragma unroll
-        for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) sh.rcnt[wave][c] = cnts[c];
-    }
-    __syncthreads();
+            for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) {
+                const uint32_t v = j < NT ? dpp_sum_u32(L.mism[j]) + Un.mism[j] : 0u;
+                if (lane == 0) sh.rcnt[wave][kCnt + j] = v;
+            }
+        }
+        __syncthreads();
 
-    ChunkPartial *out = P.partials + gchunk;
-    // histogram: thread t sums slot t/4 over a quarter of the words
-    {
-        const int slot = tid >> 2, q = tid & 3;
-        uint32_t acc = 0;
-        const uint32_t *row = sh.hist + slot * kHistCols + q * 32;
+        ChunkPartial *out = partials + c.gchunk;
+        // histogram: thread t sums slot t/4 over a quarter of the words and
+        // clears them for the next run
+        {
+            const int slot = tid >> 2, q = tid & 3;
+            uint32_t acc = 0;
+            uint32_t *row = sh.hist + slot * kHistCols + q * 32;
 #pragma unroll 8
-        for (int c = 0; c < 32; ++c) {
-            const uint32_t w = row[(c + slot + 8 * q) & 31];
-            acc += (w & 0xFFFFu) + (w >> 16);
-        }
-        acc += __shfl_xor(acc, 1);
-        acc += __shfl_xor(acc, 2);
-        if (q == 0) out->hist[slot] = acc;
-        // slots 64..66 (beyond 256/4 threads): one thread each
-        if (tid < kHistSlots - 64) {
-            const int s2 = 64 + tid;
-            uint32_t a2 = 0;
-            for (int c = 0; c < kHistCols; ++c) {
-                const uint32_t w = sh.hist[s2 * kHistCols + c];
-                a2 += (w & 0xFFFFu) + (w >> 16);
+            for (int k = 0; k < 32; ++k) {
+                const int col = (k + slot + 8 * q) & 31;
+                const uint32_t w = row[col];
+                row[col] = 0;
+                acc += (w & 0xFFFFu) + (w >> 16);
             }
-            out->hist[s2] = a2;
+            dsum_step<kDppXor1, 0xF>(acc);        // the four quarters of the slot
+            dsum_step<kDppXor2, 0xF>(acc);
+            if (q == 0) out->hist[slot] = acc;
+            // slots 64..66 (beyond 256/4 threads): one thread each
+            if (tid < kHistSlots - 64) {
+                const int s2 = 64 + tid;
+                uint32_t a2 = 0;
+                for (int k = 0; k < kHistCols; ++k) {
+                    const uint32_t w = sh.hist[s2 * kHistCols + k];
+                    sh.hist[s2 * kHistCols + k] = 0;
+                    a2 += (w & 0xFFFFu) + (w >> 16);
+                }
+                out->hist[s2] = a2;
+            }
         }
-    }
-    if (tid == 0) {
-        double s[6] = {0, 0, 0, 0, 0, 0};
-        double ma = -1.0, mr = -1.0;
-        uint32_t ia = kNone, ir = kNone, iu = kNone, fn = kNone, fv = kNone, m = 0;
-        uint64_t su = 0;
-        uint32_t cn[kCnt + PEAT_MAX_THRESHOLDS];
-        for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] = 0;
-        for (int w = 0; w < kWaves; ++w) {
-            for (int k = 0; k < 6; ++k) s[k] += sh.rd[w][k];
-            lex_merge(ma, ia, sh.rmax[w][0], sh.rix[w][0]);
-            lex_merge(mr, ir, sh.rmax[w][1], sh.rix[w][1]);
-            lex_merge(m, iu, sh.rmu[w], sh.rix[w][2]);
-            fn = min(fn, sh.rix[w][3]);
-            fv = min(fv, sh.rix[w][4]);
-            su += sh.rulp[w];
-            for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] += sh.rcnt[w][c];
+        // the waves' totals, one field per thread, waves in order
+        if (tid >= 64 && tid < 64 + kCnt + PEAT_MAX_THRESHOLDS) {
+            int k = tid;
+            // formed here rather than kept live (and spilled) across the hot loop
+            asm volatile("" : "+v"(k));
+            k -= 64;
+            uint32_t a = 0;
+            for (int w = 0; w < kWaves; ++w) a += sh.rcnt[w][k];
+            reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(out) + offsetof(ChunkPartial, cnt))[k] = a;
+        } else if (tid == 128) {
+            double ma = -1.0;
+            uint32_t ia = kNone;
+            for (int w = 0; w < kWaves; ++w) lex_merge(ma, ia, sh.rmax[w][0], sh.rix[w][0]);
+            out->max_abs = ma;
+            out->ix_abs = ia == kNone ? -1 : run_off + ia;
+        } else if (tid == 129) {
+            double mr = -1.0;
+            uint32_t ir = kNone;
+            for (int w = 0; w < kWaves; ++w) lex_merge(mr, ir, sh.rmax[w][1], sh.rix[w][1]);
+            out->max_rel = mr;
+            out->ix_rel = ir == kNone ? -1 : run_off + ir;
+        } else if (tid == 130) {
+            uint32_t m = 0, iu = kNone, fv = kNone;
+            for (int w = 0; w < kWaves; ++w) {
+                lex_merge(m, iu, sh.rmu[w], sh.rix[w][2]);
+                fv = min(fv, sh.rix[w][4]);
+            }
+            // every ULP distance in the run is 0: the first valid element is the maximum
+            if (iu == kNone || m == 0) {
+                m = 0;
+                iu = fv;
+            }
+            out->max_ulp = m;
+            out->ix_ulp = iu == kNone ? -1 : run_off + iu;
+        } else if (tid == 192) {
+            uint32_t fn = kNone, fv = kNone;
+            uint64_t su = 0;
+            for (int w = 0; w < kWaves; ++w) {
+                fn = min(fn, sh.rix[w][3]);
+                fv = min(fv, sh.rix[w][4]);
+                su += sh.rulp[w];
+            }
+            out->first_nan = fn == kNone ? -1 : run_off + fn;
+            out->first_valid = fv == kNone ? -1 : run_off + fv;
+            out->sum_ulp = su;
         }
-        // every ULP distance in the chunk is 0: the first valid element is the maximum
-        if (iu == kNone || m == 0) {
-            m = 0;
-            iu = fv;
+        // the per-wave records and the histogram are free again
+        __syncthreads();
+        lane_init(L, Un);
+    };
+
+    lane_init(L, Un);
+    reset_sums();
+    ndef = 0;
+    // Two register sets, used in turn: the loads of the next super-step are
+    // in flight while the current one is processed.  A chunk's first
+    // super-step is always in (ga, ta): the last super-step of the previous
+    // chunk issues it, before its processing when it comes from (gb, tb),
+    // after it when it comes from (ga, ta), so the chunk's sums are reduced
+    // while the next chunk's data is on its way.
+    u32x4 ga[U], ta[U], gb[U], tb[U];
+    bool pre = false;              // the current chunk's first super-step is loaded
+    // the block's chunks c0 + i, i < cnt (at most 8; 32-bit scalar arithmetic)
+    const int64_t c0 = (int64_t)blockIdx.x * P.chunk_group;
+    const int cnt = (int)__builtin_amdgcn_readfirstlane(
+        (uint32_t)(nch - c0 < P.chunk_group ? nch - c0 : P.chunk_group));
+    int run_first = 0;             // first chunk of the current run
+    int64_t run_off = 0;           // its first element in the pair
+    PairS dcur = pair_of(c0);
+    ChunkCtx cur = ctx(dcur, c0);
+    for (int i = 0; i < cnt; ++i) {
+        const int64_t c = c0 + i;
+        const bool more = i + 1 < cnt;
+        // the next chunk: same pair unless this one is the pair's last
+        PairS dnxt = dcur;
+        if (more && P.chunk_base + c + 1 >= dcur.first + dcur.nchunks) dnxt = pair_of(c + 1);
+        const ChunkCtx nxt = ctx(dnxt, more ? c + 1 : c);
+        const bool chain = more && nxt.nsuper > 0;
+        const bool run_end = !more || nxt.pair != cur.pair;
+        if (i == run_first) run_off = cur.off;
+        const uint32_t ib = (uint32_t)(i - run_first) << cur.log2;
+        if (cur.nsuper > 0) {
+            if (!pre) load(ga, ta, cur, 0);
+            // Every half step issues one set of loads (the next super-step,
+            // the next chunk's first, or a re-read of the current one when
+            // nothing follows), chosen by scalar selects, so every path has
+            // the same loads outstanding and the waits stay partial.
+            for (uint32_t s = 0;;) {
+                bool last = s + 1 >= cur.nsuper;
+                load(gb, tb, cur, last ? s : s + 1);
+                step(ga, ta, s, ib);
+                if (last) {
+                    if (chain) load(ga, ta, nxt, 0);
+                    break;
+                }
+                ++s;
+                last = s + 1 >= cur.nsuper;
+                const bool hop = last && chain;
+                load_at(ga, ta, hop ? nxt.gbase : cur.gbase, hop ? nxt.tbase : cur.tbase, hop ? nxt.len : cur.len,
+                        hop ? 0u : (last ? s : s + 1));
+                step(gb, tb, s, ib);
+                if (last) break;
+                ++s;
+                // the deferred list must hold the next two super-steps
+                if (ndef > kDeferCap - 2 * U) flush(cur, ib);
+            }
         }
-        out->s_abs = s[0];
-        out->s_sq = s[1];
-        out->s_rel = s[2];
-        out->s_g2 = s[3];
-        out->s_t2 = s[4];
-        out->s_gt = s[5];
-        out->max_abs = ma;
-        out->max_rel = mr;
-        out->ix_abs = ia == kNone ? -1 : off + ia;
-        out->ix_rel = ir == kNone ? -1 : off + ir;
-        out->ix_ulp = iu == kNone ? -1 : off + iu;
-        out->first_nan = fn == kNone ? -1 : off + fn;
-        out->first_valid = fv == kNone ? -1 : off + fv;
-        out->sum_ulp = su;
-        out->max_ulp = m;
-        for (int c = 0; c < kCnt; ++c) out->cnt[c] = cn[c];
-        for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) out->mism[j] = cn[kCnt + j];
+        // a chunk without super-steps issued no load for the next one
+        pre = chain && cur.nsuper > 0;
+        flush(cur, ib);
+        chunk_end(cur, ib, run_end);
+        if (run_end) {
+            run_end_reduce(cur, run_off);
+            run_first = i + 1;
+        }
+        dcur = dnxt;
+        cur = nxt;
     }
 }
 
 // Three blocks per CU (12 waves) where the registers allow it without
 // spilling in the hot loop: f32 with two absolute thresholds, the common case.
 template <int DG, int DT, int NT, bool RT>
-constexpr int chunk_blocks_per_cu() { return (DG == PEAT_F32 && DT == PEAT_F32 && NT == 2 && !RT) ? 3 : 2; }
+constexpr int chunk_blocks_per_cu() { return (DG == DT && NT == 2 && !RT) ? 3 : 2; }
 
 template <int DG, int DT, int NT, bool RT>
-__global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>())) sig_chunk(SigParams P) {
+__global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()))
+    sig_chunk(SigParams P, const SigDesc *__restrict__ descs, const int32_t *__restrict__ chunk_pair,
+              ChunkPartial *__restrict__ partials) {
     __shared__ Shared sh;
-    const int64_t gchunk = P.chunk_base + blockIdx.x;
-    const int pair = P.chunk_pair[gchunk];
-    const SigDesc d = P.descs[pair];
-    const int64_t cin = gchunk - d.first_chunk;
     const int tid = threadIdx.x;
     // clear the lane-private histogram counters and build the exponent table:
     // slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi
@@ -824,16 +1080,53 @@ __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()
         sh.hrow[E] = (uint32_t)(slot * kHistCols);
     }
     __syncthreads();
-    chunk_body<DG, DT, NT, RT>(P, sh, d, cin, gchunk);
+    chunk_loop<DG, DT, NT, RT>(P, sh, descs, chunk_pair, partials);
+}
+
+// Blocks of one chunk-pass instantiation that the current device holds at
+// once: its occupancy per compute unit times the compute units, looked up
+// once per device.
+template <int DG, int DT, int NT, bool RT>
+int64_t resident_blocks() {
+    constexpr int kDevs = 64;
+    static std::atomic<int32_t> cached[kDevs];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+    if (dev >= 0 && dev < kDevs) {
+        const int32_t v = cached[dev].load(std::memory_order_relaxed);
+        if (v > 0) return v;
+    }
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sig_chunk<DG, DT, NT, RT>, kBlock, 0) != hipSuccess ||
+        per_cu < 1)
+        per_cu = 1;
+    if (dev < 0 || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 256;
+    (void)hipGetLastError();        // a failed query above is not the launch's error
+    const int32_t v = per_cu * cus;
+    if (dev >= 0 && dev < kDevs) cached[dev].store(v, std::memory_order_relaxed);
+    return v;
+}
+
+
+template <int DG, int DT, int NT, bool RT>
+void launch_chunks(const SigParams &p, int64_t n, hipStream_t s) {
+    const int64_t r = resident_blocks<DG, DT, NT, RT>();
+    int64_t k = n / (kMinRounds * r);
+    k = k < 1 ? 1 : (k > kMaxGroup ? kMaxGroup : k);
+    SigParams q = p;
+    q.chunk_count = n;
+    q.chunk_group = k;
+    hipLaunchKernelGGL((sig_chunk<DG, DT, NT, RT>), dim3((unsigned)((n + k - 1) / k)), dim3(kBlock), 0, s, q,
+                       static_cast<const SigDesc *>(p.descs), static_cast<const int32_t *>(p.chunk_pair), p.partials);
 }
 
 template <int DG, int DT, bool RT>
 hipError_t launch_kind_rt(const SigParams &p, int64_t n, hipStream_t s) {
-    dim3 grid((unsigned)n), block(kBlock);
     switch (p.nthr_pad) {
-        case 2: hipLaunchKernelGGL((sig_chunk<DG, DT, 2, RT>), grid, block, 0, s, p); break;
-        case 4: hipLaunchKernelGGL((sig_chunk<DG, DT, 4, RT>), grid, block, 0, s, p); break;
-        default: hipLaunchKernelGGL((sig_chunk<DG, DT, 8, RT>), grid, block, 0, s, p); break;
+        case 2: launch_chunks<DG, DT, 2, RT>(p, n, s); break;
+        case 4: launch_chunks<DG, DT, 4, RT>(p, n, s); break;
+        default: launch_chunks<DG, DT, 8, RT>(p, n, s); break;
     }
     return hipGetLastError();
 }

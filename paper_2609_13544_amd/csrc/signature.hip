@@ -29,8 +29,13 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] = 0;
     for (int c = tid; c < m; c += kBlock) {
         const ChunkPartial &p = parts[c];
-        s[0] += p.s_abs; s[1] += p.s_sq; s[2] += p.s_rel;
-        s[3] += p.s_g2; s[4] += p.s_t2; s[5] += p.s_gt;
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {
+            double t = p.s[0][k];                 // the chunk: its waves in order
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) t += p.s[w][k];
+            s[k] += t;
+        }
         if (p.ix_abs >= 0 && (ia < 0 || p.max_abs > ma || (p.max_abs == ma && p.ix_abs < ia))) { ma = p.max_abs; ia = p.ix_abs; }
         if (p.ix_rel >= 0 && (ir < 0 || p.max_rel > mr || (p.max_rel == mr && p.ix_rel < ir))) { mr = p.max_rel; ir = p.ix_rel; }
         if (p.ix_ulp >= 0 && (iu < 0 || p.max_ulp > mu || (p.max_ulp == mu && p.ix_ulp < iu))) { mu = p.max_ulp; iu = p.ix_ulp; }

@@ -148,6 +148,31 @@ def test_async_records_match_sync():
     assert recs == sync
 
 
+@pytest.mark.parametrize("code", [0, 1])
+def test_block_chunk_sequences(code):
+    """A batch with enough chunks (over 16 per resident block) that blocks take
+    two consecutive chunks: chunks without a full super-step (short pairs,
+    unaligned pairs) alternate with full and ragged chunks, runs of two chunks
+    of one pair with runs that cross pairs, with and without special values.
+    Every record equals its single call (one chunk per block) and the oracle."""
+    sizes = [2048, 3 * 4096, 4096 + 904, 20000, 4095, 9000]
+    hosts, dev = [], []
+    for k in range(7000):
+        n = sizes[k % len(sizes)]
+        gb, tb = special_pair(n, code, seed=50000 + k, special_frac=1e-3 if k % 3 == 0 else 0.0)
+        g, t = to_device(gb, code), to_device(tb, code)
+        if k % 7 == 3:                  # not 16-byte aligned: no super-steps
+            g, t = to_device(np.concatenate([gb[:1], gb]), code)[1:], to_device(np.concatenate([tb[:1], tb]), code)[1:]
+        hosts.append((gb, tb))
+        dev.append((g, t))
+    recs = P.signature_batched(dev, synth.BINS, synth.THRESHOLDS)
+    for k, ((gb, tb), (g, t)) in enumerate(zip(hosts, dev)):
+        single = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+        assert all(recs[k][f] == v or (isinstance(v, float) and math.isnan(v) and math.isnan(recs[k][f]))
+                   for f, v in single.items()), f"pair {k}: batched and single differ"
+        assert_parity(recs[k], oracle_sig(gb, tb, code, synth.BINS, synth.THRESHOLDS), f"pair {k}")
+
+
 def test_chunk_size_rule_boundaries():
     """Pairs on both sides of the switch from ~256 to ~64 chunks per pair
     (2^22 elements) and at the 2^18-element chunk cap, against the oracle;
