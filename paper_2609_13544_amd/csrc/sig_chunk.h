@@ -520,13 +520,8 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
     return false;
 }
 
-// ---- wave reductions (fixed butterfly order) -------------------------------
+// ---- wave reductions of the finalize pass (fixed butterfly order) ----------
 __device__ __forceinline__ double wsum(double v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-__device__ __forceinline__ uint32_t wsum_u(uint32_t v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
     return v;
@@ -536,11 +531,7 @@ __device__ __forceinline__ uint64_t wsum_u64(uint64_t v) {
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
     return v;
 }
-__device__ __forceinline__ uint32_t wmin_u(uint32_t v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = min(v, (uint32_t)__shfl_xor(v, o));
-    return v;
-}
+
 // ---- wave reductions by DPP (chunk records) ---------------------------------
 // The classic six-step pattern: pairs and quads (quad_perm), half rows and
 // rows (mirrors), then rows 1 and 3 take the last lane of rows 0 and 2
@@ -644,18 +635,6 @@ __device__ __forceinline__ void dpp_max(V &v, uint32_t &ix) {
     ix = lane63_u32(ix);
 }
 
-// (value desc, index asc) over entries with index != kNone
-template <typename V>
-__device__ __forceinline__ void wmax(V &v, uint32_t &ix) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const V ov = __shfl_xor(v, o);
-        const uint32_t oi = __shfl_xor(ix, o);
-        const bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
-        v = take ? ov : v;
-        ix = take ? oi : ix;
-    }
-}
 
 // A 64-bit value that is the same in every lane, as a scalar.
 __device__ __forceinline__ uint64_t uniform_u64(uint64_t v) {

@@ -21,9 +21,9 @@
 //   finalize sum = (pass 2 + pass 3) + exact candidate sums + need * T.
 //
 // The k-th largest error T is the key with all five digits fixed; count_above
-// is k minus the copies of T taken.  Passes 2 and 3 sum in the fixed
-// per-lane / butterfly / wave order of the signature pass over chunks whose
-// size depends only on n, and the candidate sums are exact integers, so the
+// is k minus the copies of T taken.  Passes 2 and 3 sum in a fixed
+// per-lane / butterfly / wave order over chunks whose size depends only on
+// n, and the candidate sums are exact integers, so the
 // result does not depend on the order in which candidates are copied.
 #include "elements.h"
 
