@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PEAT_ABI_VERSION 4
+#define PEAT_ABI_VERSION 5
 #define PEAT_MAX_THRESHOLDS 8
 #define PEAT_MAX_BINS 64
 
@@ -220,6 +220,24 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
                                  const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                                  peat_signature_t *d_outs, void *stream);
 
+/* One step of the assessment in a single pass over the data: the random bit
+ * flips of peat_inject (Section II-B; same generator and decisions) are
+ * applied to every pair's test tensor in place, with seed seeds[k], the
+ * given rate and bitmask (valid for every pair's dtype), and the signatures
+ * of the pairs (golden, flipped test) are computed -- records, tensor bits
+ * and counts equal to peat_inject_batched followed by
+ * peat_signature_batched.  Each chunk of a test tensor is flipped (atomic
+ * bit toggles) before it is read, in the same kernel.  seeds is a host array
+ * of count seeds; d_outs a device array of count records and d_counts a
+ * device int64 array of count flip counts, written when the stream reaches
+ * the work.  Test tensors must not overlap one another or any golden tensor
+ * (PEAT_EINVAL); PEAT_ERATE for a NaN or negative rate, PEAT_EBITMASK for a
+ * bitmask that is 0 or reaches beyond a pair's type width. */
+int peat_inject_signature_batched_async(const peat_pair_t *pairs, int32_t count, const uint64_t *seeds,
+                                        double rate, uint64_t bitmask, const peat_bins_t *bins,
+                                        const peat_thresholds_t *thresholds, peat_signature_t *d_outs,
+                                        int64_t *d_counts, void *stream);
+
 /* Signature of a mixed-precision pair (Section III-C; types as in
  * peat_mixed_pair_t).  Every field keeps its definition over the exact
  * binary64 values of both sides, except the ULP distance, which is counted
@@ -360,7 +378,8 @@ int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
  * class since the last read, and clears that class.  Kernel classes:
  * 0 signature chunk pass, 1 signature finalize, 2 injection, 3 injection
  * count reduction, 4 streaming read (peat_stream_read), 5 top-k passes 1-2
- * with their selections, 6 top-k pass 3, candidate rounds and finalize. */
+ * with their selections, 6 top-k pass 3, candidate rounds and finalize,
+ * 7 chunk pass with the injection (peat_inject_signature_batched_async). */
 int peat_profile_enable(int on);
 int peat_profile_read(int kernel_class, double *total_ms, int64_t *launches);
 

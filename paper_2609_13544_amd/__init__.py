@@ -11,4 +11,5 @@ from ._binding import (  # noqa: F401
     profile_read, set_stream, signature, signature_batched, signature_batched_async, stream_read,
     strerror, topk_mean, topk_mean_batched, series_stats, spearman, normalize_scores,
     signature_mixed, signature_mixed_batched, signature_mixed_batched_async, topk_mean_mixed_batched,
+    inject_signature_batched_async, K_SIG_INJECT,
 )

@@ -24,6 +24,7 @@ MAX_THRESHOLDS, MAX_BINS = 8, 64
 
 # kernel classes of peat_profile_read
 K_SIG_CHUNK, K_SIG_FINALIZE, K_INJECT, K_INJECT_SUM, K_STREAM_READ, K_TOPK_A, K_TOPK_B = 0, 1, 2, 3, 4, 5, 6
+K_SIG_INJECT = 7   # chunk pass with the injection
 
 
 class PeatError(RuntimeError):
@@ -129,6 +130,11 @@ _PROTOS = {
     "peat_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
                                                     ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
                                                     ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_inject_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
+                                                           ctypes.POINTER(ctypes.c_uint64), ctypes.c_double,
+                                                           ctypes.c_uint64, ctypes.POINTER(Bins),
+                                                           ctypes.POINTER(Thresholds), ctypes.c_void_p,
+                                                           ctypes.c_void_p, ctypes.c_void_p]),
     "peat_inject": (ctypes.c_int64, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
                                      ctypes.c_double, ctypes.c_uint64]),
     "peat_inject_model": (ctypes.c_int64, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint64,
@@ -456,6 +462,30 @@ def signature_batched_async(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 
     _check(lib().peat_signature_batched_async(prep.arr, prep.count, ctypes.byref(b), ctypes.byref(th),
                                               d_out.data_ptr(), _stream_ptr(stream)),
            "peat_signature_batched_async")
+
+
+def inject_signature_batched_async(pairs, seeds, rate: float, bitmask: int, d_out, d_counts,
+                                   bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), stream=None) -> None:
+    """peat_inject_signature_batched_async: the bit flips of peat_inject
+    (seeds[k], rate, bitmask) go into each pair's test tensor and the
+    signatures of the flipped pairs land in d_out (device uint8, at least
+    len(pairs) * SIG_BYTES bytes); d_counts (device int64, len(pairs)) gets
+    the flip counts, when the stream gets there."""
+    prep = pairs if isinstance(pairs, PreparedPairs) else PreparedPairs(pairs)
+    _dev_tensor(d_out, "d_out")
+    _dev_tensor(d_counts, "d_counts")
+    if d_out.numel() * d_out.element_size() < prep.count * SIG_BYTES:
+        raise ValueError("d_out too small")
+    if d_counts.dtype != _torch().int64 or d_counts.numel() < prep.count:
+        raise ValueError("d_counts must be an int64 device tensor of len(pairs) entries")
+    if len(seeds) != prep.count:
+        raise ValueError("one seed per pair")
+    sd = (ctypes.c_uint64 * max(1, prep.count))(*[int(x) & (2 ** 64 - 1) for x in seeds])
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    _check(lib().peat_inject_signature_batched_async(prep.arr, prep.count, sd, float(rate), bitmask & (2 ** 64 - 1),
+                                                     ctypes.byref(b), ctypes.byref(th), d_out.data_ptr(),
+                                                     d_counts.data_ptr(), _stream_ptr(stream)),
+           "peat_inject_signature_batched_async")
 
 
 def decode_records(d_out, count: int, nthr: int | None = None) -> list[dict]:

@@ -1,6 +1,7 @@
 // Host side of libpeat: argument validation, per-device workspace and pinned
 // staging, stream ordering, optional kernel timing, and the extern "C"
 // entry points declared in include/peat.h.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -283,10 +284,13 @@ int build_descs(const peat_mixed_pair_t *pairs, int32_t count, std::vector<SigDe
 }
 
 // Common core of every signature call.  When host_outs is set the records go
-// through workspace + pinned staging and the call waits for them.
+// through workspace + pinned staging and the call waits for them.  With inj
+// (one InjDesc per pair, same-type pairs) the chunk pass first injects the
+// test tensors' bit flips and d_counts receives the flip counts.
 int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bins_t *bins,
                    const peat_thresholds_t *thr, peat_signature_t *d_outs,
-                   peat_signature_t *host_outs, hipStream_t s) {
+                   peat_signature_t *host_outs, hipStream_t s, const std::vector<InjDesc> *inj = nullptr,
+                   int64_t *d_counts = nullptr) {
     if (count < 0) return fail(PEAT_EINVAL, "count < 0");
     if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
     int rc = check_bins_thr(bins, thr);
@@ -307,27 +311,32 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
 
     const size_t b_desc = align_up(sizeof(SigDesc) * count);
+    const size_t b_inj = inj ? align_up(sizeof(InjDesc) * count) : 0;
     const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
     const size_t b_part = align_up(sizeof(ChunkPartial) * (size_t)total);
     const size_t b_out = host_outs ? align_up(sizeof(peat_signature_t) * count) : 0;
 
+    // device workspace: descriptors | injection descriptors | chunk map |
+    // chunk records | records; the first three are staged and copied at once
     char *ws;
-    if ((rc = acquire_ws(d, b_desc + b_map + b_part + b_out, s, &ws))) return rc;
+    if ((rc = acquire_ws(d, b_desc + b_inj + b_map + b_part + b_out, s, &ws))) return rc;
     Slot *sl;
-    if ((rc = acquire_slot(d, b_desc + b_map + b_out, &sl))) return rc;
+    if ((rc = acquire_slot(d, b_desc + b_inj + b_map + b_out, &sl))) return rc;
     char *h = static_cast<char *>(sl->host);
     std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
-    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc);
+    if (inj) std::memcpy(h + b_desc, inj->data(), sizeof(InjDesc) * count);
+    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc + b_inj);
     for (int k = 0; k < count; ++k)
         for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
-    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + b_inj + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
 
     SigParams P;
     P.chunk_base = 0;
     P.descs = reinterpret_cast<const SigDesc *>(ws);
-    P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc);
-    P.partials = reinterpret_cast<ChunkPartial *>(ws + b_desc + b_map);
-    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_desc + b_map + b_part) : d_outs;
+    P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc + b_inj);
+    P.partials = reinterpret_cast<ChunkPartial *>(ws + b_desc + b_inj + b_map);
+    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_desc + b_inj + b_map + b_part) : d_outs;
+    P.inj_counts = inj ? d_counts : nullptr;
     P.count = count;
     P.lo = bins->lo_log2;
     P.hi = bins->hi_log2;
@@ -346,13 +355,16 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
 
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;
-    HIP_OR_FAIL(launch_sig_chunks(P, range, s));
-    if ((rc = prof_end(d, s, 0, ev))) return rc;
+    if (inj)
+        HIP_OR_FAIL(launch_sig_chunks_inject(P, range, reinterpret_cast<const InjDesc *>(ws + b_desc), s));
+    else
+        HIP_OR_FAIL(launch_sig_chunks(P, range, s));
+    if ((rc = prof_end(d, s, inj ? 7 : 0, ev))) return rc;
     if ((rc = prof_begin(d, s, &ev))) return rc;
     HIP_OR_FAIL(launch_sig_finalize(P, s));
     if ((rc = prof_end(d, s, 1, ev))) return rc;
 
-    char *hout = h + b_desc + b_map;
+    char *hout = h + b_desc + b_inj + b_map;
     if (host_outs)
         HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_signature_t) * count, hipMemcpyDeviceToHost, s));
     if ((rc = release_slot(*sl, s))) return rc;
@@ -460,6 +472,70 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
         std::memcpy(host_counts, hout, sizeof(int64_t) * count);
     }
     return PEAT_OK;
+}
+
+// Injection and signature in one pass (same-type pairs, the bit-flip model):
+// the records and flip counts of peat_inject_batched on the test tensors
+// followed by peat_signature_batched.
+int inject_signature_core(const peat_pair_t *pairs, int32_t count, const uint64_t *seeds, double rate,
+                          uint64_t bitmask, const peat_bins_t *bins, const peat_thresholds_t *thr,
+                          peat_signature_t *d_outs, int64_t *d_counts, hipStream_t s) {
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    if ((rc = check_bins_thr(bins, thr))) return rc;
+    if (std::isnan(rate) || rate < 0) return fail(PEAT_ERATE, "rate must be >= 0");
+    if (count > 0 && !seeds) return fail(PEAT_EINVAL, "seeds is NULL");
+    for (int k = 0; k < count; ++k) {
+        const int width = elem_size(pairs[k].dtype) * 8;
+        if (bitmask == 0 || (bitmask >> width) != 0)
+            return fail(PEAT_EBITMASK, "pair %d: bitmask 0x%llx is 0 or has bits at or above bit %d", k,
+                        (unsigned long long)bitmask, width);
+    }
+    // The flips go into the test tensors, which must not overlap one another
+    // or any golden tensor of the batch (the result would depend on order).
+    {
+        struct Span { uintptr_t a, b; int test; int k; };
+        std::vector<Span> sp;
+        sp.reserve(2 * (size_t)count);
+        for (int k = 0; k < count; ++k) {
+            if (pairs[k].n == 0) continue;
+            const uintptr_t es = (uintptr_t)elem_size(pairs[k].dtype);
+            const uintptr_t g = reinterpret_cast<uintptr_t>(pairs[k].golden);
+            const uintptr_t t = reinterpret_cast<uintptr_t>(pairs[k].test);
+            sp.push_back({g, g + (uintptr_t)pairs[k].n * es, 0, k});
+            sp.push_back({t, t + (uintptr_t)pairs[k].n * es, 1, k});
+        }
+        std::sort(sp.begin(), sp.end(), [](const Span &x, const Span &y) { return x.a < y.a; });
+        // sweep: a test span may not intersect any other span
+        uintptr_t end_any = 0, end_test = 0;
+        int k_any = -1, k_test = -1;
+        for (const Span &x : sp) {
+            if (x.test && x.a < end_any)
+                return fail(PEAT_EINVAL, "pair %d: test tensor overlaps a tensor of pair %d", x.k, k_any);
+            if (!x.test && x.a < end_test)
+                return fail(PEAT_EINVAL, "pair %d: test tensor overlaps the golden tensor of pair %d", k_test, x.k);
+            if (x.b > end_any) { end_any = x.b; k_any = x.k; }
+            if (x.test && x.b > end_test) { end_test = x.b; k_test = x.k; }
+        }
+    }
+    if (count == 0) return PEAT_OK;
+    if (!d_outs || !d_counts) return fail(PEAT_EINVAL, "d_outs or d_counts is NULL");
+    std::vector<InjDesc> inj((size_t)count);
+    for (int k = 0; k < count; ++k) {
+        InjDesc &q = inj[k];
+        std::memset(&q, 0, sizeof q);
+        q.x = const_cast<void *>(pairs[k].test);
+        q.n = pairs[k].n;
+        q.seed = seeds[k];
+        q.mask = bitmask;
+        q.dtype = pairs[k].dtype;
+        q.popc = __builtin_popcountll(bitmask);
+        q.model = PEAT_MODEL_BITFLIP;
+        q.all = rate >= 1.0;
+        q.T = (q.all || rate == 0.0) ? 0 : (uint64_t)std::ldexp(rate, 64);
+    }
+    return signature_core(mp.data(), count, bins, thr, d_outs, nullptr, s, &inj, d_counts);
 }
 
 // Mean of the k largest errors: three streaming passes and the candidate
@@ -651,6 +727,14 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count, const 
     if (rc) return rc;
     return signature_core(mp.data(), count, bins, thresholds, d_outs, nullptr,
                           static_cast<hipStream_t>(stream));
+}
+
+int peat_inject_signature_batched_async(const peat_pair_t *pairs, int32_t count, const uint64_t *seeds,
+                                        double rate, uint64_t bitmask, const peat_bins_t *bins,
+                                        const peat_thresholds_t *thresholds, peat_signature_t *d_outs,
+                                        int64_t *d_counts, void *stream) {
+    return inject_signature_core(pairs, count, seeds, rate, bitmask, bins, thresholds, d_outs, d_counts,
+                                 static_cast<hipStream_t>(stream));
 }
 
 int peat_signature_mixed(const void *golden, int32_t golden_dtype, const void *test, int32_t test_dtype,

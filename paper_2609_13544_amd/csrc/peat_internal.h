@@ -80,6 +80,7 @@ struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
     uint32_t cnt[kCnt];
     uint32_t mism[PEAT_MAX_THRESHOLDS];
     uint32_t hist[kHistSlots];
+    uint32_t flips;                  // bit flips injected in the chunk (fused injection)
 };
 // the chunk pass writes the counts followed by the mismatches as one array
 static_assert(offsetof(ChunkPartial, mism) == offsetof(ChunkPartial, cnt) + kCnt * sizeof(uint32_t),
@@ -93,6 +94,7 @@ struct SigParams {
     const int32_t *chunk_pair;     // chunk -> pair index
     ChunkPartial *partials;        // one per chunk
     peat_signature_t *outs;        // one per pair (device)
+    int64_t *inj_counts;           // flips per pair (device), fused injection only
     int32_t count;                 // pairs
     int32_t lo, hi, nbins;
     int32_t nthr;                  // real thresholds
@@ -184,6 +186,10 @@ struct TopkParams {
 // [range[kind], range[kind + 1]) of the global chunk numbering.
 hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[kKinds + 1], hipStream_t s);
 hipError_t launch_sig_mixed_kind(const SigParams &p, int kind, int64_t nchunks, hipStream_t s);
+// Pass 1 of the same-type kinds with the test tensors' bit flips injected
+// first (inj: one InjDesc per pair, device); the records carry flip counts.
+hipError_t launch_sig_chunks_inject(const SigParams &p, const int64_t range[kKinds + 1], const InjDesc *inj,
+                                    hipStream_t s);
 hipError_t launch_sig_finalize(const SigParams &p, hipStream_t s);
 hipError_t launch_inject(const InjParams &p, int64_t total_segs, hipStream_t s);
 hipError_t launch_inject_sum(const InjParams &p, hipStream_t s);

@@ -49,6 +49,7 @@
 #include <atomic>
 
 #include "elements.h"
+#include "inject_span.h"
 
 namespace peat {
 namespace {
@@ -80,6 +81,8 @@ constexpr int64_t kMinRounds = 8;
 // a lane's 16-bit histogram counters hold a whole run of chunks
 static_assert(kMaxGroup * (int64_t(1) << kMaxChunkLog2) / kBlock < 65536, "histogram counter width");
 constexpr int kHistCols = kBlock / 2;     // histogram words per slot
+// the injection's candidate queues fit in the histogram's LDS
+static_assert(sizeof(uint32_t) * kWaves * kQCap <= sizeof(uint32_t) * kHistSlots * kHistCols, "queue size");
 
 __device__ __forceinline__ uint32_t hist_col(int tid) { return (uint32_t)tid & (kHistCols - 1); }
 __device__ __forceinline__ uint32_t hist_inc(int tid) { return tid < kHistCols ? 1u : 0x10000u; }
@@ -672,10 +675,10 @@ struct ChunkCtx {
 // hold neutral values there.  A run has at most kMaxGroup (2) chunks of at
 // most 2^18 elements, so a lane counts at most 2048 elements per histogram
 // slot.
-template <int DG, int DT, int NT, bool RT>
+template <int DG, int DT, int NT, bool RT, bool INJ>
 __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const SigDesc *__restrict__ descs,
                                            const int32_t *__restrict__ chunk_pair,
-                                           ChunkPartial *__restrict__ partials) {
+                                           ChunkPartial *__restrict__ partials, const InjDesc *__restrict__ inj) {
     using PT = PairTr<DG, DT>;
     constexpr int VEC = PT::VEC;
     constexpr int U = kUnroll<DG, DT>;
@@ -979,6 +982,29 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
         (uint32_t)(nch - c0 < P.chunk_group ? nch - c0 : P.chunk_group));
     int run_first = 0;             // first chunk of the current run
     int64_t run_off = 0;           // its first element in the pair
+    if constexpr (INJ) {
+        // Injection first: the bit flips of every chunk of the block are in
+        // memory (device-scope atomics) before any of their elements is
+        // loaded; the barrier orders them for the whole block.  The per-wave
+        // candidate queues borrow the histogram's LDS, cleared afterwards.
+        uint32_t(*queue)[kQCap] = reinterpret_cast<uint32_t(*)[kQCap]>(sh.hist);
+        for (int i = 0; i < cnt; ++i) {
+            const ChunkCtx x = ctx(pair_of(c0 + i), c0 + i);
+            const InjDesc &d = inj[x.pair];
+            const bool none = !d.all && d.T == 0;
+            const uint32_t f = none ? 0u : dpp_sum_u32(inject_span<true>(d, (uint64_t)x.off, x.len, queue));
+            if (lane == 0) sh.rcnt[wave][0] = f;
+            __syncthreads();
+            if (tid == 0) {
+                uint32_t t = 0;
+                for (int w = 0; w < kWaves; ++w) t += sh.rcnt[w][0];
+                partials[x.gchunk].flips = t;
+            }
+            __syncthreads();
+        }
+        for (int i = tid; i < kHistSlots * kHistCols; i += kBlock) sh.hist[i] = 0;
+        __syncthreads();
+    }
     PairS dcur = pair_of(c0);
     ChunkCtx cur = ctx(dcur, c0);
     for (int i = 0; i < cnt; ++i) {
@@ -1036,10 +1062,13 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
 template <int DG, int DT, int NT, bool RT>
 constexpr int chunk_blocks_per_cu() { return (DG == DT && NT == 2 && !RT) ? 3 : 2; }
 
-template <int DG, int DT, int NT, bool RT>
+// INJ: inject the test tensors' bit flips first (inj[pair], same decisions
+// as the injection kernel) and sign the flipped tensors; the chunk records
+// carry the flip counts.
+template <int DG, int DT, int NT, bool RT, bool INJ>
 __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()))
     sig_chunk(SigParams P, const SigDesc *__restrict__ descs, const int32_t *__restrict__ chunk_pair,
-              ChunkPartial *__restrict__ partials) {
+              ChunkPartial *__restrict__ partials, const InjDesc *__restrict__ inj) {
     __shared__ Shared sh;
     const int tid = threadIdx.x;
     // clear the lane-private histogram counters and build the exponent table:
@@ -1059,13 +1088,13 @@ __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()
         sh.hrow[E] = (uint32_t)(slot * kHistCols);
     }
     __syncthreads();
-    chunk_loop<DG, DT, NT, RT>(P, sh, descs, chunk_pair, partials);
+    chunk_loop<DG, DT, NT, RT, INJ>(P, sh, descs, chunk_pair, partials, inj);
 }
 
 // Blocks of one chunk-pass instantiation that the current device holds at
 // once: its occupancy per compute unit times the compute units, looked up
 // once per device.
-template <int DG, int DT, int NT, bool RT>
+template <int DG, int DT, int NT, bool RT, bool INJ>
 int64_t resident_blocks() {
     constexpr int kDevs = 64;
     static std::atomic<int32_t> cached[kDevs];
@@ -1076,7 +1105,7 @@ int64_t resident_blocks() {
         if (v > 0) return v;
     }
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sig_chunk<DG, DT, NT, RT>, kBlock, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sig_chunk<DG, DT, NT, RT, INJ>, kBlock, 0) != hipSuccess ||
         per_cu < 1)
         per_cu = 1;
     if (dev < 0 || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
@@ -1088,24 +1117,25 @@ int64_t resident_blocks() {
 }
 
 
-template <int DG, int DT, int NT, bool RT>
-void launch_chunks(const SigParams &p, int64_t n, hipStream_t s) {
-    const int64_t r = resident_blocks<DG, DT, NT, RT>();
+template <int DG, int DT, int NT, bool RT, bool INJ>
+void launch_chunks(const SigParams &p, int64_t n, const InjDesc *inj, hipStream_t s) {
+    const int64_t r = resident_blocks<DG, DT, NT, RT, INJ>();
     int64_t k = n / (kMinRounds * r);
     k = k < 1 ? 1 : (k > kMaxGroup ? kMaxGroup : k);
     SigParams q = p;
     q.chunk_count = n;
     q.chunk_group = k;
-    hipLaunchKernelGGL((sig_chunk<DG, DT, NT, RT>), dim3((unsigned)((n + k - 1) / k)), dim3(kBlock), 0, s, q,
-                       static_cast<const SigDesc *>(p.descs), static_cast<const int32_t *>(p.chunk_pair), p.partials);
+    hipLaunchKernelGGL((sig_chunk<DG, DT, NT, RT, INJ>), dim3((unsigned)((n + k - 1) / k)), dim3(kBlock), 0, s, q,
+                       static_cast<const SigDesc *>(p.descs), static_cast<const int32_t *>(p.chunk_pair), p.partials,
+                       inj);
 }
 
-template <int DG, int DT, bool RT>
-hipError_t launch_kind_rt(const SigParams &p, int64_t n, hipStream_t s) {
+template <int DG, int DT, bool RT, bool INJ>
+hipError_t launch_kind_rt(const SigParams &p, int64_t n, const InjDesc *inj, hipStream_t s) {
     switch (p.nthr_pad) {
-        case 2: launch_chunks<DG, DT, 2, RT>(p, n, s); break;
-        case 4: launch_chunks<DG, DT, 4, RT>(p, n, s); break;
-        default: launch_chunks<DG, DT, 8, RT>(p, n, s); break;
+        case 2: launch_chunks<DG, DT, 2, RT, INJ>(p, n, inj, s); break;
+        case 4: launch_chunks<DG, DT, 4, RT, INJ>(p, n, inj, s); break;
+        default: launch_chunks<DG, DT, 8, RT, INJ>(p, n, inj, s); break;
     }
     return hipGetLastError();
 }
@@ -1113,7 +1143,15 @@ hipError_t launch_kind_rt(const SigParams &p, int64_t n, hipStream_t s) {
 // Pass 1 over n chunks of one kind, starting at p.chunk_base.
 template <int DG, int DT>
 hipError_t launch_kind(const SigParams &p, int64_t n, hipStream_t s) {
-    return p.any_rtol ? launch_kind_rt<DG, DT, true>(p, n, s) : launch_kind_rt<DG, DT, false>(p, n, s);
+    return p.any_rtol ? launch_kind_rt<DG, DT, true, false>(p, n, nullptr, s)
+                      : launch_kind_rt<DG, DT, false, false>(p, n, nullptr, s);
+}
+
+// Pass 1 with the injection of the test tensors (same-type kinds).
+template <int DT>
+hipError_t launch_kind_inject(const SigParams &p, int64_t n, const InjDesc *inj, hipStream_t s) {
+    return p.any_rtol ? launch_kind_rt<DT, DT, true, true>(p, n, inj, s)
+                      : launch_kind_rt<DT, DT, false, true>(p, n, inj, s);
 }
 
 }  // namespace

@@ -18,12 +18,13 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     __shared__ uint64_t su[kWaves][2 + kCnt + PEAT_MAX_THRESHOLDS];
     __shared__ uint64_t sh_hist[kHistSlots];
     __shared__ uint64_t sh_hwave[kWaves][kHistSlots];
+    __shared__ uint64_t su_flips[kWaves];
 
     // binary64 sums: each thread a fixed strided subset in order, then a fixed tree
     double s[6] = {0, 0, 0, 0, 0, 0};
     double ma = -1.0, mr = -1.0;
     int64_t ia = -1, ir = -1, iu = -1, fn = -1, fv = -1;
-    uint64_t mu = 0, sulp = 0;
+    uint64_t mu = 0, sulp = 0, flips = 0;
     uint64_t cn[kCnt + PEAT_MAX_THRESHOLDS];
 #pragma unroll
     for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] = 0;
@@ -42,6 +43,7 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         if (p.first_nan >= 0 && (fn < 0 || p.first_nan < fn)) fn = p.first_nan;
         if (p.first_valid >= 0 && (fv < 0 || p.first_valid < fv)) fv = p.first_valid;
         sulp += p.sum_ulp;
+        if (P.inj_counts) flips += p.flips;
 #pragma unroll
         for (int k = 0; k < kCnt; ++k) cn[k] += p.cnt[k];
 #pragma unroll
@@ -94,6 +96,10 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         if (ofv >= 0 && (fv < 0 || ofv < fv)) fv = ofv;
     }
     sulp = wsum_u64(sulp);
+    if (P.inj_counts) {
+        flips = wsum_u64(flips);
+        if (lane == 0) su_flips[wave] = flips;
+    }
 #pragma unroll
     for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) cn[k] = wsum_u64(cn[k]);
     if (lane == 0) {
@@ -107,6 +113,11 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     }
     __syncthreads();
     if (tid != 0) return;
+    if (P.inj_counts) {
+        uint64_t f = 0;
+        for (int w = 0; w < kWaves; ++w) f += su_flips[w];
+        P.inj_counts[pair] = (int64_t)f;
+    }
     double S[6] = {0, 0, 0, 0, 0, 0};
     double MA = -1.0, MR = -1.0;
     int64_t IA = -1, IR = -1, IU = -1, FN = -1;
@@ -172,6 +183,24 @@ hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[kKinds + 1]
             case 1: e = launch_kind<PEAT_F16, PEAT_F16>(q, n, s); break;
             case 2: e = launch_kind<PEAT_BF16, PEAT_BF16>(q, n, s); break;
             default: e = launch_sig_mixed_kind(q, kind, n, s); break;
+        }
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_sig_chunks_inject(const SigParams &p, const int64_t range[kKinds + 1], const InjDesc *inj,
+                                    hipStream_t s) {
+    for (int kind = 0; kind < kSameKinds; ++kind) {
+        const int64_t n = range[kind + 1] - range[kind];
+        if (n <= 0) continue;
+        SigParams q = p;
+        q.chunk_base = range[kind];
+        hipError_t e;
+        switch (kind) {
+            case 0: e = launch_kind_inject<PEAT_F32>(q, n, inj, s); break;
+            case 1: e = launch_kind_inject<PEAT_F16>(q, n, inj, s); break;
+            default: e = launch_kind_inject<PEAT_BF16>(q, n, inj, s); break;
         }
         if (e != hipSuccess) return e;
     }

@@ -53,7 +53,7 @@ def test_struct_layouts():
 
 def test_abi_version_and_strerror():
     L = P.lib()
-    assert L.peat_abi_version() == 4
+    assert L.peat_abi_version() == 5
     for code in range(0, -8, -1):
         assert L.peat_strerror(code)
     assert L.peat_strerror(-99) == b"unknown error code"
@@ -230,3 +230,37 @@ def test_no_device_is_an_error_not_a_crash():
     rc = _sig_rc(n=0)
     assert rc in (B.EHIP, B.ENODEV)
     assert P.lib().peat_init() in (B.EHIP, B.ENODEV)
+
+
+def test_inject_signature_validation_codes():
+    """The fused injection + signature call: rate, bitmask and seeds are
+    checked, and test tensors may not overlap another tensor of the batch;
+    all before any device access (the pointers below are never touched)."""
+    L = P.lib()
+    b = B.Bins(-40, 24, 64, 0)
+    th = B.Thresholds()
+    th.count = 1
+    th.abs_tol[0] = 1e-6
+    seeds = (ctypes.c_uint64 * 3)(1, 2, 3)
+
+    def rc(pairs, rate=1e-6, mask=0x7F800000, sd=seeds, outs=None):
+        arr = (B.Pair * max(1, len(pairs)))(*[B.Pair(g, t, n, dt, 0) for g, t, n, dt in pairs])
+        return L.peat_inject_signature_batched_async(arr, len(pairs), sd, rate, mask, ctypes.byref(b),
+                                                     ctypes.byref(th), outs, outs, None)
+
+    A = 1 << 40                                  # fake, aligned device addresses
+    assert L.peat_inject_signature_batched_async(None, 0, None, 1e-6, 1, ctypes.byref(b), ctypes.byref(th),
+                                                 None, None, None) == B.OK
+    ok_pairs = [(A, A + 4096, 1000, 0), (A, A + 8192, 1000, 0)]      # shared golden, distinct tests
+    assert rc(ok_pairs) == B.EINVAL and b"d_outs" in L.peat_last_error()
+    assert rc(ok_pairs, rate=math.nan) == B.ERATE
+    assert rc(ok_pairs, rate=-1.0) == B.ERATE
+    assert rc(ok_pairs, mask=0) == B.EBITMASK
+    assert rc([(A, A + 4096, 1000, 1)], mask=1 << 16) == B.EBITMASK    # beyond binary16
+    assert rc(ok_pairs, sd=None) == B.EINVAL and b"seeds" in L.peat_last_error()
+    assert rc([(A, A, 1000, 0)]) == B.EINVAL and b"overlaps" in L.peat_last_error()
+    assert rc([(A, A + 4096, 1000, 0), (A + 16384, A + 4096 + 3996, 10, 0)]) == B.EINVAL   # two tests
+    assert rc([(A, A + 4096, 1000, 0), (A + 4100, A + 65536, 10, 0)]) == B.EINVAL          # golden in a test
+    assert rc([(A, A + 3996, 1000, 0)]) == B.EINVAL and b"overlaps" in L.peat_last_error()  # own golden
+    # adjacent tensors and empty pairs do not overlap
+    assert rc([(A, A + 4000, 1000, 0), (A + 8192, A + 4000, 0, 0)]) == B.EINVAL and b"d_outs" in L.peat_last_error()
