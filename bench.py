@@ -2,18 +2,23 @@
 """Throughput of the error-signature hot path on one MI355X.
 
 One step is one pass of the whole hot path over one batch of synthetic input
-resident in HBM: the batched bit-flip injection into every test tensor (fresh
-seeds each step), then the batched error signature of every (golden, test)
-pair.  The default workload is the Llama-7B-shaped checkpoint pair (weights
-plus both Adam moments: 873 f32 tensors, 20,215,246,848 elements per side,
-161.72 GB signed per step).
+resident in HBM: the bit-flip injection into every test tensor (fresh seeds
+each step) and the error signature of every (golden, test) pair.  Where every
+test tensor is injected with one rate and mask (the default workload) the
+step is one call, peat_inject_signature_batched_async, which injects each
+chunk and then signs it in the same kernel; the same step as two calls
+(injection, then signature) is timed after it for reference (--separate makes
+the two calls the timed step).  The default workload is the Llama-7B-shaped
+checkpoint pair (weights plus both Adam moments: 873 f32 tensors,
+20,215,246,848 elements per side, 161.72 GB signed per step).
 
 Prints ONE JSON line on stdout (everything else goes to stderr):
   value     golden+test bytes signed per second over the timed steps (GB/s)
-  roofline  the dominant kernel (signature chunk pass): algorithmic bytes per
-            launch / its average launch duration from HIP events on its stream,
-            against the 8 TB/s HBM peak; traffic from the committed rocprofv3
-            counter summary when it was taken on the current kernel source
+  roofline  the dominant kernel (the chunk pass, with the injection when the
+            step is fused): algorithmic bytes per launch / its average launch
+            duration from HIP events on its stream, against the 8 TB/s HBM
+            peak; traffic from the committed rocprofv3 counter summary when it
+            was taken on the current kernel source
   cpu_baseline  the CPU oracle on a bounded sample of the same workload
 
 Also reported: the read ceiling of the same box (peat_stream_read over a
@@ -46,7 +51,8 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "GB/s of golden+test tensor bytes signed (fraction of HBM peak), 1 MI355X"
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_13544_amd", "csrc", f)
-                  for f in ("sig_chunk.h", "signature.hip", "elements.h", "peat_internal.h")]
+                  for f in ("sig_chunk.h", "signature.hip", "elements.h", "peat_internal.h", "inject_span.h",
+                            "philox.h")]
 
 
 def log(*a):
@@ -66,10 +72,12 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def committed_traffic(workload: str):
-    """HBM bytes per sig_chunk launch from profiles/, or None when the counters
-    were taken on a different kernel source."""
-    path = os.path.join(PROFILES, f"sig_chunk_{workload}_hbm_traffic.md")
+def committed_traffic(workload: str, fused: bool = False):
+    """HBM bytes per launch of the chunk pass (with the injection when fused)
+    from profiles/, or None when the counters were taken on a different
+    kernel source."""
+    kernel = "sig_chunk_inject" if fused else "sig_chunk"
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_hbm_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -95,6 +103,13 @@ class Workload:
 
     def inject_items(self, step: int):
         return [(T, (seed + (step << 40)) & (2 ** 64 - 1), rate, mask) for T, seed, rate, mask in self.items]
+
+    def fusable(self) -> bool:
+        """Every pair's test tensor is injected, in pair order, with one rate
+        and mask: the step can be the fused injection + signature call."""
+        return (len(self.items) == len(self.pairs) > 0
+                and all(T is t for (T, *_), (_, t) in zip(self.items, self.pairs))
+                and len({(r, m) for _, _, r, m in self.items}) == 1)
 
     def bytes_signed(self) -> int:
         return sum(G.numel() * G.element_size() * 2 for G, _ in self.pairs)
@@ -176,20 +191,27 @@ WORKLOADS = {"5": Llama7B, "3": GPT13B, "2": Activations, "4": Replay, "1": Sing
 # ---------------------------------------------------------------------------
 def cpu_baseline(wl: Workload, max_threads: int):
     """The oracle, as it stands, on the workload's sampled pairs: host copies
-    of the device bytes, one oracle call per pair on a thread pool (ctypes
-    releases the GIL).  Returns GB/s of golden+test bytes signed."""
+    of the device bytes, one step per pair (the oracle's injection of the
+    test tensor when the workload injects it, then its signature) on a thread
+    pool (ctypes releases the GIL).  Returns GB/s of golden+test bytes signed."""
     import numpy as np
     import oracle
     from tests.parity import to_host_bits
 
+    inj = {id(T): (seed, rate, mask) for T, seed, rate, mask in wl.inject_items(0)}
     host = []
     t0 = time.time()
     for k in wl.sample:
         G, T = wl.pairs[k]
         code = {wl.torch.float32: 0, wl.torch.float16: 1, wl.torch.bfloat16: 2}[G.dtype]
-        host.append((to_host_bits(G), to_host_bits(T), code))
+        host.append((to_host_bits(G), to_host_bits(T), code, inj.get(id(T))))
     copy_s = time.time() - t0
-    nbytes = sum(g.nbytes + t.nbytes for g, t, _ in host)
+    nbytes = sum(g.nbytes + t.nbytes for g, t, _, _ in host)
+
+    def one(g, t, code, spec):
+        if spec is not None:
+            oracle.inject(t, dtype=code, seed=spec[0], rate=spec[1], mask=spec[2])
+        oracle.signature(g, t, dtype=code)
     threads = max(1, min(max_threads, len(host), os.cpu_count() or 1))
     work = list(range(len(host)))
     lock = threading.Lock()
@@ -200,13 +222,12 @@ def cpu_baseline(wl: Workload, max_threads: int):
                 if not work:
                     return
                 k = work.pop(0)
-            g, t, code = host[k]
-            oracle.signature(g, t, dtype=code)
+            one(*host[k])
 
     # one core, one pair: per-core rate of the oracle
-    g1, t1, c1 = host[0]
+    g1, t1, c1, s1 = host[0]
     t0 = time.time()
-    oracle.signature(g1, t1, dtype=c1)
+    one(g1, t1.copy(), c1, s1)
     per_core = (g1.nbytes + t1.nbytes) / (time.time() - t0) / 1e9
 
     t0 = time.time()
@@ -220,8 +241,9 @@ def cpu_baseline(wl: Workload, max_threads: int):
     return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "per_core_value": round(per_core, 3),
             "sample": f"{len(host)} of {len(wl.pairs)} pairs ({nbytes / 1e9:.2f} GB: "
-                      f"{', '.join(str(k) for k in wl.sample)}), oracle {dt:.1f} s wall on {threads} threads, "
-                      f"D2H copy {copy_s:.1f} s not counted"}
+                      f"{', '.join(str(k) for k in wl.sample)}), oracle "
+                      f"{'injection + ' if any(h[3] for h in host) else ''}signature, {dt:.1f} s wall on "
+                      f"{threads} threads, D2H copy {copy_s:.1f} s not counted"}
 
 
 def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
@@ -369,6 +391,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="5", choices=sorted(WORKLOADS))
+    ap.add_argument("--separate", action="store_true",
+                    help="time the step as two calls (injection, then signature) instead of the fused pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="GIB")
@@ -407,44 +431,72 @@ def main():
     prep_pairs = P.PreparedPairs(wl.pairs)
     d_out = torch.empty(len(wl.pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
     d_counts = torch.empty(max(1, len(wl.items)), dtype=torch.int64, device="cuda")
-    prepared_items = [P.PreparedItems(wl.inject_items(s)) for s in range(args.warmup + args.steps)]
+    nsteps_all = args.warmup + args.steps
+    fused = wl.fusable() and not args.separate
+    step_items = [wl.inject_items(s) for s in range(2 * nsteps_all if fused else nsteps_all)]
+    prepared_items = [P.PreparedItems(it) for it in step_items]
 
-    def step(s):
+    def step_separate(s):
         if wl.items:
             P.inject_batched_async(prepared_items[s], d_counts, stream=stream)
         P.signature_batched_async(prep_pairs, d_out, synth.BINS, synth.THRESHOLDS, stream=stream)
 
-    for s in range(args.warmup):
-        step(s)
-    torch.cuda.synchronize()
-    P.profile_enable(True)
-    for k in (P.K_SIG_CHUNK, P.K_SIG_FINALIZE, P.K_INJECT, P.K_INJECT_SUM):
-        P.profile_read(k)
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    evs[0].record(stream)
-    for j, s in enumerate(range(args.warmup, args.warmup + args.steps)):
-        step(s)
-        evs[j + 1].record(stream)
-    torch.cuda.synchronize()
-    ms_total = evs[0].elapsed_time(evs[-1])
-    step_ms = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps))
-    P.profile_enable(False)
-    chunk_ms, chunk_n = P.profile_read(P.K_SIG_CHUNK)
-    fin_ms, fin_n = P.profile_read(P.K_SIG_FINALIZE)
-    inj_ms, inj_n = P.profile_read(P.K_INJECT)
-    isum_ms, isum_n = P.profile_read(P.K_INJECT_SUM)
+    def step_fused(s):
+        _, _, rate, mask = step_items[s][0]
+        P.inject_signature_batched_async(prep_pairs, [seed for _, seed, _, _ in step_items[s]], rate, mask,
+                                         d_out, d_counts, synth.BINS, synth.THRESHOLDS, stream=stream)
 
+    classes = (P.K_SIG_CHUNK, P.K_SIG_FINALIZE, P.K_INJECT, P.K_INJECT_SUM, P.K_SIG_INJECT)
+
+    def timed(step, first):
+        """warm-up and timed steps first, first + 1, ...: total ms, sorted step
+        times, per-class (ms per launch, launches)"""
+        for s in range(first, first + args.warmup):
+            step(s)
+        torch.cuda.synchronize()
+        P.profile_enable(True)
+        for k in classes:
+            P.profile_read(k)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        torch.cuda.synchronize()
+        evs[0].record(stream)
+        for j, s in enumerate(range(first + args.warmup, first + nsteps_all)):
+            step(s)
+            evs[j + 1].record(stream)
+        torch.cuda.synchronize()
+        total = evs[0].elapsed_time(evs[-1])
+        steps = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps))
+        P.profile_enable(False)
+        per = {}
+        for k in classes:
+            ms, n = P.profile_read(k)
+            per[k] = (ms / max(1, n), n)
+        return total, steps, per
+
+    ms_total, step_ms, per = timed(step_fused if fused else step_separate, 0)
     ms_step = ms_total / args.steps
     nbytes = wl.bytes_signed()
     value = nbytes / (ms_step / 1e3) / 1e9
-    chunk_avg = chunk_ms / max(1, chunk_n)
-    achieved = nbytes / (chunk_avg / 1e3) / 1e9
     recs = P.decode_records(d_out, len(wl.pairs), nthr=len(synth.THRESHOLDS))
     flips = int(d_counts.sum().item()) if wl.items else 0
-    log(f"step {ms_step:.3f} ms: chunk {chunk_avg:.3f} ms, finalize {fin_ms / max(1, fin_n):.3f} ms, "
-        f"inject {inj_ms / max(1, inj_n):.3f} ms + {isum_ms / max(1, isum_n):.3f} ms; "
-        f"last step {flips} flips, {sum(r['n_nan_pairs'] for r in recs)} NaN pairs")
+    if fused:
+        # the same injections done by the two separate calls, for reference
+        # (fresh seeds: steps nsteps_all ... 2 nsteps_all - 1)
+        sep_total, _, sep_per = timed(step_separate, nsteps_all)
+        chunk_avg = per[P.K_SIG_INJECT][0]
+        sig_chunk_avg, inj_avg, isum_avg = sep_per[P.K_SIG_CHUNK][0], sep_per[P.K_INJECT][0], sep_per[P.K_INJECT_SUM][0]
+        fin_avg = per[P.K_SIG_FINALIZE][0]
+        dominant = "sig_chunk with injection (peat_inject_signature_batched_async)"
+    else:
+        chunk_avg = sig_chunk_avg = per[P.K_SIG_CHUNK][0]
+        inj_avg, isum_avg, fin_avg = per[P.K_INJECT][0], per[P.K_INJECT_SUM][0], per[P.K_SIG_FINALIZE][0]
+        dominant = "sig_chunk"
+    achieved = nbytes / (chunk_avg / 1e3) / 1e9
+    log(f"step {ms_step:.3f} ms ({'fused' if fused else 'separate'}): chunk pass {chunk_avg:.3f} ms, "
+        f"finalize {fin_avg:.3f} ms; last step {flips} flips, {sum(r['n_nan_pairs'] for r in recs)} NaN pairs")
+    if fused:
+        log(f"separate calls: step {sep_total / args.steps:.3f} ms = injection {inj_avg:.3f} + {isum_avg:.3f} ms "
+            f"+ signature chunk pass {sig_chunk_avg:.3f} ms")
 
     out = {
         "metric": METRIC,
@@ -462,20 +514,28 @@ def main():
         "config": {"workload": wl.name, "description": wl.description, "pairs": len(wl.pairs),
                    "elements_per_side": wl.elements(), "bytes_signed_per_step": nbytes,
                    "bins": list(synth.BINS), "thresholds": list(synth.THRESHOLDS),
-                   "step": "batched injection + batched signature" if wl.items else "batched signature"},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": committed_traffic(wl.name)},
-        "kernels_ms_per_step": {"sig_chunk": round(chunk_avg, 4),
-                                "sig_finalize": round(fin_ms / max(1, fin_n), 4),
-                                "inject": round(inj_ms / max(1, inj_n), 4) if inj_n else 0.0,
-                                "inject_sum": round(isum_ms / max(1, isum_n), 4) if isum_n else 0.0},
+                   "step": ("bit-flip injection + signature of every pair in one pass "
+                            "(peat_inject_signature_batched_async)") if fused else
+                           ("batched injection + batched signature" if wl.items else "batched signature")},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": committed_traffic(wl.name, fused)},
+        "kernels_ms_per_step": ({"sig_chunk_inject": round(chunk_avg, 4)} if fused else {}) | {
+                                "sig_chunk": round(sig_chunk_avg, 4),
+                                "sig_finalize": round(fin_avg, 4),
+                                "inject": round(inj_avg, 4) if wl.items else 0.0,
+                                "inject_sum": round(isum_avg, 4) if wl.items else 0.0},
         "step_ms": {"median": round(step_ms[len(step_ms) // 2], 4), "min": round(step_ms[0], 4),
                     "max": round(step_ms[-1], 4)},
-        "signature_only_GBps": round(nbytes / ((chunk_avg + fin_ms / max(1, fin_n)) / 1e3) / 1e9, 1),
-        "inject_Gelem_per_s": round(sum(T.numel() for T, *_ in wl.items) / (inj_ms / max(1, inj_n) / 1e3) / 1e9, 1)
-        if inj_n else None,
+        "signature_only_GBps": round(nbytes / ((sig_chunk_avg + fin_avg) / 1e3) / 1e9, 1),
+        "inject_Gelem_per_s": round(sum(T.numel() for T, *_ in wl.items) / (inj_avg / 1e3) / 1e9, 1)
+        if wl.items else None,
     }
+    if fused:
+        out["separate_calls"] = {"ms_per_step": round(sep_total / args.steps, 4),
+                                 "GBps": round(nbytes / (sep_total / args.steps / 1e3) / 1e9, 1),
+                                 "what": "the same step as peat_inject_batched_async + "
+                                         "peat_signature_batched_async (the kernel times above)"}
     if not args.no_topk:
         log("top-10% mean ...")
         out["topk_mean"] = topk_measure(torch, P, prep_pairs, nbytes)
@@ -483,7 +543,8 @@ def main():
         log("read ceiling ...")
         del prepared_items
         rc = read_ceiling(torch, P, stream)
-        rc["sig_chunk_frac_of_ceiling"] = round(achieved / rc["GBps"], 4)
+        rc["chunk_pass_frac_of_ceiling"] = round(achieved / rc["GBps"], 4)
+        rc["sig_chunk_frac_of_ceiling"] = round(nbytes / (sig_chunk_avg / 1e3) / 1e9 / rc["GBps"], 4)
         out["read_ceiling"] = rc
     if not args.no_cpu_baseline:
         log("cpu baseline ...")
