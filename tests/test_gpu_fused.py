@@ -138,3 +138,33 @@ def test_fused_llama_tensors_full_size():
     assert oracle.inject(host, dtype=0, seed=seeds[2], rate=rate, mask=mask) == counts[2]
     assert np.array_equal(to_host_bits(pairs_a[2][1]), host)
     assert_parity(recs[2], oracle_sig(gb, host, 0, synth.BINS, synth.THRESHOLDS), "attention-shaped tensor")
+
+
+THR_SETS = [(), (0.0,), (1e-7, 1e-5, 1e-3, 0.1), (0.0, 1e-9, 1e-6, 1e-4, 1e-2, 1.0, 100.0, float("inf")),
+            ((1e-6, 1e-3), (0.0, 1e-5)), ((0.0, float("inf")), (1e-3, 0.1), (1e-9, 2.0 ** -11), (0.0, 0.0))]
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_fused_threshold_and_bin_variants(code):
+    """Every instantiation of the fused pass (2, 4 or 8 compared thresholds,
+    absolute or torch.isclose-style relative tolerances) and other bin
+    layouts, against the oracle's injection followed by its signature."""
+    bins_sets = [synth.BINS, (-30, 20, 25), (-160, 136, 37)]
+    for i, thr in enumerate(THR_SETS):
+        bins = bins_sets[i % len(bins_sets)]
+        n = [70001, 4096 * 3 + 17, 250000][i % 3]
+        gb, tb = special_pair(n, code, seed=4400 + 10 * i + code)
+        seed = synth.inject_seed(13, 7 * i + code)
+        rate, mask = [1e-3, 2e-2][i % 2], MASKS[code][i % len(MASKS[code])]
+        g, t = to_device(gb, code), to_device(tb, code)
+        log(f"  dtype={code} n={n} thresholds={thr} bins={bins}")
+        d_out = torch.empty(P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+        d_counts = torch.empty(1, dtype=torch.int64, device="cuda")
+        P.inject_signature_batched_async([(g, t)], [seed], rate, mask, d_out, d_counts, bins, thr)
+        torch.cuda.synchronize()
+        nthr = len(thr)
+        rec = P.decode_records(d_out, 1, nthr=nthr)[0]
+        host = tb.copy()
+        assert int(d_counts.item()) == oracle.inject(host, dtype=code, seed=seed, rate=rate, mask=mask)
+        assert np.array_equal(to_host_bits(t), host)
+        assert_parity(rec, oracle_sig(gb, host, code, bins, thr), f"thresholds={thr}")
