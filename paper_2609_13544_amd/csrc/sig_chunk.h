@@ -523,19 +523,7 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
     return false;
 }
 
-// ---- wave reductions of the finalize pass (fixed butterfly order) ----------
-__device__ __forceinline__ double wsum(double v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-__device__ __forceinline__ uint64_t wsum_u64(uint64_t v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-
-// ---- wave reductions by DPP (chunk records) ---------------------------------
+// ---- wave reductions by DPP (chunk records, finalize) ------------------------
 // The classic six-step pattern: pairs and quads (quad_perm), half rows and
 // rows (mirrors), then rows 1 and 3 take the last lane of rows 0 and 2
 // (row_bcast:15) and rows 2 and 3 the last lane of row 1 (row_bcast:31), so

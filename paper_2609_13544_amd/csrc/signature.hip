@@ -50,20 +50,22 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) cn[kCnt + j] += p.mism[j];
     }
     // histogram: wave w sums chunks w, w + 4, ... (lane l: slots l and 64 + l),
-    // eight chunks' loads in flight per step; the waves are added in order
+    // 32 chunks' loads in flight per step (a single pair's records are read
+    // in few round trips); the waves are added in order
     {
+        constexpr int D = 32;
         uint64_t h0 = 0, h1 = 0;
         const bool two = lane < kHistSlots - 64;
         int c = wave;
-        for (; c + 7 * kWaves < m; c += 8 * kWaves) {
-            uint32_t a[8], b[8];
+        for (; c + (D - 1) * kWaves < m; c += D * kWaves) {
+            uint32_t a[D], b[D];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < D; ++u) {
                 a[u] = parts[c + u * kWaves].hist[lane];
                 b[u] = two ? parts[c + u * kWaves].hist[64 + lane] : 0u;
             }
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < D; ++u) {
                 h0 += a[u];
                 h1 += b[u];
             }
@@ -82,7 +84,7 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         sh_hist[tid] = h;
     }
 #pragma unroll
-    for (int k = 0; k < 6; ++k) s[k] = wsum(s[k]);
+    for (int k = 0; k < 6; ++k) s[k] = dpp_sum(s[k]);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
         const double ova = __shfl_xor(ma, o), ovr = __shfl_xor(mr, o);
@@ -95,13 +97,15 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         if (ofn >= 0 && (fn < 0 || ofn < fn)) fn = ofn;
         if (ofv >= 0 && (fv < 0 || ofv < fv)) fv = ofv;
     }
-    sulp = wsum_u64(sulp);
+    // integer totals by DPP in binary64, exact: a count is at most 2^46, and
+    // the ULP sum goes as two halves of 32 bits (each wave total below 2^52)
+    sulp = ((uint64_t)dpp_sum((double)(sulp >> 32)) << 32) + (uint64_t)dpp_sum((double)(sulp & 0xFFFFFFFFu));
     if (P.inj_counts) {
-        flips = wsum_u64(flips);
+        flips = (uint64_t)dpp_sum((double)flips);
         if (lane == 0) su_flips[wave] = flips;
     }
 #pragma unroll
-    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) cn[k] = wsum_u64(cn[k]);
+    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) cn[k] = (uint64_t)dpp_sum((double)cn[k]);
     if (lane == 0) {
         for (int k = 0; k < 6; ++k) sd[wave][k] = s[k];
         sd[wave][6] = ma;
