@@ -168,3 +168,32 @@ def test_fused_threshold_and_bin_variants(code):
         assert int(d_counts.item()) == oracle.inject(host, dtype=code, seed=seed, rate=rate, mask=mask)
         assert np.array_equal(to_host_bits(t), host)
         assert_parity(rec, oracle_sig(gb, host, code, bins, thr), f"thresholds={thr}")
+
+
+def test_fused_empty_pairs_shared_golden_and_repeat():
+    """Empty pairs in the batch (zero records, zero counts), two pairs sharing
+    one golden tensor (allowed: only test tensors are written), and the same
+    call twice with the same seeds (the flips undo themselves: the tensors
+    come back to their first state, and the second records are those of the
+    original tests)."""
+    code = 0
+    gb, tb = special_pair(40000, code, seed=31)
+    _, tb2 = special_pair(40000, code, seed=32)
+    g = to_device(gb, code)
+    t1, t2 = to_device(tb, code), to_device(tb2, code)
+    empty = torch.empty(0, dtype=torch.float32, device="cuda")
+    pairs = [(g, t1), (empty, torch.empty(0, dtype=torch.float32, device="cuda")), (g, t2)]
+    seeds = [synth.inject_seed(14, 1), synth.inject_seed(14, 2), synth.inject_seed(14, 3)]
+    rate, mask = 2e-3, 0xFFFFFFFF
+    recs, counts = _fused(pairs, seeds, rate, mask)
+    h1, h2 = tb.copy(), tb2.copy()
+    assert counts[0] == oracle.inject(h1, dtype=code, seed=seeds[0], rate=rate, mask=mask)
+    assert counts[2] == oracle.inject(h2, dtype=code, seed=seeds[2], rate=rate, mask=mask)
+    assert counts[1] == 0 and recs[1]["n"] == 0 and recs[1]["n_valid"] == 0
+    assert_parity(recs[0], oracle_sig(gb, h1, code, synth.BINS, synth.THRESHOLDS), "pair 0")
+    assert_parity(recs[2], oracle_sig(gb, h2, code, synth.BINS, synth.THRESHOLDS), "pair 2")
+    assert np.array_equal(to_host_bits(g), gb)
+    recs2, counts2 = _fused(pairs, seeds, rate, mask)
+    assert counts2 == counts
+    assert np.array_equal(to_host_bits(t1), tb) and np.array_equal(to_host_bits(t2), tb2)
+    assert_parity(recs2[0], oracle_sig(gb, tb, code, synth.BINS, synth.THRESHOLDS), "pair 0, second call")
