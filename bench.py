@@ -261,10 +261,32 @@ def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
         b, nb = P.profile_read(P.K_TOPK_B)
         ms = a / max(1, na) + b / max(1, nb)
         best = ms if best is None else min(best, ms)
+    # the same score when the step's signatures are at hand (default bins,
+    # one binade each): the first streaming pass is skipped where their
+    # histograms fix the k-th largest error's binade
+    d_sig = torch.empty(prep_pairs.count * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    P.signature_batched_async(prep_pairs, d_sig)
+    torch.cuda.synchronize()
+    sigs = P.decode_records(d_sig, prep_pairs.count)
+    P.topk_mean_from_signature_batched(prep_pairs, sigs)         # warm-up
+    P.profile_read(P.K_TOPK_A)
+    P.profile_read(P.K_TOPK_B)
+    best_s = None
+    for _ in range(reps):
+        recs_s = P.topk_mean_from_signature_batched(prep_pairs, sigs)
+        a, na = P.profile_read(P.K_TOPK_A)
+        b, nb = P.profile_read(P.K_TOPK_B)
+        ms = a / max(1, na) + b / max(1, nb)
+        best_s = ms if best_s is None else min(best_s, ms)
     P.profile_enable(False)
+    same = all(x[f] == y[f] or (x[f] != x[f] and y[f] != y[f]) for x, y in zip(recs, recs_s) for f in x)
     return {"ms": round(best, 3), "GBps_of_bytes_signed": round(nbytes / (best / 1e3) / 1e9, 1),
             "passes": 3, "pairs": len(recs), "k_total": int(sum(r["k"] for r in recs)),
-            "what": "peat_topk_mean_batched, num/den = 1/10, kernel time (excludes the host wait between passes 2 and 3)"}
+            "what": "peat_topk_mean_batched, num/den = 1/10, kernel time (excludes the host wait between passes 2 and 3)",
+            "from_signature": {"ms": round(best_s, 3), "GBps_of_bytes_signed": round(nbytes / (best_s / 1e3) / 1e9, 1),
+                               "records_equal": bool(same),
+                               "what": "peat_topk_mean_from_signature_batched with the pairs' signatures (bins "
+                                       "-40..24, one binade each), kernel time"}}
 
 
 def mixed_measure(torch, P, reps: int = 5, count: int = 64, shape=(4096, 4096)):

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PEAT_ABI_VERSION 5
+#define PEAT_ABI_VERSION 6
 #define PEAT_MAX_THRESHOLDS 8
 #define PEAT_MAX_BINS 64
 
@@ -280,6 +280,20 @@ int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
  * peat_mixed_pair_t; the error is |T - G| of the exact binary64 values). */
 int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
                                  int32_t den, peat_topk_t *outs);
+
+/* peat_topk_mean_batched for pairs whose error signatures the caller already
+ * holds: sigs is a host array of count records that peat_signature_batched
+ * (or its async form) wrote for the same pairs with these bins; thresholds do
+ * not matter.  The histogram counts the same errors of the same valid pairs,
+ * so with one-binade bins (hi_log2 - lo_log2 == nbins) it fixes the binade of
+ * the k-th largest error whenever that falls in a regular bin, and the first
+ * of the three streaming passes skips the pair.  Other pairs, and other bins,
+ * take all three.  outs are bit-identical to peat_topk_mean_batched's.
+ * PEAT_EINVAL when a record's n differs from its pair's or its histogram
+ * total from its n_valid.  (Section IV-B.3; Section V-D histograms.) */
+int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
+                                          int32_t den, const peat_signature_t *sigs,
+                                          const peat_bins_t *bins, peat_topk_t *outs);
 
 /* Random bit flip in place (Section II-B).  The draws come from
  * Philox4x32-10 keyed by (lo32(seed), hi32(seed)); "block c of stream s" is

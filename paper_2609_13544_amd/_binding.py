@@ -162,6 +162,9 @@ _PROTOS = {
                                                           ctypes.c_void_p, ctypes.c_void_p]),
     "peat_topk_mean_mixed_batched": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32, ctypes.c_int32,
                                                     ctypes.c_int32, ctypes.POINTER(TopK)]),
+    "peat_topk_mean_from_signature_batched": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32, ctypes.c_int32,
+                                                             ctypes.c_int32, ctypes.POINTER(Signature),
+                                                             ctypes.POINTER(Bins), ctypes.POINTER(TopK)]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
     "peat_series_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(Series)]),
@@ -267,6 +270,20 @@ def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None)
             v = int(v)
         d[name] = v
     return d
+
+
+def dict_to_sig(d: dict) -> Signature:
+    """A Signature struct holding the fields of a record dict (lists padded with 0)."""
+    s = Signature()
+    for name, typ in _SIG_FIELDS:
+        v = d[name]
+        if name in ("n_mismatch", "hist"):
+            arr = getattr(s, name)
+            for i, x in enumerate(v):
+                arr[i] = int(x)
+        else:
+            setattr(s, name, float(v) if typ is ctypes.c_double else int(v))
+    return s
 
 
 def record_to_dict(rec, nthr: int | None = None) -> dict:
@@ -440,6 +457,27 @@ def topk_mean_batched(pairs, num: int = 1, den: int = 10) -> list[dict]:
     outs = (TopK * max(1, count))()
     set_stream()
     _check(lib().peat_topk_mean_batched(arr, count, num, den, outs), "peat_topk_mean_batched")
+    return [topk_to_dict(outs[k]) for k in range(count)]
+
+
+def topk_mean_from_signature_batched(pairs, sigs, bins=(-40, 24, 64), num: int = 1, den: int = 10) -> list[dict]:
+    """peat_topk_mean_from_signature_batched: peat_topk_mean_batched given the
+    pairs' signatures (record dicts of signature_batched with these bins),
+    whose one-binade histograms let the first streaming pass skip the pairs."""
+    if isinstance(pairs, PreparedPairs):
+        arr, count = pairs.arr, pairs.count
+    else:
+        arr, count = _pairs_array(pairs), len(pairs)
+    if len(sigs) != count:
+        raise ValueError("one signature per pair")
+    recs = (Signature * max(1, count))()
+    for k, d in enumerate(sigs):
+        recs[k] = d if isinstance(d, Signature) else dict_to_sig(d)
+    b = make_bins(bins)
+    outs = (TopK * max(1, count))()
+    set_stream()
+    _check(lib().peat_topk_mean_from_signature_batched(arr, count, num, den, recs, ctypes.byref(b), outs),
+           "peat_topk_mean_from_signature_batched")
     return [topk_to_dict(outs[k]) for k in range(count)]
 
 

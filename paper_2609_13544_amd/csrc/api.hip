@@ -197,14 +197,21 @@ int check_dtype(int32_t dt) {
 
 int elem_size(int32_t dt) { return dt == PEAT_F32 ? 4 : 2; }
 
-int check_bins_thr(const peat_bins_t *bins, const peat_thresholds_t *thr) {
-    if (!bins || !thr) return fail(PEAT_EINVAL, "bins and thresholds must not be NULL");
-    if (bins->reserved != 0 || thr->reserved != 0) return fail(PEAT_EINVAL, "reserved fields must be 0");
-    const int lo = bins->lo_log2, hi = bins->hi_log2, nb = bins->nbins;
+int check_bins(const peat_bins_t &b) {
+    if (b.reserved != 0) return fail(PEAT_EINVAL, "reserved fields must be 0");
+    const int lo = b.lo_log2, hi = b.hi_log2, nb = b.nbins;
     if (lo < -1022 || hi > 1024 || lo >= hi)
         return fail(PEAT_EINVAL, "bins need -1022 <= lo_log2 < hi_log2 <= 1024 (got %d, %d)", lo, hi);
     if (nb < 1 || nb > PEAT_MAX_BINS || (hi - lo) % nb != 0)
         return fail(PEAT_EINVAL, "nbins must be in [1, 64] and divide hi_log2 - lo_log2 (got %d)", nb);
+    return PEAT_OK;
+}
+
+int check_bins_thr(const peat_bins_t *bins, const peat_thresholds_t *thr) {
+    if (!bins || !thr) return fail(PEAT_EINVAL, "bins and thresholds must not be NULL");
+    if (thr->reserved != 0) return fail(PEAT_EINVAL, "reserved fields must be 0");
+    int rc = check_bins(*bins);
+    if (rc) return rc;
     if (thr->count < 0 || thr->count > PEAT_MAX_THRESHOLDS)
         return fail(PEAT_EINVAL, "threshold count must be in [0, 8] (got %d)", thr->count);
     for (int j = 0; j < thr->count; ++j) {
@@ -541,8 +548,43 @@ int inject_signature_core(const peat_pair_t *pairs, int32_t count, const uint64_
 // Mean of the k largest errors: three streaming passes and the candidate
 // rounds (see topk.hip).  The call waits twice: once after pass 2 to size the
 // candidate buffers, once for the records.
+// Level 0 of the top-k selection from a pair's signature: its histogram
+// counts the same errors of the same valid pairs, and with one-binade bins
+// regular bin b is binade field lo + b + 1023.  Writes the state the level-0
+// selection would write and returns true when the k-th largest error lies in
+// a regular bin (otherwise pass 1 runs for the pair).
+constexpr int kBins0Host = 2048;   // level-0 digit of the top-k selection: the binade field
+
+bool topk_level0_from_sig(const peat_signature_t &g, const peat_bins_t &b, int32_t num, int32_t den,
+                          TopkState &st) {
+    if (b.hi_log2 - b.lo_log2 != b.nbins || g.n_valid <= 0) return false;
+    const uint64_t nv = (uint64_t)g.n_valid;
+    const uint64_t k = (uint64_t)(((unsigned __int128)nv * (uint32_t)num + (uint32_t)den - 1) / (uint32_t)den);
+    uint64_t acc = (uint64_t)g.hist_over;
+    if (k <= acc) return false;
+    for (int i = b.nbins - 1; i >= 0; --i) {
+        const uint64_t c = (uint64_t)g.hist[i];
+        if (acc + c >= k) {
+            const int d0 = b.lo_log2 + i + 1023;
+            if (d0 < 1 || d0 > kBins0Host - 2) return false;
+            st = TopkState{};
+            st.n_valid = nv;
+            st.k = k;
+            st.need = k - acc;
+            st.cand = c;
+            st.key = (uint64_t)d0 << 52;
+            st.level = 0;
+            st.status = kTopkActive;
+            st.d0 = d0;
+            return true;
+        }
+        acc += c;
+    }
+    return false;
+}
+
 int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den, peat_topk_t *outs,
-              hipStream_t s) {
+              hipStream_t s, const peat_signature_t *sigs = nullptr, const peat_bins_t *bins = nullptr) {
     if (count < 0) return fail(PEAT_EINVAL, "count < 0");
     if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
     if (num < 1 || den < num || den > (1 << 20))
@@ -552,6 +594,29 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
         if ((rc = check_mixed(pairs[k], k))) return rc;
     if (count == 0) return PEAT_OK;
     if (!outs) return fail(PEAT_EINVAL, "outs is NULL");
+    // level 0 from the callers' signatures, where they resolve it
+    std::vector<TopkState> pre;
+    std::vector<int32_t> skip;
+    int nskip = 0;
+    if (sigs) {
+        if (!bins) return fail(PEAT_EINVAL, "bins is NULL");
+        if ((rc = check_bins(*bins))) return rc;
+        pre.resize((size_t)count);
+        skip.assign((size_t)count, 0);
+        for (int k = 0; k < count; ++k) {
+            const peat_signature_t &g = sigs[k];
+            int64_t tot = g.hist_zero + g.hist_under + g.hist_over;
+            for (int i = 0; i < bins->nbins; ++i) tot += g.hist[i];
+            if (g.n != pairs[k].n || tot != g.n_valid)
+                return fail(PEAT_EINVAL, "signature %d does not match pair %d and these bins (n %lld vs %lld, "
+                            "histogram total %lld vs n_valid %lld)", k, k, (long long)g.n, (long long)pairs[k].n,
+                            (long long)tot, (long long)g.n_valid);
+            if (topk_level0_from_sig(g, *bins, num, den, pre[k])) {
+                skip[k] = 1;
+                ++nskip;
+            }
+        }
+    }
 
     std::lock_guard<std::mutex> lock(g_mu);
     Dev *dv;
@@ -570,19 +635,30 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     const size_t b_hist = align_up(sizeof(uint64_t) * kTopkBins * (size_t)count);
     const size_t b_part = align_up(sizeof(double) * (size_t)total);
     const size_t b_out = align_up(sizeof(peat_topk_t) * count);
+    const size_t b_skip = nskip ? align_up(sizeof(int32_t) * count) : 0;
     const size_t o_map = b_desc, o_state = o_map + b_map, o_cand = o_state + b_state;
     const size_t o_hist = o_cand + b_cand, o_pa = o_hist + b_hist, o_pb = o_pa + b_part, o_out = o_pb + b_part;
+    const size_t o_skip = o_out + b_out;
 
     char *ws;
-    if ((rc = acquire_ws(d, o_out + b_out, s, &ws))) return rc;
+    if ((rc = acquire_ws(d, o_skip + b_skip, s, &ws))) return rc;
     Slot *sl;
-    if ((rc = acquire_slot(d, b_desc + b_map + b_state + b_out, &sl))) return rc;
+    if ((rc = acquire_slot(d, b_desc + b_map + b_state + b_out + b_skip, &sl))) return rc;
     char *h = static_cast<char *>(sl->host);
     std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
     int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc);
     for (int k = 0; k < count; ++k)
         for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
     HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+    if (nskip) {
+        // the resolved pairs' level-0 states and the skip flags
+        char *hs = h + b_desc + b_map;
+        char *hk = h + b_desc + b_map + b_state + b_out;
+        std::memcpy(hs, pre.data(), sizeof(TopkState) * count);
+        std::memcpy(hk, skip.data(), sizeof(int32_t) * count);
+        HIP_OR_FAIL(hipMemcpyAsync(ws + o_state, hs, sizeof(TopkState) * count, hipMemcpyHostToDevice, s));
+        HIP_OR_FAIL(hipMemcpyAsync(ws + o_skip, hk, sizeof(int32_t) * count, hipMemcpyHostToDevice, s));
+    }
 
     TopkParams P{};
     P.chunk_base = 0;
@@ -594,17 +670,21 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     P.part_a = reinterpret_cast<double *>(ws + o_pa);
     P.part_b = reinterpret_cast<double *>(ws + o_pb);
     P.outs = reinterpret_cast<peat_topk_t *>(ws + o_out);
+    P.skip0 = nskip ? reinterpret_cast<const int32_t *>(ws + o_skip) : nullptr;
     P.count = count;
     P.num = num;
     P.den = den;
     const int64_t nhist = (int64_t)kTopkBins * count;
 
-    // passes 1 and 2 with their selections
+    // passes 1 and 2 with their selections (pass 1 only for the pairs that
+    // the signatures leave unresolved)
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;
-    HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
-    HIP_OR_FAIL(launch_topk_pass(P, 0, range, s));
-    HIP_OR_FAIL(launch_topk_select(P, 0, s));
+    if (nskip < count) {
+        HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
+        HIP_OR_FAIL(launch_topk_pass(P, 0, range, s));
+        HIP_OR_FAIL(launch_topk_select(P, 0, s));
+    }
     HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
     HIP_OR_FAIL(launch_topk_pass(P, 1, range, s));
     HIP_OR_FAIL(launch_topk_select(P, 1, s));
@@ -857,6 +937,16 @@ int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
 int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den,
                                  peat_topk_t *outs) {
     return topk_core(pairs, count, num, den, outs, t_stream);
+}
+
+int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                                          const peat_signature_t *sigs, const peat_bins_t *bins,
+                                          peat_topk_t *outs) {
+    if (count > 0 && !sigs) return fail(PEAT_EINVAL, "sigs is NULL");
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    return topk_core(mp.data(), count, num, den, outs, t_stream, sigs, bins);
 }
 
 int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream) {

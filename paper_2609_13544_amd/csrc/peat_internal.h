@@ -175,6 +175,7 @@ struct TopkParams {
     const int32_t *cblk_pair;    // candidate block -> pair
     uint64_t *xpart;             // per (round, candidate block): exact sums, 2 words
     peat_topk_t *outs;           // one per pair (device)
+    const int32_t *skip0;        // per pair: level 0 resolved from a signature histogram (or NULL)
     int64_t ncblk;               // candidate blocks
     int32_t count;               // pairs
     int32_t num, den;

@@ -20,6 +20,11 @@
 //            entries on it;
 //   finalize sum = (pass 2 + pass 3) + exact candidate sums + need * T.
 //
+// Given the pair's error signature with one-binade histogram bins (the same
+// errors over the same valid pairs), the host resolves level 0 from that
+// histogram whenever the k-th largest error falls in a regular bin, and
+// pass 1 and the level-0 selection skip the pair.
+//
 // The k-th largest error T is the key with all five digits fixed; count_above
 // is k minus the copies of T taken.  Passes 2 and 3 sum in a fixed
 // per-lane / butterfly / wave order over chunks whose size depends only on
@@ -187,6 +192,7 @@ __global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
     uint64_t *H = P.hist + (size_t)pair * kTopkBins;
 
     if constexpr (PASS == 0) {
+        if (P.skip0 && P.skip0[pair]) return;                 // level 0 already resolved
         for (int b = threadIdx.x; b < kBins0; b += kBlock) h[b] = 0;
         __syncthreads();
         for_each_error<DG, DT>(d, cin, [&](uint64_t key, double) { atomicAdd(&h[key >> 52], 1u); });
@@ -256,6 +262,7 @@ __global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
 __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     const int pair = blockIdx.x;
     const int L = P.level;
+    if (L == 0 && P.skip0 && P.skip0[pair]) return;           // state written by the host
     TopkState st = P.state[pair];
     if (L > 0 && !(st.status == kTopkActive && st.level == L - 1)) return;
     const int nb = L == 0 ? kBins0 : kTopkBins;

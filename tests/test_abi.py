@@ -53,7 +53,7 @@ def test_struct_layouts():
 
 def test_abi_version_and_strerror():
     L = P.lib()
-    assert L.peat_abi_version() == 5
+    assert L.peat_abi_version() == 6
     for code in range(0, -8, -1):
         assert L.peat_strerror(code)
     assert L.peat_strerror(-99) == b"unknown error code"
@@ -264,3 +264,47 @@ def test_inject_signature_validation_codes():
     assert rc([(A, A + 3996, 1000, 0)]) == B.EINVAL and b"overlaps" in L.peat_last_error()  # own golden
     # adjacent tensors and empty pairs do not overlap
     assert rc([(A, A + 4000, 1000, 0), (A + 8192, A + 4000, 0, 0)]) == B.EINVAL and b"d_outs" in L.peat_last_error()
+
+
+def test_topk_from_signature_validation_codes():
+    """Top-k from signatures: the records are checked against the pairs and
+    the bins before any device access (the pointers below are never touched)."""
+    L = P.lib()
+    A = 1 << 40
+    arr = (B.Pair * 1)(B.Pair(A, A + 4096, 1000, 0, 0))
+    outs = (B.TopK * 1)()
+    b = B.Bins(-40, 24, 64, 0)
+    sig = B.Signature()
+    sig.n, sig.n_valid, sig.hist_zero = 1000, 1000, 1000
+    recs = (B.Signature * 1)(sig)
+    call = L.peat_topk_mean_from_signature_batched
+    assert call(None, 0, 1, 10, None, None, None) == B.OK
+    assert call(arr, 1, 1, 10, None, ctypes.byref(b), outs) == B.EINVAL and b"sigs" in L.peat_last_error()
+    assert call(arr, 1, 1, 10, recs, None, outs) == B.EINVAL and b"bins" in L.peat_last_error()
+    assert call(arr, 1, 1, 10, recs, ctypes.byref(B.Bins(-40, 24, 7, 0)), outs) == B.EINVAL   # 7 does not divide 64
+    assert call(arr, 1, 0, 10, recs, ctypes.byref(b), outs) == B.EINVAL                       # num < 1
+    bad = B.Signature()
+    bad.n, bad.n_valid, bad.hist_zero = 999, 999, 999                  # another pair's record
+    assert call(arr, 1, 1, 10, (B.Signature * 1)(bad), ctypes.byref(b), outs) == B.EINVAL
+    assert b"does not match" in L.peat_last_error()
+    bad2 = B.Signature()
+    bad2.n, bad2.n_valid, bad2.hist_zero = 1000, 1000, 990             # histogram total below n_valid
+    assert call(arr, 1, 1, 10, (B.Signature * 1)(bad2), ctypes.byref(b), outs) == B.EINVAL
+
+
+def test_signature_dict_round_trip():
+    """dict_to_sig is the inverse of sig_to_dict (the records the top-k call
+    takes back from Python)."""
+    s = B.Signature()
+    for i, (name, typ) in enumerate(B._SIG_FIELDS):
+        if name in ("n_mismatch", "hist"):
+            arr = getattr(s, name)
+            for j in range(len(arr)):
+                arr[j] = 1000 * i + j
+        elif typ is ctypes.c_double:
+            setattr(s, name, 0.5 + i)
+        else:
+            setattr(s, name, 7 * i + 1)
+    d = B.sig_to_dict(s)
+    assert B.sig_to_dict(B.dict_to_sig(d)) == d
+    assert bytes(B.dict_to_sig(d)) == bytes(s)

@@ -137,3 +137,45 @@ def test_llama7b_tensor_full_size():
         assert got["k"] == -(-G.numel() // 10)
         del G, T
     torch.cuda.empty_cache()
+
+
+def test_from_signature_equals_three_passes():
+    """peat_topk_mean_from_signature_batched: records bit-identical to the
+    three-pass call and within the oracle's bar, both where the signature's
+    one-binade histogram resolves level 0 (regular bins) and where it cannot
+    (k-th largest error in hist_over, hist_under or hist_zero, or bins two
+    binades wide), with Inf and NaN pairs, empty pairs and unaligned views."""
+    from tests.parity import float_to_bits
+    rng = np.random.default_rng(2024)
+    cases = []
+    n = 300007
+    g = rng.standard_normal(n)
+    for code in (0, 1, 2):
+        cases.append(("specials", *special_pair(200003, code, seed=3100 + code), code))
+        cases.append(("relative 1e-3", float_to_bits(g, code), float_to_bits(g * (1 + 1e-3 * rng.standard_normal(n)), code), code))
+    g32 = g.astype(np.float32)
+    cases.append(("huge errors (over)", g32.view(np.uint32), (g32 * np.float32(3e8)).view(np.uint32), 0))
+    cases.append(("tiny errors (under)", g32.view(np.uint32),
+                  (g32 + np.float32(1e-13) * (np.arange(n) % 7 == 0)).view(np.uint32), 0))
+    t_inf = g32.copy()
+    t_inf[rng.integers(0, n, 40000)] = np.inf
+    cases.append(("Inf errors above", g32.view(np.uint32), t_inf.view(np.uint32), 0))
+    t_nan = (g32 * np.float32(1.001)).copy()
+    t_nan[rng.integers(0, n, 5000)] = np.nan
+    cases.append(("NaN pairs", g32.view(np.uint32), t_nan.view(np.uint32), 0))
+    cases.append(("identical", g32.view(np.uint32), g32.view(np.uint32).copy(), 0))
+    cases.append(("empty", np.zeros(0, np.uint32), np.zeros(0, np.uint32), 0))
+    pairs = [(to_device(gb, c), to_device(tb, c)) for _, gb, tb, c in cases]
+    gbu, tbu = special_pair(90001, 0, seed=77)
+    pairs.append((to_device(gbu, 0)[1:], to_device(tbu, 0)[1:]))
+    cases.append(("unaligned", gbu[1:], tbu[1:], 0))
+    for bins in ((-40, 24, 64), (-40, 24, 32), (-20, 10, 30)):
+        sigs = P.signature_batched(pairs, bins=bins)
+        for num, den in ((1, 10), (1, 1000), (1, 1), (3, 7)):
+            log(f"  bins={bins} frac={num}/{den}")
+            ref3 = P.topk_mean_batched(pairs, num, den)
+            got = P.topk_mean_from_signature_batched(pairs, sigs, bins, num, den)
+            for k, (name, gb, tb, c) in enumerate(cases):
+                assert same_record(got[k], ref3[k]), f"{name} bins={bins} {num}/{den}: {got[k]} != {ref3[k]}"
+                if bins == (-40, 24, 64) and (num, den) == (1, 10):
+                    assert_topk(got[k], oracle.topk(gb, tb, dtype=c, num=num, den=den), name)
