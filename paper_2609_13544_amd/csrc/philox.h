@@ -19,8 +19,9 @@ __device__ __forceinline__ void philox(uint64_t c, uint32_t s, uint64_t seed, ui
     for (int r = 0; r < 10; ++r) {
         const uint64_t p0 = (uint64_t)kPhiloxM0 * x0;
         const uint64_t p1 = (uint64_t)kPhiloxM1 * x2;
-        const uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
-        const uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+        // three-input XORs as single v_bitop3_b32 (truth table 0x96)
+        const uint32_t y0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), x1, k0, 0x96);
+        const uint32_t y2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), x3, k1, 0x96);
         x0 = y0;
         x1 = (uint32_t)p1;
         x2 = y2;
