@@ -295,6 +295,13 @@ int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t coun
                                           int32_t den, const peat_signature_t *sigs,
                                           const peat_bins_t *bins, peat_topk_t *outs);
 
+/* peat_topk_mean_from_signature_batched over mixed-precision pairs, with the
+ * records of peat_signature_mixed_batched (or its async form) for the same
+ * pairs and bins; outs are bit-identical to peat_topk_mean_mixed_batched's. */
+int peat_topk_mean_mixed_from_signature_batched(const peat_mixed_pair_t *pairs, int32_t count,
+                                                int32_t num, int32_t den, const peat_signature_t *sigs,
+                                                const peat_bins_t *bins, peat_topk_t *outs);
+
 /* Random bit flip in place (Section II-B).  The draws come from
  * Philox4x32-10 keyed by (lo32(seed), hi32(seed)); "block c of stream s" is
  * its output at counter (lo32(c), hi32(c), s, 0), four 32-bit words, bytes

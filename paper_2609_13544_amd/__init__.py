@@ -9,7 +9,7 @@ from ._binding import (  # noqa: F401
     SIG_NP_DTYPE, STREAM_SPAN, cast_round, corrupt_positions, inject_model, PeatError, PreparedItems, PreparedPairs, decode_records, dtype_code,
     finalize_stats, inject, inject_batched, inject_batched_async, lib, profile_enable,
     profile_read, set_stream, signature, signature_batched, signature_batched_async, stream_read,
-    strerror, topk_mean, topk_mean_batched, topk_mean_from_signature_batched, series_stats, spearman, normalize_scores,
+    strerror, topk_mean, topk_mean_batched, topk_mean_from_signature_batched, topk_mean_mixed_from_signature_batched, series_stats, spearman, normalize_scores,
     signature_mixed, signature_mixed_batched, signature_mixed_batched_async, topk_mean_mixed_batched,
     inject_signature_batched_async, K_SIG_INJECT,
 )

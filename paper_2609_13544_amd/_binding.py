@@ -165,6 +165,10 @@ _PROTOS = {
     "peat_topk_mean_from_signature_batched": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32, ctypes.c_int32,
                                                              ctypes.c_int32, ctypes.POINTER(Signature),
                                                              ctypes.POINTER(Bins), ctypes.POINTER(TopK)]),
+    "peat_topk_mean_mixed_from_signature_batched": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32,
+                                                                   ctypes.c_int32, ctypes.c_int32,
+                                                                   ctypes.POINTER(Signature), ctypes.POINTER(Bins),
+                                                                   ctypes.POINTER(TopK)]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
     "peat_series_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(Series)]),
@@ -479,6 +483,24 @@ def topk_mean_from_signature_batched(pairs, sigs, bins=(-40, 24, 64), num: int =
     _check(lib().peat_topk_mean_from_signature_batched(arr, count, num, den, recs, ctypes.byref(b), outs),
            "peat_topk_mean_from_signature_batched")
     return [topk_to_dict(outs[k]) for k in range(count)]
+
+
+def topk_mean_mixed_from_signature_batched(pairs, sigs, bins=(-40, 24, 64), num: int = 1,
+                                           den: int = 10) -> list[dict]:
+    """peat_topk_mean_mixed_from_signature_batched: topk_mean_mixed_batched
+    given the pairs' signatures (record dicts of signature_mixed_batched)."""
+    arr = _mixed_pairs_array(pairs)
+    if len(sigs) != len(pairs):
+        raise ValueError("one signature per pair")
+    recs = (Signature * max(1, len(pairs)))()
+    for k, d in enumerate(sigs):
+        recs[k] = d if isinstance(d, Signature) else dict_to_sig(d)
+    b = make_bins(bins)
+    outs = (TopK * max(1, len(pairs)))()
+    set_stream()
+    _check(lib().peat_topk_mean_mixed_from_signature_batched(arr, len(pairs), num, den, recs, ctypes.byref(b), outs),
+           "peat_topk_mean_mixed_from_signature_batched")
+    return [topk_to_dict(outs[k]) for k in range(len(pairs))]
 
 
 class PreparedPairs:

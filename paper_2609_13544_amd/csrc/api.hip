@@ -949,6 +949,13 @@ int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t coun
     return topk_core(mp.data(), count, num, den, outs, t_stream, sigs, bins);
 }
 
+int peat_topk_mean_mixed_from_signature_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
+                                                int32_t den, const peat_signature_t *sigs,
+                                                const peat_bins_t *bins, peat_topk_t *outs) {
+    if (count > 0 && !sigs) return fail(PEAT_EINVAL, "sigs is NULL");
+    return topk_core(pairs, count, num, den, outs, t_stream, sigs, bins);
+}
+
 int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream) {
     if (bytes < 0) return fail(PEAT_EINVAL, "bytes < 0");
     if (bytes == 0) return PEAT_OK;

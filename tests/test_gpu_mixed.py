@@ -190,12 +190,17 @@ def test_topk_mixed_every_kind():
             gb, tb = mixed_pair(n, gdt, tdt, seed=9600 + 10 * i + j)
             hosts.append((gb, tb, gdt, tdt))
             pairs.append((dev(gb, gdt), dev(tb, tdt)))
+    sigs = P.signature_mixed_batched(pairs, thresholds=THR)
     for num, den in [(1, 10), (1, 1), (3, 7)]:
         log(f"  mixed top-k {num}/{den} over {len(pairs)} pairs")
         outs = P.topk_mean_mixed_batched(pairs, num, den)
+        # given the signatures (one-binade bins): the same records, bit for bit
+        fs = P.topk_mean_mixed_from_signature_batched(pairs, sigs, num=num, den=den)
         for k, (gb, tb, gdt, tdt) in enumerate(hosts):
             ref = oracle.topk_mixed(gb, tb, gdtype=gdt, tdtype=tdt, num=num, den=den)
             assert_topk(outs[k], ref, f"{gdt}/{tdt} pair {k} {num}/{den}")
+            assert all(fs[k][f] == outs[k][f] or (fs[k][f] != fs[k][f] and outs[k][f] != outs[k][f])
+                       for f in outs[k]), f"{gdt}/{tdt} pair {k}: from signature {fs[k]} != {outs[k]}"
 
 
 def test_topk_and_histogram_of_subnormal_binary64_errors():

@@ -179,3 +179,21 @@ def test_from_signature_equals_three_passes():
                 assert same_record(got[k], ref3[k]), f"{name} bins={bins} {num}/{den}: {got[k]} != {ref3[k]}"
                 if bins == (-40, 24, 64) and (num, den) == (1, 10):
                     assert_topk(got[k], oracle.topk(gb, tb, dtype=c, num=num, den=den), name)
+
+
+def test_from_signature_with_fused_step_records():
+    """The records of the fused injection + signature call (decoded from
+    device memory) serve the top-k call on the injected tensors."""
+    pairs_host = [special_pair(n, 0, seed=5100 + n % 97) for n in (400009, 70001, 1 << 20)]
+    pairs = [(to_device(g, 0), to_device(t, 0)) for g, t in pairs_host]
+    seeds = [11, 12, 13]
+    d_out = torch.zeros(len(pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    d_counts = torch.zeros(len(pairs), dtype=torch.int64, device="cuda")
+    P.inject_signature_batched_async(pairs, seeds, 1e-4, 0x7F800000, d_out, d_counts)
+    torch.cuda.synchronize()
+    sigs = P.decode_records(d_out, len(pairs))
+    for num, den in ((1, 10), (1, 100)):
+        ref3 = P.topk_mean_batched(pairs, num, den)
+        got = P.topk_mean_from_signature_batched(pairs, sigs, num=num, den=den)
+        for k in range(len(pairs)):
+            assert same_record(got[k], ref3[k]), f"pair {k} {num}/{den}: {got[k]} != {ref3[k]}"
