@@ -201,21 +201,36 @@ int peat_init(void);
  * the calling host thread. */
 int peat_set_stream(void *stream);
 
-/* Error signature of one pair; out is host memory.  n = 0 is valid and gives
- * zero counts, NaN maxima and -1 indices. */
+/* Error signature of one pair: the Err(golden, FI) step of Algorithms 1 and
+ * 2 for one recorded tensor, with the scores of Section IV-B.3 (error =
+ * absolute difference; max, mean, variance), the closeness counts of
+ * Section III-A and the error histogram of Section V-D.  golden and test are
+ * device arrays of n elements of dtype (any alignment; 16-byte aligned
+ * pairs take the vector path); bins and thresholds as above; out is host
+ * memory, written when the call returns.  n = 0 is valid and gives zero
+ * counts, NaN maxima and -1 indices.  PEAT_EINVAL for NULL tensors with
+ * n > 0, n < 0 or n > 2^46, bad bins or thresholds; PEAT_EDTYPE for an
+ * unknown dtype. */
 int peat_signature(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
                    const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                    peat_signature_t *out);
 
-/* Signatures of count >= 0 pairs in one launch sequence; outs is a host
- * array of count records.  Each record is bit-identical to the one
- * peat_signature gives for the same pair. */
+/* Signatures of count >= 0 pairs in one launch sequence: Err() over the N
+ * recorded tensors of Algorithm 1 (the outputs of one kernel) or of a
+ * training step in Algorithm 2, each pair as in peat_signature.  pairs is a
+ * host array of count descriptors, copied before the call returns; outs is
+ * a host array of count records.  Each record is bit-identical to the one
+ * peat_signature gives for the same pair.  Errors as peat_signature's, per
+ * pair, plus PEAT_EINVAL for count < 0 or NULL arrays. */
 int peat_signature_batched(const peat_pair_t *pairs, int32_t count,
                            const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                            peat_signature_t *outs);
 
-/* As peat_signature_batched, enqueued on stream; d_outs is a device array of
- * count records written when the stream reaches the work. */
+/* As peat_signature_batched (the Err step of Algorithms 1 and 2), enqueued
+ * on stream (a hipStream_t; NULL is the null stream): d_outs is a device
+ * array of count records written when the stream reaches the work; the call
+ * returns without waiting.  The golden and test tensors must stay allocated
+ * and unchanged until then. */
 int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
                                  const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                                  peat_signature_t *d_outs, void *stream);
@@ -226,8 +241,12 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
  * given rate and bitmask (valid for every pair's dtype), and the signatures
  * of the pairs (golden, flipped test) are computed -- records, tensor bits
  * and counts equal to peat_inject_batched followed by
- * peat_signature_batched.  Each chunk of a test tensor is flipped (atomic
- * bit toggles) before it is read, in the same kernel.  seeds is a host array
+ * peat_signature_batched.  When every test tensor starts on a 128-byte
+ * boundary and no 128-byte line holding test bytes holds bytes of another
+ * tensor of the batch (separately allocated tensors always qualify), each
+ * chunk of a test tensor is flipped (atomic bit toggles) before it is read,
+ * in the same kernel; any other batch runs as the injection kernel followed
+ * by the signature pass, with the same results.  seeds is a host array
  * of count seeds; d_outs a device array of count records and d_counts a
  * device int64 array of count flip counts, written when the stream reaches
  * the work.  Test tensors must not overlap one another or any golden tensor

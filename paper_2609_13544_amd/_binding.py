@@ -504,11 +504,16 @@ def topk_mean_mixed_from_signature_batched(pairs, sigs, bins=(-40, 24, 64), num:
 
 
 class PreparedPairs:
-    """Pair descriptors built once, for repeated asynchronous calls."""
+    """Pair descriptors built once, for repeated asynchronous calls.  The
+    descriptors hold raw device addresses, so the object keeps the golden and
+    test tensors alive for as long as it exists (a freed tensor's memory could
+    otherwise be handed to another tensor and then read or, by the injecting
+    calls, written)."""
 
     def __init__(self, pairs):
         self.count = len(pairs)
         self.arr = _pairs_array(pairs)
+        self.tensors = [x for p in pairs if not isinstance(p, Pair) for x in (p[0], p[1])]
 
 
 def signature_batched_async(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), stream=None) -> None:
@@ -616,9 +621,14 @@ def _items_array(items):
 
 
 class PreparedItems:
+    """Injection descriptors built once, for repeated asynchronous calls; keeps
+    the items' tensors alive for its lifetime (the descriptors hold raw device
+    addresses that the calls write)."""
+
     def __init__(self, items):
         self.count = len(items)
         self.arr = _items_array(items)
+        self.tensors = [it[0] for it in items if not isinstance(it, InjectItem)]
 
 
 def inject_batched(items) -> list[int]:

@@ -481,9 +481,46 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
     return PEAT_OK;
 }
 
+// Whether the fused pass may inject the batch: every nonempty test tensor
+// starts on a 128-byte cache line and no line that holds test bytes holds
+// bytes of any other tensor of the batch.  Chunks are at least 4096 elements
+// (8 KiB) long, so every chunk of such a tensor then covers whole lines that
+// no other chunk, pair or block of the launch reads: the only load of a line
+// that a block flips is that block's own, after its flips.  (The other
+// caches' state at the start of the kernel is clean: the dispatch
+// invalidates the compute units' L1 caches.)  A line shared with a chunk of
+// another block could otherwise sit in the compute unit's L1 from that
+// block's load, taken before the flip reached L2, and satisfy the later read
+// with the old bits.
+bool fused_lines_private(const peat_pair_t *pairs, int32_t count) {
+    constexpr uintptr_t kLine = 128;
+    struct Span { uintptr_t a, b; int test; };
+    std::vector<Span> sp;
+    sp.reserve(2 * (size_t)count);
+    for (int k = 0; k < count; ++k) {
+        if (pairs[k].n == 0) continue;
+        const uintptr_t bytes = (uintptr_t)pairs[k].n * (uintptr_t)elem_size(pairs[k].dtype);
+        const uintptr_t g = reinterpret_cast<uintptr_t>(pairs[k].golden);
+        const uintptr_t t = reinterpret_cast<uintptr_t>(pairs[k].test);
+        if (t % kLine != 0) return false;
+        sp.push_back({g / kLine, (g + bytes + kLine - 1) / kLine, 0});
+        sp.push_back({t / kLine, (t + bytes + kLine - 1) / kLine, 1});
+    }
+    std::sort(sp.begin(), sp.end(), [](const Span &x, const Span &y) { return x.a < y.a; });
+    uintptr_t end_any = 0, end_test = 0;
+    for (const Span &x : sp) {
+        if (x.test && x.a < end_any) return false;     // a test line shared with an earlier span
+        if (!x.test && x.a < end_test) return false;   // a golden line shared with an earlier test
+        end_any = std::max(end_any, x.b);
+        if (x.test) end_test = std::max(end_test, x.b);
+    }
+    return true;
+}
+
 // Injection and signature in one pass (same-type pairs, the bit-flip model):
 // the records and flip counts of peat_inject_batched on the test tensors
-// followed by peat_signature_batched.
+// followed by peat_signature_batched.  Batches whose test tensors are not
+// line-private (fused_lines_private) take the two launches instead.
 int inject_signature_core(const peat_pair_t *pairs, int32_t count, const uint64_t *seeds, double rate,
                           uint64_t bitmask, const peat_bins_t *bins, const peat_thresholds_t *thr,
                           peat_signature_t *d_outs, int64_t *d_counts, hipStream_t s) {
@@ -528,6 +565,16 @@ int inject_signature_core(const peat_pair_t *pairs, int32_t count, const uint64_
     }
     if (count == 0) return PEAT_OK;
     if (!d_outs || !d_counts) return fail(PEAT_EINVAL, "d_outs or d_counts is NULL");
+    if (!fused_lines_private(pairs, count)) {
+        // Two launches: the injection kernel, then the signature pass; the
+        // kernel boundary orders every flip before every read.
+        std::vector<peat_inject_item_t> items((size_t)count);
+        for (int k = 0; k < count; ++k)
+            items[k] = peat_inject_item_t{const_cast<void *>(pairs[k].test), pairs[k].n, pairs[k].dtype,
+                                          PEAT_MODEL_BITFLIP, seeds[k], rate, bitmask};
+        if ((rc = inject_core(items.data(), count, d_counts, nullptr, s))) return rc;
+        return signature_core(mp.data(), count, bins, thr, d_outs, nullptr, s);
+    }
     std::vector<InjDesc> inj((size_t)count);
     for (int k = 0; k < count; ++k) {
         InjDesc &q = inj[k];

@@ -28,8 +28,11 @@ constexpr int kQCap = 64 + 32 * 64;   // per-wave queue: < 64 left over + one ap
 
 // The chosen element's new bits: a bit flip, +0 or the type's quiet NaN.
 // ATOMIC: the bit flip is one device-scope atomic XOR on the aligned 32-bit
-// word that holds the element, which leaves no copy of the line in the
-// compute unit's cache (the chunk pass streams the tensor right after).
+// word that holds the element, performed in L2 (a 16-bit neighbour in the
+// same word is XORed with zeros, so no other element can lose an update).
+// The fused chunk pass reads the flipped lines right after its own flips;
+// the host admits only batches whose test lines no other block reads, so no
+// compute unit holds a copy of such a line from before the flip.
 template <bool ATOMIC>
 __device__ __forceinline__ void flip(const InjDesc &d, uint64_t i) {
     if (d.model == PEAT_MODEL_BITFLIP) {

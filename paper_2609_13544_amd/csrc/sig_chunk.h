@@ -66,9 +66,13 @@ constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
 //     when the difference is formed in binary32 and rounded, it is at least
 //     |g|/2 in magnitude, which this limit rejects, so a fast-path error is
 //     always the exact difference;
-//   - t^2 = g^2 + 2ge + e^2 and gt = g^2 + ge hold exactly per element, and
-//     the fast path sums g^2, ge and e^2 only: their sums give those of t^2
-//     and gt with a condition number below 2.8;
+//   - the fast path sums g^2, ge and e^2 only, and the sums of t^2 and gt
+//     follow from t^2 = g^2 + 2ge + e^2 and gt = g^2 + ge (identities of
+//     exact arithmetic) with a condition number below 2.8.  When neither
+//     side is binary64, g and e have at most 24 significant bits, so the
+//     three products are exact in binary64 and only the summation rounds;
+//     with a binary64 test side e can have up to 53 bits and ge, e^2 are
+//     rounded products (2^-53 relative each), within the same tolerance;
 //   - an f32 ULP distance is below 2^24 and an f16/bf16 one below 2^11.
 constexpr double kRareRel = 0.25;
 constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
@@ -971,16 +975,21 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
     int run_first = 0;             // first chunk of the current run
     int64_t run_off = 0;           // its first element in the pair
     if constexpr (INJ) {
-        // Injection first: the bit flips of every chunk of the block are in
-        // memory (device-scope atomics) before any of their elements is
-        // loaded; the barrier orders them for the whole block.  The per-wave
-        // candidate queues borrow the histogram's LDS, cleared afterwards.
+        // Injection first: the bit flips of every chunk of the block are
+        // performed in the L2 of the block's XCD (atomics) before any of
+        // their elements is loaded.  Each wave waits until its atomics have
+        // completed (s_waitcnt 0) and the barrier then orders them before
+        // every wave's loads, which go to the same L2; no compute unit holds
+        // an older copy of these lines, because the host admits only batches
+        // whose test lines no other block reads.  The per-wave candidate
+        // queues borrow the histogram's LDS, cleared afterwards.
         uint32_t(*queue)[kQCap] = reinterpret_cast<uint32_t(*)[kQCap]>(sh.hist);
         for (int i = 0; i < cnt; ++i) {
             const ChunkCtx x = ctx(pair_of(c0 + i), c0 + i);
             const InjDesc &d = inj[x.pair];
             const bool none = !d.all && d.T == 0;
             const uint32_t f = none ? 0u : dpp_sum_u32(inject_span<true>(d, (uint64_t)x.off, x.len, queue));
+            __builtin_amdgcn_s_waitcnt(0);
             if (lane == 0) sh.rcnt[wave][0] = f;
             __syncthreads();
             if (tid == 0) {

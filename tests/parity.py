@@ -107,3 +107,30 @@ def assert_parity(got: dict, ref: dict, ctx: str = "") -> None:
 
 def oracle_sig(gb: np.ndarray, tb: np.ndarray, code: int, bins, thresholds) -> dict:
     return oracle.signature(gb, tb, dtype=code, bins=bins, thresholds=thresholds)
+
+
+def chunk_count(n: int) -> int:
+    """Chunks of an n-element pair under the library's chunk rule: the next
+    power of two >= n/256 elements below 2^22 elements (>= n/64 from 2^22 on),
+    clamped to [2^12, 2^18]."""
+    if n == 0:
+        return 0
+    target = 64 if n >= (1 << 22) else 256
+    per = -(-n // target)
+    log2 = max(12, min(18, (per - 1).bit_length()))
+    return -(-n // (1 << log2))
+
+
+# Launch-shape bound of the chunk pass: a block takes two consecutive chunks
+# once a launch has at least 2 x 8 x (resident blocks) chunks.  Resident
+# blocks are at most 3 per compute unit (a block holds ~52 KB of the 160 KB
+# of LDS) on 256 compute units, so 12288 chunks per launch force two-chunk
+# blocks.
+TWO_CHUNK_MIN = 2 * 8 * 3 * 256
+
+
+def records_equal(a: dict, b: dict) -> bool:
+    """Bit-level equality of two decoded records (NaN equals NaN)."""
+    return a.keys() == b.keys() and all(
+        a[k] == v or (isinstance(v, float) and math.isnan(v) and isinstance(a[k], float) and math.isnan(a[k]))
+        for k, v in b.items())

@@ -14,7 +14,9 @@ import torch
 import oracle
 import paper_2609_13544_amd as P
 import synth
-from tests.parity import assert_parity, oracle_sig, special_pair, to_device, to_host_bits
+from tests.parity import (NP_BITS, TORCH_INT, TWO_CHUNK_MIN, _SPECIALS, assert_parity, chunk_count, float_to_bits,
+                          oracle_sig, special_pair, to_device, to_host_bits)
+
 
 pytestmark = pytest.mark.gpu
 
@@ -70,33 +72,50 @@ def test_fused_against_oracle(code):
         assert_parity(recs[0], oracle_sig(gb, host, code, synth.BINS, synth.THRESHOLDS), f"n={n} rate={rate}")
 
 
+def _profile_counts(fn):
+    """Run fn with the library's kernel timing on; return the launches of the
+    fused chunk pass and of the injection kernel it made."""
+    P.profile_enable(True)
+    for k in (P.K_SIG_INJECT, P.K_INJECT):
+        P.profile_read(k)
+    try:
+        out = fn()
+    finally:
+        torch.cuda.synchronize()
+        fused = P.profile_read(P.K_SIG_INJECT)[1]
+        inj = P.profile_read(P.K_INJECT)[1]
+        P.profile_enable(False)
+    return out, fused, inj
+
+
 def test_fused_equals_separate_calls_many_pairs():
-    """A batch large enough for two-chunk blocks (injection of both chunks
-    before either is read), mixed types and sizes, unaligned pairs: the fused
-    call matches inject_batched + signature_batched bit for bit."""
+    """A batch of 4500 pairs of three types (about 2,200 chunks per type, so
+    one chunk per block), unaligned golden tensors (the generic path inside
+    the fused pass) and special values: the fused call runs the fused pass and
+    matches inject_batched + signature_batched bit for bit."""
     sizes = [2048, 3 * 4096, 4096 + 904, 20000, 4095, 9000, 1 << 16]
     hosts, fused_pairs, sep_pairs, seeds, codes = [], [], [], [], []
     for k in range(4500):
         code = (k // 3) % 3
         n = sizes[k % len(sizes)]
         gb, tb = special_pair(n, code, seed=90000 + k, special_frac=1e-3 if k % 5 == 0 else 0.0)
-        g = to_device(gb, code)
-        if k % 11 == 4:                          # test not 16-byte aligned
-            t1 = to_device(np.concatenate([tb[:1], tb]), code)[1:]
-            t2 = to_device(np.concatenate([tb[:1], tb]), code)[1:]
+        if k % 11 == 4:                          # golden not 16-byte aligned
+            g = to_device(np.concatenate([gb[:1], gb]), code)[1:]
         else:
-            t1, t2 = to_device(tb, code), to_device(tb, code)
+            g = to_device(gb, code)
         hosts.append((gb, tb))
-        fused_pairs.append((g, t1))
-        sep_pairs.append((g, t2))
+        fused_pairs.append((g, to_device(tb, code)))
+        sep_pairs.append((g, to_device(tb, code)))
         seeds.append(synth.inject_seed(12, k))
         codes.append(code)
     rate, mask_of = 3e-3, {0: 0x7F800000, 1: 0x7C00, 2: 0x7F80}
     # one call per dtype group (a batched call takes one bitmask)
     for code in range(3):
         idx = [k for k in range(len(codes)) if codes[k] == code]
-        log(f"  dtype={code}: {len(idx)} pairs")
-        recs, counts = _fused([fused_pairs[k] for k in idx], [seeds[k] for k in idx], rate, mask_of[code])
+        log(f"  dtype={code}: {len(idx)} pairs, {sum(chunk_count(hosts[k][0].size) for k in idx)} chunks")
+        (recs, counts), nfused, ninj = _profile_counts(
+            lambda: _fused([fused_pairs[k] for k in idx], [seeds[k] for k in idx], rate, mask_of[code]))
+        assert (nfused, ninj) == (1, 0), "expected the fused pass"
         sep_counts = P.inject_batched([(sep_pairs[k][1], seeds[k], rate, mask_of[code]) for k in idx])
         sep_recs = P.signature_batched([sep_pairs[k] for k in idx], synth.BINS, synth.THRESHOLDS)
         assert counts == sep_counts
@@ -109,6 +128,126 @@ def test_fused_equals_separate_calls_many_pairs():
             host = hosts[k][1].copy()
             assert oracle.inject(host, dtype=code, seed=seeds[k], rate=rate, mask=mask_of[code]) == counts[j]
             assert_parity(recs[j], oracle_sig(hosts[k][0], host, code, synth.BINS, synth.THRESHOLDS), f"pair {k}")
+
+
+def _bits_to_f64(bits: np.ndarray, code: int) -> np.ndarray:
+    if code == 0:
+        return bits.view(np.float32).astype(np.float64)
+    if code == 1:
+        return bits.view(np.float16).astype(np.float64)
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _packed(code: int, sizes, seed: int, align: int, gap: int, offsets=None):
+    """Seeded pairs packed into one golden and one test allocation (torch
+    allocations start on 512-byte boundaries).  Pair k starts at the first
+    multiple of `align` bytes at least `gap` bytes after the end of pair
+    k - 1, plus offsets[k] bytes.  Returns the pairs' host bits (golden, test),
+    the device pairs (views) and the flat device test buffer."""
+    es = 4 if code == 0 else 2
+    starts, pos = [], 0
+    for k, n in enumerate(sizes):
+        pos = -(-(pos + gap) // align) * align + (offsets[k] if offsets else 0)
+        assert pos % es == 0
+        starts.append(pos // es)
+        pos += n * es
+    total = pos // es + 1
+    rng = np.random.default_rng(seed)
+    gflat = float_to_bits(rng.standard_normal(total), code).copy()
+    tflat = float_to_bits(_bits_to_f64(gflat, code) * (1 + 1e-3 * rng.standard_normal(total)), code).copy()
+    gdev, tdev = to_device(gflat, code), to_device(tflat, code)
+    pairs = [(gdev[s0:s0 + n], tdev[s0:s0 + n]) for n, s0 in zip(sizes, starts)]
+    hosts = [(gflat[s0:s0 + n].copy(), tflat[s0:s0 + n].copy()) for n, s0 in zip(sizes, starts)]
+    return hosts, pairs, tdev
+
+
+def _fused_vs_separate(code, pairs, pairs2, tflat, tflat2, seeds, rate, mask, sample, path):
+    """One fused call on pairs and the two separate calls on pairs2 (an equal
+    copy): counts, flipped buffers and records equal; the sampled pairs'
+    flips and records against the oracle.  path: the expected kernels."""
+    gold = {k: to_host_bits(pairs[k][0]) for k in sample}
+    want = {k: to_host_bits(pairs[k][1]) for k in sample}
+    (recs, counts), nfused, ninj = _profile_counts(lambda: _fused(pairs, seeds, rate, mask))
+    assert (nfused, ninj) == ((1, 0) if path == "fused" else (0, 1)), (path, nfused, ninj)
+    sep_counts = P.inject_batched([(t, s, rate, mask) for (_, t), s in zip(pairs2, seeds)])
+    sep_recs = P.signature_batched(pairs2, synth.BINS, synth.THRESHOLDS)
+    assert counts == sep_counts
+    assert torch.equal(tflat.view(TORCH_INT[code]), tflat2.view(TORCH_INT[code])), "flipped tensors differ"
+    bad = [k for k in range(len(pairs)) if not _same(recs[k], sep_recs[k])]
+    assert not bad, f"fused and separate records differ for pairs {bad[:10]}"
+    for k in sample:
+        n = oracle.inject(want[k], dtype=code, seed=seeds[k], rate=rate, mask=mask)
+        assert n == counts[k], (k, n, counts[k])
+        assert np.array_equal(to_host_bits(pairs[k][1]), want[k]), f"pair {k}: flipped bits"
+        assert_parity(recs[k], oracle_sig(gold[k], want[k], code, synth.BINS, synth.THRESHOLDS),
+                      f"rate={rate} pair {k}")
+    return counts
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_fused_two_chunk_blocks(code):
+    """The launch shape the benchmark times: at least 12288 chunks in one
+    fused launch, so every block injects two consecutive chunks before it
+    reads either (see TWO_CHUNK_MIN).  About 920 pairs of 2^12..2^18
+    elements (15.4k chunks, 62 M elements) packed at line-private offsets
+    (so the fused pass runs), unaligned goldens for every 13th pair (the
+    generic path), special values;
+    two calls, in the top-byte filter regime (rate 3e-3) and in the general
+    one (0.3), every bit of the type in the mask.  Flipped tensors and records
+    equal peat_inject_batched followed by peat_signature_batched bit for bit;
+    sampled pairs match the oracle's injection followed by its signature."""
+    cycle = [1 << 16, (1 << 14) + 904, 3 * 4096 + 17, 40000, (1 << 16) - 5, 1 << 18, 4096, 70001]
+    sizes = []
+    while sum(chunk_count(n) for n in sizes) < 1.25 * TWO_CHUNK_MIN:
+        sizes.append(cycle[len(sizes) % len(cycle)])
+    nchunks = sum(chunk_count(n) for n in sizes)
+    assert nchunks >= TWO_CHUNK_MIN
+    hosts, pairs, tflat = _packed(code, sizes, seed=5100 + code, align=256, gap=256)
+    _, pairs2, tflat2 = _packed(code, sizes, seed=5100 + code, align=256, gap=256)
+    for k in range(0, len(sizes), 13):            # golden not 16-byte aligned
+        g = to_device(np.concatenate([hosts[k][0][:1], hosts[k][0]]), code)[1:]
+        pairs[k] = (g, pairs[k][1])
+        pairs2[k] = (g, pairs2[k][1])
+    rng = np.random.default_rng(77 + code)        # special values in both test copies
+    sp = np.array(list(_SPECIALS[code].values()), dtype=NP_BITS[code])
+    pos = torch.from_numpy(rng.integers(0, tflat.numel(), 20000)).cuda()
+    val = torch.from_numpy(sp[rng.integers(0, sp.size, 20000)].view(np.int32 if code == 0 else np.int16)).cuda()
+    for tf in (tflat, tflat2):
+        tf.view(TORCH_INT[code])[pos] = val
+    seeds = [synth.inject_seed(15, 10 * k + code) for k in range(len(sizes))]
+    mask = {0: 0xFFFFFFFF, 1: 0xFFFF, 2: 0xFFFF}[code]
+    sample = sorted({0, 1, 5, len(sizes) - 1, *range(13, len(sizes), 151)})
+    log(f"  dtype={code}: {len(sizes)} pairs, {nchunks} chunks (two-chunk blocks from {TWO_CHUNK_MIN})")
+    for rate in (3e-3, 0.3):
+        counts = _fused_vs_separate(code, pairs, pairs2, tflat, tflat2, seeds, rate, mask, sample, "fused")
+        log(f"    rate={rate}: {sum(counts)} flips, {len(sample)} pairs against the oracle")
+
+
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_fused_packed_offsets(code):
+    """Pairs packed in one allocation at 4/16/64/100-byte offsets (2 bytes
+    instead of 4 for f16/bf16) from their neighbours, so test tensors share
+    cache lines with other tensors: such a batch takes the two launches
+    (injection kernel, then the signature).  The same sizes at line-private
+    offsets (128-byte starts, a 128-byte gap) take the fused pass.  Both at
+    rate 1 (every element flips, every chunk edge included) and 0.3, against
+    separate calls and the oracle."""
+    es = 4 if code == 0 else 2
+    sizes = [4096 * 3 + 5, 4096, 70001, 1 << 14, 33, 4096 * 9 - 1, 100000, 8191]
+    mask = {0: 1 << 30, 1: 1 << 14, 2: 1 << 14}[code]
+    for layout in ("shared", "private"):
+        if layout == "shared":
+            kw = dict(align=es, gap=0, offsets=[[es, 16, 64, 100][k % 4] for k in range(len(sizes))])
+        else:
+            kw = dict(align=128, gap=128)
+        _, pairs, tflat = _packed(code, sizes, seed=6200 + code, **kw)
+        _, pairs2, tflat2 = _packed(code, sizes, seed=6200 + code, **kw)
+        seeds = [synth.inject_seed(16, 10 * k + code) for k in range(len(sizes))]
+        for rate in (1.0, 0.3):
+            path = "fused" if layout == "private" else "two launches"
+            counts = _fused_vs_separate(code, pairs, pairs2, tflat, tflat2, seeds, rate, mask,
+                                        list(range(len(sizes))), path)
+            log(f"  dtype={code} {layout}: rate={rate} {sum(counts)} flips ok")
 
 
 def test_fused_llama_tensors_full_size():

@@ -11,6 +11,7 @@ oracle, plus properties that hold at any size.
 from __future__ import annotations
 
 import math
+import os
 import sys
 
 import numpy as np
@@ -20,7 +21,7 @@ import torch
 import oracle
 import paper_2609_13544_amd as P
 import synth
-from tests.parity import (assert_parity, float_to_bits, oracle_sig, special_pair, to_device,
+from tests.parity import (assert_parity, float_to_bits, oracle_sig, records_equal, special_pair, to_device,
                           to_host_bits)
 
 pytestmark = pytest.mark.gpu
@@ -293,70 +294,132 @@ def test_workload3_full_sampled():
     torch.cuda.empty_cache()
 
 
+def _pool_map(fn, items, what: str):
+    """fn over items on a thread pool (the oracle's C calls release the GIL),
+    sized to the host share of one GPU; logs progress."""
+    from concurrent.futures import ThreadPoolExecutor
+    out = []
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        for j, r in enumerate(ex.map(fn, items)):
+            out.append(r)
+            if (j + 1) % 20 == 0 or j + 1 == len(items):
+                log(f"    {what}: {j + 1}/{len(items)}")
+    return out
+
+
 def test_workload4_replay():
-    """Replayed f16 calls: every 10th injected (rate 1e-7, any of 16 bits);
-    the 100 calls of the first 1000 that are injected are represented by the
-    first 30 calls here (3 injected), all checked against the oracle."""
+    """The replay workload in full: 1000 replayed f16 [4096, 4096] calls of
+    one golden output (33.5 GB of test tensors), every 10th injected at rate
+    1e-7 over all 16 bits by one batched injection, then one batched
+    signature over all 1000 calls (the workload's small-launch batched path).
+    Every injected call (100) is checked against the oracle: flip count,
+    flipped positions and bits, record.  The 900 others are untouched and
+    give the closed form of identical tensors.  Single async calls on one
+    stream give the same records (30 calls)."""
     G = synth.config4_golden("cuda")
     gb = to_host_bits(G)
-    calls = 30
-    tests, counts = [], []
-    for c in range(calls):
-        T = G.clone()
-        if synth.config4_injected(c):
-            counts.append(P.inject(T, synth.inject_seed(4, c), synth.CONFIG4_RATE, synth.CONFIG4_MASK))
-        tests.append(T)
+    calls = synth.CONFIG4_CALLS
+    tests = [G.clone() for _ in range(calls)]
+    inj = [c for c in range(calls) if synth.config4_injected(c)]
+    assert len(inj) == 100
+    counts = P.inject_batched([(tests[c], synth.inject_seed(4, c), synth.CONFIG4_RATE, synth.CONFIG4_MASK)
+                               for c in inj])
     recs = P.signature_batched([(G, T) for T in tests], synth.BINS, synth.THRESHOLDS)
-    for c in range(calls):
+    log(f"  workload 4: {sum(counts)} flips in {len(inj)} injected calls")
+    G16 = G.view(torch.int16)
+    diffs = {}
+    for c in inj:                                  # flipped positions and bits on the device
+        idx = torch.nonzero(tests[c].view(torch.int16) != G16).flatten()
+        diffs[c] = (idx.cpu().numpy(), tests[c].view(torch.int16).flatten()[idx].cpu().numpy().view(np.uint16))
+
+    def ref(c):
         tb = gb.copy()
-        if synth.config4_injected(c):
-            n = oracle.inject(tb, dtype=1, seed=synth.inject_seed(4, c), rate=synth.CONFIG4_RATE,
-                              mask=synth.CONFIG4_MASK)
-            assert n == counts[c // 10]
-            assert np.array_equal(to_host_bits(tests[c]), tb)
-            assert_parity(recs[c], oracle_sig(gb, tb, 1, synth.BINS, synth.THRESHOLDS), f"call {c}")
-        else:
-            assert recs[c]["hist_zero"] == recs[c]["n_valid"] and recs[c]["max_ulp"] == 0
+        n = oracle.inject(tb, dtype=1, seed=synth.inject_seed(4, c), rate=synth.CONFIG4_RATE,
+                          mask=synth.CONFIG4_MASK)
+        pos = np.nonzero(tb != gb)[0]
+        return n, pos, tb[pos], oracle_sig(gb, tb, 1, synth.BINS, synth.THRESHOLDS)
+
+    for j, (c, (n, pos, bits, sig)) in enumerate(zip(inj, _pool_map(ref, inj, "oracle calls"))):
+        assert n == counts[j], (c, n, counts[j])
+        assert np.array_equal(diffs[c][0], pos) and np.array_equal(diffs[c][1], bits), f"call {c}: flipped bits"
+        assert_parity(recs[c], sig, f"call {c}")
+    plain = [c for c in range(calls) if not synth.config4_injected(c)]
+    for c in plain:
+        r = recs[c]
+        assert records_equal(r, recs[plain[0]]), f"call {c}"
+    r = recs[plain[0]]
+    n = G.numel()
+    assert r["n"] == n and r["hist_zero"] == r["n_valid"] == n - r["n_nan_pairs"]
+    assert r["max_ulp"] == 0 and r["sum_ulp"] == 0 and r["max_abs"] == 0.0 and r["sum_abs"] == 0.0
+    assert r["n_mismatch"][:2] == [r["n_nan_pairs"]] * 2
     # single async calls on one stream give the same records
-    d_out = torch.empty(calls * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
-    prepared = [P.PreparedPairs([(G, T)]) for T in tests]
-    for c in range(calls):
-        P.signature_batched_async(prepared[c], d_out[c * P.SIG_BYTES:], synth.BINS, synth.THRESHOLDS)
+    sub = list(range(30))
+    d_out = torch.empty(len(sub) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    prepared = [P.PreparedPairs([(G, tests[c])]) for c in sub]
+    for j in range(len(sub)):
+        P.signature_batched_async(prepared[j], d_out[j * P.SIG_BYTES:], synth.BINS, synth.THRESHOLDS)
     torch.cuda.synchronize()
-    assert P.decode_records(d_out, calls, nthr=2) == recs
-    del tests, G
+    single = P.decode_records(d_out, len(sub), nthr=2)
+    assert all(records_equal(single[j], recs[c]) for j, c in enumerate(sub))
+    del tests, G, prepared
     torch.cuda.empty_cache()
 
 
 def test_workload5_full_sampled():
-    """Llama-7B-shaped pair (873 f32 tensors, 161.7 GB on device) in the
-    benchmark's configuration: one batched injection, one batched signature.
-    Sampled tensors (all three states of the smallest and largest shapes)
-    are checked against the oracle, injection included."""
+    """The Llama-7B-shaped pair (873 f32 tensors, 161.7 GB on device) in the
+    benchmark's own launch: one fused injection + signature call over all 873
+    pairs (rate 1e-8, exponent bits; about 77k chunks, so every block takes
+    two chunks).  Every record equals peat_signature_batched's over the
+    flipped tensors afterwards; sampled tensors (all three states of the
+    smallest and largest shapes) match the oracle's injection and signature;
+    the injection kernel with the same seeds returns the same count for every
+    tensor and restores the sampled tensors' original bits."""
+    from tests.parity import TWO_CHUNK_MIN, chunk_count
     tensors = synth.config5_all("cuda")
     log(f"  workload 5 generated: {torch.cuda.memory_allocated() / 1e9:.1f} GB")
+    pairs = [(G, T) for _, _, G, T in tensors]
+    assert sum(chunk_count(G.numel()) for G, _ in pairs) >= TWO_CHUNK_MIN
     names = [name for name, *_ in tensors]
     sample = [k for k, nm in enumerate(names) if nm in ("l0.in_norm", "norm", "l0.q", "l31.down", "embed")]
-    pre = {k: to_host_bits(tensors[k][3]) for k in sample}
-    items = [(T, synth.inject_seed(5, k), synth.CONFIG5_RATE, synth.CONFIG5_MASK)
-             for k, (_, _, _, T) in enumerate(tensors)]
-    counts = P.inject_batched(items)
-    recs = P.signature_batched([(G, T) for _, _, G, T in tensors], synth.BINS, synth.THRESHOLDS)
-    log(f"  workload 5: {sum(counts)} flips, sampling {len(sample)} tensors")
-    for k in sample:
-        name, state, G, T = tensors[k]
-        tb = pre[k]
-        n = oracle.inject(tb, dtype=0, seed=synth.inject_seed(5, k), rate=synth.CONFIG5_RATE,
-                          mask=synth.CONFIG5_MASK)
+    pre = {k: (to_host_bits(tensors[k][2]), to_host_bits(tensors[k][3])) for k in sample}
+    seeds = [synth.inject_seed(5, k) for k in range(len(pairs))]
+    d_out = torch.empty(len(pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    d_counts = torch.empty(len(pairs), dtype=torch.int64, device="cuda")
+    P.profile_enable(True)
+    P.profile_read(P.K_SIG_INJECT)
+    P.inject_signature_batched_async(P.PreparedPairs(pairs), seeds, synth.CONFIG5_RATE, synth.CONFIG5_MASK,
+                                     d_out, d_counts, synth.BINS, synth.THRESHOLDS)
+    torch.cuda.synchronize()
+    assert P.profile_read(P.K_SIG_INJECT)[1] == 1, "expected the fused pass"
+    P.profile_enable(False)
+    recs = P.decode_records(d_out, len(pairs), nthr=len(synth.THRESHOLDS))
+    counts = d_counts.cpu().tolist()
+    log(f"  workload 5: {sum(counts)} flips")
+    again = P.signature_batched(pairs, synth.BINS, synth.THRESHOLDS)
+    bad = [k for k in range(len(pairs)) if not records_equal(recs[k], again[k])]
+    assert not bad, f"fused records differ from the signature of the flipped tensors: {bad[:10]}"
+    flipped = {k: to_host_bits(tensors[k][3]) for k in sample}
+
+    def ref(k):
+        gbits, tbits = pre[k]
+        tb = tbits.copy()
+        n = oracle.inject(tb, dtype=0, seed=seeds[k], rate=synth.CONFIG5_RATE, mask=synth.CONFIG5_MASK)
+        return n, tb, oracle_sig(gbits, tb, 0, synth.BINS, synth.THRESHOLDS)
+
+    for k, (n, tb, sig) in zip(sample, _pool_map(ref, sample, "oracle tensors")):
+        name, state = tensors[k][0], tensors[k][1]
         assert n == counts[k], (name, state, n, counts[k])
-        assert np.array_equal(to_host_bits(T), tb), f"{name}/{state}: injected bits differ"
-        assert_parity(recs[k], oracle_sig(to_host_bits(G), tb, 0, synth.BINS, synth.THRESHOLDS),
-                      f"{name}/{state}")
-        log(f"    {name}/{state} ok")
+        assert np.array_equal(flipped[k], tb), f"{name}/{state}: injected bits differ"
+        assert_parity(recs[k], sig, f"{name}/{state}")
+    # the injection kernel with the same seeds: same decisions, flips undone
+    undo = P.inject_batched([(T, s, synth.CONFIG5_RATE, synth.CONFIG5_MASK) for (_, T), s in zip(pairs, seeds)])
+    assert undo == counts
+    for k in sample:
+        assert np.array_equal(to_host_bits(tensors[k][3]), pre[k][1]), f"{names[k]}: not restored"
     for r in recs:
         assert r["n_nan_pairs"] == 0 or r["n_nan_test"] > 0
         assert r["hist_zero"] + r["hist_under"] + sum(r["hist"]) + r["hist_over"] == r["n_valid"]
-    del tensors, items
+    del tensors, pairs
     torch.cuda.empty_cache()
 
 
