@@ -138,12 +138,14 @@ def _bits_to_f64(bits: np.ndarray, code: int) -> np.ndarray:
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def _packed(code: int, sizes, seed: int, align: int, gap: int, offsets=None):
+def _packed(code: int, sizes, seed: int, align: int, gap: int, offsets=None, specials: int = 0):
     """Seeded pairs packed into one golden and one test allocation (torch
     allocations start on 512-byte boundaries).  Pair k starts at the first
     multiple of `align` bytes at least `gap` bytes after the end of pair
-    k - 1, plus offsets[k] bytes.  Returns the pairs' host bits (golden, test),
-    the device pairs (views) and the flat device test buffer."""
+    k - 1, plus offsets[k] bytes; `specials` special values (NaN, Inf, zero,
+    subnormal, ...) are planted at distinct positions of the test buffer.
+    Returns the pairs' host bits (golden, test), the device pairs (views) and
+    the flat device test buffer."""
     es = 4 if code == 0 else 2
     starts, pos = [], 0
     for k, n in enumerate(sizes):
@@ -155,6 +157,9 @@ def _packed(code: int, sizes, seed: int, align: int, gap: int, offsets=None):
     rng = np.random.default_rng(seed)
     gflat = float_to_bits(rng.standard_normal(total), code).copy()
     tflat = float_to_bits(_bits_to_f64(gflat, code) * (1 + 1e-3 * rng.standard_normal(total)), code).copy()
+    if specials:
+        sp = np.array(list(_SPECIALS[code].values()), dtype=NP_BITS[code])
+        tflat[rng.choice(total, specials, replace=False)] = sp[rng.integers(0, sp.size, specials)]
     gdev, tdev = to_device(gflat, code), to_device(tflat, code)
     pairs = [(gdev[s0:s0 + n], tdev[s0:s0 + n]) for n, s0 in zip(sizes, starts)]
     hosts = [(gflat[s0:s0 + n].copy(), tflat[s0:s0 + n].copy()) for n, s0 in zip(sizes, starts)]
@@ -202,18 +207,13 @@ def test_fused_two_chunk_blocks(code):
         sizes.append(cycle[len(sizes) % len(cycle)])
     nchunks = sum(chunk_count(n) for n in sizes)
     assert nchunks >= TWO_CHUNK_MIN
-    hosts, pairs, tflat = _packed(code, sizes, seed=5100 + code, align=256, gap=256)
-    _, pairs2, tflat2 = _packed(code, sizes, seed=5100 + code, align=256, gap=256)
+    hosts, pairs, tflat = _packed(code, sizes, seed=5100 + code, align=256, gap=256, specials=20000)
+    _, pairs2, tflat2 = _packed(code, sizes, seed=5100 + code, align=256, gap=256, specials=20000)
+    assert torch.equal(tflat.view(TORCH_INT[code]), tflat2.view(TORCH_INT[code]))
     for k in range(0, len(sizes), 13):            # golden not 16-byte aligned
         g = to_device(np.concatenate([hosts[k][0][:1], hosts[k][0]]), code)[1:]
         pairs[k] = (g, pairs[k][1])
         pairs2[k] = (g, pairs2[k][1])
-    rng = np.random.default_rng(77 + code)        # special values in both test copies
-    sp = np.array(list(_SPECIALS[code].values()), dtype=NP_BITS[code])
-    pos = torch.from_numpy(rng.integers(0, tflat.numel(), 20000)).cuda()
-    val = torch.from_numpy(sp[rng.integers(0, sp.size, 20000)].view(np.int32 if code == 0 else np.int16)).cuda()
-    for tf in (tflat, tflat2):
-        tf.view(TORCH_INT[code])[pos] = val
     seeds = [synth.inject_seed(15, 10 * k + code) for k in range(len(sizes))]
     mask = {0: 0xFFFFFFFF, 1: 0xFFFF, 2: 0xFFFF}[code]
     sample = sorted({0, 1, 5, len(sizes) - 1, *range(13, len(sizes), 151)})
@@ -240,8 +240,9 @@ def test_fused_packed_offsets(code):
             kw = dict(align=es, gap=0, offsets=[[es, 16, 64, 100][k % 4] for k in range(len(sizes))])
         else:
             kw = dict(align=128, gap=128)
-        _, pairs, tflat = _packed(code, sizes, seed=6200 + code, **kw)
-        _, pairs2, tflat2 = _packed(code, sizes, seed=6200 + code, **kw)
+        _, pairs, tflat = _packed(code, sizes, seed=6200 + code, specials=300, **kw)
+        _, pairs2, tflat2 = _packed(code, sizes, seed=6200 + code, specials=300, **kw)
+        assert torch.equal(tflat.view(TORCH_INT[code]), tflat2.view(TORCH_INT[code]))
         seeds = [synth.inject_seed(16, 10 * k + code) for k in range(len(sizes))]
         for rate in (1.0, 0.3):
             path = "fused" if layout == "private" else "two launches"

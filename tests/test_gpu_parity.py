@@ -317,7 +317,7 @@ def test_workload4_replay():
     give the closed form of identical tensors.  Single async calls on one
     stream give the same records (30 calls)."""
     G = synth.config4_golden("cuda")
-    gb = to_host_bits(G)
+    gb = to_host_bits(G).reshape(-1)
     calls = synth.CONFIG4_CALLS
     tests = [G.clone() for _ in range(calls)]
     inj = [c for c in range(calls) if synth.config4_injected(c)]
@@ -326,11 +326,12 @@ def test_workload4_replay():
                                for c in inj])
     recs = P.signature_batched([(G, T) for T in tests], synth.BINS, synth.THRESHOLDS)
     log(f"  workload 4: {sum(counts)} flips in {len(inj)} injected calls")
-    G16 = G.view(torch.int16)
+    G16 = G.view(torch.int16).view(-1)
     diffs = {}
     for c in inj:                                  # flipped positions and bits on the device
-        idx = torch.nonzero(tests[c].view(torch.int16) != G16).flatten()
-        diffs[c] = (idx.cpu().numpy(), tests[c].view(torch.int16).flatten()[idx].cpu().numpy().view(np.uint16))
+        t16 = tests[c].view(torch.int16).view(-1)
+        idx = torch.nonzero(t16 != G16).flatten()
+        diffs[c] = (idx.cpu().numpy(), t16[idx].cpu().numpy().view(np.uint16))
 
     def ref(c):
         tb = gb.copy()
