@@ -19,7 +19,12 @@ Prints ONE JSON line on stdout (everything else goes to stderr):
             duration from HIP events on its stream, against the 8 TB/s HBM
             peak; traffic from the committed rocprofv3 counter summary when it
             was taken on the current kernel source
-  cpu_baseline  the CPU oracle on a bounded sample of the same workload
+  cpu_baseline  the CPU oracle on a bounded sample of the same workload, in
+            equal element slices over the host share of one GPU (16 cores)
+  other_workloads  the other paper-shaped workloads (activations with bf16
+            rounding, the GPT-1.3B checkpoint, the 1000-call f16 replay), one
+            step each (their injections, then the batched signature), each
+            with its chunk pass's fraction of the HBM peak
 
 Also reported: the read ceiling of the same box (peat_stream_read over a
 16 GiB buffer with the chunk pass's access pattern) and the signature chunk
@@ -189,31 +194,63 @@ WORKLOADS = {"5": Llama7B, "3": GPT13B, "2": Activations, "4": Replay, "1": Sing
 
 
 # ---------------------------------------------------------------------------
-def cpu_baseline(wl: Workload, max_threads: int):
-    """The oracle, as it stands, on the workload's sampled pairs: host copies
-    of the device bytes, one step per pair (the oracle's injection of the
-    test tensor when the workload injects it, then its signature) on a thread
-    pool (ctypes releases the GIL).  Returns GB/s of golden+test bytes signed."""
+def host_share() -> int:
+    """CPU cores this process may use: its affinity set, capped at the 16-core
+    host share that goes with one GPU."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(wl: Workload, threads: int, target_bytes: float = 12e9):
+    """The oracle, as it stands, on a bounded sample of the workload: host
+    copies of the sampled pairs' device bytes (about target_bytes of golden +
+    test), cut into equal element slices, one per thread (ctypes releases the
+    GIL), so every core works for the whole timed span.  Each slice is one
+    oracle step on its own: the oracle's injection of the test slice (with its
+    pair's seed, rate and mask) when the workload injects that pair, then the
+    oracle's signature of the slice -- the per-element work of the real step.
+    Returns GB/s of golden+test bytes signed."""
     import numpy as np
     import oracle
     from tests.parity import to_host_bits
 
     inj = {id(T): (seed, rate, mask) for T, seed, rate, mask in wl.inject_items(0)}
-    host = []
+    host, nbytes = [], 0
     t0 = time.time()
     for k in wl.sample:
+        if nbytes >= target_bytes:
+            break
         G, T = wl.pairs[k]
         code = {wl.torch.float32: 0, wl.torch.float16: 1, wl.torch.bfloat16: 2}[G.dtype]
-        host.append((to_host_bits(G), to_host_bits(T), code, inj.get(id(T))))
+        host.append((k, to_host_bits(G).reshape(-1), to_host_bits(T).reshape(-1), code, inj.get(id(T))))
+        nbytes += G.numel() * G.element_size() * 2
     copy_s = time.time() - t0
-    nbytes = sum(g.nbytes + t.nbytes for g, t, _, _ in host)
+    # equal element slices over the sample (slices never straddle two pairs'
+    # byte arrays: each slice is cut from one pair, the last one of a pair may
+    # be shorter)
+    elems = sum(g.size for _, g, _, _, _ in host)
+    per = -(-elems // threads)
+    slices = []
+    for k, g, t, code, spec in host:
+        for a in range(0, g.size, per):
+            slices.append((g[a:a + per], t[a:a + per].copy(), code, spec))
+    slices.sort(key=lambda x: -x[0].size)
 
     def one(g, t, code, spec):
         if spec is not None:
             oracle.inject(t, dtype=code, seed=spec[0], rate=spec[1], mask=spec[2])
         oracle.signature(g, t, dtype=code)
-    threads = max(1, min(max_threads, len(host), os.cpu_count() or 1))
-    work = list(range(len(host)))
+
+    # one core, one slice: the oracle's per-core rate
+    g1, t1, c1, s1 = slices[-1]
+    t0 = time.time()
+    one(g1, t1.copy(), c1, s1)
+    per_core = (g1.nbytes + t1.nbytes) / (time.time() - t0) / 1e9
+
+    work = list(range(len(slices)))
     lock = threading.Lock()
 
     def worker():
@@ -221,14 +258,8 @@ def cpu_baseline(wl: Workload, max_threads: int):
             with lock:
                 if not work:
                     return
-                k = work.pop(0)
-            one(*host[k])
-
-    # one core, one pair: per-core rate of the oracle
-    g1, t1, c1, s1 = host[0]
-    t0 = time.time()
-    one(g1, t1.copy(), c1, s1)
-    per_core = (g1.nbytes + t1.nbytes) / (time.time() - t0) / 1e9
+                j = work.pop(0)
+            one(*slices[j])
 
     t0 = time.time()
     ths = [threading.Thread(target=worker) for _ in range(threads)]
@@ -239,11 +270,12 @@ def cpu_baseline(wl: Workload, max_threads: int):
     dt = time.time() - t0
     del np
     return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "per_core_value": round(per_core, 3),
-            "sample": f"{len(host)} of {len(wl.pairs)} pairs ({nbytes / 1e9:.2f} GB: "
-                      f"{', '.join(str(k) for k in wl.sample)}), oracle "
-                      f"{'injection + ' if any(h[3] for h in host) else ''}signature, {dt:.1f} s wall on "
-                      f"{threads} threads, D2H copy {copy_s:.1f} s not counted"}
+            "per_core_value": round(per_core, 3), "os_cpu_count": os.cpu_count(),
+            "sample": f"{len(host)} of {len(wl.pairs)} pairs ({nbytes / 1e9:.2f} GB: pairs "
+                      f"{', '.join(str(h[0]) for h in host)}) cut into {len(slices)} slices of at most {per} "
+                      f"elements, one oracle step per slice ({'injection + ' if any(h[4] for h in host) else ''}"
+                      f"signature), {dt:.1f} s wall on {threads} threads ({threads} of os.cpu_count() = "
+                      f"{os.cpu_count()}: the host share of one GPU), D2H copy {copy_s:.1f} s not counted"}
 
 
 def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
@@ -396,6 +428,76 @@ def read_ceiling(torch, P, stream, gib: int = 16, reps: int = 5):
             "kernel": "peat_stream_read (16-byte nontemporal buffer loads, 2 MiB per 256-thread block)"}
 
 
+def time_steps(torch, P, stream, step, first: int, warmup: int, steps: int, classes):
+    """warmup untimed steps, then steps timed ones (first, first + 1, ...)
+    bracketed by events on the stream: total ms, sorted step times, and per
+    kernel class (ms per launch, launches) from the library's HIP events."""
+    for s in range(first, first + warmup):
+        step(s)
+    torch.cuda.synchronize()
+    P.profile_enable(True)
+    for k in classes:
+        P.profile_read(k)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for j, s in enumerate(range(first + warmup, first + warmup + steps)):
+        step(s)
+        evs[j + 1].record(stream)
+    torch.cuda.synchronize()
+    total = evs[0].elapsed_time(evs[-1])
+    step_ms = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(steps))
+    P.profile_enable(False)
+    per = {}
+    for k in classes:
+        ms, n = P.profile_read(k)
+        per[k] = (ms / max(1, n), n)
+    return total, step_ms, per
+
+
+def workload_leg(torch, P, synth, key: str, stream, steps: int, warmup: int):
+    """One step of another workload (its injections, then the batched
+    signature of every pair), timed like the main step; the chunk pass's
+    roofline fraction from its own kernel events."""
+    t0 = time.time()
+    wl = WORKLOADS[key](torch, P, synth)
+    torch.cuda.synchronize()
+    gen_s = time.time() - t0
+    prep = P.PreparedPairs(wl.pairs)
+    d_out = torch.empty(len(wl.pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    d_counts = torch.empty(max(1, len(wl.items)), dtype=torch.int64, device="cuda")
+    items = [P.PreparedItems(wl.inject_items(s)) for s in range(warmup + steps)] if wl.items else []
+
+    def step(s):
+        if wl.items:
+            P.inject_batched_async(items[s], d_counts, stream=stream)
+        P.signature_batched_async(prep, d_out, synth.BINS, synth.THRESHOLDS, stream=stream)
+
+    total, step_ms, per = time_steps(torch, P, stream, step, 0, warmup, steps,
+                                     (P.K_SIG_CHUNK, P.K_SIG_FINALIZE, P.K_INJECT, P.K_INJECT_SUM))
+    nbytes = wl.bytes_signed()
+    ms = total / steps
+    chunk = per[P.K_SIG_CHUNK][0]
+    out = {"description": wl.description, "pairs": len(wl.pairs), "bytes_signed_per_step": nbytes,
+           "step": "batched injection of the injected calls + batched signature of every pair" if wl.items
+           else "batched signature of every pair",
+           "ms_per_step": round(ms, 4), "GBps": round(nbytes / (ms / 1e3) / 1e9, 1),
+           "step_ms": {"median": round(step_ms[len(step_ms) // 2], 4), "min": round(step_ms[0], 4),
+                       "max": round(step_ms[-1], 4)},
+           "kernels_ms_per_step": {"sig_chunk": round(chunk, 4), "sig_finalize": round(per[P.K_SIG_FINALIZE][0], 4),
+                                   "inject": round(per[P.K_INJECT][0], 4) if wl.items else 0.0,
+                                   "inject_sum": round(per[P.K_INJECT_SUM][0], 4) if wl.items else 0.0},
+           "roofline": {"bound": "hbm", "kernel": "sig_chunk", "achieved": round(nbytes / (chunk / 1e3) / 1e9, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(nbytes / (chunk / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "traffic": committed_traffic(wl.name)},
+           "generated_s": round(gen_s, 1)}
+    log(f"  {wl.name}: step {ms:.3f} ms, chunk pass {chunk:.3f} ms = {out['roofline']['frac']:.3f} of HBM peak")
+    del wl, prep, d_out, d_counts, items
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_calibration(torch, gib: int, reps: int):
     """A plain device copy of known size, for scaling FETCH_SIZE/WRITE_SIZE."""
     n = gib * (1 << 30) // 4
@@ -416,13 +518,15 @@ def main():
     ap.add_argument("--separate", action="store_true",
                     help="time the step as two calls (injection, then signature) instead of the fused pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-threads", type=int, default=16)
+    ap.add_argument("--cpu-threads", type=int, default=16, help="at most this many (and at most the host share)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="GIB")
     ap.add_argument("--no-read-ceiling", action="store_true")
     ap.add_argument("--no-topk", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--mixed-only", action="store_true", help="only the mixed-precision measurement")
     ap.add_argument("--no-latency", action="store_true")
+    ap.add_argument("--no-others", action="store_true", help="skip the legs of workloads 2, 3 and 4")
+    ap.add_argument("--other-steps", type=int, default=5, help="timed steps of each other workload")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -470,32 +574,8 @@ def main():
 
     classes = (P.K_SIG_CHUNK, P.K_SIG_FINALIZE, P.K_INJECT, P.K_INJECT_SUM, P.K_SIG_INJECT)
 
-    def timed(step, first):
-        """warm-up and timed steps first, first + 1, ...: total ms, sorted step
-        times, per-class (ms per launch, launches)"""
-        for s in range(first, first + args.warmup):
-            step(s)
-        torch.cuda.synchronize()
-        P.profile_enable(True)
-        for k in classes:
-            P.profile_read(k)
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-        torch.cuda.synchronize()
-        evs[0].record(stream)
-        for j, s in enumerate(range(first + args.warmup, first + nsteps_all)):
-            step(s)
-            evs[j + 1].record(stream)
-        torch.cuda.synchronize()
-        total = evs[0].elapsed_time(evs[-1])
-        steps = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps))
-        P.profile_enable(False)
-        per = {}
-        for k in classes:
-            ms, n = P.profile_read(k)
-            per[k] = (ms / max(1, n), n)
-        return total, steps, per
-
-    ms_total, step_ms, per = timed(step_fused if fused else step_separate, 0)
+    ms_total, step_ms, per = time_steps(torch, P, stream, step_fused if fused else step_separate, 0,
+                                        args.warmup, args.steps, classes)
     ms_step = ms_total / args.steps
     nbytes = wl.bytes_signed()
     value = nbytes / (ms_step / 1e3) / 1e9
@@ -504,7 +584,8 @@ def main():
     if fused:
         # the same injections done by the two separate calls, for reference
         # (fresh seeds: steps nsteps_all ... 2 nsteps_all - 1)
-        sep_total, _, sep_per = timed(step_separate, nsteps_all)
+        sep_total, _, sep_per = time_steps(torch, P, stream, step_separate, nsteps_all, args.warmup, args.steps,
+                                           classes)
         chunk_avg = per[P.K_SIG_INJECT][0]
         sig_chunk_avg, inj_avg, isum_avg = sep_per[P.K_SIG_CHUNK][0], sep_per[P.K_INJECT][0], sep_per[P.K_INJECT_SUM][0]
         fin_avg = per[P.K_SIG_FINALIZE][0]
@@ -570,14 +651,25 @@ def main():
         out["read_ceiling"] = rc
     if not args.no_cpu_baseline:
         log("cpu baseline ...")
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
+        out["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_threads, host_share()))
     if not args.no_latency:
         log("single-call latency ...")
         out["latency"] = latency_measure(torch, P, synth, stream)
+    # the main workload's memory is released before the other legs
+    main_key = args.workload
+    del wl, prep_pairs, d_out, d_counts, step_items
+    prepared_items = None
+    torch.cuda.empty_cache()
+    if not args.no_others:
+        out["other_workloads"] = {}
+        for key in ("2", "3", "4"):
+            if key == main_key:
+                continue
+            log(f"workload {key} ...")
+            leg = workload_leg(torch, P, synth, key, stream, args.other_steps, 2)
+            out["other_workloads"][WORKLOADS[key].name] = leg
     if not args.no_mixed:
         log("mixed-precision pairs ...")
-        del wl, prep_pairs, d_out
-        torch.cuda.empty_cache()
         out["mixed_precision"] = mixed_measure(torch, P)
     print(json.dumps(out), flush=True)
 
