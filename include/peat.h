@@ -235,6 +235,31 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count,
                                  const peat_bins_t *bins, const peat_thresholds_t *thresholds,
                                  peat_signature_t *d_outs, void *stream);
 
+/* For callers that cannot allocate memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  The same work and
+ * records (bit-identical) as peat_signature_batched_async on the same
+ * arguments, but every intermediate buffer -- pair descriptors (48 bytes per
+ * pair), chunk map and chunk records (612 bytes per chunk), the first two
+ * parts each rounded up to 256 bytes -- lives in one static device array of
+ * PEAT_NOALLOC_SCRATCH_BYTES that every GPU the library runs on holds until
+ * the process ends.  A pair of n elements has ceil(n / C) chunks, C the
+ * smallest power of two in [2^12, 2^18] that is at least n / 256 (n < 2^22)
+ * or n / 64 (n >= 2^22).  The call makes no device, pinned or host-heap
+ * allocation; the device's one-time set-up does (events, the array's
+ * address), so call peat_init() on each device first when that matters.
+ * pairs is host memory read before the call returns (descriptors travel as
+ * kernel arguments); d_outs is a device array of count records written when
+ * the stream reaches the work.  Every call on one GPU uses the same array
+ * and it keeps the last call's contents (nothing in it needs clearing):
+ * calls on one GPU that can run at the same time (other streams, no ordering
+ * between them) race on it and give wrong records -- order them.
+ * PEAT_EINVAL, before any device access, when a batch needs more than
+ * PEAT_NOALLOC_SCRATCH_BYTES; other errors as peat_signature_batched_async. */
+#define PEAT_NOALLOC_SCRATCH_BYTES (64u << 20)
+int peat_signature_batched_noalloc(const peat_pair_t *pairs, int32_t count,
+                                   const peat_bins_t *bins, const peat_thresholds_t *thresholds,
+                                   peat_signature_t *d_outs, void *stream);
+
 /* One step of the assessment in a single pass over the data: the random bit
  * flips of peat_inject (Section II-B; same generator and decisions) are
  * applied to every pair's test tensor in place, with seed seeds[k], the

@@ -130,6 +130,9 @@ _PROTOS = {
     "peat_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
                                                     ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
                                                     ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_signature_batched_noalloc": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
+                                                      ctypes.POINTER(Bins), ctypes.POINTER(Thresholds),
+                                                      ctypes.c_void_p, ctypes.c_void_p]),
     "peat_inject_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
                                                            ctypes.POINTER(ctypes.c_uint64), ctypes.c_double,
                                                            ctypes.c_uint64, ctypes.POINTER(Bins),
@@ -527,6 +530,23 @@ def signature_batched_async(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 
     _check(lib().peat_signature_batched_async(prep.arr, prep.count, ctypes.byref(b), ctypes.byref(th),
                                               d_out.data_ptr(), _stream_ptr(stream)),
            "peat_signature_batched_async")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def signature_batched_noalloc(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3), stream=None) -> None:
+    """peat_signature_batched_noalloc: as signature_batched_async, with every
+    intermediate buffer in the library's static device scratch array (no
+    allocation by the call).  Calls on one GPU that may overlap race."""
+    prep = pairs if isinstance(pairs, PreparedPairs) else PreparedPairs(pairs)
+    _dev_tensor(d_out, "d_out")
+    if d_out.numel() * d_out.element_size() < prep.count * SIG_BYTES:
+        raise ValueError("d_out too small")
+    b, th = make_bins(bins), make_thresholds(thresholds)
+    _check(lib().peat_signature_batched_noalloc(prep.arr, prep.count, ctypes.byref(b), ctypes.byref(th),
+                                                d_out.data_ptr(), _stream_ptr(stream)),
+           "peat_signature_batched_noalloc")
 
 
 def inject_signature_batched_async(pairs, seeds, rate: float, bitmask: int, d_out, d_counts,

@@ -61,6 +61,7 @@ struct ProfRec {
 
 struct Dev {
     int state = 0;                   // 0 unchecked, 1 ok, <0 error code
+    char *scratch = nullptr;         // this device's copy of `scratch` (device address)
     void *ws = nullptr;
     size_t ws_size = 0;
     hipEvent_t ws_ev = nullptr;
@@ -76,6 +77,12 @@ struct Dev {
 
 Dev g_dev[kMaxDevices];
 
+// Scratch of peat_signature_batched_noalloc: pair descriptors, chunk map and
+// chunk records of one call.  Each device that loads the library holds its
+// own copy until the process ends; host code reaches it only through the
+// address hipGetSymbolAddress returns for the current device (Dev::scratch).
+static __device__ __align__(256) char scratch[PEAT_NOALLOC_SCRATCH_BYTES];
+
 int current_dev(Dev **out) {
     int id = 0;
     HIP_OR_FAIL(hipGetDevice(&id));
@@ -90,6 +97,11 @@ int current_dev(Dev **out) {
             HIP_OR_FAIL(hipEventCreateWithFlags(&d.ws_ev, hipEventDisableTiming));
             for (int k = 0; k < kSlots; ++k)
                 HIP_OR_FAIL(hipEventCreateWithFlags(&d.slot[k].ev, hipEventDisableTiming));
+            // this device's copy of the static scratch array (device `id` is current)
+            void *p = nullptr;
+            HIP_OR_FAIL(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+            if (!p) return fail(PEAT_EHIP, "no address for the scratch array on device %d", id);
+            d.scratch = static_cast<char *>(p);
             d.state = 1;
         }
     }
@@ -290,6 +302,24 @@ int build_descs(const peat_mixed_pair_t *pairs, int32_t count, std::vector<SigDe
     return PEAT_OK;
 }
 
+// The bins and closeness tests of a signature launch.
+void set_bins_thr(SigParams &P, const peat_bins_t &bins, const peat_thresholds_t &thr) {
+    P.lo = bins.lo_log2;
+    P.hi = bins.hi_log2;
+    P.nbins = bins.nbins;
+    P.nthr = thr.count;
+    P.nthr_pad = thr.count <= 2 ? 2 : (thr.count <= 4 ? 4 : 8);
+    P.thr_min = HUGE_VAL;
+    P.any_rtol = 0;
+    P.pad = 0;
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) {
+        P.thr[j] = j < thr.count ? thr.abs_tol[j] : HUGE_VAL;
+        P.rthr[j] = j < thr.count ? thr.rel_tol[j] : 0.0;
+        if (P.rthr[j] != 0.0) P.any_rtol = 1;
+        if (P.thr[j] < P.thr_min) P.thr_min = P.thr[j];
+    }
+}
+
 // Common core of every signature call.  When host_outs is set the records go
 // through workspace + pinned staging and the call waits for them.  With inj
 // (one InjDesc per pair, same-type pairs) the chunk pass first injects the
@@ -345,20 +375,7 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_desc + b_inj + b_map + b_part) : d_outs;
     P.inj_counts = inj ? d_counts : nullptr;
     P.count = count;
-    P.lo = bins->lo_log2;
-    P.hi = bins->hi_log2;
-    P.nbins = bins->nbins;
-    P.nthr = thr->count;
-    P.nthr_pad = thr->count <= 2 ? 2 : (thr->count <= 4 ? 4 : 8);
-    P.thr_min = HUGE_VAL;
-    P.any_rtol = 0;
-    P.pad = 0;
-    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) {
-        P.thr[j] = j < thr->count ? thr->abs_tol[j] : HUGE_VAL;
-        P.rthr[j] = j < thr->count ? thr->rel_tol[j] : 0.0;
-        if (P.rthr[j] != 0.0) P.any_rtol = 1;
-        if (P.thr[j] < P.thr_min) P.thr_min = P.thr[j];
-    }
+    set_bins_thr(P, *bins, *thr);
 
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;
@@ -793,6 +810,112 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     return PEAT_OK;
 }
 
+// ---- signatures without allocation -------------------------------------------
+// Pair descriptors reach the scratch array as kernel arguments, kFillDescs per
+// launch (the launch copies its arguments, so no host buffer has to outlive
+// the call and nothing is staged through pinned memory); each block writes
+// one descriptor and its pair's entries of the chunk map.
+constexpr int kFillDescs = 32;
+struct DescBatch {
+    SigDesc d[kFillDescs];
+    int32_t first;                   // pair index of d[0]
+    int32_t count;                   // descriptors used
+};
+
+__global__ void __launch_bounds__(kBlock) noalloc_fill(DescBatch b, SigDesc *descs, int32_t *chunk_pair) {
+    const int j = blockIdx.x;
+    if (j >= b.count) return;
+    const SigDesc &sd = b.d[j];
+    if (threadIdx.x == 0) descs[b.first + j] = sd;
+    for (int32_t c = threadIdx.x; c < sd.nchunks; c += kBlock) chunk_pair[sd.first_chunk + c] = b.first + j;
+}
+
+// peat_signature_batched_async with every intermediate buffer in `scratch`:
+// descriptors | chunk map | chunk records.  Host work is validation, two
+// scans over the pairs and the launches; no heap, pinned or device memory is
+// allocated (the device's one-time set-up in current_dev aside).  The chunk
+// records need no clearing: the chunk pass writes every field the finalize
+// reads, so what a previous call left in the array does not matter.
+int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                           const peat_thresholds_t *thr, peat_signature_t *d_outs, hipStream_t s) {
+    if (count < 0) return fail(PEAT_EINVAL, "count < 0");
+    if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
+    int rc = check_bins_thr(bins, thr);
+    if (rc) return rc;
+    // scan 1: validation and the chunks of each kind (same-type kinds only)
+    int64_t per_kind[kKinds] = {};
+    for (int k = 0; k < count; ++k) {
+        if ((rc = check_pair(pairs[k], k))) return rc;
+        const int64_t n = pairs[k].n;
+        per_kind[pair_kind(pairs[k].dtype, pairs[k].dtype)] += (n + (int64_t(1) << chunk_log2_for(n)) - 1) >>
+                                                              chunk_log2_for(n);
+    }
+    if (count == 0) return PEAT_OK;
+    if (!d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+    int64_t range[kKinds + 1];
+    int64_t total = 0;
+    for (int kind = 0; kind < kKinds; ++kind) {
+        range[kind] = total;
+        total += per_kind[kind];
+    }
+    range[kKinds] = total;
+    const size_t b_desc = align_up(sizeof(SigDesc) * (size_t)count);
+    const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
+    const size_t need = b_desc + b_map + sizeof(ChunkPartial) * (size_t)total;
+    if (total > 0x7FFFFFFF || need > (size_t)PEAT_NOALLOC_SCRATCH_BYTES)
+        return fail(PEAT_EINVAL, "batch needs %zu bytes of scratch (%lld chunks, %d pairs); the maximum is %zu",
+                    need, (long long)total, count, (size_t)PEAT_NOALLOC_SCRATCH_BYTES);
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    Dev *dv;
+    if ((rc = current_dev(&dv))) return rc;
+    char *ws = dv->scratch;
+    SigDesc *d_desc = reinterpret_cast<SigDesc *>(ws);
+    int32_t *d_map = reinterpret_cast<int32_t *>(ws + b_desc);
+
+    // scan 2: descriptors, in pair order, numbered by kind as build_descs does
+    int64_t cursor[kKinds];
+    for (int kind = 0; kind < kKinds; ++kind) cursor[kind] = range[kind];
+    DescBatch b;
+    std::memset(&b, 0, sizeof b);
+    b.first = 0;
+    for (int k = 0; k < count; ++k) {
+        SigDesc &sd = b.d[b.count++];
+        const int kind = pair_kind(pairs[k].dtype, pairs[k].dtype);
+        sd.g = pairs[k].golden;
+        sd.t = pairs[k].test;
+        sd.n = pairs[k].n;
+        sd.dtype = (int16_t)pairs[k].dtype;
+        sd.tdtype = (int16_t)pairs[k].dtype;
+        sd.chunk_log2 = chunk_log2_for(sd.n);
+        sd.nchunks = (int32_t)((sd.n + (int64_t(1) << sd.chunk_log2) - 1) >> sd.chunk_log2);
+        sd.first_chunk = cursor[kind];
+        cursor[kind] += sd.nchunks;
+        sd.aligned = ((reinterpret_cast<uintptr_t>(sd.g) | reinterpret_cast<uintptr_t>(sd.t)) & 15) == 0;
+        if (b.count == kFillDescs || k + 1 == count) {
+            hipLaunchKernelGGL(noalloc_fill, dim3((unsigned)b.count), dim3(kBlock), 0, s, b, d_desc, d_map);
+            HIP_OR_FAIL(hipGetLastError());
+            std::memset(&b, 0, sizeof b);
+            b.first = k + 1;
+        }
+    }
+
+    SigParams P;
+    P.chunk_base = 0;
+    P.chunk_count = 0;
+    P.chunk_group = 1;
+    P.descs = d_desc;
+    P.chunk_pair = d_map;
+    P.partials = reinterpret_cast<ChunkPartial *>(ws + b_desc + b_map);
+    P.outs = d_outs;
+    P.inj_counts = nullptr;
+    P.count = count;
+    set_bins_thr(P, *bins, *thr);
+    HIP_OR_FAIL(launch_sig_chunks(P, range, s));
+    HIP_OR_FAIL(launch_sig_finalize(P, s));
+    return PEAT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -854,6 +977,11 @@ int peat_signature_batched_async(const peat_pair_t *pairs, int32_t count, const 
     if (rc) return rc;
     return signature_core(mp.data(), count, bins, thresholds, d_outs, nullptr,
                           static_cast<hipStream_t>(stream));
+}
+
+int peat_signature_batched_noalloc(const peat_pair_t *pairs, int32_t count, const peat_bins_t *bins,
+                                   const peat_thresholds_t *thresholds, peat_signature_t *d_outs, void *stream) {
+    return signature_noalloc_core(pairs, count, bins, thresholds, d_outs, static_cast<hipStream_t>(stream));
 }
 
 int peat_inject_signature_batched_async(const peat_pair_t *pairs, int32_t count, const uint64_t *seeds,
