@@ -40,7 +40,7 @@ F32, F16, BF16, F64 = 0, 1, 2, 3
 _DTYPE_CODE = {np.dtype(np.float32): F32, np.dtype(np.float16): F16}
 
 OK, EINVAL, EDTYPE, EBITMASK, ERATE, ENOMEM = 0, -1, -2, -3, -4, -6
-MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN = 0, 1, 2, 3
+MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN, MODEL_UNIFORM = 0, 1, 2, 3, 4
 MAX_POSITIONS = 4096
 
 
@@ -386,8 +386,9 @@ def topk_rc(n, code, num, den) -> int:
 
 def inject_model(x: np.ndarray, *, dtype: int | None = None, seed: int, rate: float, model: int,
                  mask: int = 0) -> int:
-    """Rate-mode error model in place (0 bit flip, 1 zero, 3 NaN); returns the
-    number of chosen elements (or a negative code)."""
+    """Rate-mode error model in place (0 bit flip, 1 zero, 2 a value of the
+    uncorrupted tensor at a random index, 3 NaN, 4 a uniformly random bit
+    pattern); returns the number of chosen elements (or a negative code)."""
     if not x.flags.c_contiguous or not x.flags.writeable:
         raise ValueError("inject_model needs a writeable C-contiguous array")
     code = _code(x, dtype)

@@ -670,6 +670,7 @@ int oracle_sizeof_topk(void) { return (int)sizeof(oracle_topk_t); }
 #define ORACLE_MODEL_ZERO 1
 #define ORACLE_MODEL_VALUE 2
 #define ORACLE_MODEL_NAN 3
+#define ORACLE_MODEL_UNIFORM 4
 #define ORACLE_MAX_POSITIONS 4096
 
 /* The quiet NaN written by the NaN model: sign 0, exponent all ones, top
@@ -694,19 +695,44 @@ static uint32_t model_bits(int model, int dtype, uint32_t old, uint64_t seed, in
     return old ^ (1u << chosen_bit(seed, i, mask));
 }
 
+/* The random draws of the value models at a rate for element i: block i of
+ * stream 4.  Its 64-bit word 0, W, gives the source index floor(W n / 2^64)
+ * of the tensor-distribution model; its word 2 (32 bits), cut to the type's
+ * width, is the uniform model's bit pattern. */
+static int64_t value_source(uint64_t seed, int64_t i, int64_t n) {
+    uint32_t V[4];
+    philox_seeded(seed, (uint64_t)i, 4, V);
+    return (int64_t)(((unsigned __int128)block_word64(V, 0) * (uint64_t)n) >> 64);
+}
+static uint32_t uniform_bits(uint64_t seed, int64_t i, int dtype) {
+    uint32_t V[4];
+    philox_seeded(seed, (uint64_t)i, 4, V);
+    return dtype == ORACLE_F32 ? V[2] : (V[2] & 0xFFFFu);
+}
+
 /* Rate mode: the elements oracle_inject would flip (U_i < T, every element
  * when rate >= 1) are set to +0 (model 1), to the canonical quiet NaN
- * (model 3) or bit-flipped (model 0, identical to oracle_inject).  The
- * mask is used by the bit-flip model only.  Returns the number of chosen
- * elements or a negative error code. */
+ * (model 3), bit-flipped (model 0, identical to oracle_inject), to a
+ * uniformly random bit pattern of the type (model 4), or (model 2) to the
+ * value the uncorrupted tensor -- the tensor as it was before the call --
+ * holds at a uniformly random index, i.e. a value drawn from the tensor's
+ * own distribution.  The mask is used by the bit-flip model only.  Returns
+ * the number of chosen elements or a negative error code. */
 int64_t oracle_inject_model(void *x, int64_t n, int dtype, uint64_t seed, double rate, int model,
                             uint64_t mask) {
-    if (!dtype_width(dtype)) return ORACLE_EDTYPE;
-    if (model != ORACLE_MODEL_BITFLIP && model != ORACLE_MODEL_ZERO && model != ORACLE_MODEL_NAN)
-        return ORACLE_EINVAL;
+    int width = dtype_width(dtype);
+    if (!width) return ORACLE_EDTYPE;
+    if (model < ORACLE_MODEL_BITFLIP || model > ORACLE_MODEL_UNIFORM) return ORACLE_EINVAL;
     int rc = check_inject(dtype, rate, model == ORACLE_MODEL_BITFLIP ? mask : 1);
     if (rc) return rc;
     if (n < 0 || (n > 0 && !x)) return ORACLE_EINVAL;
+    /* the value model reads its sources from a copy taken before any write */
+    void *orig = NULL;
+    if (model == ORACLE_MODEL_VALUE && n > 0) {
+        orig = malloc((size_t)n * (size_t)(width / 8));
+        if (!orig) return ORACLE_EINVAL;
+        memcpy(orig, x, (size_t)n * (size_t)(width / 8));
+    }
     int all;
     uint64_t T = oracle_rate_threshold(rate, &all);
     int64_t count = 0;
@@ -715,9 +741,17 @@ int64_t oracle_inject_model(void *x, int64_t n, int dtype, uint64_t seed, double
         if ((i & 15) == 0) philox_seeded(seed, (uint64_t)i >> 4, 0, A);
         if ((i & 1) == 0) philox_seeded(seed, (uint64_t)i >> 1, 1, B);
         if (!(all || uniform_of(A, B, i) < T)) continue;
-        store_bits(x, i, dtype, model_bits(model, dtype, element_bits(x, i, dtype), seed, i, mask));
+        uint32_t v;
+        if (model == ORACLE_MODEL_VALUE)
+            v = element_bits(orig, value_source(seed, i, n), dtype);
+        else if (model == ORACLE_MODEL_UNIFORM)
+            v = uniform_bits(seed, i, dtype);
+        else
+            v = model_bits(model, dtype, element_bits(x, i, dtype), seed, i, mask);
+        store_bits(x, i, dtype, v);
         ++count;
     }
+    free(orig);
     return count;
 }
 
@@ -726,19 +760,22 @@ int64_t oracle_inject_model(void *x, int64_t n, int dtype, uint64_t seed, double
  * index p_j = floor(W0 * n / 2^64); the positions are the first num_pos
  * distinct p_j in order of appearance.  Position m (drawn at j) becomes +0
  * (model 1), the canonical NaN (model 3), a bit flip with the rate mode's bit
- * rule (model 0), or (model 2, random value) the uncorrupted tensor's value
- * at index floor(W1 * n / 2^64) -- a value drawn from the tensor's own
- * distribution.  0 <= num_pos <= min(n, 4096).  positions (optional) gets
- * the positions in order.  Returns num_pos or a negative error code. */
+ * rule (model 0), the low bits (the type's width) of W1 as a uniformly
+ * random bit pattern (model 4), or (model 2, random value) the uncorrupted
+ * tensor's value at index floor(W1 * n / 2^64) -- a value drawn from the
+ * tensor's own distribution.  0 <= num_pos <= min(n, 4096).  positions
+ * (optional) gets the positions in order.  Returns num_pos or a negative
+ * error code. */
 int64_t oracle_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed, int model,
                                  int64_t num_pos, uint64_t mask, int64_t *positions) {
     int width = dtype_width(dtype);
     if (!width) return ORACLE_EDTYPE;
-    if (model < ORACLE_MODEL_BITFLIP || model > ORACLE_MODEL_NAN) return ORACLE_EINVAL;
+    if (model < ORACLE_MODEL_BITFLIP || model > ORACLE_MODEL_UNIFORM) return ORACLE_EINVAL;
     if (model == ORACLE_MODEL_BITFLIP && (mask == 0 || (mask >> width) != 0)) return ORACLE_EBITMASK;
     if (n < 0 || num_pos < 0 || num_pos > n || num_pos > ORACLE_MAX_POSITIONS) return ORACLE_EINVAL;
     if (num_pos > 0 && !x) return ORACLE_EINVAL;
     int64_t pos[ORACLE_MAX_POSITIONS], src[ORACLE_MAX_POSITIONS];
+    uint32_t ubits[ORACLE_MAX_POSITIONS];
     int64_t m = 0;
     for (uint64_t j = 0; m < num_pos; ++j) {
         uint32_t W[4];
@@ -749,14 +786,16 @@ int64_t oracle_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed, i
         if (seen) continue;
         pos[m] = p;
         src[m] = (int64_t)(((unsigned __int128)block_word64(W, 1) * (uint64_t)n) >> 64);
+        ubits[m] = width == 32 ? W[2] : (W[2] & 0xFFFFu);
         ++m;
     }
     /* every source is read before any position is written */
     uint32_t val[ORACLE_MAX_POSITIONS];
     for (int64_t q = 0; q < num_pos; ++q)
-        val[q] = model == ORACLE_MODEL_VALUE ? element_bits(x, src[q], dtype)
-                                             : model_bits(model, dtype, element_bits(x, pos[q], dtype), seed,
-                                                          pos[q], mask);
+        val[q] = model == ORACLE_MODEL_VALUE     ? element_bits(x, src[q], dtype)
+                 : model == ORACLE_MODEL_UNIFORM ? ubits[q]
+                                                 : model_bits(model, dtype, element_bits(x, pos[q], dtype), seed,
+                                                              pos[q], mask);
     for (int64_t q = 0; q < num_pos; ++q) {
         store_bits(x, pos[q], dtype, val[q]);
         if (positions) positions[q] = pos[q];

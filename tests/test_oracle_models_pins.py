@@ -7,6 +7,11 @@ num_pos corrupted positions):
   bit patterns;
 * the rate-mode zero / NaN models choose exactly the elements the bit-flip
   injector flips (same decisions), and the bit-flip model equals it;
+* the random-value models at a rate against rocRAND's Philox4x32-10: the
+  bit-flip injector's elements take the uncorrupted tensor's value at
+  floor(W n / 2^64) (W from block i of stream 4; distinct values show a
+  gather that reads already written elements) or word 2 of that block as a
+  uniformly random bit pattern; uniform sources;
 * the position mode against rocRAND's Philox4x32-10: the first num_pos
   distinct floor(W0 * n / 2^64) over the blocks of stream 3 (W0, W1 their
   64-bit words), random values from floor(W1 * n / 2^64) of the uncorrupted
@@ -106,9 +111,94 @@ def test_rate_models_choose_the_bitflip_elements(code, rate):
     assert np.array_equal(x, flipped)
 
 
+def _distinct_bits(code, n, seed):
+    """n distinct finite nonzero bit patterns of the type, shuffled."""
+    rng = np.random.default_rng(seed)
+    if code == F32:
+        return rng.permutation(np.arange(0x3F800000, 0x3F800000 + n, dtype=np.uint32))
+    assert n < 0x7C00
+    return rng.permutation(np.arange(1, n + 1, dtype=np.uint16))
+
+
+def _chosen(code, base, seed, rate):
+    """Elements the bit-flip injector chooses (every bit of the type may flip)."""
+    x = base.copy()
+    cnt = oracle.inject(x, dtype=code, seed=seed, rate=rate, mask=0xFFFFFFFF if code == F32 else 0xFFFF)
+    return x != base, cnt
+
+
+def _stream4(seed, idx):
+    """Blocks i of stream 4 from rocRAND's Philox4x32-10: (64-bit word 0, word 2)."""
+    W = philox_ref.seeded(seed, idx, 4).astype(np.uint64)
+    return W[:, 0] | (W[:, 1] << np.uint64(32)), W[:, 2]
+
+
+@pytest.mark.skipif(not philox_ref.available(), reason="hipcc (for rocRAND's header) not found")
+@pytest.mark.parametrize("code", [F32, F16, BF16])
+@pytest.mark.parametrize("rate", [1.0, 0.3, 1e-3])
+def test_rate_value_model_reads_the_uncorrupted_tensor(code, rate):
+    """Random value at a rate (Section II-B; Section V-A draws the value from
+    the target tensor's distribution): the bit-flip injector's elements, and
+    only they, take the value the tensor held before the call at
+    floor(W n / 2^64), W the 64-bit word 0 of block i of stream 4 (rocRAND's
+    Philox).  Every element holds a distinct value, so a source read after
+    another chosen element was written (an in-place gather) shows."""
+    n, seed = 20000, 4242
+    base = _distinct_bits(code, n, 5)
+    chosen, cnt = _chosen(code, base, seed, rate)
+    x = base.copy()
+    assert oracle.inject_model(x, dtype=code, seed=seed, rate=rate, model=oracle.MODEL_VALUE) == cnt
+    idx = np.nonzero(chosen)[0]
+    w0, _ = _stream4(seed, idx)
+    src = np.array([(int(w) * n) >> 64 for w in w0], dtype=np.int64)
+    assert np.array_equal(x[idx], base[src])
+    assert np.array_equal(x[~chosen], base[~chosen])
+    if rate == 1.0:
+        assert cnt == n and (src != np.arange(n)).any()
+
+
+@pytest.mark.skipif(not philox_ref.available(), reason="hipcc (for rocRAND's header) not found")
+@pytest.mark.parametrize("code", [F32, F16, BF16])
+@pytest.mark.parametrize("rate", [1.0, 0.05])
+def test_rate_uniform_model(code, rate):
+    """Uniformly random bit pattern at a rate: word 2 of block i of stream 4,
+    cut to the type's width, at the bit-flip injector's elements."""
+    n, seed = 20000, 77
+    base = _distinct_bits(code, n, 6)
+    chosen, cnt = _chosen(code, base, seed, rate)
+    x = base.copy()
+    assert oracle.inject_model(x, dtype=code, seed=seed, rate=rate, model=oracle.MODEL_UNIFORM) == cnt
+    idx = np.nonzero(chosen)[0]
+    _, w2 = _stream4(seed, idx)
+    want = w2.astype(np.uint32) if code == F32 else (w2 & np.uint64(0xFFFF)).astype(np.uint16)
+    assert np.array_equal(x[idx], want)
+    assert np.array_equal(x[~chosen], base[~chosen])
+
+
+def test_value_model_sources_are_uniform():
+    """Over many seeds at rate 1, the source indices of a 16-element tensor
+    are uniform (chi-square, 15 degrees of freedom) and the bit patterns of
+    the uniform model spread over all 16 bits."""
+    n, seeds = 16, 400
+    counts = np.zeros(n)
+    ones = np.zeros(16)
+    for s in range(seeds):
+        x = np.arange(1, n + 1, dtype=np.float32)
+        assert oracle.inject_model(x, seed=s, rate=1.0, model=oracle.MODEL_VALUE) == n
+        for v in x:
+            counts[int(v) - 1] += 1
+        y = np.zeros(n, np.uint16)
+        oracle.inject_model(y, dtype=F16, seed=s, rate=1.0, model=oracle.MODEL_UNIFORM)
+        ones += ((y[:, None] >> np.arange(16, dtype=np.uint16)) & 1).sum(axis=0)
+    exp = seeds * n / n
+    assert ((counts - exp) ** 2 / exp).sum() < 45.0
+    assert np.all(np.abs(ones / (seeds * n) - 0.5) < 0.05)
+
+
 def test_rate_model_validation():
     x = np.zeros(8, np.float32)
-    assert oracle.inject_model(x, seed=1, rate=0.5, model=oracle.MODEL_VALUE) == oracle.EINVAL
+    assert oracle.inject_model(x, seed=1, rate=0.5, model=oracle.MODEL_VALUE) == 4
+    assert oracle.inject_model(x, seed=1, rate=0.5, model=5) == oracle.EINVAL
     assert oracle.inject_model(x, seed=1, rate=0.5, model=7) == oracle.EINVAL
     assert oracle.inject_model(x, seed=1, rate=float("nan"), model=oracle.MODEL_ZERO) == oracle.ERATE
     assert oracle.inject_model(x, seed=1, rate=0.5, model=oracle.MODEL_BITFLIP, mask=0) == oracle.EBITMASK
@@ -117,8 +207,8 @@ def test_rate_model_validation():
 # ---------------------------------------------------------------------------
 # position mode
 # ---------------------------------------------------------------------------
-def _ref_positions(seed, n, num_pos):
-    pos, src, seen, j = [], [], set(), 0
+def _ref_positions(seed, n, num_pos, with_bits=False):
+    pos, src, bits, seen, j = [], [], [], set(), 0
     while len(pos) < num_pos:
         W = philox_ref.seeded(seed, np.arange(j, j + 256), 3).astype(np.uint64)
         for w in W:
@@ -129,15 +219,16 @@ def _ref_positions(seed, n, num_pos):
                 seen.add(p)
                 pos.append(p)
                 src.append((w1 * n) >> 64)
+                bits.append(int(w[2]))
         j += 256
-    return pos, src
+    return (pos, src, bits) if with_bits else (pos, src)
 
 
 @pytest.mark.skipif(not philox_ref.available(), reason="hipcc (for rocRAND's header) not found")
 @pytest.mark.parametrize("seed", [0, 7, 2 ** 63 + 5])
 @pytest.mark.parametrize("n,num_pos", [(1, 1), (5, 5), (100, 3), (100000, 5), (3000, 1000), (10 ** 9, 4096)])
 def test_positions_against_rocrand_philox(seed, n, num_pos):
-    want_pos, want_src = _ref_positions(seed, n, num_pos)
+    want_pos, want_src, want_bits = _ref_positions(seed, n, num_pos, with_bits=True)
     assert len(set(want_pos)) == num_pos and all(0 <= p < n for p in want_pos)
     if n > 10 ** 6:
         # positions only: an oracle call on a dummy tensor is not needed to
@@ -145,7 +236,8 @@ def test_positions_against_rocrand_philox(seed, n, num_pos):
         return
     rng = np.random.default_rng(seed % 1000)
     x0 = (rng.random(n) + 1.0).astype(np.float32)
-    for model in (oracle.MODEL_ZERO, oracle.MODEL_NAN, oracle.MODEL_VALUE, oracle.MODEL_BITFLIP):
+    for model in (oracle.MODEL_ZERO, oracle.MODEL_NAN, oracle.MODEL_VALUE, oracle.MODEL_BITFLIP,
+                  oracle.MODEL_UNIFORM):
         x = x0.copy()
         rc, pos = oracle.corrupt_positions(x, seed=seed, model=model, num_pos=num_pos, mask=0x7FFFFF)
         assert rc == num_pos and pos == want_pos
@@ -158,6 +250,8 @@ def test_positions_against_rocrand_philox(seed, n, num_pos):
             assert np.all(x[pos].view(np.uint32) == 0x7FC00000)
         elif model == oracle.MODEL_VALUE:
             assert np.array_equal(x[pos].view(np.uint32), x0[want_src].view(np.uint32))
+        elif model == oracle.MODEL_UNIFORM:
+            assert np.array_equal(x[pos].view(np.uint32), np.array(want_bits, np.uint32))
         else:
             d = x[pos].view(np.uint32) ^ x0[pos].view(np.uint32)
             assert np.all((d & (d - 1)) == 0) and np.all(d != 0) and np.all((d & ~np.uint32(0x7FFFFF)) == 0)
@@ -187,6 +281,7 @@ def test_position_edge_cases():
     y = x.copy()
     assert oracle.corrupt_positions(y, seed=3, model=oracle.MODEL_ZERO, num_pos=9)[0] == oracle.EINVAL
     assert oracle.corrupt_positions(y, seed=3, model=9, num_pos=1)[0] == oracle.EINVAL
+    assert oracle.corrupt_positions(y, seed=3, model=5, num_pos=1)[0] == oracle.EINVAL
     assert oracle.corrupt_positions(y, seed=3, model=oracle.MODEL_BITFLIP, num_pos=1, mask=0)[0] == oracle.EBITMASK
     big = np.zeros(5000, np.float32)
     assert oracle.corrupt_positions(big, seed=3, model=oracle.MODEL_ZERO, num_pos=4097)[0] == oracle.EINVAL
