@@ -56,12 +56,13 @@ namespace {
 
 
 constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
-// Fast-path limit on the relative error: an element at or above it (or NaN)
-// sends its vector to the generic path.  A sign change between finite golden
-// and test values gives |t - g| >= |g|, i.e. a relative error of at least 1
-// (less the reciprocal's 2^-48), and a zero golden value gives Inf or NaN, so
-// this one comparison also catches every case the fast path does not handle.
-// Below the limit t lies within a factor 1.25 of g, so:
+// Fast-path limit on the relative error: an element above it (or NaN) sends
+// its vector to the generic path (one exactly at it may take either path;
+// both are exact there).  A sign change between finite golden and test
+// values gives |t - g| >= |g|, i.e. a relative error of at least 1 (less the
+// reciprocal's 2^-48), and a zero golden value gives Inf or NaN, so this one
+// comparison also catches every case the fast path does not handle.  Up to
+// the limit t lies within a factor 1.25 (plus 2^-47) of g, so:
 //   - t - g is exact in the elements' own format (Sterbenz: t/g in [1/2, 2]);
 //     when the difference is formed in binary32 and rounded, it is at least
 //     |g|/2 in magnitude, which this limit rejects, so a fast-path error is
@@ -138,6 +139,26 @@ __device__ __forceinline__ void recip2(const double *x, double *r) {
     r[0] = x[1] * inv;
     r[1] = x[0] * inv;
 }
+// Eight magnitudes of widened f16 values (in [2^-24, 2^16]) from one
+// reciprocal: the product of eight stays within [2^-192, 2^128]; the pair
+// and quad products are exact (at most 44 significant bits) and only the
+// product of all eight rounds, so each result is within about 2^-47.8 of
+// 1/x.  A zero, Inf or NaN among the eight makes all eight NaN or Inf.
+__device__ __forceinline__ void recip8(const double *x, double *r) {
+    const double p01 = x[0] * x[1], p23 = x[2] * x[3], p45 = x[4] * x[5], p67 = x[6] * x[7];
+    const double q0 = p01 * p23, q1 = p45 * p67;
+    const double inv = recip(q0 * q1);
+    const double iq0 = inv * q1, iq1 = inv * q0;
+    const double i01 = iq0 * p23, i23 = iq0 * p01, i45 = iq1 * p67, i67 = iq1 * p45;
+    r[0] = x[1] * i01;
+    r[1] = x[0] * i01;
+    r[2] = x[3] * i23;
+    r[3] = x[2] * i23;
+    r[4] = x[5] * i45;
+    r[5] = x[4] * i45;
+    r[6] = x[7] * i67;
+    r[7] = x[6] * i67;
+}
 
 struct Lane {
     double s_abs, s_rel;           // both paths
@@ -169,7 +190,7 @@ struct Uni {
 };
 
 struct Shared {
-    uint32_t hrow[2048];                   // binary64 exponent field -> slot * kBlock
+    uint8_t hrow[4096];                    // binary64 sign and exponent field -> histogram slot
     // Lane-private 16-bit counters, two per word: word [slot][t mod 128]
     // holds lane t's count in its low half when t < 128 and in its high half
     // otherwise.  The two lanes of a word are in different waves, and a lane
@@ -227,9 +248,21 @@ struct GenAcc {
     }
 };
 
+// Byte address of lane tid's counter word of a histogram slot within
+// sh.hist: slot * (kHistCols * 4) + column * 4, one shift-or given the
+// column's byte offset colb (the slot comes zero-extended from the table).
+__device__ __forceinline__ uint32_t hist_addr(uint32_t slot, uint32_t colb) { return (slot << 9) | colb; }
+static_assert(kHistCols * 4 == 512, "hist_addr shifts the slot by 9");
+__device__ __forceinline__ void hist_bump(Shared &sh, uint32_t addr, int tid) {
+    atomicAdd(reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(sh.hist) + addr), hist_inc(tid));
+}
+// Row of a binary64 value in the table: its sign and exponent field.
+__device__ __forceinline__ uint32_t hist_key(double x) {
+    return (uint32_t)((uint64_t)__double_as_longlong(x) >> 52);
+}
+
 __device__ __forceinline__ void hist_add(Shared &sh, double a, int tid) {
-    const uint32_t E = (uint32_t)(__double_as_longlong(a) >> 52);   // a >= 0: sign bit clear
-    atomicAdd(&sh.hist[sh.hrow[E] + hist_col(tid)], hist_inc(tid));
+    hist_bump(sh, hist_addr(sh.hrow[hist_key(a)], hist_col(tid) * 4u), tid);
 }
 
 // Every case of one pair (NaN, Inf, zero golden, sign change, subnormals).
@@ -372,6 +405,176 @@ __device__ __forceinline__ uint32_t fast_ulp(BG gb, BT tb, double G, double T) {
     }
 }
 
+// Threshold mismatches of a fast-path vector (every element finite, golden
+// nonzero): nothing to count for threshold k while the vector's largest
+// |err| va is at most its absolute tolerance (the allowance atol + |rtol G|
+// is never below atol; padded thresholds are +Inf), so usually no element is
+// compared.
+template <int VEC, int NT, bool RT>
+__device__ __forceinline__ void count_mismatches(Uni &U, const SigParams &P, const double *E, const double *G,
+                                                 double va) {
+    if (__ballot(va > P.thr_min) == 0) return;
+#pragma unroll
+    for (int k = 0; k < NT; ++k) {
+        if (__ballot(va > P.thr[k]) == 0) continue;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            if constexpr (RT) {
+                // torch.isclose's allowance atol + |rtol * G|, rounded step by
+                // step (never NaN here: G is finite and nonzero)
+                const double allowed = __dadd_rn(P.thr[k], __builtin_fabs(__dmul_rn(P.rthr[k], G[j])));
+                U.mism[k] += wave_count(__builtin_fabs(E[j]) > allowed);
+            } else {
+                U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
+            }
+        }
+    }
+}
+
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// vec_fast for same-type 16-bit pairs: eight elements per lane vector, two
+// per 32-bit word, worked on in pairs where the hardware has packed forms:
+//   - f16 difference by one packed subtraction per word.  On the fast path
+//     it is exact (Sterbenz; f16 subnormals are kept), so it equals the
+//     binary32 difference; where it is not exact (t/g outside [1/2, 2], a
+//     sign change, overflow) the relative error is at least 1/4 (or NaN)
+//     and the vector leaves the fast path before any of it is used;
+//   - ULP distances |t - g| of the bit patterns (same sign on the fast
+//     path) by packed max - min, their sum by one 2 x 16-bit dot product per
+//     word and the vector's largest by packed maxima;
+//   - f16 histogram rows from the binary32 error's sign and exponent (an f16
+//     error is 0 or a normal binary32 number, so the exponent is its binade)
+//     through a byte table;
+//   - f16 reciprocals of all eight magnitudes from one hardware estimate.
+// Same decisions, records and maxima as vec_fast.
+template <int DT, int NT, bool RT>
+__device__ __forceinline__ bool vec_fast16(Lane &L, Uni &U, Shared &sh, const SigParams &P,
+                                           const u32x4 &gv, const u32x4 &tv, uint32_t v, uint32_t ib, int tid) {
+    constexpr int VEC = 8;
+    const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
+    const uint32_t tw[4] = {tv.x, tv.y, tv.z, tv.w};
+    float G32[VEC], E32[VEC];
+    double G[VEC], E[VEC], R[VEC], AG[VEC], IG[VEC];
+    uint32_t d[4], row[VEC];
+    uint64_t mflag = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if constexpr (DT == PEAT_F16) {
+            const f16x2 gh = __builtin_bit_cast(f16x2, gw[q]);
+            const f16x2 eh = __builtin_bit_cast(f16x2, tw[q]) - gh;
+            G32[2 * q] = (float)gh.x;
+            G32[2 * q + 1] = (float)gh.y;
+            E32[2 * q] = (float)eh.x;
+            E32[2 * q + 1] = (float)eh.y;
+        } else {
+            G32[2 * q] = __uint_as_float(gw[q] << 16);
+            G32[2 * q + 1] = __uint_as_float(gw[q] & 0xFFFF0000u);
+            E32[2 * q] = __uint_as_float(tw[q] << 16) - G32[2 * q];
+            E32[2 * q + 1] = __uint_as_float(tw[q] & 0xFFFF0000u) - G32[2 * q + 1];
+        }
+        const u16x2 a = __builtin_bit_cast(u16x2, gw[q]), b = __builtin_bit_cast(u16x2, tw[q]);
+        d[q] = __builtin_bit_cast(uint32_t, (u16x2)(__builtin_elementwise_max(a, b) - __builtin_elementwise_min(a, b)));
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        G[j] = (double)G32[j];
+        E[j] = (double)E32[j];
+        AG[j] = __builtin_fabs(G[j]);
+    }
+    if constexpr (DT == PEAT_F16) {
+        recip8(AG, IG);
+    } else {
+        recip4(AG, IG);
+        recip4(AG + 4, IG + 4);
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        R[j] = __builtin_fabs(E[j]) * IG[j];
+        mflag |= __ballot(!(R[j] <= L.rthr));
+        row[j] = hist_key(E[j]);                      // the table is read after the branch
+    }
+    double va = absmax_f64(E[0], E[1]);
+#pragma unroll
+    for (int j = 2; j < VEC; ++j) va = absmax_f64(va, E[j]);
+    const u16x2 dm = __builtin_elementwise_max(
+        __builtin_elementwise_max(__builtin_bit_cast(u16x2, d[0]), __builtin_bit_cast(u16x2, d[1])),
+        __builtin_elementwise_max(__builtin_bit_cast(u16x2, d[2]), __builtin_bit_cast(u16x2, d[3])));
+    const uint32_t vu = max((uint32_t)dm.x, (uint32_t)dm.y);
+    mflag |= __ballot(va > U.wx_abs);
+    mflag |= __ballot(vu > U.wu);
+    if (mflag != 0) {
+        uint64_t mrare = 0, mcand = 0;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            mrare |= __ballot(!(R[j] < kRareRel));
+            mcand |= __ballot(R[j] > L.rthr);
+        }
+        if (mrare != 0) return true;
+        const uint32_t li0 = ib + (v * kBlock + tid) * VEC;
+        if (mcand != 0) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                if (R[j] > L.rthr) {
+                    const double r = __builtin_fabs(E[j]) / __builtin_fabs(G[j]);   // IEEE quotient
+                    if (r > L.mx_rel) {
+                        L.mx_rel = r;
+                        L.ix_rel = li0 + j;
+                    }
+                }
+            }
+            const double wm = wave_max_uniform(L.mx_rel);
+            L.rthr = __builtin_fmin(wm - wm * kRelMargin, kRareRel);
+        }
+        if (__ballot(va > U.wx_abs) != 0) {
+            U.wx_abs = wave_max_uniform(va);
+            if (va == U.wx_abs) {
+                uint32_t ix = kNone;
+#pragma unroll
+                for (int j = VEC - 1; j >= 0; --j)
+                    if (__builtin_fabs(E[j]) == U.wx_abs) ix = li0 + j;
+                lex_merge(L.gx_abs, L.gi_abs, U.wx_abs, ix);
+            }
+        }
+        if (__ballot(vu > U.wu) != 0) {
+            U.wu = wave_max_uniform_u(vu);
+            if (vu == U.wu) {
+                uint32_t ix = kNone;
+#pragma unroll
+                for (int j = VEC - 1; j >= 0; --j)
+                    if (((d[j >> 1] >> (16 * (j & 1))) & 0xFFFFu) == U.wu) ix = li0 + j;
+                lex_merge(L.gu, L.gi_ulp, U.wu, ix);
+            }
+        }
+    }
+
+    {
+        // the slots' LDS reads first (one round trip), then the counters
+        const uint32_t colb = hist_col(tid) * 4u;
+        uint32_t slot[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) slot[j] = sh.hrow[row[j]];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) hist_bump(sh, hist_addr(slot[j], colb), tid);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) L.s_ulp32 = __builtin_amdgcn_udot2(__builtin_bit_cast(u16x2, d[q]), (u16x2){1, 1},
+                                                                 L.s_ulp32, false);
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        L.s_abs += __builtin_fabs(E[j]);
+        L.s_sq = __builtin_fma(E[j], E[j], L.s_sq);
+        L.s_g2 = __builtin_fma(G[j], G[j], L.s_g2);
+        L.s_ge = __builtin_fma(G[j], E[j], L.s_ge);
+        L.s_rel += R[j];
+    }
+    count_mismatches<VEC, NT, RT>(U, P, E, G, va);
+    U.common += 1;
+    if (U.first == kNone) U.first = v;
+    return false;
+}
+
 // One lane vector of golden and of test (vector number v of the lane's
 // sequence).  Called in wave-uniform control flow with every lane active.
 // Returns true (wave-uniform) when the vector must go to the generic path.
@@ -384,6 +587,7 @@ __device__ __forceinline__ uint32_t fast_ulp(BG gb, BT tb, double G, double T) {
 template <int DG, int DT, int NT, bool RT>
 __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigParams &P,
                                          const u32x4 &gv, const u32x4 &tv, uint32_t v, uint32_t ib, int tid) {
+    if constexpr (DG == DT && Tr<DT>::W == 16) return vec_fast16<DT, NT, RT>(L, U, sh, P, gv, tv, v, ib, tid);
     constexpr int VEC = PairTr<DG, DT>::VEC;
     // both sides fit binary32: the difference is formed there (exact on the
     // fast path) and widened; otherwise in binary64
@@ -423,11 +627,12 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
             E[j] = Tj - G[j];
         }
         R[j] = __builtin_fabs(E[j]) * IG[j];
-        // rare (>= kRareRel or NaN), or a candidate for the max relative error
-        mflag |= __ballot(!(R[j] < L.rthr));
+        // rare (NaN, or at least kRareRel while the filter is there), or a
+        // candidate for the max relative error
+        mflag |= __ballot(!(R[j] <= L.rthr));
         // same sign on the fast path: the ULP distance is |t - g| of the bit patterns
         u[j] = fast_ulp<DG, DT>(gb, tb, G[j], Tj);
-        row[j] = sh.hrow[(uint32_t)(__double_as_longlong(E[j]) >> 52) & 0x7FFu];
+        row[j] = hist_key(E[j]);                      // the table is read after the branch
     }
     double va = absmax_f64(E[0], E[1]);
 #pragma unroll
@@ -492,8 +697,15 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
         }
     }
 
+    {
+        // the slots' LDS reads first (one round trip), then the counters
+        const uint32_t colb = hist_col(tid) * 4u;
+        uint32_t slot[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) atomicAdd(&sh.hist[row[j] + hist_col(tid)], hist_inc(tid));
+        for (int j = 0; j < VEC; ++j) slot[j] = sh.hrow[row[j]];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) hist_bump(sh, hist_addr(slot[j], colb), tid);
+    }
 #pragma unroll
     for (int j = 0; j < VEC; ++j) L.s_ulp32 += u[j];
 #pragma unroll
@@ -504,24 +716,7 @@ __device__ __forceinline__ bool vec_fast(Lane &L, Uni &U, Shared &sh, const SigP
         L.s_ge = __builtin_fma(G[j], E[j], L.s_ge);
         L.s_rel += R[j];
     }
-    // threshold mismatches: nothing to count while the vector's largest
-    // |err| is at most the smallest threshold
-    if (__ballot(va > P.thr_min) != 0) {
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-#pragma unroll
-            for (int k = 0; k < NT; ++k) {
-                if constexpr (RT) {
-                    // torch.isclose's allowance atol + |rtol * G|, rounded step by
-                    // step (never NaN here: G is finite and nonzero)
-                    const double allowed = __dadd_rn(P.thr[k], __builtin_fabs(__dmul_rn(P.rthr[k], G[j])));
-                    U.mism[k] += wave_count(__builtin_fabs(E[j]) > allowed);
-                } else {
-                    U.mism[k] += wave_count(__builtin_fabs(E[j]) > P.thr[k]);
-                }
-            }
-        }
-    }
+    count_mismatches<VEC, NT, RT>(U, P, E, G, va);
     U.common += 1;
     if (U.first == kNone) U.first = v;
     return false;
@@ -1072,7 +1267,8 @@ __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()
     // slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi
     for (int i = tid; i < kHistSlots * kHistCols; i += kBlock) sh.hist[i] = 0;
     const int w = (P.hi - P.lo) / P.nbins;
-    for (int E = tid; E < 2048; E += kBlock) {
+    for (int x = tid; x < 4096; x += kBlock) {
+        const int E = x & 2047;                // either sign: the slot of |value|
         int slot;
         if (E == 0) {
             slot = 0;
@@ -1082,7 +1278,7 @@ __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()
             const int k = E - 1023;            // a in [2^k, 2^(k+1))
             slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
         }
-        sh.hrow[E] = (uint32_t)(slot * kHistCols);
+        sh.hrow[x] = (uint8_t)slot;
     }
     __syncthreads();
     chunk_loop<DG, DT, NT, RT, INJ>(P, sh, descs, chunk_pair, partials, inj);
