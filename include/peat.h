@@ -160,13 +160,16 @@ typedef struct {
     int32_t test_dtype;
 } peat_mixed_pair_t;
 
-/* Error models (Section II-B "Error Models"; Section III-C pseudo-errors). */
+/* Error models (Section II-B "Error Models"; Section III-C pseudo-errors;
+ * Section V-A draws a random value from the target tensor's distribution). */
 typedef enum {
     PEAT_MODEL_BITFLIP = 0, /* toggle one bit of the mask (random bit flip)      */
     PEAT_MODEL_ZERO = 1,    /* set to +0 (random zero)                            */
-    PEAT_MODEL_VALUE = 2,   /* copy of the tensor's value at a random index
-                             * (random value; position mode only)                */
-    PEAT_MODEL_NAN = 3      /* set to the quiet NaN 0x7FC00000 / 0x7E00 / 0x7FC0 */
+    PEAT_MODEL_VALUE = 2,   /* the uncorrupted tensor's value at a random index
+                             * (random value from the tensor's own distribution) */
+    PEAT_MODEL_NAN = 3,     /* set to the quiet NaN 0x7FC00000 / 0x7E00 / 0x7FC0 */
+    PEAT_MODEL_UNIFORM = 4  /* a uniformly random bit pattern of the type
+                             * (random value over the type: may be Inf or NaN)   */
 } peat_model_t;
 
 #define PEAT_MAX_POSITIONS 4096
@@ -176,7 +179,7 @@ typedef struct {
                        * element size (PEAT_EINVAL otherwise) */
     int64_t n;        /* elements, >= 0 */
     int32_t dtype;    /* peat_dtype_t   */
-    int32_t model;    /* peat_model_t: BITFLIP (0), ZERO or NAN */
+    int32_t model;    /* peat_model_t */
     uint64_t seed;
     double rate;      /* error rate per element; >= 1 chooses every element */
     uint64_t bitmask; /* BITFLIP: candidate bits, nonzero, below the type
@@ -362,10 +365,14 @@ int64_t peat_inject(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed,
 
 /* peat_inject with another error model at the same rate (Section II-B):
  * the elements peat_inject would flip (same seed and rate) are set to +0
- * (PEAT_MODEL_ZERO), to the type's quiet NaN (PEAT_MODEL_NAN) or bit-flipped
- * (PEAT_MODEL_BITFLIP, identical to peat_inject).  bitmask is ignored by
- * ZERO and NAN.  Returns the number of chosen elements or a negative code
- * (PEAT_EINVAL for PEAT_MODEL_VALUE, which needs positions). */
+ * (PEAT_MODEL_ZERO), to the type's quiet NaN (PEAT_MODEL_NAN), bit-flipped
+ * (PEAT_MODEL_BITFLIP, identical to peat_inject), to the value the tensor
+ * held before the call at index floor(W * n / 2^64), W the 64-bit word 0 of
+ * block i of stream 4 (PEAT_MODEL_VALUE: a value of the tensor's own
+ * distribution, Section V-A; the library copies the tensor to its workspace
+ * first, n * element size bytes), or to word 2 of that block cut to the
+ * type's width (PEAT_MODEL_UNIFORM).  bitmask is used by BITFLIP only.
+ * Returns the number of chosen elements or a negative code. */
 int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, double rate,
                           int32_t model, uint64_t bitmask);
 
@@ -374,10 +381,11 @@ int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t 
  * takes block j of stream 3 (peat_inject's generator), its 64-bit words W0
  * and W1, and the index floor(W0 * n / 2^64); the positions are the first
  * num_pos distinct indices in order of appearance.  Each becomes +0, the
- * quiet NaN, a bit flip (peat_inject's bit rule for that index), or --
- * PEAT_MODEL_VALUE, a value from the tensor's own distribution -- the
- * uncorrupted tensor's value at floor(W1 * n / 2^64) of the draw that chose
- * it.  positions (host,
+ * quiet NaN, a bit flip (peat_inject's bit rule for that index), the low
+ * bits (the type's width) of W1 as a uniformly random bit pattern
+ * (PEAT_MODEL_UNIFORM), or -- PEAT_MODEL_VALUE, a value from the tensor's
+ * own distribution -- the uncorrupted tensor's value at
+ * floor(W1 * n / 2^64) of the draw that chose it.  positions (host,
  * num_pos entries, may be NULL) receives the positions in order.  Returns
  * num_pos or a negative code (PEAT_EINVAL also for a tensor not aligned to
  * its element size); waits for the device. */

@@ -17,7 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libpeat.so")
 
 F32, F16, BF16, F64 = 0, 1, 2, 3
-MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN = 0, 1, 2, 3
+MODEL_BITFLIP, MODEL_ZERO, MODEL_VALUE, MODEL_NAN, MODEL_UNIFORM = 0, 1, 2, 3, 4
 MAX_POSITIONS = 4096
 OK, EINVAL, EDTYPE, EBITMASK, ERATE, EHIP, ENOMEM, ENODEV = 0, -1, -2, -3, -4, -5, -6, -7
 MAX_THRESHOLDS, MAX_BINS = 8, 64
@@ -593,7 +593,9 @@ def inject(tensor, seed: int, rate: float, bitmask: int, *, dtype: int | None = 
 
 def inject_model(tensor, seed: int, rate: float, model: int, bitmask: int = 0) -> int:
     """peat_inject_model in place: the elements peat_inject would flip are set
-    to zero (MODEL_ZERO), NaN (MODEL_NAN) or bit-flipped (MODEL_BITFLIP)."""
+    to zero (MODEL_ZERO), NaN (MODEL_NAN), bit-flipped (MODEL_BITFLIP), to the
+    tensor's value before the call at a random index (MODEL_VALUE) or to a
+    uniformly random bit pattern (MODEL_UNIFORM)."""
     _dev_tensor(tensor, "tensor")
     n = tensor.numel()
     set_stream()

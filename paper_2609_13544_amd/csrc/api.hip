@@ -403,8 +403,8 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
 int check_item(const peat_inject_item_t &it, int k) {
     if (check_dtype(it.dtype)) return fail(PEAT_EDTYPE, "item %d: unknown dtype %d", k, it.dtype);
     const int width = elem_size(it.dtype) * 8;
-    if (it.model != PEAT_MODEL_BITFLIP && it.model != PEAT_MODEL_ZERO && it.model != PEAT_MODEL_NAN)
-        return fail(PEAT_EINVAL, "item %d: model %d is not BITFLIP, ZERO or NAN", k, it.model);
+    if (it.model < PEAT_MODEL_BITFLIP || it.model > PEAT_MODEL_UNIFORM)
+        return fail(PEAT_EINVAL, "item %d: unknown model %d", k, it.model);
     if (it.model == PEAT_MODEL_BITFLIP && (it.bitmask == 0 || (it.bitmask >> width) != 0))
         return fail(PEAT_EBITMASK, "item %d: bitmask 0x%llx is 0 or has bits at or above bit %d", k,
                     (unsigned long long)it.bitmask, width);
@@ -444,6 +444,8 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
         q.dtype = it.dtype;
         q.popc = __builtin_popcountll(q.mask);
         q.model = it.model;
+        q.src = nullptr;
+        q.reserved = 0;
         q.all = it.rate >= 1.0;
         // T = floor(rate * 2^64): ldexp is exact and the conversion truncates
         q.T = (q.all || it.rate == 0.0) ? 0 : (uint64_t)std::ldexp(it.rate, 64);
@@ -459,9 +461,21 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
     const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
     const size_t b_seg = align_up(sizeof(uint32_t) * (size_t)total);
     const size_t b_out = host_counts ? align_up(sizeof(int64_t) * count) : 0;
+    // the random-value items read their sources from copies of their tensors
+    // taken before the injection kernel writes anything
+    std::vector<size_t> copy_off((size_t)count, 0);
+    size_t b_copy = 0;
+    for (int k = 0; k < count; ++k) {
+        if (descs[k].model != PEAT_MODEL_VALUE || descs[k].nsegs == 0) continue;
+        copy_off[k] = b_copy;
+        b_copy += align_up((size_t)items[k].n * (size_t)elem_size(items[k].dtype));
+    }
+    const size_t o_copy = b_desc + b_map + b_seg + b_out;
 
     char *ws;
-    if ((rc = acquire_ws(d, b_desc + b_map + b_seg + b_out, s, &ws))) return rc;
+    if ((rc = acquire_ws(d, o_copy + b_copy, s, &ws))) return rc;
+    for (int k = 0; k < count; ++k)
+        if (descs[k].model == PEAT_MODEL_VALUE && descs[k].nsegs > 0) descs[k].src = ws + o_copy + copy_off[k];
     Slot *sl;
     if ((rc = acquire_slot(d, b_desc + b_map + b_out, &sl))) return rc;
     char *h = static_cast<char *>(sl->host);
@@ -470,6 +484,11 @@ int inject_core(const peat_inject_item_t *items, int32_t count, int64_t *d_count
     for (int k = 0; k < count; ++k)
         for (int32_t c = 0; c < descs[k].nsegs; ++c) hmap[descs[k].first_seg + c] = k;
     HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+    for (int k = 0; k < count; ++k)
+        if (descs[k].model == PEAT_MODEL_VALUE && descs[k].nsegs > 0)
+            HIP_OR_FAIL(hipMemcpyAsync(const_cast<void *>(descs[k].src), items[k].tensor,
+                                       (size_t)items[k].n * (size_t)elem_size(items[k].dtype),
+                                       hipMemcpyDeviceToDevice, s));
 
     InjParams P;
     P.descs = reinterpret_cast<const InjDesc *>(ws);
@@ -1031,7 +1050,7 @@ int64_t peat_inject_model(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t 
 int64_t peat_corrupt_positions(void *tensor, int64_t n, peat_dtype_t dtype, uint64_t seed, int32_t model,
                                int64_t num_pos, uint64_t bitmask, int64_t *positions) {
     if (check_dtype(dtype)) return fail(PEAT_EDTYPE, "unknown dtype %d", (int)dtype);
-    if (model < PEAT_MODEL_BITFLIP || model > PEAT_MODEL_NAN) return fail(PEAT_EINVAL, "unknown model %d", model);
+    if (model < PEAT_MODEL_BITFLIP || model > PEAT_MODEL_UNIFORM) return fail(PEAT_EINVAL, "unknown model %d", model);
     const int width = elem_size(dtype) * 8;
     if (model == PEAT_MODEL_BITFLIP && (bitmask == 0 || (bitmask >> width) != 0))
         return fail(PEAT_EBITMASK, "bitmask 0x%llx is 0 or has bits at or above bit %d",

@@ -26,7 +26,9 @@ namespace {
 
 constexpr int kQCap = 64 + 32 * 64;   // per-wave queue: < 64 left over + one append of 32 per lane
 
-// The chosen element's new bits: a bit flip, +0 or the type's quiet NaN.
+// The chosen element's new bits: a bit flip, +0, the type's quiet NaN, a
+// value of the tensor before the call (read from the copy d.src) or a
+// uniformly random bit pattern.
 // ATOMIC: the bit flip is one device-scope atomic XOR on the aligned 32-bit
 // word that holds the element, performed in L2 (a 16-bit neighbour in the
 // same word is XORed with zeros, so no other element can lose an update).
@@ -50,12 +52,27 @@ __device__ __forceinline__ void flip(const InjDesc &d, uint64_t i) {
             *p = (uint16_t)(*p ^ (1u << b));
         }
     } else {
-        const bool nan = d.model == PEAT_MODEL_NAN;
-        if (d.dtype == PEAT_F32) {
-            static_cast<uint32_t *>(d.x)[i] = nan ? 0x7FC00000u : 0u;
+        uint32_t v;
+        if (d.model == PEAT_MODEL_VALUE || d.model == PEAT_MODEL_UNIFORM) {
+            // block i of stream 4: word 0 (64 bits) picks the source, word 2
+            // is the uniform bit pattern
+            uint32_t V[4];
+            philox(i, 4, d.seed, V);
+            if (d.model == PEAT_MODEL_VALUE) {
+                const uint64_t s = __umul64hi(block_word64(V, 0), (uint64_t)d.n);
+                v = d.dtype == PEAT_F32 ? static_cast<const uint32_t *>(d.src)[s]
+                                        : static_cast<const uint16_t *>(d.src)[s];
+            } else {
+                v = V[2];
+            }
         } else {
-            static_cast<uint16_t *>(d.x)[i] = (uint16_t)(nan ? (d.dtype == PEAT_F16 ? 0x7E00u : 0x7FC0u) : 0u);
+            const bool nan = d.model == PEAT_MODEL_NAN;
+            v = nan ? (d.dtype == PEAT_F32 ? 0x7FC00000u : (d.dtype == PEAT_F16 ? 0x7E00u : 0x7FC0u)) : 0u;
         }
+        if (d.dtype == PEAT_F32)
+            static_cast<uint32_t *>(d.x)[i] = v;
+        else
+            static_cast<uint16_t *>(d.x)[i] = (uint16_t)v;
     }
 }
 

@@ -1,8 +1,8 @@
 // The paper's other error models (Section II-B "Error Models"; Section III-C
 // pseudo-errors; Section V-A settings) beyond the rate-driven injector:
 //
-//   corrupt_positions  num_pos distinct random positions (random value, zero,
-//                      NaN or bit flip), one block: positions are drawn in
+//   corrupt_positions  num_pos distinct random positions (random value of the
+//                      tensor or of the type, zero, NaN or bit flip), one block: positions are drawn in
 //                      parallel, accepted in draw order through an LDS hash
 //                      set, every source read before any position is written;
 //   cast_round         the FP16 / BF16 error: round-to-nearest-even of an f32
@@ -48,7 +48,9 @@ __global__ void __launch_bounds__(kBlock) corrupt_positions_kernel(void *x, int6
         uint32_t W[4];
         philox(j0 + tid, 3, seed, W);
         cp[tid] = (int64_t)mulhi64(block_word64(W, 0), (uint64_t)n);
-        cs[tid] = (int64_t)mulhi64(block_word64(W, 1), (uint64_t)n);
+        // the source index (random value) or the low bits of W1 (uniform bits)
+        cs[tid] = model == PEAT_MODEL_UNIFORM ? (int64_t)(dtype == PEAT_F32 ? W[2] : (W[2] & 0xFFFFu))
+                                              : (int64_t)mulhi64(block_word64(W, 1), (uint64_t)n);
         __syncthreads();
         if (tid == 0) {
             int64_t m = m_sh;
@@ -88,6 +90,8 @@ __global__ void __launch_bounds__(kBlock) corrupt_positions_kernel(void *x, int6
         uint32_t v;
         if (model == PEAT_MODEL_VALUE) {
             v = load_bits(x, dtype, src[m]);
+        } else if (model == PEAT_MODEL_UNIFORM) {
+            v = (uint32_t)src[m];
         } else if (model == PEAT_MODEL_ZERO) {
             v = 0;
         } else if (model == PEAT_MODEL_NAN) {

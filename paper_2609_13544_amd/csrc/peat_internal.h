@@ -112,13 +112,14 @@ struct InjDesc {                 // one per injected tensor (80 bytes)
     uint64_t seed;
     uint64_t T;                  // floor(rate * 2^64) when !all
     uint64_t mask;
+    const void *src;             // PEAT_MODEL_VALUE: copy of x taken before the call
     int64_t first_seg;
     int32_t nsegs;
     int32_t dtype;
     int32_t all;                 // rate >= 1
     int32_t popc;                // popcount(mask)
-    int32_t model;               // PEAT_MODEL_BITFLIP, _ZERO or _NAN
-    int32_t reserved[3];
+    int32_t model;               // peat_model_t
+    int32_t reserved;
 };
 static_assert(sizeof(InjDesc) == 80, "InjDesc layout");
 

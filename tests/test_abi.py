@@ -118,14 +118,17 @@ def test_inject_validation_codes():
     assert L.peat_inject(None, 10, 0, 1, 0.5, 1) == B.EINVAL       # NULL tensor
     assert L.peat_inject_batched(None, 0, None) == B.OK
     counts = (ctypes.c_int64 * 1)()
-    items = (B.InjectItem * 1)(B.InjectItem(None, 4, 0, 2, 0, 0.5, 1))   # random value needs positions
+    items = (B.InjectItem * 1)(B.InjectItem(None, 4, 0, 2, 0, 0.5, 1))   # random value, NULL tensor
+    assert L.peat_inject_batched(items, 1, counts) == B.EINVAL
+    items = (B.InjectItem * 1)(B.InjectItem(None, 4, 0, 5, 0, 0.5, 1))   # past the last model
     assert L.peat_inject_batched(items, 1, counts) == B.EINVAL
     items = (B.InjectItem * 1)(B.InjectItem(None, 4, 0, 9, 0, 0.5, 1))   # unknown model
     assert L.peat_inject_batched(items, 1, counts) == B.EINVAL
     # zero / NaN models ignore the mask; a NULL tensor is still an error
     assert L.peat_inject_model(None, 10, 0, 1, 0.5, 1, 0) == B.EINVAL
     assert L.peat_inject_model(None, 10, 0, 1, 0.5, 0, 0) == B.EBITMASK
-    assert L.peat_inject_model(None, 10, 0, 1, 0.5, 2, 1) == B.EINVAL
+    assert L.peat_inject_model(None, 10, 0, 1, 0.5, 2, 1) == B.EINVAL      # NULL tensor
+    assert L.peat_inject_model(None, 10, 0, 1, 0.5, 5, 1) == B.EINVAL      # unknown model
 
 
 def test_error_model_validation_codes():
@@ -136,6 +139,7 @@ def test_error_model_validation_codes():
     assert L.peat_corrupt_positions(None, 10, 0, 1, 1, 11, 0, pos) == B.EINVAL  # num_pos > n
     assert L.peat_corrupt_positions(None, 10 ** 6, 0, 1, 1, 4097, 0, pos) == B.EINVAL
     assert L.peat_corrupt_positions(None, 10, 0, 1, 7, 1, 0, pos) == B.EINVAL   # unknown model
+    assert L.peat_corrupt_positions(None, 10, 0, 1, 5, 1, 0, pos) == B.EINVAL
     assert L.peat_corrupt_positions(None, 10, 0, 1, 0, 1, 0, pos) == B.EBITMASK
     assert L.peat_corrupt_positions(None, 10, 5, 1, 1, 1, 0, pos) == B.EDTYPE
     assert L.peat_cast_round(None, 0, 1) == B.OK

@@ -1,9 +1,10 @@
 """GPU parity of the other error models against the oracle, bit for bit:
-the rate-mode zero / NaN / bit-flip models (peat_inject_model and batched
-items), the num_pos position mode with random value / zero / NaN / bit flip
-(peat_corrupt_positions), and the FP16 / BF16 cast error (peat_cast_round),
-over the three element types, ragged sizes, unaligned tensors and the
-workloads' rates."""
+the rate-mode zero / NaN / bit-flip / random-value (the tensor's own value
+at a random index, read from the tensor as it was before the call) /
+uniformly random bit pattern models (peat_inject_model and batched items),
+the num_pos position mode with the same models (peat_corrupt_positions),
+and the FP16 / BF16 cast error (peat_cast_round), over the three element
+types, ragged sizes, unaligned tensors and the workloads' rates."""
 from __future__ import annotations
 
 import sys
@@ -31,7 +32,7 @@ def test_rate_models(code):
     for n in (0, 1, 5000, (1 << 20) + 7):
         gb, _ = special_pair(n, code, seed=300 + n % 97 + code)
         for rate in (0.0, 1e-4, 1e-2, 1.0):
-            for model in (P.MODEL_ZERO, P.MODEL_NAN, P.MODEL_BITFLIP):
+            for model in (P.MODEL_ZERO, P.MODEL_NAN, P.MODEL_BITFLIP, P.MODEL_VALUE, P.MODEL_UNIFORM):
                 log(f"  dtype={code} n={n} rate={rate} model={model}")
                 x = to_device(gb, code)
                 cnt = P.inject_model(x, 1234 + n, rate, model, MASKS[code])
@@ -42,10 +43,35 @@ def test_rate_models(code):
                 assert np.array_equal(to_host_bits(x), ref)
 
 
+@pytest.mark.parametrize("code", [0, 1, 2])
+def test_rate_value_models_distinct_values(code):
+    """Random value at a rate over tensors of distinct values spanning
+    several injector segments (2^20 elements each): a chosen element must
+    get the value its source held before the call, even when the source is
+    itself chosen (rate 1 and 0.5 make that common); also the uniformly
+    random bit pattern model."""
+    for n in (3 * (1 << 20) + 11, 40000):
+        rng = np.random.default_rng(n + code)
+        if code == 0:
+            gb = rng.permutation(np.arange(0x3F800000, 0x3F800000 + n, dtype=np.uint32))
+        else:
+            gb = rng.integers(1, 0x7C00, n, dtype=np.uint16)
+        for rate in (1.0, 0.5, 1e-3):
+            for model in (P.MODEL_VALUE, P.MODEL_UNIFORM):
+                log(f"  dtype={code} n={n} rate={rate} model={model}")
+                x = to_device(gb, code)
+                cnt = P.inject_model(x, 4321 + n, rate, model)
+                ref = gb.copy()
+                assert cnt == oracle.inject_model(ref, dtype=code, seed=4321 + n, rate=rate, model=model)
+                assert np.array_equal(to_host_bits(x), ref)
+
+
 def test_rate_models_batched():
     items, refs, expect = [], [], []
     for k, (n, code, model) in enumerate([(70001, 0, P.MODEL_NAN), (4096, 1, P.MODEL_ZERO),
-                                          (200000, 2, P.MODEL_BITFLIP), (0, 0, P.MODEL_NAN)]):
+                                          (200000, 2, P.MODEL_BITFLIP), (0, 0, P.MODEL_NAN),
+                                          (300001, 0, P.MODEL_VALUE), (5000, 1, P.MODEL_UNIFORM),
+                                          (70000, 2, P.MODEL_VALUE), (1 << 20, 1, P.MODEL_VALUE)]):
         gb, _ = special_pair(n, code, seed=50 + k)
         x = to_device(gb, code)
         items.append((x, 77 + k, 3e-3, MASKS[code], model))
@@ -62,7 +88,7 @@ def test_rate_models_batched():
 def test_positions(code):
     for n, num_pos in ((1, 1), (10, 10), (1000, 5), (5000, 4096), ((1 << 20) + 3, 4096), (3, 0)):
         gb, _ = special_pair(n, code, seed=900 + n % 89 + code)
-        for model in (P.MODEL_VALUE, P.MODEL_ZERO, P.MODEL_NAN, P.MODEL_BITFLIP):
+        for model in (P.MODEL_VALUE, P.MODEL_ZERO, P.MODEL_NAN, P.MODEL_BITFLIP, P.MODEL_UNIFORM):
             for seed in (0, 2 ** 63 + 11):
                 log(f"  dtype={code} n={n} num_pos={num_pos} model={model} seed={seed}")
                 x = to_device(gb, code)
