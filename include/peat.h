@@ -309,12 +309,19 @@ int peat_signature_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t c
                                        peat_signature_t *d_outs, void *stream);
 
 /* Mean of the k largest errors of one pair, k = ceil(n_valid * num / den)
- * (num = 1, den = 10: the paper's top-10% mean); out is host memory.
+ * (num = 1, den = 10: the paper's top-10% mean of Section IV-B.3, the
+ * Analyzer's main score in Section IV-C); out is host memory.
  * 1 <= num <= den <= 2^20.  Exact selection: n_valid, k, count_above and
- * kth_value are exact; sum_topk is a binary64 sum in a fixed order (within
- * 1e-12 relative of the exact sum), bit-identical between calls.  Three
- * streaming passes over golden and test plus work on the few errors that
- * share the k-th largest's leading bits; the call waits for its result. */
+ * kth_value are exact.  sum_topk is the binary64 sum, in a fixed order, of
+ * the errors above the binade of kth_value plus the exact sum of the others
+ * (within 1e-12 relative of the exact sum), bit-identical between calls and
+ * between every entry point below.  Two streaming passes over golden and
+ * test (a binade histogram, then one pass that sums, histograms and gathers
+ * the k-th largest error's binade); a pair whose binade holds too many
+ * distinct errors for the gather takes one more pass (a gather of its top 13
+ * mantissa bits), and one whose bin still does not fit one pass per
+ * remaining digit.  No step waits on the host; the call waits for its
+ * result. */
 int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
                    int32_t num, int32_t den, peat_topk_t *out);
 
@@ -323,24 +330,50 @@ int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t
 int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
                            peat_topk_t *outs);
 
+/* As peat_topk_mean_batched, enqueued on stream (NULL: the default stream):
+ * d_outs is a device array of count records written when the stream gets
+ * there; the call returns without waiting.  The tensors must stay valid and
+ * unchanged until then.  (Section IV-B.3.) */
+int peat_topk_mean_batched_async(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                                 peat_topk_t *d_outs, void *stream);
+
 /* peat_topk_mean_batched over mixed-precision pairs (types as in
  * peat_mixed_pair_t; the error is |T - G| of the exact binary64 values). */
 int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
                                  int32_t den, peat_topk_t *outs);
+
+/* As peat_topk_mean_mixed_batched, enqueued on stream; d_outs as in
+ * peat_topk_mean_batched_async. */
+int peat_topk_mean_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
+                                       int32_t den, peat_topk_t *d_outs, void *stream);
 
 /* peat_topk_mean_batched for pairs whose error signatures the caller already
  * holds: sigs is a host array of count records that peat_signature_batched
  * (or its async form) wrote for the same pairs with these bins; thresholds do
  * not matter.  The histogram counts the same errors of the same valid pairs,
  * so with one-binade bins (hi_log2 - lo_log2 == nbins) it fixes the binade of
- * the k-th largest error whenever that falls in a regular bin, and the first
- * of the three streaming passes skips the pair.  Other pairs, and other bins,
- * take all three.  outs are bit-identical to peat_topk_mean_batched's.
- * PEAT_EINVAL when a record's n differs from its pair's or its histogram
- * total from its n_valid.  (Section IV-B.3; Section V-D histograms.) */
+ * the k-th largest error whenever that falls in a regular bin (or, with a
+ * test type other than binary64, among the zero errors), and the binade
+ * histogram pass skips the pair: one streaming pass then does the rest.
+ * Other pairs, and other bins, take the binade pass too.  outs are
+ * bit-identical to peat_topk_mean_batched's.  PEAT_EINVAL when a record's n
+ * differs from its pair's or its histogram total from its n_valid.
+ * (Section IV-B.3; Section V-D histograms.) */
 int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
                                           int32_t den, const peat_signature_t *sigs,
                                           const peat_bins_t *bins, peat_topk_t *outs);
+
+/* As peat_topk_mean_from_signature_batched, enqueued on stream: d_sigs is a
+ * device array of count records (as peat_signature_batched_async or
+ * peat_inject_signature_batched_async leave them, possibly still being
+ * written earlier on the same stream), d_outs a device array of count
+ * records written when the stream gets there.  A record whose n or
+ * histogram total does not match is ignored (its pair takes the binade
+ * pass), so a mismatch costs time, not correctness. */
+int peat_topk_mean_from_signature_batched_async(const peat_pair_t *pairs, int32_t count, int32_t num,
+                                                int32_t den, const peat_signature_t *d_sigs,
+                                                const peat_bins_t *bins, peat_topk_t *d_outs,
+                                                void *stream);
 
 /* peat_topk_mean_from_signature_batched over mixed-precision pairs, with the
  * records of peat_signature_mixed_batched (or its async form) for the same
@@ -348,6 +381,23 @@ int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t coun
 int peat_topk_mean_mixed_from_signature_batched(const peat_mixed_pair_t *pairs, int32_t count,
                                                 int32_t num, int32_t den, const peat_signature_t *sigs,
                                                 const peat_bins_t *bins, peat_topk_t *outs);
+
+/* As peat_topk_mean_mixed_from_signature_batched with device records,
+ * enqueued on stream (as peat_topk_mean_from_signature_batched_async). */
+int peat_topk_mean_mixed_from_signature_batched_async(const peat_mixed_pair_t *pairs, int32_t count,
+                                                      int32_t num, int32_t den,
+                                                      const peat_signature_t *d_sigs,
+                                                      const peat_bins_t *bins, peat_topk_t *d_outs,
+                                                      void *stream);
+
+/* Entry capacity of the top-k gathers for later calls of this process:
+ * binade_entries for the gathers of a whole binade, bin_entries for the
+ * gathers of one 13-bit bin (16 bytes of device workspace each).  -1 (the
+ * default) sizes them per call: max(2^16, 256 x chunks) and max(2^16,
+ * 64 x chunks), a chunk being one block's share of a pair.  A pair whose
+ * gather does not fit takes the next, slower route; the records do not
+ * change.  Each value must be -1 or in [0, 2^36]. */
+int peat_topk_set_entry_capacity(int64_t binade_entries, int64_t bin_entries);
 
 /* Random bit flip in place (Section II-B).  The draws come from
  * Philox4x32-10 keyed by (lo32(seed), hi32(seed)); "block c of stream s" is
@@ -450,9 +500,10 @@ int peat_finalize_stats(const peat_signature_t *sig, peat_stats_t *stats);
  * events, returns the summed duration (ms) and launch count of one kernel
  * class since the last read, and clears that class.  Kernel classes:
  * 0 signature chunk pass, 1 signature finalize, 2 injection, 3 injection
- * count reduction, 4 streaming read (peat_stream_read), 5 top-k passes 1-2
- * with their selections, 6 top-k pass 3, candidate rounds and finalize,
- * 7 chunk pass with the injection (peat_inject_signature_batched_async). */
+ * count reduction, 4 streaming read (peat_stream_read), 5 top-k level 0
+ * (state, binade histogram pass, selection), 6 top-k from the gathering pass
+ * to the records, 7 chunk pass with the injection
+ * (peat_inject_signature_batched_async). */
 int peat_profile_enable(int on);
 int peat_profile_read(int kernel_class, double *total_ms, int64_t *launches);
 

@@ -12,4 +12,6 @@ from ._binding import (  # noqa: F401
     strerror, topk_mean, topk_mean_batched, topk_mean_from_signature_batched, topk_mean_mixed_from_signature_batched, series_stats, spearman, normalize_scores,
     signature_mixed, signature_mixed_batched, signature_mixed_batched_async, topk_mean_mixed_batched,
     inject_signature_batched_async, K_SIG_INJECT, NOALLOC_SCRATCH_BYTES, signature_batched_noalloc,
+    TOPK_BYTES, decode_topk, topk_mean_batched_async, topk_mean_mixed_batched_async,
+    topk_mean_from_signature_batched_async, topk_mean_mixed_from_signature_batched_async, topk_set_entry_capacity,
 )

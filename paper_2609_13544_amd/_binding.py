@@ -172,6 +172,21 @@ _PROTOS = {
                                                                    ctypes.c_int32, ctypes.c_int32,
                                                                    ctypes.POINTER(Signature), ctypes.POINTER(Bins),
                                                                    ctypes.POINTER(TopK)]),
+    "peat_topk_mean_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32, ctypes.c_int32,
+                                                    ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
+    "peat_topk_mean_mixed_batched_async": (ctypes.c_int, [ctypes.POINTER(MixedPair), ctypes.c_int32,
+                                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                                          ctypes.c_void_p]),
+    "peat_topk_mean_from_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(Pair), ctypes.c_int32,
+                                                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                                                   ctypes.POINTER(Bins), ctypes.c_void_p,
+                                                                   ctypes.c_void_p]),
+    "peat_topk_mean_mixed_from_signature_batched_async": (ctypes.c_int, [ctypes.POINTER(MixedPair),
+                                                                         ctypes.c_int32, ctypes.c_int32,
+                                                                         ctypes.c_int32, ctypes.c_void_p,
+                                                                         ctypes.POINTER(Bins), ctypes.c_void_p,
+                                                                         ctypes.c_void_p]),
+    "peat_topk_set_entry_capacity": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64]),
     "peat_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "peat_finalize_stats": (ctypes.c_int, [ctypes.POINTER(Signature), ctypes.POINTER(Stats)]),
     "peat_series_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(Series)]),
@@ -504,6 +519,87 @@ def topk_mean_mixed_from_signature_batched(pairs, sigs, bins=(-40, 24, 64), num:
     _check(lib().peat_topk_mean_mixed_from_signature_batched(arr, len(pairs), num, den, recs, ctypes.byref(b), outs),
            "peat_topk_mean_mixed_from_signature_batched")
     return [topk_to_dict(outs[k]) for k in range(len(pairs))]
+
+
+TOPK_BYTES = ctypes.sizeof(TopK)
+
+
+def _pairs_arg(pairs):
+    if isinstance(pairs, PreparedPairs):
+        return pairs.arr, pairs.count
+    return _pairs_array(pairs), len(pairs)
+
+
+def _topk_out(d_out, count: int) -> None:
+    _dev_tensor(d_out, "d_out")
+    if d_out.numel() * d_out.element_size() < count * TOPK_BYTES:
+        raise ValueError("d_out too small")
+
+
+def _sig_in(d_sigs, count: int) -> None:
+    _dev_tensor(d_sigs, "d_sigs")
+    if d_sigs.numel() * d_sigs.element_size() < count * SIG_BYTES:
+        raise ValueError("d_sigs too small")
+
+
+def topk_mean_batched_async(pairs, d_out, num: int = 1, den: int = 10, stream=None) -> None:
+    """peat_topk_mean_batched_async: records land in d_out, a device uint8
+    tensor of at least len(pairs) * TOPK_BYTES bytes, when the stream gets
+    there (decode_topk reads them)."""
+    arr, count = _pairs_arg(pairs)
+    _topk_out(d_out, count)
+    _check(lib().peat_topk_mean_batched_async(arr, count, num, den, d_out.data_ptr(), _stream_ptr(stream)),
+           "peat_topk_mean_batched_async")
+
+
+def topk_mean_mixed_batched_async(pairs, d_out, num: int = 1, den: int = 10, stream=None) -> None:
+    """peat_topk_mean_mixed_batched_async over (golden, test) device tensor
+    pairs of any accepted type combination."""
+    arr = _mixed_pairs_array(pairs)
+    _topk_out(d_out, len(pairs))
+    _check(lib().peat_topk_mean_mixed_batched_async(arr, len(pairs), num, den, d_out.data_ptr(),
+                                                    _stream_ptr(stream)),
+           "peat_topk_mean_mixed_batched_async")
+
+
+def topk_mean_from_signature_batched_async(pairs, d_sigs, d_out, bins=(-40, 24, 64), num: int = 1,
+                                           den: int = 10, stream=None) -> None:
+    """peat_topk_mean_from_signature_batched_async: d_sigs holds the pairs'
+    device records (as signature_batched_async leaves them, with these bins)."""
+    arr, count = _pairs_arg(pairs)
+    _sig_in(d_sigs, count)
+    _topk_out(d_out, count)
+    b = make_bins(bins)
+    _check(lib().peat_topk_mean_from_signature_batched_async(arr, count, num, den, d_sigs.data_ptr(),
+                                                             ctypes.byref(b), d_out.data_ptr(),
+                                                             _stream_ptr(stream)),
+           "peat_topk_mean_from_signature_batched_async")
+
+
+def topk_mean_mixed_from_signature_batched_async(pairs, d_sigs, d_out, bins=(-40, 24, 64), num: int = 1,
+                                                 den: int = 10, stream=None) -> None:
+    """peat_topk_mean_mixed_from_signature_batched_async: mixed-precision
+    pairs with the device records of signature_mixed_batched_async."""
+    arr = _mixed_pairs_array(pairs)
+    _sig_in(d_sigs, len(pairs))
+    _topk_out(d_out, len(pairs))
+    b = make_bins(bins)
+    _check(lib().peat_topk_mean_mixed_from_signature_batched_async(arr, len(pairs), num, den, d_sigs.data_ptr(),
+                                                                   ctypes.byref(b), d_out.data_ptr(),
+                                                                   _stream_ptr(stream)),
+           "peat_topk_mean_mixed_from_signature_batched_async")
+
+
+def decode_topk(d_out, count: int) -> list[dict]:
+    """Copy device top-k records to the host and decode them."""
+    host = d_out.detach().view(-1)[: count * TOPK_BYTES].cpu().numpy().view(np.uint8)
+    buf = (TopK * max(1, count)).from_buffer_copy(host.tobytes() if count else bytes(TOPK_BYTES))
+    return [topk_to_dict(buf[k]) for k in range(count)]
+
+
+def topk_set_entry_capacity(binade_entries: int = -1, bin_entries: int = -1) -> None:
+    """peat_topk_set_entry_capacity (-1: sized per call)."""
+    _check(lib().peat_topk_set_entry_capacity(binade_entries, bin_entries), "peat_topk_set_entry_capacity")
 
 
 class PreparedPairs:

@@ -66,8 +66,6 @@ struct Dev {
     size_t ws_size = 0;
     hipEvent_t ws_ev = nullptr;
     bool ws_pending = false;
-    void *ws2 = nullptr;             // top-k candidate keys (sized after pass 2)
-    size_t ws2_size = 0;
     Slot slot[kSlots];
     int next_slot = 0;
     bool prof = false;
@@ -124,22 +122,6 @@ int acquire_ws(Dev &d, size_t bytes, hipStream_t s, char **ws) {
     }
     if (d.ws_pending) HIP_OR_FAIL(hipStreamWaitEvent(s, d.ws_ev, 0));
     *ws = static_cast<char *>(d.ws);
-    return PEAT_OK;
-}
-
-// Second workspace, used only inside a call that has synchronised its
-// stream: growing it after a device-wide synchronisation is safe.
-int acquire_ws2(Dev &d, size_t bytes, char **ws) {
-    if (bytes > d.ws2_size) {
-        HIP_OR_FAIL(hipDeviceSynchronize());
-        if (d.ws2) HIP_OR_FAIL(hipFree(d.ws2));
-        d.ws2 = nullptr;
-        d.ws2_size = 0;
-        size_t want = align_up(bytes + bytes / 4 + (size_t(1) << 20));
-        HIP_OR_FAIL(hipMalloc(&d.ws2, want));
-        d.ws2_size = want;
-    }
-    *ws = static_cast<char *>(d.ws2);
     return PEAT_OK;
 }
 
@@ -628,46 +610,20 @@ int inject_signature_core(const peat_pair_t *pairs, int32_t count, const uint64_
     return signature_core(mp.data(), count, bins, thr, d_outs, nullptr, s, &inj, d_counts);
 }
 
-// Mean of the k largest errors: three streaming passes and the candidate
-// rounds (see topk.hip).  The call waits twice: once after pass 2 to size the
-// candidate buffers, once for the records.
-// Level 0 of the top-k selection from a pair's signature: its histogram
-// counts the same errors of the same valid pairs, and with one-binade bins
-// regular bin b is binade field lo + b + 1023.  Writes the state the level-0
-// selection would write and returns true when the k-th largest error lies in
-// a regular bin (otherwise pass 1 runs for the pair).
-constexpr int kBins0Host = 2048;   // level-0 digit of the top-k selection: the binade field
+// Entries of the two top-k gather regions (binade gathers of pass A, bin
+// gathers of pass C); -1: sized per call from its chunk count.
+int64_t g_topk_cap[2] = {-1, -1};
+constexpr int64_t kTopkCapMin = int64_t(1) << 16;
+constexpr int64_t kTopkCapPerChunk[2] = {256, 64};
 
-bool topk_level0_from_sig(const peat_signature_t &g, const peat_bins_t &b, int32_t num, int32_t den,
-                          TopkState &st) {
-    if (b.hi_log2 - b.lo_log2 != b.nbins || g.n_valid <= 0) return false;
-    const uint64_t nv = (uint64_t)g.n_valid;
-    const uint64_t k = (uint64_t)(((unsigned __int128)nv * (uint32_t)num + (uint32_t)den - 1) / (uint32_t)den);
-    uint64_t acc = (uint64_t)g.hist_over;
-    if (k <= acc) return false;
-    for (int i = b.nbins - 1; i >= 0; --i) {
-        const uint64_t c = (uint64_t)g.hist[i];
-        if (acc + c >= k) {
-            const int d0 = b.lo_log2 + i + 1023;
-            if (d0 < 1 || d0 > kBins0Host - 2) return false;
-            st = TopkState{};
-            st.n_valid = nv;
-            st.k = k;
-            st.need = k - acc;
-            st.cand = c;
-            st.key = (uint64_t)d0 << 52;
-            st.level = 0;
-            st.status = kTopkActive;
-            st.d0 = d0;
-            return true;
-        }
-        acc += c;
-    }
-    return false;
-}
-
-int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den, peat_topk_t *outs,
-              hipStream_t s, const peat_signature_t *sigs = nullptr, const peat_bins_t *bins = nullptr) {
+// Mean of the k largest errors (see topk.hip): every step stream-ordered.
+// With host_outs the records go through workspace + pinned staging and the
+// call waits for them; otherwise they land in d_outs when the stream gets
+// there.  host_sigs (validated here) or d_sigs (validated on the device: a
+// record that does not match its pair is ignored) give level 0.
+int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den, peat_topk_t *host_outs,
+              peat_topk_t *d_outs, hipStream_t s, const peat_signature_t *host_sigs = nullptr,
+              const peat_signature_t *d_sigs = nullptr, const peat_bins_t *bins = nullptr) {
     if (count < 0) return fail(PEAT_EINVAL, "count < 0");
     if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
     if (num < 1 || den < num || den > (1 << 20))
@@ -676,28 +632,20 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     for (int k = 0; k < count; ++k)
         if ((rc = check_mixed(pairs[k], k))) return rc;
     if (count == 0) return PEAT_OK;
-    if (!outs) return fail(PEAT_EINVAL, "outs is NULL");
-    // level 0 from the callers' signatures, where they resolve it
-    std::vector<TopkState> pre;
-    std::vector<int32_t> skip;
-    int nskip = 0;
-    if (sigs) {
+    if (!host_outs && !d_outs) return fail(PEAT_EINVAL, "outs is NULL");
+    if (host_sigs || d_sigs) {
         if (!bins) return fail(PEAT_EINVAL, "bins is NULL");
         if ((rc = check_bins(*bins))) return rc;
-        pre.resize((size_t)count);
-        skip.assign((size_t)count, 0);
+    }
+    if (host_sigs) {
         for (int k = 0; k < count; ++k) {
-            const peat_signature_t &g = sigs[k];
+            const peat_signature_t &g = host_sigs[k];
             int64_t tot = g.hist_zero + g.hist_under + g.hist_over;
             for (int i = 0; i < bins->nbins; ++i) tot += g.hist[i];
             if (g.n != pairs[k].n || tot != g.n_valid)
                 return fail(PEAT_EINVAL, "signature %d does not match pair %d and these bins (n %lld vs %lld, "
                             "histogram total %lld vs n_valid %lld)", k, k, (long long)g.n, (long long)pairs[k].n,
                             (long long)tot, (long long)g.n_valid);
-            if (topk_level0_from_sig(g, *bins, num, den, pre[k])) {
-                skip[k] = 1;
-                ++nskip;
-            }
         }
     }
 
@@ -711,121 +659,81 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     int64_t range[kKinds + 1];
     if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
 
+    uint64_t cap[2];
+    for (int r = 0; r < 2; ++r) {
+        const int64_t c = g_topk_cap[r] >= 0 ? g_topk_cap[r] : std::max(kTopkCapMin, kTopkCapPerChunk[r] * total);
+        cap[r] = (uint64_t)c;
+    }
     const size_t b_desc = align_up(sizeof(SigDesc) * count);
     const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
+    const size_t b_sig = host_sigs ? align_up(sizeof(peat_signature_t) * count) : 0;
+    const size_t b_out = host_outs ? align_up(sizeof(peat_topk_t) * count) : 0;
     const size_t b_state = align_up(sizeof(TopkState) * count);
-    const size_t b_cand = align_up(sizeof(TopkCand) * count);
     const size_t b_hist = align_up(sizeof(uint64_t) * kTopkBins * (size_t)count);
     const size_t b_part = align_up(sizeof(double) * (size_t)total);
-    const size_t b_out = align_up(sizeof(peat_topk_t) * count);
-    const size_t b_skip = nskip ? align_up(sizeof(int32_t) * count) : 0;
-    const size_t o_map = b_desc, o_state = o_map + b_map, o_cand = o_state + b_state;
-    const size_t o_hist = o_cand + b_cand, o_pa = o_hist + b_hist, o_pb = o_pa + b_part, o_out = o_pb + b_part;
-    const size_t o_skip = o_out + b_out;
+    const size_t b_xsum = align_up(2 * sizeof(uint64_t) * count);
+    const size_t b_ovf = align_up(sizeof(uint32_t) * (2 * (size_t)count + 2));
+    const size_t b_fill = align_up(2 * sizeof(unsigned long long));
+    const size_t b_ents = align_up(sizeof(TopkEntry) * (size_t)(cap[0] + cap[1]));
+    // device workspace: descriptors | chunk map | signatures | records (the
+    // first three staged and copied as they lie) | state | histograms | chunk
+    // sums | exact sums | flags | fills | entries
+    const size_t o_map = b_desc, o_sig = o_map + b_map, o_out = o_sig + b_sig, o_state = o_out + b_out;
+    const size_t o_hist = o_state + b_state, o_part = o_hist + b_hist, o_xsum = o_part + b_part;
+    const size_t o_ovf = o_xsum + b_xsum, o_fill = o_ovf + b_ovf, o_ents = o_fill + b_fill;
 
     char *ws;
-    if ((rc = acquire_ws(d, o_skip + b_skip, s, &ws))) return rc;
+    if ((rc = acquire_ws(d, o_ents + b_ents, s, &ws))) return rc;
     Slot *sl;
-    if ((rc = acquire_slot(d, b_desc + b_map + b_state + b_out + b_skip, &sl))) return rc;
+    if ((rc = acquire_slot(d, o_state, &sl))) return rc;
     char *h = static_cast<char *>(sl->host);
     std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
-    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc);
+    int32_t *hmap = reinterpret_cast<int32_t *>(h + o_map);
     for (int k = 0; k < count; ++k)
         for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
-    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
-    if (nskip) {
-        // the resolved pairs' level-0 states and the skip flags
-        char *hs = h + b_desc + b_map;
-        char *hk = h + b_desc + b_map + b_state + b_out;
-        std::memcpy(hs, pre.data(), sizeof(TopkState) * count);
-        std::memcpy(hk, skip.data(), sizeof(int32_t) * count);
-        HIP_OR_FAIL(hipMemcpyAsync(ws + o_state, hs, sizeof(TopkState) * count, hipMemcpyHostToDevice, s));
-        HIP_OR_FAIL(hipMemcpyAsync(ws + o_skip, hk, sizeof(int32_t) * count, hipMemcpyHostToDevice, s));
-    }
+    if (host_sigs) std::memcpy(h + o_sig, host_sigs, sizeof(peat_signature_t) * count);
+    HIP_OR_FAIL(hipMemcpyAsync(ws, h, o_out, hipMemcpyHostToDevice, s));
 
     TopkParams P{};
-    P.chunk_base = 0;
     P.descs = reinterpret_cast<const SigDesc *>(ws);
     P.chunk_pair = reinterpret_cast<const int32_t *>(ws + o_map);
     P.state = reinterpret_cast<TopkState *>(ws + o_state);
-    P.cand = reinterpret_cast<const TopkCand *>(ws + o_cand);
     P.hist = reinterpret_cast<uint64_t *>(ws + o_hist);
-    P.part_a = reinterpret_cast<double *>(ws + o_pa);
-    P.part_b = reinterpret_cast<double *>(ws + o_pb);
-    P.outs = reinterpret_cast<peat_topk_t *>(ws + o_out);
-    P.skip0 = nskip ? reinterpret_cast<const int32_t *>(ws + o_skip) : nullptr;
+    P.part_a = reinterpret_cast<double *>(ws + o_part);
+    P.xsum = reinterpret_cast<uint64_t *>(ws + o_xsum);
+    P.ovf = reinterpret_cast<uint32_t *>(ws + o_ovf);
+    P.fill = reinterpret_cast<unsigned long long *>(ws + o_fill);
+    P.ents = reinterpret_cast<TopkEntry *>(ws + o_ents);
+    P.cap[0] = cap[0];
+    P.cap[1] = cap[1];
+    P.sigs = host_sigs ? reinterpret_cast<const peat_signature_t *>(ws + o_sig) : d_sigs;
+    P.outs = host_outs ? reinterpret_cast<peat_topk_t *>(ws + o_out) : d_outs;
+    if (bins) {
+        P.lo = bins->lo_log2;
+        P.hi = bins->hi_log2;
+        P.nbins = bins->nbins;
+    }
     P.count = count;
     P.num = num;
     P.den = den;
-    const int64_t nhist = (int64_t)kTopkBins * count;
 
-    // passes 1 and 2 with their selections (pass 1 only for the pairs that
-    // the signatures leave unresolved)
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;
-    if (nskip < count) {
-        HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
-        HIP_OR_FAIL(launch_topk_pass(P, 0, range, s));
-        HIP_OR_FAIL(launch_topk_select(P, 0, s));
-    }
-    HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
-    HIP_OR_FAIL(launch_topk_pass(P, 1, range, s));
-    HIP_OR_FAIL(launch_topk_select(P, 1, s));
+    HIP_OR_FAIL(launch_topk_level0(P, range, s));
     if ((rc = prof_end(d, s, 5, ev))) return rc;
-
-    // size the candidate buffers: the level-1 boundary bin of each pair
-    TopkState *hst = reinterpret_cast<TopkState *>(h + b_desc + b_map);
-    HIP_OR_FAIL(hipMemcpyAsync(hst, P.state, sizeof(TopkState) * count, hipMemcpyDeviceToHost, s));
-    HIP_OR_FAIL(hipStreamSynchronize(s));
-    std::vector<TopkCand> cands((size_t)count);
-    std::vector<int32_t> cblk;
-    uint64_t ncand = 0;
-    for (int k = 0; k < count; ++k) {
-        const bool rounds = hst[k].level == 1 && hst[k].status == kTopkActive;
-        const uint64_t c = rounds ? hst[k].cand : 0;
-        cands[k].off = ncand;
-        cands[k].first_blk = (int32_t)cblk.size();
-        cands[k].nblk = (int32_t)((c + kTopkCandBlock - 1) / kTopkCandBlock);
-        for (int32_t b = 0; b < cands[k].nblk; ++b) cblk.push_back(k);
-        ncand += c;
-    }
-    if (cblk.size() > 0x7FFFFFFF) return fail(PEAT_EINVAL, "too many top-k candidates");
-    P.ncblk = (int64_t)cblk.size();
-    // (key, count) entries: at most one per error of the level-1 bin
-    const size_t b_keys = align_up(2 * sizeof(uint64_t) * (ncand > 0 ? ncand : 1));
-    const size_t b_cblk = align_up(sizeof(int32_t) * (cblk.empty() ? 1 : cblk.size()));
-    const size_t b_x = align_up(sizeof(uint64_t) * 2 * (kTopkLevels - 2) * (cblk.empty() ? 1 : cblk.size()));
-    char *w2;
-    if ((rc = acquire_ws2(d, 2 * b_keys + b_cblk + b_x, &w2))) return rc;
-    P.keys[0] = reinterpret_cast<uint64_t *>(w2);
-    P.keys[1] = reinterpret_cast<uint64_t *>(w2 + b_keys);
-    P.cblk_pair = reinterpret_cast<const int32_t *>(w2 + 2 * b_keys);
-    P.xpart = reinterpret_cast<uint64_t *>(w2 + 2 * b_keys + b_cblk);
-    // the stream is idle here, so plain synchronous copies are ordered
-    HIP_OR_FAIL(hipMemcpy(ws + o_cand, cands.data(), sizeof(TopkCand) * count, hipMemcpyHostToDevice));
-    if (!cblk.empty())
-        HIP_OR_FAIL(hipMemcpy(w2 + 2 * b_keys, cblk.data(), sizeof(int32_t) * cblk.size(), hipMemcpyHostToDevice));
-
-    // pass 3, the candidate rounds and the records
     if ((rc = prof_begin(d, s, &ev))) return rc;
-    HIP_OR_FAIL(launch_topk_pass(P, 2, range, s));
-    if (P.ncblk > 0) {
-        for (int L = 2; L < kTopkLevels; ++L) {
-            HIP_OR_FAIL(launch_topk_zero(P.hist, nhist, s));
-            HIP_OR_FAIL(launch_topk_cand_hist(P, L, s));
-            HIP_OR_FAIL(launch_topk_select(P, L, s));
-            HIP_OR_FAIL(launch_topk_cand_sum(P, L, s));
-        }
-    }
-    HIP_OR_FAIL(launch_topk_finalize(P, s));
+    HIP_OR_FAIL(launch_topk_rest(P, range, s));
     if ((rc = prof_end(d, s, 6, ev))) return rc;
 
-    char *hout = h + b_desc + b_map + b_state;
-    HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_topk_t) * count, hipMemcpyDeviceToHost, s));
+    char *hout = h + o_out;
+    if (host_outs)
+        HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_topk_t) * count, hipMemcpyDeviceToHost, s));
     if ((rc = release_slot(*sl, s))) return rc;
     if ((rc = release_ws(d, s))) return rc;
-    HIP_OR_FAIL(hipStreamSynchronize(s));
-    std::memcpy(outs, hout, sizeof(peat_topk_t) * count);
+    if (host_outs) {
+        HIP_OR_FAIL(hipStreamSynchronize(s));
+        std::memcpy(host_outs, hout, sizeof(peat_topk_t) * count);
+    }
     return PEAT_OK;
 }
 
@@ -1117,7 +1025,7 @@ int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t
     std::vector<peat_mixed_pair_t> mp;
     int rc = same_type_pairs(&p, 1, mp);
     if (rc) return rc;
-    return topk_core(mp.data(), 1, num, den, out, t_stream);
+    return topk_core(mp.data(), 1, num, den, out, nullptr, t_stream);
 }
 
 int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
@@ -1125,12 +1033,29 @@ int peat_topk_mean_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
     std::vector<peat_mixed_pair_t> mp;
     int rc = same_type_pairs(pairs, count, mp);
     if (rc) return rc;
-    return topk_core(mp.data(), count, num, den, outs, t_stream);
+    if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
+    return topk_core(mp.data(), count, num, den, outs, nullptr, t_stream);
+}
+
+int peat_topk_mean_batched_async(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                                 peat_topk_t *d_outs, void *stream) {
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    if (count > 0 && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+    return topk_core(mp.data(), count, num, den, nullptr, d_outs, static_cast<hipStream_t>(stream));
 }
 
 int peat_topk_mean_mixed_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den,
                                  peat_topk_t *outs) {
-    return topk_core(pairs, count, num, den, outs, t_stream);
+    if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
+    return topk_core(pairs, count, num, den, outs, nullptr, t_stream);
+}
+
+int peat_topk_mean_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_t den,
+                                       peat_topk_t *d_outs, void *stream) {
+    if (count > 0 && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+    return topk_core(pairs, count, num, den, nullptr, d_outs, static_cast<hipStream_t>(stream));
 }
 
 int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t count, int32_t num, int32_t den,
@@ -1140,14 +1065,48 @@ int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t coun
     std::vector<peat_mixed_pair_t> mp;
     int rc = same_type_pairs(pairs, count, mp);
     if (rc) return rc;
-    return topk_core(mp.data(), count, num, den, outs, t_stream, sigs, bins);
+    if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
+    return topk_core(mp.data(), count, num, den, outs, nullptr, t_stream, sigs, nullptr, bins);
+}
+
+int peat_topk_mean_from_signature_batched_async(const peat_pair_t *pairs, int32_t count, int32_t num,
+                                                int32_t den, const peat_signature_t *d_sigs,
+                                                const peat_bins_t *bins, peat_topk_t *d_outs, void *stream) {
+    if (count > 0 && !d_sigs) return fail(PEAT_EINVAL, "d_sigs is NULL");
+    std::vector<peat_mixed_pair_t> mp;
+    int rc = same_type_pairs(pairs, count, mp);
+    if (rc) return rc;
+    if (count > 0 && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+    return topk_core(mp.data(), count, num, den, nullptr, d_outs, static_cast<hipStream_t>(stream), nullptr,
+                     d_sigs, bins);
 }
 
 int peat_topk_mean_mixed_from_signature_batched(const peat_mixed_pair_t *pairs, int32_t count, int32_t num,
                                                 int32_t den, const peat_signature_t *sigs,
                                                 const peat_bins_t *bins, peat_topk_t *outs) {
     if (count > 0 && !sigs) return fail(PEAT_EINVAL, "sigs is NULL");
-    return topk_core(pairs, count, num, den, outs, t_stream, sigs, bins);
+    if (count > 0 && !outs) return fail(PEAT_EINVAL, "outs is NULL");
+    return topk_core(pairs, count, num, den, outs, nullptr, t_stream, sigs, nullptr, bins);
+}
+
+int peat_topk_mean_mixed_from_signature_batched_async(const peat_mixed_pair_t *pairs, int32_t count,
+                                                      int32_t num, int32_t den, const peat_signature_t *d_sigs,
+                                                      const peat_bins_t *bins, peat_topk_t *d_outs,
+                                                      void *stream) {
+    if (count > 0 && !d_sigs) return fail(PEAT_EINVAL, "d_sigs is NULL");
+    if (count > 0 && !d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
+    return topk_core(pairs, count, num, den, nullptr, d_outs, static_cast<hipStream_t>(stream), nullptr, d_sigs,
+                     bins);
+}
+
+int peat_topk_set_entry_capacity(int64_t binade_entries, int64_t bin_entries) {
+    if (binade_entries < -1 || bin_entries < -1 || binade_entries > (int64_t(1) << 36) ||
+        bin_entries > (int64_t(1) << 36))
+        return fail(PEAT_EINVAL, "capacities must be -1 or in [0, 2^36]");
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_topk_cap[0] = binade_entries;
+    g_topk_cap[1] = bin_entries;
+    return PEAT_OK;
 }
 
 int peat_stream_read(const void *buf, int64_t bytes, uint32_t *d_sink, void *stream) {

@@ -134,53 +134,55 @@ struct InjParams {
 // ---- top-k error mean --------------------------------------------------------
 // Radix selection on the binary64 bit pattern of the error (monotone for
 // a >= 0): digit 0 = bits 62..52 (the binade, 2048 bins), digits 1-4 = 13
-// mantissa bits each (8192 bins).  Levels 0 and 1 are histograms over the
-// tensors (passes 1 and 2); pass 3 sums the errors above the level-1 bin and
-// gathers the errors inside it as (key, count) entries; levels 2-4 run on
-// those entries.
+// mantissa bits each (8192 bins).  The boundary's binade D0 comes from the
+// pair's signature or from a binade histogram; one pass then sums the errors
+// above D0, histograms digit 1 inside it and gathers its errors as
+// deduplicated (key, count) entries, on which digits 2-4 are resolved.
 constexpr int kTopkLevels = 5;
 constexpr int kTopkBins = 8192;                  // bins of digits 1-4
-constexpr int kTopkCandBlock = 16384;            // (key, count) entries per block
 enum { kTopkActive = 0, kTopkDone = 1 };
 
-struct TopkState {               // one per pair (80 bytes), device memory
+struct TopkState {               // one per pair (56 bytes), device memory
     uint64_t n_valid;
     uint64_t k;
     uint64_t need;               // k minus the errors above the boundary bin
     uint64_t cand;               // errors in the boundary bin
     uint64_t key;                // bits of the boundary fixed so far
-    uint64_t cnt[2];             // entries in keys[0] / keys[1]
     int32_t level;               // last resolved level, -1 before level 0
     int32_t status;              // kTopkActive or kTopkDone
-    int32_t d0;                  // level-0 boundary (the binade field)
-    int32_t reserved[3];
+    int32_t d0;                  // binade field of the boundary
+    int32_t reserved;
 };
-static_assert(sizeof(TopkState) == 80, "TopkState layout");
+static_assert(sizeof(TopkState) == 56, "TopkState layout");
 
-struct TopkCand {                // one per pair, written by the host after pass 2
-    uint64_t off;                // first entry slot of the pair
-    int32_t first_blk;           // first candidate block
-    int32_t nblk;                // candidate blocks (0: no candidate rounds)
+struct TopkEntry {               // errors of one key in one chunk (16 bytes)
+    uint64_t key;
+    uint32_t count;
+    int32_t pair;                // -1: an unused position
 };
+static_assert(sizeof(TopkEntry) == 16, "TopkEntry layout");
 
 struct TopkParams {
     int64_t chunk_base;          // first global chunk of this launch
+    int64_t kind_chunks;         // chunks of this launch
     const SigDesc *descs;
     const int32_t *chunk_pair;
     TopkState *state;
-    const TopkCand *cand;
     uint64_t *hist;              // count x kTopkBins counters
-    double *part_a;              // pass 2: per chunk, sum of errors above the level-0 bin
-    double *part_b;              // pass 3: per chunk, sum above the level-1 bin inside it
-    uint64_t *keys[2];           // (key, count) entry buffers, 2 words per entry
-    const int32_t *cblk_pair;    // candidate block -> pair
-    uint64_t *xpart;             // per (round, candidate block): exact sums, 2 words
+    double *part_a;              // per chunk: binary64 sum of its errors above binade D0
+    uint64_t *xsum;              // per pair: exact sum (2 words) of the significands in binade D0 above the boundary
+    uint32_t *ovf;               // per pair: [0] gather of binade D0 did not fit, [1] gather of bin (D0, D1) did not fit;
+                                 // then 2 words: some pair has flag 0 set, some pair has flag 1 set
+    TopkEntry *ents;             // cap[0] entries of binade D0 gathers, then cap[1] of bin (D0, D1) gathers
+    unsigned long long *fill;    // entries handed out in each of the two regions
+    uint64_t cap[2];
+    const peat_signature_t *sigs;    // the pairs' signatures (device), or NULL
     peat_topk_t *outs;           // one per pair (device)
-    const int32_t *skip0;        // per pair: level 0 resolved from a signature histogram (or NULL)
-    int64_t ncblk;               // candidate blocks
+    int32_t lo, hi, nbins;       // the bins of those signatures
     int32_t count;               // pairs
     int32_t num, den;
-    int32_t level;               // level of a histogram / selection launch
+    int32_t level;               // level of a selection, tensor-pass or entry launch
+    int32_t pad;
 };
 
 // Kernel launchers (defined in the .hip translation units).
@@ -199,11 +201,10 @@ hipError_t launch_corrupt_positions(void *x, int64_t n, int dtype, uint64_t seed
                                     uint64_t mask, int64_t *d_positions, hipStream_t s);
 hipError_t launch_cast_round(void *x, int64_t n, int to_dtype, hipStream_t s);
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
-hipError_t launch_topk_zero(uint64_t *p, int64_t n, hipStream_t s);
-hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[kKinds + 1], hipStream_t s);
-hipError_t launch_topk_select(const TopkParams &p, int level, hipStream_t s);
-hipError_t launch_topk_cand_hist(const TopkParams &p, int level, hipStream_t s);
-hipError_t launch_topk_cand_sum(const TopkParams &p, int level, hipStream_t s);
-hipError_t launch_topk_finalize(const TopkParams &p, hipStream_t s);
+// The top-k selection of a batch, stream-ordered (no host wait): level 0
+// (state, binade histogram where the signatures leave it open, selection),
+// then the rest up to the records.
+hipError_t launch_topk_level0(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s);
+hipError_t launch_topk_rest(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s);
 
 }  // namespace peat

@@ -1,35 +1,38 @@
 // Mean of the k largest errors of each pair (the "mean of the top 10%
 // errors" score of Section IV-B.3, the Analyzer's main score in Section IV-C),
 // by exact radix selection on the binary64 bit pattern of the error, which is
-// monotone for a >= 0:
+// monotone for a >= 0.  The whole selection is stream-ordered: every count,
+// boundary and buffer fill stays on the device, so no step waits on the host.
 //
-//   pass 1   histogram of digit 0 (bits 62..52, the binade) over the pair;
-//   select   the binade D0 holding the k-th largest error;
-//   pass 2   binary64 sum of the errors above binade D0; histogram of digit 1
-//            (bits 51..39) of the errors inside it;
-//   select   the level-1 bin D1;
-//   pass 3   binary64 sum of the errors in binade D0 above bin D1; the errors
-//            of bin (D0, D1) are gathered as (key, count) entries: each block
-//            counts its distinct keys in an LDS hash table (errors of
-//            checkpoint-like data are small multiples of the golden's ULP,
-//            so the boundary bin is mostly ties) and appends one entry per
-//            key; keys that do not fit the table become entries of count 1;
-//   rounds   digits 2-4 (13 bits each) on the entries: weighted histogram,
-//            select, exact integer sum count * significand of the entries
-//            above the boundary (they share the exponent D0), copy of the
-//            entries on it;
-//   finalize sum = (pass 2 + pass 3) + exact candidate sums + need * T.
+//   init     per pair: the state of level 0 from its signature when one is
+//            given and its histogram fixes the binade D0 of the k-th largest
+//            error (one-binade bins, boundary in a regular bin or among the
+//            zero errors); otherwise level 0 is open;
+//   pass 1   histogram of digit 0 (bits 62..52, the binade) over the pairs
+//            whose level 0 is open; select D0;
+//   pass A   binary64 sum of the errors above binade D0 (a fixed per-lane /
+//            butterfly / wave order in each chunk); histogram of digit 1
+//            (bits 51..39) inside D0; the errors of binade D0 gathered as
+//            (key, count) entries: each block counts its distinct keys in an
+//            LDS hash table (errors of checkpoint-like data are small
+//            multiples of the golden's ULP, so a binade holds few distinct
+//            values) and appends one entry per key; select D1;
+//   rounds   digits 2-4 on the entries: weighted histogram, select; then the
+//            exact integer sum count * significand of the entries above the
+//            boundary (they share the exponent D0);
+//   finalize sum = pass A + exact sum + need * T.
 //
-// Given the pair's error signature with one-binade histogram bins (the same
-// errors over the same valid pairs), the host resolves level 0 from that
-// histogram whenever the k-th largest error falls in a regular bin, and
-// pass 1 and the level-0 selection skip the pair.
+// A pair whose binade does not fit (a block's table overflows, or the entry
+// buffer is full) instead takes pass C over its tensors: the exact sum of
+// its errors in D0 above bin D1 and a gather of bin (D0, D1), whose keys
+// that do not fit the table become entries of count 1; the rounds then run
+// on those entries.  A pair whose bin does not fit either takes one
+// histogram pass over its tensors per digit (passes T2-T4) and a last pass
+// for the exact sum of digit 4 (T5).  Every route sums the errors inside D0
+// exactly, so they give bit-identical records.
 //
 // The k-th largest error T is the key with all five digits fixed; count_above
-// is k minus the copies of T taken.  Passes 2 and 3 sum in a fixed
-// per-lane / butterfly / wave order over chunks whose size depends only on
-// n, and the candidate sums are exact integers, so the
-// result does not depend on the order in which candidates are copied.
+// is k minus the copies of T taken.
 #include "elements.h"
 
 namespace peat {
@@ -46,15 +49,38 @@ __device__ __forceinline__ double opaque_double(uint32_t hi, uint32_t lo) {
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 constexpr uint64_t kMant = (uint64_t(1) << 52) - 1;
-constexpr int kTable = 512;                     // LDS hash table of pass 3 (keys per block)
+constexpr int kTable = 512;                     // LDS hash table of a gather (keys per block)
 constexpr int kProbes = 8;
 constexpr uint64_t kEmpty = ~uint64_t(0);       // never a key: errors have the sign bit clear
+constexpr int kScanGrid = 2048;                 // blocks of the fallback tensor passes
+constexpr int kEntGrid = 1024;                  // blocks of the entry rounds
+enum { kModeA = 0, kModeC = 1, kModeT = 2 };    // route of an active pair
 
 __device__ __forceinline__ int digit_shift(int level) { return level == 0 ? 52 : 52 - 13 * level; }
 
 __device__ __forceinline__ uint32_t digit_of(uint64_t key, int level) {
     if (level == 0) return (uint32_t)(key >> 52);               // sign bit is 0
     return (uint32_t)(key >> digit_shift(level)) & (kTopkBins - 1);
+}
+
+// Significand of an error of binade d0 as an integer: binade 0 (zero and
+// subnormal errors) has no implicit bit and the exponent of binade 1.
+__device__ __forceinline__ uint64_t signif(uint64_t key, int d0) {
+    return (key & kMant) | (d0 != 0 ? (uint64_t(1) << 52) : 0);
+}
+
+__device__ __forceinline__ int pair_mode(const TopkParams &P, int pair) {
+    return P.ovf[2 * pair] == 0 ? kModeA : (P.ovf[2 * pair + 1] == 0 ? kModeC : kModeT);
+}
+
+// Exact 128-bit accumulation: the carry of each low-word addition is
+// recovered from the value the atomic returns.
+__device__ __forceinline__ void atomic_add128(uint64_t *x, uint64_t lo, uint64_t hi) {
+    if (lo) {
+        const uint64_t old = atomicAdd((unsigned long long *)&x[0], (unsigned long long)lo);
+        hi += (old + lo < old) ? 1u : 0u;
+    }
+    if (hi) atomicAdd((unsigned long long *)&x[1], (unsigned long long)hi);
 }
 
 // Error of a valid pair (no NaN on either side) and its bit pattern.
@@ -140,6 +166,20 @@ __device__ __forceinline__ double block_sum(double x, double *red) {
     return s;
 }
 
+// Adds the block's per-thread integers (each below 2^64) into the pair's
+// 128-bit exact sum: wave sums in 128 bits, one atomic pair per wave.
+__device__ __forceinline__ void block_add128(uint64_t x, uint64_t *dst) {
+    uint64_t lo = x, hi = 0;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t ol = __shfl_xor(lo, o), oh = __shfl_xor(hi, o);
+        const uint64_t s = lo + ol;
+        hi += oh + (s < lo ? 1u : 0u);
+        lo = s;
+    }
+    if ((threadIdx.x & 63) == 0) atomic_add128(dst, lo, hi);
+}
+
 // Adds the block's LDS histogram to the pair's device histogram.
 __device__ __forceinline__ void flush_hist(const uint32_t *h, int nb, uint64_t *H) {
     __syncthreads();
@@ -147,132 +187,343 @@ __device__ __forceinline__ void flush_hist(const uint32_t *h, int nb, uint64_t *
         if (h[b]) atomicAdd((unsigned long long *)&H[b], (unsigned long long)h[b]);
 }
 
-// Appends the entry (key, count) to a pair's entry buffer (two words per
-// entry), one atomic per wave.
-__device__ __forceinline__ void append_entry(bool take, uint64_t key, uint64_t count, uint64_t *cnt,
-                                             uint64_t *dst) {
-    const uint64_t m = __ballot(take);
-    if (m == 0) return;
-    const int leader = __ffsll((long long)m) - 1;
-    uint64_t base = 0;
-    if ((int)(threadIdx.x & 63) == leader) base = atomicAdd((unsigned long long *)cnt, (unsigned long long)__popcll(m));
-    base = __shfl(base, leader);
-    if (take) {
-        const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-        dst[2 * (base + rank)] = key;
-        dst[2 * (base + rank) + 1] = count;
+// ---- LDS gather table ----------------------------------------------------------
+struct Table {
+    uint64_t key[kTable];
+    uint32_t cnt[kTable];
+    uint32_t full;               // some key found no slot
+    uint32_t n;                  // occupied slots (flush)
+    uint32_t pos;                // entries written (flush)
+    uint32_t ok;                 // the flush fits the buffer
+    unsigned long long base;
+};
+
+__device__ __forceinline__ void table_init(Table &t) {
+    for (int i = threadIdx.x; i < kTable; i += kBlock) {
+        t.key[i] = kEmpty;
+        t.cnt[i] = 0;
+    }
+    if (threadIdx.x == 0) {
+        t.full = 0;
+        t.n = 0;
+        t.pos = 0;
     }
 }
 
-// Counts key in the block's LDS table (open addressing); false when its
-// probe sequence is full of other keys.
-__device__ __forceinline__ bool table_count(uint64_t *tkey, uint32_t *tcnt, uint64_t key) {
+// Counts key in the table (open addressing, slots go from empty to one key
+// only); false when its probe sequence is full of other keys.
+__device__ __forceinline__ bool table_count(Table &t, uint64_t key) {
     const uint32_t h = (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> 55);    // 9 bits
 #pragma unroll 1
     for (int p = 0; p < kProbes; ++p) {
         const uint32_t slot = (h + p) & (kTable - 1);
-        const uint64_t old = atomicCAS((unsigned long long *)&tkey[slot], (unsigned long long)kEmpty,
-                                       (unsigned long long)key);
-        if (old == kEmpty || old == key) {
-            atomicAdd(&tcnt[slot], 1u);
+        uint64_t cur = __hip_atomic_load(&t.key[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (cur == kEmpty)
+            cur = atomicCAS((unsigned long long *)&t.key[slot], (unsigned long long)kEmpty, (unsigned long long)key);
+        if (cur == kEmpty || cur == key) {
+            atomicAdd(&t.cnt[slot], 1u);
             return true;
         }
     }
     return false;
 }
 
-template <int DG, int DT, int PASS>
-__global__ void __launch_bounds__(kBlock) topk_pass(TopkParams P) {
-    __shared__ uint32_t h[kTopkBins];
-    __shared__ double red[kWaves];
-    const int64_t gchunk = P.chunk_base + blockIdx.x;
-    const int pair = P.chunk_pair[gchunk];
-    const SigDesc d = P.descs[pair];
-    const int64_t cin = gchunk - d.first_chunk;
-    uint64_t *H = P.hist + (size_t)pair * kTopkBins;
-
-    if constexpr (PASS == 0) {
-        if (P.skip0 && P.skip0[pair]) return;                 // level 0 already resolved
-        for (int b = threadIdx.x; b < kBins0; b += kBlock) h[b] = 0;
-        __syncthreads();
-        for_each_error<DG, DT>(d, cin, [&](uint64_t key, double) { atomicAdd(&h[key >> 52], 1u); });
-        flush_hist(h, kBins0, H);
-    } else if constexpr (PASS == 1) {
-        const TopkState st = P.state[pair];
-        // nothing above an infinite boundary; nothing at all when k = 0
-        if (st.k == 0 || st.d0 == kBins0 - 1) {
-            if (threadIdx.x == 0) P.part_a[gchunk] = 0.0;
-            return;
+// Writes the table's keys as entries of `pair` into region r, or marks the
+// pair (flag r) when a key found no slot or the region is full; positions
+// handed out past the region's end are left to later overflows, positions
+// inside it that this block cannot use are marked unused.
+__device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r, int pair) {
+    __syncthreads();
+    for (int i = threadIdx.x; i < kTable; i += kBlock)
+        if (t.cnt[i]) atomicAdd(&t.n, 1u);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t n = t.n;
+        unsigned long long base = 0;
+        uint32_t ok = t.full == 0;
+        if (n > 0) {
+            base = atomicAdd(&P.fill[r], (unsigned long long)n);
+            if (base + n > P.cap[r]) ok = 0;
         }
-        const uint64_t d0 = (uint64_t)st.d0;
-        const bool hist1 = st.status == kTopkActive;          // the boundary binade needs ordering
-        if (hist1) {
-            for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
-            __syncthreads();
+        if (!ok) {
+            P.ovf[2 * pair + r] = 1;
+            P.ovf[2 * P.count + r] = 1;
         }
-        double s = 0.0;
-        for_each_error<DG, DT>(d, cin, [&](uint64_t key, double a) {
-            const uint64_t e = key >> 52;
-            if (e > d0) {
-                s += a;
-            } else if (e == d0 && hist1) {
-                atomicAdd(&h[digit_of(key, 1)], 1u);
+        t.base = base;
+        t.ok = ok;
+    }
+    __syncthreads();
+    TopkEntry *E = P.ents + (r ? P.cap[0] : 0);
+    const unsigned long long base = t.base;
+    if (t.ok) {
+        for (int i = threadIdx.x; i < kTable; i += kBlock)
+            if (t.cnt[i]) {
+                const uint32_t q = atomicAdd(&t.pos, 1u);
+                E[base + q] = TopkEntry{t.key[i], t.cnt[i], pair};
             }
-        });
-        const double bs = block_sum(s, red);
-        if (threadIdx.x == 0) P.part_a[gchunk] = bs;
-        if (hist1) flush_hist(h, kTopkBins, H);
     } else {
-        __shared__ uint64_t tkey[kTable];
-        __shared__ uint32_t tcnt[kTable];
-        const TopkState st = P.state[pair];
-        if (st.level < 1) {
-            if (threadIdx.x == 0) P.part_b[gchunk] = 0.0;
-            return;
-        }
-        for (int i = threadIdx.x; i < kTable; i += kBlock) {
-            tkey[i] = kEmpty;
-            tcnt[i] = 0;
-        }
-        __syncthreads();
-        const uint64_t b1 = st.key >> digit_shift(1);        // binade and digit 1 of the boundary
-        const uint64_t off = P.cand[pair].off;
-        uint64_t *cnt = &P.state[pair].cnt[0];
-        uint64_t *dst = P.keys[0] + 2 * off;
-        double s = 0.0;
-        for_each_error<DG, DT>(d, cin, [&](uint64_t key, double a) {
-            const uint64_t k1 = key >> digit_shift(1);
-            if ((k1 >> 13) == (b1 >> 13) && k1 > b1) s += a;
-            const bool in = k1 == b1;
-            const bool counted = in && table_count(tkey, tcnt, key);
-            append_entry(in && !counted, key, 1, cnt, dst);
-        });
-        const double bs = block_sum(s, red);
-        if (threadIdx.x == 0) P.part_b[gchunk] = bs;
-        __syncthreads();
-        for (int i0 = 0; i0 < kTable; i0 += kBlock) {
-            const int i = i0 + (int)threadIdx.x;
-            append_entry(tcnt[i] != 0, tkey[i], tcnt[i], cnt, dst);
+        const unsigned long long end = base + t.n < P.cap[r] ? base + t.n : P.cap[r];
+        for (unsigned long long q = base + threadIdx.x; q < end; q += kBlock) E[q] = TopkEntry{0, 0, -1};
+    }
+}
+
+// Appends (key, 1) entries of keys that found no slot to region 1, one
+// atomic per wave; a wave past the region's end marks the pair.
+__device__ __forceinline__ void spill_entry(bool take, uint64_t key, const TopkParams &P, int pair) {
+    const uint64_t m = __ballot(take);
+    if (m == 0) return;
+    const int leader = __ffsll((long long)m) - 1;
+    unsigned long long base = 0;
+    if ((int)(threadIdx.x & 63) == leader) base = atomicAdd(&P.fill[1], (unsigned long long)__popcll(m));
+    base = __shfl(base, leader);
+    if (take) {
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        const unsigned long long q = base + rank;
+        if (q < P.cap[1]) {
+            P.ents[P.cap[0] + q] = TopkEntry{key, 1u, pair};
+        } else {
+            P.ovf[2 * pair + 1] = 1;
+            P.ovf[2 * P.count + 1] = 1;
         }
     }
 }
 
-// One block per pair: the bin of the level-`level` histogram holding the
-// need-th largest remaining error.
+// ---- level 0 ----------------------------------------------------------------
+// Status after level 0 resolved to binade b: an infinite boundary fixes the
+// k-th largest error already, and so does binade 0 when it holds only zero
+// errors; with a binary64 test side it also holds the subnormal errors,
+// which the next levels order like any other binade.
+__device__ __forceinline__ void level0_status(TopkState &st, int b, int tdtype) {
+    st.d0 = b;
+    st.level = 0;
+    const bool zero_only = b == 0 && tdtype != PEAT_F64;
+    st.status = (zero_only || b == kBins0 - 1) ? kTopkDone : kTopkActive;
+}
+
+// Level 0 from the pair's signature, which counts the same errors of the same
+// valid pairs: with one-binade bins regular bin i is binade field
+// lo + i + 1023, and errors below every bin are the zero errors alone when
+// the test side is not binary64 (a difference of two narrower values is a
+// multiple of 2^-149, far above the subnormal range).  Leaves the state open
+// when the record does not match the pair or does not fix the binade.
+__device__ void level0_from_sig(const peat_signature_t &g, const SigDesc &d, const TopkParams &P,
+                                TopkState &st) {
+    if (g.n != d.n || g.n_valid < 0) return;
+    uint64_t tot = (uint64_t)g.hist_zero + (uint64_t)g.hist_under + (uint64_t)g.hist_over;
+    for (int i = 0; i < P.nbins; ++i) tot += (uint64_t)g.hist[i];
+    if (tot != (uint64_t)g.n_valid) return;
+    const uint64_t nv = (uint64_t)g.n_valid;
+    const uint64_t k = (uint64_t)(((unsigned __int128)nv * (uint32_t)P.num + (uint32_t)P.den - 1) / (uint32_t)P.den);
+    st.n_valid = nv;
+    st.k = k;
+    if (k == 0) {
+        st.level = 0;
+        st.status = kTopkDone;
+        st.d0 = 0;
+        return;
+    }
+    uint64_t acc = (uint64_t)g.hist_over;
+    if (k <= acc) return;
+    const bool one_binade = P.hi - P.lo == P.nbins;
+    for (int i = P.nbins - 1; i >= 0; --i) {
+        const uint64_t c = (uint64_t)g.hist[i];
+        if (acc + c >= k) {
+            if (!one_binade) return;
+            st.need = k - acc;
+            st.cand = c;
+            st.key = (uint64_t)(P.lo + i + 1023) << 52;
+            level0_status(st, P.lo + i + 1023, d.tdtype);
+            return;
+        }
+        acc += c;
+    }
+    acc += (uint64_t)g.hist_under;
+    if (k <= acc || d.tdtype == PEAT_F64) return;
+    st.need = k - acc;
+    st.cand = (uint64_t)g.hist_zero;
+    st.key = 0;
+    level0_status(st, 0, d.tdtype);
+}
+
+__global__ void __launch_bounds__(kBlock) topk_init(TopkParams P) {
+    const int pair = blockIdx.x * kBlock + threadIdx.x;
+    if (pair == 0) {
+        P.fill[0] = 0;
+        P.fill[1] = 0;
+        P.ovf[2 * P.count] = 0;
+        P.ovf[2 * P.count + 1] = 0;
+    }
+    if (pair >= P.count) return;
+    P.ovf[2 * pair] = 0;
+    P.ovf[2 * pair + 1] = 0;
+    P.xsum[2 * pair] = 0;
+    P.xsum[2 * pair + 1] = 0;
+    TopkState st;
+    st.n_valid = 0;
+    st.k = 0;
+    st.need = 0;
+    st.cand = 0;
+    st.key = 0;
+    st.level = -1;
+    st.status = kTopkActive;
+    st.d0 = 0;
+    st.reserved = 0;
+    if (P.sigs) level0_from_sig(P.sigs[pair], P.descs[pair], P, st);
+    P.state[pair] = st;
+}
+
+// ---- streaming passes over the tensors ----------------------------------------
+enum { kPass1 = 0, kPassA = 1, kPassC = 2, kPassT = 3 };
+
+// pass 1: binade histogram of the pairs whose level 0 is open (one chunk per block)
+template <int DG, int DT>
+__device__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
+    const int pair = P.chunk_pair[gchunk];
+    if (P.state[pair].level >= 0) return;
+    const SigDesc d = P.descs[pair];
+    for (int b = threadIdx.x; b < kBins0; b += kBlock) h[b] = 0;
+    __syncthreads();
+    for_each_error<DG, DT>(d, gchunk - d.first_chunk, [&](uint64_t key, double) { atomicAdd(&h[key >> 52], 1u); });
+    flush_hist(h, kBins0, P.hist + (size_t)pair * kTopkBins);
+}
+
+// pass A (one chunk per block)
+template <int DG, int DT>
+__device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Table &tab, double *red) {
+    const int pair = P.chunk_pair[gchunk];
+    const TopkState st = P.state[pair];
+    // nothing above an infinite boundary; nothing at all when k = 0
+    if (st.k == 0 || st.d0 == kBins0 - 1) {
+        if (threadIdx.x == 0) P.part_a[gchunk] = 0.0;
+        return;
+    }
+    const SigDesc d = P.descs[pair];
+    const uint64_t d0 = (uint64_t)st.d0;
+    const bool active = st.status == kTopkActive;            // the boundary binade needs ordering
+    if (active) {
+        for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
+        table_init(tab);
+        __syncthreads();
+    }
+    double s = 0.0;
+    for_each_error<DG, DT>(d, gchunk - d.first_chunk, [&](uint64_t key, double a) {
+        const uint64_t e = key >> 52;
+        if (e > d0) {
+            s += a;
+        } else if (e == d0 && active) {
+            atomicAdd(&h[digit_of(key, 1)], 1u);
+            if (!__hip_atomic_load(&tab.full, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) && !table_count(tab, key))
+                tab.full = 1;
+        }
+    });
+    const double bs = block_sum(s, red);
+    if (threadIdx.x == 0) P.part_a[gchunk] = bs;
+    if (active) {
+        flush_hist(h, kTopkBins, P.hist + (size_t)pair * kTopkBins);
+        table_flush(tab, P, 0, pair);
+    }
+}
+
+// pass C (pairs whose binade did not fit): exact sum of their errors in D0
+// above bin D1 and gather of bin (D0, D1)
+template <int DG, int DT>
+__device__ void passC_chunk(const TopkParams &P, int64_t gchunk, Table &tab) {
+    const int pair = P.chunk_pair[gchunk];
+    const TopkState st = P.state[pair];
+    if (!(st.status == kTopkActive && st.level == 1 && P.ovf[2 * pair] != 0)) return;
+    const SigDesc d = P.descs[pair];
+    table_init(tab);
+    __syncthreads();
+    const uint64_t b1 = st.key >> digit_shift(1);           // binade and digit 1 of the boundary
+    const int d0 = st.d0;
+    uint64_t x = 0;
+    for_each_error<DG, DT>(d, gchunk - d.first_chunk, [&](uint64_t key, double) {
+        const uint64_t k1 = key >> digit_shift(1);
+        if ((k1 >> 13) == (b1 >> 13) && k1 > b1) x += signif(key, d0);
+        const bool in = k1 == b1;
+        const bool counted = in && table_count(tab, key);
+        spill_entry(in && !counted, key, P, pair);
+    });
+    block_add128(x, P.xsum + 2 * pair);
+    tab.full = 0;                                            // keys without a slot went out as entries
+    table_flush(tab, P, 1, pair);
+    __syncthreads();
+}
+
+// pass T_L (pairs whose bin (D0, D1) did not fit either): histogram of digit
+// L (L <= 4) among the errors on the level L-1 prefix, and (L >= 3) the
+// exact sum of the errors on the level L-2 prefix above digit D_{L-1}
+template <int DG, int DT>
+__device__ void passT_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
+    const int L = P.level;
+    const int pair = P.chunk_pair[gchunk];
+    const TopkState st = P.state[pair];
+    const bool want = L <= kTopkLevels - 1 ? (st.status == kTopkActive && st.level == L - 1) : st.level == L - 1;
+    if (!(want && P.ovf[2 * pair] != 0 && P.ovf[2 * pair + 1] != 0)) return;
+    const SigDesc d = P.descs[pair];
+    const bool hist = L <= kTopkLevels - 1;
+    const bool sum = L >= 3;
+    if (hist) {
+        for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
+        __syncthreads();
+    }
+    const int sh = digit_shift(hist ? L - 1 : 0);
+    const uint64_t ph = st.key >> sh;
+    const int sx = digit_shift(sum ? L - 2 : 0);
+    const uint64_t px = st.key >> sx;
+    const uint32_t dl = digit_of(st.key, sum ? L - 1 : 0);
+    const int d0 = st.d0;
+    uint64_t x = 0;
+    for_each_error<DG, DT>(d, gchunk - d.first_chunk, [&](uint64_t key, double) {
+        if (hist && (key >> sh) == ph) atomicAdd(&h[digit_of(key, L)], 1u);
+        if (sum && (key >> sx) == px && digit_of(key, L - 1) > dl) x += signif(key, d0);
+    });
+    if (sum) block_add128(x, P.xsum + 2 * pair);
+    if (hist) flush_hist(h, kTopkBins, P.hist + (size_t)pair * kTopkBins);
+    __syncthreads();
+}
+
+template <int DG, int DT, int OP>
+__global__ void __launch_bounds__(kBlock) topk_scan(TopkParams P) {
+    __shared__ uint32_t h[kTopkBins];
+    __shared__ double red[kWaves];
+    if constexpr (OP == kPass1) {
+        pass1_chunk<DG, DT>(P, P.chunk_base + blockIdx.x, h);
+    } else if constexpr (OP == kPassA) {
+        __shared__ Table tab;
+        passA_chunk<DG, DT>(P, P.chunk_base + blockIdx.x, h, tab, red);
+    } else if constexpr (OP == kPassC) {
+        __shared__ Table tab;
+        if (P.ovf[2 * P.count] == 0) return;                 // every binade fitted
+        for (int64_t c = blockIdx.x; c < P.kind_chunks; c += gridDim.x) passC_chunk<DG, DT>(P, P.chunk_base + c, tab);
+    } else {
+        if (P.ovf[2 * P.count + 1] == 0) return;             // every bin fitted
+        for (int64_t c = blockIdx.x; c < P.kind_chunks; c += gridDim.x) passT_chunk<DG, DT>(P, P.chunk_base + c, h);
+    }
+}
+
+// ---- selection -----------------------------------------------------------------
+// One block per pair: the bin of the level-L histogram holding the need-th
+// largest remaining error; the histogram is cleared for the next level.
 __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     const int pair = blockIdx.x;
     const int L = P.level;
-    if (L == 0 && P.skip0 && P.skip0[pair]) return;           // state written by the host
     TopkState st = P.state[pair];
-    if (L > 0 && !(st.status == kTopkActive && st.level == L - 1)) return;
+    if (L == 0 ? st.level != -1 : !(st.status == kTopkActive && st.level == L - 1)) return;
     const int nb = L == 0 ? kBins0 : kTopkBins;
     const int seg = nb / kBlock;
-    const uint64_t *H = P.hist + (size_t)pair * kTopkBins;
+    uint64_t *H = P.hist + (size_t)pair * kTopkBins;
+    __shared__ uint64_t hs[kTopkBins];
     __shared__ uint64_t ssum[kBlock];
+    for (int b = threadIdx.x; b < nb; b += kBlock) {
+        hs[b] = H[b];
+        H[b] = 0;
+    }
+    __syncthreads();
     {
         const int top = nb - (int)threadIdx.x * seg;          // thread t: bins [top - seg, top)
         uint64_t x = 0;
-        for (int b = top - 1; b >= top - seg; --b) x += H[b];
+        for (int b = top - 1; b >= top - seg; --b) x += hs[b];
         ssum[threadIdx.x] = x;
     }
     __syncthreads();
@@ -286,11 +537,10 @@ __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
         st.need = st.k;
         st.cand = 0;
         st.key = 0;
-        st.cnt[0] = st.cnt[1] = 0;
-        st.level = 0;
-        st.d0 = 0;
         if (st.k == 0) {
+            st.level = 0;
             st.status = kTopkDone;
+            st.d0 = 0;
             P.state[pair] = st;
             return;
         }
@@ -303,107 +553,62 @@ __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     int t = 0;
     while (t < kBlock - 1 && acc + ssum[t] < need) acc += ssum[t++];
     int b = nb - t * seg - 1;
-    while (b > nb - (t + 1) * seg && acc + H[b] < need) acc += H[b--];
+    while (b > nb - (t + 1) * seg && acc + hs[b] < need) acc += hs[b--];
     st.need = need - acc;                     // copies of the boundary bin taken, >= 1
-    st.cand = H[b];
+    st.cand = hs[b];
     st.key |= (uint64_t)b << digit_shift(L);
-    st.level = L;
     if (L == 0) {
-        st.d0 = b;
-        // An infinite boundary fixes the k-th largest error already, and so
-        // does binade 0 when it holds only zero errors: with a binary64 test
-        // side it also holds the subnormal errors, which the next levels
-        // order like any other binade.
-        const bool zero_only = b == 0 && P.descs[pair].tdtype != PEAT_F64;
-        st.status = (zero_only || b == kBins0 - 1) ? kTopkDone : kTopkActive;
+        level0_status(st, b, P.descs[pair].tdtype);
     } else {
+        st.level = L;
         st.status = L == kTopkLevels - 1 ? kTopkDone : kTopkActive;
     }
-    // the buffer the next copy fills starts empty
-    if (L == 1) st.cnt[0] = 0;
-    if (L >= 2) st.cnt[(L - 1) & 1] = 0;
     P.state[pair] = st;
 }
 
-// Candidate rounds (levels 2-4): keys[(L - 2) & 1] holds the (key, count)
-// entries of the pair's current boundary bin.
-__global__ void __launch_bounds__(kBlock) topk_cand_hist(TopkParams P) {
-    __shared__ unsigned long long h[kTopkBins];
-    const int L = P.level;
-    const int pair = P.cblk_pair[blockIdx.x];
-    const TopkState st = P.state[pair];
-    if (!(st.status == kTopkActive && st.level == L - 1)) return;
-    const int src = (L - 2) & 1;
-    const uint64_t n = st.cnt[src];
-    const uint64_t lo = (uint64_t)(blockIdx.x - P.cand[pair].first_blk) * kTopkCandBlock;
-    if (lo >= n) return;
-    const uint64_t hi = n - lo < (uint64_t)kTopkCandBlock ? n : lo + kTopkCandBlock;
-    for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
-    __syncthreads();
-    const uint64_t *e = P.keys[src] + 2 * P.cand[pair].off;
-    for (uint64_t i = lo + threadIdx.x; i < hi; i += kBlock)
-        atomicAdd(&h[digit_of(e[2 * i], L)], (unsigned long long)e[2 * i + 1]);
-    __syncthreads();
-    uint64_t *H = P.hist + (size_t)pair * kTopkBins;
-    for (int b = threadIdx.x; b < kTopkBins; b += kBlock)
-        if (h[b]) atomicAdd((unsigned long long *)&H[b], h[b]);
-}
-
-// Exact sum of the entries above the level-L boundary (count * significand,
-// all with exponent field d0) and copy of the entries on it.  Writes the
-// block's 128-bit sum for every block, zero when it has nothing to do.
-__global__ void __launch_bounds__(kBlock) topk_cand_sum(TopkParams P) {
-    __shared__ uint64_t red[kWaves][2];
-    const int L = P.level;
-    const int pair = P.cblk_pair[blockIdx.x];
-    const TopkState st = P.state[pair];
-    unsigned __int128 acc = 0;
-    if (st.level == L) {
-        const int src = (L - 2) & 1, dst = src ^ 1;
-        const uint64_t n = st.cnt[src];
-        const uint64_t lo = (uint64_t)(blockIdx.x - P.cand[pair].first_blk) * kTopkCandBlock;
-        const uint64_t hi = lo >= n ? lo : (n - lo < (uint64_t)kTopkCandBlock ? n : lo + kTopkCandBlock);
-        const uint32_t D = digit_of(st.key, L);
-        const uint64_t lead = st.d0 != 0 ? (uint64_t(1) << 52) : 0;   // implicit bit
-        const uint64_t *e = P.keys[src] + 2 * P.cand[pair].off;
-        uint64_t *out = P.keys[dst] + 2 * P.cand[pair].off;
-        uint64_t *cnt = &P.state[pair].cnt[dst];
-        for (uint64_t i0 = lo; i0 < hi; i0 += kBlock) {
-            const uint64_t i = i0 + threadIdx.x;
-            const bool in = i < hi;
-            const uint64_t key = in ? e[2 * i] : 0, c = in ? e[2 * i + 1] : 0;
-            const uint32_t dg = digit_of(key, L);
-            if (in && dg > D) acc += (unsigned __int128)c * ((key & kMant) | lead);
-            if (L < kTopkLevels - 1) append_entry(in && dg == D, key, c, cnt, out);
+// ---- rounds on the entries -------------------------------------------------------
+// Region 0 holds the binade gathers of pass A, region 1 the bin gathers of
+// pass C; an entry counts for its pair when the pair takes that route.
+template <typename F>
+__device__ __forceinline__ void for_each_entry(const TopkParams &P, F &&f) {
+    for (int r = 0; r < 2; ++r) {
+        const unsigned long long fill = P.fill[r];
+        const uint64_t n = fill < P.cap[r] ? fill : P.cap[r];
+        const TopkEntry *E = P.ents + (r ? P.cap[0] : 0);
+        for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (uint64_t)gridDim.x * kBlock) {
+            const TopkEntry e = E[i];
+            if (e.pair < 0 || e.pair >= P.count) continue;
+            if (pair_mode(P, e.pair) != (r ? kModeC : kModeA)) continue;
+            f(e);
         }
-    }
-    uint64_t lo_sum = (uint64_t)acc, hi_sum = (uint64_t)(acc >> 64);
-    // 128-bit block sum (integer: any order)
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const uint64_t ol = __shfl_xor(lo_sum, o), oh = __shfl_xor(hi_sum, o);
-        const uint64_t s = lo_sum + ol;
-        hi_sum += oh + (s < lo_sum);
-        lo_sum = s;
-    }
-    if ((threadIdx.x & 63) == 0) {
-        red[threadIdx.x >> 6][0] = lo_sum;
-        red[threadIdx.x >> 6][1] = hi_sum;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint64_t l = 0, h = 0;
-        for (int w = 0; w < kWaves; ++w) {
-            const uint64_t s = l + red[w][0];
-            h += red[w][1] + (s < l);
-            l = s;
-        }
-        uint64_t *x = P.xpart + 2 * ((size_t)(L - 2) * P.ncblk + blockIdx.x);
-        x[0] = l;
-        x[1] = h;
     }
 }
 
+// Level L (2-4): weighted histogram of digit L over the entries on the
+// pair's level L-1 prefix.
+__global__ void __launch_bounds__(kBlock) topk_ent_hist(TopkParams P) {
+    const int L = P.level;
+    for_each_entry(P, [&](const TopkEntry &e) {
+        const TopkState &st = P.state[e.pair];
+        if (!(st.status == kTopkActive && st.level == L - 1)) return;
+        const int sh = digit_shift(L - 1);
+        if ((e.key >> sh) != (st.key >> sh)) return;
+        atomicAdd((unsigned long long *)&P.hist[(size_t)e.pair * kTopkBins + digit_of(e.key, L)],
+                  (unsigned long long)e.count);
+    });
+}
+
+// Exact sum of the entries above the fixed boundary.
+__global__ void __launch_bounds__(kBlock) topk_ent_sum(TopkParams P) {
+    for_each_entry(P, [&](const TopkEntry &e) {
+        const TopkState &st = P.state[e.pair];
+        if (st.level != kTopkLevels - 1 || e.key <= st.key) return;
+        const unsigned __int128 v = (unsigned __int128)e.count * signif(e.key, st.d0);
+        atomic_add128(P.xsum + 2 * e.pair, (uint64_t)v, (uint64_t)(v >> 64));
+    });
+}
+
+// ---- records -------------------------------------------------------------------
 // Fixed-order sum over the pair's chunk partials (thread t sums chunks t,
 // t + 256, ... in order; then butterflies and waves in order).
 __device__ __forceinline__ double chunk_sum(const double *part, int64_t first, int64_t n, double *red) {
@@ -420,7 +625,6 @@ __global__ void __launch_bounds__(kBlock) topk_finalize(TopkParams P) {
     const SigDesc d = P.descs[pair];
     const TopkState st = P.state[pair];
     const double sa = chunk_sum(P.part_a, d.first_chunk, d.nchunks, red);
-    const double sb = chunk_sum(P.part_b, d.first_chunk, d.nchunks, red);
     if (threadIdx.x != 0) return;
     const double qnan = opaque_double(0x7FF80000u, 0u);
     const double inf = opaque_double(0x7FF00000u, 0u);
@@ -443,22 +647,14 @@ __global__ void __launch_bounds__(kBlock) topk_finalize(TopkParams P) {
         o.sum_topk = sa;
         o.mean_topk = sa / (double)st.k;
     } else {
-        // exact sum of the candidate parts: rounds 2-4, then need copies of T
-        unsigned __int128 x = 0;
-        const TopkCand c = P.cand[pair];
-        for (int r = 0; r < kTopkLevels - 2; ++r)
-            for (int b = 0; b < c.nblk; ++b) {
-                const uint64_t *xp = P.xpart + 2 * ((size_t)r * P.ncblk + c.first_blk + b);
-                x += ((unsigned __int128)xp[1] << 64) | xp[0];
-            }
-        // binade 0 (subnormal errors) has no implicit bit and the exponent of binade 1
-        const uint64_t lead = st.d0 != 0 ? (uint64_t(1) << 52) : 0;
-        x += (unsigned __int128)st.need * ((st.key & kMant) | lead);
+        // exact sum inside binade D0: everything above T, then need copies of T
+        unsigned __int128 x = ((unsigned __int128)P.xsum[2 * pair + 1] << 64) | P.xsum[2 * pair];
+        x += (unsigned __int128)st.need * signif(st.key, st.d0);
         const double xd = (double)(uint64_t)(x >> 64) * 0x1p64 + (double)(uint64_t)x;
         const double sc = __builtin_ldexp(xd, (st.d0 != 0 ? st.d0 : 1) - 1075);
         o.count_above = (int64_t)(st.k - st.need);
         o.kth_value = __longlong_as_double((long long)st.key);
-        o.sum_topk = (sa + sb) + sc;
+        o.sum_topk = sa + sc;
         o.mean_topk = o.sum_topk / (double)st.k;
     }
     P.outs[pair] = o;
@@ -468,30 +664,34 @@ __global__ void __launch_bounds__(kBlock) topk_zero(uint64_t *p, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) p[i] = 0;
 }
 
-template <int DG, int DT, int PASS>
-void launch_one(const TopkParams &q, int64_t n, hipStream_t s) {
-    hipLaunchKernelGGL((topk_pass<DG, DT, PASS>), dim3((unsigned)n), dim3(kBlock), 0, s, q);
+// ---- launches ---------------------------------------------------------------------
+template <int DG, int DT, int OP>
+void launch_one(const TopkParams &q, hipStream_t s) {
+    const int64_t n = q.kind_chunks;
+    const int64_t grid = (OP == kPass1 || OP == kPassA) ? n : (n < kScanGrid ? n : kScanGrid);
+    hipLaunchKernelGGL((topk_scan<DG, DT, OP>), dim3((unsigned)grid), dim3(kBlock), 0, s, q);
 }
 
-template <int PASS>
-hipError_t launch_pass_kinds(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
+template <int OP>
+hipError_t launch_scan(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
     static_assert(kKindTypes[3][1] == PEAT_F64 && kKindTypes[9][0] == PEAT_BF16, "kind table order");
     for (int kind = 0; kind < kKinds; ++kind) {
         const int64_t n = range[kind + 1] - range[kind];
         if (n <= 0) continue;
         TopkParams q = p;
         q.chunk_base = range[kind];
+        q.kind_chunks = n;
         switch (kind) {
-            case 0: launch_one<PEAT_F32, PEAT_F32, PASS>(q, n, s); break;
-            case 1: launch_one<PEAT_F16, PEAT_F16, PASS>(q, n, s); break;
-            case 2: launch_one<PEAT_BF16, PEAT_BF16, PASS>(q, n, s); break;
-            case 3: launch_one<PEAT_F32, PEAT_F64, PASS>(q, n, s); break;
-            case 4: launch_one<PEAT_F32, PEAT_F16, PASS>(q, n, s); break;
-            case 5: launch_one<PEAT_F32, PEAT_BF16, PASS>(q, n, s); break;
-            case 6: launch_one<PEAT_F16, PEAT_F32, PASS>(q, n, s); break;
-            case 7: launch_one<PEAT_BF16, PEAT_F32, PASS>(q, n, s); break;
-            case 8: launch_one<PEAT_F16, PEAT_F64, PASS>(q, n, s); break;
-            default: launch_one<PEAT_BF16, PEAT_F64, PASS>(q, n, s); break;
+            case 0: launch_one<PEAT_F32, PEAT_F32, OP>(q, s); break;
+            case 1: launch_one<PEAT_F16, PEAT_F16, OP>(q, s); break;
+            case 2: launch_one<PEAT_BF16, PEAT_BF16, OP>(q, s); break;
+            case 3: launch_one<PEAT_F32, PEAT_F64, OP>(q, s); break;
+            case 4: launch_one<PEAT_F32, PEAT_F16, OP>(q, s); break;
+            case 5: launch_one<PEAT_F32, PEAT_BF16, OP>(q, s); break;
+            case 6: launch_one<PEAT_F16, PEAT_F32, OP>(q, s); break;
+            case 7: launch_one<PEAT_BF16, PEAT_F32, OP>(q, s); break;
+            case 8: launch_one<PEAT_F16, PEAT_F64, OP>(q, s); break;
+            default: launch_one<PEAT_BF16, PEAT_F64, OP>(q, s); break;
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -499,47 +699,45 @@ hipError_t launch_pass_kinds(const TopkParams &p, const int64_t range[kKinds + 1
     return hipSuccess;
 }
 
-}  // namespace
-
-hipError_t launch_topk_zero(uint64_t *p, int64_t n, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    const int64_t blocks = (n + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL(topk_zero, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(kBlock), 0, s, p, n);
-    return hipGetLastError();
-}
-
-hipError_t launch_topk_pass(const TopkParams &p, int pass, const int64_t range[kKinds + 1], hipStream_t s) {
-    if (pass == 0) return launch_pass_kinds<0>(p, range, s);
-    if (pass == 1) return launch_pass_kinds<1>(p, range, s);
-    return launch_pass_kinds<2>(p, range, s);
-}
-
-hipError_t launch_topk_select(const TopkParams &p, int level, hipStream_t s) {
-    if (p.count <= 0) return hipSuccess;
+hipError_t launch_select(const TopkParams &p, int level, hipStream_t s) {
     TopkParams q = p;
     q.level = level;
     hipLaunchKernelGGL(topk_select, dim3((unsigned)p.count), dim3(kBlock), 0, s, q);
     return hipGetLastError();
 }
 
-hipError_t launch_topk_cand_hist(const TopkParams &p, int level, hipStream_t s) {
-    if (p.ncblk <= 0) return hipSuccess;
-    TopkParams q = p;
-    q.level = level;
-    hipLaunchKernelGGL(topk_cand_hist, dim3((unsigned)p.ncblk), dim3(kBlock), 0, s, q);
-    return hipGetLastError();
-}
+}  // namespace
 
-hipError_t launch_topk_cand_sum(const TopkParams &p, int level, hipStream_t s) {
-    if (p.ncblk <= 0) return hipSuccess;
-    TopkParams q = p;
-    q.level = level;
-    hipLaunchKernelGGL(topk_cand_sum, dim3((unsigned)p.ncblk), dim3(kBlock), 0, s, q);
-    return hipGetLastError();
-}
-
-hipError_t launch_topk_finalize(const TopkParams &p, hipStream_t s) {
+hipError_t launch_topk_level0(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
     if (p.count <= 0) return hipSuccess;
+    hipError_t e;
+    const int64_t nhist = (int64_t)kTopkBins * p.count;
+    const int64_t zb = (nhist + kBlock - 1) / kBlock;
+    hipLaunchKernelGGL(topk_zero, dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(kBlock), 0, s, p.hist, nhist);
+    hipLaunchKernelGGL(topk_init, dim3((unsigned)((p.count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scan<kPass1>(p, range, s)) != hipSuccess) return e;
+    return launch_select(p, 0, s);
+}
+
+hipError_t launch_topk_rest(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
+    if (p.count <= 0) return hipSuccess;
+    hipError_t e;
+    if ((e = launch_scan<kPassA>(p, range, s)) != hipSuccess) return e;
+    if ((e = launch_select(p, 1, s)) != hipSuccess) return e;
+    if ((e = launch_scan<kPassC>(p, range, s)) != hipSuccess) return e;
+    TopkParams q = p;
+    for (int L = 2; L <= kTopkLevels - 1; ++L) {
+        q.level = L;
+        hipLaunchKernelGGL(topk_ent_hist, dim3(kEntGrid), dim3(kBlock), 0, s, q);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_scan<kPassT>(q, range, s)) != hipSuccess) return e;
+        if ((e = launch_select(p, L, s)) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(topk_ent_sum, dim3(kEntGrid), dim3(kBlock), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    q.level = kTopkLevels;
+    if ((e = launch_scan<kPassT>(q, range, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(topk_finalize, dim3((unsigned)p.count), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }

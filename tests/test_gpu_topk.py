@@ -2,10 +2,12 @@
 the top 10% errors") against the oracle's sort: n_valid, k, count_above and
 the k-th largest error bit-exact; the sum and mean within 1e-12 relative
 (both are binary64 sums of k non-negative terms: the device's fixed tree plus
-exact integer candidate sums against the oracle's compensated sum).  Cases
-span several chunks with ragged tails in the three element types, special
-values, heavy ties (the candidate rounds on many equal keys), a zero and an
-infinite k-th error, unaligned pointers, batched against single calls, and a
+an exact integer sum inside the k-th largest error's binade, against the
+oracle's compensated sum).  Cases span several chunks with ragged tails in
+the three element types, special values, heavy ties, a zero and an infinite
+k-th error, unaligned pointers, batched against single calls, every route
+of the selection (binade gather, bin gather, one pass per digit) against the
+others, the stream-ordered forms against the synchronous ones, and a
 full-size Llama-7B-shaped tensor."""
 from __future__ import annotations
 
@@ -197,3 +199,125 @@ def test_from_signature_with_fused_step_records():
         got = P.topk_mean_from_signature_batched(pairs, sigs, num=num, den=den)
         for k in range(len(pairs)):
             assert same_record(got[k], ref3[k]), f"pair {k} {num}/{den}: {got[k]} != {ref3[k]}"
+
+
+def _route_cases():
+    """Pairs whose boundary binade holds few distinct errors (checkpoint-like
+    relative noise: the binade gather fits), many (independent values: the
+    gather overflows its table), ties on a grid, special values, a binary64
+    test side with subnormal errors, a zero k-th error, empty and unaligned
+    views; each spans several chunks with a ragged tail."""
+    from tests.parity import float_to_bits
+    rng = np.random.default_rng(8080)
+    cases = []
+    n = 600007
+    g = rng.standard_normal(n)
+    g32 = (0.02 * g).astype(np.float32)
+    t32 = (g32 * (1 + 1e-7 * rng.standard_normal(n))).astype(np.float32)
+    cases.append(("checkpoint f32", g32.view(np.uint32), t32.view(np.uint32), (0, 0)))
+    cases.append(("independent f32", float_to_bits(g, 0), float_to_bits(rng.standard_normal(n), 0), (0, 0)))
+    for code in (1, 2):
+        cases.append((f"independent dtype={code}", float_to_bits(g, code),
+                      float_to_bits(g + 0.01 * rng.standard_normal(n), code), (code, code)))
+        cases.append((f"specials dtype={code}", *special_pair(300001, code, seed=8100 + code), (code, code)))
+    q = rng.integers(0, 6, n).astype(np.float64)
+    cases.append(("grid ties", float_to_bits(g, 0), float_to_bits(g + q * 0.25, 0), (0, 0)))
+    t_zero = g32.copy()
+    t_zero[rng.integers(0, n, 40)] += 1.0
+    cases.append(("zero kth", g32.view(np.uint32), t_zero.view(np.uint32), (0, 0)))
+    # binary64 test side: 3% normal errors, the rest subnormal (the k-th
+    # largest error in binade 0, ordered by the later digits), with few and
+    # with many distinct values
+    normal = rng.random(n) < 0.03
+    gz = np.where(normal, g32, np.float32(0))
+    for name, vals in (("few", rng.integers(0, 8, n) << 20), ("many", rng.integers(0, 1 << 40, n))):
+        t64 = np.where(normal, gz.astype(np.float64) * (1 + 1e-3 * rng.standard_normal(n)),
+                       np.ldexp(vals.astype(np.float64), -1074))
+        cases.append((f"f32 vs f64 subnormal errors, {name}", gz.view(np.uint32), t64.view(np.uint64), (0, 3)))
+    cases.append(("empty", np.zeros(0, np.uint32), np.zeros(0, np.uint32), (0, 0)))
+    return cases
+
+
+def _dev(bits, code):
+    if code == 3:
+        return torch.from_numpy(bits.view(np.float64).copy()).cuda()
+    return to_device(bits, code)
+
+
+def _mixed_device(cases):
+    return [(_dev(gb, cg), _dev(tb, ct)) for _, gb, tb, (cg, ct) in cases]
+
+
+@pytest.mark.parametrize("caps", [(-1, -1), (0, -1), (0, 0), (64, 1 << 12)])
+def test_routes_give_identical_records(caps):
+    """Every route through the selection (binade gather, bin gather, one
+    histogram pass per digit, and capacities that overflow part way) gives
+    records bit-identical to the default route's and within the oracle's bar."""
+    cases = _route_cases()
+    pairs = _mixed_device(cases)
+    ref = {}
+    try:
+        P.topk_set_entry_capacity(-1, -1)
+        for num, den in ((1, 10), (1, 1000), (3, 7)):
+            ref[(num, den)] = P.topk_mean_mixed_batched(pairs, num, den)
+        P.topk_set_entry_capacity(*caps)
+        for num, den in ((1, 10), (1, 1000), (3, 7)):
+            log(f"  caps={caps} frac={num}/{den}")
+            got = P.topk_mean_mixed_batched(pairs, num, den)
+            for k, (name, gb, tb, (cg, ct)) in enumerate(cases):
+                assert same_record(got[k], ref[(num, den)][k]), f"{name} {num}/{den}: {got[k]} != {ref[(num, den)][k]}"
+                if (num, den) == (1, 10):
+                    assert_topk(got[k], oracle.topk_mixed(gb, tb, gdtype=cg, tdtype=ct, num=num, den=den), name)
+    finally:
+        P.topk_set_entry_capacity(-1, -1)
+
+
+def test_async_entry_points_match_sync():
+    """The stream-ordered forms: records in device memory equal to the
+    synchronous calls', with the signature records handed over on the same
+    stream (no host copy in between), and a record that does not match its
+    pair ignored rather than trusted."""
+    cases = _route_cases()
+    same = [(gb, tb, cg) for _, gb, tb, (cg, ct) in cases if cg == ct]
+    pairs = [(to_device(gb, c), to_device(tb, c)) for gb, tb, c in same]
+    prep = P.PreparedPairs(pairs)
+    stream = torch.cuda.Stream()
+    bins = (-40, 24, 64)
+    d_sig = torch.zeros(len(pairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    d_out = torch.zeros(len(pairs) * P.TOPK_BYTES, dtype=torch.uint8, device="cuda")
+    d_out2 = torch.zeros_like(d_out)
+    with torch.cuda.stream(stream):
+        P.signature_batched_async(prep, d_sig, bins, stream=stream)
+        P.topk_mean_from_signature_batched_async(prep, d_sig, d_out, bins, 1, 10, stream=stream)
+        P.topk_mean_batched_async(prep, d_out2, 1, 10, stream=stream)
+    stream.synchronize()
+    ref = P.topk_mean_batched(pairs, 1, 10)
+    got = P.decode_topk(d_out, len(pairs))
+    got2 = P.decode_topk(d_out2, len(pairs))
+    sigs = P.decode_records(d_sig, len(pairs))
+    got3 = P.topk_mean_from_signature_batched(pairs, sigs, bins, 1, 10)
+    for k in range(len(pairs)):
+        assert same_record(got[k], ref[k]) and same_record(got2[k], ref[k]) and same_record(got3[k], ref[k]), f"pair {k}"
+    # a record of another pair (n differs): ignored on the device
+    if len(pairs) >= 2:
+        host = d_sig.view(-1).cpu().numpy().copy()
+        rec = host.reshape(len(pairs), P.SIG_BYTES)
+        rec[0], rec[-1] = rec[-1].copy(), rec[0].copy()
+        d_bad = torch.from_numpy(host).cuda()
+        P.topk_mean_from_signature_batched_async(prep, d_bad, d_out, bins, 1, 10)
+        torch.cuda.synchronize()
+        got4 = P.decode_topk(d_out, len(pairs))
+        for k in range(len(pairs)):
+            assert same_record(got4[k], ref[k]), f"swapped records, pair {k}"
+    # mixed-precision forms
+    mpairs = _mixed_device(cases)
+    d_msig = torch.zeros(len(mpairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    d_mout = torch.zeros(len(mpairs) * P.TOPK_BYTES, dtype=torch.uint8, device="cuda")
+    d_mout2 = torch.zeros_like(d_mout)
+    P.signature_mixed_batched_async(mpairs, d_msig, bins)
+    P.topk_mean_mixed_from_signature_batched_async(mpairs, d_msig, d_mout, bins, 1, 10)
+    P.topk_mean_mixed_batched_async(mpairs, d_mout2, 1, 10)
+    torch.cuda.synchronize()
+    mref = P.topk_mean_mixed_batched(mpairs, 1, 10)
+    for k, (a, b) in enumerate(zip(P.decode_topk(d_mout, len(mpairs)), P.decode_topk(d_mout2, len(mpairs)))):
+        assert same_record(a, mref[k]) and same_record(b, mref[k]), f"mixed pair {k}"
