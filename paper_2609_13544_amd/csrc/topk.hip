@@ -151,6 +151,71 @@ __device__ __forceinline__ void for_each_error(const SigDesc &d, int64_t cin, F 
     }
 }
 
+// As for_each_error, one lane vector at a time: f(key, a, ok) with arrays of
+// VEC elements (ok: the element exists and is a valid pair), so that work on
+// the elements of a vector can be issued together.  Tail elements come one
+// per call, in element 0.
+template <int DG, int DT, typename F>
+__device__ __forceinline__ void for_each_error_vec(const SigDesc &d, int64_t cin, F &&f) {
+    using PT = PairTr<DG, DT>;
+    constexpr int VEC = PT::VEC;
+    constexpr int ESZG = Tr<DG>::W / 8, ESZT = Tr<DT>::W / 8;
+    constexpr int BG = PT::BG, BT = PT::BT;
+    constexpr int U = VEC > 4 ? 2 : 4;                        // vectors in flight per lane
+    const int64_t off = cin << d.chunk_log2;
+    const int64_t rest = d.n - off;
+    const uint32_t len = (uint32_t)(rest < (int64_t(1) << d.chunk_log2) ? rest : (int64_t(1) << d.chunk_log2));
+    const char *gbase = static_cast<const char *>(d.g) + off * ESZG;
+    const char *tbase = static_cast<const char *>(d.t) + off * ESZT;
+    const uint32_t nvec = d.aligned ? len / VEC : 0;
+    constexpr int NB = VEC < 4 ? VEC : 4;                     // elements per call
+    uint64_t key[NB];
+    double a[NB];
+    bool ok[NB];
+    if (nvec > 0) {
+        const __amdgpu_buffer_rsrc_t grs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)gbase, (short)0, (int)(nvec * BG), kBufFlags);
+        const __amdgpu_buffer_rsrc_t trs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)tbase, (short)0, (int)(nvec * BT), kBufFlags);
+        uint32_t v = threadIdx.x;
+        for (; v + (U - 1) * kBlock < nvec; v += U * kBlock) {
+            u32x4 gv[U], tv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                gv[u] = buf_load<BG, kLoadNT>(grs, (int)((v + u * kBlock) * BG), 0);
+                tv[u] = buf_load<BT, kLoadNT>(trs, (int)((v + u * kBlock) * BT), 0);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+                for (int jb = 0; jb < VEC; jb += NB) {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+                        ok[j] = error_of<DG, DT>(lane_elem<DG>(gv[u], jb + j), lane_elem<DT>(tv[u], jb + j), key[j], a[j]);
+                    f(key, a, ok);
+                }
+            }
+        }
+        for (; v < nvec; v += kBlock) {
+            const u32x4 gv = buf_load<BG, kLoadNT>(grs, (int)(v * BG), 0);
+            const u32x4 tv = buf_load<BT, kLoadNT>(trs, (int)(v * BT), 0);
+#pragma unroll
+            for (int jb = 0; jb < VEC; jb += NB) {
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+                    ok[j] = error_of<DG, DT>(lane_elem<DG>(gv, jb + j), lane_elem<DT>(tv, jb + j), key[j], a[j]);
+                f(key, a, ok);
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 1; j < NB; ++j) ok[j] = false;
+    for (uint32_t i = nvec * VEC + threadIdx.x; i < len; i += kBlock) {
+        ok[0] = error_of<DG, DT>(load_elem<DG>(gbase, i), load_elem<DT>(tbase, i), key[0], a[0]);
+        f(key, a, ok);
+    }
+}
+
 // Block sum of one binary64 per thread in a fixed order (wave butterflies,
 // then the waves in order); the result is valid in thread 0.
 __device__ __forceinline__ double block_sum(double x, double *red) {
@@ -212,8 +277,12 @@ __device__ __forceinline__ void table_init(Table &t) {
 
 // Counts key in the table (open addressing, slots go from empty to one key
 // only); false when its probe sequence is full of other keys.
+__device__ __forceinline__ uint32_t table_slot(uint64_t key) {
+    return (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> 55);                 // 9 bits
+}
+
 __device__ __forceinline__ bool table_count(Table &t, uint64_t key) {
-    const uint32_t h = (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> 55);    // 9 bits
+    const uint32_t h = table_slot(key);
 #pragma unroll 1
     for (int p = 0; p < kProbes; ++p) {
         const uint32_t slot = (h + p) & (kTable - 1);
@@ -238,7 +307,9 @@ __device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r
         if (t.cnt[i]) atomicAdd(&t.n, 1u);
     __syncthreads();
     if (threadIdx.x == 0) {
-        const uint32_t n = t.n;
+        // positions are taken only for a complete table; taken positions that
+        // run past the region's end are given back as unused entries
+        uint32_t n = t.full ? 0u : t.n;
         unsigned long long base = 0;
         uint32_t ok = t.full == 0;
         if (n > 0) {
@@ -251,6 +322,7 @@ __device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r
         }
         t.base = base;
         t.ok = ok;
+        t.n = n;
     }
     __syncthreads();
     TopkEntry *E = P.ents + (r ? P.cap[0] : 0);
@@ -387,7 +459,10 @@ __device__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
     flush_hist(h, kBins0, P.hist + (size_t)pair * kTopkBins);
 }
 
-// pass A (one chunk per block)
+// pass A (one chunk per block).  Each error of binade D0 is counted once:
+// in the gather table, or (once a key of this thread found no slot) in the
+// digit-1 histogram; at the end the table's counts go into that histogram
+// too (in LDS when the block overflowed, else straight to the pair's).
 template <int DG, int DT>
 __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Table &tab, double *red) {
     const int pair = P.chunk_pair[gchunk];
@@ -406,22 +481,60 @@ __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Ta
         __syncthreads();
     }
     double s = 0.0;
-    for_each_error<DG, DT>(d, gchunk - d.first_chunk, [&](uint64_t key, double a) {
-        const uint64_t e = key >> 52;
-        if (e > d0) {
-            s += a;
-        } else if (e == d0 && active) {
-            atomicAdd(&h[digit_of(key, 1)], 1u);
-            if (!__hip_atomic_load(&tab.full, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) && !table_count(tab, key))
-                tab.full = 1;
+    bool spill = false;                                       // this thread's keys go to the histogram
+    for_each_error_vec<DG, DT>(d, gchunk - d.first_chunk, [&](const auto &key, const auto &a, const auto &ok) {
+        constexpr int V = sizeof(ok) / sizeof(ok[0]);
+        bool in[V];
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            const uint64_t e = key[j] >> 52;
+            if (ok[j] && e > d0) s += a[j];
+            in[j] = ok[j] && e == d0 && active;
         }
+        if (!spill) {
+            // first probes of the vector's keys issued together; a key found
+            // there is counted, others take the full probe sequence
+            uint32_t slot[V];
+            uint64_t cur[V];
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                slot[j] = table_slot(key[j]);
+                cur[j] = in[j] ? __hip_atomic_load(&tab.key[slot[j]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
+                               : kEmpty;
+            }
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                if (!in[j]) continue;
+                if (cur[j] == key[j]) {
+                    atomicAdd(&tab.cnt[slot[j]], 1u);
+                    in[j] = false;
+                } else if (table_count(tab, key[j])) {
+                    in[j] = false;
+                } else {
+                    spill = true;
+                    tab.full = 1;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < V; ++j)
+            if (in[j]) atomicAdd(&h[digit_of(key[j], 1)], 1u);
     });
     const double bs = block_sum(s, red);
     if (threadIdx.x == 0) P.part_a[gchunk] = bs;
-    if (active) {
-        flush_hist(h, kTopkBins, P.hist + (size_t)pair * kTopkBins);
-        table_flush(tab, P, 0, pair);
+    if (!active) return;
+    __syncthreads();
+    uint64_t *H = P.hist + (size_t)pair * kTopkBins;
+    if (tab.full) {
+        for (int i = threadIdx.x; i < kTable; i += kBlock)
+            if (tab.cnt[i]) atomicAdd(&h[digit_of(tab.key[i], 1)], tab.cnt[i]);
+        flush_hist(h, kTopkBins, H);
+    } else {
+        for (int i = threadIdx.x; i < kTable; i += kBlock)
+            if (tab.cnt[i])
+                atomicAdd((unsigned long long *)&H[digit_of(tab.key[i], 1)], (unsigned long long)tab.cnt[i]);
     }
+    table_flush(tab, P, 0, pair);
 }
 
 // pass C (pairs whose binade did not fit): exact sum of their errors in D0
