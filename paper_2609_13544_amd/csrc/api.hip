@@ -284,6 +284,15 @@ int build_descs(const peat_mixed_pair_t *pairs, int32_t count, std::vector<SigDe
     return PEAT_OK;
 }
 
+// Elements of each kind's pairs (the chunk pass sizes its block groups by them).
+void set_kind_elems(SigParams &P, const peat_mixed_pair_t *pairs, int32_t count) {
+    for (int kind = 0; kind < kKinds; ++kind) P.kind_elems[kind] = 0;
+    for (int k = 0; k < count; ++k) {
+        const int kind = pair_kind(pairs[k].golden_dtype, pairs[k].test_dtype);
+        if (kind >= 0) P.kind_elems[kind] += pairs[k].n;
+    }
+}
+
 // The bins and closeness tests of a signature launch.
 void set_bins_thr(SigParams &P, const peat_bins_t &bins, const peat_thresholds_t &thr) {
     P.lo = bins.lo_log2;
@@ -293,7 +302,6 @@ void set_bins_thr(SigParams &P, const peat_bins_t &bins, const peat_thresholds_t
     P.nthr_pad = thr.count <= 2 ? 2 : (thr.count <= 4 ? 4 : 8);
     P.thr_min = HUGE_VAL;
     P.any_rtol = 0;
-    P.pad = 0;
     for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) {
         P.thr[j] = j < thr.count ? thr.abs_tol[j] : HUGE_VAL;
         P.rthr[j] = j < thr.count ? thr.rel_tol[j] : 0.0;
@@ -329,35 +337,50 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     int64_t range[kKinds + 1];
     if ((rc = build_descs(pairs, count, descs, range, &total))) return rc;
 
-    const size_t b_desc = align_up(sizeof(SigDesc) * count);
+    // A lone pair without injection travels in the kernel arguments: nothing
+    // to stage, and no copy ahead of the chunk pass.
+    const bool single = count == 1 && !inj;
+    const size_t b_desc = single ? 0 : align_up(sizeof(SigDesc) * count);
     const size_t b_inj = inj ? align_up(sizeof(InjDesc) * count) : 0;
-    const size_t b_map = align_up(sizeof(int32_t) * (size_t)total);
+    const size_t b_map = single ? 0 : align_up(sizeof(int32_t) * (size_t)total);
     const size_t b_part = align_up(sizeof(ChunkPartial) * (size_t)total);
     const size_t b_out = host_outs ? align_up(sizeof(peat_signature_t) * count) : 0;
+    const size_t b_stage = b_desc + b_inj + b_map;
 
     // device workspace: descriptors | injection descriptors | chunk map |
     // chunk records | records; the first three are staged and copied at once
     char *ws;
-    if ((rc = acquire_ws(d, b_desc + b_inj + b_map + b_part + b_out, s, &ws))) return rc;
-    Slot *sl;
-    if ((rc = acquire_slot(d, b_desc + b_inj + b_map + b_out, &sl))) return rc;
-    char *h = static_cast<char *>(sl->host);
-    std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
-    if (inj) std::memcpy(h + b_desc, inj->data(), sizeof(InjDesc) * count);
-    int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc + b_inj);
-    for (int k = 0; k < count; ++k)
-        for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
-    HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + b_inj + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+    if ((rc = acquire_ws(d, b_stage + b_part + b_out, s, &ws))) return rc;
+    Slot *sl = nullptr;
+    char *h = nullptr;
+    if (b_stage + b_out > 0) {
+        if ((rc = acquire_slot(d, b_stage + b_out, &sl))) return rc;
+        h = static_cast<char *>(sl->host);
+    }
+    if (!single) {
+        std::memcpy(h, descs.data(), sizeof(SigDesc) * count);
+        if (inj) std::memcpy(h + b_desc, inj->data(), sizeof(InjDesc) * count);
+        int32_t *hmap = reinterpret_cast<int32_t *>(h + b_desc + b_inj);
+        for (int k = 0; k < count; ++k)
+            for (int32_t c = 0; c < descs[k].nchunks; ++c) hmap[descs[k].first_chunk + c] = k;
+        HIP_OR_FAIL(hipMemcpyAsync(ws, h, b_desc + b_inj + sizeof(int32_t) * (size_t)total, hipMemcpyHostToDevice, s));
+    }
 
-    SigParams P;
+    SigParams P{};
     P.chunk_base = 0;
-    P.descs = reinterpret_cast<const SigDesc *>(ws);
-    P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc + b_inj);
-    P.partials = reinterpret_cast<ChunkPartial *>(ws + b_desc + b_inj + b_map);
-    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_desc + b_inj + b_map + b_part) : d_outs;
+    P.single = single ? 1 : 0;
+    if (single) {
+        P.one = descs[0];
+    } else {
+        P.descs = reinterpret_cast<const SigDesc *>(ws);
+        P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc + b_inj);
+    }
+    P.partials = reinterpret_cast<ChunkPartial *>(ws + b_stage);
+    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_stage + b_part) : d_outs;
     P.inj_counts = inj ? d_counts : nullptr;
     P.count = count;
     set_bins_thr(P, *bins, *thr);
+    set_kind_elems(P, pairs, count);
 
     hipEvent_t ev;
     if ((rc = prof_begin(d, s, &ev))) return rc;
@@ -370,10 +393,10 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     HIP_OR_FAIL(launch_sig_finalize(P, s));
     if ((rc = prof_end(d, s, 1, ev))) return rc;
 
-    char *hout = h + b_desc + b_inj + b_map;
+    char *hout = h ? h + b_stage : nullptr;
     if (host_outs)
         HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_signature_t) * count, hipMemcpyDeviceToHost, s));
-    if ((rc = release_slot(*sl, s))) return rc;
+    if (sl && (rc = release_slot(*sl, s))) return rc;
     if ((rc = release_ws(d, s))) return rc;
     if (host_outs) {
         HIP_OR_FAIL(hipStreamSynchronize(s));
@@ -827,7 +850,7 @@ int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_b
         }
     }
 
-    SigParams P;
+    SigParams P{};
     P.chunk_base = 0;
     P.chunk_count = 0;
     P.chunk_group = 1;
@@ -838,6 +861,7 @@ int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_b
     P.inj_counts = nullptr;
     P.count = count;
     set_bins_thr(P, *bins, *thr);
+    for (int k = 0; k < count; ++k) P.kind_elems[pair_kind(pairs[k].dtype, pairs[k].dtype)] += pairs[k].n;
     HIP_OR_FAIL(launch_sig_chunks(P, range, s));
     HIP_OR_FAIL(launch_sig_finalize(P, s));
     return PEAT_OK;

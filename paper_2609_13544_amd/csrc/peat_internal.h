@@ -103,7 +103,10 @@ struct SigParams {
     double rthr[PEAT_MAX_THRESHOLDS];  // relative tolerances
     double thr_min;                // smallest thr (+Inf when there are none)
     int32_t any_rtol;              // some relative tolerance is nonzero
-    int32_t pad;
+    int32_t single;                // one pair, described by `one` (descs and chunk_pair unused)
+    SigDesc one;
+    int64_t kind_elems[kKinds];    // elements of the pairs of each kind
+    int64_t launch_elems;          // elements of this launch's chunks
 };
 
 struct InjDesc {                 // one per injected tensor (80 bytes)

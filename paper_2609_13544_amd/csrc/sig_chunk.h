@@ -78,11 +78,14 @@ constexpr double kRelMargin = 0x1p-30;   // relative slack of the max-rel filter
 constexpr double kRareRel = 0.25;
 constexpr int kDeferCap = 32;            // deferred vectors per wave before a flush
 // Chunks per block: one while the launch has few chunks (every chunk gets a
-// block of its own), two once there are enough for at least kMinRounds rounds
-// of resident blocks: block start-up is shared by two chunks while blocks stay
-// short enough for the hardware to balance the load at the end of the launch.
-constexpr int64_t kMaxGroup = 2;
+// block of its own); more once there are enough for at least kMinRounds
+// rounds of resident blocks, up to about kGroupElems elements per block at
+// the launch's average chunk size (two chunks of 2^18, eight of 2^16): block
+// start-up is shared by the group while blocks stay short enough for the
+// hardware to balance the load at the end of the launch.
+constexpr int64_t kMaxGroup = 8;
 constexpr int64_t kMinRounds = 8;
+constexpr int64_t kGroupElems = int64_t(1) << 19;
 // a lane's 16-bit histogram counters hold a whole run of chunks
 static_assert(kMaxGroup * (int64_t(1) << kMaxChunkLog2) / kBlock < 65536, "histogram counter width");
 constexpr int kHistCols = kBlock / 2;     // histogram words per slot
@@ -859,8 +862,8 @@ struct ChunkCtx {
 // independent of grouping, so it is carried over the block's run of
 // consecutive chunks of one pair (indices relative to the run) and reduced
 // once, into the record of the run's last chunk; the other records of the run
-// hold neutral values there.  A run has at most kMaxGroup (2) chunks of at
-// most 2^18 elements, so a lane counts at most 2048 elements per histogram
+// hold neutral values there.  A run has at most kMaxGroup (8) chunks of at
+// most 2^18 elements, so a lane counts at most 8192 elements per histogram
 // slot.
 template <int DG, int DT, int NT, bool RT, bool INJ>
 __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const SigDesc *__restrict__ descs,
@@ -887,8 +890,8 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
     };
     auto pair_of = [&](int64_t c) {
         PairS d;
-        d.pair = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)chunk_pair[P.chunk_base + c]);
-        const SigDesc &dm = descs[d.pair];
+        d.pair = P.single ? 0 : (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)chunk_pair[P.chunk_base + c]);
+        const SigDesc &dm = P.single ? P.one : descs[d.pair];
         d.g = reinterpret_cast<const char *>(uniform_u64(reinterpret_cast<uint64_t>(dm.g)));
         d.t = reinterpret_cast<const char *>(uniform_u64(reinterpret_cast<uint64_t>(dm.t)));
         d.n = (int64_t)uniform_u64((uint64_t)dm.n);
@@ -1042,7 +1045,7 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
             dpp_max(mxr, ixr);
             dpp_max(mu, ixu);
             const uint32_t fnan = dpp_min_u32(L.first_nan), fval = dpp_min_u32(L.first_valid);
-            // at most 2^43 per lane (2048 distances below 2^32): exact in binary64
+            // at most 2^45 per lane (8192 distances below 2^32): exact in binary64
             const uint64_t sulp = (uint64_t)dpp_sum((double)L.s_ulp);
             if (lane == 0) {
                 sh.rmax[wave][0] = mxa;
@@ -1089,16 +1092,21 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
             dsum_step<kDppXor1, 0xF>(acc);        // the four quarters of the slot
             dsum_step<kDppXor2, 0xF>(acc);
             if (q == 0) out->hist[slot] = acc;
-            // slots 64..66 (beyond 256/4 threads): one thread each
-            if (tid < kHistSlots - 64) {
-                const int s2 = 64 + tid;
+            // slots 64..66 (beyond 256/4 threads): 32 threads each, four
+            // words per thread, summed across the 32 lanes (one half-wave)
+            static_assert(kHistSlots - 64 <= 3 && kHistCols == 4 * 32, "tail slots");
+            if (tid < 32 * (kHistSlots - 64)) {
+                const int s2 = 64 + (tid >> 5), k0 = (tid & 31) * 4;
                 uint32_t a2 = 0;
-                for (int k = 0; k < kHistCols; ++k) {
-                    const uint32_t w = sh.hist[s2 * kHistCols + k];
-                    sh.hist[s2 * kHistCols + k] = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t w = sh.hist[s2 * kHistCols + k0 + k];
+                    sh.hist[s2 * kHistCols + k0 + k] = 0;
                     a2 += (w & 0xFFFFu) + (w >> 16);
                 }
-                out->hist[s2] = a2;
+#pragma unroll
+                for (int o = 16; o >= 1; o >>= 1) a2 += __shfl_xor(a2, o);
+                if ((tid & 31) == 0) out->hist[s2] = a2;
             }
         }
         // the waves' totals, one field per thread, waves in order
@@ -1313,8 +1321,11 @@ int64_t resident_blocks() {
 template <int DG, int DT, int NT, bool RT, bool INJ>
 void launch_chunks(const SigParams &p, int64_t n, const InjDesc *inj, hipStream_t s) {
     const int64_t r = resident_blocks<DG, DT, NT, RT, INJ>();
+    const int64_t avg = p.launch_elems / n;
+    int64_t kmax = kGroupElems / (avg > 0 ? avg : 1);
+    kmax = kmax < 2 ? 2 : (kmax > kMaxGroup ? kMaxGroup : kmax);
     int64_t k = n / (kMinRounds * r);
-    k = k < 1 ? 1 : (k > kMaxGroup ? kMaxGroup : k);
+    k = k < 1 ? 1 : (k > kmax ? kmax : k);
     SigParams q = p;
     q.chunk_count = n;
     q.chunk_group = k;

@@ -8,7 +8,7 @@ namespace {
 // ---- pass 2 ----------------------------------------------------------------
 __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     const int pair = blockIdx.x;
-    const SigDesc d = P.descs[pair];
+    const SigDesc d = P.single ? P.one : P.descs[pair];
     const ChunkPartial *parts = P.partials + d.first_chunk;
     const int m = d.nchunks;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -37,13 +37,19 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
             for (int w = 1; w < kWaves; ++w) t += p.s[w][k];
             s[k] += t;
         }
-        if (p.ix_abs >= 0 && (ia < 0 || p.max_abs > ma || (p.max_abs == ma && p.ix_abs < ia))) { ma = p.max_abs; ia = p.ix_abs; }
-        if (p.ix_rel >= 0 && (ir < 0 || p.max_rel > mr || (p.max_rel == mr && p.ix_rel < ir))) { mr = p.max_rel; ir = p.ix_rel; }
-        if (p.ix_ulp >= 0 && (iu < 0 || p.max_ulp > mu || (p.max_ulp == mu && p.ix_ulp < iu))) { mu = p.max_ulp; iu = p.ix_ulp; }
-        if (p.first_nan >= 0 && (fn < 0 || p.first_nan < fn)) fn = p.first_nan;
-        if (p.first_valid >= 0 && (fv < 0 || p.first_valid < fv)) fv = p.first_valid;
-        sulp += p.sum_ulp;
-        if (P.inj_counts) flips += p.flips;
+        // every field read before any comparison, so the loads go out together
+        // instead of one round trip per branch
+        const double pma = p.max_abs, pmr = p.max_rel;
+        const int64_t pia = p.ix_abs, pir = p.ix_rel, piu = p.ix_ulp, pfn = p.first_nan, pfv = p.first_valid;
+        const uint64_t pmu = p.max_ulp, psu = p.sum_ulp;
+        const uint32_t pfl = p.flips;
+        if (pia >= 0 && (ia < 0 || pma > ma || (pma == ma && pia < ia))) { ma = pma; ia = pia; }
+        if (pir >= 0 && (ir < 0 || pmr > mr || (pmr == mr && pir < ir))) { mr = pmr; ir = pir; }
+        if (piu >= 0 && (iu < 0 || pmu > mu || (pmu == mu && piu < iu))) { mu = pmu; iu = piu; }
+        if (pfn >= 0 && (fn < 0 || pfn < fn)) fn = pfn;
+        if (pfv >= 0 && (fv < 0 || pfv < fv)) fv = pfv;
+        sulp += psu;
+        if (P.inj_counts) flips += pfl;
 #pragma unroll
         for (int k = 0; k < kCnt; ++k) cn[k] += p.cnt[k];
 #pragma unroll
@@ -181,6 +187,7 @@ hipError_t launch_sig_chunks(const SigParams &p, const int64_t range[kKinds + 1]
         if (n <= 0) continue;
         SigParams q = p;
         q.chunk_base = range[kind];
+        q.launch_elems = p.kind_elems[kind];
         hipError_t e;
         switch (kind) {
             case 0: e = launch_kind<PEAT_F32, PEAT_F32>(q, n, s); break;
@@ -200,6 +207,7 @@ hipError_t launch_sig_chunks_inject(const SigParams &p, const int64_t range[kKin
         if (n <= 0) continue;
         SigParams q = p;
         q.chunk_base = range[kind];
+        q.launch_elems = p.kind_elems[kind];
         hipError_t e;
         switch (kind) {
             case 0: e = launch_kind_inject<PEAT_F32>(q, n, inj, s); break;

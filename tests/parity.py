@@ -129,6 +129,15 @@ def chunk_count(n: int) -> int:
 TWO_CHUNK_MIN = 2 * 8 * 3 * 256
 
 
+def group_size(nchunks: int, nelems: int, resident: int = 3 * 256) -> int:
+    """Chunks per block of a chunk-pass launch: nchunks // (8 x resident),
+    clamped to [1, kmax] with kmax = 2^19 // (average chunk size) in [2, 8]."""
+    if nchunks == 0:
+        return 1
+    kmax = max(2, min(8, (1 << 19) // max(1, nelems // nchunks)))
+    return max(1, min(kmax, nchunks // (8 * resident)))
+
+
 def records_equal(a: dict, b: dict) -> bool:
     """Bit-level equality of two decoded records (NaN equals NaN)."""
     return a.keys() == b.keys() and all(
