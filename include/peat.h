@@ -315,13 +315,13 @@ int peat_signature_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t c
  * kth_value are exact.  sum_topk is the binary64 sum, in a fixed order, of
  * the errors above the binade of kth_value plus the exact sum of the others
  * (within 1e-12 relative of the exact sum), bit-identical between calls and
- * between every entry point below.  Two streaming passes over golden and
+ * between the entry points below (the signature-fed ones as they state).  Two streaming passes over golden and
  * test (a binade histogram, then one pass that sums, histograms and gathers
  * the k-th largest error's binade); a pair whose binade holds too many
  * distinct errors for the gather takes one more pass (a gather of its top 13
  * mantissa bits), and one whose bin still does not fit one pass per
  * remaining digit.  No step waits on the host; the call waits for its
- * result. */
+ * result.  sum_topk and mean_topk are equal across the routes. */
 int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
                    int32_t num, int32_t den, peat_topk_t *out);
 
@@ -351,14 +351,20 @@ int peat_topk_mean_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t c
  * holds: sigs is a host array of count records that peat_signature_batched
  * (or its async form) wrote for the same pairs with these bins; thresholds do
  * not matter.  The histogram counts the same errors of the same valid pairs,
- * so with one-binade bins (hi_log2 - lo_log2 == nbins) it fixes the binade of
- * the k-th largest error whenever that falls in a regular bin (or, with a
- * test type other than binary64, among the zero errors), and the binade
- * histogram pass skips the pair: one streaming pass then does the rest.
- * Other pairs, and other bins, take the binade pass too.  outs are
- * bit-identical to peat_topk_mean_batched's.  PEAT_EINVAL when a record's n
- * differs from its pair's or its histogram total from its n_valid.
- * (Section IV-B.3; Section V-D histograms.) */
+ * so it bounds the k-th largest error to one bin, and the binade histogram
+ * pass skips the pair: one streaming pass does the rest.  With one-binade
+ * bins (hi_log2 - lo_log2 == nbins) and the boundary in a regular bin (or,
+ * with a test type other than binary64, among the zero errors) that bin is
+ * the boundary's binade, and outs are bit-identical to
+ * peat_topk_mean_batched's.  Otherwise (the under or over bin, or wider
+ * bins) the pass gathers the bin's whole range of binades, and n_valid, k,
+ * count_above and kth_value are identical while sum_topk and mean_topk are
+ * formed in another order (within 1e-12 relative; equal whenever the errors
+ * inside the range sum exactly in binary64).  A range with too many
+ * distinct errors for the gather falls back to the binade pass (and then
+ * bit-identical records).  PEAT_EINVAL when a record's n differs from its
+ * pair's or its histogram total from its n_valid.  (Section IV-B.3;
+ * Section V-D histograms.) */
 int peat_topk_mean_from_signature_batched(const peat_pair_t *pairs, int32_t count, int32_t num,
                                           int32_t den, const peat_signature_t *sigs,
                                           const peat_bins_t *bins, peat_topk_t *outs);
@@ -377,7 +383,7 @@ int peat_topk_mean_from_signature_batched_async(const peat_pair_t *pairs, int32_
 
 /* peat_topk_mean_from_signature_batched over mixed-precision pairs, with the
  * records of peat_signature_mixed_batched (or its async form) for the same
- * pairs and bins; outs are bit-identical to peat_topk_mean_mixed_batched's. */
+ * pairs and bins; outs relate to peat_topk_mean_mixed_batched's as above. */
 int peat_topk_mean_mixed_from_signature_batched(const peat_mixed_pair_t *pairs, int32_t count,
                                                 int32_t num, int32_t den, const peat_signature_t *sigs,
                                                 const peat_bins_t *bins, peat_topk_t *outs);

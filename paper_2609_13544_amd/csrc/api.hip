@@ -638,6 +638,7 @@ int inject_signature_core(const peat_pair_t *pairs, int32_t count, const uint64_
 int64_t g_topk_cap[2] = {-1, -1};
 constexpr int64_t kTopkCapMin = int64_t(1) << 16;
 constexpr int64_t kTopkCapPerChunk[2] = {256, 64};
+constexpr int kBins0Topk = 2048;         // binade field values (exact sums per binade)
 
 // Mean of the k largest errors (see topk.hip): every step stream-ordered.
 // With host_outs the records go through workspace + pinned staging and the
@@ -694,8 +695,8 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     const size_t b_state = align_up(sizeof(TopkState) * count);
     const size_t b_hist = align_up(sizeof(uint64_t) * kTopkBins * (size_t)count);
     const size_t b_part = align_up(sizeof(double) * (size_t)total);
-    const size_t b_xsum = align_up(2 * sizeof(uint64_t) * count);
-    const size_t b_ovf = align_up(sizeof(uint32_t) * (2 * (size_t)count + 2));
+    const size_t b_xsum = align_up(2 * sizeof(uint64_t) * kBins0Topk * (size_t)count);
+    const size_t b_ovf = align_up(sizeof(uint32_t) * (2 * (size_t)count + 3));
     const size_t b_fill = align_up(2 * sizeof(unsigned long long));
     const size_t b_ents = align_up(sizeof(TopkEntry) * (size_t)(cap[0] + cap[1]));
     // device workspace: descriptors | chunk map | signatures | records (the

@@ -140,28 +140,31 @@ struct InjParams {
 // mantissa bits each (8192 bins).  The boundary's binade D0 comes from the
 // pair's signature or from a binade histogram; one pass then sums the errors
 // above D0, histograms digit 1 inside it and gathers its errors as
-// deduplicated (key, count) entries, on which digits 2-4 are resolved.
+// deduplicated (key, count) entries, on which digits 2-4 are resolved.  When
+// the signature only bounds the k-th largest error to a window of binades,
+// that pass gathers the whole window and every level comes from the entries.
 constexpr int kTopkLevels = 5;
 constexpr int kTopkBins = 8192;                  // bins of digits 1-4
 enum { kTopkActive = 0, kTopkDone = 1 };
 
-struct TopkState {               // one per pair (56 bytes), device memory
+struct TopkState {               // one per pair (72 bytes), device memory
     uint64_t n_valid;
     uint64_t k;
-    uint64_t need;               // k minus the errors above the boundary bin
-    uint64_t cand;               // errors in the boundary bin
+    uint64_t need;               // k minus the errors above the boundary bin (or window)
+    uint64_t cand;               // errors in the boundary bin (or window)
     uint64_t key;                // bits of the boundary fixed so far
-    int32_t level;               // last resolved level, -1 before level 0
+    uint64_t wlo, whi;           // window [wlo, whi) of error keys holding the k-th largest
+    int32_t level;               // last resolved level; -1 before level 0, -2 window gather pending
     int32_t status;              // kTopkActive or kTopkDone
     int32_t d0;                  // binade field of the boundary
-    int32_t reserved;
+    int32_t round;               // gathering pass that serves the pair (0, or 1 after a window overflowed)
 };
-static_assert(sizeof(TopkState) == 56, "TopkState layout");
+static_assert(sizeof(TopkState) == 72, "TopkState layout");
 
 struct TopkEntry {               // errors of one key in one chunk (16 bytes)
     uint64_t key;
     uint32_t count;
-    int32_t pair;                // -1: an unused position
+    int32_t pair;                // pair | round << 30; -1: an unused position
 };
 static_assert(sizeof(TopkEntry) == 16, "TopkEntry layout");
 
@@ -173,9 +176,10 @@ struct TopkParams {
     TopkState *state;
     uint64_t *hist;              // count x kTopkBins counters
     double *part_a;              // per chunk: binary64 sum of its errors above binade D0
-    uint64_t *xsum;              // per pair: exact sum (2 words) of the significands in binade D0 above the boundary
-    uint32_t *ovf;               // per pair: [0] gather of binade D0 did not fit, [1] gather of bin (D0, D1) did not fit;
-                                 // then 2 words: some pair has flag 0 set, some pair has flag 1 set
+    uint64_t *xsum;              // per pair and binade: exact sum (2 words) of the significands above the boundary
+    uint32_t *ovf;               // per pair: [0] gather of binade D0 (or window) did not fit, [1] gather of bin
+                                 // (D0, D1) did not fit; then 3 words: some pair has flag 0 set, some pair has
+                                 // flag 1 set, some window gather did not fit
     TopkEntry *ents;             // cap[0] entries of binade D0 gathers, then cap[1] of bin (D0, D1) gathers
     unsigned long long *fill;    // entries handed out in each of the two regions
     uint64_t cap[2];
@@ -185,7 +189,7 @@ struct TopkParams {
     int32_t count;               // pairs
     int32_t num, den;
     int32_t level;               // level of a selection, tensor-pass or entry launch
-    int32_t pad;
+    int32_t round;               // gathering-pass round of a launch
 };
 
 // Kernel launchers (defined in the .hip translation units).

@@ -69,6 +69,19 @@ __device__ __forceinline__ uint64_t signif(uint64_t key, int d0) {
     return (key & kMant) | (d0 != 0 ? (uint64_t(1) << 52) : 0);
 }
 
+// Entries carry their pair and the round of the gathering pass that wrote
+// them; a pair whose window gather did not fit is gathered again in round 1
+// and ignores what round 0 left.
+constexpr uint32_t kPairMask = (1u << 30) - 1;
+__device__ __forceinline__ int32_t entry_tag(int pair, int round) { return (int32_t)((uint32_t)pair | ((uint32_t)round << 30)); }
+
+// The pair's exact sum of significands of binade b (two words).
+__device__ __forceinline__ uint64_t *xsum_of(const TopkParams &P, int pair, int b) {
+    return P.xsum + 2 * ((size_t)pair * kBins0 + (size_t)b);
+}
+
+__device__ __forceinline__ bool is_window(const TopkState &st) { return st.whi != 0; }
+
 __device__ __forceinline__ int pair_mode(const TopkParams &P, int pair) {
     return P.ovf[2 * pair] == 0 ? kModeA : (P.ovf[2 * pair + 1] == 0 ? kModeC : kModeT);
 }
@@ -301,7 +314,8 @@ __device__ __forceinline__ bool table_count(Table &t, uint64_t key) {
 // pair (flag r) when a key found no slot or the region is full; positions
 // handed out past the region's end are left to later overflows, positions
 // inside it that this block cannot use are marked unused.
-__device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r, int pair) {
+__device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r, int pair, int round,
+                                            bool window) {
     __syncthreads();
     for (int i = threadIdx.x; i < kTable; i += kBlock)
         if (t.cnt[i]) atomicAdd(&t.n, 1u);
@@ -318,7 +332,7 @@ __device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r
         }
         if (!ok) {
             P.ovf[2 * pair + r] = 1;
-            P.ovf[2 * P.count + r] = 1;
+            P.ovf[2 * P.count + (window ? 2 : r)] = 1;
         }
         t.base = base;
         t.ok = ok;
@@ -331,7 +345,7 @@ __device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r
         for (int i = threadIdx.x; i < kTable; i += kBlock)
             if (t.cnt[i]) {
                 const uint32_t q = atomicAdd(&t.pos, 1u);
-                E[base + q] = TopkEntry{t.key[i], t.cnt[i], pair};
+                E[base + q] = TopkEntry{t.key[i], t.cnt[i], entry_tag(pair, round)};
             }
     } else {
         const unsigned long long end = base + t.n < P.cap[r] ? base + t.n : P.cap[r];
@@ -341,7 +355,7 @@ __device__ __forceinline__ void table_flush(Table &t, const TopkParams &P, int r
 
 // Appends (key, 1) entries of keys that found no slot to region 1, one
 // atomic per wave; a wave past the region's end marks the pair.
-__device__ __forceinline__ void spill_entry(bool take, uint64_t key, const TopkParams &P, int pair) {
+__device__ __forceinline__ void spill_entry(bool take, uint64_t key, const TopkParams &P, int pair, int round) {
     const uint64_t m = __ballot(take);
     if (m == 0) return;
     const int leader = __ffsll((long long)m) - 1;
@@ -352,7 +366,7 @@ __device__ __forceinline__ void spill_entry(bool take, uint64_t key, const TopkP
         const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
         const unsigned long long q = base + rank;
         if (q < P.cap[1]) {
-            P.ents[P.cap[0] + q] = TopkEntry{key, 1u, pair};
+            P.ents[P.cap[0] + q] = TopkEntry{key, 1u, entry_tag(pair, round)};
         } else {
             P.ovf[2 * pair + 1] = 1;
             P.ovf[2 * P.count + 1] = 1;
@@ -373,11 +387,15 @@ __device__ __forceinline__ void level0_status(TopkState &st, int b, int tdtype) 
 }
 
 // Level 0 from the pair's signature, which counts the same errors of the same
-// valid pairs: with one-binade bins regular bin i is binade field
-// lo + i + 1023, and errors below every bin are the zero errors alone when
-// the test side is not binary64 (a difference of two narrower values is a
-// multiple of 2^-149, far above the subnormal range).  Leaves the state open
-// when the record does not match the pair or does not fix the binade.
+// valid pairs.  Bin i of the record covers the error keys from that of
+// 2^(lo + i w) up to that of 2^(lo + (i + 1) w); with one-binade bins (w = 1)
+// a regular bin is binade field lo + i + 1023 and fixes level 0.  A wider bin,
+// the under bin (keys 1 up to that of 2^lo) or the over bin (from 2^hi up,
+// +Inf included) leaves a window of binades, which the gathering pass
+// collects whole.  Errors below every bin are the zero errors alone when the
+// test side is not binary64 (a difference of two narrower values is a
+// multiple of 2^-149, far above the subnormal range): the k-th largest error
+// is then 0.  Leaves the state open when the record does not match the pair.
 __device__ void level0_from_sig(const peat_signature_t &g, const SigDesc &d, const TopkParams &P,
                                 TopkState &st) {
     if (g.n != d.n || g.n_valid < 0) return;
@@ -394,23 +412,45 @@ __device__ void level0_from_sig(const peat_signature_t &g, const SigDesc &d, con
         st.d0 = 0;
         return;
     }
-    uint64_t acc = (uint64_t)g.hist_over;
-    if (k <= acc) return;
-    const bool one_binade = P.hi - P.lo == P.nbins;
+    auto key_of = [](int e) { return (uint64_t)(e + 1023) << 52; };      // key of 2^e
+    uint64_t acc = 0;
+    auto window = [&](uint64_t lo, uint64_t hi, uint64_t c) {
+        st.need = k - acc;
+        st.cand = c;
+        st.wlo = lo;
+        st.whi = hi;
+        st.level = -2;
+        st.status = kTopkActive;
+    };
+    const uint64_t over = (uint64_t)g.hist_over;
+    if (k <= over) {
+        window(key_of(P.hi), uint64_t(1) << 63, over);
+        return;
+    }
+    acc = over;
+    const int w = (P.hi - P.lo) / P.nbins;
     for (int i = P.nbins - 1; i >= 0; --i) {
         const uint64_t c = (uint64_t)g.hist[i];
         if (acc + c >= k) {
-            if (!one_binade) return;
-            st.need = k - acc;
-            st.cand = c;
-            st.key = (uint64_t)(P.lo + i + 1023) << 52;
-            level0_status(st, P.lo + i + 1023, d.tdtype);
+            if (w == 1) {
+                st.need = k - acc;
+                st.cand = c;
+                st.key = key_of(P.lo + i);
+                level0_status(st, P.lo + i + 1023, d.tdtype);
+            } else {
+                window(key_of(P.lo + i * w), key_of(P.lo + (i + 1) * w), c);
+            }
             return;
         }
         acc += c;
     }
-    acc += (uint64_t)g.hist_under;
-    if (k <= acc || d.tdtype == PEAT_F64) return;
+    const uint64_t under = (uint64_t)g.hist_under;
+    if (k <= acc + under) {
+        window(1, key_of(P.lo), under);
+        return;
+    }
+    acc += under;
+    if (d.tdtype == PEAT_F64) return;
     st.need = k - acc;
     st.cand = (uint64_t)g.hist_zero;
     st.key = 0;
@@ -424,22 +464,23 @@ __global__ void __launch_bounds__(kBlock) topk_init(TopkParams P) {
         P.fill[1] = 0;
         P.ovf[2 * P.count] = 0;
         P.ovf[2 * P.count + 1] = 0;
+        P.ovf[2 * P.count + 2] = 0;
     }
     if (pair >= P.count) return;
     P.ovf[2 * pair] = 0;
     P.ovf[2 * pair + 1] = 0;
-    P.xsum[2 * pair] = 0;
-    P.xsum[2 * pair + 1] = 0;
     TopkState st;
     st.n_valid = 0;
     st.k = 0;
     st.need = 0;
     st.cand = 0;
     st.key = 0;
+    st.wlo = 0;
+    st.whi = 0;
     st.level = -1;
     st.status = kTopkActive;
     st.d0 = 0;
-    st.reserved = 0;
+    st.round = 0;
     if (P.sigs) level0_from_sig(P.sigs[pair], P.descs[pair], P, st);
     P.state[pair] = st;
 }
@@ -451,7 +492,7 @@ enum { kPass1 = 0, kPassA = 1, kPassC = 2, kPassT = 3 };
 template <int DG, int DT>
 __device__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
     const int pair = P.chunk_pair[gchunk];
-    if (P.state[pair].level >= 0) return;
+    if (P.state[pair].level != -1) return;
     const SigDesc d = P.descs[pair];
     for (int b = threadIdx.x; b < kBins0; b += kBlock) h[b] = 0;
     __syncthreads();
@@ -459,37 +500,45 @@ __device__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
     flush_hist(h, kBins0, P.hist + (size_t)pair * kTopkBins);
 }
 
-// pass A (one chunk per block).  Each error of binade D0 is counted once:
-// in the gather table, or (once a key of this thread found no slot) in the
-// digit-1 histogram; at the end the table's counts go into that histogram
-// too (in LDS when the block overflowed, else straight to the pair's).
+// pass A (one chunk per block in round 0; round 1 serves the pairs whose
+// window did not fit, after their binade pass).  Sums the errors above the
+// gathered range and gathers the range: binade D0, or the pair's window.
+// For binade D0 each error is counted once: in the gather table, or (once a
+// key of this thread found no slot) in the digit-1 histogram; at the end the
+// table's counts go into that histogram too (in LDS when the block
+// overflowed, else straight to the pair's).  A window that does not fit is
+// given up (the pair is gathered again by binade).
 template <int DG, int DT>
 __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Table &tab, double *red) {
     const int pair = P.chunk_pair[gchunk];
     const TopkState st = P.state[pair];
+    if (st.round != P.round) return;                          // served by the other round
     // nothing above an infinite boundary; nothing at all when k = 0
-    if (st.k == 0 || st.d0 == kBins0 - 1) {
+    if (st.k == 0 || (st.level >= 0 && st.d0 == kBins0 - 1)) {
         if (threadIdx.x == 0) P.part_a[gchunk] = 0.0;
         return;
     }
     const SigDesc d = P.descs[pair];
-    const uint64_t d0 = (uint64_t)st.d0;
-    const bool active = st.status == kTopkActive;            // the boundary binade needs ordering
+    const bool win = st.level == -2;
+    const uint64_t glo = win ? st.wlo : (uint64_t)st.d0 << 52;           // the gathered keys [glo, ghi)
+    const uint64_t ghi = win ? st.whi : (uint64_t)(st.d0 + 1) << 52;
+    const bool active = st.status == kTopkActive;            // the range needs ordering
+    const bool hist1 = active && !win;
     if (active) {
-        for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
+        if (hist1)
+            for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
         table_init(tab);
         __syncthreads();
     }
     double s = 0.0;
-    bool spill = false;                                       // this thread's keys go to the histogram
+    bool spill = false;                                       // this thread's keys find no slot
     for_each_error_vec<DG, DT>(d, gchunk - d.first_chunk, [&](const auto &key, const auto &a, const auto &ok) {
         constexpr int V = sizeof(ok) / sizeof(ok[0]);
         bool in[V];
 #pragma unroll
         for (int j = 0; j < V; ++j) {
-            const uint64_t e = key[j] >> 52;
-            if (ok[j] && e > d0) s += a[j];
-            in[j] = ok[j] && e == d0 && active;
+            if (ok[j] && key[j] >= ghi) s += a[j];
+            in[j] = ok[j] && key[j] >= glo && key[j] < ghi && active;
         }
         if (!spill) {
             // first probes of the vector's keys issued together; a key found
@@ -516,25 +565,30 @@ __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Ta
                 }
             }
         }
+        if (hist1) {
 #pragma unroll
-        for (int j = 0; j < V; ++j)
-            if (in[j]) atomicAdd(&h[digit_of(key[j], 1)], 1u);
+            for (int j = 0; j < V; ++j)
+                if (in[j]) atomicAdd(&h[digit_of(key[j], 1)], 1u);
+        }
     });
     const double bs = block_sum(s, red);
     if (threadIdx.x == 0) P.part_a[gchunk] = bs;
     if (!active) return;
     __syncthreads();
-    uint64_t *H = P.hist + (size_t)pair * kTopkBins;
-    if (tab.full) {
-        for (int i = threadIdx.x; i < kTable; i += kBlock)
-            if (tab.cnt[i]) atomicAdd(&h[digit_of(tab.key[i], 1)], tab.cnt[i]);
-        flush_hist(h, kTopkBins, H);
-    } else {
-        for (int i = threadIdx.x; i < kTable; i += kBlock)
-            if (tab.cnt[i])
-                atomicAdd((unsigned long long *)&H[digit_of(tab.key[i], 1)], (unsigned long long)tab.cnt[i]);
+    if (hist1) {
+        uint64_t *H = P.hist + (size_t)pair * kTopkBins;
+        if (tab.full) {
+            for (int i = threadIdx.x; i < kTable; i += kBlock)
+                if (tab.cnt[i]) atomicAdd(&h[digit_of(tab.key[i], 1)], tab.cnt[i]);
+            flush_hist(h, kTopkBins, H);
+        } else {
+            for (int i = threadIdx.x; i < kTable; i += kBlock)
+                if (tab.cnt[i])
+                    atomicAdd((unsigned long long *)&H[digit_of(tab.key[i], 1)], (unsigned long long)tab.cnt[i]);
+        }
     }
-    table_flush(tab, P, 0, pair);
+    table_flush(tab, P, 0, pair, st.round, win);
+    __syncthreads();
 }
 
 // pass C (pairs whose binade did not fit): exact sum of their errors in D0
@@ -555,11 +609,11 @@ __device__ void passC_chunk(const TopkParams &P, int64_t gchunk, Table &tab) {
         if ((k1 >> 13) == (b1 >> 13) && k1 > b1) x += signif(key, d0);
         const bool in = k1 == b1;
         const bool counted = in && table_count(tab, key);
-        spill_entry(in && !counted, key, P, pair);
+        spill_entry(in && !counted, key, P, pair, st.round);
     });
-    block_add128(x, P.xsum + 2 * pair);
+    block_add128(x, xsum_of(P, pair, d0));
     tab.full = 0;                                            // keys without a slot went out as entries
-    table_flush(tab, P, 1, pair);
+    table_flush(tab, P, 1, pair, st.round, false);
     __syncthreads();
 }
 
@@ -591,7 +645,7 @@ __device__ void passT_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
         if (hist && (key >> sh) == ph) atomicAdd(&h[digit_of(key, L)], 1u);
         if (sum && (key >> sx) == px && digit_of(key, L - 1) > dl) x += signif(key, d0);
     });
-    if (sum) block_add128(x, P.xsum + 2 * pair);
+    if (sum) block_add128(x, xsum_of(P, pair, d0));
     if (hist) flush_hist(h, kTopkBins, P.hist + (size_t)pair * kTopkBins);
     __syncthreads();
 }
@@ -601,10 +655,24 @@ __global__ void __launch_bounds__(kBlock) topk_scan(TopkParams P) {
     __shared__ uint32_t h[kTopkBins];
     __shared__ double red[kWaves];
     if constexpr (OP == kPass1) {
-        pass1_chunk<DG, DT>(P, P.chunk_base + blockIdx.x, h);
+        if (P.round == 0) {
+            pass1_chunk<DG, DT>(P, P.chunk_base + blockIdx.x, h);
+        } else {
+            if (P.ovf[2 * P.count + 2] == 0) return;         // every window fitted
+            for (int64_t c = blockIdx.x; c < P.kind_chunks; c += gridDim.x) {
+                pass1_chunk<DG, DT>(P, P.chunk_base + c, h);
+                __syncthreads();
+            }
+        }
     } else if constexpr (OP == kPassA) {
         __shared__ Table tab;
-        passA_chunk<DG, DT>(P, P.chunk_base + blockIdx.x, h, tab, red);
+        if (P.round == 0) {
+            passA_chunk<DG, DT>(P, P.chunk_base + blockIdx.x, h, tab, red);
+        } else {
+            if (P.ovf[2 * P.count + 2] == 0) return;         // every window fitted
+            for (int64_t c = blockIdx.x; c < P.kind_chunks; c += gridDim.x)
+                passA_chunk<DG, DT>(P, P.chunk_base + c, h, tab, red);
+        }
     } else if constexpr (OP == kPassC) {
         __shared__ Table tab;
         if (P.ovf[2 * P.count] == 0) return;                 // every binade fitted
@@ -616,30 +684,46 @@ __global__ void __launch_bounds__(kBlock) topk_scan(TopkParams P) {
 }
 
 // ---- selection -----------------------------------------------------------------
+// Loads the pair's histogram (nb bins) into LDS and clears it for the next
+// level; every thread of the block takes part.
+__device__ __forceinline__ void take_hist(uint64_t *H, int nb, uint64_t *hs, uint64_t *ssum) {
+    const int seg = nb / kBlock;
+    for (int b = threadIdx.x; b < nb; b += kBlock) {
+        hs[b] = H[b];
+        H[b] = 0;
+    }
+    __syncthreads();
+    const int top = nb - (int)threadIdx.x * seg;              // thread t: bins [top - seg, top)
+    uint64_t x = 0;
+    for (int b = top - 1; b >= top - seg; --b) x += hs[b];
+    ssum[threadIdx.x] = x;
+    __syncthreads();
+}
+
+// The bin holding the need-th largest counted error (thread 0): walks the
+// segments, then the bins, from the top; acc receives the count above it.
+__device__ __forceinline__ int walk_hist(const uint64_t *hs, const uint64_t *ssum, int nb, uint64_t need,
+                                         uint64_t &acc) {
+    const int seg = nb / kBlock;
+    acc = 0;
+    int t = 0;
+    while (t < kBlock - 1 && acc + ssum[t] < need) acc += ssum[t++];
+    int b = nb - t * seg - 1;
+    while (b > nb - (t + 1) * seg && acc + hs[b] < need) acc += hs[b--];
+    return b;
+}
+
 // One block per pair: the bin of the level-L histogram holding the need-th
-// largest remaining error; the histogram is cleared for the next level.
+// largest remaining error.
 __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     const int pair = blockIdx.x;
     const int L = P.level;
     TopkState st = P.state[pair];
     if (L == 0 ? st.level != -1 : !(st.status == kTopkActive && st.level == L - 1)) return;
     const int nb = L == 0 ? kBins0 : kTopkBins;
-    const int seg = nb / kBlock;
-    uint64_t *H = P.hist + (size_t)pair * kTopkBins;
     __shared__ uint64_t hs[kTopkBins];
     __shared__ uint64_t ssum[kBlock];
-    for (int b = threadIdx.x; b < nb; b += kBlock) {
-        hs[b] = H[b];
-        H[b] = 0;
-    }
-    __syncthreads();
-    {
-        const int top = nb - (int)threadIdx.x * seg;          // thread t: bins [top - seg, top)
-        uint64_t x = 0;
-        for (int b = top - 1; b >= top - seg; --b) x += hs[b];
-        ssum[threadIdx.x] = x;
-    }
-    __syncthreads();
+    take_hist(P.hist + (size_t)pair * kTopkBins, nb, hs, ssum);
     if (threadIdx.x != 0) return;
     uint64_t need;
     if (L == 0) {
@@ -661,12 +745,8 @@ __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     } else {
         need = st.need;
     }
-    // walk the segments, then the bins, from the top
-    uint64_t acc = 0;
-    int t = 0;
-    while (t < kBlock - 1 && acc + ssum[t] < need) acc += ssum[t++];
-    int b = nb - t * seg - 1;
-    while (b > nb - (t + 1) * seg && acc + hs[b] < need) acc += hs[b--];
+    uint64_t acc;
+    const int b = walk_hist(hs, ssum, nb, need, acc);
     st.need = need - acc;                     // copies of the boundary bin taken, >= 1
     st.cand = hs[b];
     st.key |= (uint64_t)b << digit_shift(L);
@@ -679,9 +759,42 @@ __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
     P.state[pair] = st;
 }
 
+// One block per pair whose window was gathered: level 0 from the binade
+// histogram of its entries (need counts from the top of the window).  A
+// window that did not fit reopens level 0 for a binade pass and a second
+// gathering round.
+__global__ void __launch_bounds__(kBlock) topk_select_window(TopkParams P) {
+    const int pair = blockIdx.x;
+    TopkState st = P.state[pair];
+    if (st.level != -2) return;
+    if (P.ovf[2 * pair] != 0) {
+        if (threadIdx.x == 0) {
+            st.level = -1;
+            st.round = 1;
+            st.wlo = st.whi = 0;
+            st.need = st.cand = 0;
+            P.ovf[2 * pair] = 0;
+            P.state[pair] = st;
+        }
+        return;
+    }
+    __shared__ uint64_t hs[kBins0];
+    __shared__ uint64_t ssum[kBlock];
+    take_hist(P.hist + (size_t)pair * kTopkBins, kBins0, hs, ssum);
+    if (threadIdx.x != 0) return;
+    uint64_t acc;
+    const int b = walk_hist(hs, ssum, kBins0, st.need, acc);
+    st.need -= acc;
+    st.cand = hs[b];
+    st.key = (uint64_t)b << 52;
+    level0_status(st, b, P.descs[pair].tdtype);
+    P.state[pair] = st;
+}
+
 // ---- rounds on the entries -------------------------------------------------------
-// Region 0 holds the binade gathers of pass A, region 1 the bin gathers of
-// pass C; an entry counts for its pair when the pair takes that route.
+// Region 0 holds the binade and window gathers of pass A, region 1 the bin
+// gathers of pass C; an entry counts for its pair when the pair takes that
+// route and the entry comes from the pair's gathering round.
 template <typename F>
 __device__ __forceinline__ void for_each_entry(const TopkParams &P, F &&f) {
     for (int r = 0; r < 2; ++r) {
@@ -690,34 +803,44 @@ __device__ __forceinline__ void for_each_entry(const TopkParams &P, F &&f) {
         const TopkEntry *E = P.ents + (r ? P.cap[0] : 0);
         for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (uint64_t)gridDim.x * kBlock) {
             const TopkEntry e = E[i];
-            if (e.pair < 0 || e.pair >= P.count) continue;
-            if (pair_mode(P, e.pair) != (r ? kModeC : kModeA)) continue;
-            f(e);
+            if (e.pair < 0) continue;
+            const int pair = (int)((uint32_t)e.pair & kPairMask);
+            if (pair >= P.count) continue;
+            if (pair_mode(P, pair) != (r ? kModeC : kModeA)) continue;
+            const TopkState &st = P.state[pair];
+            if ((int)((uint32_t)e.pair >> 30) != st.round) continue;
+            f(e, pair, st);
         }
     }
 }
 
-// Level L (2-4): weighted histogram of digit L over the entries on the
-// pair's level L-1 prefix.
+// Level L: weighted histogram of digit L over the entries on the pair's
+// level L-1 prefix.  Level 0 serves the window pairs (every entry is in the
+// window), level 1 the window pairs only (the others got their digit-1
+// histogram from pass A), levels 2-4 every pair on entries.
 __global__ void __launch_bounds__(kBlock) topk_ent_hist(TopkParams P) {
     const int L = P.level;
-    for_each_entry(P, [&](const TopkEntry &e) {
-        const TopkState &st = P.state[e.pair];
-        if (!(st.status == kTopkActive && st.level == L - 1)) return;
-        const int sh = digit_shift(L - 1);
-        if ((e.key >> sh) != (st.key >> sh)) return;
-        atomicAdd((unsigned long long *)&P.hist[(size_t)e.pair * kTopkBins + digit_of(e.key, L)],
+    for_each_entry(P, [&](const TopkEntry &e, int pair, const TopkState &st) {
+        if (L == 0) {
+            if (st.level != -2) return;
+        } else {
+            if (!(st.status == kTopkActive && st.level == L - 1)) return;
+            if (L == 1 && !is_window(st)) return;
+            const int sh = digit_shift(L - 1);
+            if ((e.key >> sh) != (st.key >> sh)) return;
+        }
+        atomicAdd((unsigned long long *)&P.hist[(size_t)pair * kTopkBins + digit_of(e.key, L)],
                   (unsigned long long)e.count);
     });
 }
 
-// Exact sum of the entries above the fixed boundary.
+// Exact sums of the entries above the fixed boundary, per binade.
 __global__ void __launch_bounds__(kBlock) topk_ent_sum(TopkParams P) {
-    for_each_entry(P, [&](const TopkEntry &e) {
-        const TopkState &st = P.state[e.pair];
+    for_each_entry(P, [&](const TopkEntry &e, int pair, const TopkState &st) {
         if (st.level != kTopkLevels - 1 || e.key <= st.key) return;
-        const unsigned __int128 v = (unsigned __int128)e.count * signif(e.key, st.d0);
-        atomic_add128(P.xsum + 2 * e.pair, (uint64_t)v, (uint64_t)(v >> 64));
+        const int b = (int)(e.key >> 52);
+        const unsigned __int128 v = (unsigned __int128)e.count * signif(e.key, b);
+        atomic_add128(xsum_of(P, pair, b), (uint64_t)v, (uint64_t)(v >> 64));
     });
 }
 
@@ -732,12 +855,32 @@ __device__ __forceinline__ double chunk_sum(const double *part, int64_t first, i
     return r;
 }
 
+// The binary64 value of an exact significand sum of binade b (the boundary's
+// binade with need copies of T added).
+__device__ __forceinline__ double binade_value(const TopkParams &P, int pair, const TopkState &st, int b) {
+    const uint64_t *xp = xsum_of(P, pair, b);
+    unsigned __int128 x = ((unsigned __int128)xp[1] << 64) | xp[0];
+    if (b == st.d0) x += (unsigned __int128)st.need * signif(st.key, st.d0);
+    if (x == 0) return 0.0;
+    const double xd = (double)(uint64_t)(x >> 64) * 0x1p64 + (double)(uint64_t)x;
+    return __builtin_ldexp(xd, (b != 0 ? b : 1) - 1075);
+}
+
 __global__ void __launch_bounds__(kBlock) topk_finalize(TopkParams P) {
     __shared__ double red[kWaves];
+    __shared__ double xb[kBins0];
     const int pair = blockIdx.x;
     const SigDesc d = P.descs[pair];
     const TopkState st = P.state[pair];
     const double sa = chunk_sum(P.part_a, d.first_chunk, d.nchunks, red);
+    // a window's binades above D0: their exact sums converted in parallel,
+    // added in a fixed order (from the top) below
+    const bool ordinary = st.k != 0 && st.d0 != kBins0 - 1 && !(st.d0 == 0 && st.level == 0);
+    const int top = ordinary && is_window(st) ? (int)((st.whi - 1) >> 52) : st.d0;
+    if (ordinary && top > st.d0) {
+        for (int b = st.d0 + threadIdx.x; b <= top; b += kBlock) xb[b] = binade_value(P, pair, st, b);
+        __syncthreads();
+    }
     if (threadIdx.x != 0) return;
     const double qnan = opaque_double(0x7FF80000u, 0u);
     const double inf = opaque_double(0x7FF00000u, 0u);
@@ -754,17 +897,21 @@ __global__ void __launch_bounds__(kBlock) topk_finalize(TopkParams P) {
         o.kth_value = inf;
         o.sum_topk = inf;
         o.mean_topk = inf;
-    } else if (st.d0 == 0 && st.level == 0) {        // the k-th largest error is 0
+    } else if (!ordinary) {                           // the k-th largest error is 0
         o.count_above = (int64_t)(st.k - st.need);
         o.kth_value = 0.0;
         o.sum_topk = sa;
         o.mean_topk = sa / (double)st.k;
     } else {
-        // exact sum inside binade D0: everything above T, then need copies of T
-        unsigned __int128 x = ((unsigned __int128)P.xsum[2 * pair + 1] << 64) | P.xsum[2 * pair];
-        x += (unsigned __int128)st.need * signif(st.key, st.d0);
-        const double xd = (double)(uint64_t)(x >> 64) * 0x1p64 + (double)(uint64_t)x;
-        const double sc = __builtin_ldexp(xd, (st.d0 != 0 ? st.d0 : 1) - 1075);
+        // exact sums: binade D0 (everything above T, then need copies of T)
+        // and, for a window, each binade above it
+        double sc;
+        if (top > st.d0) {
+            sc = 0.0;
+            for (int b = top; b >= st.d0; --b) sc += xb[b];
+        } else {
+            sc = binade_value(P, pair, st, st.d0);
+        }
         o.count_above = (int64_t)(st.k - st.need);
         o.kth_value = __longlong_as_double((long long)st.key);
         o.sum_topk = sa + sc;
@@ -781,7 +928,8 @@ __global__ void __launch_bounds__(kBlock) topk_zero(uint64_t *p, int64_t n) {
 template <int DG, int DT, int OP>
 void launch_one(const TopkParams &q, hipStream_t s) {
     const int64_t n = q.kind_chunks;
-    const int64_t grid = (OP == kPass1 || OP == kPassA) ? n : (n < kScanGrid ? n : kScanGrid);
+    const bool full = (OP == kPass1 || OP == kPassA) && q.round == 0;   // one chunk per block
+    const int64_t grid = full ? n : (n < kScanGrid ? n : kScanGrid);
     hipLaunchKernelGGL((topk_scan<DG, DT, OP>), dim3((unsigned)grid), dim3(kBlock), 0, s, q);
 }
 
@@ -824,34 +972,56 @@ hipError_t launch_select(const TopkParams &p, int level, hipStream_t s) {
 hipError_t launch_topk_level0(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
     if (p.count <= 0) return hipSuccess;
     hipError_t e;
-    const int64_t nhist = (int64_t)kTopkBins * p.count;
-    const int64_t zb = (nhist + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL(topk_zero, dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(kBlock), 0, s, p.hist, nhist);
+    auto zero = [&](uint64_t *x, int64_t n) {
+        const int64_t zb = (n + kBlock - 1) / kBlock;
+        hipLaunchKernelGGL(topk_zero, dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(kBlock), 0, s, x, n);
+    };
+    zero(p.hist, (int64_t)kTopkBins * p.count);
+    zero(p.xsum, (int64_t)2 * kBins0 * p.count);
     hipLaunchKernelGGL(topk_init, dim3((unsigned)((p.count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = launch_scan<kPass1>(p, range, s)) != hipSuccess) return e;
-    return launch_select(p, 0, s);
+    TopkParams q = p;
+    q.round = 0;
+    if ((e = launch_scan<kPass1>(q, range, s)) != hipSuccess) return e;
+    return launch_select(q, 0, s);
 }
 
 hipError_t launch_topk_rest(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
     if (p.count <= 0) return hipSuccess;
     hipError_t e;
-    if ((e = launch_scan<kPassA>(p, range, s)) != hipSuccess) return e;
-    if ((e = launch_select(p, 1, s)) != hipSuccess) return e;
-    if ((e = launch_scan<kPassC>(p, range, s)) != hipSuccess) return e;
     TopkParams q = p;
-    for (int L = 2; L <= kTopkLevels - 1; ++L) {
+    auto ent_hist = [&](int L) {
         q.level = L;
         hipLaunchKernelGGL(topk_ent_hist, dim3(kEntGrid), dim3(kBlock), 0, s, q);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return hipGetLastError();
+    };
+    // round 0: binade D0 or the window; level 0 of the windows from their entries
+    q.round = 0;
+    if ((e = launch_scan<kPassA>(q, range, s)) != hipSuccess) return e;
+    if ((e = ent_hist(0)) != hipSuccess) return e;
+    hipLaunchKernelGGL(topk_select_window, dim3((unsigned)p.count), dim3(kBlock), 0, s, q);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // round 1: windows that did not fit take the binade pass and are gathered again
+    q.round = 1;
+    if ((e = launch_scan<kPass1>(q, range, s)) != hipSuccess) return e;
+    if ((e = launch_select(q, 0, s)) != hipSuccess) return e;
+    if ((e = launch_scan<kPassA>(q, range, s)) != hipSuccess) return e;
+    q.round = 0;
+    // level 1 (the windows from their entries), the bin gathers, levels 2-4
+    if ((e = ent_hist(1)) != hipSuccess) return e;
+    if ((e = launch_select(q, 1, s)) != hipSuccess) return e;
+    if ((e = launch_scan<kPassC>(q, range, s)) != hipSuccess) return e;
+    for (int L = 2; L <= kTopkLevels - 1; ++L) {
+        if ((e = ent_hist(L)) != hipSuccess) return e;
+        q.level = L;
         if ((e = launch_scan<kPassT>(q, range, s)) != hipSuccess) return e;
-        if ((e = launch_select(p, L, s)) != hipSuccess) return e;
+        if ((e = launch_select(q, L, s)) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(topk_ent_sum, dim3(kEntGrid), dim3(kBlock), 0, s, p);
+    hipLaunchKernelGGL(topk_ent_sum, dim3(kEntGrid), dim3(kBlock), 0, s, q);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     q.level = kTopkLevels;
     if ((e = launch_scan<kPassT>(q, range, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(topk_finalize, dim3((unsigned)p.count), dim3(kBlock), 0, s, p);
+    hipLaunchKernelGGL(topk_finalize, dim3((unsigned)p.count), dim3(kBlock), 0, s, q);
     return hipGetLastError();
 }
 

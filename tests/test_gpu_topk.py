@@ -46,6 +46,21 @@ def assert_topk(got: dict, ref: dict, ctx: str = ""):
             assert abs(a - b) <= 1e-12 * abs(b), f"{ctx}: {key} {a!r} vs {b!r}"
 
 
+def close_record(a: dict, b: dict) -> bool:
+    """The exact fields equal; sum and mean equal or within 1e-12 relative
+    (a window gather sums its binades in another order)."""
+    for key in ("n_valid", "k", "count_above", "kth_value"):
+        if not (a[key] == b[key] or (math.isnan(a[key]) and math.isnan(b[key]))):
+            return False
+    for key in ("sum_topk", "mean_topk"):
+        x, y = a[key], b[key]
+        if x == y or (math.isnan(x) and math.isnan(y)):
+            continue
+        if math.isinf(y) or abs(x - y) > 1e-12 * abs(y):
+            return False
+    return True
+
+
 def same_record(a: dict, b: dict) -> bool:
     """Bit-identical records (NaN fields compare equal to NaN)."""
     return all(a[k] == b[k] or (isinstance(a[k], float) and math.isnan(a[k]) and math.isnan(b[k]))
@@ -141,12 +156,13 @@ def test_llama7b_tensor_full_size():
     torch.cuda.empty_cache()
 
 
-def test_from_signature_equals_three_passes():
-    """peat_topk_mean_from_signature_batched: records bit-identical to the
-    three-pass call and within the oracle's bar, both where the signature's
-    one-binade histogram resolves level 0 (regular bins) and where it cannot
-    (k-th largest error in hist_over, hist_under or hist_zero, or bins two
-    binades wide), with Inf and NaN pairs, empty pairs and unaligned views."""
+def test_from_signature_equals_standalone():
+    """peat_topk_mean_from_signature_batched against the standalone call and
+    the oracle: bit-identical where the signature's one-binade histogram
+    fixes level 0 (regular bins, zero errors), the exact fields identical
+    and the sums within 1e-12 where it leaves a window of binades (k-th
+    largest error in hist_over or hist_under, or bins two binades wide),
+    with Inf and NaN pairs, empty pairs and unaligned views."""
     from tests.parity import float_to_bits
     rng = np.random.default_rng(2024)
     cases = []
@@ -175,12 +191,77 @@ def test_from_signature_equals_three_passes():
         sigs = P.signature_batched(pairs, bins=bins)
         for num, den in ((1, 10), (1, 1000), (1, 1), (3, 7)):
             log(f"  bins={bins} frac={num}/{den}")
-            ref3 = P.topk_mean_batched(pairs, num, den)
+            ref = P.topk_mean_batched(pairs, num, den)
             got = P.topk_mean_from_signature_batched(pairs, sigs, bins, num, den)
+            again = P.topk_mean_from_signature_batched(pairs, sigs, bins, num, den)
             for k, (name, gb, tb, c) in enumerate(cases):
-                assert same_record(got[k], ref3[k]), f"{name} bins={bins} {num}/{den}: {got[k]} != {ref3[k]}"
+                ctx = f"{name} bins={bins} {num}/{den}"
+                assert same_record(got[k], again[k]), ctx
+                if _fixes_binade(sigs[k], bins, num, den):
+                    assert same_record(got[k], ref[k]), f"{ctx}: {got[k]} != {ref[k]}"
+                else:
+                    assert close_record(got[k], ref[k]), f"{ctx}: {got[k]} vs {ref[k]}"
                 if bins == (-40, 24, 64) and (num, den) == (1, 10):
                     assert_topk(got[k], oracle.topk(gb, tb, dtype=c, num=num, den=den), name)
+
+
+def _fixes_binade(sig: dict, bins, num: int, den: int) -> bool:
+    """Whether a record's histogram fixes the binade of the k-th largest
+    error: a regular one-binade bin, or the zero errors (no binary64 test
+    side here); records that do not match are not given."""
+    lo, hi, nb = bins
+    nv = sig["n_valid"]
+    k = -(-nv * num // den)
+    if k == 0:
+        return True
+    acc = sig["hist_over"]
+    if k <= acc:
+        return False
+    for i in range(nb - 1, -1, -1):
+        acc += sig["hist"][i]
+        if k <= acc:
+            return hi - lo == nb
+    return k > acc + sig["hist_under"]
+
+
+def _window_cases():
+    """f32 pairs whose top-10 % boundary lies below 2^-40 (the default bins'
+    under bin): Adam second-moment-like values with relative noise (a few
+    distinct errors per binade: the window fits the gather) and errors
+    spread over about a hundred binades (the window does not fit; the pair
+    is gathered again by binade), plus huge errors (the over bin)."""
+    rng = np.random.default_rng(4242)
+    n = 300007
+    v = (rng.standard_normal(n) * 1e-3).astype(np.float32) ** 2
+    t = (v * (1 + 1e-7 * rng.standard_normal(n))).astype(np.float32)
+    z = np.zeros(n, np.float32)
+    spread = np.ldexp(rng.integers(1, 9, n).astype(np.float64), -40 - rng.integers(3, 103, n)).astype(np.float32)
+    g32 = rng.standard_normal(n).astype(np.float32)
+    return [("adam v", v.view(np.uint32), t.view(np.uint32)),
+            ("spread below 2^-40", z.view(np.uint32), spread.view(np.uint32)),
+            ("huge errors", g32.view(np.uint32), (g32 * np.float32(3e8)).view(np.uint32))]
+
+
+@pytest.mark.parametrize("caps", [(-1, -1), (0, -1), (0, 0), (16, 1 << 10)])
+def test_from_signature_windows(caps):
+    """Windows of binades gathered whole, given up and gathered again by
+    binade, or overflowing further: every route against the standalone call
+    (exact fields identical, sums within 1e-12) and the oracle."""
+    cases = _window_cases()
+    pairs = [(to_device(gb, 0), to_device(tb, 0)) for _, gb, tb in cases]
+    try:
+        P.topk_set_entry_capacity(*caps)
+        for bins in ((-40, 24, 64), (-40, 24, 32)):
+            sigs = P.signature_batched(pairs, bins=bins)
+            for num, den in ((1, 10), (1, 3)):
+                log(f"  caps={caps} bins={bins} frac={num}/{den}")
+                ref = P.topk_mean_batched(pairs, num, den)
+                got = P.topk_mean_from_signature_batched(pairs, sigs, bins, num, den)
+                for k, (name, gb, tb) in enumerate(cases):
+                    assert close_record(got[k], ref[k]), f"{name}: {got[k]} vs {ref[k]}"
+                    assert_topk(got[k], oracle.topk(gb, tb, dtype=0, num=num, den=den), name)
+    finally:
+        P.topk_set_entry_capacity(-1, -1)
 
 
 def test_from_signature_with_fused_step_records():
@@ -198,7 +279,7 @@ def test_from_signature_with_fused_step_records():
         ref3 = P.topk_mean_batched(pairs, num, den)
         got = P.topk_mean_from_signature_batched(pairs, sigs, num=num, den=den)
         for k in range(len(pairs)):
-            assert same_record(got[k], ref3[k]), f"pair {k} {num}/{den}: {got[k]} != {ref3[k]}"
+            assert close_record(got[k], ref3[k]), f"pair {k} {num}/{den}: {got[k]} != {ref3[k]}"
 
 
 def _route_cases():
@@ -297,7 +378,7 @@ def test_async_entry_points_match_sync():
     sigs = P.decode_records(d_sig, len(pairs))
     got3 = P.topk_mean_from_signature_batched(pairs, sigs, bins, 1, 10)
     for k in range(len(pairs)):
-        assert same_record(got[k], ref[k]) and same_record(got2[k], ref[k]) and same_record(got3[k], ref[k]), f"pair {k}"
+        assert same_record(got[k], got3[k]) and same_record(got2[k], ref[k]) and close_record(got[k], ref[k]), f"pair {k}"
     # a record of another pair (n differs): ignored on the device
     if len(pairs) >= 2:
         host = d_sig.view(-1).cpu().numpy().copy()
@@ -308,7 +389,7 @@ def test_async_entry_points_match_sync():
         torch.cuda.synchronize()
         got4 = P.decode_topk(d_out, len(pairs))
         for k in range(len(pairs)):
-            assert same_record(got4[k], ref[k]), f"swapped records, pair {k}"
+            assert close_record(got4[k], ref[k]), f"swapped records, pair {k}"
     # mixed-precision forms
     mpairs = _mixed_device(cases)
     d_msig = torch.zeros(len(mpairs) * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
@@ -320,4 +401,4 @@ def test_async_entry_points_match_sync():
     torch.cuda.synchronize()
     mref = P.topk_mean_mixed_batched(mpairs, 1, 10)
     for k, (a, b) in enumerate(zip(P.decode_topk(d_mout, len(mpairs)), P.decode_topk(d_mout2, len(mpairs)))):
-        assert same_record(a, mref[k]) and same_record(b, mref[k]), f"mixed pair {k}"
+        assert close_record(a, mref[k]) and same_record(b, mref[k]), f"mixed pair {k}"
