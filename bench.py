@@ -284,7 +284,8 @@ def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
     gathering pass and the rounds), and the stream-ordered
     peat_topk_mean_from_signature_batched_async fed with the device records
     of the step's signature call on the same stream (the binade pass skips
-    the pairs whose histograms fix the k-th largest error's binade).  Best of
+    every pair whose record bounds the k-th largest error to one bin; the
+    gathering pass collects that bin's range).  Best of
     reps from the library's kernel events: level 0 (class K_TOPK_A) and the
     rest (K_TOPK_B); nothing in either waits on the host."""
     def timed(call):
