@@ -154,4 +154,15 @@ __device__ __forceinline__ uint32_t narrow_bits(double x) {
     }
 }
 
+// Bits of a binary32 value (bit pattern fb, not NaN) rounded to the 16-bit
+// format DN: nearest, ties to even, Inf beyond DN's range.
+template <int DN>
+__device__ __forceinline__ uint32_t narrow_f32_bits(uint32_t fb) {
+    if constexpr (DN == PEAT_F16) {
+        return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)__uint_as_float(fb));
+    } else {
+        return (fb + 0x7FFFu + ((fb >> 16) & 1u)) >> 16;
+    }
+}
+
 }  // namespace peat

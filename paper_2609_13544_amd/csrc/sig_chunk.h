@@ -396,9 +396,16 @@ __device__ __forceinline__ uint32_t fast_ulp(BG gb, BT tb, double G, double T) {
         b = tb;
     } else if constexpr (PT::GOLDEN_NARROW) {
         a = (uint32_t)gb;
-        b = narrow_bits<DG, DT>(T);
+        // a binary32 wider side is rounded from its own bits
+        if constexpr (DT == PEAT_F32)
+            b = narrow_f32_bits<DG>((uint32_t)tb);
+        else
+            b = narrow_bits<DG, DT>(T);
     } else {
-        a = narrow_bits<DT, DG>(G);
+        if constexpr (DG == PEAT_F32)
+            a = narrow_f32_bits<DT>((uint32_t)gb);
+        else
+            a = narrow_bits<DT, DG>(G);
         b = (uint32_t)tb;
     }
     if constexpr (PT::WN == 32) {
