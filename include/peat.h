@@ -315,13 +315,17 @@ int peat_signature_mixed_batched_async(const peat_mixed_pair_t *pairs, int32_t c
  * kth_value are exact.  sum_topk is the binary64 sum, in a fixed order, of
  * the errors above the binade of kth_value plus the exact sum of the others
  * (within 1e-12 relative of the exact sum), bit-identical between calls and
- * between the entry points below (the signature-fed ones as they state).  Two streaming passes over golden and
- * test (a binade histogram, then one pass that sums, histograms and gathers
- * the k-th largest error's binade); a pair whose binade holds too many
- * distinct errors for the gather takes one more pass (a gather of its top 13
- * mantissa bits), and one whose bin still does not fit one pass per
- * remaining digit.  No step waits on the host; the call waits for its
- * result.  sum_topk and mean_topk are equal across the routes. */
+ * between the entry points below (the signature-fed ones as they state).
+ * One streaming pass over golden and test in the common case: a small
+ * strided sample of each pair (about 8 K elements) guesses the binade of the
+ * k-th largest error, and one pass sums the errors above it, gathers its
+ * errors and counts the pair's errors, which confirm the guess; a wrong
+ * guess, a pair below 2^16 elements, or one whose sampled binade holds many
+ * distinct errors takes a binade-histogram pass first (two passes).  A pair
+ * whose binade holds too many distinct errors for the gather takes one more
+ * pass (a gather of its top 13 mantissa bits), and one whose bin still does
+ * not fit one pass per remaining digit.  Every route gives the same record.
+ * No step waits on the host; the call waits for its result. */
 int peat_topk_mean(const void *golden, const void *test, int64_t n, peat_dtype_t dtype,
                    int32_t num, int32_t den, peat_topk_t *out);
 

@@ -697,14 +697,15 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     const size_t b_part = align_up(sizeof(double) * (size_t)total);
     const size_t b_xsum = align_up(2 * sizeof(uint64_t) * kBins0Topk * (size_t)count);
     const size_t b_ovf = align_up(sizeof(uint32_t) * (2 * (size_t)count + 3));
+    const size_t b_cnt = align_up(2 * sizeof(uint64_t) * count);
     const size_t b_fill = align_up(2 * sizeof(unsigned long long));
     const size_t b_ents = align_up(sizeof(TopkEntry) * (size_t)(cap[0] + cap[1]));
     // device workspace: descriptors | chunk map | signatures | records (the
     // first three staged and copied as they lie) | state | histograms | chunk
-    // sums | exact sums | flags | fills | entries
+    // sums | exact sums | flags | counts | fills | entries
     const size_t o_map = b_desc, o_sig = o_map + b_map, o_out = o_sig + b_sig, o_state = o_out + b_out;
     const size_t o_hist = o_state + b_state, o_part = o_hist + b_hist, o_xsum = o_part + b_part;
-    const size_t o_ovf = o_xsum + b_xsum, o_fill = o_ovf + b_ovf, o_ents = o_fill + b_fill;
+    const size_t o_ovf = o_xsum + b_xsum, o_cnt = o_ovf + b_ovf, o_fill = o_cnt + b_cnt, o_ents = o_fill + b_fill;
 
     char *ws;
     if ((rc = acquire_ws(d, o_ents + b_ents, s, &ws))) return rc;
@@ -726,6 +727,7 @@ int topk_core(const peat_mixed_pair_t *pairs, int32_t count, int32_t num, int32_
     P.part_a = reinterpret_cast<double *>(ws + o_part);
     P.xsum = reinterpret_cast<uint64_t *>(ws + o_xsum);
     P.ovf = reinterpret_cast<uint32_t *>(ws + o_ovf);
+    P.counts = reinterpret_cast<uint64_t *>(ws + o_cnt);
     P.fill = reinterpret_cast<unsigned long long *>(ws + o_fill);
     P.ents = reinterpret_cast<TopkEntry *>(ws + o_ents);
     P.cap[0] = cap[0];

@@ -142,12 +142,13 @@ struct InjParams {
 // above D0, histograms digit 1 inside it and gathers its errors as
 // deduplicated (key, count) entries, on which digits 2-4 are resolved.  When
 // the signature only bounds the k-th largest error to a window of binades,
-// that pass gathers the whole window and every level comes from the entries.
+// or a sample of the pair suggests one, that pass gathers the whole window
+// and every level comes from the entries.
 constexpr int kTopkLevels = 5;
 constexpr int kTopkBins = 8192;                  // bins of digits 1-4
 enum { kTopkActive = 0, kTopkDone = 1 };
 
-struct TopkState {               // one per pair (72 bytes), device memory
+struct TopkState {               // one per pair (80 bytes), device memory
     uint64_t n_valid;
     uint64_t k;
     uint64_t need;               // k minus the errors above the boundary bin (or window)
@@ -158,8 +159,10 @@ struct TopkState {               // one per pair (72 bytes), device memory
     int32_t status;              // kTopkActive or kTopkDone
     int32_t d0;                  // binade field of the boundary
     int32_t round;               // gathering pass that serves the pair (0, or 1 after a window overflowed)
+    int32_t sampled;             // the binade is a guess from a sample: pass A counts the errors to confirm it
+    int32_t reserved;
 };
-static_assert(sizeof(TopkState) == 72, "TopkState layout");
+static_assert(sizeof(TopkState) == 80, "TopkState layout");
 
 struct TopkEntry {               // errors of one key in one chunk (16 bytes)
     uint64_t key;
@@ -177,6 +180,7 @@ struct TopkParams {
     uint64_t *hist;              // count x kTopkBins counters
     double *part_a;              // per chunk: binary64 sum of its errors above binade D0
     uint64_t *xsum;              // per pair and binade: exact sum (2 words) of the significands above the boundary
+    uint64_t *counts;            // per pair: valid errors, errors above a guessed binade
     uint32_t *ovf;               // per pair: [0] gather of binade D0 (or window) did not fit, [1] gather of bin
                                  // (D0, D1) did not fit; then 3 words: some pair has flag 0 set, some pair has
                                  // flag 1 set, some window gather did not fit

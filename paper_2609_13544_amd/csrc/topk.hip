@@ -5,22 +5,31 @@
 // boundary and buffer fill stays on the device, so no step waits on the host.
 //
 //   init     per pair: the state of level 0 from its signature when one is
-//            given and its histogram fixes the binade D0 of the k-th largest
+//            given: its histogram fixes the binade D0 of the k-th largest
 //            error (one-binade bins, boundary in a regular bin or among the
-//            zero errors); otherwise level 0 is open;
+//            zero errors) or bounds it to a window of binades (the under or
+//            over bin, wider bins); otherwise level 0 is open;
+//   sample   per open pair of 2^16 elements or more: a strided sample of
+//            8 K elements guesses D0 (a one-binade window whose guess pass A
+//            confirms by counting);
 //   pass 1   histogram of digit 0 (bits 62..52, the binade) over the pairs
-//            whose level 0 is open; select D0;
-//   pass A   binary64 sum of the errors above binade D0 (a fixed per-lane /
-//            butterfly / wave order in each chunk); histogram of digit 1
-//            (bits 51..39) inside D0; the errors of binade D0 gathered as
-//            (key, count) entries: each block counts its distinct keys in an
-//            LDS hash table (errors of checkpoint-like data are small
-//            multiples of the golden's ULP, so a binade holds few distinct
-//            values) and appends one entry per key; select D1;
-//   rounds   digits 2-4 on the entries: weighted histogram, select; then the
-//            exact integer sum count * significand of the entries above the
-//            boundary (they share the exponent D0);
-//   finalize sum = pass A + exact sum + need * T.
+//            whose level 0 is still open; select D0;
+//   pass A   binary64 sum of the errors above the gathered range (a fixed
+//            per-lane / butterfly / wave order in each chunk) and a gather of
+//            the range -- binade D0 or the window -- as (key, count) entries:
+//            each block counts its distinct keys in an LDS hash table (errors
+//            of checkpoint-like data are small multiples of the golden's ULP,
+//            so a binade holds few distinct values) and appends one entry per
+//            key; for binade D0 also the digit-1 (bits 51..39) histogram;
+//   windows  level 0 of a window from its entries' binades (a signature's
+//            window) or from the counts (a guess); a window that does not
+//            fit, or a wrong guess, reopens level 0: pass 1 and pass A again
+//            for those pairs (round 1);
+//   rounds   digits 1-4 on the entries as needed: weighted histogram, select;
+//            then the exact integer sums count * significand of the entries
+//            above the boundary, per binade;
+//   finalize sum = pass A + the exact sums (binade D0 with need copies of T,
+//            and a signature's window binades above it, from the top).
 //
 // A pair whose binade does not fit (a block's table overflows, or the entry
 // buffer is full) instead takes pass C over its tensors: the exact sum of
@@ -29,7 +38,9 @@
 // on those entries.  A pair whose bin does not fit either takes one
 // histogram pass over its tensors per digit (passes T2-T4) and a last pass
 // for the exact sum of digit 4 (T5).  Every route sums the errors inside D0
-// exactly, so they give bit-identical records.
+// exactly and the others in the lanes' order, so they give bit-identical
+// records; only a signature's window of several binades sums the binades
+// between D0 and its top exactly instead.
 //
 // The k-th largest error T is the key with all five digits fixed; count_above
 // is k minus the copies of T taken.
@@ -469,6 +480,8 @@ __global__ void __launch_bounds__(kBlock) topk_init(TopkParams P) {
     if (pair >= P.count) return;
     P.ovf[2 * pair] = 0;
     P.ovf[2 * pair + 1] = 0;
+    P.counts[2 * pair] = 0;
+    P.counts[2 * pair + 1] = 0;
     TopkState st;
     st.n_valid = 0;
     st.k = 0;
@@ -481,7 +494,106 @@ __global__ void __launch_bounds__(kBlock) topk_init(TopkParams P) {
     st.status = kTopkActive;
     st.d0 = 0;
     st.round = 0;
+    st.sampled = 0;
+    st.reserved = 0;
     if (P.sigs) level0_from_sig(P.sigs[pair], P.descs[pair], P, st);
+    P.state[pair] = st;
+}
+
+// ---- a window from a sample ----------------------------------------------------
+constexpr int kSampleRuns = 256;                // one run of consecutive elements per thread
+constexpr int kSampleRun = 32;
+constexpr int64_t kSampleMinN = int64_t(1) << 16;
+constexpr int kSampleSet = 8192;                // LDS hash set of the sample's window keys
+constexpr int kSampleMaxDistinct = 256;         // more distinct sampled keys in the binade: no guess
+
+// One block per open pair of this kind (n >= 2^16): errors of 256 runs of 32
+// consecutive elements spread over the pair, and the binade of the sample's
+// k-th largest error as a guess of binade D0 -- unless it holds zero or
+// infinite errors, or its sampled errors take more than 256 distinct values
+// (the gathering pass would not fit them).  Pass A then gathers that binade
+// and counts the pair's valid errors and those above it, which confirm the
+// guess exactly; a wrong guess costs the binade pass and a second gathering
+// pass over the pair.  A right guess gives the records of the binade-pass
+// route.
+template <int DG, int DT>
+__global__ void __launch_bounds__(kBlock) topk_sample(TopkParams P) {
+    const int pair = blockIdx.x;
+    const SigDesc d = P.descs[pair];
+    if (d.dtype != DG || d.tdtype != DT || d.n < kSampleMinN) return;
+    TopkState st = P.state[pair];
+    if (st.level != -1) return;
+    __shared__ uint32_t h[kBins0];
+    __shared__ uint64_t set[kSampleSet];
+    __shared__ uint32_t nvalid, distinct;
+    __shared__ int bs;
+    for (int b = threadIdx.x; b < kBins0; b += kBlock) h[b] = 0;
+    for (int i = threadIdx.x; i < kSampleSet; i += kBlock) set[i] = kEmpty;
+    if (threadIdx.x == 0) {
+        nvalid = 0;
+        distinct = 0;
+    }
+    __syncthreads();
+    constexpr int ESZG = Tr<DG>::W / 8, ESZT = Tr<DT>::W / 8;
+    const char *g = static_cast<const char *>(d.g);
+    const char *t = static_cast<const char *>(d.t);
+    int64_t start = (int64_t)threadIdx.x * d.n / kSampleRuns;
+    if (start > d.n - kSampleRun) start = d.n - kSampleRun;
+    uint64_t keys[kSampleRun];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int i = 0; i < kSampleRun; ++i) {
+        double a;
+        const bool ok = error_of<DG, DT>(load_elem<DG>(g + start * ESZG, (uint32_t)i),
+                                         load_elem<DT>(t + start * ESZT, (uint32_t)i), keys[i], a);
+        if (!ok) keys[i] = kEmpty;
+        else {
+            ++mine;
+            atomicAdd(&h[keys[i] >> 52], 1u);
+        }
+    }
+    atomicAdd(&nvalid, mine);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint64_t ks = ((uint64_t)nvalid * (uint32_t)P.num + (uint32_t)P.den - 1) / (uint32_t)P.den;
+        int b = -1;
+        uint64_t acc = 0;
+        if (ks > 0)
+            for (b = kBins0 - 1; b > 0 && acc + h[b] < ks; --b) acc += h[b];
+        bs = b;
+    }
+    __syncthreads();
+    const int b = bs;
+    if (b < 1 || b > kBins0 - 2) return;                      // no sample boundary, or zero or infinite errors
+    const uint64_t wlo = (uint64_t)b << 52, whi = (uint64_t)(b + 1) << 52;
+    // distinct sampled keys inside the binade
+#pragma unroll
+    for (int i = 0; i < kSampleRun; ++i) {
+        const uint64_t key = keys[i];
+        if (key == kEmpty || key < wlo || key >= whi) continue;
+        uint32_t slot = (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> 51);   // 13 bits
+#pragma unroll 1
+        for (int p = 0; p < kSampleSet; ++p, slot = (slot + 1) & (kSampleSet - 1)) {
+            const uint64_t old = atomicCAS((unsigned long long *)&set[slot], (unsigned long long)kEmpty,
+                                           (unsigned long long)key);
+            if (old == kEmpty) {
+                atomicAdd(&distinct, 1u);
+                break;
+            }
+            if (old == key) break;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x != 0 || distinct > kSampleMaxDistinct) return;
+    st.wlo = wlo;
+    st.whi = whi;
+    st.level = -2;
+    st.status = kTopkActive;
+    st.sampled = 1;
+    st.k = ~uint64_t(0);                                       // counted by pass A
+    st.n_valid = 0;
+    st.need = 0;
+    st.cand = 0;
     P.state[pair] = st;
 }
 
@@ -490,7 +602,7 @@ enum { kPass1 = 0, kPassA = 1, kPassC = 2, kPassT = 3 };
 
 // pass 1: binade histogram of the pairs whose level 0 is open (one chunk per block)
 template <int DG, int DT>
-__device__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
+__device__ __forceinline__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
     const int pair = P.chunk_pair[gchunk];
     if (P.state[pair].level != -1) return;
     const SigDesc d = P.descs[pair];
@@ -509,7 +621,7 @@ __device__ void pass1_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
 // overflowed, else straight to the pair's).  A window that does not fit is
 // given up (the pair is gathered again by binade).
 template <int DG, int DT>
-__device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Table &tab, double *red) {
+__device__ __forceinline__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Table &tab, double *red) {
     const int pair = P.chunk_pair[gchunk];
     const TopkState st = P.state[pair];
     if (st.round != P.round) return;                          // served by the other round
@@ -524,6 +636,8 @@ __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Ta
     const uint64_t ghi = win ? st.whi : (uint64_t)(st.d0 + 1) << 52;
     const bool active = st.status == kTopkActive;            // the range needs ordering
     const bool hist1 = active && !win;
+    const bool samp = st.sampled != 0;                        // a guessed binade: count the valid errors and those above
+    uint32_t nv = 0, na = 0;                                  // this lane's counts
     if (active) {
         if (hist1)
             for (int b = threadIdx.x; b < kTopkBins; b += kBlock) h[b] = 0;
@@ -570,7 +684,26 @@ __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Ta
             for (int j = 0; j < V; ++j)
                 if (in[j]) atomicAdd(&h[digit_of(key[j], 1)], 1u);
         }
+        if (samp) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                nv += ok[j] ? 1u : 0u;
+                na += (ok[j] && key[j] >= ghi) ? 1u : 0u;
+            }
+        }
     });
+    if (samp) {
+        // lane counts (at most 2^10 each) summed over the wave
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            nv += __shfl_xor(nv, o);
+            na += __shfl_xor(na, o);
+        }
+        if ((threadIdx.x & 63) == 0) {
+            atomicAdd((unsigned long long *)&P.counts[2 * pair], (unsigned long long)nv);
+            atomicAdd((unsigned long long *)&P.counts[2 * pair + 1], (unsigned long long)na);
+        }
+    }
     const double bs = block_sum(s, red);
     if (threadIdx.x == 0) P.part_a[gchunk] = bs;
     if (!active) return;
@@ -594,7 +727,7 @@ __device__ void passA_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h, Ta
 // pass C (pairs whose binade did not fit): exact sum of their errors in D0
 // above bin D1 and gather of bin (D0, D1)
 template <int DG, int DT>
-__device__ void passC_chunk(const TopkParams &P, int64_t gchunk, Table &tab) {
+__device__ __forceinline__ void passC_chunk(const TopkParams &P, int64_t gchunk, Table &tab) {
     const int pair = P.chunk_pair[gchunk];
     const TopkState st = P.state[pair];
     if (!(st.status == kTopkActive && st.level == 1 && P.ovf[2 * pair] != 0)) return;
@@ -621,7 +754,7 @@ __device__ void passC_chunk(const TopkParams &P, int64_t gchunk, Table &tab) {
 // L (L <= 4) among the errors on the level L-1 prefix, and (L >= 3) the
 // exact sum of the errors on the level L-2 prefix above digit D_{L-1}
 template <int DG, int DT>
-__device__ void passT_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
+__device__ __forceinline__ void passT_chunk(const TopkParams &P, int64_t gchunk, uint32_t *h) {
     const int L = P.level;
     const int pair = P.chunk_pair[gchunk];
     const TopkState st = P.state[pair];
@@ -773,6 +906,7 @@ __global__ void __launch_bounds__(kBlock) topk_select_window(TopkParams P) {
             st.round = 1;
             st.wlo = st.whi = 0;
             st.need = st.cand = 0;
+            st.sampled = 0;
             P.ovf[2 * pair] = 0;
             P.state[pair] = st;
         }
@@ -782,6 +916,33 @@ __global__ void __launch_bounds__(kBlock) topk_select_window(TopkParams P) {
     __shared__ uint64_t ssum[kBlock];
     take_hist(P.hist + (size_t)pair * kTopkBins, kBins0, hs, ssum);
     if (threadIdx.x != 0) return;
+    if (st.sampled) {
+        // the pair's counts decide whether the guessed binade holds the
+        // boundary; otherwise level 0 reopens for a binade pass (round 1)
+        const uint64_t nv = P.counts[2 * pair], above = P.counts[2 * pair + 1];
+        uint64_t w = 0;
+        for (int t = 0; t < kBlock; ++t) w += ssum[t];
+        st.n_valid = nv;
+        st.k = (uint64_t)(((unsigned __int128)nv * (uint32_t)P.num + (uint32_t)P.den - 1) / (uint32_t)P.den);
+        if (st.k == 0) {
+            st.level = 0;
+            st.status = kTopkDone;
+            st.d0 = 0;
+            P.state[pair] = st;
+            return;
+        }
+        if (st.k <= above || st.k > above + w) {
+            st.level = -1;
+            st.round = 1;
+            st.wlo = st.whi = 0;
+            st.need = st.cand = 0;
+            st.sampled = 0;
+            P.ovf[2 * P.count + 2] = 1;
+            P.state[pair] = st;
+            return;
+        }
+        st.need = st.k - above;
+    }
     uint64_t acc;
     const int b = walk_hist(hs, ssum, kBins0, st.need, acc);
     st.need -= acc;
@@ -960,6 +1121,30 @@ hipError_t launch_scan(const TopkParams &p, const int64_t range[kKinds + 1], hip
     return hipSuccess;
 }
 
+// The sample kernel of every kind present (one block per pair; blocks of
+// other kinds' pairs return at once).
+hipError_t launch_sample(const TopkParams &p, const int64_t range[kKinds + 1], hipStream_t s) {
+    for (int kind = 0; kind < kKinds; ++kind) {
+        if (range[kind + 1] - range[kind] <= 0) continue;
+        const dim3 grid((unsigned)p.count), block(kBlock);
+        switch (kind) {
+            case 0: hipLaunchKernelGGL((topk_sample<PEAT_F32, PEAT_F32>), grid, block, 0, s, p); break;
+            case 1: hipLaunchKernelGGL((topk_sample<PEAT_F16, PEAT_F16>), grid, block, 0, s, p); break;
+            case 2: hipLaunchKernelGGL((topk_sample<PEAT_BF16, PEAT_BF16>), grid, block, 0, s, p); break;
+            case 3: hipLaunchKernelGGL((topk_sample<PEAT_F32, PEAT_F64>), grid, block, 0, s, p); break;
+            case 4: hipLaunchKernelGGL((topk_sample<PEAT_F32, PEAT_F16>), grid, block, 0, s, p); break;
+            case 5: hipLaunchKernelGGL((topk_sample<PEAT_F32, PEAT_BF16>), grid, block, 0, s, p); break;
+            case 6: hipLaunchKernelGGL((topk_sample<PEAT_F16, PEAT_F32>), grid, block, 0, s, p); break;
+            case 7: hipLaunchKernelGGL((topk_sample<PEAT_BF16, PEAT_F32>), grid, block, 0, s, p); break;
+            case 8: hipLaunchKernelGGL((topk_sample<PEAT_F16, PEAT_F64>), grid, block, 0, s, p); break;
+            default: hipLaunchKernelGGL((topk_sample<PEAT_BF16, PEAT_F64>), grid, block, 0, s, p); break;
+        }
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_select(const TopkParams &p, int level, hipStream_t s) {
     TopkParams q = p;
     q.level = level;
@@ -980,6 +1165,7 @@ hipError_t launch_topk_level0(const TopkParams &p, const int64_t range[kKinds + 
     zero(p.xsum, (int64_t)2 * kBins0 * p.count);
     hipLaunchKernelGGL(topk_init, dim3((unsigned)((p.count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_sample(p, range, s)) != hipSuccess) return e;
     TopkParams q = p;
     q.round = 0;
     if ((e = launch_scan<kPass1>(q, range, s)) != hipSuccess) return e;

@@ -402,3 +402,43 @@ def test_async_entry_points_match_sync():
     mref = P.topk_mean_mixed_batched(mpairs, 1, 10)
     for k, (a, b) in enumerate(zip(P.decode_topk(d_mout, len(mpairs)), P.decode_topk(d_mout2, len(mpairs)))):
         assert close_record(a, mref[k]) and same_record(b, mref[k]), f"mixed pair {k}"
+
+
+def test_standalone_guess_misses_and_hits():
+    """The standalone call guesses the boundary's binade from a strided
+    sample of the pair.  Large errors placed only between the sampled runs
+    (256 runs of 32 elements) make the guess wrong, which costs the binade
+    pass and a second gathering pass; the records stay exact, equal for
+    single and batched calls and for every entry capacity."""
+    n = 1 << 20
+    rng = np.random.default_rng(5150)
+    g = rng.standard_normal(n).astype(np.float32)
+    t = (g * (1 + 1e-6 * rng.standard_normal(n))).astype(np.float32)
+    sampled = np.zeros(n, bool)
+    for r in range(256):
+        st = min(r * n // 256, n - 32)
+        sampled[st:st + 32] = True
+    hidden = np.flatnonzero(~sampled)
+    big = rng.choice(hidden, size=n // 7, replace=False)
+    t_miss = t.copy()
+    t_miss[big] = g[big] + np.float32(2.0 ** -5) * (1 + rng.random(big.size).astype(np.float32))
+    cases = [("guess right", g, t), ("guess wrong", g, t_miss)]
+    pairs = [(to_device(a.view(np.uint32), 0), to_device(b.view(np.uint32), 0)) for _, a, b in cases]
+    try:
+        for caps in ((-1, -1), (0, -1), (0, 0)):
+            P.topk_set_entry_capacity(*caps)
+            batched = P.topk_mean_batched(pairs, 1, 10)
+            for k, (name, a, b) in enumerate(cases):
+                log(f"  {name} caps={caps}")
+                single = P.topk_mean(*pairs[k], 1, 10)
+                assert same_record(single, batched[k]), f"{name} caps={caps}"
+                if caps == (-1, -1):
+                    assert_topk(single, oracle.topk(a.view(np.uint32), b.view(np.uint32), dtype=0, num=1, den=10),
+                                name)
+            if caps == (-1, -1):
+                refs = batched
+            else:
+                for k in range(len(cases)):
+                    assert same_record(batched[k], refs[k]), f"{cases[k][0]} caps={caps}"
+    finally:
+        P.topk_set_entry_capacity(-1, -1)
