@@ -280,8 +280,9 @@ def cpu_baseline(wl: Workload, threads: int, target_bytes: float = 12e9):
 
 def topk_measure(torch, P, prep_pairs, nbytes: int, reps: int = 3):
     """The paper's main score, the mean of the top 10% errors, over every pair
-    of the workload: peat_topk_mean_batched (binade histogram pass, then the
-    gathering pass and the rounds), and the stream-ordered
+    of the workload: peat_topk_mean_batched (a sampled guess of each pair's
+    boundary binade, the gathering pass that confirms it, the binade pass
+    only where a guess fails, and the rounds), and the stream-ordered
     peat_topk_mean_from_signature_batched_async fed with the device records
     of the step's signature call on the same stream (the binade pass skips
     every pair whose record bounds the k-th largest error to one bin; the
