@@ -81,8 +81,8 @@ __device__ __forceinline__ uint64_t signif(uint64_t key, int d0) {
 }
 
 // Entries carry their pair and the round of the gathering pass that wrote
-// them; a pair whose window gather did not fit is gathered again in round 1
-// and ignores what round 0 left.
+// them; a pair whose window did not fit, or whose guessed binade was wrong,
+// is gathered again in round 1 and ignores what round 0 left.
 constexpr uint32_t kPairMask = (1u << 30) - 1;
 __device__ __forceinline__ int32_t entry_tag(int pair, int round) { return (int32_t)((uint32_t)pair | ((uint32_t)round << 30)); }
 
@@ -893,8 +893,9 @@ __global__ void __launch_bounds__(kBlock) topk_select(TopkParams P) {
 }
 
 // One block per pair whose window was gathered: level 0 from the binade
-// histogram of its entries (need counts from the top of the window).  A
-// window that did not fit reopens level 0 for a binade pass and a second
+// histogram of its entries (need counts from the top of the window; for a
+// guess, from pass A's counts, which also confirm it).  A window that did
+// not fit, or a wrong guess, reopens level 0 for a binade pass and a second
 // gathering round.
 __global__ void __launch_bounds__(kBlock) topk_select_window(TopkParams P) {
     const int pair = blockIdx.x;
@@ -1187,7 +1188,7 @@ hipError_t launch_topk_rest(const TopkParams &p, const int64_t range[kKinds + 1]
     if ((e = ent_hist(0)) != hipSuccess) return e;
     hipLaunchKernelGGL(topk_select_window, dim3((unsigned)p.count), dim3(kBlock), 0, s, q);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // round 1: windows that did not fit take the binade pass and are gathered again
+    // round 1: windows that did not fit and wrong guesses take the binade pass and are gathered again
     q.round = 1;
     if ((e = launch_scan<kPass1>(q, range, s)) != hipSuccess) return e;
     if ((e = launch_select(q, 0, s)) != hipSuccess) return e;
