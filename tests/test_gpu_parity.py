@@ -120,6 +120,53 @@ def test_workload1_full():
     _check_pair(G.reshape(-1).view(np.uint32), T.reshape(-1).view(np.uint32), 0, ctx="workload 1")
 
 
+@pytest.mark.parametrize("code", [1, 2])
+def test_equal_vectors(code):
+    """Test tensors equal to their golden bit for bit over most of the pair
+    (the 16-bit kernels' equal-vector branch) with differences planted at a
+    low rate (some in a chunk's first vector), special goldens (zero, -0,
+    +-Inf, NaN, subnormal, the largest finite) that T repeats, +-0 pairs, and
+    bf16 values whose products leave binary32's normal range; each against
+    the oracle under absolute and relative thresholds, and single == batched."""
+    rng = np.random.default_rng(2609 + code)
+    sp = {1: [0x0000, 0x8000, 0x7C00, 0xFC00, 0x7E00, 0x0001, 0x83FF, 0x7BFF],
+          2: [0x0000, 0x8000, 0x7F80, 0xFF80, 0x7FC0, 0x0001, 0x807F, 0x7F7F]}[code]
+    cases = []
+    for n in (4096 * 64 + 4097, (1 << 20) + 3, 300005):
+        gb, _ = special_pair(n, code, seed=4400 + n, special_frac=0.0)
+        cases.append((f"all equal n={n}", gb, gb.copy()))
+        tb = gb.copy()
+        idx = rng.integers(0, n, max(1, n // 20000))
+        tb[idx] ^= np.asarray(1 << rng.integers(0, 16, idx.size), dtype=np.uint16)
+        tb[np.arange(0, n, 4096 * 3)] ^= 1                 # the first element of every third chunk
+        cases.append((f"planted flips n={n}", gb, tb))
+        g2 = gb.copy()
+        for val in sp:
+            g2[rng.integers(0, n, 3)] = val
+        cases.append((f"special goldens n={n}", g2, g2.copy()))
+        t3 = g2.copy()
+        z = rng.integers(0, n, 5)
+        g2z = g2.copy()
+        g2z[z] = 0x0000
+        t3[z] = 0x8000                                      # +0 against -0
+        cases.append((f"signed zeros n={n}", g2z, t3))
+    if code == 2:                                           # bf16 magnitudes near 2^+-120
+        n = 70001
+        big = float_to_bits(np.exp2(rng.uniform(100, 127, n)) * rng.choice([-1.0, 1.0], n), 2)
+        tiny = float_to_bits(np.exp2(rng.uniform(-133, -100, n)), 2)
+        cases.append(("bf16 huge", big, big.copy()))
+        cases.append(("bf16 tiny", tiny, tiny.copy()))
+    thr_rt = ((1e-6, 1e-3), (0.0, 1e-5))
+    for ctx, gb, tb in cases:
+        log(f"  dtype={code} {ctx}")
+        _check_pair(gb, tb, code, ctx=ctx)
+        _check_pair(gb, tb, code, thr=thr_rt, ctx=ctx + " rtol")
+    dev = [(to_device(gb, code), to_device(tb, code)) for _, gb, tb in cases]
+    batched = P.signature_batched(dev, synth.BINS, synth.THRESHOLDS)
+    for k, (g, t) in enumerate(dev):
+        assert records_equal(batched[k], P.signature(g, t, synth.BINS, synth.THRESHOLDS)), cases[k][0]
+
+
 def test_batched_equals_single_and_is_deterministic():
     pairs_host = []
     rng = np.random.default_rng(4)
