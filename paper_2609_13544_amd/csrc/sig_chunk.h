@@ -1275,28 +1275,34 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
         const uint32_t ib = (uint32_t)(i - run_first) << cur.log2;
         if (cur.nsuper > 0) {
             if (!pre) load(ga, ta, cur, 0);
-            // Every half step issues one set of loads (the next super-step,
-            // the next chunk's first, or a re-read of the current one when
-            // nothing follows), chosen by scalar selects, so every path has
-            // the same loads outstanding and the waits stay partial.
-            for (uint32_t s = 0;;) {
-                bool last = s + 1 >= cur.nsuper;
-                load(gb, tb, cur, last ? s : s + 1);
+            // Pairs of super-steps are pipelined: each half step issues one
+            // set of loads (the next super-step, or the next chunk's first at
+            // the end) before it works, so the waits stay partial.  An odd
+            // last super-step, loaded into (ga, ta) by the last pair (or by
+            // the chunk's start), is worked after the loop, and only then is
+            // the next chunk's first loaded into (ga, ta).  So no load into
+            // (gb, tb) is ever in flight when the chunk ends (its registers
+            // are reused there), and the next chunk's loads, in (ga, ta), stay
+            // in flight through the chunk's end.
+            const uint32_t npair = cur.nsuper & ~1u;
+            const bool odd = (cur.nsuper & 1u) != 0;
+            for (uint32_t s = 0; s < npair; s += 2) {
+                load(gb, tb, cur, s + 1);
                 step(ga, ta, s, ib);
-                if (last) {
-                    if (chain) load(ga, ta, nxt, 0);
-                    break;
-                }
-                ++s;
-                last = s + 1 >= cur.nsuper;
-                const bool hop = last && chain;
+                const bool last = s + 2 >= npair;
+                const bool hop = last && !odd && chain;
+                // (ga, ta) next: super-step s + 2 (the odd last one included),
+                // the next chunk's first, or a re-read when nothing follows
                 load_at(ga, ta, hop ? nxt.gbase : cur.gbase, hop ? nxt.tbase : cur.tbase, hop ? nxt.len : cur.len,
-                        hop ? 0u : (last ? s : s + 1));
-                step(gb, tb, s, ib);
-                if (last) break;
-                ++s;
-                // the deferred list must hold the next two super-steps
+                        hop ? 0u : (last && !odd ? s + 1 : s + 2));
+                step(gb, tb, s + 1, ib);
+                // the deferred list must hold the next two super-steps (or the
+                // odd last one)
                 if (ndef > kDeferCap - 2 * U) flush(cur, ib);
+            }
+            if (odd) {
+                step(ga, ta, npair, ib);
+                if (chain) load(ga, ta, nxt, 0);
             }
         }
         // a chunk without super-steps issued no load for the next one
