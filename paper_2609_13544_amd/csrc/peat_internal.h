@@ -70,6 +70,10 @@ static_assert(sizeof(SigDesc) == 48, "SigDesc layout");
 enum { C_VALID, C_FINITE, C_REL, C_NAN_G, C_NAN_T, C_INF_G, C_INF_T, C_NANPAIR, kCnt };
 
 struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
+    // 1 when the chunk ends its block's run of chunks of one pair: only then
+    // do the exact fields below (maxima to histogram) hold the run's values,
+    // otherwise they are not written
+    int64_t run_end;
     // binary64 sums of each wave of the block: |err|, err^2, rel, g^2, t^2, g*t
     double s[kWaves][6];
     double max_abs, max_rel;
@@ -85,6 +89,8 @@ struct alignas(16) ChunkPartial {   // one per chunk, written by the chunk pass
 // the chunk pass writes the counts followed by the mismatches as one array
 static_assert(offsetof(ChunkPartial, mism) == offsetof(ChunkPartial, cnt) + kCnt * sizeof(uint32_t),
               "ChunkPartial counts");
+// wave 0 writes run_end and its six sums as seven consecutive 8-byte words
+static_assert(offsetof(ChunkPartial, s) == sizeof(int64_t), "ChunkPartial run_end");
 
 struct SigParams {
     int64_t chunk_base;            // first global chunk of this launch

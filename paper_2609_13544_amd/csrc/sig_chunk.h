@@ -1057,36 +1057,21 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
             const double f_t2 = (L.s_g2 + 2.0 * L.s_ge) + L.s_sq;
             const double f_gt = L.s_g2 + L.s_ge;
             const double lane_sums[6] = {L.s_abs, L.s_sq + ga.sq, L.s_rel, L.s_g2 + ga.g2, f_t2 + ga.t2, f_gt + ga.gt};
+            // One store per wave: lanes 0-5 write its six totals (wave 0: lane 0
+            // the run-end flag, lanes 1-6 the totals).  A chunk that does not
+            // end the run writes nothing else: its record's exact fields are
+            // left as they are and the finalize skips them.
+            const int w0 = wave == 0 ? 1 : 0;
+            uint64_t word = run_end ? 1u : 0u;
 #pragma unroll
             for (int k = 0; k < 6; ++k) {
                 const double v = dpp_sum(lane_sums[k]);
-                if (lane == 0) out->s[wave][k] = v;
+                if (lane == k + w0) word = (uint64_t)__double_as_longlong(v);
             }
+            uint64_t *row = reinterpret_cast<uint64_t *>(out) + (w0 ? 0 : 1 + 6 * wave);
+            if (lane < 6 + w0) row[lane] = word;
         }
         reset_sums();
-        if (!run_end && wave == 0) {
-            // neutral values: this chunk's counts, maxima and histogram are
-            // carried into the record of the run's last chunk
-            out->hist[lane] = 0;
-            if (lane < kHistSlots - 64) out->hist[64 + lane] = 0;
-            if (lane < kCnt + PEAT_MAX_THRESHOLDS) {
-                int k = lane;
-                asm volatile("" : "+v"(k));
-                reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(out) + offsetof(ChunkPartial, cnt))[k] = 0;
-            }
-            if (lane == 0) {
-                // -1 formed here rather than kept live (and spilled) across the hot loop
-                int32_t m1;
-                asm volatile("v_mov_b32 %0, -1" : "=v"(m1));
-                const int64_t none = m1;
-                out->max_abs = (double)none;
-                out->max_rel = (double)none;
-                out->ix_abs = out->ix_rel = out->ix_ulp = none;
-                out->first_nan = out->first_valid = none;
-                out->sum_ulp = 0;
-                out->max_ulp = 0;
-            }
-        }
     };
 
     // End of a run: counts, maxima, first indices, ULP sum and histogram of

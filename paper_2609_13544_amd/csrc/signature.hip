@@ -38,22 +38,30 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
             s[k] += t;
         }
         // every field read before any comparison, so the loads go out together
-        // instead of one round trip per branch
+        // instead of one round trip per branch; the exact fields count only
+        // in a record that ends its block's run (the others were not written)
+        const int64_t pend = p.run_end;
         const double pma = p.max_abs, pmr = p.max_rel;
         const int64_t pia = p.ix_abs, pir = p.ix_rel, piu = p.ix_ulp, pfn = p.first_nan, pfv = p.first_valid;
         const uint64_t pmu = p.max_ulp, psu = p.sum_ulp;
         const uint32_t pfl = p.flips;
-        if (pia >= 0 && (ia < 0 || pma > ma || (pma == ma && pia < ia))) { ma = pma; ia = pia; }
-        if (pir >= 0 && (ir < 0 || pmr > mr || (pmr == mr && pir < ir))) { mr = pmr; ir = pir; }
-        if (piu >= 0 && (iu < 0 || pmu > mu || (pmu == mu && piu < iu))) { mu = pmu; iu = piu; }
-        if (pfn >= 0 && (fn < 0 || pfn < fn)) fn = pfn;
-        if (pfv >= 0 && (fv < 0 || pfv < fv)) fv = pfv;
-        sulp += psu;
+        uint32_t pcn[kCnt + PEAT_MAX_THRESHOLDS];
+#pragma unroll
+        for (int k = 0; k < kCnt; ++k) pcn[k] = p.cnt[k];
+#pragma unroll
+        for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) pcn[kCnt + j] = p.mism[j];
         if (P.inj_counts) flips += pfl;
+        // (no early exit: that would let the compiler load the exact fields
+        // only after the flag, one more round trip per record)
+        const bool e = pend != 0;
+        if (e && pia >= 0 && (ia < 0 || pma > ma || (pma == ma && pia < ia))) { ma = pma; ia = pia; }
+        if (e && pir >= 0 && (ir < 0 || pmr > mr || (pmr == mr && pir < ir))) { mr = pmr; ir = pir; }
+        if (e && piu >= 0 && (iu < 0 || pmu > mu || (pmu == mu && piu < iu))) { mu = pmu; iu = piu; }
+        if (e && pfn >= 0 && (fn < 0 || pfn < fn)) fn = pfn;
+        if (e && pfv >= 0 && (fv < 0 || pfv < fv)) fv = pfv;
+        sulp += e ? psu : 0u;
 #pragma unroll
-        for (int k = 0; k < kCnt; ++k) cn[k] += p.cnt[k];
-#pragma unroll
-        for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) cn[kCnt + j] += p.mism[j];
+        for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) cn[k] += e ? pcn[k] : 0u;
     }
     // histogram: wave w sums chunks w, w + 4, ... (lane l: slots l and 64 + l),
     // 32 chunks' loads in flight per step (a single pair's records are read
@@ -62,23 +70,35 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
         constexpr int D = 32;
         uint64_t h0 = 0, h1 = 0;
         const bool two = lane < kHistSlots - 64;
+        // every lane loads a valid slot (its value is masked afterwards): a
+        // load only some lanes make becomes a branch with a full wait inside,
+        // which would take the loads one round trip at a time
+        const int lb = 64 + (two ? lane : 0);
         int c = wave;
         for (; c + (D - 1) * kWaves < m; c += D * kWaves) {
             uint32_t a[D], b[D];
 #pragma unroll
             for (int u = 0; u < D; ++u) {
                 a[u] = parts[c + u * kWaves].hist[lane];
-                b[u] = two ? parts[c + u * kWaves].hist[64 + lane] : 0u;
+                b[u] = parts[c + u * kWaves].hist[lb];
             }
+            // the step's run-end flags, lane u reading chunk u's, issued after
+            // the histogram rows so that one wait covers all of them (a wait
+            // for the flags first costs a round trip per step)
+            const int64_t fl = parts[c + (lane & (D - 1)) * kWaves].run_end;
+            const uint64_t em = __ballot(fl != 0);
 #pragma unroll
             for (int u = 0; u < D; ++u) {
-                h0 += a[u];
-                h1 += b[u];
+                const bool e = (em >> u) & 1u;
+                h0 += e ? a[u] : 0u;
+                h1 += (e && two) ? b[u] : 0u;
             }
         }
         for (; c < m; c += kWaves) {
-            h0 += parts[c].hist[lane];
-            if (two) h1 += parts[c].hist[64 + lane];
+            const bool e = parts[c].run_end != 0;
+            const uint32_t a = parts[c].hist[lane], b = parts[c].hist[lb];
+            h0 += e ? a : 0u;
+            h1 += (e && two) ? b : 0u;
         }
         sh_hwave[wave][lane] = h0;
         if (two) sh_hwave[wave][64 + lane] = h1;
