@@ -473,11 +473,12 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 // With no negative absolute tolerance a zero error is close under every
 // threshold (the allowance atol + |rtol g| is at least atol >= 0).  What is
 // left is the sum of g^2, in the same order as below, and eight counts in the
-// zero bin, so the records are bit-identical to the full path's.  A golden that is zero, infinite or NaN
-// (excluded from the relative or finite fields) sends the vector down the
-// full path: each half-vector's product of four binary32 goldens is normal
-// only if none of them is (four f16 magnitudes stay within [2^-96, 2^64];
-// a bf16 product that leaves the normal range just takes the full path).
+// zero bin, so the records are bit-identical to the full path's.  A golden
+// that is zero, infinite or NaN (excluded from the relative or finite
+// fields) sends the vector down the full path: each half-vector's product of
+// four binary32 goldens is normal only if none of them is (four f16
+// magnitudes stay within [2^-96, 2^64]; a bf16 product that leaves the
+// normal range just takes the full path).
 // Replays of a deterministic kernel's output are bit-identical to the golden
 // except where a fault struck, so this is their common case.
 template <int DT, int NT, bool RT>
@@ -912,12 +913,13 @@ struct ChunkCtx {
 //
 // Only the binary64 sums depend on how elements are grouped, so only they
 // are reduced per chunk, per wave, with no block barrier: each wave writes its
-// six totals into the chunk record.  Everything else (counts, maxima with
-// their lowest index, first indices, the ULP sum, the histogram) is exact and
-// independent of grouping, so it is carried over the block's run of
-// consecutive chunks of one pair (indices relative to the run) and reduced
-// once, into the record of the run's last chunk; the other records of the run
-// hold neutral values there.  A run has at most kMaxGroup (8) chunks of at
+// six totals into the chunk record (one store).  Everything else (counts,
+// maxima with their lowest index, first indices, the ULP sum, the histogram)
+// is exact and independent of grouping, so it is carried over the block's run
+// of consecutive chunks of one pair (indices relative to the run) and reduced
+// once, into the record of the run's last chunk, whose run-end flag is 1; the
+// other records of the run carry a flag of 0 and no exact fields, and the
+// finalize skips those fields.  A run has at most kMaxGroup (8) chunks of at
 // most 2^18 elements, so a lane counts at most 8192 elements per histogram
 // slot.
 template <int DG, int DT, int NT, bool RT, bool INJ>
