@@ -192,7 +192,7 @@ struct Uni {
     uint32_t wu;                           // running max ULP
 };
 
-struct Shared {
+struct alignas(16) Shared {
     uint8_t hrow[4096];                    // binary64 sign and exponent field -> histogram slot
     // Lane-private 16-bit counters, two per word: word [slot][t mod 128]
     // holds lane t's count in its low half when t < 128 and in its high half
@@ -209,6 +209,36 @@ struct Shared {
     uint64_t rulp[kWaves];
     uint32_t rcnt[kWaves][kCnt + PEAT_MAX_THRESHOLDS];
 };
+
+// Clear the lane-private histogram counters and build the exponent table:
+// slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi; four
+// exponent fields per word, the same slots for either sign.
+__device__ __forceinline__ void init_tables(Shared &sh, const SigParams &P, int tid) {
+    uint4 *h4 = reinterpret_cast<uint4 *>(sh.hist);
+    for (int i = tid; i < kHistSlots * kHistCols / 4; i += kBlock) h4[i] = make_uint4(0u, 0u, 0u, 0u);
+    const int w = (P.hi - P.lo) / P.nbins;
+    uint32_t *t4 = reinterpret_cast<uint32_t *>(sh.hrow);
+    for (int q = tid; q < 512; q += kBlock) {
+        uint32_t word = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int E = 4 * q + j;           // biased exponent of |value|
+            int slot;
+            if (E == 0) {
+                slot = 0;
+            } else if (E == 2047) {
+                slot = P.nbins + 2;            // infinite error
+            } else {
+                const int k = E - 1023;        // a in [2^k, 2^(k+1))
+                slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
+            }
+            word |= (uint32_t)slot << (8 * j);
+        }
+        t4[q] = word;
+        t4[512 + q] = word;
+    }
+}
+static_assert((kHistSlots * kHistCols) % 4 == 0 && offsetof(Shared, hist) % 16 == 0, "16-byte histogram clears");
 
 __device__ __forceinline__ void lane_init(Lane &L, Uni &U) {
     L.s_abs = L.s_rel = L.s_sq = L.s_g2 = L.s_ge = 0.0;
@@ -829,7 +859,8 @@ __device__ __forceinline__ void dmax_step(V &v, uint32_t &ix) {
     else
         ov = dpp_u32<C, RM>(v, v);
     const uint32_t oi = dpp_u32<C, RM>(ix, ix);
-    const bool take = (oi != kNone) && (ix == kNone || ov > v || (ov == v && oi < ix));
+    // bitwise, not short-circuit: no branch per comparison
+    const bool take = (oi != kNone) & ((ix == kNone) | (ov > v) | ((ov == v) & (oi < ix)));
     v = take ? ov : v;
     ix = take ? oi : ix;
 }
@@ -867,21 +898,28 @@ __device__ __forceinline__ uint32_t dpp_min_u32(uint32_t v) {
     dmin_step<kDppBcast31, 0xC>(v);
     return lane63_u32(v);
 }
-// Wave (value desc, index asc) maximum over entries with index != kNone, as
-// scalars.
-template <typename V>
-__device__ __forceinline__ void dpp_max(V &v, uint32_t &ix) {
-    dmax_step<kDppXor1, 0xF>(v, ix);
-    dmax_step<kDppXor2, 0xF>(v, ix);
-    dmax_step<kDppHalfMirror, 0xF>(v, ix);
-    dmax_step<kDppMirror, 0xF>(v, ix);
-    dmax_step<kDppBcast15, 0xA>(v, ix);
-    dmax_step<kDppBcast31, 0xC>(v, ix);
-    if constexpr (sizeof(V) == 8)
-        v = lane63_f64(v);
-    else
-        v = lane63_u32(v);
-    ix = lane63_u32(ix);
+// Wave (value desc, index asc) maxima over entries with index != kNone of
+// |err|, the relative error and the ULP distance, as scalars; the three go
+// step by step so that their data moves overlap.
+template <int C, int RM>
+__device__ __forceinline__ void dmax3_step(double &a, uint32_t &ia, double &r, uint32_t &ir, uint32_t &u, uint32_t &iu) {
+    dmax_step<C, RM>(a, ia);
+    dmax_step<C, RM>(r, ir);
+    dmax_step<C, RM>(u, iu);
+}
+__device__ __forceinline__ void dpp_max3(double &a, uint32_t &ia, double &r, uint32_t &ir, uint32_t &u, uint32_t &iu) {
+    dmax3_step<kDppXor1, 0xF>(a, ia, r, ir, u, iu);
+    dmax3_step<kDppXor2, 0xF>(a, ia, r, ir, u, iu);
+    dmax3_step<kDppHalfMirror, 0xF>(a, ia, r, ir, u, iu);
+    dmax3_step<kDppMirror, 0xF>(a, ia, r, ir, u, iu);
+    dmax3_step<kDppBcast15, 0xA>(a, ia, r, ir, u, iu);
+    dmax3_step<kDppBcast31, 0xC>(a, ia, r, ir, u, iu);
+    a = lane63_f64(a);
+    r = lane63_f64(r);
+    u = lane63_u32(u);
+    ia = lane63_u32(ia);
+    ir = lane63_u32(ir);
+    iu = lane63_u32(iu);
 }
 
 
@@ -1083,9 +1121,7 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
         {
             double mxa = L.gx_abs, mxr = L.mx_rel;
             uint32_t ixa = L.gi_abs, ixr = L.ix_rel, mu = L.gu, ixu = L.gi_ulp;
-            dpp_max(mxa, ixa);
-            dpp_max(mxr, ixr);
-            dpp_max(mu, ixu);
+            dpp_max3(mxa, ixa, mxr, ixr, mu, ixu);
             const uint32_t fnan = dpp_min_u32(L.first_nan), fval = dpp_min_u32(L.first_valid);
             // at most 2^45 per lane (8192 distances below 2^32): exact in binary64
             const uint64_t sulp = (uint64_t)dpp_sum((double)L.s_ulp);
@@ -1119,17 +1155,19 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
 
         ChunkPartial *out = partials + c.gchunk;
         // histogram: thread t sums slot t/4 over a quarter of the words and
-        // clears them for the next run
+        // clears them for the next run, 16 bytes at a time (the groups are
+        // rotated so that eight consecutive lanes touch all 32 banks)
         {
             const int slot = tid >> 2, q = tid & 3;
             uint32_t acc = 0;
-            uint32_t *row = sh.hist + slot * kHistCols + q * 32;
-#pragma unroll 8
-            for (int k = 0; k < 32; ++k) {
-                const int col = (k + slot + 8 * q) & 31;
-                const uint32_t w = row[col];
-                row[col] = 0;
-                acc += (w & 0xFFFFu) + (w >> 16);
+            uint4 *row = reinterpret_cast<uint4 *>(sh.hist + slot * kHistCols + q * 32);
+#pragma unroll 2
+            for (int k = 0; k < 8; ++k) {
+                const int g = (k + slot + 2 * q) & 7;
+                const uint4 w = row[g];
+                row[g] = make_uint4(0u, 0u, 0u, 0u);
+                acc += ((w.x & 0xFFFFu) + (w.x >> 16)) + ((w.y & 0xFFFFu) + (w.y >> 16)) +
+                       ((w.z & 0xFFFFu) + (w.z >> 16)) + ((w.w & 0xFFFFu) + (w.w >> 16));
             }
             dsum_step<kDppXor1, 0xF>(acc);        // the four quarters of the slot
             dsum_step<kDppXor2, 0xF>(acc);
@@ -1244,11 +1282,16 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
             }
             __syncthreads();
         }
-        for (int i = tid; i < kHistSlots * kHistCols; i += kBlock) sh.hist[i] = 0;
-        __syncthreads();
     }
     PairS dcur = pair_of(c0);
     ChunkCtx cur = ctx(dcur, c0);
+    // the block's first super-step is in flight while it sets up its tables
+    if (cur.nsuper > 0) {
+        load(ga, ta, cur, 0);
+        pre = true;
+    }
+    init_tables(sh, P, tid);
+    __syncthreads();
     for (int i = 0; i < cnt; ++i) {
         const int64_t c = c0 + i;
         const bool more = i + 1 < cnt;
@@ -1318,25 +1361,6 @@ __global__ void __launch_bounds__(kBlock, (chunk_blocks_per_cu<DG, DT, NT, RT>()
     sig_chunk(SigParams P, const SigDesc *__restrict__ descs, const int32_t *__restrict__ chunk_pair,
               ChunkPartial *__restrict__ partials, const InjDesc *__restrict__ inj) {
     __shared__ Shared sh;
-    const int tid = threadIdx.x;
-    // clear the lane-private histogram counters and build the exponent table:
-    // slot 0 error 0, slot 1 below 2^lo, slots 2.. bins, last slot >= 2^hi
-    for (int i = tid; i < kHistSlots * kHistCols; i += kBlock) sh.hist[i] = 0;
-    const int w = (P.hi - P.lo) / P.nbins;
-    for (int x = tid; x < 4096; x += kBlock) {
-        const int E = x & 2047;                // either sign: the slot of |value|
-        int slot;
-        if (E == 0) {
-            slot = 0;
-        } else if (E == 2047) {
-            slot = P.nbins + 2;                // infinite error
-        } else {
-            const int k = E - 1023;            // a in [2^k, 2^(k+1))
-            slot = k < P.lo ? 1 : (k >= P.hi ? P.nbins + 2 : 2 + (k - P.lo) / w);
-        }
-        sh.hrow[x] = (uint8_t)slot;
-    }
-    __syncthreads();
     chunk_loop<DG, DT, NT, RT, INJ>(P, sh, descs, chunk_pair, partials, inj);
 }
 

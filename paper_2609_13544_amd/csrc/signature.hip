@@ -6,197 +6,326 @@ namespace peat {
 namespace {
 
 // ---- pass 2 ----------------------------------------------------------------
+// The output record as 8-byte words in declaration order: n, the eight
+// counts, first_nan_index, the mismatch counts, hist_zero, hist_under,
+// hist_over, the bins, max_abs .. argmax_rel and the six sums.
+constexpr int kW_n = 0, kW_cnt = 1, kW_fnan = kW_cnt + kCnt, kW_mism = kW_fnan + 1,
+              kW_hzero = kW_mism + PEAT_MAX_THRESHOLDS, kW_hunder = kW_hzero + 1, kW_hover = kW_hzero + 2,
+              kW_hist = kW_hzero + 3, kW_maxabs = kW_hist + PEAT_MAX_BINS, kW_ixabs = kW_maxabs + 1,
+              kW_maxulp = kW_maxabs + 2, kW_ixulp = kW_maxabs + 3, kW_sumulp = kW_maxabs + 4,
+              kW_maxrel = kW_maxabs + 5, kW_ixrel = kW_maxabs + 6, kW_sums = kW_maxabs + 7, kOutWords = kW_sums + 6;
+static_assert(sizeof(peat_signature_t) == kOutWords * 8, "peat_signature_t words");
+static_assert(offsetof(peat_signature_t, n_valid) == (kW_cnt + C_VALID) * 8 &&
+                  offsetof(peat_signature_t, n_finite) == (kW_cnt + C_FINITE) * 8 &&
+                  offsetof(peat_signature_t, n_rel) == (kW_cnt + C_REL) * 8 &&
+                  offsetof(peat_signature_t, n_nan_golden) == (kW_cnt + C_NAN_G) * 8 &&
+                  offsetof(peat_signature_t, n_nan_test) == (kW_cnt + C_NAN_T) * 8 &&
+                  offsetof(peat_signature_t, n_inf_golden) == (kW_cnt + C_INF_G) * 8 &&
+                  offsetof(peat_signature_t, n_inf_test) == (kW_cnt + C_INF_T) * 8 &&
+                  offsetof(peat_signature_t, n_nan_pairs) == (kW_cnt + C_NANPAIR) * 8,
+              "peat_signature_t counts");
+static_assert(offsetof(peat_signature_t, first_nan_index) == kW_fnan * 8 &&
+                  offsetof(peat_signature_t, n_mismatch) == kW_mism * 8 &&
+                  offsetof(peat_signature_t, hist_zero) == kW_hzero * 8 &&
+                  offsetof(peat_signature_t, hist_under) == kW_hunder * 8 &&
+                  offsetof(peat_signature_t, hist_over) == kW_hover * 8 && offsetof(peat_signature_t, hist) == kW_hist * 8,
+              "peat_signature_t histogram");
+static_assert(offsetof(peat_signature_t, max_abs) == kW_maxabs * 8 &&
+                  offsetof(peat_signature_t, argmax_abs) == kW_ixabs * 8 &&
+                  offsetof(peat_signature_t, max_ulp) == kW_maxulp * 8 &&
+                  offsetof(peat_signature_t, argmax_ulp) == kW_ixulp * 8 &&
+                  offsetof(peat_signature_t, sum_ulp) == kW_sumulp * 8 &&
+                  offsetof(peat_signature_t, max_rel) == kW_maxrel * 8 &&
+                  offsetof(peat_signature_t, argmax_rel) == kW_ixrel * 8 &&
+                  offsetof(peat_signature_t, sum_abs) == kW_sums * 8 && offsetof(peat_signature_t, sum_gt) == (kW_sums + 5) * 8,
+              "peat_signature_t maxima and sums");
+static_assert(kHistSlots == 67, "histogram tail: three slots beyond the wave's 64 lanes");
+
+// Output word of histogram slot s (zero | under | bins | over, then unused
+// slots, which are zero, onto the unused bins): a bijection of the 67 slots
+// onto the words hist_zero .. hist[63].
+__device__ __forceinline__ int slot_word(int s, int nb) {
+    return s == 0 ? kW_hzero
+                  : (s == 1 ? kW_hunder : (s == nb + 2 ? kW_hover : (s <= nb + 1 ? kW_hist + s - 2 : kW_hist + s - 3)));
+}
+
+// The fields of a chunk record that the finalize reads.
+struct RecF {
+    double s[kWaves][6];
+    int64_t end, ia, ir, iu, fn;
+    double ma, mr;
+    uint64_t su;
+    uint32_t mu, fl;
+    uint32_t cn[kCnt + PEAT_MAX_THRESHOLDS];
+};
+__device__ __forceinline__ RecF load_rec(const ChunkPartial &p) {
+    RecF r;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w)
+#pragma unroll
+        for (int k = 0; k < 6; ++k) r.s[w][k] = p.s[w][k];
+    r.end = p.run_end;
+    r.ma = p.max_abs;
+    r.mr = p.max_rel;
+    r.ia = p.ix_abs;
+    r.ir = p.ix_rel;
+    r.iu = p.ix_ulp;
+    r.fn = p.first_nan;
+    r.su = p.sum_ulp;
+    r.mu = p.max_ulp;
+    r.fl = p.flips;
+#pragma unroll
+    for (int k = 0; k < kCnt; ++k) r.cn[k] = p.cnt[k];
+#pragma unroll
+    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) r.cn[kCnt + j] = p.mism[j];
+    return r;
+}
+
+// (value desc, index asc) maximum over entries with index >= 0.
+template <typename V>
+__device__ __forceinline__ void lex_take(V &v, int64_t &ix, V ov, int64_t oi) {
+    // bitwise, not short-circuit: no branch per comparison
+    const bool take = (oi >= 0) & ((ix < 0) | (ov > v) | ((ov == v) & (oi < ix)));
+    v = take ? ov : v;
+    ix = take ? oi : ix;
+}
+
+// A thread's share of a pair: binary64 sums over its records in order (each
+// record's waves in order), the maxima, first NaN and counts of the records
+// that end a run (the others carry no exact fields).
+struct FinAcc {
+    double s[6];
+    double ma, mr;
+    int64_t ia, ir, iu;
+    uint64_t fn;                             // first NaN index, ~0 = none
+    uint64_t mu, sulp, flips;
+    uint64_t cn[kCnt + PEAT_MAX_THRESHOLDS];
+};
+__device__ __forceinline__ void fin_merge(FinAcc &A, const RecF &r, bool have) {
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+        double t = r.s[0][k];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) t += r.s[w][k];
+        // the sum starts at +0 and never becomes -0, so adding +0 is exact
+        A.s[k] += have ? t : 0.0;
+    }
+    const bool e = have && r.end != 0;
+    lex_take(A.ma, A.ia, r.ma, e ? r.ia : int64_t(-1));
+    lex_take(A.mr, A.ir, r.mr, e ? r.ir : int64_t(-1));
+    lex_take(A.mu, A.iu, (uint64_t)r.mu, e ? r.iu : int64_t(-1));
+    A.fn = (e && r.fn >= 0 && (uint64_t)r.fn < A.fn) ? (uint64_t)r.fn : A.fn;
+    A.sulp += e ? r.su : 0u;
+    A.flips += have ? r.fl : 0u;
+#pragma unroll
+    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) A.cn[k] += e ? r.cn[k] : 0u;
+}
+
+template <int C, int RM>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t old, uint64_t x) {
+    const uint32_t lo = dpp_u32<C, RM>((uint32_t)old, (uint32_t)x);
+    const uint32_t hi = dpp_u32<C, RM>((uint32_t)(old >> 32), (uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+// One step of the wave reductions of the three maxima and the first NaN,
+// interleaved so that their data moves overlap.  A lane that DPP does not
+// write keeps its own entry, which merges with itself unchanged.
+template <int C, int RM>
+__device__ __forceinline__ void fin_step(FinAcc &A) {
+    const double oma = dpp_f64<C, RM>(A.ma, A.ma), omr = dpp_f64<C, RM>(A.mr, A.mr);
+    const uint64_t omu = dpp_u64<C, RM>(A.mu, A.mu), ofn = dpp_u64<C, RM>(A.fn, A.fn);
+    const int64_t oia = (int64_t)dpp_u64<C, RM>((uint64_t)A.ia, (uint64_t)A.ia);
+    const int64_t oir = (int64_t)dpp_u64<C, RM>((uint64_t)A.ir, (uint64_t)A.ir);
+    const int64_t oiu = (int64_t)dpp_u64<C, RM>((uint64_t)A.iu, (uint64_t)A.iu);
+    lex_take(A.ma, A.ia, oma, oia);
+    lex_take(A.mr, A.ir, omr, oir);
+    lex_take(A.mu, A.iu, omu, oiu);
+    A.fn = ofn < A.fn ? ofn : A.fn;
+}
+__device__ __forceinline__ uint64_t lane63_u64(uint64_t v) {
+    return ((uint64_t)lane63_u32((uint32_t)(v >> 32)) << 32) | lane63_u32((uint32_t)v);
+}
+// Wave total of nonnegative integers: in 32 bits when the total is known to
+// stay below 2^31 (small, uniform), else exactly in binary64 (below 2^53).
+__device__ __forceinline__ uint64_t wave_total(uint64_t v, bool small) {
+    return small ? (uint64_t)dpp_sum_u32((uint32_t)v) : (uint64_t)dpp_sum((double)v);
+}
+
 __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     const int pair = blockIdx.x;
-    const SigDesc d = P.single ? P.one : P.descs[pair];
-    const ChunkPartial *parts = P.partials + d.first_chunk;
-    const int m = d.nchunks;
+    // the pair's fields (uniform: scalar loads from the arguments or the table)
+    int64_t n, first;
+    int m;
+    if (P.single) {
+        n = P.one.n;
+        first = P.one.first_chunk;
+        m = P.one.nchunks;
+    } else {
+        n = P.descs[pair].n;
+        first = P.descs[pair].first_chunk;
+        m = P.descs[pair].nchunks;
+    }
+    n = (int64_t)uniform_u64((uint64_t)n);
+    m = (int)__builtin_amdgcn_readfirstlane((uint32_t)m);
+    const ChunkPartial *parts = P.partials + (int64_t)uniform_u64((uint64_t)first);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-
-    __shared__ double sd[kWaves][8];
-    __shared__ int64_t si[kWaves][5];
-    __shared__ uint64_t su[kWaves][2 + kCnt + PEAT_MAX_THRESHOLDS];
-    __shared__ uint64_t sh_hist[kHistSlots];
-    __shared__ uint64_t sh_hwave[kWaves][kHistSlots];
-    __shared__ uint64_t su_flips[kWaves];
-
-    // binary64 sums: each thread a fixed strided subset in order, then a fixed tree
-    double s[6] = {0, 0, 0, 0, 0, 0};
-    double ma = -1.0, mr = -1.0;
-    int64_t ia = -1, ir = -1, iu = -1, fn = -1, fv = -1;
-    uint64_t mu = 0, sulp = 0, flips = 0;
-    uint64_t cn[kCnt + PEAT_MAX_THRESHOLDS];
-#pragma unroll
-    for (int c = 0; c < kCnt + PEAT_MAX_THRESHOLDS; ++c) cn[c] = 0;
-    for (int c = tid; c < m; c += kBlock) {
-        const ChunkPartial &p = parts[c];
-#pragma unroll
-        for (int k = 0; k < 6; ++k) {
-            double t = p.s[0][k];                 // the chunk: its waves in order
-#pragma unroll
-            for (int w = 1; w < kWaves; ++w) t += p.s[w][k];
-            s[k] += t;
-        }
-        // every field read before any comparison, so the loads go out together
-        // instead of one round trip per branch; the exact fields count only
-        // in a record that ends its block's run (the others were not written)
-        const int64_t pend = p.run_end;
-        const double pma = p.max_abs, pmr = p.max_rel;
-        const int64_t pia = p.ix_abs, pir = p.ix_rel, piu = p.ix_ulp, pfn = p.first_nan, pfv = p.first_valid;
-        const uint64_t pmu = p.max_ulp, psu = p.sum_ulp;
-        const uint32_t pfl = p.flips;
-        uint32_t pcn[kCnt + PEAT_MAX_THRESHOLDS];
-#pragma unroll
-        for (int k = 0; k < kCnt; ++k) pcn[k] = p.cnt[k];
-#pragma unroll
-        for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j) pcn[kCnt + j] = p.mism[j];
-        if (P.inj_counts) flips += pfl;
-        // (no early exit: that would let the compiler load the exact fields
-        // only after the flag, one more round trip per record)
-        const bool e = pend != 0;
-        if (e && pia >= 0 && (ia < 0 || pma > ma || (pma == ma && pia < ia))) { ma = pma; ia = pia; }
-        if (e && pir >= 0 && (ir < 0 || pmr > mr || (pmr == mr && pir < ir))) { mr = pmr; ir = pir; }
-        if (e && piu >= 0 && (iu < 0 || pmu > mu || (pmu == mu && piu < iu))) { mu = pmu; iu = piu; }
-        if (e && pfn >= 0 && (fn < 0 || pfn < fn)) fn = pfn;
-        if (e && pfv >= 0 && (fv < 0 || pfv < fv)) fv = pfv;
-        sulp += e ? psu : 0u;
-#pragma unroll
-        for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) cn[k] += e ? pcn[k] : 0u;
-    }
-    // histogram: wave w sums chunks w, w + 4, ... (lane l: slots l and 64 + l),
-    // 32 chunks' loads in flight per step (a single pair's records are read
-    // in few round trips); the waves are added in order
-    {
-        constexpr int D = 32;
-        uint64_t h0 = 0, h1 = 0;
-        const bool two = lane < kHistSlots - 64;
-        // every lane loads a valid slot (its value is masked afterwards): a
-        // load only some lanes make becomes a branch with a full wait inside,
-        // which would take the loads one round trip at a time
-        const int lb = 64 + (two ? lane : 0);
-        int c = wave;
-        for (; c + (D - 1) * kWaves < m; c += D * kWaves) {
-            uint32_t a[D], b[D];
-#pragma unroll
-            for (int u = 0; u < D; ++u) {
-                a[u] = parts[c + u * kWaves].hist[lane];
-                b[u] = parts[c + u * kWaves].hist[lb];
-            }
-            // the step's run-end flags, lane u reading chunk u's, issued after
-            // the histogram rows so that one wait covers all of them (a wait
-            // for the flags first costs a round trip per step)
-            const int64_t fl = parts[c + (lane & (D - 1)) * kWaves].run_end;
-            const uint64_t em = __ballot(fl != 0);
-#pragma unroll
-            for (int u = 0; u < D; ++u) {
-                const bool e = (em >> u) & 1u;
-                h0 += e ? a[u] : 0u;
-                h1 += (e && two) ? b[u] : 0u;
-            }
-        }
-        for (; c < m; c += kWaves) {
-            const bool e = parts[c].run_end != 0;
-            const uint32_t a = parts[c].hist[lane], b = parts[c].hist[lb];
-            h0 += e ? a : 0u;
-            h1 += (e && two) ? b : 0u;
-        }
-        sh_hwave[wave][lane] = h0;
-        if (two) sh_hwave[wave][64 + lane] = h1;
-    }
-    __syncthreads();
-    if (tid < kHistSlots) {
-        uint64_t h = 0;
-        for (int w = 0; w < kWaves; ++w) h += sh_hwave[w][tid];
-        sh_hist[tid] = h;
-    }
-#pragma unroll
-    for (int k = 0; k < 6; ++k) s[k] = dpp_sum(s[k]);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const double ova = __shfl_xor(ma, o), ovr = __shfl_xor(mr, o);
-        const int64_t oia = __shfl_xor(ia, o), oir = __shfl_xor(ir, o), oiu = __shfl_xor(iu, o);
-        const uint64_t omu = __shfl_xor(mu, o);
-        const int64_t ofn = __shfl_xor(fn, o), ofv = __shfl_xor(fv, o);
-        if (oia >= 0 && (ia < 0 || ova > ma || (ova == ma && oia < ia))) { ma = ova; ia = oia; }
-        if (oir >= 0 && (ir < 0 || ovr > mr || (ovr == mr && oir < ir))) { mr = ovr; ir = oir; }
-        if (oiu >= 0 && (iu < 0 || omu > mu || (omu == mu && oiu < iu))) { mu = omu; iu = oiu; }
-        if (ofn >= 0 && (fn < 0 || ofn < fn)) fn = ofn;
-        if (ofv >= 0 && (fv < 0 || ofv < fv)) fv = ofv;
-    }
-    // integer totals by DPP in binary64, exact: a count is at most 2^46, and
-    // the ULP sum goes as two halves of 32 bits (each wave total below 2^52)
-    sulp = ((uint64_t)dpp_sum((double)(sulp >> 32)) << 32) + (uint64_t)dpp_sum((double)(sulp & 0xFFFFFFFFu));
-    if (P.inj_counts) {
-        flips = (uint64_t)dpp_sum((double)flips);
-        if (lane == 0) su_flips[wave] = flips;
-    }
-#pragma unroll
-    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) cn[k] = (uint64_t)dpp_sum((double)cn[k]);
-    if (lane == 0) {
-        for (int k = 0; k < 6; ++k) sd[wave][k] = s[k];
-        sd[wave][6] = ma;
-        sd[wave][7] = mr;
-        si[wave][0] = ia; si[wave][1] = ir; si[wave][2] = iu; si[wave][3] = fn; si[wave][4] = fv;
-        su[wave][0] = mu;
-        su[wave][1] = sulp;
-        for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) su[wave][2 + k] = cn[k];
-    }
-    __syncthreads();
-    if (tid != 0) return;
-    if (P.inj_counts) {
-        uint64_t f = 0;
-        for (int w = 0; w < kWaves; ++w) f += su_flips[w];
-        P.inj_counts[pair] = (int64_t)f;
-    }
-    double S[6] = {0, 0, 0, 0, 0, 0};
-    double MA = -1.0, MR = -1.0;
-    int64_t IA = -1, IR = -1, IU = -1, FN = -1;
-    uint64_t MU = 0, SU = 0, CN[kCnt + PEAT_MAX_THRESHOLDS];
-    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) CN[k] = 0;
-    for (int w = 0; w < kWaves; ++w) {
-        for (int k = 0; k < 6; ++k) S[k] += sd[w][k];
-        const double va = sd[w][6], vr = sd[w][7];
-        const int64_t xa = si[w][0], xr = si[w][1], xu = si[w][2];
-        if (xa >= 0 && (IA < 0 || va > MA || (va == MA && xa < IA))) { MA = va; IA = xa; }
-        if (xr >= 0 && (IR < 0 || vr > MR || (vr == MR && xr < IR))) { MR = vr; IR = xr; }
-        if (xu >= 0 && (IU < 0 || su[w][0] > MU || (su[w][0] == MU && xu < IU))) { MU = su[w][0]; IU = xu; }
-        if (si[w][3] >= 0 && (FN < 0 || si[w][3] < FN)) FN = si[w][3];
-        SU += su[w][1];
-        for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) CN[k] += su[w][2 + k];
-    }
     const int nb = P.nbins;
-    peat_signature_t o;
-    o.n = d.n;
-    o.n_valid = (int64_t)CN[C_VALID];
-    o.n_finite = (int64_t)CN[C_FINITE];
-    o.n_rel = (int64_t)CN[C_REL];
-    o.n_nan_golden = (int64_t)CN[C_NAN_G];
-    o.n_nan_test = (int64_t)CN[C_NAN_T];
-    o.n_inf_golden = (int64_t)CN[C_INF_G];
-    o.n_inf_test = (int64_t)CN[C_INF_T];
-    o.n_nan_pairs = (int64_t)CN[C_NANPAIR];
-    o.first_nan_index = FN;
-    for (int j = 0; j < PEAT_MAX_THRESHOLDS; ++j)
-        o.n_mismatch[j] = j < P.nthr ? (int64_t)(CN[kCnt + j] + CN[C_NANPAIR]) : 0;
-    o.hist_zero = (int64_t)sh_hist[0];
-    o.hist_under = (int64_t)sh_hist[1];
-    o.hist_over = (int64_t)sh_hist[nb + 2];
-    for (int b = 0; b < PEAT_MAX_BINS; ++b) o.hist[b] = b < nb ? (int64_t)sh_hist[2 + b] : 0;
-    const double qnan = __longlong_as_double(0x7FF8000000000000LL);
-    o.max_abs = IA >= 0 ? MA : qnan;
-    o.argmax_abs = IA;
-    o.max_ulp = IU >= 0 ? (int64_t)MU : 0;
-    o.argmax_ulp = IU;
-    o.sum_ulp = SU;
-    o.max_rel = IR >= 0 ? MR : qnan;
-    o.argmax_rel = IR;
-    o.sum_abs = S[0];
-    o.sum_sq = S[1];
-    o.sum_rel = S[2];
-    o.sum_g2 = S[3];
-    o.sum_t2 = S[4];
-    o.sum_gt = S[5];
-    P.outs[pair] = o;
+
+    __shared__ uint64_t wv[kWaves][kOutWords + 1];   // each wave's additive words (+ flips)
+    __shared__ double wd[kWaves][8];                 // six sums, max_abs, max_rel
+    __shared__ int64_t wi[kWaves][4];                // argmax_abs, argmax_rel, argmax_ulp, first NaN
+    __shared__ uint64_t wmu[kWaves];
+
+    FinAcc A;
+#pragma unroll
+    for (int k = 0; k < 6; ++k) A.s[k] = 0.0;
+    A.ma = A.mr = -1.0;
+    A.ia = A.ir = A.iu = -1;
+    A.fn = ~uint64_t(0);
+    A.mu = A.sulp = A.flips = 0;
+#pragma unroll
+    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) A.cn[k] = 0;
+    // histogram: wave w sums chunks w, w + 4, ... in steps of 64 chunks; lane
+    // l holds slot l, and lane l < 63 the tail slot 64 + l % 3 of the step's
+    // chunks l / 3 + 21 j (every chunk and tail slot once)
+    uint64_t h0 = 0, ht = 0;
+    if (m > 0) {                              // uniform: no record to read otherwise
+        const int last = m - 1;
+        const int tr = lane / 3, tslot = 64 + lane % 3;
+        uint32_t a[64], tl[4];
+        int64_t flag;
+        // every load reads a record of the pair (indices clamped to the last);
+        // what lies beyond the pair is masked afterwards, so no load sits in a
+        // branch of its own
+        auto hload = [&](int c) {
+#pragma unroll
+            for (int u = 0; u < 64; ++u) a[u] = parts[min(c + u * kWaves, last)].hist[lane];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) tl[j] = parts[min(c + min(tr + 21 * j, 63) * kWaves, last)].hist[tslot];
+            flag = parts[min(c + lane * kWaves, last)].run_end;
+        };
+        auto hadd = [&](int c) {
+            // bit u: chunk c + 4u exists and ends a run (only those rows were written)
+            const uint64_t em = __ballot(c + lane * kWaves < m && flag != 0);
+#pragma unroll
+            for (int u = 0; u < 64; ++u) h0 += ((em >> u) & 1u) ? a[u] : 0u;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = tr + 21 * j;
+                ht += (lane < 63 && r < 64 && ((em >> r) & 1u)) ? tl[j] : 0u;
+            }
+        };
+        // the thread's first record and the wave's first histogram step go
+        // out together: one round trip for a pair of up to 256 chunks
+        const bool have0 = tid < m;
+        const RecF r0 = load_rec(parts[have0 ? tid : last]);
+        int c = wave;
+        hload(c);
+        // all of these loads are issued before any of them is used
+        __builtin_amdgcn_sched_barrier(0);
+        fin_merge(A, r0, have0);
+        for (int rc = tid + kBlock; rc < m; rc += kBlock) fin_merge(A, load_rec(parts[rc]), true);
+        for (;;) {
+            hadd(c);
+            c += 64 * kWaves;
+            if (c >= m) break;
+            hload(c);
+        }
+    }
+
+    // wave totals
+    // up to this bound a wave's records (at most m / 4 chunks of 2^18
+    // elements) count fewer than 2^31 elements
+    const bool small = m <= kBlock * 64;
+#pragma unroll
+    for (int k = 0; k < 6; ++k) A.s[k] = dpp_sum(A.s[k]);
+    fin_step<kDppXor1, 0xF>(A);
+    fin_step<kDppXor2, 0xF>(A);
+    fin_step<kDppHalfMirror, 0xF>(A);
+    fin_step<kDppMirror, 0xF>(A);
+    fin_step<kDppBcast15, 0xA>(A);
+    fin_step<kDppBcast31, 0xC>(A);
+    uint64_t tot[kCnt + PEAT_MAX_THRESHOLDS];
+#pragma unroll
+    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) tot[k] = wave_total(A.cn[k], small);
+    // ULP sum in two 32-bit halves (each wave total below 2^38: exact)
+    const uint64_t sulp = ((uint64_t)dpp_sum((double)(A.sulp >> 32)) << 32) +
+                          (uint64_t)dpp_sum((double)(A.sulp & 0xFFFFFFFFu));
+    const uint64_t flips = P.inj_counts ? (uint64_t)dpp_sum((double)A.flips) : 0u;
+    const uint64_t t0 = wave_total(lane % 3 == 0 ? ht : 0u, small);
+    const uint64_t t1 = wave_total(lane % 3 == 1 ? ht : 0u, small);
+    const uint64_t t2 = wave_total(lane % 3 == 2 ? ht : 0u, small);
+
+    // this wave's additive words by output word: lane l slot l (lanes 0-2 the
+    // tail slots too), lanes 0-15 the counts, 16 the ULP sum, 17 the flips
+    uint64_t *row = wv[wave];
+    row[slot_word(lane, nb)] = h0;
+    uint64_t v = 0;
+#pragma unroll
+    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) v = lane == k ? tot[k] : v;
+    v = lane == 16 ? sulp : (lane == 17 ? flips : v);
+    const int vw = lane < kCnt ? kW_cnt + lane
+                               : (lane < 16 ? kW_mism + lane - kCnt : (lane == 16 ? kW_sumulp : kOutWords));
+    if (lane < 18) row[vw] = v;
+    if (lane < 3) row[slot_word(64 + lane, nb)] = lane == 0 ? t0 : (lane == 1 ? t1 : t2);
+    // the reductions' results, read from lane 63 by every lane: a lane read
+    // inside the branch below would let the compiler move the last step's
+    // selects into it, where lane 63 does not execute them
+    const double wma = lane63_f64(A.ma), wmr = lane63_f64(A.mr);
+    const int64_t wia = (int64_t)lane63_u64((uint64_t)A.ia), wir = (int64_t)lane63_u64((uint64_t)A.ir);
+    const int64_t wiu = (int64_t)lane63_u64((uint64_t)A.iu), wfn = (int64_t)lane63_u64(A.fn);  // ~0 is -1
+    const uint64_t wmuv = lane63_u64(A.mu);
+    if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < 6; ++k) wd[wave][k] = A.s[k];
+        wd[wave][6] = wma;
+        wd[wave][7] = wmr;
+        wi[wave][0] = wia;
+        wi[wave][1] = wir;
+        wi[wave][2] = wiu;
+        wi[wave][3] = wfn;
+        wmu[wave] = wmuv;
+    }
+    __syncthreads();
+
+    // one output word per thread, the waves in order; two stores per block.
+    // Every thread forms every merged value (broadcast LDS reads) and keeps
+    // its own word by selects, so the waves do not diverge here.
+    if (tid > kOutWords) return;
+    const int t = tid;
+    const int ks = min(max(t - kW_sums, 0), 5);
+    uint64_t add = 0, nanp = 0, MU = 0;
+    double S = 0.0, MA = -1.0, MR = -1.0;
+    int64_t IA = -1, IR = -1, IU = -1;
+    uint64_t FN = ~uint64_t(0);
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        add += wv[w][t];
+        nanp += wv[w][kW_cnt + C_NANPAIR];
+        S += wd[w][ks];
+        lex_take(MA, IA, wd[w][6], wi[w][0]);
+        lex_take(MR, IR, wd[w][7], wi[w][1]);
+        lex_take(MU, IU, wmu[w], wi[w][2]);
+        const uint64_t x = (uint64_t)wi[w][3];     // -1 (none) is the largest
+        FN = x < FN ? x : FN;
+    }
+    const uint64_t qnan = 0x7FF8000000000000ull;
+    const int j = t - kW_mism;
+    uint64_t word = add;                      // counts, histogram, sum_ulp, flips
+    word = t == kW_n ? (uint64_t)n : word;
+    word = t == kW_fnan ? FN : word;
+    word = ((j >= 0) & (j < PEAT_MAX_THRESHOLDS)) ? (j < P.nthr ? add + nanp : 0u) : word;
+    word = t == kW_maxabs ? (IA >= 0 ? (uint64_t)__double_as_longlong(MA) : qnan) : word;
+    word = t == kW_ixabs ? (uint64_t)IA : word;
+    word = t == kW_maxulp ? (IU >= 0 ? MU : 0u) : word;
+    word = t == kW_ixulp ? (uint64_t)IU : word;
+    word = t == kW_maxrel ? (IR >= 0 ? (uint64_t)__double_as_longlong(MR) : qnan) : word;
+    word = t == kW_ixrel ? (uint64_t)IR : word;
+    word = ((t >= kW_sums) & (t < kW_sums + 6)) ? (uint64_t)__double_as_longlong(S) : word;
+    if (t < kOutWords)
+        reinterpret_cast<uint64_t *>(P.outs + pair)[t] = word;
+    else if (P.inj_counts)
+        P.inj_counts[pair] = (int64_t)word;
 }
 
 }  // namespace
