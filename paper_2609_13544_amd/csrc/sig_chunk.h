@@ -985,8 +985,16 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
     };
     auto pair_of = [&](int64_t c) {
         PairS d;
-        d.pair = P.single ? 0 : (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)chunk_pair[P.chunk_base + c]);
-        const SigDesc &dm = P.single ? P.one : descs[d.pair];
+        // one uniform branch: the descriptor comes from the kernel arguments
+        // or from the table, each path's fields in one batch of scalar loads
+        SigDesc dm;
+        if (P.single) {
+            d.pair = 0;
+            dm = P.one;
+        } else {
+            d.pair = (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)chunk_pair[P.chunk_base + c]);
+            dm = descs[d.pair];
+        }
         d.g = reinterpret_cast<const char *>(uniform_u64(reinterpret_cast<uint64_t>(dm.g)));
         d.t = reinterpret_cast<const char *>(uniform_u64(reinterpret_cast<uint64_t>(dm.t)));
         d.n = (int64_t)uniform_u64((uint64_t)dm.n);

@@ -50,6 +50,8 @@ __device__ __forceinline__ int slot_word(int s, int nb) {
 }
 
 // The fields of a chunk record that the finalize reads.
+constexpr int kRecParts = (int)(sizeof(ChunkPartial) / 16);    // 16-byte parts of a record
+static_assert(sizeof(ChunkPartial) % 16 == 0, "records are copied in 16-byte parts");
 struct RecF {
     double s[kWaves][6];
     int64_t end, ia, ir, iu, fn;
@@ -175,6 +177,8 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     __shared__ double wd[kWaves][8];                 // six sums, max_abs, max_rel
     __shared__ int64_t wi[kWaves][4];                // argmax_abs, argmax_rel, argmax_ulp, first NaN
     __shared__ uint64_t wmu[kWaves];
+    // kBlock records (152 KiB of the 160 KiB of LDS of a gfx950 workgroup)
+    __shared__ u32x4 stage[kBlock * kRecParts];
 
     FinAcc A;
 #pragma unroll
@@ -185,52 +189,46 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     A.mu = A.sulp = A.flips = 0;
 #pragma unroll
     for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) A.cn[k] = 0;
-    // histogram: wave w sums chunks w, w + 4, ... in steps of 64 chunks; lane
-    // l holds slot l, and lane l < 63 the tail slot 64 + l % 3 of the step's
-    // chunks l / 3 + 21 j (every chunk and tail slot once)
+    // The pair's records go to LDS kBlock at a time in one coalesced copy (a
+    // thread reading its own record from memory would touch a different
+    // cache line in every lane of a load, more lines than the L1 holds);
+    // thread t then merges record t of the batch, and wave w sums the
+    // histogram rows of records w, w + 4, ...: lane l slot l, and lane l < 63
+    // the tail slot 64 + l % 3 of records l / 3 + 21 j (every record and tail
+    // slot once).
     uint64_t h0 = 0, ht = 0;
-    if (m > 0) {                              // uniform: no record to read otherwise
-        const int last = m - 1;
-        const int tr = lane / 3, tslot = 64 + lane % 3;
-        uint32_t a[64], tl[4];
-        int64_t flag;
-        // every load reads a record of the pair (indices clamped to the last);
-        // what lies beyond the pair is masked afterwards, so no load sits in a
-        // branch of its own
-        auto hload = [&](int c) {
+    const ChunkPartial *srec = reinterpret_cast<const ChunkPartial *>(stage);
+    const int tr = lane / 3, tslot = 64 + lane % 3;
+    for (int base = 0; base < m; base += kBlock) {   // uniform
+        const int cnt = min(m - base, kBlock);
+        // all parts in flight at once: buffer loads from one scalar base with
+        // the part's offset in the instruction (reads past the batch return 0)
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(parts + base), (short)0, cnt * (int)sizeof(ChunkPartial), kBufFlags);
+        u32x4 v[kRecParts];
 #pragma unroll
-            for (int u = 0; u < 64; ++u) a[u] = parts[min(c + u * kWaves, last)].hist[lane];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) tl[j] = parts[min(c + min(tr + 21 * j, 63) * kWaves, last)].hist[tslot];
-            flag = parts[min(c + lane * kWaves, last)].run_end;
-        };
-        auto hadd = [&](int c) {
-            // bit u: chunk c + 4u exists and ends a run (only those rows were written)
-            const uint64_t em = __ballot(c + lane * kWaves < m && flag != 0);
-#pragma unroll
-            for (int u = 0; u < 64; ++u) h0 += ((em >> u) & 1u) ? a[u] : 0u;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = tr + 21 * j;
-                ht += (lane < 63 && r < 64 && ((em >> r) & 1u)) ? tl[j] : 0u;
-            }
-        };
-        // the thread's first record and the wave's first histogram step go
-        // out together: one round trip for a pair of up to 256 chunks
-        const bool have0 = tid < m;
-        const RecF r0 = load_rec(parts[have0 ? tid : last]);
-        int c = wave;
-        hload(c);
-        // all of these loads are issued before any of them is used
+        for (int k = 0; k < kRecParts; ++k) v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, tid * 16, k * kBlock * 16, 0);
+        // (the scheduler would otherwise pair each load with its store and
+        // wait for it, one round trip per part)
         __builtin_amdgcn_sched_barrier(0);
-        fin_merge(A, r0, have0);
-        for (int rc = tid + kBlock; rc < m; rc += kBlock) fin_merge(A, load_rec(parts[rc]), true);
-        for (;;) {
-            hadd(c);
-            c += 64 * kWaves;
-            if (c >= m) break;
-            hload(c);
+#pragma unroll
+        for (int k = 0; k < kRecParts; ++k) stage[tid + k * kBlock] = v[k];
+        __syncthreads();
+        fin_merge(A, load_rec(srec[min(tid, cnt - 1)]), tid < cnt);
+        // bit u: record wave + 4u exists and ends a run (only those rows were written)
+        const uint64_t em = __ballot(wave + lane * kWaves < cnt && srec[min(wave + lane * kWaves, cnt - 1)].run_end != 0);
+#pragma unroll
+        for (int u = 0; u < 64; ++u) {
+            const uint32_t x = srec[min(wave + u * kWaves, cnt - 1)].hist[lane];
+            h0 += ((em >> u) & 1u) ? x : 0u;
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = tr + 21 * j;
+            const uint32_t x = srec[min(wave + min(r, 63) * kWaves, cnt - 1)].hist[tslot];
+            ht += (lane < 63 && r < 64 && ((em >> r) & 1u)) ? x : 0u;
+        }
+        __syncthreads();                            // the stage is free again
     }
 
     // wave totals
