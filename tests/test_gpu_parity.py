@@ -261,6 +261,32 @@ def test_index_beyond_2_31():
     torch.cuda.empty_cache()
 
 
+def test_more_than_16384_chunks():
+    """A pair of more than 2^32 f16 elements (16385 chunks of 2^18): the
+    finalize reads its records in many batches and forms the counts in
+    binary64 (beyond 2^31 per wave); planted values near both ends."""
+    n = (1 << 32) + (1 << 18) + 123
+    g = torch.zeros(n, dtype=torch.float16, device="cuda")
+    t = torch.zeros(n, dtype=torch.float16, device="cuda")
+    t[5] = 2.0
+    t[n - 7] = -2.0               # ties |err| = 2 with index 5
+    t[n - 3] = float("inf")
+    t[(1 << 32) + 11] = 0.25
+    got = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+    assert got["n"] == n and got["n_valid"] == n and got["n_finite"] == n - 1 and got["n_inf_test"] == 1
+    assert got["n_nan_pairs"] == 0 and got["first_nan_index"] == -1
+    assert got["max_abs"] == math.inf and got["argmax_abs"] == n - 3
+    assert got["argmax_ulp"] == n - 3 and got["max_ulp"] == 0x7C00
+    assert got["n_rel"] == 0 and math.isnan(got["max_rel"]) and got["argmax_rel"] == -1
+    assert got["hist_zero"] == n - 4 and got["hist_over"] == 1
+    assert got["hist"][41] == 2 and got["hist"][38] == 1
+    assert got["sum_abs"] == 4.25 and got["sum_sq"] == 8.0625
+    assert got["sum_ulp"] == 2 * 0x4000 + 0x3400 + 0x7C00
+    assert got["n_mismatch"] == [4, 4]
+    del g, t
+    torch.cuda.empty_cache()
+
+
 # ---------------------------------------------------------------------------
 # injector
 # ---------------------------------------------------------------------------
