@@ -257,13 +257,27 @@ int same_type_pairs(const peat_pair_t *pairs, int32_t count, std::vector<peat_mi
 int build_descs(const peat_mixed_pair_t *pairs, int32_t count, std::vector<SigDesc> &descs,
                 int64_t range[kKinds + 1], int64_t *total_out) {
     descs.assign((size_t)count, SigDesc{});
-    std::vector<int> kinds((size_t)count);
-    for (int k = 0; k < count; ++k) kinds[k] = pair_kind(pairs[k].golden_dtype, pairs[k].test_dtype);
+    // Within a kind the pairs with the largest chunks come first, so that a
+    // launch ends on its smallest chunks and its last round of blocks is
+    // short (a chunk's record does not depend on where it lies in the launch
+    // or on which block works it).  A stable counting sort by (kind, chunk
+    // class); the pairs of a class keep their order.
+    constexpr int kClasses = kMaxChunkLog2 - kMinChunkLog2 + 1;
+    std::vector<int> key((size_t)count), order((size_t)count);
+    int start[kKinds * kClasses + 1] = {};
+    for (int k = 0; k < count; ++k) {
+        key[k] = pair_kind(pairs[k].golden_dtype, pairs[k].test_dtype) * kClasses +
+                 (kMaxChunkLog2 - chunk_log2_for(pairs[k].n));
+        ++start[key[k] + 1];
+    }
+    for (int i = 0; i < kKinds * kClasses; ++i) start[i + 1] += start[i];
+    for (int k = 0; k < count; ++k) order[start[key[k]]++] = k;
     int64_t total = 0;
+    int pos = 0;
     for (int kind = 0; kind < kKinds; ++kind) {
         range[kind] = total;
-        for (int k = 0; k < count; ++k) {
-            if (kinds[k] != kind) continue;
+        for (; pos < count && key[order[pos]] / kClasses == kind; ++pos) {
+            const int k = order[pos];
             SigDesc &sd = descs[k];
             sd.g = pairs[k].golden;
             sd.t = pairs[k].test;
@@ -795,21 +809,28 @@ int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_b
     if (count > 0 && !pairs) return fail(PEAT_EINVAL, "pairs is NULL");
     int rc = check_bins_thr(bins, thr);
     if (rc) return rc;
-    // scan 1: validation and the chunks of each kind (same-type kinds only)
-    int64_t per_kind[kKinds] = {};
+    // scan 1: validation and the chunks of each kind and chunk class
+    // (same-type kinds only; the classes ordered as build_descs orders them)
+    constexpr int kClasses = kMaxChunkLog2 - kMinChunkLog2 + 1;
+    int64_t per_class[kKinds * kClasses] = {};
     for (int k = 0; k < count; ++k) {
         if ((rc = check_pair(pairs[k], k))) return rc;
         const int64_t n = pairs[k].n;
-        per_kind[pair_kind(pairs[k].dtype, pairs[k].dtype)] += (n + (int64_t(1) << chunk_log2_for(n)) - 1) >>
-                                                              chunk_log2_for(n);
+        const int lg = chunk_log2_for(n);
+        per_class[pair_kind(pairs[k].dtype, pairs[k].dtype) * kClasses + (kMaxChunkLog2 - lg)] +=
+            (n + (int64_t(1) << lg) - 1) >> lg;
     }
     if (count == 0) return PEAT_OK;
     if (!d_outs) return fail(PEAT_EINVAL, "d_outs is NULL");
     int64_t range[kKinds + 1];
+    int64_t cursor[kKinds * kClasses];
     int64_t total = 0;
     for (int kind = 0; kind < kKinds; ++kind) {
         range[kind] = total;
-        total += per_kind[kind];
+        for (int c = 0; c < kClasses; ++c) {
+            cursor[kind * kClasses + c] = total;
+            total += per_class[kind * kClasses + c];
+        }
     }
     range[kKinds] = total;
     const size_t b_desc = align_up(sizeof(SigDesc) * (size_t)count);
@@ -826,9 +847,8 @@ int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_b
     SigDesc *d_desc = reinterpret_cast<SigDesc *>(ws);
     int32_t *d_map = reinterpret_cast<int32_t *>(ws + b_desc);
 
-    // scan 2: descriptors, in pair order, numbered by kind as build_descs does
-    int64_t cursor[kKinds];
-    for (int kind = 0; kind < kKinds; ++kind) cursor[kind] = range[kind];
+    // scan 2: descriptors, in pair order, numbered by kind and chunk class
+    // as build_descs numbers them
     DescBatch b;
     std::memset(&b, 0, sizeof b);
     b.first = 0;
@@ -842,8 +862,9 @@ int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_b
         sd.tdtype = (int16_t)pairs[k].dtype;
         sd.chunk_log2 = chunk_log2_for(sd.n);
         sd.nchunks = (int32_t)((sd.n + (int64_t(1) << sd.chunk_log2) - 1) >> sd.chunk_log2);
-        sd.first_chunk = cursor[kind];
-        cursor[kind] += sd.nchunks;
+        int64_t &cur = cursor[kind * kClasses + (kMaxChunkLog2 - sd.chunk_log2)];
+        sd.first_chunk = cur;
+        cur += sd.nchunks;
         sd.aligned = ((reinterpret_cast<uintptr_t>(sd.g) | reinterpret_cast<uintptr_t>(sd.t)) & 15) == 0;
         if (b.count == kFillDescs || k + 1 == count) {
             hipLaunchKernelGGL(noalloc_fill, dim3((unsigned)b.count), dim3(kBlock), 0, s, b, d_desc, d_map);
