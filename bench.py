@@ -375,9 +375,10 @@ def mixed_measure(torch, P, reps: int = 5, count: int = 64, shape=(4096, 4096)):
 
 def latency_measure(torch, P, synth, stream, reps: int = 50):
     """Per-call times of single-pair signatures (async call, HIP events on the
-    stream, chunk pass + finalize): the 1024x1024 f32 pair warm and cold
-    (cold: after reading 1 GiB so the pair is in no cache), the host round
-    trip of the synchronous call, and one f16 [4096, 4096] replay call."""
+    stream, chunk pass + finalize): the 1024x1024 f32 pair warm, with the
+    queue busy when the call is enqueued (the device's share), and cold
+    (after reading 1 GiB so the pair is in no cache), the host round trip of
+    the synchronous call, and one f16 [4096, 4096] replay call."""
     import statistics
     G, T = synth.config1()
     g, t = torch.from_numpy(G).cuda(), torch.from_numpy(T).cuda()
@@ -389,9 +390,14 @@ def latency_measure(torch, P, synth, stream, reps: int = 50):
     flush.fill_(1)
     sink = torch.zeros(-(-flush.numel() // P.STREAM_SPAN), dtype=torch.int32, device="cuda")
 
-    def timed(prep, cold=False):
+    def timed(prep, cold=False, busy=False):
         if cold:
             P.stream_read(flush, sink, stream=stream)
+        if busy:
+            # the queue is still working when the call is enqueued, so the
+            # events see the kernels and their dispatch, not the host's launch
+            with torch.cuda.stream(stream):
+                torch.cuda._sleep(200000)
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record(stream)
@@ -405,6 +411,7 @@ def latency_measure(torch, P, synth, stream, reps: int = 50):
         timed(p1)
         timed(p4)
     warm = statistics.median(timed(p1) for _ in range(reps))
+    device = statistics.median(timed(p1, busy=True) for _ in range(reps))
     cold = statistics.median(timed(p1, cold=True) for _ in range(10))
     f16 = statistics.median(timed(p4) for _ in range(20))
     walls = []
@@ -414,11 +421,13 @@ def latency_measure(torch, P, synth, stream, reps: int = 50):
         walls.append((time.perf_counter() - t0) * 1e6)
     del flush, sink
     torch.cuda.empty_cache()
-    return {"single_f32_1024x1024": {"warm_us": round(warm, 1), "cold_us": round(cold, 1),
+    return {"single_f32_1024x1024": {"warm_us": round(warm, 1), "device_us": round(device, 1),
+                                     "cold_us": round(cold, 1),
                                      "sync_call_wall_us": round(statistics.median(walls), 1)},
             "replay_f16_4096x4096_call_us": round(f16, 1),
             "what": "async single-pair signature, HIP events around the call on its stream (chunk pass + "
-                    "finalize + launch gaps); cold = after a 1 GiB read; sync = host round trip of peat_signature"}
+                    "finalize + launch gaps); device = the same with the queue busy when the call is enqueued "
+                    "(no host launch time); cold = after a 1 GiB read; sync = host round trip of peat_signature"}
 
 
 def read_ceiling(torch, P, stream, gib: int = 16, reps: int = 5):
