@@ -149,8 +149,29 @@ __device__ __forceinline__ uint64_t lane63_u64(uint64_t v) {
 }
 // Wave total of nonnegative integers: in 32 bits when the total is known to
 // stay below 2^31 (small, uniform), else exactly in binary64 (below 2^53).
-__device__ __forceinline__ uint64_t wave_total(uint64_t v, bool small) {
-    return small ? (uint64_t)dpp_sum_u32((uint32_t)v) : (uint64_t)dpp_sum((double)v);
+// No test for an all-zero wave: without that branch the compiler interleaves
+// the finalize's many totals, whose DPP steps would otherwise wait on one
+// another.
+__device__ __forceinline__ uint32_t dpp_sum_u32_all(uint32_t v) {
+    dsum_step<kDppXor1, 0xF>(v);
+    dsum_step<kDppXor2, 0xF>(v);
+    dsum_step<kDppHalfMirror, 0xF>(v);
+    dsum_step<kDppMirror, 0xF>(v);
+    dsum_step<kDppBcast15, 0xA>(v);
+    dsum_step<kDppBcast31, 0xC>(v);
+    return lane63_u32(v);
+}
+// The wave totals of a finalize's counts (kCnt + PEAT_MAX_THRESHOLDS) and
+// three tail histogram slots, all under one uniform branch.
+constexpr int kTot = kCnt + PEAT_MAX_THRESHOLDS + 3;
+__device__ __forceinline__ void wave_totals(const uint64_t (&v)[kTot], uint64_t (&t)[kTot], bool small) {
+    if (small) {
+#pragma unroll
+        for (int k = 0; k < kTot; ++k) t[k] = dpp_sum_u32_all((uint32_t)v[k]);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kTot; ++k) t[k] = (uint64_t)dpp_sum((double)v[k]);
+    }
 }
 
 __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
@@ -243,16 +264,17 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     fin_step<kDppMirror, 0xF>(A);
     fin_step<kDppBcast15, 0xA>(A);
     fin_step<kDppBcast31, 0xC>(A);
-    uint64_t tot[kCnt + PEAT_MAX_THRESHOLDS];
+    uint64_t vals[kTot], tot[kTot];
 #pragma unroll
-    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) tot[k] = wave_total(A.cn[k], small);
+    for (int k = 0; k < kCnt + PEAT_MAX_THRESHOLDS; ++k) vals[k] = A.cn[k];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) vals[kCnt + PEAT_MAX_THRESHOLDS + q] = lane % 3 == q ? ht : 0u;
+    wave_totals(vals, tot, small);
+    const uint64_t t0 = tot[kTot - 3], t1 = tot[kTot - 2], t2 = tot[kTot - 1];
     // ULP sum in two 32-bit halves (each wave total below 2^38: exact)
     const uint64_t sulp = ((uint64_t)dpp_sum((double)(A.sulp >> 32)) << 32) +
                           (uint64_t)dpp_sum((double)(A.sulp & 0xFFFFFFFFu));
     const uint64_t flips = P.inj_counts ? (uint64_t)dpp_sum((double)A.flips) : 0u;
-    const uint64_t t0 = wave_total(lane % 3 == 0 ? ht : 0u, small);
-    const uint64_t t1 = wave_total(lane % 3 == 1 ? ht : 0u, small);
-    const uint64_t t2 = wave_total(lane % 3 == 2 ? ht : 0u, small);
 
     // this wave's additive words by output word: lane l slot l (lanes 0-2 the
     // tail slots too), lanes 0-15 the counts, 16 the ULP sum, 17 the flips
