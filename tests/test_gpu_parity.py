@@ -261,6 +261,36 @@ def test_index_beyond_2_31():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("m", [255, 256, 257, 512])
+def test_finalize_batch_boundaries(m):
+    """Pairs of m chunks of 2^18 f16 elements around the finalize's batches
+    of 256 records: values planted in the first, 256th, 257th and last
+    chunks, with ties across batches (the lowest index must win)."""
+    c = 1 << 18
+    n = m * c
+    g = torch.zeros(n, dtype=torch.float16, device="cuda")
+    t = torch.zeros(n, dtype=torch.float16, device="cuda")
+    plant = {3: 0.5, n - 1: -0.5}                # first and last chunk: |err| 0.5
+    if m > 255:
+        plant[255 * c + 7] = 0.5                 # the 256th chunk, last of the first batch
+    if m > 256:
+        plant[256 * c + 9] = -0.5                # the 257th, first of the second batch
+    for i, v in plant.items():
+        t[i] = v
+    t[n - 2] = float("nan")
+    got = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+    k = len(plant)
+    assert got["n"] == n and got["n_valid"] == n - 1 and got["n_nan_pairs"] == 1
+    assert got["first_nan_index"] == n - 2 and got["n_nan_test"] == 1
+    assert got["max_abs"] == 0.5 and got["argmax_abs"] == 3
+    assert got["max_ulp"] == 0x3800 and got["argmax_ulp"] == 3
+    assert got["hist_zero"] == n - 1 - k and got["hist"][39] == k
+    assert got["sum_abs"] == 0.5 * k and got["sum_sq"] == 0.25 * k and got["sum_ulp"] == k * 0x3800
+    assert got["n_mismatch"] == [k + 1, k + 1]
+    del g, t
+    torch.cuda.empty_cache()
+
+
 def test_more_than_16384_chunks():
     """A pair of more than 2^32 f16 elements (16385 chunks of 2^18): the
     finalize reads its records in many batches and forms the counts in
