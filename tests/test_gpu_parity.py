@@ -183,6 +183,28 @@ def test_batched_equals_single_and_is_deterministic():
         assert_parity(batched[k], oracle_sig(gb, tb, c, synth.BINS, synth.THRESHOLDS), f"pair {k}")
 
 
+def test_batched_mixed_chunk_sizes():
+    """A batch whose pairs have chunks of 2^12, 2^13, 2^14, 2^17 and 2^18
+    elements, in no order of size, across the three same-type kinds: the
+    launch works them largest chunks first, yet every record equals its
+    single call bit for bit; the smaller pairs also equal the oracle."""
+    spec = [(5000, 0), ((1 << 24) + 7, 0), ((1 << 21) + 3, 1), (1 << 20, 0), ((1 << 22) + 5, 1),
+            (600000, 2), (1 << 21, 0), (1 << 23, 1), (3 << 20, 2), ((1 << 24) + 7, 1), (4097, 2)]
+    hosts, dev = [], []
+    for k, (n, code) in enumerate(spec):
+        gb, tb = special_pair(n, code, seed=61000 + k)
+        hosts.append((gb, tb, code))
+        dev.append((to_device(gb, code), to_device(tb, code)))
+    recs = P.signature_batched(dev, synth.BINS, synth.THRESHOLDS)
+    for k, ((gb, tb, code), (g, t)) in enumerate(zip(hosts, dev)):
+        single = P.signature(g, t, synth.BINS, synth.THRESHOLDS)
+        assert records_equal(recs[k], single), f"pair {k} (n={spec[k][0]}): batched and single differ"
+        if spec[k][0] <= (1 << 21) + 3:
+            assert_parity(recs[k], oracle_sig(gb, tb, code, synth.BINS, synth.THRESHOLDS), f"pair {k}")
+    del dev
+    torch.cuda.empty_cache()
+
+
 def test_async_records_match_sync():
     gb, tb = special_pair(123457, 1, seed=3)
     g, t = to_device(gb, 1), to_device(tb, 1)
