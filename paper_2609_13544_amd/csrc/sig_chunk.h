@@ -1031,7 +1031,9 @@ __device__ __forceinline__ void chunk_loop(const SigParams &P, Shared &sh, const
     // offsets are loop-invariant registers and the super-step moves only the
     // scalar offset, so no address register is rewritten while loads that
     // read it are in flight.  The resources cover the chunk (at most 2^18
-    // elements = 2 MiB of binary64); reads past its end return zero.
+    // elements = 2 MiB of binary64); only its full super-steps are loaded
+    // here (the hardware does not range-check the scalar offset), the ragged
+    // rest element by element at the chunk's end.
     auto load_at = [&](u32x4 (&g)[U], u32x4 (&t)[U], const char *gb, const char *tb, uint32_t len, uint32_t s) {
         const __amdgpu_buffer_rsrc_t grs =
             __builtin_amdgcn_make_buffer_rsrc((void *)gb, (short)0, (int)(len * ESZG), kBufFlags);

@@ -222,13 +222,17 @@ __global__ void __launch_bounds__(kBlock) sig_finalize(SigParams P) {
     const int tr = lane / 3, tslot = 64 + lane % 3;
     for (int base = 0; base < m; base += kBlock) {   // uniform
         const int cnt = min(m - base, kBlock);
-        // all parts in flight at once: buffer loads from one scalar base with
-        // the part's offset in the instruction (reads past the batch return 0)
+        // all parts in flight at once: buffer loads from one scalar base; a
+        // part past the batch re-reads the batch's last part, so every load
+        // lies within the batch's records (the offset is the per-lane one: a
+        // scalar offset is not part of the hardware's range check)
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
             (void *)(parts + base), (short)0, cnt * (int)sizeof(ChunkPartial), kBufFlags);
+        const int lim = cnt * kRecParts - 1;
         u32x4 v[kRecParts];
 #pragma unroll
-        for (int k = 0; k < kRecParts; ++k) v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, tid * 16, k * kBlock * 16, 0);
+        for (int k = 0; k < kRecParts; ++k)
+            v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, min(tid + k * kBlock, lim) * 16, 0, 0);
         // (the scheduler would otherwise pair each load with its store and
         // wait for it, one round trip per part)
         __builtin_amdgcn_sched_barrier(0);
