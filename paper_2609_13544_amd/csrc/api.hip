@@ -362,9 +362,11 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     const size_t b_stage = b_desc + b_inj + b_map;
 
     // device workspace: descriptors | injection descriptors | chunk map |
-    // chunk records | records; the first three are staged and copied at once
+    // chunk records; the first three are staged and copied at once.  A
+    // synchronous call's records go straight to the pinned host slot behind
+    // the staged part (the finalize writes them there: no copy afterwards).
     char *ws;
-    if ((rc = acquire_ws(d, b_stage + b_part + b_out, s, &ws))) return rc;
+    if ((rc = acquire_ws(d, b_stage + b_part, s, &ws))) return rc;
     Slot *sl = nullptr;
     char *h = nullptr;
     if (b_stage + b_out > 0) {
@@ -390,7 +392,7 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
         P.chunk_pair = reinterpret_cast<const int32_t *>(ws + b_desc + b_inj);
     }
     P.partials = reinterpret_cast<ChunkPartial *>(ws + b_stage);
-    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(ws + b_stage + b_part) : d_outs;
+    P.outs = host_outs ? reinterpret_cast<peat_signature_t *>(h + b_stage) : d_outs;
     P.inj_counts = inj ? d_counts : nullptr;
     P.count = count;
     set_bins_thr(P, *bins, *thr);
@@ -408,8 +410,6 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     if ((rc = prof_end(d, s, 1, ev))) return rc;
 
     char *hout = h ? h + b_stage : nullptr;
-    if (host_outs)
-        HIP_OR_FAIL(hipMemcpyAsync(hout, P.outs, sizeof(peat_signature_t) * count, hipMemcpyDeviceToHost, s));
     if (sl && (rc = release_slot(*sl, s))) return rc;
     if ((rc = release_ws(d, s))) return rc;
     if (host_outs) {
