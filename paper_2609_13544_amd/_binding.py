@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import struct
 import threading
 
 import numpy as np
@@ -278,19 +279,39 @@ def _stream_ptr(stream) -> int | None:
     return stream.cuda_stream
 
 
-def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None) -> dict:
-    d = {}
-    for name, _ in _SIG_FIELDS:
-        v = getattr(s, name)
-        if name == "n_mismatch":
-            v = [int(x) for x in v][: (MAX_THRESHOLDS if nthr is None else nthr)]
-        elif name == "hist":
-            v = [int(x) for x in v]
-        elif isinstance(v, float):
-            v = float(v)
+def _sig_layout():
+    """One struct format for the whole record and, per field, its slice of
+    the unpacked values (None for a scalar)."""
+    codes = {ctypes.c_int64: "q", ctypes.c_uint64: "Q", ctypes.c_double: "d"}
+    fmt, layout, pos = "<", [], 0
+    for name, typ in _SIG_FIELDS:
+        if hasattr(typ, "_length_"):
+            fmt += codes[typ._type_] * typ._length_
+            layout.append((name, pos, typ._length_))
+            pos += typ._length_
         else:
-            v = int(v)
-        d[name] = v
+            fmt += codes[typ]
+            layout.append((name, pos, None))
+            pos += 1
+    return struct.Struct(fmt), layout
+
+
+_SIG_STRUCT, _SIG_LAYOUT = _sig_layout()
+assert _SIG_STRUCT.size == ctypes.sizeof(Signature)
+
+
+def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None) -> dict:
+    """The record's fields by name (ints, floats, lists for the two arrays;
+    n_mismatch cut to the thresholds used), unpacked in one step."""
+    vals = _SIG_STRUCT.unpack(ctypes.string_at(ctypes.addressof(s), _SIG_STRUCT.size))
+    d = {}
+    for name, pos, length in _SIG_LAYOUT:
+        if length is None:
+            d[name] = vals[pos]
+        elif name == "n_mismatch":
+            d[name] = list(vals[pos:pos + (MAX_THRESHOLDS if nthr is None else nthr)])
+        else:
+            d[name] = list(vals[pos:pos + length])
     return d
 
 

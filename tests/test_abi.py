@@ -312,3 +312,28 @@ def test_signature_dict_round_trip():
     d = B.sig_to_dict(s)
     assert B.sig_to_dict(B.dict_to_sig(d)) == d
     assert bytes(B.dict_to_sig(d)) == bytes(s)
+
+
+def test_sig_to_dict_matches_field_by_field_reading():
+    """The one-step unpacking of a record equals reading the struct field by
+    field (random bit patterns: NaN and infinite doubles, negative and
+    unsigned 64-bit integers), for every number of thresholds."""
+    import random
+    rng = random.Random(11)
+    for _ in range(200):
+        raw = bytes(rng.getrandbits(8) for _ in range(ctypes.sizeof(B.Signature)))
+        s = B.Signature.from_buffer_copy(raw)
+        for nthr in (None, 0, 1, 2, 8):
+            d = B.sig_to_dict(s, nthr=nthr)
+            assert list(d) == [name for name, _ in B._SIG_FIELDS]
+            for name, typ in B._SIG_FIELDS:
+                want = getattr(s, name)
+                got = d[name]
+                if name in ("n_mismatch", "hist"):
+                    want = list(want)[: (B.MAX_THRESHOLDS if nthr is None else nthr)] if name == "n_mismatch" \
+                        else list(want)
+                    assert got == want and all(type(x) is int for x in got), name
+                elif typ is ctypes.c_double:
+                    assert type(got) is float and (got == want or (math.isnan(got) and math.isnan(want))), name
+                else:
+                    assert type(got) is int and got == want, name
