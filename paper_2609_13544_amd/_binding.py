@@ -238,12 +238,17 @@ def _torch():
     return torch
 
 
+_DTYPE_CODES: dict = {}
+
+
 def dtype_code(t) -> int:
-    torch = _torch()
-    m = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16, torch.float64: F64}
-    if t.dtype not in m:
+    if not _DTYPE_CODES:
+        torch = _torch()
+        _DTYPE_CODES.update({torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16, torch.float64: F64})
+    code = _DTYPE_CODES.get(t.dtype)
+    if code is None:
         raise TypeError(f"unsupported dtype {t.dtype}")
-    return m[t.dtype]
+    return code
 
 
 def _dev_tensor(t, name: str):
