@@ -305,10 +305,9 @@ _SIG_STRUCT, _SIG_LAYOUT = _sig_layout()
 assert _SIG_STRUCT.size == ctypes.sizeof(Signature)
 
 
-def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None) -> dict:
-    """The record's fields by name (ints, floats, lists for the two arrays;
-    n_mismatch cut to the thresholds used), unpacked in one step."""
-    vals = _SIG_STRUCT.unpack(ctypes.string_at(ctypes.addressof(s), _SIG_STRUCT.size))
+def _vals_to_dict(vals, nthr: int | None) -> dict:
+    """A record's unpacked values by field name (ints, floats, lists for the
+    two arrays; n_mismatch cut to the thresholds used)."""
     d = {}
     for name, pos, length in _SIG_LAYOUT:
         if length is None:
@@ -318,6 +317,17 @@ def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None)
         else:
             d[name] = list(vals[pos:pos + length])
     return d
+
+
+def sig_to_dict(s: Signature, nbins: int | None = None, nthr: int | None = None) -> dict:
+    """The record's fields by name, unpacked in one step."""
+    return _vals_to_dict(_SIG_STRUCT.unpack(ctypes.string_at(ctypes.addressof(s), _SIG_STRUCT.size)), nthr)
+
+
+def _records_to_dicts(buf, count: int, nthr: int | None) -> list[dict]:
+    """count consecutive records held in a bytes-like buffer, decoded."""
+    raw = bytes(memoryview(buf).cast("B")[: count * _SIG_STRUCT.size])
+    return [_vals_to_dict(v, nthr) for v in _SIG_STRUCT.iter_unpack(raw)]
 
 
 def dict_to_sig(d: dict) -> Signature:
@@ -336,19 +346,7 @@ def dict_to_sig(d: dict) -> Signature:
 
 def record_to_dict(rec, nthr: int | None = None) -> dict:
     """Convert one element of a SIG_NP_DTYPE array to a dict."""
-    d = {}
-    for name, _ in _SIG_FIELDS:
-        v = rec[name]
-        if name == "n_mismatch":
-            v = [int(x) for x in v][: (MAX_THRESHOLDS if nthr is None else nthr)]
-        elif name == "hist":
-            v = [int(x) for x in v]
-        elif isinstance(v, (float, np.floating)):
-            v = float(v)
-        else:
-            v = int(v)
-        d[name] = v
-    return d
+    return _vals_to_dict(_SIG_STRUCT.unpack(rec.tobytes()), nthr)
 
 
 # ---------------------------------------------------------------------------
@@ -400,7 +398,7 @@ def signature_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> lis
     set_stream()
     _check(lib().peat_signature_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
            "peat_signature_batched")
-    return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+    return _records_to_dicts(outs, len(pairs), len(thresholds))
 
 
 def signature_mixed(golden, test, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) -> dict:
@@ -445,7 +443,7 @@ def signature_mixed_batched(pairs, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3)) 
     set_stream()
     _check(lib().peat_signature_mixed_batched(arr, len(pairs), ctypes.byref(b), ctypes.byref(th), outs),
            "peat_signature_mixed_batched")
-    return [sig_to_dict(outs[k], nthr=len(thresholds)) for k in range(len(pairs))]
+    return _records_to_dicts(outs, len(pairs), len(thresholds))
 
 
 def signature_mixed_batched_async(pairs, d_out, bins=(-40, 24, 64), thresholds=(1e-6, 1e-3),
@@ -698,8 +696,7 @@ def inject_signature_batched_async(pairs, seeds, rate: float, bitmask: int, d_ou
 def decode_records(d_out, count: int, nthr: int | None = None) -> list[dict]:
     """Copy device records to the host and decode them."""
     host = d_out.detach().view(-1)[: count * SIG_BYTES].cpu().numpy().view(np.uint8)
-    recs = host.view(SIG_NP_DTYPE)
-    return [record_to_dict(r, nthr) for r in recs]
+    return _records_to_dicts(host, count, nthr)
 
 
 def inject(tensor, seed: int, rate: float, bitmask: int, *, dtype: int | None = None, n: int | None = None) -> int:

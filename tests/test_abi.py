@@ -337,3 +337,29 @@ def test_sig_to_dict_matches_field_by_field_reading():
                     assert type(got) is float and (got == want or (math.isnan(got) and math.isnan(want))), name
                 else:
                     assert type(got) is int and got == want, name
+
+
+def test_batched_record_decoding_matches_single():
+    """Records decoded in one pass over a buffer (batched calls, device
+    records) and one by one from numpy records equal sig_to_dict's."""
+    import numpy as np
+    rng = np.random.default_rng(12)
+    raw = rng.integers(0, 256, size=(64, ctypes.sizeof(B.Signature)), dtype=np.uint8)
+    arr = (B.Signature * 64).from_buffer_copy(raw.tobytes())
+    recs = raw.view(B.SIG_NP_DTYPE).reshape(-1)
+
+    def same(a, b):
+        assert list(a) == list(b)
+        for k in a:
+            if isinstance(a[k], float) and math.isnan(a[k]):
+                assert math.isnan(b[k])
+            else:
+                assert a[k] == b[k] and type(a[k]) is type(b[k]), k
+
+    for nthr in (None, 2):
+        batch = B._records_to_dicts(raw, 64, nthr)
+        assert len(batch) == 64
+        for i in range(64):
+            ref = B.sig_to_dict(arr[i], nthr=nthr)
+            same(ref, batch[i])
+            same(ref, B.record_to_dict(recs[i], nthr))
