@@ -1,0 +1,137 @@
+"""Randomised batch-structure sweep: a pair's record may not depend on the
+batch it is signed in.  Each seeded case draws a batch of 1..47 pairs (type
+combinations same-type or mixed, element counts from empty through both
+chunk-size classes with ragged tails, element offsets 0..3, relative noise,
+NaN/Inf/zero/equal values planted, histogram bins and 0..4 thresholds) and
+checks, bit for bit:
+
+- the mixed batched call against one single call per pair;
+- for same-type batches, the same-type batched, stream-ordered and
+  allocation-free calls against the single calls;
+- the fused injection + signature (one bit mask and rate for the batch, one
+  seed per pair) against injection, then signature: flip counts, the flipped
+  tensors and the records.
+
+The single calls themselves are checked against the oracle in the parity
+tests; this sweep covers the launch structure (chunk classes, launch order,
+grouping of chunks per block, finalize batches) that only batches exercise."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_13544_amd as P
+
+pytestmark = pytest.mark.gpu
+
+F32, F16, BF16, F64 = P.F32, P.F16, P.BF16, P.F64
+TORCH_DT = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16, F64: torch.float64}
+SAME = [(F32, F32), (F16, F16), (BF16, BF16)]
+MIXED = [(F32, F64), (F32, F16), (F32, BF16), (F16, F32), (BF16, F32), (F16, F64), (BF16, F64)]
+BINS = [(-40, 24, 64), (-30, 20, 25), (-24, 16, 8)]
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def same_bits(a, b) -> bool:
+    """Record equality with NaN equal to NaN and the sign of zero compared."""
+    if isinstance(a, dict):
+        return a.keys() == b.keys() and all(same_bits(a[k], b[k]) for k in a)
+    if isinstance(a, (list, tuple)):
+        return len(a) == len(b) and all(same_bits(x, y) for x, y in zip(a, b))
+    if isinstance(a, float) and isinstance(b, float):
+        if math.isnan(a) or math.isnan(b):
+            return math.isnan(a) and math.isnan(b)
+        return a == b and math.copysign(1.0, a) == math.copysign(1.0, b)
+    return a == b
+
+
+def _draw_n(rng) -> int:
+    r = rng.random()
+    if r < 0.1:
+        return int(rng.integers(0, 40))
+    if r < 0.5:
+        return int(rng.integers(40, 1 << 16))
+    if r < 0.85:
+        return int(rng.integers(1 << 16, 1 << 22))
+    return int(rng.integers(1 << 22, (1 << 23) + 4099))
+
+
+def _pair(gdt: int, tdt: int, n: int, off: int, rel: float, gen):
+    m = n + off
+    base = torch.randn(m, device="cuda", dtype=torch.float64, generator=gen)
+    e = torch.randint(-12, 12, (m,), device="cuda", generator=gen).double()
+    G = (base * torch.exp2(e)).to(TORCH_DT[gdt])
+    T = (G.double() * (1 + rel * torch.randn(m, device="cuda", dtype=torch.float64, generator=gen))).to(TORCH_DT[tdt])
+    if n > 8:
+        k = max(1, n // 997)
+        for val in (float("nan"), float("inf"), 0.0, -0.0):
+            T[torch.randint(0, m, (k,), device="cuda", generator=gen)] = val
+        G[torch.randint(0, m, (k,), device="cuda", generator=gen)] = 0.0
+        idx = torch.randint(0, m, (k,), device="cuda", generator=gen)
+        T[idx] = G[idx].to(TORCH_DT[tdt])
+    return G[off:], T[off:]
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_batch_structure(seed):
+    rng = np.random.default_rng(1_000_003 + seed)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    count = int(rng.integers(1, 48))
+    bins = BINS[rng.integers(len(BINS))]
+    thr = tuple(float(10.0 ** rng.uniform(-8, -1)) for _ in range(int(rng.integers(0, 5))))
+    same_only = rng.random() < 0.5
+    pairs, kinds = [], []
+    for _ in range(count):
+        kd = SAME[rng.integers(3)] if same_only or rng.random() < 0.4 else MIXED[rng.integers(len(MIXED))]
+        n = _draw_n(rng)
+        pairs.append(_pair(kd[0], kd[1], n, int(rng.integers(0, 4)), float(10.0 ** rng.uniform(-7, -1)), gen))
+        kinds.append(kd)
+    log(f"  seed={seed} pairs={count} same_type={same_only} "
+        f"elements={sum(g.numel() for g, _ in pairs)} bins={bins} thresholds={len(thr)}")
+
+    single = [P.signature_mixed(g, t, bins, thr) for g, t in pairs]
+    batched = P.signature_mixed_batched(pairs, bins, thr)
+    for k in range(count):
+        assert same_bits(single[k], batched[k]), f"mixed batched, pair {k} {kinds[k]} n={pairs[k][0].numel()}"
+    if not same_only:
+        return
+
+    for k, r in enumerate(P.signature_batched(pairs, bins, thr)):
+        assert same_bits(single[k], r), f"same-type batched, pair {k}"
+    d = torch.empty(count * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    P.signature_batched_async(pairs, d, bins, thr)
+    torch.cuda.synchronize()
+    for k, r in enumerate(P.decode_records(d, count, len(thr))):
+        assert same_bits(single[k], r), f"stream-ordered batched, pair {k}"
+    d.fill_(0xA5)
+    P.signature_batched_noalloc(pairs, d, bins, thr)
+    torch.cuda.synchronize()
+    for k, r in enumerate(P.decode_records(d, count, len(thr))):
+        assert same_bits(single[k], r), f"allocation-free batched, pair {k}"
+
+    rate = float(10.0 ** rng.uniform(-5, -2))
+    seeds = [int(x) for x in rng.integers(0, 2 ** 62, count)]
+    mask = 0xFFFFFFFF if all(kd[0] == F32 for kd in kinds) else 0xFFFF
+    fused_t = [t.clone() for _, t in pairs]
+    sep_t = [t.clone() for _, t in pairs]
+    sep_counts = [P.inject(sep_t[k], seeds[k], rate, mask) for k in range(count)]
+    sep_recs = P.signature_batched([(pairs[k][0], sep_t[k]) for k in range(count)], bins, thr)
+    d_counts = torch.empty(count, dtype=torch.int64, device="cuda")
+    P.inject_signature_batched_async([(pairs[k][0], fused_t[k]) for k in range(count)], seeds, rate, mask,
+                                     d, d_counts, bins, thr)
+    torch.cuda.synchronize()
+    assert d_counts.cpu().tolist() == sep_counts
+    for k in range(count):
+        assert torch.equal(fused_t[k].view(torch.uint8), sep_t[k].view(torch.uint8)), f"fused flips, pair {k}"
+    for k, r in enumerate(P.decode_records(d, count, len(thr))):
+        assert same_bits(sep_recs[k], r), f"fused record, pair {k}"
+    log(f"    fused: {sum(sep_counts)} flips at rate {rate:.2e}")
