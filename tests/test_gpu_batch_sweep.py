@@ -10,7 +10,9 @@ checks, bit for bit:
   allocation-free calls against the single calls;
 - the fused injection + signature (one bit mask and rate for the batch, one
   seed per pair) against injection, then signature: flip counts, the flipped
-  tensors and the records.
+  tensors and the records;
+- the top-k mean of such batches: batched and stream-ordered calls against
+  one call per pair, the signature-fed forms to their summation tolerance.
 
 The single calls themselves are checked against the oracle in the parity
 tests; this sweep covers the launch structure (chunk classes, launch order,
@@ -135,3 +137,65 @@ def test_batch_structure(seed):
     for k, r in enumerate(P.decode_records(d, count, len(thr))):
         assert same_bits(sep_recs[k], r), f"fused record, pair {k}"
     log(f"    fused: {sum(sep_counts)} flips at rate {rate:.2e}")
+
+
+def _close_topk(got: dict, ref: dict, ctx: str) -> None:
+    """Signature-fed top-k: exact fields equal, sums within 1e-12 (a window's
+    binades are summed per binade there, in the lanes' order standalone)."""
+    for key in ("n_valid", "k", "count_above", "kth_value"):
+        assert same_bits(got[key], ref[key]), f"{ctx}: {key} {got[key]!r} != {ref[key]!r}"
+    for key in ("sum_topk", "mean_topk"):
+        a, b = got[key], ref[key]
+        if math.isnan(b) or math.isinf(b):
+            assert same_bits(a, b), f"{ctx}: {key} {a!r} != {b!r}"
+        else:
+            assert abs(a - b) <= 1e-12 * abs(b), f"{ctx}: {key} {a!r} vs {b!r}"
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_topk_batch_structure(seed):
+    """The top-k mean of a random batch (as above, with a random fraction
+    num/den): batched and stream-ordered calls bit-equal to one call per
+    pair; the signature-fed forms (host records, and device records on the
+    stream for same-type batches) to the tolerance of their summation order."""
+    rng = np.random.default_rng(2_000_003 + seed)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(10_000 + seed)
+    count = int(rng.integers(1, 40))
+    same_only = rng.random() < 0.5
+    num = int(rng.integers(1, 8))
+    den = int(rng.integers(num, 60))
+    bins = BINS[rng.integers(len(BINS))] if rng.random() < 0.5 else (-40, 24, 64)
+    pairs, kinds = [], []
+    for _ in range(count):
+        kd = SAME[rng.integers(3)] if same_only or rng.random() < 0.4 else MIXED[rng.integers(len(MIXED))]
+        n = _draw_n(rng)
+        pairs.append(_pair(kd[0], kd[1], n, int(rng.integers(0, 4)), float(10.0 ** rng.uniform(-7, -1)), gen))
+        kinds.append(kd)
+    log(f"  seed={seed} pairs={count} same_type={same_only} "
+        f"elements={sum(g.numel() for g, _ in pairs)} num/den={num}/{den} bins={bins}")
+
+    single = [P.topk_mean_mixed_batched([p], num, den)[0] for p in pairs]
+    for k, r in enumerate(P.topk_mean_mixed_batched(pairs, num, den)):
+        assert same_bits(single[k], r), f"mixed batched, pair {k} {kinds[k]}"
+    d = torch.empty(count * P.TOPK_BYTES, dtype=torch.uint8, device="cuda")
+    P.topk_mean_mixed_batched_async(pairs, d, num, den)
+    torch.cuda.synchronize()
+    for k, r in enumerate(P.decode_topk(d, count)):
+        assert same_bits(single[k], r), f"mixed stream-ordered, pair {k}"
+    sigs = P.signature_mixed_batched(pairs, bins, ())
+    for k, r in enumerate(P.topk_mean_mixed_from_signature_batched(pairs, sigs, bins, num, den)):
+        _close_topk(r, single[k], f"mixed from signature, pair {k} {kinds[k]}")
+    if not same_only:
+        return
+    for k, r in enumerate(P.topk_mean_batched(pairs, num, den)):
+        assert same_bits(single[k], r), f"same-type batched, pair {k}"
+    for k, (g, t) in enumerate(pairs):
+        assert same_bits(single[k], P.topk_mean(g, t, num, den)), f"same-type single, pair {k}"
+    d_sigs = torch.empty(count * P.SIG_BYTES, dtype=torch.uint8, device="cuda")
+    P.signature_batched_async(pairs, d_sigs, bins, ())
+    d.fill_(0)
+    P.topk_mean_from_signature_batched_async(pairs, d_sigs, d, bins, num, den)
+    torch.cuda.synchronize()
+    for k, r in enumerate(P.decode_topk(d, count)):
+        _close_topk(r, single[k], f"same-type from device signature, pair {k}")
