@@ -8,6 +8,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "peat_internal.h"
@@ -307,6 +308,28 @@ void set_kind_elems(SigParams &P, const peat_mixed_pair_t *pairs, int32_t count)
     }
 }
 
+// Golden reuse: a batch in which at most half as many distinct golden
+// tensors as pairs appear (a replay batch signs many test tensors against one
+// golden), together at most kKeepGoldenBytes, has its goldens read with the
+// default cache policy, so that the shared lines are served from the caches
+// instead of HBM; otherwise every byte is read once, nontemporally.
+constexpr int64_t kKeepGoldenBytes = int64_t(64) << 20;
+template <typename PairT, typename DtypeFn>
+int32_t golden_reuse(const PairT *pairs, int32_t count, DtypeFn golden_dtype) {
+    if (count < 2) return 0;
+    std::vector<std::pair<uintptr_t, int64_t>> g((size_t)count);
+    for (int k = 0; k < count; ++k)
+        g[k] = {reinterpret_cast<uintptr_t>(pairs[k].golden), pairs[k].n * elem_bytes(golden_dtype(pairs[k]))};
+    std::sort(g.begin(), g.end());
+    int64_t distinct = 0, bytes = 0;
+    for (size_t i = 0; i < g.size(); ++i) {
+        if (i + 1 < g.size() && g[i + 1].first == g[i].first) continue;   // the largest extent of a pointer
+        ++distinct;
+        bytes += g[i].second;
+    }
+    return (2 * distinct <= count && bytes <= kKeepGoldenBytes) ? 1 : 0;
+}
+
 // The bins and closeness tests of a signature launch.
 void set_bins_thr(SigParams &P, const peat_bins_t &bins, const peat_thresholds_t &thr) {
     P.lo = bins.lo_log2;
@@ -385,6 +408,7 @@ int signature_core(const peat_mixed_pair_t *pairs, int32_t count, const peat_bin
     SigParams P{};
     P.chunk_base = 0;
     P.single = single ? 1 : 0;
+    P.gkeep = golden_reuse(pairs, count, [](const peat_mixed_pair_t &q) { return q.golden_dtype; });
     if (single) {
         P.one = descs[0];
     } else {
@@ -884,6 +908,7 @@ int signature_noalloc_core(const peat_pair_t *pairs, int32_t count, const peat_b
     P.outs = d_outs;
     P.inj_counts = nullptr;
     P.count = count;
+    P.gkeep = golden_reuse(pairs, count, [](const peat_pair_t &q) { return q.dtype; });
     set_bins_thr(P, *bins, *thr);
     for (int k = 0; k < count; ++k) P.kind_elems[pair_kind(pairs[k].dtype, pairs[k].dtype)] += pairs[k].n;
     HIP_OR_FAIL(launch_sig_chunks(P, range, s));

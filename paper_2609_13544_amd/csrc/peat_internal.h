@@ -110,6 +110,9 @@ struct SigParams {
     double thr_min;                // smallest thr (+Inf when there are none)
     int32_t any_rtol;              // some relative tolerance is nonzero
     int32_t single;                // one pair, described by `one` (descs and chunk_pair unused)
+    // most pairs share a few golden tensors (a replay batch): golden loads
+    // keep the default cache policy so that the shared lines stay cached
+    int32_t gkeep;
     SigDesc one;
     int64_t kind_elems[kKinds];    // elements of the pairs of each kind
     int64_t launch_elems;          // elements of this launch's chunks
